@@ -1,0 +1,227 @@
+/*
+ * eahr.h -- C ABI of libeahr.so: the PVS dense channel on an MI355X (gfx950),
+ * the PBM sparse channel and exact adaptive weighted-RRF fusion on the host.
+ *
+ * Paper: "Exact Adaptive Hybrid Retrieval Without Fixed Top-L Cutoffs".
+ *
+ * Conventions (all entry points):
+ *  - Every function returning int returns EAHR_OK (0) or a negative EAHR_E_*.
+ *    On error nothing is returned through output pointers except where stated.
+ *  - Item identifiers are int64 at the ABI.  Dense ids are row numbers in a
+ *    pvs_index (0 .. rows-1, inserts get new, larger ids); sparse document ids
+ *    must use the same numbering, so one identifier names one item in both
+ *    channels.  The total identifier order used for every tie is ascending id.
+ *  - Input pointers are borrowed for the duration of the call only.  Handles
+ *    are owned by the library and released with their *_free / *_close call.
+ *    Output buffers are caller-owned host memory unless stated otherwise.
+ *  - Pointers tagged with a ptr_kind argument may be host (EAHR_PTR_HOST) or
+ *    device (EAHR_PTR_DEVICE, memory of the GPU the index lives on).
+ *  - Calls on one handle are not thread-safe; a pvs_state must not be used
+ *    while its pvs_index is being modified.
+ */
+#ifndef EAHR_H
+#define EAHR_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---------------------------------------------------------------- status */
+enum {
+    EAHR_OK = 0,
+    EAHR_E_INVALID = -1,    /* bad argument (null pointer, size, unknown epoch, ...) */
+    EAHR_E_NONFINITE = -2,  /* NaN or Inf in a corpus row or a query (App. A.1)      */
+    EAHR_E_RANGE = -3,      /* dimension too large: a_m >= 1, or 127^2 d >= 2^31      */
+    EAHR_E_OOM = -4,        /* device or host allocation failed                       */
+    EAHR_E_HIP = -5,        /* HIP runtime error                                      */
+    EAHR_E_FAILED = -6      /* a ranked list failed (Sec. 2.1): see per-query status  */
+};
+
+/* Ranked-list states (Sec. 2.1): an Open list may extend its exact prefix, an
+ * Exhausted list is complete, a Failed list invalidates the request. */
+enum { EAHR_LIST_OPEN = 0, EAHR_LIST_EXHAUSTED = 1, EAHR_LIST_FAILED = 2 };
+
+enum { EAHR_PTR_HOST = 0, EAHR_PTR_DEVICE = 1 };
+
+typedef struct pvs_index pvs_index;
+typedef struct pvs_state pvs_state;
+typedef struct pbm_index pbm_index;
+typedef struct pbm_state pbm_state;
+
+/* ------------------------------------------------------------ PVS (dense) */
+
+/* pvs_build -- quantise a float32 corpus (Sec. 2.3.1).
+ *   corpus  n x d float32, row-major, host or device (ptr_kind).
+ *   stream  hipStream_t every later call on this index and its states uses
+ *           (NULL: the default stream).
+ * Per row v the index stores the scale s_v = fl32(||v||_inf / 127) (1 for a zero
+ * row), the codes z_v = clip(round_half_away(fl32(v_j / s_v)), -127, 127), the
+ * float32 norms ||v||_2 and ||v - s_v z_v||_2 rounded up, and a copy of the
+ * float32 row for authoritative scoring.  Epoch 0 (all n rows visible) is
+ * created.  Errors: EAHR_E_NONFINITE for NaN/Inf anywhere in the corpus,
+ * EAHR_E_RANGE when d > 4096 (guard and Int32 accumulator range, App. A.1). */
+int pvs_build(const float* corpus, int64_t n, int32_t d, int32_t ptr_kind,
+              void* stream, pvs_index** out);
+
+/* pvs_insert -- append n_new rows (quantised on insert); their ids are
+ * *first_id .. *first_id + n_new - 1.  They are visible in the live state and
+ * in epochs taken afterwards, never in earlier epochs. */
+int pvs_insert(pvs_index* idx, const float* rows, int64_t n_new, int32_t ptr_kind,
+               int64_t* first_id);
+
+/* pvs_delete -- hide ids (host array) from the live state; earlier epochs are
+ * unchanged (the visible set of a request is fixed by its snapshot, Sec. 2.4). */
+int pvs_delete(pvs_index* idx, const int64_t* ids, int64_t n);
+
+/* pvs_snapshot -- freeze the live visible set as a new epoch. */
+int pvs_snapshot(pvs_index* idx, int64_t* epoch);
+
+/* pvs_info -- rows, dimension and visible-row count of an epoch. */
+int pvs_info(const pvs_index* idx, int64_t epoch, int64_t* rows, int32_t* d,
+             int64_t* visible);
+
+/* pvs_open -- encode a batch of B queries (B x d float32, host or device) the
+ * same way as corpus rows and create resumable state on epoch `epoch`.
+ * Errors: EAHR_E_NONFINITE for NaN/Inf in a query. */
+int pvs_open(const pvs_index* idx, int64_t epoch, const float* q, int32_t B,
+             int32_t ptr_kind, pvs_state** out);
+
+/* pvs_next -- extend each active query's exact dense prefix by up to m ranks
+ * (Sec. 2.3.1 resumable generation).  The complete list orders the visible
+ * rows by (authoritative float32 inner product descending, id ascending);
+ * the authoritative score is one float32 dot product in a fixed order.
+ *   active  B flags (NULL: all active); inactive queries are left untouched.
+ *   ids     B x m, scores B x m: row b receives count[b] (id, score) pairs.
+ *   count   B: number written; count[b] < m only when status[b] is
+ *           EAHR_LIST_EXHAUSTED.
+ *   status  B: EAHR_LIST_* after the call.  Failed is sticky: it is set when a
+ *           rescored score lies outside its interval (App. A.1); such a query
+ *           returns count 0 from then on.
+ * Returns EAHR_OK even when some queries failed (see status). */
+int pvs_next(pvs_state* st, int32_t m, const uint8_t* active, int64_t* ids,
+             float* scores, int32_t* count, int32_t* status);
+
+/* Counters of one state (summed over its queries). */
+typedef struct {
+    int64_t scans;           /* full interval scans over the codes             */
+    int64_t sample_scans;    /* threshold-estimation passes over sampled rows  */
+    int64_t rows_scanned;    /* visible-or-not rows streamed by full scans     */
+    int64_t bytes_scanned;   /* code + metadata bytes streamed by full scans   */
+    int64_t candidates;      /* rows rescored in float32                       */
+    int64_t certified;       /* ranks certified by scans                       */
+    int64_t emitted;         /* ranks returned by pvs_next                     */
+    int64_t rescans;         /* scans repeated with a lower threshold          */
+} pvs_counters;
+
+int pvs_stats(const pvs_state* st, pvs_counters* out);
+
+/* Debug / test entry points (not on the retrieval path):
+ * pvs_read_index -- copy rows [row0, row0+n) of the index to host: codes
+ *   n x d int8 (row-major), meta n x 3 float32 (s_v, ||v||_2 up, ||e_v||_2 up).
+ * pvs_read_query -- copy the encoded batch: codes B x d int8, meta B x 4
+ *   float32 (s_q, ||q||_2 up, ||q_hat||_2 up, ||e_q||_2 up).
+ * pvs_intervals -- score intervals [lo, hi] of query b against n host-listed
+ *   rows, computed by the scan's own device code.
+ * pvs_scores -- authoritative float32 scores of query b against n rows. */
+int pvs_read_index(const pvs_index* idx, int64_t row0, int64_t n, int8_t* codes,
+                   float* meta);
+int pvs_read_query(const pvs_state* st, int8_t* codes, float* meta);
+int pvs_intervals(const pvs_state* st, int32_t b, const int64_t* rows, int64_t n,
+                  float* lo, float* hi);
+int pvs_scores(const pvs_state* st, int32_t b, const int64_t* rows, int64_t n,
+               float* scores);
+
+void pvs_close(pvs_state* st);
+void pvs_free(pvs_index* idx);
+
+/* ------------------------------------------------------------ PBM (sparse) */
+
+/* pbm_build -- Posting Block-Max index over term-major postings (Sec. 2.3.2).
+ *   term_ptr  vocab+1 offsets into docs/impacts; docs of one term strictly
+ *             ascending and < n_docs; impacts finite and >= 0 (App. A.2).
+ *   range_size  documents per contiguous id range (>= 1).
+ * The index stores, per term and range, the maximum impact m_t(R) and where
+ * the term's postings for R start.  Copies its inputs.  Host only. */
+int pbm_build(const int64_t* term_ptr, int32_t vocab, const int32_t* docs,
+              const float* impacts, int64_t n_docs, int32_t range_size,
+              pbm_index** out);
+void pbm_free(pbm_index* idx);
+
+/* A sparse query: n_terms distinct term ids with weights q_t >= 0. */
+typedef struct {
+    const int32_t* terms;
+    const float* weights;
+    int32_t n_terms;
+} eahr_sparse_query;
+
+/* pbm_open / pbm_next -- resumable exact sparse ranking of one query: items
+ * with S(x) > 0 in (S descending, id ascending) order, S accumulated in float32
+ * in ascending term order.  Same count/status contract as pvs_next. */
+int pbm_open(const pbm_index* idx, const eahr_sparse_query* q, pbm_state** out);
+int pbm_next(pbm_state* st, int32_t m, int64_t* ids, float* scores, int32_t* count,
+             int32_t* status);
+void pbm_close(pbm_state* st);
+
+/* pbm_debug_set_blockmax -- test hook: overwrite m_t(R) of one (term, range)
+ * entry so that a later pbm_open sees metadata that no longer covers its
+ * postings; pbm_next then reports EAHR_LIST_FAILED (App. A.2).  Returns
+ * EAHR_E_INVALID when the term has no postings in that range. */
+int pbm_debug_set_blockmax(pbm_index* idx, int32_t term, int64_t range, float value);
+
+/* -------------------------------------------------------- EAHR (fusion) */
+
+typedef struct {
+    int32_t K;           /* requested result size                                */
+    int32_t depth0;      /* first cumulative depth requested from each list (20)  */
+    int32_t growth;      /* depth multiplier per round (2)                        */
+    int32_t k_rrf;       /* rank constant k >= 1                                  */
+    int32_t w_dense;     /* rank-scaled weights w_i >= 0 (Sec. 2.1), integers     */
+    int32_t w_sparse;
+} eahr_params;
+
+typedef struct {
+    int64_t dense_depth;    /* d_i: ranks read from each list        */
+    int64_t sparse_depth;
+    int64_t dense_len;      /* n_i, or -1 while unknown (list Open)  */
+    int64_t sparse_len;
+    int32_t dense_status;   /* EAHR_LIST_* at the end                */
+    int32_t sparse_status;
+    int32_t rounds;         /* depth rounds taken                    */
+    int32_t resolved;       /* 1 when the ordered Top-K was fixed    */
+} eahr_query_stats;
+
+/* eahr_topk -- the ordered Top-K of complete-list weighted RRF (Sec. 2.1) for
+ * B queries, without a preset per-list depth: every Open list with positive
+ * weight advances to cumulative depth depth0 * growth^j, and after every round
+ * positions are fixed one at a time with the unread-rank bounds (Sec. 2.2).
+ * Exhausted lists contribute their complete rankings.
+ *   q_dense   B x d float32 (host or device, q_ptr_kind); q_sparse: B queries.
+ *   out_ids   B x K; out_count[b] = q_K = min(K, |U+|) (no zero-score padding).
+ *   out_status[b] = 0 on success, EAHR_LIST_FAILED when a list failed.
+ *   stats     B entries or NULL.
+ * Returns EAHR_E_FAILED if any query failed (others are still valid). */
+int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index* sparse,
+              const float* q_dense, int32_t q_ptr_kind,
+              const eahr_sparse_query* q_sparse, int32_t B, const eahr_params* params,
+              int64_t* out_ids, int32_t* out_count, int32_t* out_status,
+              eahr_query_stats* stats);
+
+/* eahr_fuse_lists -- the same fusion over two complete rankings given as host
+ * arrays of distinct ids (e.g. controlled rank streams, Sec. 3.4).  Both lists
+ * advance together: by `step` ranks per round (step > 0, certification after
+ * every step) or to cumulative depth depth0 * growth^j (step = 0).  A list is
+ * Exhausted once all of it has been read.  Host only; no GPU involved.
+ *   out_ids  K entries (q_K valid, rest -1);  stats  one entry or NULL. */
+int eahr_fuse_lists(const int64_t* list_d, int64_t n_d, const int64_t* list_s,
+                    int64_t n_s, const eahr_params* params, int32_t step,
+                    int64_t* out_ids, int32_t* out_count, eahr_query_stats* stats);
+
+/* Last error message of the calling thread (static storage, never NULL). */
+const char* eahr_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* EAHR_H */

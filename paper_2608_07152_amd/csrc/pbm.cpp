@@ -1,0 +1,227 @@
+// Posting Block-Max (PBM): resumable exact sparse ranking on the host
+// (Sec. 2.3.2, App. A.2).
+//
+// The identifier space is cut into contiguous ranges of `range_size` ids.
+// For every term and range the index keeps m_t(R), the largest impact of the
+// term inside R (absent: no entry, i.e. 0).  A query's range bound
+// H(R) = sum_t q_t m_t(R) and every document score S(x) = sum_t q_t p_t(x) are
+// accumulated in float32 in ascending term order, one rounding per multiply
+// and add, so H(R) >= S(x) for every x in R (App. A.2).  Ranges are expanded
+// in (H descending, first id ascending) order; a scored item is published
+// once no unexpanded range can hold an item that precedes it.
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <memory>
+#include <new>
+#include <queue>
+#include <vector>
+
+#include "common.h"
+#include "eahr.h"
+#include "pbm_internal.h"
+
+extern "C" int pbm_build(const int64_t* term_ptr, int32_t vocab, const int32_t* docs,
+                         const float* impacts, int64_t n_docs, int32_t range_size,
+                         pbm_index** out) {
+    if (!out) EAHR_FAIL(EAHR_E_INVALID, "pbm_build: out is NULL");
+    *out = nullptr;
+    if (!term_ptr || vocab < 0 || n_docs < 0 || range_size < 1)
+        EAHR_FAIL(EAHR_E_INVALID, "pbm_build: bad arguments");
+    if (term_ptr[0] != 0) EAHR_FAIL(EAHR_E_INVALID, "pbm_build: term_ptr[0] != 0");
+    for (int32_t t = 0; t < vocab; ++t)
+        if (term_ptr[t + 1] < term_ptr[t]) EAHR_FAIL(EAHR_E_INVALID, "pbm_build: term_ptr not monotone");
+    const int64_t P = term_ptr[vocab];
+    if (P > 0 && (!docs || !impacts)) EAHR_FAIL(EAHR_E_INVALID, "pbm_build: NULL postings");
+    std::unique_ptr<pbm_index> ix(new (std::nothrow) pbm_index());
+    if (!ix) EAHR_FAIL(EAHR_E_OOM, "pbm_build: host allocation");
+    ix->vocab = vocab;
+    ix->n_docs = n_docs;
+    ix->range_size = range_size;
+    ix->n_ranges = (n_docs + range_size - 1) / range_size;
+    try {
+        ix->term_ptr.assign(term_ptr, term_ptr + vocab + 1);
+        ix->docs.assign(docs, docs + P);
+        ix->imp.assign(impacts, impacts + P);
+        ix->bm_ptr.assign(static_cast<size_t>(vocab) + 1, 0);
+    } catch (const std::bad_alloc&) {
+        EAHR_FAIL(EAHR_E_OOM, "pbm_build: host allocation");
+    }
+    for (int32_t t = 0; t < vocab; ++t) {
+        int64_t cur_range = -1;
+        for (int64_t p = term_ptr[t]; p < term_ptr[t + 1]; ++p) {
+            const int32_t x = docs[p];
+            const float v = impacts[p];
+            if (x < 0 || x >= n_docs) EAHR_FAIL(EAHR_E_INVALID, "pbm_build: doc id out of range");
+            if (p > term_ptr[t] && docs[p - 1] >= x)
+                EAHR_FAIL(EAHR_E_INVALID, "pbm_build: docs of term %d not strictly ascending", t);
+            if (!std::isfinite(v) || v < 0.0f)
+                EAHR_FAIL(EAHR_E_INVALID, "pbm_build: impact must be finite and >= 0");
+            const int64_t r = x / range_size;
+            if (r != cur_range) {
+                ix->bm_range.push_back(r);
+                ix->bm_max.push_back(v);
+                ix->bm_off.push_back(p);
+                cur_range = r;
+            } else {
+                ix->bm_max.back() = std::max(ix->bm_max.back(), v);
+            }
+        }
+        ix->bm_ptr[t + 1] = static_cast<int64_t>(ix->bm_range.size());
+    }
+    *out = ix.release();
+    return EAHR_OK;
+}
+
+extern "C" void pbm_free(pbm_index* ix) { delete ix; }
+
+extern "C" int pbm_debug_set_blockmax(pbm_index* ix, int32_t term, int64_t range, float value) {
+    if (!ix || term < 0 || term >= ix->vocab) EAHR_FAIL(EAHR_E_INVALID, "pbm_debug_set_blockmax: bad term");
+    for (int64_t e = ix->bm_ptr[term]; e < ix->bm_ptr[term + 1]; ++e) {
+        if (ix->bm_range[e] == range) {
+            ix->bm_max[e] = value;
+            return EAHR_OK;
+        }
+    }
+    EAHR_FAIL(EAHR_E_INVALID, "pbm_debug_set_blockmax: term has no postings in range");
+}
+
+// entry of `term` for `range`, or -1
+static int64_t find_entry(const pbm_index* ix, int32_t term, int64_t range) {
+    const int64_t* b = ix->bm_range.data() + ix->bm_ptr[term];
+    const int64_t* e = ix->bm_range.data() + ix->bm_ptr[term + 1];
+    const int64_t* it = std::lower_bound(b, e, range);
+    if (it == e || *it != range) return -1;
+    return it - ix->bm_range.data();
+}
+
+extern "C" int pbm_open(const pbm_index* ix, const eahr_sparse_query* q, pbm_state** out) {
+    if (!out) EAHR_FAIL(EAHR_E_INVALID, "pbm_open: out is NULL");
+    *out = nullptr;
+    if (!ix || !q || q->n_terms < 0 || (q->n_terms > 0 && (!q->terms || !q->weights)))
+        EAHR_FAIL(EAHR_E_INVALID, "pbm_open: bad arguments");
+    std::unique_ptr<pbm_state> st(new (std::nothrow) pbm_state());
+    if (!st) EAHR_FAIL(EAHR_E_OOM, "pbm_open: host allocation");
+    st->ix = ix;
+    std::vector<std::pair<int32_t, float>> tw;
+    for (int32_t i = 0; i < q->n_terms; ++i) {
+        const int32_t t = q->terms[i];
+        const float w = q->weights[i];
+        if (t < 0 || t >= ix->vocab) EAHR_FAIL(EAHR_E_INVALID, "pbm_open: term id out of range");
+        if (!std::isfinite(w) || w < 0.0f) EAHR_FAIL(EAHR_E_INVALID, "pbm_open: weight must be finite and >= 0");
+        tw.emplace_back(t, w);
+    }
+    std::sort(tw.begin(), tw.end());
+    for (size_t i = 1; i < tw.size(); ++i)
+        if (tw[i].first == tw[i - 1].first) EAHR_FAIL(EAHR_E_INVALID, "pbm_open: duplicate term");
+    for (auto& p : tw) {
+        if (p.second == 0.0f) continue;   // a zero weight contributes exactly 0
+        st->terms.push_back(p.first);
+        st->w.push_back(p.second);
+    }
+    // H(R) in ascending term order over the ranges any query term touches
+    std::vector<float> H(static_cast<size_t>(ix->n_ranges), 0.0f);
+    std::vector<uint8_t> touched(static_cast<size_t>(ix->n_ranges), 0);
+    std::vector<int64_t> list;
+    for (size_t i = 0; i < st->terms.size(); ++i) {
+        const int32_t t = st->terms[i];
+        const float w = st->w[i];
+        for (int64_t e = ix->bm_ptr[t]; e < ix->bm_ptr[t + 1]; ++e) {
+            const int64_t r = ix->bm_range[e];
+            const float c = w * ix->bm_max[e];
+            H[r] = H[r] + c;
+            if (!touched[r]) {
+                touched[r] = 1;
+                list.push_back(r);
+            }
+        }
+    }
+    for (int64_t r : list)
+        if (H[r] > 0.0f) st->ranges.push(pbm_state::Range{H[r], r});
+    *out = st.release();
+    return EAHR_OK;
+}
+
+// Score every document of range r that carries a query term and queue the
+// positive ones; fails when a score exceeds the range bound (metadata that
+// does not cover its postings, App. A.2).
+static bool expand(pbm_state* st, const pbm_state::Range& R) {
+    const pbm_index* ix = st->ix;
+    const int64_t start = R.r * ix->range_size;
+    const int64_t len = std::min<int64_t>(ix->range_size, ix->n_docs - start);
+    if (st->acc.size() < static_cast<size_t>(len)) {
+        st->acc.assign(static_cast<size_t>(len), 0.0f);
+        st->seen.assign(static_cast<size_t>(len), 0);
+    }
+    st->touched.clear();
+    for (size_t i = 0; i < st->terms.size(); ++i) {
+        const int32_t t = st->terms[i];
+        const int64_t e = find_entry(ix, t, R.r);
+        if (e < 0) continue;
+        const int64_t p_end = (e + 1 < ix->bm_ptr[t + 1]) ? ix->bm_off[e + 1] : ix->term_ptr[t + 1];
+        const float w = st->w[i];
+        st->postings_visited += p_end - ix->bm_off[e];
+        for (int64_t p = ix->bm_off[e]; p < p_end; ++p) {
+            const int64_t off = ix->docs[p] - start;
+            const float c = w * ix->imp[p];
+            st->acc[off] = st->acc[off] + c;
+            if (!st->seen[off]) {
+                st->seen[off] = 1;
+                st->touched.push_back(static_cast<int32_t>(off));
+            }
+        }
+    }
+    bool ok = true;
+    for (int32_t off : st->touched) {
+        const float s = st->acc[off];
+        if (s > R.H) ok = false;
+        if (s > 0.0f) st->items.push(pbm_state::Item{s, start + off});
+        st->acc[off] = 0.0f;
+        st->seen[off] = 0;
+    }
+    return ok;
+}
+
+static bool can_publish(const pbm_state* st, const pbm_state::Item& it) {
+    if (st->ranges.empty()) return true;
+    const auto& R = st->ranges.top();
+    const int64_t start = R.r * st->ix->range_size;
+    return it.s > R.H || (it.s == R.H && it.id < start);
+}
+
+extern "C" int pbm_next(pbm_state* st, int32_t m, int64_t* ids, float* scores, int32_t* count,
+                        int32_t* status) {
+    if (!st || m < 0 || (m > 0 && (!ids || !scores)) || !count || !status)
+        EAHR_FAIL(EAHR_E_INVALID, "pbm_next: bad arguments");
+    int32_t n = 0;
+    if (!st->failed) {
+        while (n < m) {
+            while (n < m && !st->items.empty() && can_publish(st, st->items.top())) {
+                const auto it = st->items.top();
+                st->items.pop();
+                ids[n] = it.id;
+                scores[n] = it.s;
+                ++n;
+            }
+            if (n == m) break;
+            if (st->ranges.empty()) break;   // items empty too: list complete
+            const auto R = st->ranges.top();
+            st->ranges.pop();
+            st->ranges_expanded += 1;
+            if (!expand(st, R)) {
+                st->failed = true;
+                n = 0;
+                break;
+            }
+        }
+    }
+    st->emitted += n;
+    *count = n;
+    if (st->failed) *status = EAHR_LIST_FAILED;
+    else if (st->ranges.empty() && st->items.empty()) *status = EAHR_LIST_EXHAUSTED;
+    else *status = EAHR_LIST_OPEN;
+    return EAHR_OK;
+}
+
+extern "C" void pbm_close(pbm_state* st) { delete st; }

@@ -1,0 +1,55 @@
+// Host structures of the Posting Block-Max sparse channel.
+#pragma once
+#include <cstdint>
+#include <queue>
+#include <vector>
+
+#include "eahr.h"
+
+struct pbm_index {
+    int32_t vocab = 0;
+    int64_t n_docs = 0;
+    int32_t range_size = 1;
+    int64_t n_ranges = 0;
+    std::vector<int64_t> term_ptr;   // vocab + 1
+    std::vector<int32_t> docs;       // postings, ascending per term
+    std::vector<float> imp;
+    // block-max entries of term t: [bm_ptr[t], bm_ptr[t+1]), ascending range
+    std::vector<int64_t> bm_ptr;
+    std::vector<int64_t> bm_range;   // range number
+    std::vector<float> bm_max;       // m_t(R)
+    std::vector<int64_t> bm_off;     // first posting of the term inside the range
+};
+
+struct pbm_state {
+    struct Range {
+        float H;
+        int64_t r;
+    };
+    struct RangeOrder {   // max-heap on (H desc, first id asc)
+        bool operator()(const Range& a, const Range& b) const {
+            return a.H < b.H || (a.H == b.H && a.r > b.r);
+        }
+    };
+    struct Item {
+        float s;
+        int64_t id;
+    };
+    struct ItemOrder {    // max-heap on (S desc, id asc)
+        bool operator()(const Item& a, const Item& b) const {
+            return a.s < b.s || (a.s == b.s && a.id > b.id);
+        }
+    };
+    const pbm_index* ix = nullptr;
+    std::vector<int32_t> terms;   // ascending term ids with nonzero weight
+    std::vector<float> w;
+    std::priority_queue<Range, std::vector<Range>, RangeOrder> ranges;
+    std::priority_queue<Item, std::vector<Item>, ItemOrder> items;
+    std::vector<float> acc;       // per-range scratch
+    std::vector<uint8_t> seen;
+    std::vector<int32_t> touched;
+    int64_t emitted = 0;
+    int64_t ranges_expanded = 0;
+    int64_t postings_visited = 0;
+    bool failed = false;
+};

@@ -1,0 +1,725 @@
+// Host runtime of the PVS dense channel: index storage in HBM, snapshots,
+// per-query resumable state and the scan -> rescore -> sort -> certify driver.
+//
+// Certification rule (Sec. 2.3.1 exact prefixes): a scan with threshold tau
+// collects every eligible visible row with hi >= tau, rescores them in float32
+// and certifies those with s32 >= tau.  Any row left out has
+// s32 <= hi < tau, so the certified rows, in (s32 desc, id asc) order, are
+// exactly the next ranks after the last certified key.  tau only changes the
+// work done, never the result; it is estimated from a sampled subset of
+// blocks and lowered when a scan certifies too few ranks.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <limits>
+#include <memory>
+#include <new>
+#include <vector>
+
+#include "common.h"
+#include "eahr.h"
+#include "pvs_internal.h"
+#include "pvs_kernels.h"
+
+using pvs::ScanQ;
+
+namespace {
+
+int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+// Smallest float32 >= a / (1 - a), a = (8m + 64) * 2^-23 (App. A.1): num/den
+// with num = 8m + 64 and den = 2^23 - num, compared exactly in integers.
+float gamma_of(int32_t m) {
+    const int64_t num = 8LL * m + 64;
+    const int64_t den = (1LL << 23) - num;
+    float f = static_cast<float>(static_cast<double>(num) / static_cast<double>(den));
+    auto ge = [&](float x) {  // x >= num / den  <=>  M * den >= num * 2^-e
+        int e;
+        const double mant = std::frexp(static_cast<double>(x), &e);   // x = mant * 2^e
+        const __int128 M = static_cast<__int128>(std::ldexp(mant, 53));  // x = M * 2^(e-53)
+        const int sh = 53 - e;                                          // > 0 here
+        return M * den >= static_cast<__int128>(num) << sh;
+    };
+    while (!ge(f)) f = std::nextafter(f, std::numeric_limits<float>::infinity());
+    while (ge(std::nextafter(f, 0.0f))) f = std::nextafter(f, 0.0f);
+    return f;
+}
+
+template <typename T>
+int dev_alloc(T** p, size_t count) {
+    *p = nullptr;
+    if (count == 0) count = 1;
+    HIP_TRY(hipMalloc(reinterpret_cast<void**>(p), count * sizeof(T)));
+    return EAHR_OK;
+}
+
+template <typename T>
+void dev_free(T*& p) {
+    if (p) (void)hipFree(p);
+    p = nullptr;
+}
+
+bool is_device_ptr(const void* p) {
+    hipPointerAttribute_t a;
+    if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+        (void)hipGetLastError();
+        return false;
+    }
+    return a.type == hipMemoryTypeDevice;
+}
+
+}  // namespace
+
+// ======================================================================= index
+pvs_index::~pvs_index() {
+    dev_free(codes);
+    dev_free(scale);
+    dev_free(vnorm);
+    dev_free(enorm);
+    dev_free(frows);
+    dev_free(live);
+    dev_free(flags);
+    dev_free(staging);
+    for (auto& s : snaps) dev_free(s.vis);
+}
+
+static int index_grow(pvs_index* ix, int64_t need_rows) {
+    if (need_rows <= ix->cap) return EAHR_OK;
+    int64_t cap = std::max<int64_t>(need_rows, ix->cap + ix->cap / 2);
+    cap = round_up(std::max<int64_t>(cap, 64), 64);
+    int8_t* codes;
+    float *scale, *vnorm, *enorm, *frows;
+    uint64_t* live;
+    EAHR_TRY(dev_alloc(&codes, static_cast<size_t>(cap) * ix->dp));
+    EAHR_TRY(dev_alloc(&scale, cap));
+    EAHR_TRY(dev_alloc(&vnorm, cap));
+    EAHR_TRY(dev_alloc(&enorm, cap));
+    EAHR_TRY(dev_alloc(&frows, static_cast<size_t>(cap) * ix->df));
+    EAHR_TRY(dev_alloc(&live, cap / 64));
+    hipStream_t s = ix->stream;
+    HIP_TRY(hipMemsetAsync(codes, 0, static_cast<size_t>(cap) * ix->dp, s));
+    HIP_TRY(hipMemsetAsync(scale, 0, cap * sizeof(float), s));
+    HIP_TRY(hipMemsetAsync(vnorm, 0, cap * sizeof(float), s));
+    HIP_TRY(hipMemsetAsync(enorm, 0, cap * sizeof(float), s));
+    HIP_TRY(hipMemsetAsync(live, 0, cap / 64 * sizeof(uint64_t), s));
+    if (ix->cap > 0) {
+        HIP_TRY(hipMemcpyAsync(codes, ix->codes, static_cast<size_t>(ix->cap) * ix->dp,
+                               hipMemcpyDeviceToDevice, s));
+        HIP_TRY(hipMemcpyAsync(scale, ix->scale, ix->cap * sizeof(float), hipMemcpyDeviceToDevice, s));
+        HIP_TRY(hipMemcpyAsync(vnorm, ix->vnorm, ix->cap * sizeof(float), hipMemcpyDeviceToDevice, s));
+        HIP_TRY(hipMemcpyAsync(enorm, ix->enorm, ix->cap * sizeof(float), hipMemcpyDeviceToDevice, s));
+        HIP_TRY(hipMemcpyAsync(frows, ix->frows, static_cast<size_t>(ix->cap) * ix->df * sizeof(float),
+                               hipMemcpyDeviceToDevice, s));
+        HIP_TRY(hipMemcpyAsync(live, ix->live, ix->cap / 64 * sizeof(uint64_t), hipMemcpyDeviceToDevice, s));
+        HIP_TRY(hipStreamSynchronize(s));
+    }
+    dev_free(ix->codes);
+    dev_free(ix->scale);
+    dev_free(ix->vnorm);
+    dev_free(ix->enorm);
+    dev_free(ix->frows);
+    dev_free(ix->live);
+    ix->codes = codes;
+    ix->scale = scale;
+    ix->vnorm = vnorm;
+    ix->enorm = enorm;
+    ix->frows = frows;
+    ix->live = live;
+    ix->cap = cap;
+    return EAHR_OK;
+}
+
+// Quantise n rows (host or device) into rows [row0, row0 + n) of the index.
+static int index_quantize(pvs_index* ix, const float* src, int64_t n, int32_t ptr_kind, int64_t row0) {
+    hipStream_t s = ix->stream;
+    HIP_TRY(hipMemsetAsync(ix->flags, 0, 4 * sizeof(uint32_t), s));
+    const bool dev = (ptr_kind == EAHR_PTR_DEVICE);
+    const int64_t chunk = 65536;
+    for (int64_t r = 0; r < n; r += chunk) {
+        const int64_t k = std::min(chunk, n - r);
+        const float* p = src + r * ix->d;
+        if (!dev) {
+            if (!ix->staging) EAHR_TRY(dev_alloc(&ix->staging, static_cast<size_t>(chunk) * ix->d));
+            HIP_TRY(hipMemcpyAsync(ix->staging, p, static_cast<size_t>(k) * ix->d * sizeof(float),
+                                   hipMemcpyHostToDevice, s));
+            p = ix->staging;
+        }
+        pvs::launch_quantize(p, k, ix->d, ix->d, row0 + r, true, ix->codes, ix->dp, ix->scale,
+                             ix->vnorm, ix->enorm, nullptr, ix->frows, ix->df, ix->flags, s);
+        HIP_TRY(hipGetLastError());
+        if (!dev) HIP_TRY(hipStreamSynchronize(s));   // staging buffer is reused
+    }
+    uint32_t fl[4];
+    HIP_TRY(hipMemcpyAsync(fl, ix->flags, sizeof(fl), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    if (fl[0]) EAHR_FAIL(EAHR_E_NONFINITE, "non-finite value in corpus rows");
+    float nv, nev;
+    std::memcpy(&nv, &fl[1], 4);
+    std::memcpy(&nev, &fl[2], 4);
+    ix->nv_max = std::max(ix->nv_max, nv);
+    ix->nev_max = std::max(ix->nev_max, nev);
+    return EAHR_OK;
+}
+
+static int take_snapshot(pvs_index* ix, int64_t* epoch) {
+    pvs_index::Snapshot sn;
+    sn.rows = ix->rows;
+    const int64_t words = std::max<int64_t>(1, (ix->rows + 63) / 64);
+    EAHR_TRY(dev_alloc(&sn.vis, words));
+    HIP_TRY(hipMemcpyAsync(sn.vis, ix->live, words * sizeof(uint64_t), hipMemcpyDeviceToDevice,
+                           ix->stream));
+    unsigned long long* cnt;
+    EAHR_TRY(dev_alloc(&cnt, 1));
+    HIP_TRY(hipMemsetAsync(cnt, 0, sizeof(unsigned long long), ix->stream));
+    pvs::launch_popcount(sn.vis, words, cnt, ix->stream);
+    unsigned long long h = 0;
+    HIP_TRY(hipMemcpyAsync(&h, cnt, sizeof(h), hipMemcpyDeviceToHost, ix->stream));
+    HIP_TRY(hipStreamSynchronize(ix->stream));
+    dev_free(cnt);
+    sn.visible = static_cast<int64_t>(h);
+    ix->snaps.push_back(sn);
+    if (epoch) *epoch = static_cast<int64_t>(ix->snaps.size()) - 1;
+    return EAHR_OK;
+}
+
+extern "C" int pvs_build(const float* corpus, int64_t n, int32_t d, int32_t ptr_kind, void* stream,
+                         pvs_index** out) {
+    if (!out) EAHR_FAIL(EAHR_E_INVALID, "pvs_build: out is NULL");
+    *out = nullptr;
+    if (n < 0 || d <= 0 || (n > 0 && !corpus)) EAHR_FAIL(EAHR_E_INVALID, "pvs_build: bad arguments");
+    if (d > pvs::kMaxDim) EAHR_FAIL(EAHR_E_RANGE, "pvs_build: d=%d exceeds %d", d, pvs::kMaxDim);
+    if (n >= (1LL << 31) - 64) EAHR_FAIL(EAHR_E_RANGE, "pvs_build: too many rows");
+    if (ptr_kind != EAHR_PTR_HOST && ptr_kind != EAHR_PTR_DEVICE)
+        EAHR_FAIL(EAHR_E_INVALID, "pvs_build: bad ptr_kind");
+    std::unique_ptr<pvs_index> ix(new (std::nothrow) pvs_index());
+    if (!ix) EAHR_FAIL(EAHR_E_OOM, "pvs_build: host allocation");
+    HIP_TRY(hipGetDevice(&ix->device));
+    ix->stream = static_cast<hipStream_t>(stream);
+    ix->d = d;
+    ix->dp = static_cast<int32_t>(round_up(d, 64));
+    ix->df = static_cast<int32_t>(round_up(d, 4));
+    ix->nchunk = ix->dp / 16;
+    ix->gamma = gamma_of(d);
+    EAHR_TRY(dev_alloc(&ix->flags, 4));
+    EAHR_TRY(index_grow(ix.get(), std::max<int64_t>(n, 64)));
+    if (n > 0) {
+        EAHR_TRY(index_quantize(ix.get(), corpus, n, ptr_kind, 0));
+        pvs::launch_set_bits(ix->live, 0, n, ix->stream);
+        HIP_TRY(hipGetLastError());
+    }
+    ix->rows = n;
+    EAHR_TRY(take_snapshot(ix.get(), nullptr));
+    *out = ix.release();
+    return EAHR_OK;
+}
+
+extern "C" int pvs_insert(pvs_index* ix, const float* rows, int64_t n_new, int32_t ptr_kind,
+                          int64_t* first_id) {
+    if (!ix || n_new < 0 || (n_new > 0 && !rows)) EAHR_FAIL(EAHR_E_INVALID, "pvs_insert: bad arguments");
+    if (ix->rows + n_new >= (1LL << 31) - 64) EAHR_FAIL(EAHR_E_RANGE, "pvs_insert: too many rows");
+    if (first_id) *first_id = ix->rows;
+    if (n_new == 0) return EAHR_OK;
+    EAHR_TRY(index_grow(ix, ix->rows + n_new));
+    EAHR_TRY(index_quantize(ix, rows, n_new, ptr_kind, ix->rows));
+    pvs::launch_set_bits(ix->live, ix->rows, n_new, ix->stream);
+    HIP_TRY(hipGetLastError());
+    ix->rows += n_new;
+    return EAHR_OK;
+}
+
+extern "C" int pvs_delete(pvs_index* ix, const int64_t* ids, int64_t n) {
+    if (!ix || n < 0 || (n > 0 && !ids)) EAHR_FAIL(EAHR_E_INVALID, "pvs_delete: bad arguments");
+    for (int64_t i = 0; i < n; ++i)
+        if (ids[i] < 0 || ids[i] >= ix->rows) EAHR_FAIL(EAHR_E_INVALID, "pvs_delete: id out of range");
+    if (n == 0) return EAHR_OK;
+    int64_t* d_ids;
+    EAHR_TRY(dev_alloc(&d_ids, n));
+    HIP_TRY(hipMemcpyAsync(d_ids, ids, n * sizeof(int64_t), hipMemcpyHostToDevice, ix->stream));
+    pvs::launch_clear_ids(ix->live, d_ids, n, ix->stream);
+    HIP_TRY(hipGetLastError());
+    HIP_TRY(hipStreamSynchronize(ix->stream));
+    dev_free(d_ids);
+    return EAHR_OK;
+}
+
+extern "C" int pvs_snapshot(pvs_index* ix, int64_t* epoch) {
+    if (!ix) EAHR_FAIL(EAHR_E_INVALID, "pvs_snapshot: NULL index");
+    return take_snapshot(ix, epoch);
+}
+
+extern "C" int pvs_info(const pvs_index* ix, int64_t epoch, int64_t* rows, int32_t* d,
+                        int64_t* visible) {
+    if (!ix || epoch < 0 || epoch >= static_cast<int64_t>(ix->snaps.size()))
+        EAHR_FAIL(EAHR_E_INVALID, "pvs_info: bad index or epoch");
+    if (rows) *rows = ix->snaps[epoch].rows;
+    if (d) *d = ix->d;
+    if (visible) *visible = ix->snaps[epoch].visible;
+    return EAHR_OK;
+}
+
+extern "C" void pvs_free(pvs_index* ix) { delete ix; }
+
+extern "C" int pvs_read_index(const pvs_index* ix, int64_t row0, int64_t n, int8_t* codes,
+                              float* meta) {
+    if (!ix || row0 < 0 || n < 0 || row0 + n > ix->rows) EAHR_FAIL(EAHR_E_INVALID, "pvs_read_index: bad range");
+    if (n == 0) return EAHR_OK;
+    const int64_t b0 = row0 / 64, b1 = (row0 + n - 1) / 64 + 1;
+    std::vector<int8_t> blk(static_cast<size_t>(b1 - b0) * 64 * ix->dp);
+    HIP_TRY(hipMemcpy(blk.data(), ix->codes + b0 * 64 * ix->dp, blk.size(), hipMemcpyDeviceToHost));
+    if (codes) {
+        for (int64_t i = 0; i < n; ++i) {
+            const int64_t r = row0 + i;
+            const int64_t rb = r / 64 - b0, rr = r % 64;
+            for (int32_t j = 0; j < ix->d; ++j) {
+                const int64_t off = ((rb * ix->nchunk + j / 16) * 64 + rr) * 16 + j % 16;
+                codes[i * ix->d + j] = blk[off];
+            }
+        }
+    }
+    if (meta) {
+        std::vector<float> s(n), a(n), e(n);
+        HIP_TRY(hipMemcpy(s.data(), ix->scale + row0, n * sizeof(float), hipMemcpyDeviceToHost));
+        HIP_TRY(hipMemcpy(a.data(), ix->vnorm + row0, n * sizeof(float), hipMemcpyDeviceToHost));
+        HIP_TRY(hipMemcpy(e.data(), ix->enorm + row0, n * sizeof(float), hipMemcpyDeviceToHost));
+        for (int64_t i = 0; i < n; ++i) {
+            meta[3 * i] = s[i];
+            meta[3 * i + 1] = a[i];
+            meta[3 * i + 2] = e[i];
+        }
+    }
+    return EAHR_OK;
+}
+
+// ======================================================================= state
+pvs_state::~pvs_state() {
+    dev_free(qcodes);
+    dev_free(qrows);
+    dev_free(qscale);
+    dev_free(qnorm);
+    dev_free(qenorm);
+    dev_free(qhnorm);
+    dev_free(qflags);
+    release_scan_buffers();
+    if (h_scanq) (void)hipHostFree(h_scanq);
+    if (h_counts) (void)hipHostFree(h_counts);
+    if (h_packed) (void)hipHostFree(h_packed);
+}
+
+void pvs_state::release_scan_buffers() {
+    dev_free(scanq);
+    dev_free(cand_row);
+    dev_free(cand_lo);
+    dev_free(cand_hi);
+    dev_free(keys);
+    dev_free(keys_tmp);
+    dev_free(counts);
+    dev_free(packed);
+    dev_free(sample);
+    buf_nq = 0;
+    buf_cap = 0;
+    buf_sample = 0;
+}
+
+// counts layout: [cand nq][cert nq][fail nq][offs nq + 1]
+static int ensure_scan_buffers(pvs_state* st, int32_t nq, int64_t cap, int64_t sample_ld) {
+    if (nq <= st->buf_nq && cap <= st->buf_cap && sample_ld <= st->buf_sample) return EAHR_OK;
+    nq = std::max(nq, st->buf_nq);
+    cap = std::max(cap, st->buf_cap);
+    sample_ld = std::max(sample_ld, st->buf_sample);
+    HIP_TRY(hipStreamSynchronize(st->ix->stream));
+    st->release_scan_buffers();
+    const size_t tot = static_cast<size_t>(nq) * cap;
+    EAHR_TRY(dev_alloc(&st->scanq, nq));
+    EAHR_TRY(dev_alloc(&st->cand_row, tot));
+    EAHR_TRY(dev_alloc(&st->cand_lo, tot));
+    EAHR_TRY(dev_alloc(&st->cand_hi, tot));
+    EAHR_TRY(dev_alloc(&st->keys, tot));
+    EAHR_TRY(dev_alloc(&st->keys_tmp, tot));
+    EAHR_TRY(dev_alloc(&st->counts, 4 * static_cast<size_t>(nq) + 1));
+    EAHR_TRY(dev_alloc(&st->packed, tot));
+    EAHR_TRY(dev_alloc(&st->sample, static_cast<size_t>(nq) * sample_ld));
+    if (st->h_scanq) (void)hipHostFree(st->h_scanq);
+    if (st->h_counts) (void)hipHostFree(st->h_counts);
+    if (st->h_packed) (void)hipHostFree(st->h_packed);
+    st->h_scanq = nullptr;
+    st->h_counts = nullptr;
+    st->h_packed = nullptr;
+    HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&st->h_scanq), nq * sizeof(ScanQ)));
+    HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&st->h_counts), (4 * static_cast<size_t>(nq) + 1) * sizeof(int32_t)));
+    HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&st->h_packed), tot * sizeof(uint64_t)));
+    st->buf_nq = nq;
+    st->buf_cap = cap;
+    st->buf_sample = sample_ld;
+    return EAHR_OK;
+}
+
+extern "C" int pvs_open(const pvs_index* ix, int64_t epoch, const float* q, int32_t B,
+                        int32_t ptr_kind, pvs_state** out) {
+    if (!out) EAHR_FAIL(EAHR_E_INVALID, "pvs_open: out is NULL");
+    *out = nullptr;
+    if (!ix || B <= 0 || !q) EAHR_FAIL(EAHR_E_INVALID, "pvs_open: bad arguments");
+    if (epoch < 0 || epoch >= static_cast<int64_t>(ix->snaps.size()))
+        EAHR_FAIL(EAHR_E_INVALID, "pvs_open: unknown epoch %lld", static_cast<long long>(epoch));
+    if (ptr_kind != EAHR_PTR_HOST && ptr_kind != EAHR_PTR_DEVICE)
+        EAHR_FAIL(EAHR_E_INVALID, "pvs_open: bad ptr_kind");
+    std::unique_ptr<pvs_state> st(new (std::nothrow) pvs_state());
+    if (!st) EAHR_FAIL(EAHR_E_OOM, "pvs_open: host allocation");
+    st->ix = ix;
+    st->epoch = epoch;
+    st->B = B;
+    st->n_rows = ix->snaps[epoch].rows;
+    st->n_vis = ix->snaps[epoch].visible;
+    st->vis = ix->snaps[epoch].vis;
+    hipStream_t s = ix->stream;
+    EAHR_TRY(dev_alloc(&st->qcodes, static_cast<size_t>(B) * ix->dp));
+    EAHR_TRY(dev_alloc(&st->qrows, static_cast<size_t>(B) * ix->df));
+    EAHR_TRY(dev_alloc(&st->qscale, B));
+    EAHR_TRY(dev_alloc(&st->qnorm, B));
+    EAHR_TRY(dev_alloc(&st->qenorm, B));
+    EAHR_TRY(dev_alloc(&st->qhnorm, B));
+    EAHR_TRY(dev_alloc(&st->qflags, 4));
+    HIP_TRY(hipMemsetAsync(st->qflags, 0, 4 * sizeof(uint32_t), s));
+    const float* src = q;
+    float* tmp = nullptr;
+    if (ptr_kind == EAHR_PTR_HOST) {
+        EAHR_TRY(dev_alloc(&tmp, static_cast<size_t>(B) * ix->d));
+        HIP_TRY(hipMemcpyAsync(tmp, q, static_cast<size_t>(B) * ix->d * sizeof(float),
+                               hipMemcpyHostToDevice, s));
+        src = tmp;
+    }
+    pvs::launch_quantize(src, B, ix->d, ix->d, 0, false, st->qcodes, ix->dp, st->qscale, st->qnorm,
+                         st->qenorm, st->qhnorm, st->qrows, ix->df, st->qflags, s);
+    HIP_TRY(hipGetLastError());
+    std::vector<float> sc(B), nq(B), ne(B), nh(B);
+    uint32_t fl[4];
+    HIP_TRY(hipMemcpyAsync(sc.data(), st->qscale, B * sizeof(float), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipMemcpyAsync(nq.data(), st->qnorm, B * sizeof(float), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipMemcpyAsync(ne.data(), st->qenorm, B * sizeof(float), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipMemcpyAsync(nh.data(), st->qhnorm, B * sizeof(float), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipMemcpyAsync(fl, st->qflags, sizeof(fl), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    dev_free(tmp);
+    if (fl[0]) EAHR_FAIL(EAHR_E_NONFINITE, "pvs_open: non-finite value in a query");
+    st->q.resize(B);
+    const double NV = ix->nv_max, NEV = ix->nev_max, g = ix->gamma;
+    for (int32_t b = 0; b < B; ++b) {
+        auto& Q = st->q[b];
+        Q.sq = sc[b];
+        Q.nq = nq[b];
+        Q.neq = ne[b];
+        Q.nqh = nh[b];
+        // bound of E + G over every row: |c| <= ||q_hat|| (||v|| + ||e_v||)
+        const double E = ne[b] * NV + nh[b] * NEV;
+        const double c = nh[b] * (NV + NEV);
+        const double G = (c + E + nq[b] * NV) * g;
+        Q.wmax = static_cast<float>((E + G) * 1.01 + 1e-30);
+    }
+    *out = st.release();
+    return EAHR_OK;
+}
+
+extern "C" void pvs_close(pvs_state* st) {
+    if (st && st->ix) (void)hipStreamSynchronize(st->ix->stream);
+    delete st;
+}
+
+extern "C" int pvs_read_query(const pvs_state* st, int8_t* codes, float* meta) {
+    if (!st) EAHR_FAIL(EAHR_E_INVALID, "pvs_read_query: NULL state");
+    const pvs_index* ix = st->ix;
+    if (codes) {
+        std::vector<int8_t> all(static_cast<size_t>(st->B) * ix->dp);
+        HIP_TRY(hipMemcpy(all.data(), st->qcodes, all.size(), hipMemcpyDeviceToHost));
+        for (int32_t b = 0; b < st->B; ++b)
+            std::memcpy(codes + static_cast<size_t>(b) * ix->d, all.data() + static_cast<size_t>(b) * ix->dp, ix->d);
+    }
+    if (meta) {
+        for (int32_t b = 0; b < st->B; ++b) {
+            meta[4 * b] = st->q[b].sq;
+            meta[4 * b + 1] = st->q[b].nq;
+            meta[4 * b + 2] = st->q[b].nqh;
+            meta[4 * b + 3] = st->q[b].neq;
+        }
+    }
+    return EAHR_OK;
+}
+
+static ScanQ make_scanq(const pvs_state* st, int32_t b) {
+    const auto& Q = st->q[b];
+    ScanQ s{};
+    s.qi = b;
+    s.tau = -std::numeric_limits<float>::infinity();
+    s.has_cert = Q.has_cert ? 1 : 0;
+    s.s_cert = Q.s_cert;
+    s.id_cert = Q.id_cert;
+    s.k = 0;
+    s.sq = Q.sq;
+    s.nq = Q.nq;
+    s.nqh = Q.nqh;
+    s.neq = Q.neq;
+    s.wmax = Q.wmax;
+    return s;
+}
+
+static pvs::IndexView view_of(const pvs_index* ix) {
+    pvs::IndexView v;
+    v.codes = reinterpret_cast<const uint4*>(ix->codes);
+    v.scale = ix->scale;
+    v.vnorm = ix->vnorm;
+    v.enorm = ix->enorm;
+    v.rows = ix->frows;
+    v.d = ix->d;
+    v.dp = ix->dp;
+    v.df = ix->df;
+    v.nchunk = ix->nchunk;
+    return v;
+}
+
+extern "C" int pvs_intervals(const pvs_state* st, int32_t b, const int64_t* rows, int64_t n,
+                             float* lo, float* hi) {
+    if (!st || b < 0 || b >= st->B || n < 0 || (n > 0 && (!rows || !lo || !hi)))
+        EAHR_FAIL(EAHR_E_INVALID, "pvs_intervals: bad arguments");
+    for (int64_t i = 0; i < n; ++i)
+        if (rows[i] < 0 || rows[i] >= st->n_rows) EAHR_FAIL(EAHR_E_INVALID, "pvs_intervals: row out of range");
+    if (n == 0) return EAHR_OK;
+    const pvs_index* ix = st->ix;
+    hipStream_t s = ix->stream;
+    ScanQ q = make_scanq(st, b);
+    ScanQ* dq;
+    int64_t* dr;
+    float *dlo, *dhi;
+    EAHR_TRY(dev_alloc(&dq, 1));
+    EAHR_TRY(dev_alloc(&dr, n));
+    EAHR_TRY(dev_alloc(&dlo, n));
+    EAHR_TRY(dev_alloc(&dhi, n));
+    HIP_TRY(hipMemcpyAsync(dq, &q, sizeof(q), hipMemcpyHostToDevice, s));
+    HIP_TRY(hipMemcpyAsync(dr, rows, n * sizeof(int64_t), hipMemcpyHostToDevice, s));
+    pvs::launch_intervals(view_of(ix), st->qcodes, dq, ix->gamma, dr, n, dlo, dhi, s);
+    HIP_TRY(hipGetLastError());
+    HIP_TRY(hipMemcpyAsync(lo, dlo, n * sizeof(float), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipMemcpyAsync(hi, dhi, n * sizeof(float), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    dev_free(dq);
+    dev_free(dr);
+    dev_free(dlo);
+    dev_free(dhi);
+    return EAHR_OK;
+}
+
+extern "C" int pvs_scores(const pvs_state* st, int32_t b, const int64_t* rows, int64_t n,
+                          float* scores) {
+    if (!st || b < 0 || b >= st->B || n < 0 || (n > 0 && (!rows || !scores)))
+        EAHR_FAIL(EAHR_E_INVALID, "pvs_scores: bad arguments");
+    for (int64_t i = 0; i < n; ++i)
+        if (rows[i] < 0 || rows[i] >= st->n_rows) EAHR_FAIL(EAHR_E_INVALID, "pvs_scores: row out of range");
+    if (n == 0) return EAHR_OK;
+    const pvs_index* ix = st->ix;
+    hipStream_t s = ix->stream;
+    int64_t* dr;
+    float* dout;
+    EAHR_TRY(dev_alloc(&dr, n));
+    EAHR_TRY(dev_alloc(&dout, n));
+    HIP_TRY(hipMemcpyAsync(dr, rows, n * sizeof(int64_t), hipMemcpyHostToDevice, s));
+    pvs::launch_scores(view_of(ix), st->qrows, b, dr, n, dout, s);
+    HIP_TRY(hipGetLastError());
+    HIP_TRY(hipMemcpyAsync(scores, dout, n * sizeof(float), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    dev_free(dr);
+    dev_free(dout);
+    return EAHR_OK;
+}
+
+// ============================================================== scan driver
+static inline float key_score(uint64_t key) {
+    const uint32_t k = ~static_cast<uint32_t>(key >> 32);
+    const uint32_t bits = (k & 0x80000000u) ? (k & 0x7fffffffu) : ~k;
+    float f;
+    std::memcpy(&f, &bits, 4);
+    return f;
+}
+
+// Certified ranks of query b that may still have lo <= s_cert: they score at
+// most s_cert + 2 * wmax, because lo >= s32 - 2 * wmax.
+static int64_t lower_overlap(const pvs_state* st, int32_t b) {
+    const auto& Q = st->q[b];
+    if (!Q.has_cert) return 0;
+    const double lim = static_cast<double>(Q.s_cert) + 2.0 * Q.wmax;
+    int64_t a = 0;
+    for (int64_t i = static_cast<int64_t>(Q.cache_score.size()) - 1; i >= 0; --i) {
+        if (Q.cache_score[i] > lim) break;
+        ++a;
+    }
+    return a;
+}
+
+// One scan round over the queries in `todo`; removes the queries it finished.
+static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
+    const pvs_index* ix = st->ix;
+    hipStream_t s = ix->stream;
+    const int32_t nq = static_cast<int32_t>(todo.size());
+    const int64_t nblocks = (st->n_rows + 63) / 64;
+    if (nblocks == 0) {
+        for (int32_t b : todo) st->q[b].cert_exhausted = true;
+        todo.clear();
+        return EAHR_OK;
+    }
+    int64_t stride = 1;
+    while (nblocks / (stride * 2) >= pvs::kSampleBlocks) stride *= 2;
+    const int64_t nsb = (nblocks + stride - 1) / stride;
+    const int64_t sample_ld = nsb * 64;
+    const double frac = static_cast<double>(nsb) / static_cast<double>(nblocks);
+
+    int64_t cap = std::max<int64_t>(st->buf_cap, pvs::kMinCap);
+    for (int32_t b : todo) cap = std::max(cap, st->q[b].cap_hint);
+    cap = round_up(cap, 256);
+    EAHR_TRY(ensure_scan_buffers(st, nq, cap, sample_ld));
+    cap = st->buf_cap;
+
+    const int64_t mmin = std::max<int64_t>(pvs::kTargetMin, std::min<int64_t>(pvs::kTargetMax, pvs::kTargetBudget / nq));
+    for (int32_t i = 0; i < nq; ++i) {
+        const int32_t b = todo[i];
+        auto& Q = st->q[b];
+        ScanQ sq = make_scanq(st, b);
+        const int64_t avail = static_cast<int64_t>(Q.cache_score.size()) - Q.emitted;
+        const int64_t need = std::max<int64_t>(1, m - avail);
+        const int64_t target = std::max(need, mmin) + lower_overlap(st, b);
+        double k = (stride == 1) ? static_cast<double>(target)
+                                 : std::max(4.0, std::ceil(2.0 * target * frac));
+        for (int r = 0; r < Q.retries; ++r) k *= 4.0;
+        sq.k = static_cast<int32_t>(std::min(k, 2.0e9));
+        st->h_scanq[i] = sq;
+    }
+    int32_t* d_cand = st->counts;
+    int32_t* d_cert = st->counts + nq;
+    int32_t* d_fail = st->counts + 2 * nq;
+    int32_t* d_offs = st->counts + 3 * nq;
+    HIP_TRY(hipMemcpyAsync(st->scanq, st->h_scanq, nq * sizeof(ScanQ), hipMemcpyHostToDevice, s));
+    HIP_TRY(hipMemsetAsync(st->counts, 0, (4 * static_cast<size_t>(nq) + 1) * sizeof(int32_t), s));
+    const pvs::IndexView v = view_of(ix);
+    pvs::launch_scan(v, st->vis, nblocks, st->qcodes, st->scanq, nq, ix->gamma, true, stride,
+                     st->sample, sample_ld, nullptr, nullptr, nullptr, nullptr, 0, s);
+    pvs::launch_select(st->sample, sample_ld, sample_ld, st->scanq, nq, s);
+    pvs::launch_scan(v, st->vis, nblocks, st->qcodes, st->scanq, nq, ix->gamma, false, 1, nullptr,
+                     0, st->cand_row, st->cand_lo, st->cand_hi, d_cand, cap, s);
+    HIP_TRY(hipGetLastError());
+    HIP_TRY(hipMemcpyAsync(st->h_counts, d_cand, nq * sizeof(int32_t), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    st->stats.scans += 1;
+    st->stats.sample_scans += 1;
+    st->stats.rows_scanned += nblocks * 64;
+    st->stats.bytes_scanned += nblocks * 64 * (static_cast<int64_t>(ix->d) + 12) + nblocks * 8;
+
+    std::vector<int32_t> cand(st->h_counts, st->h_counts + nq);
+    int64_t max_cnt = 0, total = 0;
+    for (int32_t i = 0; i < nq; ++i) {
+        const int64_t c = std::min<int64_t>(cand[i], cap);
+        max_cnt = std::max(max_cnt, c);
+        total += c;
+    }
+    pvs::launch_rescore(v, st->qrows, st->scanq, nq, st->cand_row, st->cand_lo, st->cand_hi, d_cand,
+                        cap, max_cnt, st->keys, d_cert, d_fail, s);
+    uint64_t* sorted = pvs::launch_segmented_sort(st->keys, st->keys_tmp, d_cand, nq, cap, max_cnt, s);
+    pvs::launch_pack(sorted, d_cert, nq, cap, max_cnt, d_offs, st->packed, s);
+    HIP_TRY(hipGetLastError());
+    HIP_TRY(hipMemcpyAsync(st->h_counts + nq, d_cert, (3 * static_cast<size_t>(nq) + 1) * sizeof(int32_t),
+                           hipMemcpyDeviceToHost, s));
+    if (total > 0)
+        HIP_TRY(hipMemcpyAsync(st->h_packed, st->packed, total * sizeof(uint64_t), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    const int32_t* h_cert = st->h_counts + nq;
+    const int32_t* h_fail = st->h_counts + 2 * nq;
+    const int32_t* h_offs = st->h_counts + 3 * nq;
+
+    std::vector<int32_t> keep;
+    int64_t grow = 0;
+    for (int32_t i = 0; i < nq; ++i) {
+        const int32_t b = todo[i];
+        auto& Q = st->q[b];
+        if (h_fail[i]) {
+            Q.failed = true;
+            continue;
+        }
+        if (cand[i] > cap) {   // candidate list overflowed: redo with room for all
+            Q.cap_hint = round_up(static_cast<int64_t>(cand[i]) + cand[i] / 4 + 256, 256);
+            grow = std::max(grow, Q.cap_hint);
+            keep.push_back(b);
+            continue;
+        }
+        st->stats.candidates += cand[i];
+        const int64_t c = h_cert[i];
+        const uint64_t* kp = st->h_packed + h_offs[i];
+        Q.cache_id.reserve(Q.cache_id.size() + c);
+        Q.cache_score.reserve(Q.cache_score.size() + c);
+        for (int64_t j = 0; j < c; ++j) {
+            Q.cache_id.push_back(static_cast<int32_t>(kp[j] & 0xffffffffu));
+            Q.cache_score.push_back(key_score(kp[j]));
+        }
+        st->stats.certified += c;
+        if (c > 0) {
+            Q.has_cert = true;
+            Q.s_cert = Q.cache_score.back();
+            Q.id_cert = Q.cache_id.back();
+        }
+        const int64_t avail = static_cast<int64_t>(Q.cache_score.size()) - Q.emitted;
+        if (static_cast<int64_t>(Q.cache_score.size()) >= st->n_vis) {
+            Q.cert_exhausted = true;
+            Q.retries = 0;
+        } else if (avail >= m) {
+            Q.retries = 0;
+        } else {
+            Q.retries += 1;
+            st->stats.rescans += 1;
+            keep.push_back(b);
+        }
+    }
+    todo.swap(keep);
+    if (grow > 0) EAHR_TRY(ensure_scan_buffers(st, st->buf_nq, grow, st->buf_sample));
+    return EAHR_OK;
+}
+
+extern "C" int pvs_next(pvs_state* st, int32_t m, const uint8_t* active, int64_t* ids,
+                        float* scores, int32_t* count, int32_t* status) {
+    if (!st || m < 0 || (m > 0 && (!ids || !scores)) || !count || !status)
+        EAHR_FAIL(EAHR_E_INVALID, "pvs_next: bad arguments");
+    const int32_t B = st->B;
+    std::vector<int32_t> todo;
+    for (int32_t b = 0; b < B; ++b) {
+        if (active && !active[b]) continue;
+        auto& Q = st->q[b];
+        if (Q.failed || Q.cert_exhausted) continue;
+        const int64_t avail = static_cast<int64_t>(Q.cache_score.size()) - Q.emitted;
+        if (avail < m) todo.push_back(b);
+    }
+    for (int guard = 0; !todo.empty(); ++guard) {
+        if (guard > 200) EAHR_FAIL(EAHR_E_HIP, "pvs_next: scan loop did not converge");
+        EAHR_TRY(scan_round(st, todo, m));
+    }
+    for (int32_t b = 0; b < B; ++b) {
+        if (active && !active[b]) continue;
+        auto& Q = st->q[b];
+        if (Q.failed) {
+            count[b] = 0;
+            status[b] = EAHR_LIST_FAILED;
+            continue;
+        }
+        const int64_t avail = static_cast<int64_t>(Q.cache_score.size()) - Q.emitted;
+        const int64_t take = std::min<int64_t>(m, avail);
+        for (int64_t j = 0; j < take; ++j) {
+            ids[static_cast<int64_t>(b) * m + j] = Q.cache_id[Q.emitted + j];
+            scores[static_cast<int64_t>(b) * m + j] = Q.cache_score[Q.emitted + j];
+        }
+        Q.emitted += take;
+        st->stats.emitted += take;
+        count[b] = static_cast<int32_t>(take);
+        status[b] = (Q.emitted >= st->n_vis) ? EAHR_LIST_EXHAUSTED : EAHR_LIST_OPEN;
+    }
+    return EAHR_OK;
+}
+
+extern "C" int pvs_stats(const pvs_state* st, pvs_counters* out) {
+    if (!st || !out) EAHR_FAIL(EAHR_E_INVALID, "pvs_stats: bad arguments");
+    *out = st->stats;
+    return EAHR_OK;
+}

@@ -1,0 +1,93 @@
+// Host-side structures of the PVS runtime (index in HBM, per-query state).
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <vector>
+
+#include "eahr.h"
+#include "pvs_kernels.h"
+
+namespace pvs {
+// Threshold estimation samples every stride-th code block, with the stride
+// the largest power of two that keeps at least this many blocks sampled.
+constexpr int64_t kSampleBlocks = 2048;
+// Smallest per-query candidate capacity allocated for a scan.
+constexpr int64_t kMinCap = 4096;
+// Ranks a scan aims to certify per query beyond the request: about
+// kTargetBudget / (queries in the scan), clamped to [kTargetMin, kTargetMax].
+// A single-query scan streams the whole code array, so certifying a deep
+// prefix at once is cheap; a large batch shares one scan among many queries
+// and pays float32 rescoring per candidate instead.
+constexpr int64_t kTargetMin = 64;
+constexpr int64_t kTargetMax = 2048;
+constexpr int64_t kTargetBudget = 8192;
+}  // namespace pvs
+
+struct pvs_index {
+    struct Snapshot {
+        int64_t rows = 0;      // physical rows visible to the epoch (prefix)
+        int64_t visible = 0;   // set bits of vis
+        uint64_t* vis = nullptr;  // device bitmap, one word per 64-row block
+    };
+    int device = 0;
+    hipStream_t stream = nullptr;
+    int32_t d = 0, dp = 0, df = 0, nchunk = 0;
+    int64_t rows = 0, cap = 0;
+    int8_t* codes = nullptr;   // cap x dp, chunk-major 64-row blocks
+    float* scale = nullptr;    // s_v
+    float* vnorm = nullptr;    // ||v||_2 rounded up
+    float* enorm = nullptr;    // ||e_v||_2 rounded up
+    float* frows = nullptr;    // cap x df float32 rows
+    uint64_t* live = nullptr;  // live visibility bitmap
+    uint32_t* flags = nullptr;
+    float* staging = nullptr;  // host->device staging for quantisation
+    float nv_max = 0.0f, nev_max = 0.0f;
+    float gamma = 0.0f;
+    std::vector<Snapshot> snaps;
+    ~pvs_index();
+};
+
+struct pvs_state {
+    struct Query {
+        float sq = 0, nq = 0, nqh = 0, neq = 0, wmax = 0;
+        bool has_cert = false;          // a rank has been certified
+        float s_cert = 0.0f;            // key (s_cert, id_cert) of the last certified rank
+        int32_t id_cert = -1;
+        std::vector<int32_t> cache_id;  // certified ranks in order
+        std::vector<float> cache_score;
+        int64_t emitted = 0;            // ranks returned by pvs_next
+        bool failed = false;
+        bool cert_exhausted = false;    // every visible row certified
+        int retries = 0;                // consecutive scans that certified too few
+        int64_t cap_hint = 0;           // candidate capacity needed by the last overflow
+    };
+    const pvs_index* ix = nullptr;
+    int64_t epoch = 0;
+    int32_t B = 0;
+    int64_t n_rows = 0, n_vis = 0;
+    const uint64_t* vis = nullptr;
+    int8_t* qcodes = nullptr;   // B x dp row-major
+    float* qrows = nullptr;     // B x df
+    float *qscale = nullptr, *qnorm = nullptr, *qenorm = nullptr, *qhnorm = nullptr;
+    uint32_t* qflags = nullptr;
+    std::vector<Query> q;
+    pvs_counters stats{};
+    // scan buffers, sized for buf_nq queries of buf_cap candidates
+    int32_t buf_nq = 0;
+    int64_t buf_cap = 0, buf_sample = 0;
+    pvs::ScanQ* scanq = nullptr;
+    int32_t* cand_row = nullptr;
+    float* cand_lo = nullptr;
+    float* cand_hi = nullptr;
+    uint64_t* keys = nullptr;
+    uint64_t* keys_tmp = nullptr;
+    int32_t* counts = nullptr;
+    uint64_t* packed = nullptr;
+    float* sample = nullptr;
+    pvs::ScanQ* h_scanq = nullptr;   // pinned host mirrors
+    int32_t* h_counts = nullptr;
+    uint64_t* h_packed = nullptr;
+    void release_scan_buffers();
+    ~pvs_state();
+};

@@ -1,0 +1,84 @@
+// Internal interface between the PVS host runtime and its gfx950 kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pvs {
+
+constexpr int kBlockRows = 64;     // rows per code block (one wavefront lane per row)
+constexpr int kChunk = 16;         // bytes of one code chunk (one 16-byte load per lane)
+constexpr int kMaxDim = 4096;      // 127^2 * 4096 < 2^31 and a_m < 1
+constexpr int kSortTile = 2048;    // keys sorted per workgroup in LDS
+constexpr int kMaxGemvQueries = 8; // queries per GEMV scan pass
+
+// Per scanning query, uploaded before every scan.  All fields are read
+// uniformly by a wavefront (scalar loads).
+struct ScanQ {
+    int32_t qi;        // query index inside its state
+    float tau;         // interval threshold: candidates have hi >= tau,
+                       // certified ranks have s32 >= tau
+    float s_cert;      // score of the last certified rank (valid if has_cert)
+    int32_t id_cert;   // its row id
+    int32_t has_cert;
+    int32_t k;         // rank of tau among sampled lower bounds (select pass)
+    float sq;          // s_q
+    float nq;          // ||q||_2 rounded up
+    float nqh;         // ||q_hat||_2 rounded up
+    float neq;         // ||e_q||_2 rounded up
+    float wmax;        // upper bound of E + G over every row of the index
+    int32_t pad;
+};
+static_assert(sizeof(ScanQ) == 48, "ScanQ layout");
+
+// Row storage of an index.  Codes of 64 consecutive rows form one block laid
+// out chunk-major: byte j of row r lives at
+//   ((r / 64) * nchunk + j / 16) * 1024 + (r % 64) * 16 + j % 16,
+// so one 16-byte load per lane streams a whole 1 KiB chunk of a block.
+struct IndexView {
+    const uint4* codes;
+    const float* scale;
+    const float* vnorm;
+    const float* enorm;
+    const float* rows;     // float32 rows, stride df floats
+    int32_t d, dp, df, nchunk;
+};
+
+// Launchers (all asynchronous on `stream`).
+void launch_quantize(const float* src, int64_t nrows, int32_t d, int64_t src_stride,
+                     int64_t row0, bool tiled, int8_t* codes, int32_t dp, float* scale,
+                     float* vnorm, float* enorm, float* hnorm, float* rows, int32_t df,
+                     uint32_t* flags, hipStream_t stream);
+
+void launch_scan(const IndexView& ix, const uint64_t* vis, int64_t nblocks, const int8_t* qcodes,
+                 const ScanQ* sq, int32_t nq, float gamma, bool sample, int64_t sample_stride,
+                 float* sample_lo, int64_t sample_ld, int32_t* cand_row, float* cand_lo,
+                 float* cand_hi, int32_t* cand_cnt, int64_t cap, hipStream_t stream);
+
+void launch_select(const float* sample_lo, int64_t n, int64_t ld, ScanQ* sq, int32_t nq,
+                   hipStream_t stream);
+
+void launch_rescore(const IndexView& ix, const float* qrows, const ScanQ* sq, int32_t nq,
+                    const int32_t* cand_row, const float* cand_lo, const float* cand_hi,
+                    const int32_t* cand_cnt, int64_t cap, int64_t max_cnt, uint64_t* keys,
+                    int32_t* cert_cnt, int32_t* fail, hipStream_t stream);
+
+// Sorts keys[b*cap + (0..cnt_b)] ascending for every b; returns the buffer
+// holding the result (keys or tmp).
+uint64_t* launch_segmented_sort(uint64_t* keys, uint64_t* tmp, const int32_t* cnt, int32_t nq,
+                                int64_t cap, int64_t max_cnt, hipStream_t stream);
+
+void launch_pack(const uint64_t* keys, const int32_t* cert_cnt, int32_t nq, int64_t cap,
+                 int64_t max_cnt, int32_t* offs, uint64_t* packed, hipStream_t stream);
+
+void launch_intervals(const IndexView& ix, const int8_t* qcodes, const ScanQ* sq, float gamma,
+                      const int64_t* rows, int64_t n, float* lo, float* hi, hipStream_t stream);
+
+void launch_scores(const IndexView& ix, const float* qrows, int32_t qi, const int64_t* rows,
+                   int64_t n, float* out, hipStream_t stream);
+
+void launch_set_bits(uint64_t* vis, int64_t first, int64_t n, hipStream_t stream);
+void launch_clear_ids(uint64_t* vis, const int64_t* ids, int64_t n, hipStream_t stream);
+void launch_popcount(const uint64_t* vis, int64_t nwords, unsigned long long* out,
+                     hipStream_t stream);
+
+}  // namespace pvs

@@ -1,0 +1,115 @@
+"""Host fusion of the library (eahr_fuse_lists, sparse-only eahr_topk) against
+the oracle's complete-list weighted RRF and certification reference
+(Sec. 2.1, 2.2, 3.4).  Host only."""
+import json
+import os
+
+import numpy as np
+import pytest
+
+from oracle import certify, rrf
+from oracle import sparse as osparse
+from paper_2608_07152_amd import datagen, eahr
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_fuse_lists_equals_complete_rrf(seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(1, 400))
+    a = rng.permutation(n)
+    kind = seed % 4
+    if kind == 0:
+        b = rng.permutation(n)[: int(rng.integers(0, n + 1))]
+    elif kind == 1:
+        b = a[::-1].copy()
+    elif kind == 2:   # overlapping heads
+        b = np.concatenate([a[:10][::-1], rng.permutation(a[10:])])
+    else:
+        b = a.copy()
+    wts = [int(rng.integers(0, 3)), int(rng.integers(1, 3))]
+    k = int(rng.choice([1, 2, 60]))
+    K = int(rng.integers(1, 30))
+    got, st = eahr.eahr_fuse_lists(a, b, K=K, k_rrf=k, w_dense=wts[0], w_sparse=wts[1],
+                                   step=int(rng.choice([0, 1, 16])))
+    want = rrf.rrf_topk([a, b], wts, k, K)
+    assert list(got) == want
+    assert st["resolved"] == 1
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_fuse_lists_stops_where_reference_first_resolves(seed):
+    rng = np.random.default_rng(500 + seed)
+    n = int(rng.integers(20, 120))
+    a = rng.permutation(n)
+    b = np.concatenate([a[:8][rng.permutation(8)], rng.permutation(a[8:])])
+    K, step = 5, 4
+    got, st = eahr.eahr_fuse_lists(a, b, K=K, step=step)
+    d = step
+    while True:
+        A, ok = certify.certify_ref([a, b], [1, 1], 60, K, [d, d])
+        if ok or d >= n:
+            break
+        d = min(n, d + step)
+    assert st["dense_depth"] == min(d, n) and st["sparse_depth"] == min(d, n)
+    assert list(got) == A
+
+
+def test_fuse_lists_controlled_correlated_streams():
+    g = json.load(open(os.path.join(GOLDEN, "e5_controlled_streams.json")))
+    want = g["outcomes"]["correlated_32_block_permutation"]["first_resolved_depth"]
+    for n in g["sizes"]:
+        for seed in g["seeds"]:
+            rng = np.random.default_rng(seed)
+            a = rng.permutation(n)
+            order = np.lexsort((rng.random(n), np.arange(n) // g["block"]))
+            b = a[order]
+            got, st = eahr.eahr_fuse_lists(a, b, K=g["K"], step=g["check_every"])
+            assert st["dense_depth"] == want and st["sparse_depth"] == want
+            assert list(got) == rrf.rrf_topk([a, b], [1, 1], 60, g["K"])
+
+
+def test_fuse_lists_anticorrelated_streams_exhaust_both():
+    for n, seed in ((100_000, 1729), (30_000, 2027)):
+        rng = np.random.default_rng(seed)
+        a = rng.permutation(n)
+        got, st = eahr.eahr_fuse_lists(a, a[::-1], K=20, step=16)
+        assert st["dense_status"] == eahr.LIST_EXHAUSTED and st["sparse_status"] == eahr.LIST_EXHAUSTED
+        assert st["dense_depth"] == n and st["sparse_depth"] == n
+        assert list(got) == rrf.rrf_topk([a, a[::-1]], [1, 1], 60, 20)
+
+
+def test_fuse_lists_no_padding_and_zero_weight():
+    got, st = eahr.eahr_fuse_lists(np.arange(50), np.array([42, 7, 9]), K=20, w_dense=0)
+    assert list(got) == [42, 7, 9]
+    got, _ = eahr.eahr_fuse_lists(np.arange(50), np.array([42, 7, 9]), K=5, w_sparse=0)
+    assert list(got) == [0, 1, 2, 3, 4]
+    got, _ = eahr.eahr_fuse_lists(np.zeros(0, np.int64), np.zeros(0, np.int64), K=5)
+    assert list(got) == []
+
+
+def test_fuse_lists_weight_two_to_one():
+    rng = np.random.default_rng(77)
+    for _ in range(10):
+        n = 300
+        a = rng.permutation(n)
+        b = np.concatenate([rng.permutation(a[:40]), rng.permutation(a[40:])])
+        got, _ = eahr.eahr_fuse_lists(a, b, K=20, w_dense=2, w_sparse=1)
+        assert list(got) == rrf.rrf_topk([a, b], [2, 1], 60, 20)
+
+
+def test_sparse_only_topk_through_eahr_topk():
+    # the dense channel is not touched when its weight is 0 (no GPU needed)
+    w = datagen.workload("tiny", n=5000)
+    _, lab = datagen.corpus(w)
+    post = datagen.bm25_impacts(w, datagen.sparse_docs(w, lab))
+    _, qlab = datagen.queries(w, count=5)
+    qs = datagen.sparse_queries(w, qlab)
+    idx = eahr.pbm_build(post.term_ptr, post.doc, post.impact, w.n, 512)
+    ids, cnt, stt, stats = eahr.eahr_topk(None, idx, None, qs, K=20, w_dense=0, w_sparse=1)
+    for b, (t, wt) in enumerate(qs):
+        S = osparse.sparse_scores(post.term_ptr, post.doc, post.impact, t, wt, w.n)
+        want = list(osparse.sparse_ranking(S)[:20])
+        assert list(ids[b, :cnt[b]]) == want
+        assert stt[b] == 0

@@ -1,0 +1,98 @@
+"""PBM sparse channel through the C ABI against the brute-force oracle
+(Sec. 2.3.2, App. A.2).  Host only."""
+import numpy as np
+import pytest
+
+from oracle import sparse as osparse
+from paper_2608_07152_amd import datagen, eahr
+
+
+@pytest.fixture(scope="module")
+def tiny_sparse():
+    w = datagen.workload("tiny", n=6000)
+    _, lab = datagen.corpus(w)
+    docs = datagen.sparse_docs(w, lab)
+    post = datagen.bm25_impacts(w, docs)
+    _, qlab = datagen.queries(w, count=6)
+    qs = datagen.sparse_queries(w, qlab)
+    return w, post, qs
+
+
+def _oracle_ranking(post, n, terms, wts):
+    S = osparse.sparse_scores(post.term_ptr, post.doc, post.impact, terms, wts, n)
+    r = osparse.sparse_ranking(S)
+    return r, S[r]
+
+
+@pytest.mark.parametrize("range_size", [1, 7, 256, 4096, 10 ** 6])
+def test_pbm_full_ranking_bit_exact(tiny_sparse, range_size):
+    w, post, qs = tiny_sparse
+    idx = eahr.pbm_build(post.term_ptr, post.doc, post.impact, w.n, range_size)
+    for terms, wts in qs:
+        want_ids, want_s = _oracle_ranking(post, w.n, terms, wts)
+        st = eahr.pbm_open(idx, terms, wts)
+        ids, sc, status = eahr.pbm_next(st, w.n + 5)
+        assert status == eahr.LIST_EXHAUSTED
+        assert np.array_equal(ids, want_ids)
+        assert np.array_equal(sc, want_s)
+
+
+def test_pbm_split_calls_equal_one_call(tiny_sparse):
+    w, post, qs = tiny_sparse
+    idx = eahr.pbm_build(post.term_ptr, post.doc, post.impact, w.n, 128)
+    terms, wts = qs[0]
+    want_ids, _ = _oracle_ranking(post, w.n, terms, wts)
+    st = eahr.pbm_open(idx, terms, wts)
+    got = []
+    for m in (1, 2, 20, 0, 40, 3, 1000, 10 ** 6):
+        ids, _, status = eahr.pbm_next(st, m)
+        assert len(ids) == m or status == eahr.LIST_EXHAUSTED
+        got.extend(ids)
+    assert np.array_equal(np.array(got), want_ids)
+
+
+def test_pbm_weights_and_ties():
+    # hand index with exact ties across ranges and zero-weight terms
+    term_ptr = np.array([0, 4, 8, 9])
+    docs = np.array([0, 3, 5, 9, 1, 3, 5, 8, 2], dtype=np.int32)
+    imp = np.array([1, 2, 2, 1, 1, 0, 0, 1, 5], dtype=np.float32)
+    idx = eahr.pbm_build(term_ptr, docs, imp, 10, 3)
+    for terms, wts in (([0, 1], [1.0, 1.0]), ([1, 0, 2], [2.0, 1.0, 0.0]), ([2], [0.5])):
+        st = eahr.pbm_open(idx, terms, wts)
+        ids, sc, status = eahr.pbm_next(st, 100)
+        want, want_s = _oracle_ranking(
+            eahr_post(term_ptr, docs, imp), 10, np.array(terms), np.array(wts, dtype=np.float32))
+        assert np.array_equal(ids, want) and np.array_equal(sc, want_s)
+        assert status == eahr.LIST_EXHAUSTED
+
+
+def eahr_post(term_ptr, docs, imp):
+    return datagen.Postings(len(term_ptr) - 1, term_ptr, docs, imp)
+
+
+def test_pbm_empty_query_is_exhausted():
+    idx = eahr.pbm_build(np.array([0, 1]), np.array([0], np.int32), np.array([1], np.float32), 1, 4)
+    st = eahr.pbm_open(idx, [], [])
+    ids, _, status = eahr.pbm_next(st, 5)
+    assert len(ids) == 0 and status == eahr.LIST_EXHAUSTED
+
+
+def test_pbm_uncovered_blockmax_fails(tiny_sparse):
+    w, post, qs = tiny_sparse
+    idx = eahr.pbm_build(post.term_ptr, post.doc, post.impact, w.n, 64)
+    terms, wts = qs[1]
+    t = int(terms[0])
+    first_doc = int(post.doc[post.term_ptr[t]])
+    eahr.pbm_debug_set_blockmax(idx, t, first_doc // 64, 0.0)
+    st = eahr.pbm_open(idx, terms, wts)
+    ids, _, status = eahr.pbm_next(st, w.n)
+    assert status == eahr.LIST_FAILED
+
+
+def test_pbm_rejects_bad_postings():
+    with pytest.raises(eahr.EahrError):
+        eahr.pbm_build(np.array([0, 2]), np.array([3, 3], np.int32), np.ones(2, np.float32), 5, 2)
+    with pytest.raises(eahr.EahrError):
+        eahr.pbm_build(np.array([0, 1]), np.array([0], np.int32), np.array([-1.0], np.float32), 5, 2)
+    with pytest.raises(eahr.EahrError):
+        eahr.pbm_build(np.array([0, 1]), np.array([0], np.int32), np.array([np.inf], np.float32), 5, 2)
