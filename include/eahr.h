@@ -117,6 +117,25 @@ typedef struct {
 
 int pvs_stats(const pvs_state* st, pvs_counters* out);
 
+/* Process-wide kernel timing of the dense channel, measured with HIP events
+ * recorded on the index's stream around each kernel group of a scan (all
+ * states, all threads).  Disabled by default; enabling adds event records and
+ * no synchronisation.  Times in milliseconds, bytes algorithmic:
+ * rows * (d + 12) + 8 bytes per 64-row visibility word for a full scan pass. */
+typedef struct {
+    double scan_ms;          /* full interval scans (kernel time)            */
+    int64_t scan_launches;   /* kernel launches those scans used             */
+    int64_t scan_bytes;      /* algorithmic bytes those launches streamed    */
+    double sample_ms;        /* threshold sampling + selection               */
+    double rescore_ms;       /* float32 rescoring of candidates              */
+    int64_t rescore_rows;
+    double sort_ms;          /* candidate sort and packing                   */
+    int64_t scan_rounds;
+} pvs_profile;
+
+int pvs_profile_enable(int32_t on);   /* also clears the accumulators */
+int pvs_profile_read(pvs_profile* out);
+
 /* Debug / test entry points (not on the retrieval path):
  * pvs_read_index -- copy rows [row0, row0+n) of the index to host: codes
  *   n x d int8 (row-major), meta n x 3 float32 (s_v, ||v||_2 up, ||e_v||_2 up).

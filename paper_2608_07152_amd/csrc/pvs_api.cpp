@@ -15,7 +15,9 @@
 #include <cstdint>
 #include <cstring>
 #include <limits>
+#include <atomic>
 #include <memory>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -61,6 +63,10 @@ void dev_free(T*& p) {
     if (p) (void)hipFree(p);
     p = nullptr;
 }
+
+std::atomic<int> g_prof_on{0};
+std::mutex g_prof_mu;
+pvs_profile g_prof{};
 
 bool is_device_ptr(const void* p) {
     hipPointerAttribute_t a;
@@ -306,6 +312,8 @@ pvs_state::~pvs_state() {
     if (h_scanq) (void)hipHostFree(h_scanq);
     if (h_counts) (void)hipHostFree(h_counts);
     if (h_packed) (void)hipHostFree(h_packed);
+    for (auto& e : ev)
+        if (e) (void)hipEventDestroy(e);
 }
 
 void pvs_state::release_scan_buffers() {
@@ -597,12 +605,22 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     int32_t* d_offs = st->counts + 3 * nq;
     HIP_TRY(hipMemcpyAsync(st->scanq, st->h_scanq, nq * sizeof(ScanQ), hipMemcpyHostToDevice, s));
     HIP_TRY(hipMemsetAsync(st->counts, 0, (4 * static_cast<size_t>(nq) + 1) * sizeof(int32_t), s));
+    const bool prof = g_prof_on.load(std::memory_order_relaxed) != 0;
+    if (prof && !st->ev[0])
+        for (auto& e : st->ev) HIP_TRY(hipEventCreate(&e));
+    auto mark = [&](int i) -> int {
+        if (prof) HIP_TRY(hipEventRecord(st->ev[i], s));
+        return EAHR_OK;
+    };
     const pvs::IndexView v = view_of(ix);
+    EAHR_TRY(mark(0));
     pvs::launch_scan(v, st->vis, nblocks, st->qcodes, st->scanq, nq, ix->gamma, true, stride,
                      st->sample, sample_ld, nullptr, nullptr, nullptr, nullptr, 0, s);
     pvs::launch_select(st->sample, sample_ld, sample_ld, st->scanq, nq, s);
+    EAHR_TRY(mark(1));
     pvs::launch_scan(v, st->vis, nblocks, st->qcodes, st->scanq, nq, ix->gamma, false, 1, nullptr,
                      0, st->cand_row, st->cand_lo, st->cand_hi, d_cand, cap, s);
+    EAHR_TRY(mark(2));
     HIP_TRY(hipGetLastError());
     HIP_TRY(hipMemcpyAsync(st->h_counts, d_cand, nq * sizeof(int32_t), hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
@@ -618,16 +636,36 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
         max_cnt = std::max(max_cnt, c);
         total += c;
     }
+    EAHR_TRY(mark(3));
     pvs::launch_rescore(v, st->qrows, st->scanq, nq, st->cand_row, st->cand_lo, st->cand_hi, d_cand,
                         cap, max_cnt, st->keys, d_cert, d_fail, s);
+    EAHR_TRY(mark(4));
     uint64_t* sorted = pvs::launch_segmented_sort(st->keys, st->keys_tmp, d_cand, nq, cap, max_cnt, s);
     pvs::launch_pack(sorted, d_cert, nq, cap, max_cnt, d_offs, st->packed, s);
+    EAHR_TRY(mark(5));
     HIP_TRY(hipGetLastError());
     HIP_TRY(hipMemcpyAsync(st->h_counts + nq, d_cert, (3 * static_cast<size_t>(nq) + 1) * sizeof(int32_t),
                            hipMemcpyDeviceToHost, s));
     if (total > 0)
         HIP_TRY(hipMemcpyAsync(st->h_packed, st->packed, total * sizeof(uint64_t), hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
+    if (prof) {
+        float t[5];
+        HIP_TRY(hipEventElapsedTime(&t[0], st->ev[0], st->ev[1]));
+        HIP_TRY(hipEventElapsedTime(&t[1], st->ev[1], st->ev[2]));
+        HIP_TRY(hipEventElapsedTime(&t[2], st->ev[3], st->ev[4]));
+        HIP_TRY(hipEventElapsedTime(&t[3], st->ev[4], st->ev[5]));
+        std::lock_guard<std::mutex> lk(g_prof_mu);
+        g_prof.sample_ms += t[0];
+        g_prof.scan_ms += t[1];
+        const int64_t launches = (nq + pvs::kMaxGemvQueries - 1) / pvs::kMaxGemvQueries;
+        g_prof.scan_launches += launches;
+        g_prof.scan_bytes += launches * (st->n_rows * (static_cast<int64_t>(ix->d) + 12) + nblocks * 8);
+        g_prof.rescore_ms += t[2];
+        g_prof.rescore_rows += total;
+        g_prof.sort_ms += t[3];
+        g_prof.scan_rounds += 1;
+    }
     const int32_t* h_cert = st->h_counts + nq;
     const int32_t* h_fail = st->h_counts + 2 * nq;
     const int32_t* h_offs = st->h_counts + 3 * nq;
@@ -721,5 +759,19 @@ extern "C" int pvs_next(pvs_state* st, int32_t m, const uint8_t* active, int64_t
 extern "C" int pvs_stats(const pvs_state* st, pvs_counters* out) {
     if (!st || !out) EAHR_FAIL(EAHR_E_INVALID, "pvs_stats: bad arguments");
     *out = st->stats;
+    return EAHR_OK;
+}
+
+extern "C" int pvs_profile_enable(int32_t on) {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    g_prof = pvs_profile{};
+    g_prof_on.store(on ? 1 : 0);
+    return EAHR_OK;
+}
+
+extern "C" int pvs_profile_read(pvs_profile* out) {
+    if (!out) EAHR_FAIL(EAHR_E_INVALID, "pvs_profile_read: NULL");
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    *out = g_prof;
     return EAHR_OK;
 }

@@ -85,6 +85,7 @@ struct pvs_state {
     int32_t* counts = nullptr;
     uint64_t* packed = nullptr;
     float* sample = nullptr;
+    hipEvent_t ev[7] = {};             // profiling events (created on first use)
     pvs::ScanQ* h_scanq = nullptr;   // pinned host mirrors
     int32_t* h_counts = nullptr;
     uint64_t* h_packed = nullptr;

@@ -154,15 +154,26 @@ def corpus_chunk(w: Workload, chunk: int, ctr: Optional[np.ndarray] = None
 
 
 def _corpus_chunk_job(args):
-    w, c = args
-    return corpus_chunk(w, c)
+    """Worker: write chunk c straight into the shared output buffer."""
+    from multiprocessing import shared_memory
+    w, c, shm_name = args
+    shm = shared_memory.SharedMemory(name=shm_name)
+    try:
+        out = np.ndarray((w.n, w.d), dtype=np.float32, buffer=shm.buf)
+        x, lab = corpus_chunk(w, c)
+        out[c * CHUNK_ROWS: c * CHUNK_ROWS + len(x)] = x
+        del out
+    finally:
+        shm.close()
+    return lab
 
 
-def corpus(w: Workload, out: Optional[np.ndarray] = None,
-           workers: Optional[int] = None) -> Tuple[np.ndarray, np.ndarray]:
-    """Whole base corpus, float32 [n, d] and int32 labels [n]."""
-    if out is None:
-        out = np.empty((w.n, w.d), dtype=np.float32)
+def corpus(w: Workload, workers: Optional[int] = None) -> Tuple[np.ndarray, np.ndarray]:
+    """Whole base corpus, float32 [n, d] and int32 labels [n].
+
+    Large corpora are produced by worker processes writing into one shared
+    buffer, which is copied once into an ordinary array and released."""
+    out = np.empty((w.n, w.d), dtype=np.float32)
     labels = np.empty(w.n, dtype=np.int32)
     nc = n_chunks(w.n)
     workers = workers or _workers()
@@ -173,10 +184,37 @@ def corpus(w: Workload, out: Optional[np.ndarray] = None,
             out[c * CHUNK_ROWS: c * CHUNK_ROWS + len(x)] = x
             labels[c * CHUNK_ROWS: c * CHUNK_ROWS + len(x)] = lab
         return out, labels
-    with ProcessPoolExecutor(max_workers=workers) as ex:
-        for c, (x, lab) in enumerate(ex.map(_corpus_chunk_job, [(w, c) for c in range(nc)])):
+    try:
+        st = os.statvfs("/dev/shm")
+        shm_free = st.f_bavail * st.f_frsize
+    except OSError:
+        shm_free = 0
+    if shm_free < out.nbytes + (1 << 30):
+        # not enough shared memory: threads write into `out` directly
+        from concurrent.futures import ThreadPoolExecutor
+        ctr = centers(w)
+
+        def fill(c):
+            x, lab = corpus_chunk(w, c, ctr)
             out[c * CHUNK_ROWS: c * CHUNK_ROWS + len(x)] = x
             labels[c * CHUNK_ROWS: c * CHUNK_ROWS + len(x)] = lab
+
+        with ThreadPoolExecutor(max_workers=workers) as ex:
+            list(ex.map(fill, range(nc)))
+        return out, labels
+    from multiprocessing import shared_memory
+    shm = shared_memory.SharedMemory(create=True, size=max(1, out.nbytes))
+    try:
+        with ProcessPoolExecutor(max_workers=workers) as ex:
+            jobs = [(w, c, shm.name) for c in range(nc)]
+            for c, lab in enumerate(ex.map(_corpus_chunk_job, jobs)):
+                labels[c * CHUNK_ROWS: c * CHUNK_ROWS + len(lab)] = lab
+        view = np.ndarray((w.n, w.d), dtype=np.float32, buffer=shm.buf)
+        out[...] = view
+        del view
+    finally:
+        shm.close()
+        shm.unlink()
     return out, labels
 
 

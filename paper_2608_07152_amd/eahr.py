@@ -68,6 +68,15 @@ class pvs_counters(C.Structure):
         return {f: getattr(self, f) for f, _ in self._fields_}
 
 
+class pvs_profile(C.Structure):
+    _fields_ = [("scan_ms", C.c_double), ("scan_launches", C.c_int64), ("scan_bytes", C.c_int64),
+                ("sample_ms", C.c_double), ("rescore_ms", C.c_double), ("rescore_rows", C.c_int64),
+                ("sort_ms", C.c_double), ("scan_rounds", C.c_int64)]
+
+    def as_dict(self):
+        return {f: getattr(self, f) for f, _ in self._fields_}
+
+
 _P = C.c_void_p
 _i32, _i64, _f32p = C.c_int32, C.c_int64, C.POINTER(C.c_float)
 _i64p, _i32p, _u8p, _i8p = C.POINTER(C.c_int64), C.POINTER(C.c_int32), C.POINTER(C.c_uint8), C.POINTER(C.c_int8)
@@ -82,6 +91,8 @@ SIGNATURES = {
     "pvs_open": (C.c_int, [_P, _i64, _P, _i32, _i32, C.POINTER(_P)]),
     "pvs_next": (C.c_int, [_P, _i32, _u8p, _i64p, _f32p, _i32p, _i32p]),
     "pvs_stats": (C.c_int, [_P, C.POINTER(pvs_counters)]),
+    "pvs_profile_enable": (C.c_int, [_i32]),
+    "pvs_profile_read": (C.c_int, [C.POINTER(pvs_profile)]),
     "pvs_read_index": (C.c_int, [_P, _i64, _i64, _i8p, _f32p]),
     "pvs_read_query": (C.c_int, [_P, _i8p, _f32p]),
     "pvs_intervals": (C.c_int, [_P, _i32, _i64p, _i64, _f32p, _f32p]),
@@ -112,6 +123,13 @@ def load() -> C.CDLL:
         return _lib
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2608_07152_amd.build`")
+    # torch ships its own HIP runtime under the same SONAME (libamdhip64.so.7).
+    # Loading torch first makes the library bind to that copy, so the process
+    # holds one HIP runtime and torch device pointers and streams are valid here.
+    try:
+        import torch  # noqa: F401
+    except ImportError:  # pragma: no cover
+        pass
     lib = C.CDLL(LIB_PATH)
     for name, (res, args) in SIGNATURES.items():
         fn = getattr(lib, name)
@@ -288,6 +306,16 @@ def pvs_stats(state: PvsState) -> dict:
     c = pvs_counters()
     _check(load().pvs_stats(state.h, C.byref(c)))
     return c.as_dict()
+
+
+def pvs_profile_enable(on: bool = True) -> None:
+    _check(load().pvs_profile_enable(1 if on else 0))
+
+
+def pvs_profile_read() -> dict:
+    p = pvs_profile()
+    _check(load().pvs_profile_read(C.byref(p)))
+    return p.as_dict()
 
 
 def pvs_read_index(index: PvsIndex, row0: int, n: int):

@@ -252,6 +252,13 @@ def test_nonfinite_inputs_rejected(E):
     assert ei.value.code == E.EAHR_E_NONFINITE
 
 
+def test_single_hip_runtime_in_process(E):
+    import re
+    maps = open("/proc/self/maps").read()
+    assert len(set(re.findall(r"\S*libamdhip64\S*", maps))) == 1
+    assert "libeahr.so" in maps
+
+
 def test_device_pointer_inputs(E, tiny):
     import torch
     w, x, q = tiny
