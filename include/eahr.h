@@ -131,6 +131,7 @@ typedef struct {
     int64_t rescore_rows;
     double sort_ms;          /* candidate sort and packing                   */
     int64_t scan_rounds;
+    int64_t mfma_launches;   /* scan launches that used the Int8 MFMA kernel */
 } pvs_profile;
 
 int pvs_profile_enable(int32_t on);   /* also clears the accumulators */

@@ -13,6 +13,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdint>
+#include <cstdlib>
 #include <cstring>
 #include <limits>
 #include <atomic>
@@ -326,6 +327,7 @@ void pvs_state::release_scan_buffers() {
     dev_free(counts);
     dev_free(packed);
     dev_free(sample);
+    dev_free(qfrag);
     buf_nq = 0;
     buf_cap = 0;
     buf_sample = 0;
@@ -349,6 +351,11 @@ static int ensure_scan_buffers(pvs_state* st, int32_t nq, int64_t cap, int64_t s
     EAHR_TRY(dev_alloc(&st->counts, 4 * static_cast<size_t>(nq) + 1));
     EAHR_TRY(dev_alloc(&st->packed, tot));
     EAHR_TRY(dev_alloc(&st->sample, static_cast<size_t>(nq) * sample_ld));
+    {
+        int8_t* f;
+        EAHR_TRY(dev_alloc(&f, static_cast<size_t>(st->ix->dp / 32) * 8 * 64 * 16));
+        st->qfrag = f;
+    }
     if (st->h_scanq) (void)hipHostFree(st->h_scanq);
     if (st->h_counts) (void)hipHostFree(st->h_counts);
     if (st->h_packed) (void)hipHostFree(st->h_packed);
@@ -378,6 +385,10 @@ extern "C" int pvs_open(const pvs_index* ix, int64_t epoch, const float* q, int3
     st->ix = ix;
     st->epoch = epoch;
     st->B = B;
+    if (const char* p = std::getenv("EAHR_SCAN_PATH")) {
+        if (std::strcmp(p, "gemv") == 0) st->path = pvs::ScanPath::Gemv;
+        else if (std::strcmp(p, "mfma") == 0) st->path = pvs::ScanPath::Mfma;
+    }
     st->n_rows = ix->snaps[epoch].rows;
     st->n_vis = ix->snaps[epoch].visible;
     st->vis = ix->snaps[epoch].vis;
@@ -590,9 +601,11 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
         const int32_t b = todo[i];
         auto& Q = st->q[b];
         ScanQ sq = make_scanq(st, b);
-        const int64_t avail = static_cast<int64_t>(Q.cache_score.size()) - Q.emitted;
+        const int64_t have = static_cast<int64_t>(Q.cache_score.size());
+        const int64_t avail = have - Q.emitted;
         const int64_t need = std::max<int64_t>(1, m - avail);
-        const int64_t target = std::max(need, mmin) + lower_overlap(st, b);
+        const int64_t spec = std::min(pvs::kSpecFactor * (Q.emitted + m) - have, pvs::kSpecBudget / nq);
+        const int64_t target = std::max({need, mmin, spec}) + lower_overlap(st, b);
         double k = (stride == 1) ? static_cast<double>(target)
                                  : std::max(4.0, std::ceil(2.0 * target * frac));
         for (int r = 0; r < Q.retries; ++r) k *= 4.0;
@@ -614,12 +627,25 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     };
     const pvs::IndexView v = view_of(ix);
     EAHR_TRY(mark(0));
-    pvs::launch_scan(v, st->vis, nblocks, st->qcodes, st->scanq, nq, ix->gamma, true, stride,
-                     st->sample, sample_ld, nullptr, nullptr, nullptr, nullptr, 0, s);
+    const bool mfma = st->path == pvs::ScanPath::Mfma ||
+                      (st->path == pvs::ScanPath::Auto && nq >= pvs::kMfmaMinQueries);
+    if (mfma) {
+        pvs::launch_scan_mfma(v, st->vis, nblocks, st->qcodes, st->scanq, nq, ix->gamma, true, stride,
+                              st->sample, sample_ld, nullptr, nullptr, nullptr, nullptr, 0, st->qfrag, s);
+    } else {
+        pvs::launch_scan(v, st->vis, nblocks, st->qcodes, st->scanq, nq, ix->gamma, true, stride,
+                         st->sample, sample_ld, nullptr, nullptr, nullptr, nullptr, 0, s);
+    }
     pvs::launch_select(st->sample, sample_ld, sample_ld, st->scanq, nq, s);
     EAHR_TRY(mark(1));
-    pvs::launch_scan(v, st->vis, nblocks, st->qcodes, st->scanq, nq, ix->gamma, false, 1, nullptr,
-                     0, st->cand_row, st->cand_lo, st->cand_hi, d_cand, cap, s);
+    if (mfma) {
+        pvs::launch_scan_mfma(v, st->vis, nblocks, st->qcodes, st->scanq, nq, ix->gamma, false, 1,
+                              nullptr, 0, st->cand_row, st->cand_lo, st->cand_hi, d_cand, cap,
+                              st->qfrag, s);
+    } else {
+        pvs::launch_scan(v, st->vis, nblocks, st->qcodes, st->scanq, nq, ix->gamma, false, 1, nullptr,
+                         0, st->cand_row, st->cand_lo, st->cand_hi, d_cand, cap, s);
+    }
     EAHR_TRY(mark(2));
     HIP_TRY(hipGetLastError());
     HIP_TRY(hipMemcpyAsync(st->h_counts, d_cand, nq * sizeof(int32_t), hipMemcpyDeviceToHost, s));
@@ -658,8 +684,10 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
         std::lock_guard<std::mutex> lk(g_prof_mu);
         g_prof.sample_ms += t[0];
         g_prof.scan_ms += t[1];
-        const int64_t launches = (nq + pvs::kMaxGemvQueries - 1) / pvs::kMaxGemvQueries;
+        const int64_t per = mfma ? pvs::kMaxMfmaQueries : pvs::kMaxGemvQueries;
+        const int64_t launches = (nq + per - 1) / per;
         g_prof.scan_launches += launches;
+        if (mfma) g_prof.mfma_launches += launches;
         g_prof.scan_bytes += launches * (st->n_rows * (static_cast<int64_t>(ix->d) + 12) + nblocks * 8);
         g_prof.rescore_ms += t[2];
         g_prof.rescore_rows += total;

@@ -22,6 +22,17 @@ constexpr int64_t kMinCap = 4096;
 constexpr int64_t kTargetMin = 64;
 constexpr int64_t kTargetMax = 2048;
 constexpr int64_t kTargetBudget = 8192;
+// Callers extend prefixes geometrically, so a scan also certifies ahead:
+// up to kSpecFactor times the depth reached after the request, within
+// kSpecBudget ranks per scan shared by its queries.  Rescoring a row costs
+// about 1/1000 of streaming the codes once, so over-certifying is cheap next
+// to an extra scan.
+constexpr int64_t kSpecFactor = 8;
+constexpr int64_t kSpecBudget = int64_t(1) << 20;
+// Scans of at least this many queries use the Int8 MFMA kernel; smaller ones
+// the dot4 GEMV kernel.  EAHR_SCAN_PATH=gemv|mfma forces one path (testing).
+constexpr int32_t kMfmaMinQueries = 4;
+enum class ScanPath { Auto, Gemv, Mfma };
 }  // namespace pvs
 
 struct pvs_index {
@@ -85,6 +96,8 @@ struct pvs_state {
     int32_t* counts = nullptr;
     uint64_t* packed = nullptr;
     float* sample = nullptr;
+    void* qfrag = nullptr;             // query codes in MFMA operand order
+    pvs::ScanPath path = pvs::ScanPath::Auto;
     hipEvent_t ev[7] = {};             // profiling events (created on first use)
     pvs::ScanQ* h_scanq = nullptr;   // pinned host mirrors
     int32_t* h_counts = nullptr;

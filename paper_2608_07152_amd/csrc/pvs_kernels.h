@@ -10,6 +10,7 @@ constexpr int kChunk = 16;         // bytes of one code chunk (one 16-byte load 
 constexpr int kMaxDim = 4096;      // 127^2 * 4096 < 2^31 and a_m < 1
 constexpr int kSortTile = 2048;    // keys sorted per workgroup in LDS
 constexpr int kMaxGemvQueries = 8; // queries per GEMV scan pass
+constexpr int kMaxMfmaQueries = 256;  // queries per MFMA scan pass (8 tiles of 32)
 
 // Per scanning query, uploaded before every scan.  All fields are read
 // uniformly by a wavefront (scalar loads).
@@ -53,6 +54,15 @@ void launch_scan(const IndexView& ix, const uint64_t* vis, int64_t nblocks, cons
                  const ScanQ* sq, int32_t nq, float gamma, bool sample, int64_t sample_stride,
                  float* sample_lo, int64_t sample_ld, int32_t* cand_row, float* cand_lo,
                  float* cand_hi, int32_t* cand_cnt, int64_t cap, hipStream_t stream);
+
+// Int8 MFMA variant (same outputs as launch_scan).  `frag` is device scratch
+// of (dp / 32) * 8 KiB for the query codes in MFMA operand order.
+void launch_scan_mfma(const IndexView& ix, const uint64_t* vis, int64_t nblocks,
+                      const int8_t* qcodes, const ScanQ* sq, int32_t nq, float gamma, bool sample,
+                      int64_t sample_stride, float* sample_lo, int64_t sample_ld, int32_t* cand_row,
+                      float* cand_lo, float* cand_hi, int32_t* cand_cnt, int64_t cap, void* frag,
+                      hipStream_t stream);
+int mfma_tiles_for(int32_t nq);
 
 void launch_select(const float* sample_lo, int64_t n, int64_t ld, ScanQ* sq, int32_t nq,
                    hipStream_t stream);

@@ -299,6 +299,173 @@ void launch_scan(const IndexView& ix, const uint64_t* vis, int64_t nblocks, cons
     }
 }
 
+// -------------------------------------------------------------- MFMA scan
+// For query batches the code x query product is a dense Int8 contraction:
+// V_MFMA_I32_32X32X32_I8 with the corpus block as A (32 rows x 32 bytes per
+// instruction) and the query codes as B.  Operand layout (lane l, byte j):
+// A[l % 32][16 (l / 32) + j], B[16 (l / 32) + j][l % 32]; accumulator r of lane
+// l holds C[8 (r / 4) + 4 (l / 32) + r % 4][l % 32].  A 16-byte A fragment is
+// therefore 32 consecutive rows of one code chunk: two contiguous 512-byte
+// runs of the chunk-major block layout.
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v16i __attribute__((ext_vector_type(16)));
+
+// Query codes of one pass in MFMA B-fragment order:
+// frag[(s * nqt + u) * 64 + lane] = 16 code bytes of query 32 u + lane % 32,
+// bytes 32 s + 16 (lane / 32) .. +15; queries past nq are zero.
+__global__ __launch_bounds__(64) void k_qfrag(const int8_t* __restrict__ qcodes, int32_t dp,
+                                              const ScanQ* __restrict__ sq, int32_t nq, int32_t nqt,
+                                              uint4* __restrict__ frag) {
+    const int lane = threadIdx.x;
+    const int s = blockIdx.x / nqt, u = blockIdx.x % nqt;
+    const int b = 32 * u + (lane & 31);
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (b < nq) {
+        const int64_t off = static_cast<int64_t>(sq[b].qi) * dp + 32 * s + 16 * (lane >> 5);
+        v = *reinterpret_cast<const uint4*>(qcodes + off);
+    }
+    frag[(static_cast<int64_t>(s) * nqt + u) * 64 + lane] = v;
+}
+
+// One wavefront per 64-row block and NQT tiles of 32 queries: 2 x NQT
+// accumulators of 32 x 32.  Epilogue per (row, query): the centre score is
+// compared with tau - wmax first (wmax bounds E + G over every row, with a
+// relative margin), and only rows that may reach tau get the exact interval.
+template <int NQT, bool SAMPLE>
+__global__ __launch_bounds__(256) void k_scan_mfma(
+    const uint4* __restrict__ codes, const float* __restrict__ scale,
+    const float* __restrict__ vnorm, const float* __restrict__ enorm,
+    const uint64_t* __restrict__ vis, int64_t nblocks, int32_t nchunk,
+    const v4i* __restrict__ qfrag, const ScanQ* __restrict__ sq, int32_t nq, float gamma,
+    int64_t sample_stride, float* __restrict__ sample_lo, int64_t sample_ld,
+    int32_t* __restrict__ cand_row, float* __restrict__ cand_lo, float* __restrict__ cand_hi,
+    int32_t* __restrict__ cand_cnt, int64_t cap) {
+    const int lane = threadIdx.x & 63;
+    const int64_t w = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+    const int64_t blk = SAMPLE ? w * sample_stride : w;
+    if (blk >= nblocks) return;
+    v16i acc[2][NQT];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int u = 0; u < NQT; ++u) acc[t][u] = v16i{};
+    const uint4* A = codes + blk * nchunk * 64 + (lane >> 5) * 64 + (lane & 31);
+    const int nsteps = nchunk >> 1;
+#pragma unroll 2
+    for (int s = 0; s < nsteps; ++s) {
+        const u32x4 a0 = load_nt(A + 2 * s * 64);
+        const u32x4 a1 = load_nt(A + 2 * s * 64 + 32);
+        v4i va0, va1;
+        __builtin_memcpy(&va0, &a0, 16);
+        __builtin_memcpy(&va1, &a1, 16);
+#pragma unroll
+        for (int u = 0; u < NQT; ++u) {
+            const v4i vb = qfrag[(s * NQT + u) * 64 + lane];
+            acc[0][u] = __builtin_amdgcn_mfma_i32_32x32x32_i8(va0, vb, acc[0][u], 0, 0, 0);
+            acc[1][u] = __builtin_amdgcn_mfma_i32_32x32x32_i8(va1, vb, acc[1][u], 0, 0, 0);
+        }
+    }
+    const uint64_t vbits = vis[blk];
+#pragma unroll
+    for (int u = 0; u < NQT; ++u) {
+        const int b = 32 * u + (lane & 31);
+        if (b >= nq) continue;
+        const ScanQ Q = sq[b];
+        // conservative pre-test: hi >= tau implies c >= thr
+        const float thr = Q.tau - Q.wmax * 1.001f - 0x1p-20f * (fabsf(Q.tau) + Q.wmax);
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int rib = 32 * t + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                const int64_t row = blk * 64 + rib;
+                const int dot = acc[t][u][r];
+                const float sv = scale[row];
+                if (SAMPLE) {
+                    float lo, hi;
+                    pair_interval(Q, sv, vnorm[row], enorm[row], dot, gamma, lo, hi);
+                    const bool elig = ((vbits >> rib) & 1ull) && (!Q.has_cert || lo <= Q.s_cert);
+                    sample_lo[b * sample_ld + w * 64 + rib] = elig ? lo : -INFINITY;
+                } else {
+                    const float c = (Q.sq * sv) * static_cast<float>(dot);
+                    if (c >= thr && ((vbits >> rib) & 1ull)) {
+                        float lo, hi;
+                        pair_interval(Q, sv, vnorm[row], enorm[row], dot, gamma, lo, hi);
+                        if (hi >= Q.tau && (!Q.has_cert || lo <= Q.s_cert)) {
+                            const int pos = atomicAdd(&cand_cnt[b], 1);
+                            if (pos < cap) {
+                                const int64_t o = static_cast<int64_t>(b) * cap + pos;
+                                cand_row[o] = static_cast<int32_t>(row);
+                                cand_lo[o] = lo;
+                                cand_hi[o] = hi;
+                            }
+                        }
+                    }
+                }
+            }
+        }
+    }
+}
+
+template <int NQT>
+static void mfma_pass(const IndexView& ix, const uint64_t* vis, int64_t nblocks, const v4i* qfrag,
+                      const ScanQ* sq, int32_t nq, float gamma, bool sample, int64_t sample_stride,
+                      float* sample_lo, int64_t sample_ld, int32_t* cand_row, float* cand_lo,
+                      float* cand_hi, int32_t* cand_cnt, int64_t cap, hipStream_t stream) {
+    const int64_t waves = sample ? (nblocks + sample_stride - 1) / sample_stride : nblocks;
+    const uint32_t grid = static_cast<uint32_t>((waves + 3) / 4);
+    if (sample) {
+        hipLaunchKernelGGL((k_scan_mfma<NQT, true>), dim3(grid), dim3(256), 0, stream, ix.codes,
+                           ix.scale, ix.vnorm, ix.enorm, vis, nblocks, ix.nchunk, qfrag, sq, nq,
+                           gamma, sample_stride, sample_lo, sample_ld, cand_row, cand_lo, cand_hi,
+                           cand_cnt, cap);
+    } else {
+        hipLaunchKernelGGL((k_scan_mfma<NQT, false>), dim3(grid), dim3(256), 0, stream, ix.codes,
+                           ix.scale, ix.vnorm, ix.enorm, vis, nblocks, ix.nchunk, qfrag, sq, nq,
+                           gamma, sample_stride, sample_lo, sample_ld, cand_row, cand_lo, cand_hi,
+                           cand_cnt, cap);
+    }
+}
+
+int mfma_tiles_for(int32_t nq) {
+    const int t = (nq + 31) / 32;
+    return t <= 1 ? 1 : t <= 2 ? 2 : t <= 4 ? 4 : 8;
+}
+
+void launch_scan_mfma(const IndexView& ix, const uint64_t* vis, int64_t nblocks,
+                      const int8_t* qcodes, const ScanQ* sq, int32_t nq, float gamma, bool sample,
+                      int64_t sample_stride, float* sample_lo, int64_t sample_ld, int32_t* cand_row,
+                      float* cand_lo, float* cand_hi, int32_t* cand_cnt, int64_t cap, void* frag,
+                      hipStream_t stream) {
+    for (int32_t q0 = 0; q0 < nq; q0 += kMaxMfmaQueries) {
+        const int32_t n = (nq - q0 < kMaxMfmaQueries) ? (nq - q0) : kMaxMfmaQueries;
+        const int nqt = mfma_tiles_for(n);
+        const ScanQ* s = sq + q0;
+        hipLaunchKernelGGL(k_qfrag, dim3((ix.dp / 32) * nqt), dim3(64), 0, stream, qcodes, ix.dp, s,
+                           n, nqt, static_cast<uint4*>(frag));
+        const v4i* qf = static_cast<const v4i*>(frag);
+        float* sl = sample_lo ? sample_lo + q0 * sample_ld : nullptr;
+        int32_t* cr = cand_row ? cand_row + q0 * cap : nullptr;
+        float* cl = cand_lo ? cand_lo + q0 * cap : nullptr;
+        float* ch = cand_hi ? cand_hi + q0 * cap : nullptr;
+        int32_t* cc = cand_cnt ? cand_cnt + q0 : nullptr;
+#define PVS_MFMA_CASE(N)                                                                        \
+    case N:                                                                                     \
+        mfma_pass<N>(ix, vis, nblocks, qf, s, n, gamma, sample, sample_stride, sl, sample_ld, cr, \
+                     cl, ch, cc, cap, stream);                                                  \
+        break;
+        switch (nqt) {
+            PVS_MFMA_CASE(1)
+            PVS_MFMA_CASE(2)
+            PVS_MFMA_CASE(4)
+            PVS_MFMA_CASE(8)
+            default:
+                break;
+        }
+#undef PVS_MFMA_CASE
+    }
+}
+
 // ------------------------------------------------------------ threshold
 // One workgroup per query: tau = the k-th largest finite sampled lower bound
 // (radix select over order-preserving keys, 8 bits per pass); -inf when

@@ -71,7 +71,8 @@ class pvs_counters(C.Structure):
 class pvs_profile(C.Structure):
     _fields_ = [("scan_ms", C.c_double), ("scan_launches", C.c_int64), ("scan_bytes", C.c_int64),
                 ("sample_ms", C.c_double), ("rescore_ms", C.c_double), ("rescore_rows", C.c_int64),
-                ("sort_ms", C.c_double), ("scan_rounds", C.c_int64)]
+                ("sort_ms", C.c_double), ("scan_rounds", C.c_int64),
+                ("mfma_launches", C.c_int64)]
 
     def as_dict(self):
         return {f: getattr(self, f) for f, _ in self._fields_}

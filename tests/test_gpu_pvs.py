@@ -252,6 +252,28 @@ def test_nonfinite_inputs_rejected(E):
     assert ei.value.code == E.EAHR_E_NONFINITE
 
 
+def _open_with_path(E, idx, q, path, monkeypatch):
+    monkeypatch.setenv("EAHR_SCAN_PATH", path)
+    st = E.pvs_open(idx, q)
+    monkeypatch.delenv("EAHR_SCAN_PATH")
+    return st
+
+
+@pytest.mark.parametrize("B", [1, 5, 40, 100, 300])
+def test_mfma_and_gemv_scans_agree(E, tiny, tiny_index, monkeypatch, B):
+    """The Int8 MFMA scan (query tiles of 32, passes of 256) and the dot4 GEMV
+    scan produce the same ranks, bit for bit."""
+    w, x, q = tiny
+    qb, _ = datagen.queries(datagen.workload("tiny"), count=B)
+    a = _open_with_path(E, tiny_index, qb, "mfma", monkeypatch)
+    g = _open_with_path(E, tiny_index, qb, "gemv", monkeypatch)
+    ia, sa, _ = _drain(E, a, [20, 300])
+    ig, sg, _ = _drain(E, g, [20, 300])
+    assert ia == ig and sa == sg
+    for b in range(0, B, max(1, B // 4)):
+        check_dense_prefix(qb[b], x, ia[b], sa[b])
+
+
 def test_single_hip_runtime_in_process(E):
     import re
     maps = open("/proc/self/maps").read()
