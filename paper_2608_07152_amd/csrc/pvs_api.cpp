@@ -310,64 +310,96 @@ pvs_state::~pvs_state() {
     dev_free(qhnorm);
     dev_free(qflags);
     release_scan_buffers();
-    if (h_scanq) (void)hipHostFree(h_scanq);
-    if (h_counts) (void)hipHostFree(h_counts);
-    if (h_packed) (void)hipHostFree(h_packed);
     for (auto& e : ev)
         if (e) (void)hipEventDestroy(e);
 }
 
 void pvs_state::release_scan_buffers() {
     dev_free(scanq);
+    dev_free(counts);
+    dev_free(sample_lo);
+    dev_free(sample_hi);
+    dev_free(qfrag);
     dev_free(cand_row);
     dev_free(cand_lo);
     dev_free(cand_hi);
     dev_free(keys);
     dev_free(keys_tmp);
-    dev_free(counts);
     dev_free(packed);
-    dev_free(sample);
-    dev_free(qfrag);
+    if (h_scanq) (void)hipHostFree(h_scanq);
+    if (h_counts) (void)hipHostFree(h_counts);
+    if (h_packed) (void)hipHostFree(h_packed);
+    h_scanq = nullptr;
+    h_counts = nullptr;
+    h_packed = nullptr;
     buf_nq = 0;
-    buf_cap = 0;
     buf_sample = 0;
+    pool_cap = 0;
+    h_packed_cap = 0;
 }
 
+// Per-query scan buffers for nq queries and samples of sample_ld rows.
 // counts layout: [cand nq][cert nq][fail nq][offs nq + 1]
-static int ensure_scan_buffers(pvs_state* st, int32_t nq, int64_t cap, int64_t sample_ld) {
-    if (nq <= st->buf_nq && cap <= st->buf_cap && sample_ld <= st->buf_sample) return EAHR_OK;
+static int ensure_query_buffers(pvs_state* st, int32_t nq, int64_t sample_ld) {
+    if (nq <= st->buf_nq && sample_ld <= st->buf_sample) return EAHR_OK;
     nq = std::max(nq, st->buf_nq);
-    cap = std::max(cap, st->buf_cap);
     sample_ld = std::max(sample_ld, st->buf_sample);
     HIP_TRY(hipStreamSynchronize(st->ix->stream));
-    st->release_scan_buffers();
-    const size_t tot = static_cast<size_t>(nq) * cap;
-    EAHR_TRY(dev_alloc(&st->scanq, nq));
-    EAHR_TRY(dev_alloc(&st->cand_row, tot));
-    EAHR_TRY(dev_alloc(&st->cand_lo, tot));
-    EAHR_TRY(dev_alloc(&st->cand_hi, tot));
-    EAHR_TRY(dev_alloc(&st->keys, tot));
-    EAHR_TRY(dev_alloc(&st->keys_tmp, tot));
-    EAHR_TRY(dev_alloc(&st->counts, 4 * static_cast<size_t>(nq) + 1));
-    EAHR_TRY(dev_alloc(&st->packed, tot));
-    EAHR_TRY(dev_alloc(&st->sample, static_cast<size_t>(nq) * sample_ld));
-    {
-        int8_t* f;
-        EAHR_TRY(dev_alloc(&f, static_cast<size_t>(st->ix->dp / 32) * 8 * 64 * 16));
-        st->qfrag = f;
-    }
+    dev_free(st->scanq);
+    dev_free(st->counts);
+    dev_free(st->sample_lo);
+    dev_free(st->sample_hi);
+    dev_free(st->qfrag);
     if (st->h_scanq) (void)hipHostFree(st->h_scanq);
     if (st->h_counts) (void)hipHostFree(st->h_counts);
-    if (st->h_packed) (void)hipHostFree(st->h_packed);
     st->h_scanq = nullptr;
     st->h_counts = nullptr;
-    st->h_packed = nullptr;
+    EAHR_TRY(dev_alloc(&st->scanq, nq));
+    EAHR_TRY(dev_alloc(&st->counts, 4 * static_cast<size_t>(nq) + 1));
+    EAHR_TRY(dev_alloc(&st->sample_lo, static_cast<size_t>(nq) * sample_ld));
+    EAHR_TRY(dev_alloc(&st->sample_hi, static_cast<size_t>(nq) * sample_ld));
+    int8_t* f;
+    EAHR_TRY(dev_alloc(&f, static_cast<size_t>(st->ix->dp / 32) * 8 * 64 * 16));
+    st->qfrag = f;
     HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&st->h_scanq), nq * sizeof(ScanQ)));
-    HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&st->h_counts), (4 * static_cast<size_t>(nq) + 1) * sizeof(int32_t)));
-    HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&st->h_packed), tot * sizeof(uint64_t)));
+    HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&st->h_counts),
+                          (4 * static_cast<size_t>(nq) + 1) * sizeof(int32_t)));
     st->buf_nq = nq;
-    st->buf_cap = cap;
     st->buf_sample = sample_ld;
+    return EAHR_OK;
+}
+
+// Candidate pool of `slots` entries shared by the regions of one scan.
+static int ensure_pool(pvs_state* st, int64_t slots) {
+    if (slots <= st->pool_cap) return EAHR_OK;
+    slots = std::max<int64_t>(slots + slots / 4, pvs::kMinCap);
+    HIP_TRY(hipStreamSynchronize(st->ix->stream));
+    dev_free(st->cand_row);
+    dev_free(st->cand_lo);
+    dev_free(st->cand_hi);
+    dev_free(st->keys);
+    dev_free(st->keys_tmp);
+    dev_free(st->packed);
+    st->pool_cap = 0;
+    const size_t n = static_cast<size_t>(slots);
+    EAHR_TRY(dev_alloc(&st->cand_row, n));
+    EAHR_TRY(dev_alloc(&st->cand_lo, n));
+    EAHR_TRY(dev_alloc(&st->cand_hi, n));
+    EAHR_TRY(dev_alloc(&st->keys, n));
+    EAHR_TRY(dev_alloc(&st->keys_tmp, n));
+    EAHR_TRY(dev_alloc(&st->packed, n));
+    st->pool_cap = slots;
+    return EAHR_OK;
+}
+
+static int ensure_host_packed(pvs_state* st, int64_t n) {
+    if (n <= st->h_packed_cap) return EAHR_OK;
+    n = std::max<int64_t>(n + n / 4, 4096);
+    if (st->h_packed) (void)hipHostFree(st->h_packed);
+    st->h_packed = nullptr;
+    st->h_packed_cap = 0;
+    HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&st->h_packed), n * sizeof(uint64_t)));
+    st->h_packed_cap = n;
     return EAHR_OK;
 }
 
@@ -574,10 +606,16 @@ static int64_t lower_overlap(const pvs_state* st, int32_t b) {
 }
 
 // One scan round over the queries in `todo`; removes the queries it finished.
+//  1. sample pass + select: tau and the sampled hit count of every query;
+//  2. candidate regions sized from the hits (host), main scan;
+//  3. rescore, sort, pack; certified ranks appended to each query's cache.
+// Queries whose region overflowed are scanned again with room for all of
+// their candidates; queries that certified too few ranks again with a lower
+// threshold.
 static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     const pvs_index* ix = st->ix;
     hipStream_t s = ix->stream;
-    const int32_t nq = static_cast<int32_t>(todo.size());
+    int32_t nq = static_cast<int32_t>(todo.size());
     const int64_t nblocks = (st->n_rows + 63) / 64;
     if (nblocks == 0) {
         for (int32_t b : todo) st->q[b].cert_exhausted = true;
@@ -589,12 +627,7 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     const int64_t nsb = (nblocks + stride - 1) / stride;
     const int64_t sample_ld = nsb * 64;
     const double frac = static_cast<double>(nsb) / static_cast<double>(nblocks);
-
-    int64_t cap = std::max<int64_t>(st->buf_cap, pvs::kMinCap);
-    for (int32_t b : todo) cap = std::max(cap, st->q[b].cap_hint);
-    cap = round_up(cap, 256);
-    EAHR_TRY(ensure_scan_buffers(st, nq, cap, sample_ld));
-    cap = st->buf_cap;
+    EAHR_TRY(ensure_query_buffers(st, nq, sample_ld));
 
     const int64_t mmin = std::max<int64_t>(pvs::kTargetMin, std::min<int64_t>(pvs::kTargetMax, pvs::kTargetBudget / nq));
     for (int32_t i = 0; i < nq; ++i) {
@@ -612,12 +645,8 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
         sq.k = static_cast<int32_t>(std::min(k, 2.0e9));
         st->h_scanq[i] = sq;
     }
-    int32_t* d_cand = st->counts;
-    int32_t* d_cert = st->counts + nq;
-    int32_t* d_fail = st->counts + 2 * nq;
-    int32_t* d_offs = st->counts + 3 * nq;
-    HIP_TRY(hipMemcpyAsync(st->scanq, st->h_scanq, nq * sizeof(ScanQ), hipMemcpyHostToDevice, s));
-    HIP_TRY(hipMemsetAsync(st->counts, 0, (4 * static_cast<size_t>(nq) + 1) * sizeof(int32_t), s));
+    const bool mfma = st->path == pvs::ScanPath::Mfma ||
+                      (st->path == pvs::ScanPath::Auto && nq >= pvs::kMfmaMinQueries);
     const bool prof = g_prof_on.load(std::memory_order_relaxed) != 0;
     if (prof && !st->ev[0])
         for (auto& e : st->ev) HIP_TRY(hipEventCreate(&e));
@@ -626,59 +655,98 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
         return EAHR_OK;
     };
     const pvs::IndexView v = view_of(ix);
+    auto scan = [&](bool sample, const pvs::ScanOut& o, int32_t n) {
+        if (mfma) pvs::launch_scan_mfma(v, st->vis, nblocks, st->qcodes, st->scanq, n, ix->gamma, sample, o, st->qfrag, s);
+        else pvs::launch_scan(v, st->vis, nblocks, st->qcodes, st->scanq, n, ix->gamma, sample, o, s);
+    };
+
+    // 1. threshold and candidate estimate from the sampled blocks
+    HIP_TRY(hipMemcpyAsync(st->scanq, st->h_scanq, nq * sizeof(ScanQ), hipMemcpyHostToDevice, s));
+    pvs::ScanOut so;
+    so.sample_lo = st->sample_lo;
+    so.sample_hi = st->sample_hi;
+    so.sample_ld = sample_ld;
+    so.sample_stride = stride;
     EAHR_TRY(mark(0));
-    const bool mfma = st->path == pvs::ScanPath::Mfma ||
-                      (st->path == pvs::ScanPath::Auto && nq >= pvs::kMfmaMinQueries);
-    if (mfma) {
-        pvs::launch_scan_mfma(v, st->vis, nblocks, st->qcodes, st->scanq, nq, ix->gamma, true, stride,
-                              st->sample, sample_ld, nullptr, nullptr, nullptr, nullptr, 0, st->qfrag, s);
-    } else {
-        pvs::launch_scan(v, st->vis, nblocks, st->qcodes, st->scanq, nq, ix->gamma, true, stride,
-                         st->sample, sample_ld, nullptr, nullptr, nullptr, nullptr, 0, s);
-    }
-    pvs::launch_select(st->sample, sample_ld, sample_ld, st->scanq, nq, s);
+    scan(true, so, nq);
+    pvs::launch_select(st->sample_lo, st->sample_hi, sample_ld, sample_ld, st->scanq, nq, s);
     EAHR_TRY(mark(1));
-    if (mfma) {
-        pvs::launch_scan_mfma(v, st->vis, nblocks, st->qcodes, st->scanq, nq, ix->gamma, false, 1,
-                              nullptr, 0, st->cand_row, st->cand_lo, st->cand_hi, d_cand, cap,
-                              st->qfrag, s);
-    } else {
-        pvs::launch_scan(v, st->vis, nblocks, st->qcodes, st->scanq, nq, ix->gamma, false, 1, nullptr,
-                         0, st->cand_row, st->cand_lo, st->cand_hi, d_cand, cap, s);
+    HIP_TRY(hipGetLastError());
+    HIP_TRY(hipMemcpyAsync(st->h_scanq, st->scanq, nq * sizeof(ScanQ), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+
+    // 2. candidate regions: the sample saw every block when stride == 1.
+    //    Queries past the pool limit wait for the next round (kept in todo).
+    int64_t total = 0;
+    int32_t run = 0;
+    for (; run < nq; ++run) {
+        ScanQ& sq = st->h_scanq[run];
+        const auto& Q = st->q[todo[run]];
+        int64_t cap = (stride == 1)
+                          ? static_cast<int64_t>(sq.sample_hits)
+                          : static_cast<int64_t>(std::ceil(sq.sample_hits / frac * pvs::kCapSlack)) + pvs::kCapPad;
+        cap = std::max(cap, Q.cap_hint);
+        cap = std::min<int64_t>(std::max<int64_t>(cap, 1), st->n_rows);
+        if (run > 0 && total + cap > pvs::kPoolMax) break;
+        sq.cand_off = total;
+        sq.cand_cap = cap;
+        total += cap;
     }
+    std::vector<int32_t> later(todo.begin() + run, todo.end());
+    todo.resize(run);
+    nq = run;
+    EAHR_TRY(ensure_pool(st, total));
+    HIP_TRY(hipMemcpyAsync(st->scanq, st->h_scanq, nq * sizeof(ScanQ), hipMemcpyHostToDevice, s));
+    int32_t* d_cand = st->counts;
+    int32_t* d_cert = st->counts + nq;
+    int32_t* d_fail = st->counts + 2 * nq;
+    int32_t* d_offs = st->counts + 3 * nq;
+    HIP_TRY(hipMemsetAsync(st->counts, 0, (4 * static_cast<size_t>(nq) + 1) * sizeof(int32_t), s));
+    pvs::ScanOut mo;
+    mo.cand_row = st->cand_row;
+    mo.cand_lo = st->cand_lo;
+    mo.cand_hi = st->cand_hi;
+    mo.cand_cnt = d_cand;
     EAHR_TRY(mark(2));
+    scan(false, mo, nq);
+    EAHR_TRY(mark(3));
     HIP_TRY(hipGetLastError());
     HIP_TRY(hipMemcpyAsync(st->h_counts, d_cand, nq * sizeof(int32_t), hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
     st->stats.scans += 1;
     st->stats.sample_scans += 1;
     st->stats.rows_scanned += nblocks * 64;
-    st->stats.bytes_scanned += nblocks * 64 * (static_cast<int64_t>(ix->d) + 12) + nblocks * 8;
+    st->stats.bytes_scanned += st->n_rows * (static_cast<int64_t>(ix->d) + 12) + nblocks * 8;
 
+    // 3. rescore, order and pack the certified ranks
     std::vector<int32_t> cand(st->h_counts, st->h_counts + nq);
-    int64_t max_cnt = 0, total = 0;
+    int64_t max_cnt = 0, kept = 0;
     for (int32_t i = 0; i < nq; ++i) {
-        const int64_t c = std::min<int64_t>(cand[i], cap);
+        const int64_t c = std::min<int64_t>(cand[i], st->h_scanq[i].cand_cap);
         max_cnt = std::max(max_cnt, c);
-        total += c;
+        kept += c;
     }
-    EAHR_TRY(mark(3));
     pvs::launch_rescore(v, st->qrows, st->scanq, nq, st->cand_row, st->cand_lo, st->cand_hi, d_cand,
-                        cap, max_cnt, st->keys, d_cert, d_fail, s);
+                        max_cnt, st->keys, d_cert, d_fail, s);
     EAHR_TRY(mark(4));
-    uint64_t* sorted = pvs::launch_segmented_sort(st->keys, st->keys_tmp, d_cand, nq, cap, max_cnt, s);
-    pvs::launch_pack(sorted, d_cert, nq, cap, max_cnt, d_offs, st->packed, s);
+    uint64_t* sorted = pvs::launch_segmented_sort(st->keys, st->keys_tmp, d_cand, st->scanq, nq, max_cnt, s);
+    pvs::launch_pack(sorted, d_cert, st->scanq, nq, max_cnt, d_offs, st->packed, s);
     EAHR_TRY(mark(5));
     HIP_TRY(hipGetLastError());
+    EAHR_TRY(ensure_host_packed(st, kept));
     HIP_TRY(hipMemcpyAsync(st->h_counts + nq, d_cert, (3 * static_cast<size_t>(nq) + 1) * sizeof(int32_t),
                            hipMemcpyDeviceToHost, s));
-    if (total > 0)
-        HIP_TRY(hipMemcpyAsync(st->h_packed, st->packed, total * sizeof(uint64_t), hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
+    const int32_t* h_cert = st->h_counts + nq;
+    const int32_t* h_fail = st->h_counts + 2 * nq;
+    const int32_t* h_offs = st->h_counts + 3 * nq;
+    if (h_offs[nq] > 0)
+        HIP_TRY(hipMemcpy(st->h_packed, st->packed, static_cast<size_t>(h_offs[nq]) * sizeof(uint64_t),
+                          hipMemcpyDeviceToHost));
     if (prof) {
-        float t[5];
+        float t[4];
         HIP_TRY(hipEventElapsedTime(&t[0], st->ev[0], st->ev[1]));
-        HIP_TRY(hipEventElapsedTime(&t[1], st->ev[1], st->ev[2]));
+        HIP_TRY(hipEventElapsedTime(&t[1], st->ev[2], st->ev[3]));
         HIP_TRY(hipEventElapsedTime(&t[2], st->ev[3], st->ev[4]));
         HIP_TRY(hipEventElapsedTime(&t[3], st->ev[4], st->ev[5]));
         std::lock_guard<std::mutex> lk(g_prof_mu);
@@ -690,16 +758,12 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
         if (mfma) g_prof.mfma_launches += launches;
         g_prof.scan_bytes += launches * (st->n_rows * (static_cast<int64_t>(ix->d) + 12) + nblocks * 8);
         g_prof.rescore_ms += t[2];
-        g_prof.rescore_rows += total;
+        g_prof.rescore_rows += kept;
         g_prof.sort_ms += t[3];
         g_prof.scan_rounds += 1;
     }
-    const int32_t* h_cert = st->h_counts + nq;
-    const int32_t* h_fail = st->h_counts + 2 * nq;
-    const int32_t* h_offs = st->h_counts + 3 * nq;
 
     std::vector<int32_t> keep;
-    int64_t grow = 0;
     for (int32_t i = 0; i < nq; ++i) {
         const int32_t b = todo[i];
         auto& Q = st->q[b];
@@ -707,12 +771,12 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
             Q.failed = true;
             continue;
         }
-        if (cand[i] > cap) {   // candidate list overflowed: redo with room for all
-            Q.cap_hint = round_up(static_cast<int64_t>(cand[i]) + cand[i] / 4 + 256, 256);
-            grow = std::max(grow, Q.cap_hint);
+        if (cand[i] > st->h_scanq[i].cand_cap) {   // region overflowed: redo with room for all
+            Q.cap_hint = static_cast<int64_t>(cand[i]) + cand[i] / 4 + 256;
             keep.push_back(b);
             continue;
         }
+        Q.cap_hint = 0;
         st->stats.candidates += cand[i];
         const int64_t c = h_cert[i];
         const uint64_t* kp = st->h_packed + h_offs[i];
@@ -740,8 +804,8 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
             keep.push_back(b);
         }
     }
+    keep.insert(keep.end(), later.begin(), later.end());
     todo.swap(keep);
-    if (grow > 0) EAHR_TRY(ensure_scan_buffers(st, st->buf_nq, grow, st->buf_sample));
     return EAHR_OK;
 }
 

@@ -12,8 +12,14 @@ namespace pvs {
 // Threshold estimation samples every stride-th code block, with the stride
 // the largest power of two that keeps at least this many blocks sampled.
 constexpr int64_t kSampleBlocks = 2048;
-// Smallest per-query candidate capacity allocated for a scan.
+// Smallest candidate pool allocated for a scan, and the largest pool one scan
+// round may use (queries beyond it wait for the next round).
 constexpr int64_t kMinCap = 4096;
+constexpr int64_t kPoolMax = int64_t(1) << 28;
+// Candidate regions are sized from the sample: hits / sampled fraction times
+// kCapSlack plus kCapPad slots.
+constexpr double kCapSlack = 1.5;
+constexpr int64_t kCapPad = 2048;
 // Ranks a scan aims to certify per query beyond the request: about
 // kTargetBudget / (queries in the scan), clamped to [kTargetMin, kTargetMax].
 // A single-query scan streams the whole code array, so certifying a deep
@@ -84,24 +90,28 @@ struct pvs_state {
     uint32_t* qflags = nullptr;
     std::vector<Query> q;
     pvs_counters stats{};
-    // scan buffers, sized for buf_nq queries of buf_cap candidates
+    // per-query scan buffers, sized for buf_nq queries and buf_sample rows
     int32_t buf_nq = 0;
-    int64_t buf_cap = 0, buf_sample = 0;
+    int64_t buf_sample = 0;
     pvs::ScanQ* scanq = nullptr;
+    int32_t* counts = nullptr;
+    float* sample_lo = nullptr;
+    float* sample_hi = nullptr;
+    void* qfrag = nullptr;             // query codes in MFMA operand order
+    // candidate pool (pool_cap slots) split into per-query regions per scan
+    int64_t pool_cap = 0;
     int32_t* cand_row = nullptr;
     float* cand_lo = nullptr;
     float* cand_hi = nullptr;
     uint64_t* keys = nullptr;
     uint64_t* keys_tmp = nullptr;
-    int32_t* counts = nullptr;
     uint64_t* packed = nullptr;
-    float* sample = nullptr;
-    void* qfrag = nullptr;             // query codes in MFMA operand order
     pvs::ScanPath path = pvs::ScanPath::Auto;
     hipEvent_t ev[7] = {};             // profiling events (created on first use)
-    pvs::ScanQ* h_scanq = nullptr;   // pinned host mirrors
+    pvs::ScanQ* h_scanq = nullptr;     // pinned host mirrors
     int32_t* h_counts = nullptr;
     uint64_t* h_packed = nullptr;
+    int64_t h_packed_cap = 0;
     void release_scan_buffers();
     ~pvs_state();
 };

@@ -27,9 +27,11 @@ struct ScanQ {
     float nqh;         // ||q_hat||_2 rounded up
     float neq;         // ||e_q||_2 rounded up
     float wmax;        // upper bound of E + G over every row of the index
-    int32_t pad;
+    int32_t sample_hits;  // sampled eligible rows with hi >= tau (select pass)
+    int64_t cand_off;  // first slot of this query's candidate region
+    int64_t cand_cap;  // slots in the region
 };
-static_assert(sizeof(ScanQ) == 48, "ScanQ layout");
+static_assert(sizeof(ScanQ) == 64, "ScanQ layout");
 
 // Row storage of an index.  Codes of 64 consecutive rows form one block laid
 // out chunk-major: byte j of row r lives at
@@ -50,34 +52,49 @@ void launch_quantize(const float* src, int64_t nrows, int32_t d, int64_t src_str
                      float* vnorm, float* enorm, float* hnorm, float* rows, int32_t df,
                      uint32_t* flags, hipStream_t stream);
 
+// Outputs of a scan pass.  Sample pass: lower and upper bounds of every
+// (query, row) pair of the sampled blocks, row-major [query][sample_ld],
+// -inf / -inf for ineligible rows.  Main pass: candidates of query b go to
+// slots cand_off .. cand_off + cand_cap - 1 of its ScanQ; cand_cnt[b] counts
+// every candidate, including those past the region.
+struct ScanOut {
+    float* sample_lo = nullptr;
+    float* sample_hi = nullptr;
+    int64_t sample_ld = 0;
+    int64_t sample_stride = 1;   // sampled blocks are multiples of this
+    int32_t* cand_row = nullptr;
+    float* cand_lo = nullptr;
+    float* cand_hi = nullptr;
+    int32_t* cand_cnt = nullptr;
+};
+
 void launch_scan(const IndexView& ix, const uint64_t* vis, int64_t nblocks, const int8_t* qcodes,
-                 const ScanQ* sq, int32_t nq, float gamma, bool sample, int64_t sample_stride,
-                 float* sample_lo, int64_t sample_ld, int32_t* cand_row, float* cand_lo,
-                 float* cand_hi, int32_t* cand_cnt, int64_t cap, hipStream_t stream);
+                 const ScanQ* sq, int32_t nq, float gamma, bool sample, const ScanOut& o,
+                 hipStream_t stream);
 
 // Int8 MFMA variant (same outputs as launch_scan).  `frag` is device scratch
 // of (dp / 32) * 8 KiB for the query codes in MFMA operand order.
 void launch_scan_mfma(const IndexView& ix, const uint64_t* vis, int64_t nblocks,
                       const int8_t* qcodes, const ScanQ* sq, int32_t nq, float gamma, bool sample,
-                      int64_t sample_stride, float* sample_lo, int64_t sample_ld, int32_t* cand_row,
-                      float* cand_lo, float* cand_hi, int32_t* cand_cnt, int64_t cap, void* frag,
-                      hipStream_t stream);
+                      const ScanOut& o, void* frag, hipStream_t stream);
 int mfma_tiles_for(int32_t nq);
 
-void launch_select(const float* sample_lo, int64_t n, int64_t ld, ScanQ* sq, int32_t nq,
-                   hipStream_t stream);
+// tau = k-th largest finite sampled lower bound; sample_hits = sampled pairs
+// with hi >= tau (both written into sq).
+void launch_select(const float* sample_lo, const float* sample_hi, int64_t n, int64_t ld,
+                   ScanQ* sq, int32_t nq, hipStream_t stream);
 
 void launch_rescore(const IndexView& ix, const float* qrows, const ScanQ* sq, int32_t nq,
                     const int32_t* cand_row, const float* cand_lo, const float* cand_hi,
-                    const int32_t* cand_cnt, int64_t cap, int64_t max_cnt, uint64_t* keys,
-                    int32_t* cert_cnt, int32_t* fail, hipStream_t stream);
+                    const int32_t* cand_cnt, int64_t max_cnt, uint64_t* keys, int32_t* cert_cnt,
+                    int32_t* fail, hipStream_t stream);
 
-// Sorts keys[b*cap + (0..cnt_b)] ascending for every b; returns the buffer
-// holding the result (keys or tmp).
-uint64_t* launch_segmented_sort(uint64_t* keys, uint64_t* tmp, const int32_t* cnt, int32_t nq,
-                                int64_t cap, int64_t max_cnt, hipStream_t stream);
+// Sorts every query's candidate keys (its region, min(cnt, cap) entries)
+// ascending; returns the buffer holding the result (keys or tmp).
+uint64_t* launch_segmented_sort(uint64_t* keys, uint64_t* tmp, const int32_t* cnt,
+                                const ScanQ* sq, int32_t nq, int64_t max_cnt, hipStream_t stream);
 
-void launch_pack(const uint64_t* keys, const int32_t* cert_cnt, int32_t nq, int64_t cap,
+void launch_pack(const uint64_t* keys, const int32_t* cert_cnt, const ScanQ* sq, int32_t nq,
                  int64_t max_cnt, int32_t* offs, uint64_t* packed, hipStream_t stream);
 
 void launch_intervals(const IndexView& ix, const int8_t* qcodes, const ScanQ* sq, float gamma,

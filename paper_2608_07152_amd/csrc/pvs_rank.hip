@@ -1,0 +1,208 @@
+// Candidate rescoring, ordering and packing of the PVS dense channel.
+//
+// Every candidate gets its authoritative float32 score (row_score, one fixed
+// order), is checked against its interval (App. A.1: a score outside it fails
+// the request), and receives a 64-bit sort key.  A scan with threshold tau
+// certifies exactly the candidates with s32 >= tau whose key follows the last
+// certified key; their keys are (~mono(s32) << 32 | row), so ascending keys
+// are (score descending, id ascending).  Other candidates get (~0 << 32 | row)
+// and sort after every certified one.  Keys are unique inside a query.
+#include "pvs_device.h"
+
+namespace pvs {
+
+// One wavefront per candidate; grid.y = query.
+template <int J>
+__global__ __launch_bounds__(256) void k_rescore(
+    const float4* __restrict__ rows, int32_t df4, const float4* __restrict__ qrows,
+    const ScanQ* __restrict__ sq, const int32_t* __restrict__ cand_row,
+    const float* __restrict__ cand_lo, const float* __restrict__ cand_hi,
+    const int32_t* __restrict__ cand_cnt, uint64_t* __restrict__ keys,
+    int32_t* __restrict__ cert_cnt, int32_t* __restrict__ fail) {
+    const int lane = threadIdx.x & 63;
+    const int b = blockIdx.y;
+    const ScanQ Q = sq[b];
+    float4 qv[J];
+    load_query_row<J>(qrows, Q.qi, df4, lane, qv);
+    const int64_t n = min(static_cast<int64_t>(cand_cnt[b]), Q.cand_cap);
+    int local_cert = 0;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6); i < n;
+         i += static_cast<int64_t>(gridDim.x) * 4) {
+        const int64_t at = Q.cand_off + i;
+        const int32_t row = cand_row[at];
+        const float s = row_score<J>(rows + static_cast<int64_t>(row) * df4, qv, lane, df4);
+        if (lane == 0) {
+            const float lo = cand_lo[at];
+            const float hi = cand_hi[at];
+            if (!(lo <= s && s <= hi)) fail[b] = 1;
+            const bool dropped = Q.has_cert && (s > Q.s_cert || (s == Q.s_cert && row <= Q.id_cert));
+            const bool cert = !dropped && s >= Q.tau;
+            const uint64_t hiw = cert ? static_cast<uint64_t>(~mono32(s)) : 0xffffffffull;
+            keys[at] = (hiw << 32) | static_cast<uint32_t>(row);
+            local_cert += cert;
+        }
+    }
+    if (lane == 0 && local_cert) atomicAdd(&cert_cnt[b], local_cert);
+}
+
+template <int J>
+static void rescore_j(const IndexView& ix, const float* qrows, const ScanQ* sq, int32_t nq,
+                      const int32_t* cand_row, const float* cand_lo, const float* cand_hi,
+                      const int32_t* cand_cnt, int64_t max_cnt, uint64_t* keys, int32_t* cert_cnt,
+                      int32_t* fail, hipStream_t stream) {
+    int64_t gx = (max_cnt + 3) / 4;
+    if (gx > 4096) gx = 4096;
+    if (gx < 1) gx = 1;
+    hipLaunchKernelGGL((k_rescore<J>), dim3(static_cast<uint32_t>(gx), nq), dim3(256), 0, stream,
+                       reinterpret_cast<const float4*>(ix.rows), ix.df / 4,
+                       reinterpret_cast<const float4*>(qrows), sq, cand_row, cand_lo, cand_hi,
+                       cand_cnt, keys, cert_cnt, fail);
+}
+
+void launch_rescore(const IndexView& ix, const float* qrows, const ScanQ* sq, int32_t nq,
+                    const int32_t* cand_row, const float* cand_lo, const float* cand_hi,
+                    const int32_t* cand_cnt, int64_t max_cnt, uint64_t* keys, int32_t* cert_cnt,
+                    int32_t* fail, hipStream_t stream) {
+    if (nq <= 0 || max_cnt <= 0) return;
+#define PVS_RS(N)                                                                              \
+    case N:                                                                                    \
+        rescore_j<N>(ix, qrows, sq, nq, cand_row, cand_lo, cand_hi, cand_cnt, max_cnt, keys,   \
+                     cert_cnt, fail, stream);                                                  \
+        break;
+    switch (row_chunks(ix.df)) {
+        PVS_RS(1)
+        PVS_RS(2)
+        PVS_RS(3)
+        PVS_RS(4)
+        PVS_RS(8)
+        PVS_RS(16)
+        default:
+            break;
+    }
+#undef PVS_RS
+}
+
+// ------------------------------------------------------------------ sorting
+// Ascending sort of every tile of kSortTile keys of every query's region
+// (bitonic network in LDS; keys past the region's count are padded with ~0
+// and not written back).
+__global__ __launch_bounds__(256) void k_sort_tiles(uint64_t* __restrict__ keys,
+                                                    const int32_t* __restrict__ cnt,
+                                                    const ScanQ* __restrict__ sq) {
+    __shared__ uint64_t s[kSortTile];
+    const int b = blockIdx.y;
+    const int64_t n = min(static_cast<int64_t>(cnt[b]), sq[b].cand_cap);
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kSortTile;
+    if (base >= n) return;
+    uint64_t* k = keys + sq[b].cand_off + base;
+    const int64_t m = min(static_cast<int64_t>(kSortTile), n - base);
+    for (int i = threadIdx.x; i < kSortTile; i += 256) s[i] = (i < m) ? k[i] : ~0ull;
+    __syncthreads();
+    for (int size = 2; size <= kSortTile; size <<= 1) {
+        for (int stride = size >> 1; stride > 0; stride >>= 1) {
+            for (int i = threadIdx.x; i < kSortTile; i += 256) {
+                const int j = i ^ stride;
+                if (j > i) {
+                    const bool asc = (i & size) == 0;
+                    const uint64_t a = s[i], c = s[j];
+                    if ((a > c) == asc) {
+                        s[i] = c;
+                        s[j] = a;
+                    }
+                }
+            }
+            __syncthreads();
+        }
+    }
+    for (int i = threadIdx.x; i < m; i += 256) k[i] = s[i];
+}
+
+// One merge level: runs of length `run` are merged pairwise.  Keys are unique
+// inside a region, so an element's output slot is its offset in its own run
+// plus the number of smaller keys in the partner run (binary search).
+__global__ __launch_bounds__(256) void k_merge(const uint64_t* __restrict__ src,
+                                               uint64_t* __restrict__ dst,
+                                               const int32_t* __restrict__ cnt,
+                                               const ScanQ* __restrict__ sq, int64_t run) {
+    const int b = blockIdx.y;
+    const int64_t n = min(static_cast<int64_t>(cnt[b]), sq[b].cand_cap);
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    if (i >= n) return;
+    const uint64_t* s = src + sq[b].cand_off;
+    uint64_t* d = dst + sq[b].cand_off;
+    const uint64_t key = s[i];
+    const int64_t start = (i / (2 * run)) * (2 * run);
+    const int64_t mid = min(start + run, n);
+    const int64_t end = min(start + 2 * run, n);
+    int64_t lo, hi, own;
+    if (i < mid) {
+        lo = mid;
+        hi = end;
+        own = i - start;
+    } else {
+        lo = start;
+        hi = mid;
+        own = i - mid;
+    }
+    const int64_t first = lo;
+    while (lo < hi) {
+        const int64_t m = (lo + hi) >> 1;
+        if (s[m] < key) lo = m + 1;
+        else hi = m;
+    }
+    d[start + own + (lo - first)] = key;
+}
+
+uint64_t* launch_segmented_sort(uint64_t* keys, uint64_t* tmp, const int32_t* cnt,
+                                const ScanQ* sq, int32_t nq, int64_t max_cnt, hipStream_t stream) {
+    if (nq <= 0 || max_cnt <= 0) return keys;
+    const int64_t tiles = (max_cnt + kSortTile - 1) / kSortTile;
+    hipLaunchKernelGGL(k_sort_tiles, dim3(static_cast<uint32_t>(tiles), nq), dim3(256), 0, stream,
+                       keys, cnt, sq);
+    uint64_t* a = keys;
+    uint64_t* b = tmp;
+    for (int64_t run = kSortTile; run < max_cnt; run *= 2) {
+        const int64_t g = (max_cnt + 255) / 256;
+        hipLaunchKernelGGL(k_merge, dim3(static_cast<uint32_t>(g), nq), dim3(256), 0, stream, a, b,
+                           cnt, sq, run);
+        uint64_t* t = a;
+        a = b;
+        b = t;
+    }
+    return a;
+}
+
+// ----------------------------------------------------------------- packing
+__global__ __launch_bounds__(64) void k_offsets(const int32_t* __restrict__ cert, int32_t nq,
+                                                int32_t* __restrict__ offs) {
+    if (threadIdx.x == 0) {
+        int32_t acc = 0;
+        for (int b = 0; b < nq; ++b) {
+            offs[b] = acc;
+            acc += cert[b];
+        }
+        offs[nq] = acc;
+    }
+}
+
+__global__ __launch_bounds__(256) void k_pack(const uint64_t* __restrict__ keys,
+                                              const int32_t* __restrict__ cert,
+                                              const int32_t* __restrict__ offs,
+                                              const ScanQ* __restrict__ sq,
+                                              uint64_t* __restrict__ packed) {
+    const int b = blockIdx.y;
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    if (i < cert[b]) packed[offs[b] + i] = keys[sq[b].cand_off + i];
+}
+
+void launch_pack(const uint64_t* keys, const int32_t* cert_cnt, const ScanQ* sq, int32_t nq,
+                 int64_t max_cnt, int32_t* offs, uint64_t* packed, hipStream_t stream) {
+    if (nq <= 0) return;
+    hipLaunchKernelGGL(k_offsets, dim3(1), dim3(64), 0, stream, cert_cnt, nq, offs);
+    if (max_cnt <= 0) return;
+    const int64_t g = (max_cnt + 255) / 256;
+    hipLaunchKernelGGL(k_pack, dim3(static_cast<uint32_t>(g), nq), dim3(256), 0, stream, keys,
+                       cert_cnt, offs, sq, packed);
+}
+
+}  // namespace pvs

@@ -1,0 +1,401 @@
+// Interval scans of the PVS dense channel (Sec. 2.3.1): every visible row's
+// Int8 codes are streamed once per scan; each (query, row) pair gets its exact
+// integer dot product and its score interval (pvs_device.h), and rows whose
+// interval can reach the query's threshold tau are appended to the query's
+// candidate region.  A sample pass over every sample_stride-th block records
+// the bounds from which tau is selected.
+//
+// Two kernels compute the same integers: a dot4 GEMV for a few queries and an
+// Int8 MFMA contraction for batches.
+#include "pvs_device.h"
+
+namespace pvs {
+
+// ------------------------------------------------------------------- GEMV
+// One wavefront per 64-row block (lane = row); QB queries per pass, their
+// codes read through scalar loads.  Appends use one atomic per wavefront and
+// query (ballot + prefix count).
+template <int QB, bool SAMPLE>
+__global__ __launch_bounds__(256) void k_scan_gemv(
+    const uint4* __restrict__ codes, const float* __restrict__ scale,
+    const float* __restrict__ vnorm, const float* __restrict__ enorm,
+    const uint64_t* __restrict__ vis, int64_t nblocks, int32_t nchunk,
+    const int8_t* __restrict__ qcodes, int32_t dp, const ScanQ* __restrict__ sq, float gamma,
+    ScanOut o) {
+    const int lane = threadIdx.x & 63;
+    const int64_t w = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+    const int64_t blk = SAMPLE ? w * o.sample_stride : w;
+    if (blk >= nblocks) return;
+    const int64_t row = blk * 64 + lane;
+    const uint64_t vbits = vis[blk];
+    const bool visible = (vbits >> lane) & 1ull;
+    const float sv = scale[row];
+    const float nv = vnorm[row];
+    const float nev = enorm[row];
+
+    const int4* qp[QB];
+#pragma unroll
+    for (int b = 0; b < QB; ++b)
+        qp[b] = reinterpret_cast<const int4*>(qcodes + static_cast<int64_t>(sq[b].qi) * dp);
+    int acc[QB];
+#pragma unroll
+    for (int b = 0; b < QB; ++b) acc[b] = 0;
+    const uint4* cp = codes + blk * nchunk * 64 + lane;
+#pragma unroll 4
+    for (int c = 0; c < nchunk; ++c) {
+        const u32x4 x = load_nt(cp + c * 64);
+#pragma unroll
+        for (int b = 0; b < QB; ++b) {
+            const int4 qc = qp[b][c];
+            int a = acc[b];
+            a = __builtin_amdgcn_sdot4(static_cast<int>(x.x), qc.x, a, false);
+            a = __builtin_amdgcn_sdot4(static_cast<int>(x.y), qc.y, a, false);
+            a = __builtin_amdgcn_sdot4(static_cast<int>(x.z), qc.z, a, false);
+            a = __builtin_amdgcn_sdot4(static_cast<int>(x.w), qc.w, a, false);
+            acc[b] = a;
+        }
+    }
+#pragma unroll
+    for (int b = 0; b < QB; ++b) {
+        const ScanQ Q = sq[b];
+        float lo, hi;
+        pair_interval(Q, sv, nv, nev, acc[b], gamma, lo, hi);
+        const bool elig = visible && (!Q.has_cert || lo <= Q.s_cert);
+        if (SAMPLE) {
+            const int64_t i = b * o.sample_ld + w * 64 + lane;
+            o.sample_lo[i] = elig ? lo : -INFINITY;
+            o.sample_hi[i] = elig ? hi : -INFINITY;
+        } else {
+            const bool take = elig && hi >= Q.tau;
+            const uint64_t mask = __ballot(take);
+            if (mask) {
+                const int leader = __ffsll(static_cast<unsigned long long>(mask)) - 1;
+                int base = 0;
+                if (lane == leader) base = atomicAdd(&o.cand_cnt[b], __popcll(mask));
+                base = __shfl(base, leader, 64);
+                if (take) {
+                    const int64_t pos = base + __popcll(mask & ((1ull << lane) - 1ull));
+                    if (pos < Q.cand_cap) {
+                        const int64_t at = Q.cand_off + pos;
+                        o.cand_row[at] = static_cast<int32_t>(row);
+                        o.cand_lo[at] = lo;
+                        o.cand_hi[at] = hi;
+                    }
+                }
+            }
+        }
+    }
+}
+
+template <int QB>
+static void gemv_pass(const IndexView& ix, const uint64_t* vis, int64_t nblocks,
+                      const int8_t* qcodes, const ScanQ* sq, float gamma, bool sample,
+                      const ScanOut& o, hipStream_t stream) {
+    const int64_t waves = sample ? (nblocks + o.sample_stride - 1) / o.sample_stride : nblocks;
+    const uint32_t grid = static_cast<uint32_t>((waves + 3) / 4);
+    if (sample) {
+        hipLaunchKernelGGL((k_scan_gemv<QB, true>), dim3(grid), dim3(256), 0, stream, ix.codes,
+                           ix.scale, ix.vnorm, ix.enorm, vis, nblocks, ix.nchunk, qcodes, ix.dp,
+                           sq, gamma, o);
+    } else {
+        hipLaunchKernelGGL((k_scan_gemv<QB, false>), dim3(grid), dim3(256), 0, stream, ix.codes,
+                           ix.scale, ix.vnorm, ix.enorm, vis, nblocks, ix.nchunk, qcodes, ix.dp,
+                           sq, gamma, o);
+    }
+}
+
+static ScanOut shift_out(const ScanOut& o, int32_t q0) {
+    ScanOut s = o;
+    if (s.sample_lo) s.sample_lo += q0 * o.sample_ld;
+    if (s.sample_hi) s.sample_hi += q0 * o.sample_ld;
+    if (s.cand_cnt) s.cand_cnt += q0;
+    return s;
+}
+
+void launch_scan(const IndexView& ix, const uint64_t* vis, int64_t nblocks, const int8_t* qcodes,
+                 const ScanQ* sq, int32_t nq, float gamma, bool sample, const ScanOut& o,
+                 hipStream_t stream) {
+    for (int32_t q0 = 0; q0 < nq; q0 += kMaxGemvQueries) {
+        const int qb = (nq - q0 < kMaxGemvQueries) ? (nq - q0) : kMaxGemvQueries;
+        const ScanOut so = shift_out(o, q0);
+        const ScanQ* s = sq + q0;
+#define PVS_GEMV_CASE(N)                                                    \
+    case N:                                                                 \
+        gemv_pass<N>(ix, vis, nblocks, qcodes, s, gamma, sample, so, stream); \
+        break;
+        switch (qb) {
+            PVS_GEMV_CASE(1)
+            PVS_GEMV_CASE(2)
+            PVS_GEMV_CASE(3)
+            PVS_GEMV_CASE(4)
+            PVS_GEMV_CASE(5)
+            PVS_GEMV_CASE(6)
+            PVS_GEMV_CASE(7)
+            PVS_GEMV_CASE(8)
+            default:
+                break;
+        }
+#undef PVS_GEMV_CASE
+    }
+}
+
+// -------------------------------------------------------------- MFMA scan
+// For query batches the code x query product is a dense Int8 contraction:
+// V_MFMA_I32_32X32X32_I8 with the corpus block as A (32 rows x 32 bytes per
+// instruction) and the query codes as B.  Operand layout (lane l, byte j):
+// A[l % 32][16 (l / 32) + j], B[16 (l / 32) + j][l % 32]; accumulator r of lane
+// l holds C[8 (r / 4) + 4 (l / 32) + r % 4][l % 32].  A 16-byte A fragment is
+// therefore 32 consecutive rows of one code chunk: two contiguous 512-byte
+// runs of the chunk-major block layout.
+
+// Query codes of one pass in MFMA B-fragment order:
+// frag[(s * nqt + u) * 64 + lane] = 16 code bytes of query 32 u + lane % 32,
+// bytes 32 s + 16 (lane / 32) .. +15; queries past nq are zero.
+__global__ __launch_bounds__(64) void k_qfrag(const int8_t* __restrict__ qcodes, int32_t dp,
+                                              const ScanQ* __restrict__ sq, int32_t nq, int32_t nqt,
+                                              uint4* __restrict__ frag) {
+    const int lane = threadIdx.x;
+    const int s = blockIdx.x / nqt, u = blockIdx.x % nqt;
+    const int b = 32 * u + (lane & 31);
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (b < nq) {
+        const int64_t off = static_cast<int64_t>(sq[b].qi) * dp + 32 * s + 16 * (lane >> 5);
+        v = *reinterpret_cast<const uint4*>(qcodes + off);
+    }
+    frag[(static_cast<int64_t>(s) * nqt + u) * 64 + lane] = v;
+}
+
+// One wavefront per 64-row block and NQT tiles of 32 queries: 2 x NQT
+// accumulators of 32 x 32.  Epilogue per query tile: lane l owns query
+// 32 u + l % 32 and 32 of the block's rows; the centre-score pre-test skips
+// the exact interval for rows that cannot reach tau; survivors of lanes l and
+// l ^ 32 (same query) reserve their slots with one atomic.
+template <int NQT, bool SAMPLE>
+__global__ __launch_bounds__(256) void k_scan_mfma(
+    const uint4* __restrict__ codes, const float* __restrict__ scale,
+    const float* __restrict__ vnorm, const float* __restrict__ enorm,
+    const uint64_t* __restrict__ vis, int64_t nblocks, int32_t nchunk,
+    const v4i* __restrict__ qfrag, const ScanQ* __restrict__ sq, int32_t nq, float gamma,
+    ScanOut o) {
+    const int lane = threadIdx.x & 63;
+    const int64_t w = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+    const int64_t blk = SAMPLE ? w * o.sample_stride : w;
+    if (blk >= nblocks) return;
+    v16i acc[2][NQT];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int u = 0; u < NQT; ++u) acc[t][u] = v16i{};
+    const uint4* A = codes + blk * nchunk * 64 + (lane >> 5) * 64 + (lane & 31);
+    const int nsteps = nchunk >> 1;
+#pragma unroll 2
+    for (int s = 0; s < nsteps; ++s) {
+        const u32x4 a0 = load_nt(A + 2 * s * 64);
+        const u32x4 a1 = load_nt(A + 2 * s * 64 + 32);
+        v4i va0, va1;
+        __builtin_memcpy(&va0, &a0, 16);
+        __builtin_memcpy(&va1, &a1, 16);
+#pragma unroll
+        for (int u = 0; u < NQT; ++u) {
+            const v4i vb = qfrag[(s * NQT + u) * 64 + lane];
+            acc[0][u] = __builtin_amdgcn_mfma_i32_32x32x32_i8(va0, vb, acc[0][u], 0, 0, 0);
+            acc[1][u] = __builtin_amdgcn_mfma_i32_32x32x32_i8(va1, vb, acc[1][u], 0, 0, 0);
+        }
+    }
+    const uint64_t vbits = vis[blk];
+#pragma unroll
+    for (int u = 0; u < NQT; ++u) {
+        const int b = 32 * u + (lane & 31);
+        const bool valid = b < nq;
+        const ScanQ Q = sq[valid ? b : 0];
+        if (SAMPLE) {
+            if (!valid) continue;
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int rib = 32 * t + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                    const int64_t row = blk * 64 + rib;
+                    float lo, hi;
+                    pair_interval(Q, scale[row], vnorm[row], enorm[row], acc[t][u][r], gamma, lo, hi);
+                    const bool elig = ((vbits >> rib) & 1ull) && (!Q.has_cert || lo <= Q.s_cert);
+                    const int64_t i = b * o.sample_ld + w * 64 + rib;
+                    o.sample_lo[i] = elig ? lo : -INFINITY;
+                    o.sample_hi[i] = elig ? hi : -INFINITY;
+                }
+            }
+            continue;
+        }
+        const float thr = center_threshold(Q);
+        uint32_t mask = 0;
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int rib = 32 * t + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                const int64_t row = blk * 64 + rib;
+                const float sv = scale[row];
+                const float c = (Q.sq * sv) * static_cast<float>(acc[t][u][r]);
+                if (valid && c >= thr && ((vbits >> rib) & 1ull)) {
+                    float lo, hi;
+                    pair_interval(Q, sv, vnorm[row], enorm[row], acc[t][u][r], gamma, lo, hi);
+                    if (hi >= Q.tau && (!Q.has_cert || lo <= Q.s_cert)) mask |= 1u << (16 * t + r);
+                }
+            }
+        }
+        const int mine = __popc(mask);
+        const int other = __shfl_xor(mine, 32, 64);
+        int base = 0;
+        if (lane < 32 && mine + other > 0) base = atomicAdd(&o.cand_cnt[b], mine + other);
+        base = __shfl(base, lane & 31, 64);
+        if (!mask) continue;
+        int64_t pos = base + ((lane >= 32) ? other : 0);
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                if (!((mask >> (16 * t + r)) & 1u)) continue;
+                const int rib = 32 * t + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                const int64_t row = blk * 64 + rib;
+                if (pos < Q.cand_cap) {
+                    float lo, hi;
+                    pair_interval(Q, scale[row], vnorm[row], enorm[row], acc[t][u][r], gamma, lo, hi);
+                    const int64_t at = Q.cand_off + pos;
+                    o.cand_row[at] = static_cast<int32_t>(row);
+                    o.cand_lo[at] = lo;
+                    o.cand_hi[at] = hi;
+                }
+                ++pos;
+            }
+        }
+    }
+}
+
+template <int NQT>
+static void mfma_pass(const IndexView& ix, const uint64_t* vis, int64_t nblocks, const v4i* qfrag,
+                      const ScanQ* sq, int32_t nq, float gamma, bool sample, const ScanOut& o,
+                      hipStream_t stream) {
+    const int64_t waves = sample ? (nblocks + o.sample_stride - 1) / o.sample_stride : nblocks;
+    const uint32_t grid = static_cast<uint32_t>((waves + 3) / 4);
+    if (sample) {
+        hipLaunchKernelGGL((k_scan_mfma<NQT, true>), dim3(grid), dim3(256), 0, stream, ix.codes,
+                           ix.scale, ix.vnorm, ix.enorm, vis, nblocks, ix.nchunk, qfrag, sq, nq,
+                           gamma, o);
+    } else {
+        hipLaunchKernelGGL((k_scan_mfma<NQT, false>), dim3(grid), dim3(256), 0, stream, ix.codes,
+                           ix.scale, ix.vnorm, ix.enorm, vis, nblocks, ix.nchunk, qfrag, sq, nq,
+                           gamma, o);
+    }
+}
+
+int mfma_tiles_for(int32_t nq) {
+    const int t = (nq + 31) / 32;
+    return t <= 1 ? 1 : t <= 2 ? 2 : t <= 4 ? 4 : 8;
+}
+
+void launch_scan_mfma(const IndexView& ix, const uint64_t* vis, int64_t nblocks,
+                      const int8_t* qcodes, const ScanQ* sq, int32_t nq, float gamma, bool sample,
+                      const ScanOut& o, void* frag, hipStream_t stream) {
+    for (int32_t q0 = 0; q0 < nq; q0 += kMaxMfmaQueries) {
+        const int32_t n = (nq - q0 < kMaxMfmaQueries) ? (nq - q0) : kMaxMfmaQueries;
+        const int nqt = mfma_tiles_for(n);
+        const ScanQ* s = sq + q0;
+        hipLaunchKernelGGL(k_qfrag, dim3((ix.dp / 32) * nqt), dim3(64), 0, stream, qcodes, ix.dp, s,
+                           n, nqt, static_cast<uint4*>(frag));
+        const v4i* qf = static_cast<const v4i*>(frag);
+        const ScanOut so = shift_out(o, q0);
+#define PVS_MFMA_CASE(N)                                                          \
+    case N:                                                                       \
+        mfma_pass<N>(ix, vis, nblocks, qf, s, n, gamma, sample, so, stream);      \
+        break;
+        switch (nqt) {
+            PVS_MFMA_CASE(1)
+            PVS_MFMA_CASE(2)
+            PVS_MFMA_CASE(4)
+            PVS_MFMA_CASE(8)
+            default:
+                break;
+        }
+#undef PVS_MFMA_CASE
+    }
+}
+
+// ------------------------------------------------------------ threshold
+// One workgroup per query: tau = the k-th largest finite sampled lower bound
+// (radix select over order-preserving keys, 8 bits per pass), -inf when fewer
+// than k are finite; then sample_hits = sampled pairs with hi >= tau.
+__global__ __launch_bounds__(1024) void k_select(const float* __restrict__ sample_lo,
+                                                 const float* __restrict__ sample_hi, int64_t n,
+                                                 int64_t ld, ScanQ* __restrict__ sq) {
+    __shared__ uint32_t hist[256];
+    __shared__ uint32_t s_digit;
+    __shared__ uint32_t s_rest;
+    __shared__ uint32_t s_total;
+    __shared__ uint32_t s_hits;
+    __shared__ float s_tau;
+    const int b = blockIdx.x;
+    const float* x = sample_lo + b * ld;
+    const float* y = sample_hi + b * ld;
+    uint32_t k = static_cast<uint32_t>(sq[b].k);
+    if (threadIdx.x == 0) {
+        s_total = 0;
+        s_hits = 0;
+    }
+    __syncthreads();
+    uint32_t local = 0;
+    for (int64_t i = threadIdx.x; i < n; i += blockDim.x) local += (x[i] != -INFINITY);
+    atomicAdd(&s_total, local);
+    __syncthreads();
+    const uint32_t total = s_total;
+    if (k == 0 || k > total) {
+        if (threadIdx.x == 0) s_tau = -INFINITY;
+    } else {
+        uint32_t prefix = 0, pmask = 0;
+        for (int pass = 0; pass < 4; ++pass) {
+            const int shift = 24 - 8 * pass;
+            for (int i = threadIdx.x; i < 256; i += blockDim.x) hist[i] = 0;
+            __syncthreads();
+            for (int64_t i = threadIdx.x; i < n; i += blockDim.x) {
+                const float v = x[i];
+                if (v == -INFINITY) continue;
+                const uint32_t key = mono32(v);
+                if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+            }
+            __syncthreads();
+            if (threadIdx.x == 0) {
+                uint32_t cum = 0;
+                int dgt = 255;
+                for (; dgt > 0; --dgt) {
+                    if (cum + hist[dgt] >= k) break;
+                    cum += hist[dgt];
+                }
+                s_digit = static_cast<uint32_t>(dgt);
+                s_rest = k - cum;
+            }
+            __syncthreads();
+            prefix |= s_digit << shift;
+            pmask |= 255u << shift;
+            k = s_rest;
+            __syncthreads();
+        }
+        if (threadIdx.x == 0) s_tau = unmono32(prefix);
+    }
+    __syncthreads();
+    const float tau = s_tau;
+    uint32_t hits = 0;
+    for (int64_t i = threadIdx.x; i < n; i += blockDim.x) hits += (y[i] != -INFINITY && y[i] >= tau);
+    atomicAdd(&s_hits, hits);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        sq[b].tau = tau;
+        sq[b].sample_hits = static_cast<int32_t>(s_hits);
+    }
+}
+
+void launch_select(const float* sample_lo, const float* sample_hi, int64_t n, int64_t ld,
+                   ScanQ* sq, int32_t nq, hipStream_t stream) {
+    if (nq <= 0) return;
+    hipLaunchKernelGGL(k_select, dim3(nq), dim3(1024), 0, stream, sample_lo, sample_hi, n, ld, sq);
+}
+
+}  // namespace pvs
