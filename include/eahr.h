@@ -132,6 +132,9 @@ typedef struct {
     double sort_ms;          /* candidate sort and packing                   */
     int64_t scan_rounds;
     int64_t mfma_launches;   /* scan launches that used the Int8 MFMA kernel */
+    double host_dense_ms;    /* eahr_topk: wall time of its pvs_next calls   */
+    double host_sparse_ms;   /* eahr_topk: wall time of its PBM rounds       */
+    double host_fuse_ms;     /* eahr_topk: wall time of certification        */
 } pvs_profile;
 
 int pvs_profile_enable(int32_t on);   /* also clears the accumulators */

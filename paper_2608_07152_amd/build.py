@@ -42,7 +42,7 @@ def build(verbose: bool = True) -> str:
     hipcc = _hipcc()
     os.makedirs(BUILD_DIR, exist_ok=True)
     common = ["-O3", "-fPIC", "-std=c++17", "-I", INCLUDE, "-I", CSRC, "-ffp-contract=off",
-              "-Wall", "-Wno-unused-function"]
+              "-Wall", "-Wno-unused-function", "-pthread"]
     objs = []
     for src in HIP_SOURCES:
         obj = os.path.join(BUILD_DIR, src + ".o")
@@ -57,7 +57,7 @@ def build(verbose: bool = True) -> str:
               os.path.join(CSRC, src), "-o", obj])
         objs.append(obj)
     tmp = OUT + ".tmp"
-    _run([hipcc, "-shared", f"--offload-arch={ARCH}", "-o", tmp, *objs])
+    _run([hipcc, "-shared", f"--offload-arch={ARCH}", "-pthread", "-o", tmp, *objs])
     os.replace(tmp, OUT)
     return OUT
 

@@ -11,20 +11,24 @@
 // only (L = g_d(r_d), U = L + u_s), seen by the sparse list only.  Inside a
 // single-list group L and U strictly decrease with the rank, so the group's
 // best L and best U belong to its first unfixed member; the both-seen group
-// is kept ordered by (F desc, id asc).  x_dag and the strongest competitor
-// y are therefore among at most six items, and each position is decided as
-// in Sec. 2.2: (L(x_dag), x_dag) must precede (U(y), y) for every other
-// remaining y, and L(x_dag) > B strictly.
+// is a binary heap on (F desc, id asc), whose best two items are the root and
+// the better child.  x_dag and its strongest competitor y are therefore among
+// at most six items, and each position is decided as in Sec. 2.2:
+// (L(x_dag), x_dag) must precede (U(y), y) for every other remaining y, and
+// L(x_dag) > B strictly.
 #include <algorithm>
+#include <atomic>
+#include <chrono>
 #include <cstdint>
 #include <cstring>
 #include <memory>
 #include <new>
-#include <set>
+#include <thread>
 #include <vector>
 
 #include "common.h"
 #include "eahr.h"
+#include "pvs_internal.h"
 
 namespace {
 
@@ -72,7 +76,7 @@ struct ItemMap {
     size_t used = 0;
     ItemMap() { slots.assign(64, Slot{-1, {0, 0}, 0}); }
     static size_t hash(int64_t id) {
-        uint64_t x = static_cast<uint64_t>(id) * 0x9E3779B97F4A7C15ull;
+        const uint64_t x = static_cast<uint64_t>(id) * 0x9E3779B97F4A7C15ull;
         return static_cast<size_t>(x ^ (x >> 29));
     }
     Slot* find(int64_t id) {
@@ -94,6 +98,11 @@ struct ItemMap {
             }
         }
     }
+    void reserve(size_t n) {
+        size_t want = 64;
+        while (want < 2 * n + 2) want *= 2;
+        if (want > slots.size()) rehash(want);
+    }
     void rehash(size_t n) {
         std::vector<Slot> old;
         old.swap(slots);
@@ -110,12 +119,13 @@ struct ItemMap {
     }
 };
 
-struct BothOrder {   // (F desc, id asc)
-    bool operator()(const std::pair<Frac, int64_t>& a, const std::pair<Frac, int64_t>& b) const {
-        const int c = cmp(a.first, b.first);
-        if (c != 0) return c > 0;
-        return a.second < b.second;
-    }
+struct Scored {
+    Frac F;
+    int64_t id;
+};
+// heap order: a below b when b precedes a
+struct HeapLess {
+    bool operator()(const Scored& a, const Scored& b) const { return precedes(b.F, b.id, a.F, a.id); }
 };
 
 struct Fusion {
@@ -124,21 +134,22 @@ struct Fusion {
     bool open[2] = {true, true};
     int64_t cursor[2] = {0, 0};     // first possibly single-list unfixed item
     ItemMap items;
-    std::set<std::pair<Frac, int64_t>, BothOrder> both;
+    std::vector<Scored> both;       // binary heap of unfixed both-seen items
     std::vector<int64_t> A;
     bool resolved = false;
 
-    Frac F_both(const ItemMap::Slot* s) const {
-        return add(g(*P, 0, s->rank[0]), g(*P, 1, s->rank[1]));
-    }
-
-    void append(int i, const int64_t* ids, int32_t n) {
-        for (int32_t j = 0; j < n; ++j) {
+    void append(int i, const int64_t* ids, int64_t n) {
+        items.reserve(items.used + static_cast<size_t>(n));
+        list[i].reserve(list[i].size() + static_cast<size_t>(n));
+        for (int64_t j = 0; j < n; ++j) {
             const int64_t x = ids[j];
             list[i].push_back(x);
             ItemMap::Slot* s = items.get(x);
             s->rank[i] = static_cast<int32_t>(list[i].size());
-            if (!s->fixed && s->rank[1 - i] > 0) both.insert({F_both(s), x});
+            if (!s->fixed && s->rank[1 - i] > 0) {
+                both.push_back(Scored{add(g(*P, 0, s->rank[0]), g(*P, 1, s->rank[1])), x});
+                std::push_heap(both.begin(), both.end(), HeapLess());
+            }
         }
     }
 
@@ -168,12 +179,8 @@ struct Fusion {
             };
             Cand c[3];
             int nc = 0;
-            if (!both.empty()) {
-                const auto& top = *both.begin();
-                c[nc++] = Cand{top.second, top.first, top.first, 0, -1};
-            }
+            if (!both.empty()) c[nc++] = Cand{both[0].id, both[0].F, both[0].F, 0, -1};
             for (int i = 0; i < 2; ++i) {
-                cursor[i] = std::max<int64_t>(cursor[i], 0);
                 const int64_t p = single_from(i, cursor[i]);
                 if (p >= 0) {
                     cursor[i] = p;
@@ -196,9 +203,11 @@ struct Fusion {
                     continue;
                 }
                 if (X.kind == 0) {
-                    auto it = both.begin();
-                    ++it;
-                    if (it != both.end()) ok = precedes(X.L, X.id, it->first, it->second);
+                    const size_t n = both.size();
+                    int64_t second = -1;
+                    if (n > 1) second = 1;
+                    if (n > 2 && HeapLess()(both[1], both[2])) second = 2;
+                    if (second >= 0) ok = precedes(X.L, X.id, both[second].F, both[second].id);
                 } else {
                     const int i = X.kind - 1;
                     const int64_t p = single_from(i, X.pos + 1);
@@ -210,9 +219,11 @@ struct Fusion {
             }
             if (!ok) break;
             A.push_back(X.id);
-            ItemMap::Slot* s = items.find(X.id);
-            s->fixed = 1;
-            if (X.kind == 0) both.erase(both.begin());
+            items.find(X.id)->fixed = 1;
+            if (X.kind == 0) {
+                std::pop_heap(both.begin(), both.end(), HeapLess());
+                both.pop_back();
+            }
         }
         if (static_cast<int64_t>(A.size()) >= P->K) {
             resolved = true;
@@ -220,6 +231,56 @@ struct Fusion {
                    single_from(1, cursor[1]) < 0) {
             resolved = true;   // nothing unseen or remaining can score: q_K = |A|
         }
+    }
+};
+
+int check_params(const eahr_params& ep) {
+    if (ep.K < 0 || ep.depth0 < 1 || ep.growth < 2 || ep.k_rrf < 1 || ep.k_rrf > (1 << 20) ||
+        ep.w_dense < 0 || ep.w_dense > 1024 || ep.w_sparse < 0 || ep.w_sparse > 1024)
+        EAHR_FAIL(EAHR_E_INVALID, "eahr: parameters out of range");
+    return EAHR_OK;
+}
+
+int host_threads() {
+    unsigned n = std::thread::hardware_concurrency();
+    if (n == 0) n = 1;
+    return static_cast<int>(std::min(n, 16u));
+}
+
+// f(i) for i in [0, n) on up to `threads` threads (the caller is one of them).
+template <typename F>
+void parallel_for(int64_t n, int threads, F&& f) {
+    if (n <= 0) return;
+    if (threads <= 1 || n == 1) {
+        for (int64_t i = 0; i < n; ++i) f(i);
+        return;
+    }
+    std::atomic<int64_t> next{0};
+    auto work = [&]() {
+        for (int64_t i = next.fetch_add(1); i < n; i = next.fetch_add(1)) f(i);
+    };
+    const int extra = static_cast<int>(std::min<int64_t>(threads, n)) - 1;
+    std::vector<std::thread> pool;
+    pool.reserve(extra);
+    for (int t = 0; t < extra; ++t) pool.emplace_back(work);
+    work();
+    for (auto& t : pool) t.join();
+}
+
+double ms_since(std::chrono::steady_clock::time_point t0) {
+    return std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+}
+
+template <typename T>
+struct RawBuf {   // uninitialised growable host buffer
+    std::unique_ptr<T[]> p;
+    size_t n = 0;
+    T* get(size_t want) {
+        if (want > n) {
+            p.reset(new T[want]);
+            n = want;
+        }
+        return p.get();
     }
 };
 
@@ -233,13 +294,14 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
     if (!params || B <= 0 || !out_ids || !out_count || !out_status)
         EAHR_FAIL(EAHR_E_INVALID, "eahr_topk: bad arguments");
     const eahr_params& ep = *params;
-    if (ep.K < 0 || ep.depth0 < 1 || ep.growth < 2 || ep.k_rrf < 1 || ep.k_rrf > (1 << 20) ||
-        ep.w_dense < 0 || ep.w_dense > 1024 || ep.w_sparse < 0 || ep.w_sparse > 1024)
-        EAHR_FAIL(EAHR_E_INVALID, "eahr_topk: parameters out of range");
+    EAHR_TRY(check_params(ep));
     const bool use_dense = ep.w_dense > 0, use_sparse = ep.w_sparse > 0;
     if (use_dense && (!dense || !q_dense)) EAHR_FAIL(EAHR_E_INVALID, "eahr_topk: dense channel missing");
     if (use_sparse && (!sparse || !q_sparse)) EAHR_FAIL(EAHR_E_INVALID, "eahr_topk: sparse channel missing");
-    Params P{ep.K, ep.k_rrf, {ep.w_dense, ep.w_sparse}};
+    const Params P{ep.K, ep.k_rrf, {ep.w_dense, ep.w_sparse}};
+    const int threads = host_threads();
+    const bool prof = pvs_profile_on();
+    double t_dense = 0, t_sparse = 0, t_fuse = 0;
 
     std::vector<Fusion> F(B);
     std::vector<int32_t> dstat(B, EAHR_LIST_EXHAUSTED), sstat(B, EAHR_LIST_EXHAUSTED);
@@ -251,6 +313,7 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
         F[b].open[1] = use_sparse;
         if (use_dense) dstat[b] = EAHR_LIST_OPEN;
         if (use_sparse) sstat[b] = EAHR_LIST_OPEN;
+        if (ep.K == 0) F[b].resolved = true;
     }
     struct Cleanup {
         pvs_state* st = nullptr;
@@ -266,76 +329,98 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
         cl.sp.assign(B, nullptr);
         for (int32_t b = 0; b < B; ++b) EAHR_TRY(pbm_open(sparse, &q_sparse[b], &cl.sp[b]));
     }
-    if (ep.K == 0) {
-        for (int32_t b = 0; b < B; ++b) F[b].resolved = true;
-    }
-    std::vector<int64_t> ids;
-    std::vector<float> scores;
-    std::vector<int32_t> cnt(B), sts(B);
-    std::vector<uint8_t> active(B);
+    RawBuf<int64_t> dids;
+    RawBuf<float> dscores;
+    std::vector<int32_t> dcnt(B, 0), dsts(B);
+    std::vector<uint8_t> dact(B, 0);
+    std::vector<std::vector<int64_t>> sids(B);
+    std::vector<std::vector<float>> sscores(B);
+    std::vector<int32_t> scnt(B, 0), ssts(B, EAHR_LIST_OPEN);
+    std::vector<uint8_t> sact(B, 0);
+    std::vector<int> sparse_rc(B, EAHR_OK);
     int64_t depth = ep.depth0;
     for (;;) {
         bool any = false;
         for (int32_t b = 0; b < B; ++b) any |= !F[b].resolved && !failed[b];
         if (!any) break;
-        // dense channel: one batched call for every query still needing ranks
-        if (use_dense) {
-            int64_t m = 0;
-            for (int32_t b = 0; b < B; ++b) {
-                active[b] = !F[b].resolved && !failed[b] && F[b].open[0] &&
-                            static_cast<int64_t>(F[b].list[0].size()) < depth;
-                if (active[b]) m = std::max<int64_t>(m, depth - static_cast<int64_t>(F[b].list[0].size()));
-            }
-            if (m > 0) {
-                if (m > (1LL << 30)) m = 1LL << 30;
-                ids.resize(static_cast<size_t>(B) * m);
-                scores.resize(static_cast<size_t>(B) * m);
-                EAHR_TRY(pvs_next(cl.st, static_cast<int32_t>(m), active.data(), ids.data(),
-                                  scores.data(), cnt.data(), sts.data()));
-                for (int32_t b = 0; b < B; ++b) {
-                    if (!active[b]) continue;
-                    if (sts[b] == EAHR_LIST_FAILED) {
-                        failed[b] = 1;
-                        dstat[b] = EAHR_LIST_FAILED;
-                        continue;
-                    }
-                    F[b].append(0, ids.data() + static_cast<size_t>(b) * m, cnt[b]);
-                    if (sts[b] == EAHR_LIST_EXHAUSTED) {
-                        F[b].open[0] = false;
-                        dstat[b] = EAHR_LIST_EXHAUSTED;
-                    }
+        // requests of this round: every Open list of an unresolved query to `depth`
+        int64_t m = 0;
+        for (int32_t b = 0; b < B; ++b) {
+            const bool live = !F[b].resolved && !failed[b];
+            dact[b] = live && use_dense && F[b].open[0] &&
+                      static_cast<int64_t>(F[b].list[0].size()) < depth;
+            sact[b] = live && use_sparse && F[b].open[1] &&
+                      static_cast<int64_t>(F[b].list[1].size()) < depth;
+            dcnt[b] = 0;
+            scnt[b] = 0;
+            if (dact[b]) m = std::max<int64_t>(m, depth - static_cast<int64_t>(F[b].list[0].size()));
+        }
+        if (m > (1LL << 30)) m = 1LL << 30;
+        // sparse channel on worker threads while the dense channel runs on the GPU
+        std::thread sparse_thread;
+        auto t_round = std::chrono::steady_clock::now();
+        auto sparse_work = [&]() {
+            const auto t0 = std::chrono::steady_clock::now();
+            parallel_for(B, std::max(1, threads - 1), [&](int64_t b) {
+                if (!sact[b]) return;
+                const int64_t need = std::min<int64_t>(depth - static_cast<int64_t>(F[b].list[1].size()), 1LL << 30);
+                sids[b].resize(static_cast<size_t>(need));
+                sscores[b].resize(static_cast<size_t>(need));
+                sparse_rc[b] = pbm_next(cl.sp[b], static_cast<int32_t>(need), sids[b].data(),
+                                        sscores[b].data(), &scnt[b], &ssts[b]);
+            });
+            t_sparse += ms_since(t0);
+        };
+        bool any_sparse = false;
+        for (int32_t b = 0; b < B; ++b) any_sparse |= sact[b] != 0;
+        if (any_sparse) sparse_thread = std::thread(sparse_work);
+        int dense_rc = EAHR_OK;
+        if (m > 0) {
+            const auto t0 = std::chrono::steady_clock::now();
+            int64_t* ids = dids.get(static_cast<size_t>(B) * m);
+            float* sc = dscores.get(static_cast<size_t>(B) * m);
+            dense_rc = pvs_next(cl.st, static_cast<int32_t>(m), dact.data(), ids, sc, dcnt.data(), dsts.data());
+            t_dense += ms_since(t0);
+        }
+        if (sparse_thread.joinable()) sparse_thread.join();
+        (void)t_round;
+        EAHR_TRY(dense_rc);
+        for (int32_t b = 0; b < B; ++b) EAHR_TRY(sparse_rc[b]);
+        // merge this round's ranks and certify, one query per task
+        const auto t0 = std::chrono::steady_clock::now();
+        parallel_for(B, threads, [&](int64_t b) {
+            if (F[b].resolved || failed[b]) return;
+            if (dact[b]) {
+                if (dsts[b] == EAHR_LIST_FAILED) {
+                    failed[b] = 1;
+                    dstat[b] = EAHR_LIST_FAILED;
+                    return;
+                }
+                F[b].append(0, dids.p.get() + static_cast<size_t>(b) * m, dcnt[b]);
+                if (dsts[b] == EAHR_LIST_EXHAUSTED) {
+                    F[b].open[0] = false;
+                    dstat[b] = EAHR_LIST_EXHAUSTED;
                 }
             }
-        }
-        if (use_sparse) {
-            for (int32_t b = 0; b < B; ++b) {
-                if (F[b].resolved || failed[b] || !F[b].open[1]) continue;
-                const int64_t need = depth - static_cast<int64_t>(F[b].list[1].size());
-                if (need <= 0) continue;
-                const int32_t m = static_cast<int32_t>(std::min<int64_t>(need, 1LL << 30));
-                ids.resize(m);
-                scores.resize(m);
-                int32_t c = 0, s = 0;
-                EAHR_TRY(pbm_next(cl.sp[b], m, ids.data(), scores.data(), &c, &s));
-                if (s == EAHR_LIST_FAILED) {
+            if (sact[b]) {
+                if (ssts[b] == EAHR_LIST_FAILED) {
                     failed[b] = 1;
                     sstat[b] = EAHR_LIST_FAILED;
-                    continue;
+                    return;
                 }
-                F[b].append(1, ids.data(), c);
-                if (s == EAHR_LIST_EXHAUSTED) {
+                F[b].append(1, sids[b].data(), scnt[b]);
+                if (ssts[b] == EAHR_LIST_EXHAUSTED) {
                     F[b].open[1] = false;
                     sstat[b] = EAHR_LIST_EXHAUSTED;
                 }
             }
-        }
-        for (int32_t b = 0; b < B; ++b) {
-            if (F[b].resolved || failed[b]) continue;
             rounds[b] += 1;
             F[b].certify();
-        }
+        });
+        t_fuse += ms_since(t0);
         depth = (depth > (INT64_MAX / ep.growth)) ? INT64_MAX : depth * ep.growth;
     }
+    if (prof) pvs_profile_add_host(t_dense, t_sparse, t_fuse);
     bool any_failed = false;
     for (int32_t b = 0; b < B; ++b) {
         const auto& f = F[b];
@@ -367,19 +452,14 @@ extern "C" int eahr_fuse_lists(const int64_t* list_d, int64_t n_d, const int64_t
         (n_d > 0 && !list_d) || (n_s > 0 && !list_s))
         EAHR_FAIL(EAHR_E_INVALID, "eahr_fuse_lists: bad arguments");
     const eahr_params& ep = *params;
-    if (ep.K < 0 || ep.depth0 < 1 || ep.growth < 2 || ep.k_rrf < 1 || ep.k_rrf > (1 << 20) ||
-        ep.w_dense < 0 || ep.w_dense > 1024 || ep.w_sparse < 0 || ep.w_sparse > 1024)
-        EAHR_FAIL(EAHR_E_INVALID, "eahr_fuse_lists: parameters out of range");
+    EAHR_TRY(check_params(ep));
     if (n_d >= (1LL << 31) || n_s >= (1LL << 31)) EAHR_FAIL(EAHR_E_RANGE, "eahr_fuse_lists: lists too long");
-    Params P{ep.K, ep.k_rrf, {ep.w_dense, ep.w_sparse}};
+    const Params P{ep.K, ep.k_rrf, {ep.w_dense, ep.w_sparse}};
     Fusion f;
     f.P = &P;
     const int64_t* lists[2] = {list_d, list_s};
     const int64_t lens[2] = {n_d, n_s};
-    for (int i = 0; i < 2; ++i) {
-        f.open[i] = P.w[i] > 0;
-        if (f.open[i] && lens[i] == 0) f.open[i] = false;
-    }
+    for (int i = 0; i < 2; ++i) f.open[i] = P.w[i] > 0 && lens[i] > 0;
     if (ep.K == 0) f.resolved = true;
     int32_t rounds = 0;
     int64_t depth = step > 0 ? step : ep.depth0;
@@ -388,7 +468,7 @@ extern "C" int eahr_fuse_lists(const int64_t* list_d, int64_t n_d, const int64_t
             if (!f.open[i]) continue;
             const int64_t have = static_cast<int64_t>(f.list[i].size());
             const int64_t upto = std::min(depth, lens[i]);
-            if (upto > have) f.append(i, lists[i] + have, static_cast<int32_t>(upto - have));
+            if (upto > have) f.append(i, lists[i] + have, upto - have);
             if (static_cast<int64_t>(f.list[i].size()) == lens[i]) f.open[i] = false;
         }
         rounds += 1;

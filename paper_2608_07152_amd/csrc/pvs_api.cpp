@@ -867,3 +867,12 @@ extern "C" int pvs_profile_read(pvs_profile* out) {
     *out = g_prof;
     return EAHR_OK;
 }
+
+bool pvs_profile_on() { return g_prof_on.load(std::memory_order_relaxed) != 0; }
+
+void pvs_profile_add_host(double dense_ms, double sparse_ms, double fuse_ms) {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    g_prof.host_dense_ms += dense_ms;
+    g_prof.host_sparse_ms += sparse_ms;
+    g_prof.host_fuse_ms += fuse_ms;
+}

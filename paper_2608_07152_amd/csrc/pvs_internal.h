@@ -41,6 +41,10 @@ constexpr int32_t kMfmaMinQueries = 4;
 enum class ScanPath { Auto, Gemv, Mfma };
 }  // namespace pvs
 
+// Process-wide profile hooks used by the host fusion (pvs_profile_enable).
+bool pvs_profile_on();
+void pvs_profile_add_host(double dense_ms, double sparse_ms, double fuse_ms);
+
 struct pvs_index {
     struct Snapshot {
         int64_t rows = 0;      // physical rows visible to the epoch (prefix)

@@ -72,7 +72,8 @@ class pvs_profile(C.Structure):
     _fields_ = [("scan_ms", C.c_double), ("scan_launches", C.c_int64), ("scan_bytes", C.c_int64),
                 ("sample_ms", C.c_double), ("rescore_ms", C.c_double), ("rescore_rows", C.c_int64),
                 ("sort_ms", C.c_double), ("scan_rounds", C.c_int64),
-                ("mfma_launches", C.c_int64)]
+                ("mfma_launches", C.c_int64), ("host_dense_ms", C.c_double),
+                ("host_sparse_ms", C.c_double), ("host_fuse_ms", C.c_double)]
 
     def as_dict(self):
         return {f: getattr(self, f) for f, _ in self._fields_}
