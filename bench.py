@@ -6,18 +6,22 @@ clustered vectors of d = 768 (4,096 centres, std 0.5) with a BM25 sparse
 channel (vocab 30,000, Poisson(60) documents, Zipf(1.1) + topic mix), K = 20,
 RRF k = 60, weights 1:1.  All inputs are seeded synthetic data; the index
 (int8 codes, scales, norms, float32 rows) and the queries are resident in HBM
-before the timed region.
+before a timed region starts.
 
-One step = one eahr_topk call on a batch of --batch queries: the PVS dense
-channel on the GPU (scan, threshold selection, rescoring, sort, certification)
+One step = one eahr_topk call on a batch of queries: the PVS dense channel on
+the GPU (threshold sampling, interval scan, rescoring, sort, certification)
 plus PBM and weighted-RRF certification on the host, with depth doubling from
-20 until the ordered Top-20 is fixed.
+20 until the ordered Top-20 is fixed.  The headline is the batch of 256
+queries (value = queries/s); batches of 1 (distinct queries of the 200-query
+single-request set, one per step) and 64 are timed in the same run and
+reported under ``per_batch``.
 
-Prints one JSON line.  ``roofline`` is for the dominant kernel, the full
-interval scan: algorithmic bytes per launch, N (d + 12) + N/8, divided by its
-average launch time measured with HIP events on the library's stream.
+``roofline`` is for the dominant kernel, the full interval scan of the
+headline batch: algorithmic bytes per launch, N (d + 12) + 8 N / 64, divided by
+its average launch time measured with HIP events on the library's stream.
 ``cpu_baseline`` times the CPU oracle (exhaustive float64 dense ranking, brute
-force sparse ranking, exact complete-list RRF) on a few queries of the batch.
+force sparse ranking, exact complete-list RRF) on a few queries of the
+headline batch and checks their Top-20.
 """
 from __future__ import annotations
 
@@ -45,13 +49,13 @@ def parse():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="passage")
-    ap.add_argument("--batch", type=int, default=64, help="queries per eahr_topk call")
+    ap.add_argument("--batch", type=int, default=256, help="queries per eahr_topk call (headline)")
+    ap.add_argument("--extra", default="1:20,64:3", help="extra batch:steps configurations")
     ap.add_argument("--n", type=int, default=None, help="override corpus rows (quick runs only)")
     ap.add_argument("--weights", default="1:1")
     ap.add_argument("--range-size", type=int, default=4096)
     ap.add_argument("--cpu-queries", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--scan-only", action="store_true", help="time pvs_next(20) instead of eahr_topk")
     return ap.parse_args()
 
 
@@ -79,6 +83,12 @@ def cpu_baseline(x, post, q, qs, K, wts, n_queries):
     return out, el, blas
 
 
+def query_set_for(w, batch):
+    if w.name != "passage":
+        return "default"
+    return {64: "b64", 256: "b256"}.get(batch, "single")
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -101,75 +111,102 @@ def main():
     log(f"workload {w.name}: n={w.n} d={w.d} centers={w.centers}")
     x, lab = datagen.corpus(w)
     log("dense corpus generated")
-    qset = {64: "b64", 256: "b256"}.get(args.batch, "single")
-    if args.workload != "passage":
-        qset = "default"
-    q, qlab = datagen.queries(w, qset, count=args.batch)
-    off = datagen.query_set_offset(w, qset)
+    configs = [(args.batch, args.steps, args.warmup)]
+    for item in filter(None, args.extra.split(",")):
+        bsz, st = (int(v) for v in item.split(":"))
+        configs.append((bsz, st, 1))
+    qsets = {}
+    for bsz, steps, _ in configs:
+        name = query_set_for(w, bsz)
+        if name not in qsets:
+            cnt = datagen.QUERY_SETS[w.name][name][1]
+            qsets[name] = datagen.queries(w, name, count=max(cnt, bsz))
     if w.adversarial:
-        post, qs = datagen.adversarial_postings(w, x, q)
+        post = None
     else:
         docs = datagen.sparse_docs(w, lab)
         log(f"sparse documents generated: {len(docs.doc)} postings")
         post = datagen.bm25_impacts(w, docs)
         del docs
-        qs = datagen.sparse_queries(w, qlab, off)
+    sparse_q = {}
+    for name, (q, qlab) in qsets.items():
+        if w.adversarial:
+            post_a, sq = datagen.adversarial_postings(w, x, q)
+            post = post_a
+        else:
+            sq = datagen.sparse_queries(w, qlab, datagen.query_set_offset(w, name))
+        sparse_q[name] = sq
     log("sparse impacts computed")
-
     idx = eahr.pvs_build(x)
     torch.cuda.synchronize()
     log("pvs index built")
     pbm = eahr.pbm_build(post.term_ptr, post.doc, post.impact, w.n, args.range_size)
     log("pbm index built")
-    qd = torch.from_numpy(q).cuda()
+    qdev = {name: torch.from_numpy(q).cuda() for name, (q, _) in qsets.items()}
     torch.cuda.synchronize()
 
-    def step():
-        if args.scan_only:
-            st = eahr.pvs_open(idx, qd)
-            eahr.pvs_next(st, K)
-            st.close()
-            return None
-        return eahr.eahr_topk(idx, pbm, qd, qs, K=K, w_dense=wts[0], w_sparse=wts[1])
+    def run_config(bsz, steps, warmup):
+        name = query_set_for(w, bsz)
+        qd, qs = qdev[name], sparse_q[name]
+        pool = qd.shape[0]
 
-    for i in range(args.warmup):
-        step()
-        log(f"warmup step {i + 1}/{args.warmup} done")
-    eahr.pvs_profile_enable(True)
-    torch.cuda.synchronize()
-    t = time.perf_counter()
-    res = None
-    for i in range(args.steps):
-        res = step()
-    torch.cuda.synchronize()
-    el = time.perf_counter() - t
-    prof = eahr.pvs_profile_read()
-    eahr.pvs_profile_enable(False)
-    log(f"timed {args.steps} steps in {el:.3f}s")
+        def batch_at(i):
+            s = (i * bsz) % pool
+            if s + bsz > pool:
+                s = 0
+            return qd[s:s + bsz], qs[s:s + bsz]
 
-    qps = args.steps * args.batch / el
-    launches = max(1, prof["scan_launches"])
-    avg_ms = prof["scan_ms"] / launches
-    bytes_per_launch = prof["scan_bytes"] / launches
-    achieved = bytes_per_launch / (avg_ms * 1e-3) / 1e9 if avg_ms > 0 else 0.0
-    depth = {}
-    if res is not None:
-        ids, cnt, stt, stats = res
-        depth = {
-            "dense_depth_mean": float(np.mean([s["dense_depth"] for s in stats])),
-            "dense_depth_max": int(max(s["dense_depth"] for s in stats)),
+        for i in range(warmup):
+            a, b = batch_at(i)
+            eahr.eahr_topk(idx, pbm, a, b, K=K, w_dense=wts[0], w_sparse=wts[1])
+        eahr.pvs_profile_enable(True)
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        res = []
+        for i in range(steps):
+            a, b = batch_at(warmup + i)
+            res.append(eahr.eahr_topk(idx, pbm, a, b, K=K, w_dense=wts[0], w_sparse=wts[1]))
+        torch.cuda.synchronize()
+        el = time.perf_counter() - t
+        prof = eahr.pvs_profile_read()
+        eahr.pvs_profile_enable(False)
+        launches = max(1, prof["scan_launches"])
+        avg_ms = prof["scan_ms"] / launches
+        bpl = prof["scan_bytes"] / launches
+        achieved = bpl / (avg_ms * 1e-3) / 1e9 if avg_ms > 0 else 0.0
+        stats = [s for r in res for s in r[3]]
+        dd = np.array([s["dense_depth"] for s in stats])
+        out = {
+            "batch": bsz, "steps": steps, "queries_per_s": steps * bsz / el,
+            "ms_per_step": el / steps * 1e3,
+            "scan_kernel": "k_scan_mfma" if prof["mfma_launches"] else "k_scan_gemv",
+            "scan_gbs": achieved, "scan_frac": achieved / HBM_PEAK_GBS, "scan_avg_launch_ms": avg_ms,
+            "scan_launches": prof["scan_launches"], "scan_bytes_per_launch": bpl,
+            "kernel_ms": {"scan": prof["scan_ms"], "sample_select": prof["sample_ms"],
+                          "rescore": prof["rescore_ms"], "sort_pack": prof["sort_ms"]},
+            "rescored_rows": prof["rescore_rows"],
+            "host_ms": {"dense_calls": prof["host_dense_ms"], "sparse_rounds": prof["host_sparse_ms"],
+                        "certify": prof["host_fuse_ms"]},
+            "dense_depth": {"mean": float(dd.mean()), "median": float(np.median(dd)), "max": int(dd.max())},
             "sparse_depth_mean": float(np.mean([s["sparse_depth"] for s in stats])),
-            "rounds_mean": float(np.mean([s["rounds"] for s in stats])),
-            "failed": int(np.sum(stt != 0)),
+            "failed": int(sum(int(np.sum(r[2] != 0)) for r in res)),
         }
+        log(f"batch {bsz}: {out['queries_per_s']:.1f} q/s, scan {achieved:.0f} GB/s")
+        return out, res
+
+    head, head_res = run_config(*configs[0])
+    per_batch = [head]
+    for cfg in configs[1:]:
+        per_batch.append(run_config(*cfg)[0])
+
     line = {
         "metric": "exact Top-20 EAHR queries/s at 8.8Mx768 (PVS scan HBM GB/s in roofline)",
-        "value": qps,
+        "value": head["queries_per_s"],
         "unit": "queries/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": el / args.steps * 1e3,
+        "ms_per_step": head["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -178,27 +215,27 @@ def main():
         "config": {"workload": f"{w.name} N={w.n} d={w.d} batch={args.batch} K={K} k=60 "
                                f"weights={wts[0]}:{wts[1]}",
                    "global_batch": args.batch, "parallelism": "single GPU"},
-        "roofline": {"bound": "hbm", "kernel": "k_scan_gemv (full interval scan)",
-                     "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
-                     "avg_launch_ms": avg_ms, "launches": prof["scan_launches"],
-                     "bytes_per_launch": bytes_per_launch},
-        "breakdown_ms": {"scan": prof["scan_ms"], "sample_select": prof["sample_ms"],
-                         "rescore": prof["rescore_ms"], "sort_pack": prof["sort_ms"],
-                         "rescored_rows": prof["rescore_rows"], "scan_rounds": prof["scan_rounds"]},
-        "eahr": depth,
+        "roofline": {"bound": "hbm", "kernel": head["scan_kernel"], "achieved": head["scan_gbs"],
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": head["scan_frac"],
+                     "traffic": None, "avg_launch_ms": head["scan_avg_launch_ms"],
+                     "launches": head["scan_launches"],
+                     "bytes_per_launch": head["scan_bytes_per_launch"]},
+        "per_batch": per_batch,
     }
-    if not args.no_cpu_baseline and res is not None:
-        nqc = min(args.cpu_queries, args.batch)
+    if not args.no_cpu_baseline:
+        bsz = configs[0][0]
+        name = query_set_for(w, bsz)
+        q = qsets[name][0]
+        qs = sparse_q[name]
+        nqc = min(args.cpu_queries, bsz)
         log(f"cpu oracle on {nqc} queries")
         want, cel, cores = cpu_baseline(x, post, q, qs, K, wts, nqc)
-        ids, cnt, _, _ = res
+        ids, cnt, _, _ = head_res[0]
         match = sum(list(ids[b, :cnt[b]]) == want[b] for b in range(nqc))
         line["cpu_baseline"] = {"value": nqc / cel, "unit": "queries/s", "cores": cores,
                                 "kind": "oracle",
-                                "sample": f"{nqc} queries of the batch over the full corpus "
-                                          f"(exhaustive fp64 dense sort, brute-force sparse, "
-                                          f"exact RRF)"}
+                                "sample": f"{nqc} queries of the headline batch over the full corpus "
+                                          f"(exhaustive fp64 dense sort, brute-force sparse, exact RRF)"}
         line["oracle_check"] = {"queries": nqc, "top20_equal": int(match)}
         log(f"cpu oracle {cel:.1f}s, {match}/{nqc} Top-20 equal")
     print(json.dumps(line), flush=True)

@@ -24,6 +24,7 @@
 
 #include "common.h"
 #include "eahr.h"
+#include "host_parallel.h"
 #include "pvs_internal.h"
 #include "pvs_kernels.h"
 
@@ -763,6 +764,29 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
         g_prof.scan_rounds += 1;
     }
 
+    // decode the certified keys of every query into its cache (in parallel)
+    std::vector<int64_t> old_size(nq, 0);
+    std::vector<uint8_t> usable(nq, 0);
+    for (int32_t i = 0; i < nq; ++i) {
+        auto& Q = st->q[todo[i]];
+        usable[i] = !h_fail[i] && cand[i] <= st->h_scanq[i].cand_cap;
+        old_size[i] = static_cast<int64_t>(Q.cache_id.size());
+        if (usable[i]) {
+            Q.cache_id.resize(old_size[i] + h_cert[i]);
+            Q.cache_score.resize(old_size[i] + h_cert[i]);
+        }
+    }
+    eahr::parallel_for(nq, eahr::host_threads(), [&](int64_t i) {
+        if (!usable[i]) return;
+        auto& Q = st->q[todo[i]];
+        const uint64_t* kp = st->h_packed + h_offs[i];
+        int32_t* id = Q.cache_id.data() + old_size[i];
+        float* sc = Q.cache_score.data() + old_size[i];
+        for (int64_t j = 0; j < h_cert[i]; ++j) {
+            id[j] = static_cast<int32_t>(kp[j] & 0xffffffffu);
+            sc[j] = key_score(kp[j]);
+        }
+    });
     std::vector<int32_t> keep;
     for (int32_t i = 0; i < nq; ++i) {
         const int32_t b = todo[i];
@@ -779,13 +803,6 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
         Q.cap_hint = 0;
         st->stats.candidates += cand[i];
         const int64_t c = h_cert[i];
-        const uint64_t* kp = st->h_packed + h_offs[i];
-        Q.cache_id.reserve(Q.cache_id.size() + c);
-        Q.cache_score.reserve(Q.cache_score.size() + c);
-        for (int64_t j = 0; j < c; ++j) {
-            Q.cache_id.push_back(static_cast<int32_t>(kp[j] & 0xffffffffu));
-            Q.cache_score.push_back(key_score(kp[j]));
-        }
         st->stats.certified += c;
         if (c > 0) {
             Q.has_cert = true;
