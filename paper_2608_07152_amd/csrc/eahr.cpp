@@ -1,21 +1,8 @@
-// Exact adaptive weighted-RRF fusion of the dense (PVS) and sparse (PBM)
-// channels (Sec. 2.1, Sec. 2.2).
-//
-// g_i(r) = 1 / (r / w_i + k - 1) = w_i / (r + w_i (k - 1)) with integer k and
-// w_i, so every bound is a sum of at most two unit terms w / D and compares
-// exactly as a fraction (numerators < 2^43, denominators < 2^64, products
-// < 2^107 in unsigned 128-bit integers).
-//
-// Certification: after every depth round the remaining observed items fall
-// into three groups: seen by both lists (L = U = F), seen by the dense list
-// only (L = g_d(r_d), U = L + u_s), seen by the sparse list only.  Inside a
-// single-list group L and U strictly decrease with the rank, so the group's
-// best L and best U belong to its first unfixed member; the both-seen group
-// is a binary heap on (F desc, id asc), whose best two items are the root and
-// the better child.  x_dag and its strongest competitor y are therefore among
-// at most six items, and each position is decided as in Sec. 2.2:
-// (L(x_dag), x_dag) must precede (U(y), y) for every other remaining y, and
-// L(x_dag) > B strictly.
+// eahr_topk and eahr_fuse_lists: the depth-round driver of exact adaptive
+// weighted-RRF fusion (Sec. 2.1, 2.2).  Every Open list with positive weight
+// advances to cumulative depth depth0 * growth^j; after each round the
+// positions are certified (fusion.h).  Exhausted lists contribute their
+// complete rankings, so a request either resolves early or at exhaustion.
 #include <algorithm>
 #include <atomic>
 #include <chrono>
@@ -28,212 +15,14 @@
 
 #include "common.h"
 #include "eahr.h"
+#include "fusion.h"
 #include "host_parallel.h"
 #include "pvs_internal.h"
 
 namespace {
 
-typedef unsigned __int128 u128;
-
-struct Frac {
-    u128 num = 0;
-    u128 den = 1;
-};
-
-inline int cmp(const Frac& a, const Frac& b) {
-    const u128 l = a.num * b.den, r = b.num * a.den;
-    return (l < r) ? -1 : (l > r) ? 1 : 0;
-}
-inline Frac add(const Frac& a, const Frac& b) {
-    if (a.num == 0) return b;
-    if (b.num == 0) return a;
-    return Frac{a.num * b.den + b.num * a.den, a.den * b.den};
-}
-
-struct Params {
-    int64_t K, k, w[2];
-};
-
-// g_i(r), 1-based r; 0 when w_i = 0.
-inline Frac g(const Params& P, int i, int64_t r) {
-    if (P.w[i] == 0) return Frac{0, 1};
-    return Frac{static_cast<u128>(P.w[i]), static_cast<u128>(r + P.w[i] * (P.k - 1))};
-}
-
-// (a, x) precedes (b, y): a > b, or a == b and x < y.
-inline bool precedes(const Frac& a, int64_t x, const Frac& b, int64_t y) {
-    const int c = cmp(a, b);
-    return c > 0 || (c == 0 && x < y);
-}
-
-// Open-addressing map id -> (rank in dense, rank in sparse, fixed flag).
-struct ItemMap {
-    struct Slot {
-        int64_t id;
-        int32_t rank[2];
-        int32_t fixed;
-    };
-    std::vector<Slot> slots;
-    size_t used = 0;
-    ItemMap() { slots.assign(64, Slot{-1, {0, 0}, 0}); }
-    static size_t hash(int64_t id) {
-        const uint64_t x = static_cast<uint64_t>(id) * 0x9E3779B97F4A7C15ull;
-        return static_cast<size_t>(x ^ (x >> 29));
-    }
-    Slot* find(int64_t id) {
-        const size_t mask = slots.size() - 1;
-        for (size_t h = hash(id) & mask;; h = (h + 1) & mask) {
-            if (slots[h].id == id) return &slots[h];
-            if (slots[h].id < 0) return nullptr;
-        }
-    }
-    Slot* get(int64_t id) {
-        if ((used + 1) * 2 > slots.size()) rehash(slots.size() * 2);
-        const size_t mask = slots.size() - 1;
-        for (size_t h = hash(id) & mask;; h = (h + 1) & mask) {
-            if (slots[h].id == id) return &slots[h];
-            if (slots[h].id < 0) {
-                slots[h] = Slot{id, {0, 0}, 0};
-                ++used;
-                return &slots[h];
-            }
-        }
-    }
-    void reserve(size_t n) {
-        size_t want = 64;
-        while (want < 2 * n + 2) want *= 2;
-        if (want > slots.size()) rehash(want);
-    }
-    void rehash(size_t n) {
-        std::vector<Slot> old;
-        old.swap(slots);
-        slots.assign(n, Slot{-1, {0, 0}, 0});
-        used = 0;
-        const size_t mask = n - 1;
-        for (const Slot& s : old) {
-            if (s.id < 0) continue;
-            size_t h = hash(s.id) & mask;
-            while (slots[h].id >= 0) h = (h + 1) & mask;
-            slots[h] = s;
-            ++used;
-        }
-    }
-};
-
-struct Scored {
-    Frac F;
-    int64_t id;
-};
-// heap order: a below b when b precedes a
-struct HeapLess {
-    bool operator()(const Scored& a, const Scored& b) const { return precedes(b.F, b.id, a.F, a.id); }
-};
-
-struct Fusion {
-    const Params* P = nullptr;
-    std::vector<int64_t> list[2];   // exact prefixes read so far
-    bool open[2] = {true, true};
-    int64_t cursor[2] = {0, 0};     // first possibly single-list unfixed item
-    ItemMap items;
-    std::vector<Scored> both;       // binary heap of unfixed both-seen items
-    std::vector<int64_t> A;
-    bool resolved = false;
-
-    void append(int i, const int64_t* ids, int64_t n) {
-        items.reserve(items.used + static_cast<size_t>(n));
-        list[i].reserve(list[i].size() + static_cast<size_t>(n));
-        for (int64_t j = 0; j < n; ++j) {
-            const int64_t x = ids[j];
-            list[i].push_back(x);
-            ItemMap::Slot* s = items.get(x);
-            s->rank[i] = static_cast<int32_t>(list[i].size());
-            if (!s->fixed && s->rank[1 - i] > 0) {
-                both.push_back(Scored{add(g(*P, 0, s->rank[0]), g(*P, 1, s->rank[1])), x});
-                std::push_heap(both.begin(), both.end(), HeapLess());
-            }
-        }
-    }
-
-    // first unfixed item of list i, at or after position p, seen only by i
-    int64_t single_from(int i, int64_t p) {
-        for (; p < static_cast<int64_t>(list[i].size()); ++p) {
-            const ItemMap::Slot* s = items.find(list[i][p]);
-            if (!s->fixed && s->rank[1 - i] == 0) return p;
-        }
-        return -1;
-    }
-
-    Frac u(int i) const {
-        return open[i] ? g(*P, i, static_cast<int64_t>(list[i].size()) + 1) : Frac{0, 1};
-    }
-
-    void certify() {
-        if (resolved) return;
-        const Frac ui[2] = {u(0), u(1)};
-        const Frac B = add(ui[0], ui[1]);
-        while (static_cast<int64_t>(A.size()) < P->K) {
-            struct Cand {
-                int64_t id;
-                Frac L, U;
-                int kind;        // 0: both, 1: dense only, 2: sparse only
-                int64_t pos;     // list position for single-list items
-            };
-            Cand c[3];
-            int nc = 0;
-            if (!both.empty()) c[nc++] = Cand{both[0].id, both[0].F, both[0].F, 0, -1};
-            for (int i = 0; i < 2; ++i) {
-                const int64_t p = single_from(i, cursor[i]);
-                if (p >= 0) {
-                    cursor[i] = p;
-                    const Frac L = g(*P, i, p + 1);
-                    c[nc++] = Cand{list[i][p], L, add(L, ui[1 - i]), 1 + i, p};
-                } else {
-                    cursor[i] = static_cast<int64_t>(list[i].size());
-                }
-            }
-            if (nc == 0) break;
-            int xd = 0;
-            for (int j = 1; j < nc; ++j)
-                if (precedes(c[j].L, c[j].id, c[xd].L, c[xd].id)) xd = j;
-            const Cand& X = c[xd];
-            bool ok = cmp(X.L, B) > 0;
-            // strongest remaining competitor of each group, x_dag excluded
-            for (int j = 0; ok && j < nc; ++j) {
-                if (j != xd) {
-                    ok = precedes(X.L, X.id, c[j].U, c[j].id);
-                    continue;
-                }
-                if (X.kind == 0) {
-                    const size_t n = both.size();
-                    int64_t second = -1;
-                    if (n > 1) second = 1;
-                    if (n > 2 && HeapLess()(both[1], both[2])) second = 2;
-                    if (second >= 0) ok = precedes(X.L, X.id, both[second].F, both[second].id);
-                } else {
-                    const int i = X.kind - 1;
-                    const int64_t p = single_from(i, X.pos + 1);
-                    if (p >= 0) {
-                        const Frac L = g(*P, i, p + 1);
-                        ok = precedes(X.L, X.id, add(L, ui[1 - i]), list[i][p]);
-                    }
-                }
-            }
-            if (!ok) break;
-            A.push_back(X.id);
-            items.find(X.id)->fixed = 1;
-            if (X.kind == 0) {
-                std::pop_heap(both.begin(), both.end(), HeapLess());
-                both.pop_back();
-            }
-        }
-        if (static_cast<int64_t>(A.size()) >= P->K) {
-            resolved = true;
-        } else if (B.num == 0 && both.empty() && single_from(0, cursor[0]) < 0 &&
-                   single_from(1, cursor[1]) < 0) {
-            resolved = true;   // nothing unseen or remaining can score: q_K = |A|
-        }
-    }
-};
+using ::eahr::Fusion;
+using ::eahr::Params;
 
 int check_params(const eahr_params& ep) {
     if (ep.K < 0 || ep.depth0 < 1 || ep.growth < 2 || ep.k_rrf < 1 || ep.k_rrf > (1 << 20) ||
@@ -287,8 +76,8 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
     std::vector<uint8_t> failed(B, 0);
     for (int32_t b = 0; b < B; ++b) {
         F[b].P = &P;
-        F[b].open[0] = use_dense;
-        F[b].open[1] = use_sparse;
+        F[b].L[0].open = use_dense;
+        F[b].L[1].open = use_sparse;
         if (use_dense) dstat[b] = EAHR_LIST_OPEN;
         if (use_sparse) sstat[b] = EAHR_LIST_OPEN;
         if (ep.K == 0) F[b].resolved = true;
@@ -325,13 +114,13 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
         int64_t m = 0;
         for (int32_t b = 0; b < B; ++b) {
             const bool live = !F[b].resolved && !failed[b];
-            dact[b] = live && use_dense && F[b].open[0] &&
-                      static_cast<int64_t>(F[b].list[0].size()) < depth;
-            sact[b] = live && use_sparse && F[b].open[1] &&
-                      static_cast<int64_t>(F[b].list[1].size()) < depth;
+            dact[b] = live && use_dense && F[b].L[0].open &&
+                      static_cast<int64_t>(F[b].L[0].size()) < depth;
+            sact[b] = live && use_sparse && F[b].L[1].open &&
+                      static_cast<int64_t>(F[b].L[1].size()) < depth;
             dcnt[b] = 0;
             scnt[b] = 0;
-            if (dact[b]) m = std::max<int64_t>(m, depth - static_cast<int64_t>(F[b].list[0].size()));
+            if (dact[b]) m = std::max<int64_t>(m, depth - static_cast<int64_t>(F[b].L[0].size()));
         }
         if (m > (1LL << 30)) m = 1LL << 30;
         // sparse channel on worker threads while the dense channel runs on the GPU
@@ -341,7 +130,7 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
             const auto t0 = std::chrono::steady_clock::now();
             parallel_for(B, std::max(1, threads - 1), [&](int64_t b) {
                 if (!sact[b]) return;
-                const int64_t need = std::min<int64_t>(depth - static_cast<int64_t>(F[b].list[1].size()), 1LL << 30);
+                const int64_t need = std::min<int64_t>(depth - static_cast<int64_t>(F[b].L[1].size()), 1LL << 30);
                 sids[b].resize(static_cast<size_t>(need));
                 sscores[b].resize(static_cast<size_t>(need));
                 sparse_rc[b] = pbm_next(cl.sp[b], static_cast<int32_t>(need), sids[b].data(),
@@ -376,7 +165,7 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
                 }
                 F[b].append(0, dids.p.get() + static_cast<size_t>(b) * m, dcnt[b]);
                 if (dsts[b] == EAHR_LIST_EXHAUSTED) {
-                    F[b].open[0] = false;
+                    F[b].L[0].open = false;
                     dstat[b] = EAHR_LIST_EXHAUSTED;
                 }
             }
@@ -388,7 +177,7 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
                 }
                 F[b].append(1, sids[b].data(), scnt[b]);
                 if (ssts[b] == EAHR_LIST_EXHAUSTED) {
-                    F[b].open[1] = false;
+                    F[b].L[1].open = false;
                     sstat[b] = EAHR_LIST_EXHAUSTED;
                 }
             }
@@ -409,8 +198,8 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
         any_failed |= failed[b] != 0;
         if (stats) {
             eahr_query_stats& s = stats[b];
-            s.dense_depth = static_cast<int64_t>(f.list[0].size());
-            s.sparse_depth = static_cast<int64_t>(f.list[1].size());
+            s.dense_depth = static_cast<int64_t>(f.L[0].size());
+            s.sparse_depth = static_cast<int64_t>(f.L[1].size());
             s.dense_len = (dstat[b] == EAHR_LIST_EXHAUSTED) ? s.dense_depth : -1;
             s.sparse_len = (sstat[b] == EAHR_LIST_EXHAUSTED) ? s.sparse_depth : -1;
             s.dense_status = dstat[b];
@@ -432,28 +221,32 @@ extern "C" int eahr_fuse_lists(const int64_t* list_d, int64_t n_d, const int64_t
     const eahr_params& ep = *params;
     EAHR_TRY(check_params(ep));
     if (n_d >= (1LL << 31) || n_s >= (1LL << 31)) EAHR_FAIL(EAHR_E_RANGE, "eahr_fuse_lists: lists too long");
+    for (int64_t j = 0; j < n_d; ++j)
+        if (list_d[j] < 0 || list_d[j] >= (1LL << 31)) EAHR_FAIL(EAHR_E_RANGE, "eahr_fuse_lists: id outside [0, 2^31)");
+    for (int64_t j = 0; j < n_s; ++j)
+        if (list_s[j] < 0 || list_s[j] >= (1LL << 31)) EAHR_FAIL(EAHR_E_RANGE, "eahr_fuse_lists: id outside [0, 2^31)");
     const Params P{ep.K, ep.k_rrf, {ep.w_dense, ep.w_sparse}};
     Fusion f;
     f.P = &P;
     const int64_t* lists[2] = {list_d, list_s};
     const int64_t lens[2] = {n_d, n_s};
-    for (int i = 0; i < 2; ++i) f.open[i] = P.w[i] > 0 && lens[i] > 0;
+    for (int i = 0; i < 2; ++i) f.L[i].open = P.w[i] > 0 && lens[i] > 0;
     if (ep.K == 0) f.resolved = true;
     int32_t rounds = 0;
     int64_t depth = step > 0 ? step : ep.depth0;
     while (!f.resolved) {
         for (int i = 0; i < 2; ++i) {
-            if (!f.open[i]) continue;
-            const int64_t have = static_cast<int64_t>(f.list[i].size());
+            if (!f.L[i].open) continue;
+            const int64_t have = static_cast<int64_t>(f.L[i].size());
             const int64_t upto = std::min(depth, lens[i]);
             if (upto > have) f.append(i, lists[i] + have, upto - have);
-            if (static_cast<int64_t>(f.list[i].size()) == lens[i]) f.open[i] = false;
+            if (static_cast<int64_t>(f.L[i].size()) == lens[i]) f.L[i].open = false;
         }
         rounds += 1;
         f.certify();
         if (step > 0) depth += step;
         else depth = (depth > INT64_MAX / ep.growth) ? INT64_MAX : depth * ep.growth;
-        if (!f.resolved && !f.open[0] && !f.open[1]) {
+        if (!f.resolved && !f.L[0].open && !f.L[1].open) {
             f.certify();   // both complete: certification resolves every position
             if (!f.resolved) EAHR_FAIL(EAHR_E_INVALID, "eahr_fuse_lists: lists hold duplicate ids");
         }
@@ -462,12 +255,12 @@ extern "C" int eahr_fuse_lists(const int64_t* list_d, int64_t n_d, const int64_t
     for (int64_t j = 0; j < ep.K; ++j) out_ids[j] = (j < q) ? f.A[j] : -1;
     *out_count = static_cast<int32_t>(q);
     if (stats) {
-        stats->dense_depth = static_cast<int64_t>(f.list[0].size());
-        stats->sparse_depth = static_cast<int64_t>(f.list[1].size());
-        stats->dense_len = f.open[0] ? -1 : stats->dense_depth;
-        stats->sparse_len = f.open[1] ? -1 : stats->sparse_depth;
-        stats->dense_status = f.open[0] ? EAHR_LIST_OPEN : EAHR_LIST_EXHAUSTED;
-        stats->sparse_status = f.open[1] ? EAHR_LIST_OPEN : EAHR_LIST_EXHAUSTED;
+        stats->dense_depth = static_cast<int64_t>(f.L[0].size());
+        stats->sparse_depth = static_cast<int64_t>(f.L[1].size());
+        stats->dense_len = f.L[0].open ? -1 : stats->dense_depth;
+        stats->sparse_len = f.L[1].open ? -1 : stats->sparse_depth;
+        stats->dense_status = f.L[0].open ? EAHR_LIST_OPEN : EAHR_LIST_EXHAUSTED;
+        stats->sparse_status = f.L[1].open ? EAHR_LIST_OPEN : EAHR_LIST_EXHAUSTED;
         stats->rounds = rounds;
         stats->resolved = f.resolved ? 1 : 0;
     }

@@ -1,0 +1,249 @@
+// Certification core of exact adaptive weighted-RRF fusion (Sec. 2.1, 2.2).
+//
+// g_i(r) = 1 / (r / w_i + k - 1) = w_i / (r + w_i (k - 1)) with integer k and
+// w_i, so every bound is a sum of at most two unit terms w / D and compares
+// exactly as a fraction (numerators < 2^43, denominators < 2^64, products
+// < 2^107 in unsigned 128-bit integers).
+//
+// After every depth round the remaining observed items fall into three
+// groups: seen by both lists (L = U = F), seen by the dense list only
+// (L = g_d(r_d), U = L + u_s), seen by the sparse list only.  Inside a
+// single-list group L and U strictly decrease with the rank, so the group's
+// best L and best U belong to its first unfixed member; the both-seen group
+// is a binary heap on (F desc, id asc), whose best two items are the root and
+// the better child.  x_dag and its strongest competitor y are therefore among
+// at most six items, and each position is decided as in Sec. 2.2:
+// (L(x_dag), x_dag) must precede (U(y), y) for every other remaining y, and
+// L(x_dag) > B strictly.
+//
+// Bookkeeping without per-item hashing: each list keeps its prefix sorted by
+// id, so the ranks of a round are radix-sorted and merge-joined against the
+// other list to find items seen by both; a union-find over list positions
+// ("next live single-list position") skips items that became both-seen or
+// fixed in amortised constant time.  Ids must lie in [0, 2^31).
+#pragma once
+#include <algorithm>
+#include <cstdint>
+#include <vector>
+
+namespace eahr {
+
+typedef unsigned __int128 u128;
+
+struct Frac {
+    u128 num = 0;
+    u128 den = 1;
+};
+
+inline int cmp(const Frac& a, const Frac& b) {
+    const u128 l = a.num * b.den, r = b.num * a.den;
+    return (l < r) ? -1 : (l > r) ? 1 : 0;
+}
+inline Frac add(const Frac& a, const Frac& b) {
+    if (a.num == 0) return b;
+    if (b.num == 0) return a;
+    return Frac{a.num * b.den + b.num * a.den, a.den * b.den};
+}
+
+struct Params {
+    int64_t K, k, w[2];
+};
+
+// g_i(r), 1-based r; 0 when w_i = 0.
+inline Frac g(const Params& P, int i, int64_t r) {
+    if (P.w[i] == 0) return Frac{0, 1};
+    return Frac{static_cast<u128>(P.w[i]), static_cast<u128>(r + P.w[i] * (P.k - 1))};
+}
+
+// (a, x) precedes (b, y): a > b, or a == b and x < y.
+inline bool precedes(const Frac& a, int64_t x, const Frac& b, int64_t y) {
+    const int c = cmp(a, b);
+    return c > 0 || (c == 0 && x < y);
+}
+
+// Ascending sort of (id << 32 | rank) keys by id (ids < 2^31, distinct).
+inline void sort_by_id(std::vector<uint64_t>& a, std::vector<uint64_t>& tmp) {
+    const size_t n = a.size();
+    if (n < 4096) {
+        std::sort(a.begin(), a.end());
+        return;
+    }
+    tmp.resize(n);
+    std::vector<uint32_t> cnt(65536);
+    for (int pass = 0; pass < 2; ++pass) {
+        const int shift = 32 + 16 * pass;
+        std::fill(cnt.begin(), cnt.end(), 0u);
+        for (size_t i = 0; i < n; ++i) ++cnt[(a[i] >> shift) & 0xffff];
+        uint32_t sum = 0;
+        for (auto& c : cnt) {
+            const uint32_t t = c;
+            c = sum;
+            sum += t;
+        }
+        for (size_t i = 0; i < n; ++i) tmp[cnt[(a[i] >> shift) & 0xffff]++] = a[i];
+        a.swap(tmp);
+    }
+}
+
+struct Scored {
+    Frac F;
+    int64_t id;
+};
+// heap order: a below b when b precedes a
+struct HeapLess {
+    bool operator()(const Scored& a, const Scored& b) const { return precedes(b.F, b.id, a.F, a.id); }
+};
+
+struct Fusion {
+    struct List {
+        std::vector<int64_t> ids;      // exact prefix read so far
+        std::vector<uint64_t> by_id;   // (id << 32 | rank), ascending id
+        std::vector<int32_t> next;     // union-find: live single-list position at or after p
+        bool open = true;
+        int64_t cursor = 0;
+
+        int64_t find(int64_t p) {
+            while (next[p] != p) {
+                next[p] = next[next[p]];
+                p = next[p];
+            }
+            return p;
+        }
+        void kill(int64_t p) { next[p] = static_cast<int32_t>(p + 1); }
+        int64_t size() const { return static_cast<int64_t>(ids.size()); }
+    };
+
+    const Params* P = nullptr;
+    List L[2];
+    std::vector<Scored> both;   // binary heap of unfixed both-seen items
+    std::vector<int64_t> A;     // fixed prefix
+    bool resolved = false;
+    std::vector<uint64_t> batch, tmp, merged;
+
+    Fusion() {
+        for (auto& l : L) l.next.assign(1, 0);   // sentinel
+    }
+
+    bool fixed(int64_t x) const { return std::find(A.begin(), A.end(), x) != A.end(); }
+
+    // Append n ranks to list i (ids must be new to the list).
+    void append(int i, const int64_t* ids, int64_t n) {
+        if (n <= 0) return;
+        List& me = L[i];
+        List& other = L[1 - i];
+        const int64_t p0 = me.size();
+        me.ids.insert(me.ids.end(), ids, ids + n);
+        me.next.resize(static_cast<size_t>(p0 + n + 1));
+        for (int64_t p = p0; p <= p0 + n; ++p) me.next[p] = static_cast<int32_t>(p);
+        batch.resize(static_cast<size_t>(n));
+        for (int64_t j = 0; j < n; ++j)
+            batch[j] = (static_cast<uint64_t>(ids[j]) << 32) | static_cast<uint64_t>(p0 + j + 1);
+        sort_by_id(batch, tmp);
+        // merge-join with the other list: items now seen by both
+        size_t a = 0, b = 0;
+        const auto& ob = other.by_id;
+        while (a < batch.size() && b < ob.size()) {
+            const uint64_t xa = batch[a] >> 32, xb = ob[b] >> 32;
+            if (xa < xb) {
+                ++a;
+            } else if (xb < xa) {
+                ++b;
+            } else {
+                const int64_t ri = static_cast<int64_t>(batch[a] & 0xffffffffu);
+                const int64_t rj = static_cast<int64_t>(ob[b] & 0xffffffffu);
+                me.kill(ri - 1);
+                other.kill(rj - 1);
+                const int64_t x = static_cast<int64_t>(xa);
+                if (!fixed(x)) {
+                    const int64_t r0 = (i == 0) ? ri : rj, r1 = (i == 0) ? rj : ri;
+                    both.push_back(Scored{add(g(*P, 0, r0), g(*P, 1, r1)), x});
+                    std::push_heap(both.begin(), both.end(), HeapLess());
+                }
+                ++a;
+                ++b;
+            }
+        }
+        merged.resize(me.by_id.size() + batch.size());
+        std::merge(me.by_id.begin(), me.by_id.end(), batch.begin(), batch.end(), merged.begin());
+        me.by_id.swap(merged);
+    }
+
+    int64_t single_from(int i, int64_t p) {
+        const int64_t q = L[i].find(p);
+        return q < L[i].size() ? q : -1;
+    }
+
+    Frac u(int i) const {
+        return L[i].open ? g(*P, i, L[i].size() + 1) : Frac{0, 1};
+    }
+
+    void certify() {
+        if (resolved) return;
+        const Frac ui[2] = {u(0), u(1)};
+        const Frac B = add(ui[0], ui[1]);
+        while (static_cast<int64_t>(A.size()) < P->K) {
+            struct Cand {
+                int64_t id;
+                Frac L, U;
+                int kind;        // 0: both, 1: dense only, 2: sparse only
+                int64_t pos;     // list position for single-list items
+            };
+            Cand c[3];
+            int nc = 0;
+            if (!both.empty()) c[nc++] = Cand{both[0].id, both[0].F, both[0].F, 0, -1};
+            for (int i = 0; i < 2; ++i) {
+                const int64_t p = single_from(i, L[i].cursor);
+                if (p >= 0) {
+                    L[i].cursor = p;
+                    const Frac Li = g(*P, i, p + 1);
+                    c[nc++] = Cand{L[i].ids[p], Li, add(Li, ui[1 - i]), 1 + i, p};
+                } else {
+                    L[i].cursor = L[i].size();
+                }
+            }
+            if (nc == 0) break;
+            int xd = 0;
+            for (int j = 1; j < nc; ++j)
+                if (precedes(c[j].L, c[j].id, c[xd].L, c[xd].id)) xd = j;
+            const Cand X = c[xd];
+            bool ok = cmp(X.L, B) > 0;
+            // strongest remaining competitor of each group, x_dag excluded
+            for (int j = 0; ok && j < nc; ++j) {
+                if (j != xd) {
+                    ok = precedes(X.L, X.id, c[j].U, c[j].id);
+                    continue;
+                }
+                if (X.kind == 0) {
+                    const size_t n = both.size();
+                    int64_t second = -1;
+                    if (n > 1) second = 1;
+                    if (n > 2 && HeapLess()(both[1], both[2])) second = 2;
+                    if (second >= 0) ok = precedes(X.L, X.id, both[second].F, both[second].id);
+                } else {
+                    const int i = X.kind - 1;
+                    const int64_t p = single_from(i, X.pos + 1);
+                    if (p >= 0) {
+                        const Frac Li = g(*P, i, p + 1);
+                        ok = precedes(X.L, X.id, add(Li, ui[1 - i]), L[i].ids[p]);
+                    }
+                }
+            }
+            if (!ok) break;
+            A.push_back(X.id);
+            if (X.kind == 0) {
+                std::pop_heap(both.begin(), both.end(), HeapLess());
+                both.pop_back();
+            } else {
+                L[X.kind - 1].kill(X.pos);
+            }
+        }
+        if (static_cast<int64_t>(A.size()) >= P->K) {
+            resolved = true;
+        } else if (B.num == 0 && both.empty() && single_from(0, L[0].cursor) < 0 &&
+                   single_from(1, L[1].cursor) < 0) {
+            resolved = true;   // nothing unseen or remaining can score: q_K = |A|
+        }
+    }
+};
+
+}  // namespace eahr

@@ -81,6 +81,8 @@ bool is_device_ptr(const void* p) {
 
 }  // namespace
 
+static void free_buffers(ScanBuffers& b);
+
 // ======================================================================= index
 pvs_index::~pvs_index() {
     dev_free(codes);
@@ -92,6 +94,7 @@ pvs_index::~pvs_index() {
     dev_free(flags);
     dev_free(staging);
     for (auto& s : snaps) dev_free(s.vis);
+    free_buffers(spare);
 }
 
 static int index_grow(pvs_index* ix, int64_t need_rows) {
@@ -339,6 +342,61 @@ void pvs_state::release_scan_buffers() {
     h_packed_cap = 0;
 }
 
+// Move the scan buffers between a state and an index's spare slot.
+#define PVS_BUFFER_FIELDS(X)                                                                 \
+    X(buf_nq) X(buf_sample) X(scanq) X(counts) X(sample_lo) X(sample_hi) X(qfrag) X(pool_cap) \
+    X(cand_row) X(cand_lo) X(cand_hi) X(keys) X(keys_tmp) X(packed) X(h_scanq) X(h_counts)    \
+    X(h_packed) X(h_packed_cap)
+
+static void adopt_buffers(pvs_state* st, ScanBuffers& b) {
+#define PVS_MOVE_IN(f) st->f = b.f;
+    PVS_BUFFER_FIELDS(PVS_MOVE_IN)
+#undef PVS_MOVE_IN
+    b = ScanBuffers{};
+}
+
+static void donate_buffers(pvs_state* st, ScanBuffers& b) {
+#define PVS_MOVE_OUT(f) b.f = st->f;
+    PVS_BUFFER_FIELDS(PVS_MOVE_OUT)
+#undef PVS_MOVE_OUT
+    st->buf_nq = 0;
+    st->buf_sample = 0;
+    st->pool_cap = 0;
+    st->h_packed_cap = 0;
+    st->scanq = nullptr;
+    st->counts = nullptr;
+    st->sample_lo = nullptr;
+    st->sample_hi = nullptr;
+    st->qfrag = nullptr;
+    st->cand_row = nullptr;
+    st->cand_lo = nullptr;
+    st->cand_hi = nullptr;
+    st->keys = nullptr;
+    st->keys_tmp = nullptr;
+    st->packed = nullptr;
+    st->h_scanq = nullptr;
+    st->h_counts = nullptr;
+    st->h_packed = nullptr;
+}
+
+static void free_buffers(ScanBuffers& b) {
+    dev_free(b.scanq);
+    dev_free(b.counts);
+    dev_free(b.sample_lo);
+    dev_free(b.sample_hi);
+    dev_free(b.qfrag);
+    dev_free(b.cand_row);
+    dev_free(b.cand_lo);
+    dev_free(b.cand_hi);
+    dev_free(b.keys);
+    dev_free(b.keys_tmp);
+    dev_free(b.packed);
+    if (b.h_scanq) (void)hipHostFree(b.h_scanq);
+    if (b.h_counts) (void)hipHostFree(b.h_counts);
+    if (b.h_packed) (void)hipHostFree(b.h_packed);
+    b = ScanBuffers{};
+}
+
 // Per-query scan buffers for nq queries and samples of sample_ld rows.
 // counts layout: [cand nq][cert nq][fail nq][offs nq + 1]
 static int ensure_query_buffers(pvs_state* st, int32_t nq, int64_t sample_ld) {
@@ -425,6 +483,10 @@ extern "C" int pvs_open(const pvs_index* ix, int64_t epoch, const float* q, int3
     st->n_rows = ix->snaps[epoch].rows;
     st->n_vis = ix->snaps[epoch].visible;
     st->vis = ix->snaps[epoch].vis;
+    if (ix->has_spare) {
+        adopt_buffers(st.get(), ix->spare);
+        ix->has_spare = false;
+    }
     hipStream_t s = ix->stream;
     EAHR_TRY(dev_alloc(&st->qcodes, static_cast<size_t>(B) * ix->dp));
     EAHR_TRY(dev_alloc(&st->qrows, static_cast<size_t>(B) * ix->df));
@@ -474,7 +536,13 @@ extern "C" int pvs_open(const pvs_index* ix, int64_t epoch, const float* q, int3
 }
 
 extern "C" void pvs_close(pvs_state* st) {
-    if (st && st->ix) (void)hipStreamSynchronize(st->ix->stream);
+    if (st && st->ix) {
+        (void)hipStreamSynchronize(st->ix->stream);
+        if (!st->ix->has_spare) {
+            donate_buffers(st, st->ix->spare);
+            st->ix->has_spare = true;
+        }
+    }
     delete st;
 }
 

@@ -45,6 +45,30 @@ enum class ScanPath { Auto, Gemv, Mfma };
 bool pvs_profile_on();
 void pvs_profile_add_host(double dense_ms, double sparse_ms, double fuse_ms);
 
+// Scan buffers of a state (device, plus pinned host mirrors).  A closing
+// state hands them to its index, and the next state opened on that index
+// adopts them, so repeated requests do not re-allocate them.
+struct ScanBuffers {
+    int32_t buf_nq = 0;
+    int64_t buf_sample = 0;
+    pvs::ScanQ* scanq = nullptr;
+    int32_t* counts = nullptr;
+    float* sample_lo = nullptr;
+    float* sample_hi = nullptr;
+    void* qfrag = nullptr;
+    int64_t pool_cap = 0;
+    int32_t* cand_row = nullptr;
+    float* cand_lo = nullptr;
+    float* cand_hi = nullptr;
+    uint64_t* keys = nullptr;
+    uint64_t* keys_tmp = nullptr;
+    uint64_t* packed = nullptr;
+    pvs::ScanQ* h_scanq = nullptr;
+    int32_t* h_counts = nullptr;
+    uint64_t* h_packed = nullptr;
+    int64_t h_packed_cap = 0;
+};
+
 struct pvs_index {
     struct Snapshot {
         int64_t rows = 0;      // physical rows visible to the epoch (prefix)
@@ -66,6 +90,8 @@ struct pvs_index {
     float nv_max = 0.0f, nev_max = 0.0f;
     float gamma = 0.0f;
     std::vector<Snapshot> snaps;
+    mutable ScanBuffers spare;   // buffers of the last closed state
+    mutable bool has_spare = false;
     ~pvs_index();
 };
 

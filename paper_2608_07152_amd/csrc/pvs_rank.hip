@@ -26,20 +26,53 @@ __global__ __launch_bounds__(256) void k_rescore(
     load_query_row<J>(qrows, Q.qi, df4, lane, qv);
     const int64_t n = min(static_cast<int64_t>(cand_cnt[b]), Q.cand_cap);
     int local_cert = 0;
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6); i < n;
-         i += static_cast<int64_t>(gridDim.x) * 4) {
-        const int64_t at = Q.cand_off + i;
-        const int32_t row = cand_row[at];
-        const float s = row_score<J>(rows + static_cast<int64_t>(row) * df4, qv, lane, df4);
-        if (lane == 0) {
-            const float lo = cand_lo[at];
-            const float hi = cand_hi[at];
-            if (!(lo <= s && s <= hi)) fail[b] = 1;
-            const bool dropped = Q.has_cert && (s > Q.s_cert || (s == Q.s_cert && row <= Q.id_cert));
-            const bool cert = !dropped && s >= Q.tau;
-            const uint64_t hiw = cert ? static_cast<uint64_t>(~mono32(s)) : 0xffffffffull;
-            keys[at] = (hiw << 32) | static_cast<uint32_t>(row);
-            local_cert += cert;
+    // R candidates per wavefront iteration keep R * J 16-byte loads in flight
+    constexpr int R = (J <= 4) ? 4 : 1;
+    const int64_t wave = __builtin_amdgcn_readfirstlane(
+        static_cast<int>(blockIdx.x * 4 + (threadIdx.x >> 6)));
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * 4 * R;
+    for (int64_t i0 = wave * R; i0 < n; i0 += stride) {
+        int32_t row[R];
+        float4 v[R][J];
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+            const int64_t i = i0 + k;
+            row[k] = (i < n) ? cand_row[Q.cand_off + i] : -1;
+            const float4* rp = rows + static_cast<int64_t>(row[k] < 0 ? 0 : row[k]) * df4;
+#pragma unroll
+            for (int t = 0; t < J; ++t) {
+                const int idx = 64 * t + lane;
+                v[k][t] = (row[k] >= 0 && idx < df4) ? rp[idx] : make_float4(0, 0, 0, 0);
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+            if (row[k] < 0) break;
+            // same accumulation order as row_score: (t, x, y, z, w), then the butterfly
+            float acc = 0.0f;
+#pragma unroll
+            for (int t = 0; t < J; ++t) {
+                if (64 * t + lane < df4) {
+                    acc = fmaf(qv[t].x, v[k][t].x, acc);
+                    acc = fmaf(qv[t].y, v[k][t].y, acc);
+                    acc = fmaf(qv[t].z, v[k][t].z, acc);
+                    acc = fmaf(qv[t].w, v[k][t].w, acc);
+                }
+            }
+            for (int off = 32; off > 0; off >>= 1) acc = acc + __shfl_xor(acc, off, 64);
+            const float s = acc;
+            if (lane == 0) {
+                const int64_t at = Q.cand_off + i0 + k;
+                const float lo = cand_lo[at];
+                const float hi = cand_hi[at];
+                if (!(lo <= s && s <= hi)) fail[b] = 1;
+                const bool dropped =
+                    Q.has_cert && (s > Q.s_cert || (s == Q.s_cert && row[k] <= Q.id_cert));
+                const bool cert = !dropped && s >= Q.tau;
+                const uint64_t hiw = cert ? static_cast<uint64_t>(~mono32(s)) : 0xffffffffull;
+                keys[at] = (hiw << 32) | static_cast<uint32_t>(row[k]);
+                local_cert += cert;
+            }
         }
     }
     if (lane == 0 && local_cert) atomicAdd(&cert_cnt[b], local_cert);

@@ -165,8 +165,9 @@ __global__ __launch_bounds__(64) void k_qfrag(const int8_t* __restrict__ qcodes,
     frag[(static_cast<int64_t>(s) * nqt + u) * 64 + lane] = v;
 }
 
-// One wavefront per 64-row block and NQT tiles of 32 queries: 2 x NQT
-// accumulators of 32 x 32.  Epilogue per query tile: lane l owns query
+// One wavefront per 64-row block and NQT tiles of 32 queries, processed NQS
+// tiles at a time (2 x NQS accumulators of 32 x 32; a second half re-reads
+// the block's codes from L2).  Epilogue per query tile: lane l owns query
 // 32 u + l % 32 and 32 of the block's rows; the centre-score pre-test skips
 // the exact interval for rows that cannot reach tau; survivors of lanes l and
 // l ^ 32 (same query) reserve their slots with one atomic.
@@ -177,17 +178,27 @@ __global__ __launch_bounds__(256) void k_scan_mfma(
     const uint64_t* __restrict__ vis, int64_t nblocks, int32_t nchunk,
     const v4i* __restrict__ qfrag, const ScanQ* __restrict__ sq, int32_t nq, float gamma,
     ScanOut o) {
+    constexpr int NQS = NQT < 4 ? NQT : 4;
     const int lane = threadIdx.x & 63;
     const int64_t w = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
     const int64_t blk = SAMPLE ? w * o.sample_stride : w;
     if (blk >= nblocks) return;
-    v16i acc[2][NQT];
+    const uint64_t vbits = vis[blk];
+    float svr[2][16];   // scales of this lane's 32 rows
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int u = 0; u < NQT; ++u) acc[t][u] = v16i{};
+        for (int r = 0; r < 16; ++r)
+            svr[t][r] = scale[blk * 64 + 32 * t + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)];
     const uint4* A = codes + blk * nchunk * 64 + (lane >> 5) * 64 + (lane & 31);
     const int nsteps = nchunk >> 1;
+#pragma unroll 1
+    for (int u0 = 0; u0 < NQT; u0 += NQS) {
+    v16i acc[2][NQS];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int u = 0; u < NQS; ++u) acc[t][u] = v16i{};
 #pragma unroll 2
     for (int s = 0; s < nsteps; ++s) {
         const u32x4 a0 = load_nt(A + 2 * s * 64);
@@ -196,15 +207,15 @@ __global__ __launch_bounds__(256) void k_scan_mfma(
         __builtin_memcpy(&va0, &a0, 16);
         __builtin_memcpy(&va1, &a1, 16);
 #pragma unroll
-        for (int u = 0; u < NQT; ++u) {
-            const v4i vb = qfrag[(s * NQT + u) * 64 + lane];
+        for (int u = 0; u < NQS; ++u) {
+            const v4i vb = qfrag[(s * NQT + u0 + u) * 64 + lane];
             acc[0][u] = __builtin_amdgcn_mfma_i32_32x32x32_i8(va0, vb, acc[0][u], 0, 0, 0);
             acc[1][u] = __builtin_amdgcn_mfma_i32_32x32x32_i8(va1, vb, acc[1][u], 0, 0, 0);
         }
     }
-    const uint64_t vbits = vis[blk];
 #pragma unroll
-    for (int u = 0; u < NQT; ++u) {
+    for (int uu = 0; uu < NQS; ++uu) {
+        const int u = u0 + uu;
         const int b = 32 * u + (lane & 31);
         const bool valid = b < nq;
         const ScanQ Q = sq[valid ? b : 0];
@@ -217,7 +228,7 @@ __global__ __launch_bounds__(256) void k_scan_mfma(
                     const int rib = 32 * t + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
                     const int64_t row = blk * 64 + rib;
                     float lo, hi;
-                    pair_interval(Q, scale[row], vnorm[row], enorm[row], acc[t][u][r], gamma, lo, hi);
+                    pair_interval(Q, svr[t][r], vnorm[row], enorm[row], acc[t][uu][r], gamma, lo, hi);
                     const bool elig = ((vbits >> rib) & 1ull) && (!Q.has_cert || lo <= Q.s_cert);
                     const int64_t i = b * o.sample_ld + w * 64 + rib;
                     o.sample_lo[i] = elig ? lo : -INFINITY;
@@ -234,11 +245,11 @@ __global__ __launch_bounds__(256) void k_scan_mfma(
             for (int r = 0; r < 16; ++r) {
                 const int rib = 32 * t + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
                 const int64_t row = blk * 64 + rib;
-                const float sv = scale[row];
-                const float c = (Q.sq * sv) * static_cast<float>(acc[t][u][r]);
+                const float sv = svr[t][r];
+                const float c = (Q.sq * sv) * static_cast<float>(acc[t][uu][r]);
                 if (valid && c >= thr && ((vbits >> rib) & 1ull)) {
                     float lo, hi;
-                    pair_interval(Q, sv, vnorm[row], enorm[row], acc[t][u][r], gamma, lo, hi);
+                    pair_interval(Q, sv, vnorm[row], enorm[row], acc[t][uu][r], gamma, lo, hi);
                     if (hi >= Q.tau && (!Q.has_cert || lo <= Q.s_cert)) mask |= 1u << (16 * t + r);
                 }
             }
@@ -259,7 +270,7 @@ __global__ __launch_bounds__(256) void k_scan_mfma(
                 const int64_t row = blk * 64 + rib;
                 if (pos < Q.cand_cap) {
                     float lo, hi;
-                    pair_interval(Q, scale[row], vnorm[row], enorm[row], acc[t][u][r], gamma, lo, hi);
+                    pair_interval(Q, svr[t][r], vnorm[row], enorm[row], acc[t][uu][r], gamma, lo, hi);
                     const int64_t at = Q.cand_off + pos;
                     o.cand_row[at] = static_cast<int32_t>(row);
                     o.cand_lo[at] = lo;
@@ -268,6 +279,7 @@ __global__ __launch_bounds__(256) void k_scan_mfma(
                 ++pos;
             }
         }
+    }
     }
 }
 
