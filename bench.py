@@ -170,18 +170,23 @@ def main():
         el = time.perf_counter() - t
         prof = eahr.pvs_profile_read()
         eahr.pvs_profile_enable(False)
-        launches = max(1, prof["scan_launches"])
-        avg_ms = prof["scan_ms"] / launches
-        bpl = prof["scan_bytes"] / launches
+        # dominant scan kernel variant = most total scan time
+        vms = prof["variant_ms"]
+        v = max(range(len(vms)), key=lambda i: vms[i])
+        launches = max(1, prof["variant_launches"][v])
+        avg_ms = vms[v] / launches
+        bpl = prof["variant_bytes"][v] / launches
         achieved = bpl / (avg_ms * 1e-3) / 1e9 if avg_ms > 0 else 0.0
+        variants = {eahr.pvs_profile.VARIANTS[i]: {"ms": vms[i], "launches": prof["variant_launches"][i]}
+                    for i in range(len(vms)) if prof["variant_launches"][i]}
         stats = [s for r in res for s in r[3]]
         dd = np.array([s["dense_depth"] for s in stats])
         out = {
             "batch": bsz, "steps": steps, "queries_per_s": steps * bsz / el,
             "ms_per_step": el / steps * 1e3,
-            "scan_kernel": "k_scan_mfma" if prof["mfma_launches"] else "k_scan_gemv",
+            "scan_kernel": eahr.pvs_profile.VARIANTS[v],
             "scan_gbs": achieved, "scan_frac": achieved / HBM_PEAK_GBS, "scan_avg_launch_ms": avg_ms,
-            "scan_launches": prof["scan_launches"], "scan_bytes_per_launch": bpl,
+            "scan_launches": launches, "scan_bytes_per_launch": bpl, "scan_variants": variants,
             "kernel_ms": {"scan": prof["scan_ms"], "sample_select": prof["sample_ms"],
                           "rescore": prof["rescore_ms"], "sort_pack": prof["sort_ms"]},
             "rescored_rows": prof["rescore_rows"],

@@ -135,6 +135,12 @@ typedef struct {
     double host_dense_ms;    /* eahr_topk: wall time of its pvs_next calls   */
     double host_sparse_ms;   /* eahr_topk: wall time of its PBM rounds       */
     double host_fuse_ms;     /* eahr_topk: wall time of certification        */
+    /* Full scans per kernel variant: [0..7] dot4 GEMV with 1..8 queries per
+     * launch, [8..11] Int8 MFMA with 1, 2, 4, 8 tiles of 32 queries.  A scan
+     * pass of one variant is one launch. */
+    double variant_ms[12];
+    int64_t variant_launches[12];
+    int64_t variant_bytes[12];
 } pvs_profile;
 
 int pvs_profile_enable(int32_t on);   /* also clears the accumulators */

@@ -85,31 +85,63 @@ inline void sort_by_id(std::vector<uint64_t>& a, std::vector<uint64_t>& tmp) {
     }
 }
 
+// A both-seen item: its ranks define F exactly; f is F in float64 (relative
+// error below 2^-50), used to order items whose values are far apart.
 struct Scored {
-    Frac F;
+    double f;
+    int32_t r0, r1;
     int64_t id;
 };
-// heap order: a below b when b precedes a
+
+inline Frac exact_F(const Params& P, const Scored& s) {
+    return add(g(P, 0, s.r0), g(P, 1, s.r1));
+}
+
+// heap order: a below b when b precedes a (exact; float64 decides only when
+// the two values differ by more than 1e-12 relative)
 struct HeapLess {
-    bool operator()(const Scored& a, const Scored& b) const { return precedes(b.F, b.id, a.F, a.id); }
+    const Params* P;
+    bool operator()(const Scored& a, const Scored& b) const {
+        const double d = b.f - a.f, m = (a.f > b.f ? a.f : b.f) * 1e-12;
+        if (d > m) return true;
+        if (d < -m) return false;
+        const int c = cmp(exact_F(*P, b), exact_F(*P, a));
+        return c > 0 || (c == 0 && b.id < a.id);
+    }
 };
+
+inline double g_double(const Params& P, int i, int64_t r) {
+    if (P.w[i] == 0) return 0.0;
+    return static_cast<double>(P.w[i]) / static_cast<double>(r + P.w[i] * (P.k - 1));
+}
 
 struct Fusion {
     struct List {
         std::vector<int64_t> ids;      // exact prefix read so far
         std::vector<uint64_t> by_id;   // (id << 32 | rank), ascending id
-        std::vector<int32_t> next;     // union-find: live single-list position at or after p
+        std::vector<uint64_t> alive;   // bit p: position p is an unfixed single-list item
         bool open = true;
         int64_t cursor = 0;
 
-        int64_t find(int64_t p) {
-            while (next[p] != p) {
-                next[p] = next[next[p]];
-                p = next[p];
+        // first live position at or after p (size() if none)
+        int64_t find(int64_t p) const {
+            const int64_t n = size();
+            if (p >= n) return n;
+            size_t w = static_cast<size_t>(p >> 6);
+            uint64_t bits = alive[w] & (~0ull << (p & 63));
+            while (!bits) {
+                if (++w >= alive.size()) return n;
+                bits = alive[w];
             }
-            return p;
+            const int64_t q = static_cast<int64_t>(w * 64 + __builtin_ctzll(bits));
+            return q < n ? q : n;
         }
-        void kill(int64_t p) { next[p] = static_cast<int32_t>(p + 1); }
+        void kill(int64_t p) { alive[p >> 6] &= ~(1ull << (p & 63)); }
+        void grow(int64_t n_new) {   // new positions start live
+            const int64_t p0 = size();
+            alive.resize(static_cast<size_t>((p0 + n_new + 63) >> 6), 0);
+            for (int64_t p = p0; p < p0 + n_new; ++p) alive[p >> 6] |= 1ull << (p & 63);
+        }
         int64_t size() const { return static_cast<int64_t>(ids.size()); }
     };
 
@@ -120,10 +152,6 @@ struct Fusion {
     bool resolved = false;
     std::vector<uint64_t> batch, tmp, merged;
 
-    Fusion() {
-        for (auto& l : L) l.next.assign(1, 0);   // sentinel
-    }
-
     bool fixed(int64_t x) const { return std::find(A.begin(), A.end(), x) != A.end(); }
 
     // Append n ranks to list i (ids must be new to the list).
@@ -132,14 +160,14 @@ struct Fusion {
         List& me = L[i];
         List& other = L[1 - i];
         const int64_t p0 = me.size();
+        me.grow(n);
         me.ids.insert(me.ids.end(), ids, ids + n);
-        me.next.resize(static_cast<size_t>(p0 + n + 1));
-        for (int64_t p = p0; p <= p0 + n; ++p) me.next[p] = static_cast<int32_t>(p);
         batch.resize(static_cast<size_t>(n));
         for (int64_t j = 0; j < n; ++j)
             batch[j] = (static_cast<uint64_t>(ids[j]) << 32) | static_cast<uint64_t>(p0 + j + 1);
         sort_by_id(batch, tmp);
         // merge-join with the other list: items now seen by both
+        const size_t heap0 = both.size();
         size_t a = 0, b = 0;
         const auto& ob = other.by_id;
         while (a < batch.size() && b < ob.size()) {
@@ -156,12 +184,21 @@ struct Fusion {
                 const int64_t x = static_cast<int64_t>(xa);
                 if (!fixed(x)) {
                     const int64_t r0 = (i == 0) ? ri : rj, r1 = (i == 0) ? rj : ri;
-                    both.push_back(Scored{add(g(*P, 0, r0), g(*P, 1, r1)), x});
-                    std::push_heap(both.begin(), both.end(), HeapLess());
+                    both.push_back(Scored{g_double(*P, 0, r0) + g_double(*P, 1, r1),
+                                          static_cast<int32_t>(r0), static_cast<int32_t>(r1), x});
                 }
                 ++a;
                 ++b;
             }
+        }
+        // restore the heap: one push per new item, or a linear rebuild when
+        // the round added many
+        const size_t added = both.size() - heap0;
+        if (added > heap0 / 8) {
+            std::make_heap(both.begin(), both.end(), HeapLess{P});
+        } else {
+            for (size_t k = heap0 + 1; k <= both.size(); ++k)
+                std::push_heap(both.begin(), both.begin() + k, HeapLess{P});
         }
         merged.resize(me.by_id.size() + batch.size());
         std::merge(me.by_id.begin(), me.by_id.end(), batch.begin(), batch.end(), merged.begin());
@@ -190,7 +227,10 @@ struct Fusion {
             };
             Cand c[3];
             int nc = 0;
-            if (!both.empty()) c[nc++] = Cand{both[0].id, both[0].F, both[0].F, 0, -1};
+            if (!both.empty()) {
+                const Frac F0 = exact_F(*P, both[0]);
+                c[nc++] = Cand{both[0].id, F0, F0, 0, -1};
+            }
             for (int i = 0; i < 2; ++i) {
                 const int64_t p = single_from(i, L[i].cursor);
                 if (p >= 0) {
@@ -217,8 +257,9 @@ struct Fusion {
                     const size_t n = both.size();
                     int64_t second = -1;
                     if (n > 1) second = 1;
-                    if (n > 2 && HeapLess()(both[1], both[2])) second = 2;
-                    if (second >= 0) ok = precedes(X.L, X.id, both[second].F, both[second].id);
+                    if (n > 2 && HeapLess{P}(both[1], both[2])) second = 2;
+                    if (second >= 0)
+                        ok = precedes(X.L, X.id, exact_F(*P, both[second]), both[second].id);
                 } else {
                     const int i = X.kind - 1;
                     const int64_t p = single_from(i, X.pos + 1);
@@ -231,7 +272,7 @@ struct Fusion {
             if (!ok) break;
             A.push_back(X.id);
             if (X.kind == 0) {
-                std::pop_heap(both.begin(), both.end(), HeapLess());
+                std::pop_heap(both.begin(), both.end(), HeapLess{P});
                 both.pop_back();
             } else {
                 L[X.kind - 1].kill(X.pos);

@@ -146,6 +146,29 @@ extern "C" int pbm_open(const pbm_index* ix, const eahr_sparse_query* q, pbm_sta
 // Score every document of range r that carries a query term and queue the
 // positive ones; fails when a score exceeds the range bound (metadata that
 // does not cover its postings, App. A.2).
+static inline uint32_t ord32(float f) {
+    uint32_t b;
+    std::memcpy(&b, &f, 4);
+    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+static inline float unord32(uint32_t k) {
+    const uint32_t b = (k & 0x80000000u) ? (k & 0x7fffffffu) : ~k;
+    float f;
+    std::memcpy(&f, &b, 4);
+    return f;
+}
+static inline uint64_t item_key(float s, int64_t id) {
+    return (static_cast<uint64_t>(~ord32(s + 0.0f)) << 32) | static_cast<uint64_t>(id);
+}
+static inline uint64_t bound_key(const pbm_state* st) {
+    if (st->ranges.empty()) return ~0ull;
+    const auto& R = st->ranges.top();
+    return (static_cast<uint64_t>(~ord32(R.H)) << 32) | static_cast<uint64_t>(R.r * st->ix->range_size);
+}
+
+// Score every document of range R that carries a query term and add the
+// positive ones to the pool; fails when a score exceeds the range bound
+// (metadata that does not cover its postings, App. A.2).
 static bool expand(pbm_state* st, const pbm_state::Range& R) {
     const pbm_index* ix = st->ix;
     const int64_t start = R.r * ix->range_size;
@@ -176,18 +199,42 @@ static bool expand(pbm_state* st, const pbm_state::Range& R) {
     for (int32_t off : st->touched) {
         const float s = st->acc[off];
         if (s > R.H) ok = false;
-        if (s > 0.0f) st->items.push(pbm_state::Item{s, start + off});
+        if (s > 0.0f) st->pool.push_back(item_key(s, start + off));
         st->acc[off] = 0.0f;
         st->seen[off] = 0;
     }
     return ok;
 }
 
-static bool can_publish(const pbm_state* st, const pbm_state::Item& it) {
-    if (st->ranges.empty()) return true;
-    const auto& R = st->ranges.top();
-    const int64_t start = R.r * st->ix->range_size;
-    return it.s > R.H || (it.s == R.H && it.id < start);
+// Refill the ready run with at least `want` publishable items when the
+// remaining ranges allow: expand ranges in bound order until enough pooled
+// items precede the next range's bound (counted whenever the pool has grown
+// by half since the last count), then move those items out of the pool and
+// sort them.  Returns false on a failed expansion.
+static bool refill(pbm_state* st, size_t want) {
+    st->ready.clear();
+    st->ready_pos = 0;
+    size_t checked = 0;
+    for (;;) {
+        if (st->ranges.empty()) break;
+        if (st->pool.size() >= want && st->pool.size() >= checked + checked / 2) {
+            const uint64_t bk = bound_key(st);
+            size_t n = 0;
+            for (uint64_t k : st->pool) n += (k < bk);
+            if (n >= want) break;
+            checked = st->pool.size();
+        }
+        const auto R = st->ranges.top();
+        st->ranges.pop();
+        st->ranges_expanded += 1;
+        if (!expand(st, R)) return false;
+    }
+    const uint64_t bk = bound_key(st);
+    auto mid = std::partition(st->pool.begin(), st->pool.end(), [bk](uint64_t k) { return k < bk; });
+    st->ready.assign(st->pool.begin(), mid);
+    st->pool.erase(st->pool.begin(), mid);
+    std::sort(st->ready.begin(), st->ready.end());
+    return true;
 }
 
 extern "C" int pbm_next(pbm_state* st, int32_t m, int64_t* ids, float* scores, int32_t* count,
@@ -197,19 +244,15 @@ extern "C" int pbm_next(pbm_state* st, int32_t m, int64_t* ids, float* scores, i
     int32_t n = 0;
     if (!st->failed) {
         while (n < m) {
-            while (n < m && !st->items.empty() && can_publish(st, st->items.top())) {
-                const auto it = st->items.top();
-                st->items.pop();
-                ids[n] = it.id;
-                scores[n] = it.s;
+            if (st->ready_pos < st->ready.size()) {
+                const uint64_t k = st->ready[st->ready_pos++];
+                ids[n] = static_cast<int64_t>(k & 0xffffffffu);
+                scores[n] = unord32(~static_cast<uint32_t>(k >> 32));
                 ++n;
+                continue;
             }
-            if (n == m) break;
-            if (st->ranges.empty()) break;   // items empty too: list complete
-            const auto R = st->ranges.top();
-            st->ranges.pop();
-            st->ranges_expanded += 1;
-            if (!expand(st, R)) {
+            if (st->ranges.empty() && st->pool.empty()) break;   // list complete
+            if (!refill(st, static_cast<size_t>(m - n))) {
                 st->failed = true;
                 n = 0;
                 break;
@@ -219,7 +262,8 @@ extern "C" int pbm_next(pbm_state* st, int32_t m, int64_t* ids, float* scores, i
     st->emitted += n;
     *count = n;
     if (st->failed) *status = EAHR_LIST_FAILED;
-    else if (st->ranges.empty() && st->items.empty()) *status = EAHR_LIST_EXHAUSTED;
+    else if (st->ranges.empty() && st->pool.empty() && st->ready_pos >= st->ready.size())
+        *status = EAHR_LIST_EXHAUSTED;
     else *status = EAHR_LIST_OPEN;
     return EAHR_OK;
 }

@@ -31,20 +31,16 @@ struct pbm_state {
             return a.H < b.H || (a.H == b.H && a.r > b.r);
         }
     };
-    struct Item {
-        float s;
-        int64_t id;
-    };
-    struct ItemOrder {    // max-heap on (S desc, id asc)
-        bool operator()(const Item& a, const Item& b) const {
-            return a.s < b.s || (a.s == b.s && a.id > b.id);
-        }
-    };
     const pbm_index* ix = nullptr;
     std::vector<int32_t> terms;   // ascending term ids with nonzero weight
     std::vector<float> w;
     std::priority_queue<Range, std::vector<Range>, RangeOrder> ranges;
-    std::priority_queue<Item, std::vector<Item>, ItemOrder> items;
+    // Scored items as keys (~ord(S) << 32 | id): ascending keys are
+    // (S desc, id asc), and an item precedes range R's bound exactly when its
+    // key is below (~ord(H(R)) << 32 | first id of R).
+    std::vector<uint64_t> pool;   // scored, not yet publishable
+    std::vector<uint64_t> ready;  // publishable, sorted; ready[ready_pos..] pending
+    size_t ready_pos = 0;
     std::vector<float> acc;       // per-range scratch
     std::vector<uint8_t> seen;
     std::vector<int32_t> touched;

@@ -825,7 +825,16 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
         const int64_t launches = (nq + per - 1) / per;
         g_prof.scan_launches += launches;
         if (mfma) g_prof.mfma_launches += launches;
-        g_prof.scan_bytes += launches * (st->n_rows * (static_cast<int64_t>(ix->d) + 12) + nblocks * 8);
+        const int64_t pass_bytes = st->n_rows * (static_cast<int64_t>(ix->d) + 12) + nblocks * 8;
+        g_prof.scan_bytes += launches * pass_bytes;
+        // kernel variant of the first launch (the only one when nq fits one pass)
+        const int first = static_cast<int>(std::min<int64_t>(nq, per));
+        int v = mfma ? 8 + (pvs::mfma_tiles_for(first) == 1 ? 0 : pvs::mfma_tiles_for(first) == 2 ? 1
+                            : pvs::mfma_tiles_for(first) == 4 ? 2 : 3)
+                     : first - 1;
+        g_prof.variant_ms[v] += t[1];
+        g_prof.variant_launches[v] += launches;
+        g_prof.variant_bytes[v] += launches * pass_bytes;
         g_prof.rescore_ms += t[2];
         g_prof.rescore_rows += kept;
         g_prof.sort_ms += t[3];

@@ -73,10 +73,19 @@ class pvs_profile(C.Structure):
                 ("sample_ms", C.c_double), ("rescore_ms", C.c_double), ("rescore_rows", C.c_int64),
                 ("sort_ms", C.c_double), ("scan_rounds", C.c_int64),
                 ("mfma_launches", C.c_int64), ("host_dense_ms", C.c_double),
-                ("host_sparse_ms", C.c_double), ("host_fuse_ms", C.c_double)]
+                ("host_sparse_ms", C.c_double), ("host_fuse_ms", C.c_double),
+                ("variant_ms", C.c_double * 12), ("variant_launches", C.c_int64 * 12),
+                ("variant_bytes", C.c_int64 * 12)]
+
+    VARIANTS = [f"k_scan_gemv<{q}>" for q in range(1, 9)] + \
+        [f"k_scan_mfma<{t}>" for t in (1, 2, 4, 8)]
 
     def as_dict(self):
-        return {f: getattr(self, f) for f, _ in self._fields_}
+        out = {}
+        for f, _ in self._fields_:
+            v = getattr(self, f)
+            out[f] = list(v) if f.startswith("variant_") else v
+        return out
 
 
 _P = C.c_void_p
