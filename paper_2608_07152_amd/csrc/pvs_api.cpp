@@ -751,8 +751,10 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     for (; run < nq; ++run) {
         ScanQ& sq = st->h_scanq[run];
         const auto& Q = st->q[todo[run]];
+        // exact count when the sample saw every block, plus room for the
+        // unused tails of per-workgroup slices (at most cap / 16)
         int64_t cap = (stride == 1)
-                          ? static_cast<int64_t>(sq.sample_hits)
+                          ? static_cast<int64_t>(sq.sample_hits) + sq.sample_hits / 8 + 64
                           : static_cast<int64_t>(std::ceil(sq.sample_hits / frac * pvs::kCapSlack)) + pvs::kCapPad;
         cap = std::max(cap, Q.cap_hint);
         cap = std::min<int64_t>(std::max<int64_t>(cap, 1), st->n_rows);

@@ -94,6 +94,19 @@ __device__ __forceinline__ float center_threshold(const ScanQ& Q) {
     return Q.tau - Q.wmax * 1.001f - 0x1p-20f * (fabsf(Q.tau) + Q.wmax);
 }
 
+// The same pre-test for one block, whose visible rows have norms at most nvb
+// (||v||) and nevb (||e_v||): E + G over those rows is bounded as wmax is over
+// the index (|c| <= ||q_hat|| (||v|| + ||e_v||)), with a 1 % margin that
+// absorbs the float32 rounding of the bound.
+__device__ __forceinline__ float block_threshold(const ScanQ& Q, float nvb, float nevb,
+                                                 float gamma) {
+    const float E = Q.neq * nvb + Q.nqh * nevb;
+    const float cb = Q.nqh * (nvb + nevb);
+    const float G = (cb + E + Q.nq * nvb) * gamma;
+    const float w = fminf((E + G) * 1.01f, Q.wmax);
+    return Q.tau - w * 1.001f - 0x1p-20f * (fabsf(Q.tau) + w);
+}
+
 // Authoritative float32 score of one row (fixed order, see the file header).
 template <int J>
 __device__ __forceinline__ float row_score(const float4* __restrict__ rp, const float4 (&qv)[J],

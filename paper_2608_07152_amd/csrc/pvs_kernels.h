@@ -11,6 +11,7 @@ constexpr int kMaxDim = 4096;      // 127^2 * 4096 < 2^31 and a_m < 1
 constexpr int kSortTile = 2048;    // keys sorted per workgroup in LDS
 constexpr int kMaxGemvQueries = 8; // queries per GEMV scan pass
 constexpr int kMaxMfmaQueries = 256;  // queries per MFMA scan pass (8 tiles of 32)
+constexpr int kMaxChunk = 256;     // largest slice of a candidate region one workgroup reserves
 
 // Per scanning query, uploaded before every scan.  All fields are read
 // uniformly by a wavefront (scalar loads).
@@ -56,7 +57,9 @@ void launch_quantize(const float* src, int64_t nrows, int32_t d, int64_t src_str
 // (query, row) pair of the sampled blocks, row-major [query][sample_ld],
 // -inf / -inf for ineligible rows.  Main pass: candidates of query b go to
 // slots cand_off .. cand_off + cand_cap - 1 of its ScanQ; cand_cnt[b] counts
-// every candidate, including those past the region.
+// every slot handed out, including those past the region.  A slot may hold
+// the sentinel row -1 (part of a reserved slice left unused), which is no
+// candidate.
 struct ScanOut {
     float* sample_lo = nullptr;
     float* sample_hi = nullptr;

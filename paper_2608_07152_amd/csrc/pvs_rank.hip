@@ -47,7 +47,12 @@ __global__ __launch_bounds__(256) void k_rescore(
         }
 #pragma unroll
         for (int k = 0; k < R; ++k) {
-            if (row[k] < 0) break;
+            if (i0 + k >= n) break;
+            if (row[k] < 0) {   // sentinel slot: a unique key after every real one
+                if (lane == 0)
+                    keys[Q.cand_off + i0 + k] = ~0ull - static_cast<uint64_t>(i0 + k);
+                continue;
+            }
             // same accumulation order as row_score: (t, x, y, z, w), then the butterfly
             float acc = 0.0f;
 #pragma unroll
@@ -150,9 +155,10 @@ __global__ __launch_bounds__(256) void k_sort_tiles(uint64_t* __restrict__ keys,
     for (int i = threadIdx.x; i < m; i += 256) k[i] = s[i];
 }
 
-// One merge level: runs of length `run` are merged pairwise.  Keys are unique
-// inside a region, so an element's output slot is its offset in its own run
-// plus the number of smaller keys in the partner run (binary search).
+// One merge level: runs of length `run` are merged pairwise.  An element's
+// output slot is its offset in its own run plus the number of keys of the
+// partner run that precede it (binary search; smaller keys, and for the right
+// run also equal ones, so the merge is stable).
 __global__ __launch_bounds__(256) void k_merge(const uint64_t* __restrict__ src,
                                                uint64_t* __restrict__ dst,
                                                const int32_t* __restrict__ cnt,
@@ -178,9 +184,10 @@ __global__ __launch_bounds__(256) void k_merge(const uint64_t* __restrict__ src,
         own = i - mid;
     }
     const int64_t first = lo;
+    const bool left = i < mid;   // ties (none expected) go to the left run first
     while (lo < hi) {
         const int64_t m = (lo + hi) >> 1;
-        if (s[m] < key) lo = m + 1;
+        if (s[m] < key || (!left && s[m] == key)) lo = m + 1;
         else hi = m;
     }
     d[start + own + (lo - first)] = key;

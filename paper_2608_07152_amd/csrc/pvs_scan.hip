@@ -7,6 +7,8 @@
 //
 // Two kernels compute the same integers: a dot4 GEMV for a few queries and an
 // Int8 MFMA contraction for batches.
+#include <algorithm>
+
 #include "pvs_device.h"
 
 namespace pvs {
@@ -184,12 +186,18 @@ __global__ __launch_bounds__(256) void k_scan_mfma(
     const int64_t blk = SAMPLE ? w * o.sample_stride : w;
     if (blk >= nblocks) return;
     const uint64_t vbits = vis[blk];
-    float svr[2][16];   // scales of this lane's 32 rows
+    // scale and norms of this lane's 32 rows, loaded before the K loop so the
+    // epilogue's interval tests never wait on memory
+    float svr[2][16], vnr[2][16], enr[2][16];
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-            svr[t][r] = scale[blk * 64 + 32 * t + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)];
+        for (int r = 0; r < 16; ++r) {
+            const int64_t row = blk * 64 + 32 * t + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+            svr[t][r] = scale[row];
+            vnr[t][r] = vnorm[row];
+            enr[t][r] = enorm[row];
+        }
     const uint4* A = codes + blk * nchunk * 64 + (lane >> 5) * 64 + (lane & 31);
     const int nsteps = nchunk >> 1;
 #pragma unroll 1
@@ -228,7 +236,7 @@ __global__ __launch_bounds__(256) void k_scan_mfma(
                     const int rib = 32 * t + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
                     const int64_t row = blk * 64 + rib;
                     float lo, hi;
-                    pair_interval(Q, svr[t][r], vnorm[row], enorm[row], acc[t][uu][r], gamma, lo, hi);
+                    pair_interval(Q, svr[t][r], vnr[t][r], enr[t][r], acc[t][uu][r], gamma, lo, hi);
                     const bool elig = ((vbits >> rib) & 1ull) && (!Q.has_cert || lo <= Q.s_cert);
                     const int64_t i = b * o.sample_ld + w * 64 + rib;
                     o.sample_lo[i] = elig ? lo : -INFINITY;
@@ -249,7 +257,7 @@ __global__ __launch_bounds__(256) void k_scan_mfma(
                 const float c = (Q.sq * sv) * static_cast<float>(acc[t][uu][r]);
                 if (valid && c >= thr && ((vbits >> rib) & 1ull)) {
                     float lo, hi;
-                    pair_interval(Q, sv, vnorm[row], enorm[row], acc[t][uu][r], gamma, lo, hi);
+                    pair_interval(Q, sv, vnr[t][r], enr[t][r], acc[t][uu][r], gamma, lo, hi);
                     if (hi >= Q.tau && (!Q.has_cert || lo <= Q.s_cert)) mask |= 1u << (16 * t + r);
                 }
             }
@@ -270,7 +278,7 @@ __global__ __launch_bounds__(256) void k_scan_mfma(
                 const int64_t row = blk * 64 + rib;
                 if (pos < Q.cand_cap) {
                     float lo, hi;
-                    pair_interval(Q, svr[t][r], vnorm[row], enorm[row], acc[t][uu][r], gamma, lo, hi);
+                    pair_interval(Q, svr[t][r], vnr[t][r], enr[t][r], acc[t][uu][r], gamma, lo, hi);
                     const int64_t at = Q.cand_off + pos;
                     o.cand_row[at] = static_cast<int32_t>(row);
                     o.cand_lo[at] = lo;
@@ -283,6 +291,236 @@ __global__ __launch_bounds__(256) void k_scan_mfma(
     }
 }
 
+// Wide batches (NQT = 4 or 8 tiles of 32 queries).  A persistent workgroup
+// of 4 wavefronts per CU takes 4 consecutive blocks at a time, one per
+// wavefront, and runs the K loop once per half of 4 query tiles (2 x 4
+// accumulators of 32 x 32).  The K loop has no branches: it advances PA steps
+// per stage (PA divides the step count), the A fragments of the next stage
+// stream into a register ring while the current stage multiplies, and the B
+// fragments of one stage (PA x 4 KiB) are loaded once per workgroup one stage
+// ahead and shared by the 4 wavefronts through double-buffered LDS, with one
+// barrier per stage.  A second half re-reads the block's codes from cache.
+//
+// Epilogue: lane l owns query 32 u + l % 32 and 32 of the block's rows.  A
+// per-block bound of E + G (from the block's largest norms) gives a centre
+// threshold below which no row of the block can reach tau; invisible rows
+// carry a NaN scale so they fail it.  Candidates are appended through chunks
+// of each query's region that the workgroup reserves with one global atomic
+// per chunk (per-wave atomics on B hot counters serialise); slots of a chunk
+// left unused at the end hold the sentinel row -1, which the region's count
+// includes and rescoring skips.
+template <int NQT, int PA>
+__global__ __launch_bounds__(256, 1) void k_scan_mfma_wide(
+    const uint4* __restrict__ codes, const float* __restrict__ scale,
+    const float* __restrict__ vnorm, const float* __restrict__ enorm,
+    const uint64_t* __restrict__ vis, int64_t nblocks, int32_t nchunk,
+    const v4i* __restrict__ qfrag, const ScanQ* __restrict__ sq, int32_t nq, float gamma,
+    ScanOut o) {
+    constexpr int NQS = 4;                     // tiles per half
+    __shared__ v4i bsm[2][PA][NQS * 64];       // B fragments of two stages
+    __shared__ float s_meta[4][3][64];         // scale (NaN if invisible), norm, error norm
+    __shared__ int32_t s_wcnt[4][NQS * 32];    // per wave counts, then offsets
+    __shared__ int32_t s_pos[NQT * 32];        // next free slot of each query's chunk
+    __shared__ int32_t s_end[NQT * 32];        // end of that chunk
+    __shared__ int32_t s_old[NQS * 32], s_room[NQS * 32], s_new[NQS * 32];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    for (int b = tid; b < NQT * 32; b += 256) s_pos[b] = s_end[b] = 0;
+    __syncthreads();
+    const int nsteps = nchunk >> 1;            // a multiple of PA
+    const int64_t ngroups = (nblocks + 3) / 4;
+    for (int64_t grp = blockIdx.x; grp < ngroups; grp += gridDim.x) {
+        const int64_t blk = grp * 4 + wave;
+        const bool have = blk < nblocks;
+        const uint4* A = codes + (have ? blk : 0) * nchunk * 64 + (lane >> 5) * 64 + (lane & 31);
+        float nvb = 0.0f, nevb = 0.0f;         // largest norms of the block's visible rows
+        {
+            const int64_t row = (have ? blk : 0) * 64 + lane;
+            const bool v = have && ((vis[have ? blk : 0] >> lane) & 1ull);
+            const float nv = vnorm[row], nev = enorm[row];
+            s_meta[wave][0][lane] = v ? scale[row] : __builtin_nanf("");
+            s_meta[wave][1][lane] = nv;
+            s_meta[wave][2][lane] = nev;
+            nvb = wave_max(v ? nv : 0.0f);
+            nevb = wave_max(v ? nev : 0.0f);
+        }
+#pragma unroll 1
+        for (int u0 = 0; u0 < NQT; u0 += NQS) {
+            v16i acc[2][NQS];
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int u = 0; u < NQS; ++u) acc[t][u] = v16i{};
+            // stage 0: B into LDS, A into the register ring
+            v4i bst[PA];
+            v4i a[PA][2];
+#pragma unroll
+            for (int p = 0; p < PA; ++p) bst[p] = qfrag[(p * NQT + u0) * 64 + tid];
+#pragma unroll
+            for (int p = 0; p < PA; ++p) bsm[0][p][tid] = bst[p];
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int p = 0; p < PA; ++p) {
+                const u32x4 x0 = load_nt(A + 2 * p * 64);
+                const u32x4 x1 = load_nt(A + 2 * p * 64 + 32);
+                __builtin_memcpy(&a[p][0], &x0, 16);
+                __builtin_memcpy(&a[p][1], &x1, 16);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            __syncthreads();
+            // Scheduling barriers pin the order: the B loads of the next stage
+            // are issued first and stored to LDS at the end of the stage, the
+            // A load of step + PA right after step's MFMAs, and the LDS reads
+            // of step + 1 before step's MFMAs, so each load has about a stage
+            // of MFMA work to arrive.
+            for (int s0 = 0; s0 < nsteps; s0 += PA) {
+                const int cur = (s0 / PA) & 1;
+#pragma unroll
+                for (int p = 0; p < PA; ++p) {
+                    const int sn = min(s0 + PA + p, nsteps - 1);
+                    bst[p] = qfrag[(sn * NQT + u0) * 64 + tid];
+                }
+                v4i vb[2][NQS];
+#pragma unroll
+                for (int u = 0; u < NQS; ++u) vb[0][u] = bsm[cur][0][u * 64 + lane];
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int p = 0; p < PA; ++p) {
+                    if (p + 1 < PA) {
+#pragma unroll
+                        for (int u = 0; u < NQS; ++u) vb[(p + 1) & 1][u] = bsm[cur][p + 1][u * 64 + lane];
+                    }
+#pragma unroll
+                    for (int u = 0; u < NQS; ++u) {
+                        acc[0][u] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[p][0], vb[p & 1][u], acc[0][u], 0, 0, 0);
+                        acc[1][u] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[p][1], vb[p & 1][u], acc[1][u], 0, 0, 0);
+                    }
+                    const int sn = min(s0 + PA + p, nsteps - 1);
+                    const u32x4 y0 = load_nt(A + 2 * sn * 64);
+                    const u32x4 y1 = load_nt(A + 2 * sn * 64 + 32);
+                    __builtin_memcpy(&a[p][0], &y0, 16);
+                    __builtin_memcpy(&a[p][1], &y1, 16);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+#pragma unroll
+                for (int p = 0; p < PA; ++p) bsm[cur ^ 1][p][tid] = bst[p];
+                __syncthreads();
+            }
+            // candidate masks of this half; lanes l and l ^ 32 hold one query
+            uint32_t mask[NQS];
+            int other[NQS];
+#pragma unroll
+            for (int uu = 0; uu < NQS; ++uu) {
+                const int b = 32 * (u0 + uu) + (lane & 31);
+                const bool valid = have && b < nq;
+                const ScanQ Q = sq[b < nq ? b : 0];
+                const float thr = block_threshold(Q, nvb, nevb, gamma);
+                uint32_t mk = 0;
+#pragma unroll
+                for (int t = 0; t < 2; ++t) {
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int rib = 32 * t + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                        const float sv = s_meta[wave][0][rib];
+                        const float c = (Q.sq * sv) * static_cast<float>(acc[t][uu][r]);
+                        if (valid && c >= thr) {
+                            float lo, hi;
+                            pair_interval(Q, sv, s_meta[wave][1][rib], s_meta[wave][2][rib],
+                                          acc[t][uu][r], gamma, lo, hi);
+                            if (hi >= Q.tau && (!Q.has_cert || lo <= Q.s_cert)) mk |= 1u << (16 * t + r);
+                        }
+                    }
+                }
+                mask[uu] = mk;
+                const int mine = __popc(mk);
+                other[uu] = __shfl_xor(mine, 32, 64);
+                if (lane < 32) s_wcnt[wave][32 * uu + lane] = mine + other[uu];
+            }
+            __syncthreads();
+            // one thread per query: wave offsets, and a new chunk of the
+            // query's region when the current one is too small
+            if (tid < NQS * 32) {
+                const int b = 32 * u0 + tid;
+                int tot = 0;
+#pragma unroll
+                for (int w = 0; w < 4; ++w) {
+                    const int c = s_wcnt[w][tid];
+                    s_wcnt[w][tid] = tot;
+                    tot += c;
+                }
+                const int old = s_pos[b];
+                const int room = s_end[b] - old;
+                int nb = 0;
+                if (tot > room) {
+                    const int need = tot - room;
+                    const int64_t cap = sq[b].cand_cap;
+                    const int64_t per = cap / (16 * static_cast<int64_t>(gridDim.x));
+                    const int chunk = static_cast<int>(per < 1 ? 1 : per > kMaxChunk ? kMaxChunk : per);
+                    const int take = need > chunk ? need : chunk;
+                    nb = atomicAdd(&o.cand_cnt[b], take);
+                    s_pos[b] = nb + need;
+                    s_end[b] = nb + take;
+                } else {
+                    s_pos[b] = old + tot;
+                }
+                s_old[tid] = old;
+                s_room[tid] = room;
+                s_new[tid] = nb;
+            }
+            __syncthreads();
+            if (have) {
+#pragma unroll
+                for (int uu = 0; uu < NQS; ++uu) {
+                    if (!mask[uu]) continue;
+                    const int ql = 32 * uu + (lane & 31);
+                    const ScanQ Q = sq[32 * u0 + ql];
+                    const int old = s_old[ql], room = s_room[ql], nb = s_new[ql];
+                    int j = s_wcnt[wave][ql] + ((lane >= 32) ? other[uu] : 0);
+#pragma unroll
+                    for (int t = 0; t < 2; ++t) {
+#pragma unroll
+                        for (int r = 0; r < 16; ++r) {
+                            if (!((mask[uu] >> (16 * t + r)) & 1u)) continue;
+                            const int rib = 32 * t + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                            const int64_t row = blk * 64 + rib;
+                            const int64_t pos = (j < room) ? old + j : nb + (j - room);
+                            if (pos < Q.cand_cap) {
+                                float lo, hi;
+                                pair_interval(Q, s_meta[wave][0][rib], s_meta[wave][1][rib],
+                                              s_meta[wave][2][rib], acc[t][uu][r], gamma, lo, hi);
+                                const int64_t at = Q.cand_off + pos;
+                                o.cand_row[at] = static_cast<int32_t>(row);
+                                o.cand_lo[at] = lo;
+                                o.cand_hi[at] = hi;
+                            }
+                            ++j;
+                        }
+                    }
+                }
+            }
+            __syncthreads();   // bsm, the metadata and the chunk tables are reused next
+        }
+    }
+    // unused tails of this workgroup's chunks become sentinel rows (-1)
+    for (int b = tid; b < NQT * 32 && b < nq; b += 256) {
+        const ScanQ Q = sq[b];
+        const int64_t e = s_end[b] < Q.cand_cap ? s_end[b] : Q.cand_cap;
+        for (int64_t p = s_pos[b]; p < e; ++p) o.cand_row[Q.cand_off + p] = -1;
+    }
+}
+
+static int cu_count() {
+    static int n = 0;
+    if (n == 0) {
+        int dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+            n = 256;
+    }
+    return n;
+}
+
 template <int NQT>
 static void mfma_pass(const IndexView& ix, const uint64_t* vis, int64_t nblocks, const v4i* qfrag,
                       const ScanQ* sq, int32_t nq, float gamma, bool sample, const ScanOut& o,
@@ -293,6 +531,27 @@ static void mfma_pass(const IndexView& ix, const uint64_t* vis, int64_t nblocks,
         hipLaunchKernelGGL((k_scan_mfma<NQT, true>), dim3(grid), dim3(256), 0, stream, ix.codes,
                            ix.scale, ix.vnorm, ix.enorm, vis, nblocks, ix.nchunk, qfrag, sq, nq,
                            gamma, o);
+    } else if (NQT >= 4) {
+        constexpr int W = NQT >= 4 ? NQT : 4;
+        const int64_t groups = (nblocks + 3) / 4;
+        const uint32_t g = static_cast<uint32_t>(std::min<int64_t>(groups, cu_count()));
+        const int nsteps = ix.nchunk / 2;
+        if (nsteps % 8 == 0)
+            hipLaunchKernelGGL((k_scan_mfma_wide<W, 8>), dim3(g), dim3(256), 0, stream, ix.codes,
+                               ix.scale, ix.vnorm, ix.enorm, vis, nblocks, ix.nchunk, qfrag, sq, nq,
+                               gamma, o);
+        else if (nsteps % 4 == 0)
+            hipLaunchKernelGGL((k_scan_mfma_wide<W, 4>), dim3(g), dim3(256), 0, stream, ix.codes,
+                               ix.scale, ix.vnorm, ix.enorm, vis, nblocks, ix.nchunk, qfrag, sq, nq,
+                               gamma, o);
+        else if (nsteps % 2 == 0)
+            hipLaunchKernelGGL((k_scan_mfma_wide<W, 2>), dim3(g), dim3(256), 0, stream, ix.codes,
+                               ix.scale, ix.vnorm, ix.enorm, vis, nblocks, ix.nchunk, qfrag, sq, nq,
+                               gamma, o);
+        else
+            hipLaunchKernelGGL((k_scan_mfma_wide<W, 1>), dim3(g), dim3(256), 0, stream, ix.codes,
+                               ix.scale, ix.vnorm, ix.enorm, vis, nblocks, ix.nchunk, qfrag, sq, nq,
+                               gamma, o);
     } else {
         hipLaunchKernelGGL((k_scan_mfma<NQT, false>), dim3(grid), dim3(256), 0, stream, ix.codes,
                            ix.scale, ix.vnorm, ix.enorm, vis, nblocks, ix.nchunk, qfrag, sq, nq,
