@@ -34,6 +34,15 @@ int check_params(const eahr_params& ep) {
 using ::eahr::host_threads;
 using ::eahr::parallel_for;
 
+// Dense work-ahead while a round's sparse channel runs: never past this depth
+// per query, nor past this many ranks summed over the round's dense queries.
+// A further level starts only while its estimated time (ranks it may certify
+// times the measured time per certified rank of earlier work-ahead) fits in
+// the sparse channel's estimated remaining time (elapsed time scaled by the
+// share of its queries still to finish).
+constexpr int64_t kFillMaxDepth = int64_t(1) << 17;
+constexpr int64_t kFillBudget = int64_t(1) << 25;
+
 double ms_since(std::chrono::steady_clock::time_point t0) {
     return std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
 }
@@ -106,6 +115,8 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
     std::vector<uint8_t> sact(B, 0);
     std::vector<int> sparse_rc(B, EAHR_OK);
     int64_t depth = ep.depth0;
+    double fill_ms = 0.0;            // measured cost of dense work-ahead
+    int64_t fill_ranks = 0;
     for (;;) {
         bool any = false;
         for (int32_t b = 0; b < B; ++b) any |= !F[b].resolved && !failed[b];
@@ -125,7 +136,9 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
         if (m > (1LL << 30)) m = 1LL << 30;
         // sparse channel on worker threads while the dense channel runs on the GPU
         std::thread sparse_thread;
-        auto t_round = std::chrono::steady_clock::now();
+        std::atomic<bool> sparse_done{false};
+        std::atomic<int64_t> sparse_finished{0};
+        const auto t_sparse0 = std::chrono::steady_clock::now();
         auto sparse_work = [&]() {
             const auto t0 = std::chrono::steady_clock::now();
             parallel_for(B, std::max(1, threads - 1), [&](int64_t b) {
@@ -135,8 +148,10 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
                 sscores[b].resize(static_cast<size_t>(need));
                 sparse_rc[b] = pbm_next(cl.sp[b], static_cast<int32_t>(need), sids[b].data(),
                                         sscores[b].data(), &scnt[b], &ssts[b]);
+                sparse_finished.fetch_add(1, std::memory_order_relaxed);
             });
             t_sparse += ms_since(t0);
+            sparse_done.store(true, std::memory_order_release);
         };
         bool any_sparse = false;
         for (int32_t b = 0; b < B; ++b) any_sparse |= sact[b] != 0;
@@ -147,10 +162,38 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
             int64_t* ids = dids.get(static_cast<size_t>(B) * m);
             float* sc = dscores.get(static_cast<size_t>(B) * m);
             dense_rc = pvs_next(cl.st, static_cast<int32_t>(m), dact.data(), ids, sc, dcnt.data(), dsts.data());
+            // While the sparse channel is still busy, certify the dense ranks
+            // of the next depths ahead (they are served from the cache later;
+            // the output does not depend on it).
+            int64_t nd = 0, ns = 0;
+            for (int32_t b = 0; b < B; ++b) {
+                nd += dact[b];
+                ns += sact[b];
+            }
+            const int64_t cap = std::min<int64_t>(kFillMaxDepth, kFillBudget / std::max<int64_t>(nd, 1));
+            int64_t ahead = depth;
+            while (dense_rc == EAHR_OK && sparse_thread.joinable() && ahead <= cap / ep.growth &&
+                   !sparse_done.load(std::memory_order_acquire)) {
+                // remaining sparse time: from the finished share, or (none
+                // finished yet) at least the time it has run so far
+                const int64_t fin = sparse_finished.load(std::memory_order_relaxed);
+                const double run = ms_since(t_sparse0);
+                const double left = fin > 0 ? run * static_cast<double>(ns - fin) / fin : run;
+                const double rate = fill_ranks > 0 ? fill_ms / static_cast<double>(fill_ranks) : 0.0;
+                const double est = rate * static_cast<double>((ahead * ep.growth - ahead) * nd);
+                if (est > left) break;
+                ahead *= ep.growth;
+                const auto tf = std::chrono::steady_clock::now();
+                int64_t added = 0;
+                dense_rc = pvs_fill(cl.st, ahead, dact.data(), &added);
+                if (added > 0) {
+                    fill_ms += ms_since(tf);
+                    fill_ranks += added;
+                }
+            }
             t_dense += ms_since(t0);
         }
         if (sparse_thread.joinable()) sparse_thread.join();
-        (void)t_round;
         EAHR_TRY(dense_rc);
         for (int32_t b = 0; b < B; ++b) EAHR_TRY(sparse_rc[b]);
         // merge this round's ranks and certify, one query per task

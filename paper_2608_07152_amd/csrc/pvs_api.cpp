@@ -944,6 +944,33 @@ extern "C" int pvs_next(pvs_state* st, int32_t m, const uint8_t* active, int64_t
     return EAHR_OK;
 }
 
+int pvs_fill(pvs_state* st, int64_t depth, const uint8_t* active, int64_t* added) {
+    if (!st || depth < 0) EAHR_FAIL(EAHR_E_INVALID, "pvs_fill: bad arguments");
+    std::vector<int32_t> todo;
+    int64_t m = 0, before = 0;
+    for (int32_t b = 0; b < st->B; ++b) {
+        if (active && !active[b]) continue;
+        const auto& Q = st->q[b];
+        before += static_cast<int64_t>(Q.cache_score.size());
+        if (Q.failed || Q.cert_exhausted) continue;
+        if (static_cast<int64_t>(Q.cache_score.size()) >= depth) continue;
+        todo.push_back(b);
+        m = std::max<int64_t>(m, depth - Q.emitted);
+    }
+    m = std::min<int64_t>(m, int64_t(1) << 30);
+    for (int guard = 0; !todo.empty(); ++guard) {
+        if (guard > 200) EAHR_FAIL(EAHR_E_HIP, "pvs_fill: scan loop did not converge");
+        EAHR_TRY(scan_round(st, todo, static_cast<int32_t>(m)));
+    }
+    if (added) {
+        int64_t after = 0;
+        for (int32_t b = 0; b < st->B; ++b)
+            if (!active || active[b]) after += static_cast<int64_t>(st->q[b].cache_score.size());
+        *added = after - before;
+    }
+    return EAHR_OK;
+}
+
 extern "C" int pvs_stats(const pvs_state* st, pvs_counters* out) {
     if (!st || !out) EAHR_FAIL(EAHR_E_INVALID, "pvs_stats: bad arguments");
     *out = st->stats;

@@ -107,6 +107,19 @@ __device__ __forceinline__ float block_threshold(const ScanQ& Q, float nvb, floa
     return Q.tau - w * 1.001f - 0x1p-20f * (fabsf(Q.tau) + w);
 }
 
+// Threshold for fl(s_v * dot) equivalent to `thr` for c = fl(fl(s_q s_v) dot),
+// loosened so that c >= thr implies fl(s_v * dot) >= the result: the two
+// products differ by at most 3 roundings (relative 2^-22), the margin is
+// 2^-20 relative plus an absolute term for results near zero.  A tiny s_q
+// (or an overflowing quotient) gives -inf: every pair then takes the exact
+// test.
+__device__ __forceinline__ float scaled_threshold(float thr, float sq) {
+    if (!(sq >= 0x1p-20f)) return -INFINITY;
+    const float t = thr / sq;
+    const float r = t - fabsf(t) * 0x1p-20f - 0x1p-100f;
+    return (r > -INFINITY && r < INFINITY) ? r : -INFINITY;
+}
+
 // Authoritative float32 score of one row (fixed order, see the file header).
 template <int J>
 __device__ __forceinline__ float row_score(const float4* __restrict__ rp, const float4 (&qv)[J],

@@ -41,6 +41,13 @@ constexpr int32_t kMfmaMinQueries = 4;
 enum class ScanPath { Auto, Gemv, Mfma };
 }  // namespace pvs
 
+// Deepen the certified caches of the active queries of a state to `depth`
+// ranks each (or to exhaustion) without emitting anything; a later pvs_next
+// is then served from the caches.  The host fusion calls it while the CPU
+// sparse channel of a round is still running, so the GPU works ahead.
+// `added` (optional) receives the number of ranks certified by the call.
+int pvs_fill(pvs_state* st, int64_t depth, const uint8_t* active, int64_t* added);
+
 // Process-wide profile hooks used by the host fusion (pvs_profile_enable).
 bool pvs_profile_on();
 void pvs_profile_add_host(double dense_ms, double sparse_ms, double fuse_ms);

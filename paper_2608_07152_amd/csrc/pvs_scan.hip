@@ -291,8 +291,8 @@ __global__ __launch_bounds__(256) void k_scan_mfma(
     }
 }
 
-// Wide batches (NQT = 4 or 8 tiles of 32 queries).  A persistent workgroup
-// of 4 wavefronts per CU takes 4 consecutive blocks at a time, one per
+// Wide batches (NQT = 4 or 8 tiles of 32 queries).  Persistent workgroups
+// of 4 wavefronts, two per CU, take 4 consecutive blocks at a time, one per
 // wavefront, and runs the K loop once per half of 4 query tiles (2 x 4
 // accumulators of 32 x 32).  The K loop has no branches: it advances PA steps
 // per stage (PA divides the step count), the A fragments of the next stage
@@ -310,7 +310,7 @@ __global__ __launch_bounds__(256) void k_scan_mfma(
 // left unused at the end hold the sentinel row -1, which the region's count
 // includes and rescoring skips.
 template <int NQT, int PA>
-__global__ __launch_bounds__(256, 1) void k_scan_mfma_wide(
+__global__ __launch_bounds__(256, 2) void k_scan_mfma_wide(
     const uint4* __restrict__ codes, const float* __restrict__ scale,
     const float* __restrict__ vnorm, const float* __restrict__ enorm,
     const uint64_t* __restrict__ vis, int64_t nblocks, int32_t nchunk,
@@ -319,6 +319,7 @@ __global__ __launch_bounds__(256, 1) void k_scan_mfma_wide(
     constexpr int NQS = 4;                     // tiles per half
     __shared__ v4i bsm[2][PA][NQS * 64];       // B fragments of two stages
     __shared__ float s_meta[4][3][64];         // scale (NaN if invisible), norm, error norm
+    __shared__ ScanQ s_q[NQT * 32];            // the scanning queries
     __shared__ int32_t s_wcnt[4][NQS * 32];    // per wave counts, then offsets
     __shared__ int32_t s_pos[NQT * 32];        // next free slot of each query's chunk
     __shared__ int32_t s_end[NQT * 32];        // end of that chunk
@@ -326,7 +327,10 @@ __global__ __launch_bounds__(256, 1) void k_scan_mfma_wide(
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    for (int b = tid; b < NQT * 32; b += 256) s_pos[b] = s_end[b] = 0;
+    for (int b = tid; b < NQT * 32; b += 256) {
+        s_pos[b] = s_end[b] = 0;
+        if (b < nq) s_q[b] = sq[b];
+    }
     __syncthreads();
     const int nsteps = nchunk >> 1;            // a multiple of PA
     const int64_t ngroups = (nblocks + 3) / 4;
@@ -407,33 +411,47 @@ __global__ __launch_bounds__(256, 1) void k_scan_mfma_wide(
                 for (int p = 0; p < PA; ++p) bsm[cur ^ 1][p][tid] = bst[p];
                 __syncthreads();
             }
-            // candidate masks of this half; lanes l and l ^ 32 hold one query
+            // Candidate masks of this half; lanes l and l ^ 32 hold one query.
+            // Rows run outermost so a row's scale is read once for the 4
+            // tiles; the per-pair pre-test is one convert, one multiply and
+            // one compare against the block threshold divided by s_q (with a
+            // margin that covers the rounding of both products), and only
+            // pairs that pass it evaluate the exact interval.
             uint32_t mask[NQS];
             int other[NQS];
+            float thq[NQS];
 #pragma unroll
             for (int uu = 0; uu < NQS; ++uu) {
+                mask[uu] = 0;
                 const int b = 32 * (u0 + uu) + (lane & 31);
-                const bool valid = have && b < nq;
-                const ScanQ Q = sq[b < nq ? b : 0];
-                const float thr = block_threshold(Q, nvb, nevb, gamma);
-                uint32_t mk = 0;
+                thq[uu] = INFINITY;
+                if (have && b < nq) {
+                    const ScanQ& Q = s_q[b];
+                    thq[uu] = scaled_threshold(block_threshold(Q, nvb, nevb, gamma), Q.sq);
+                }
+            }
 #pragma unroll
-                for (int t = 0; t < 2; ++t) {
+            for (int t = 0; t < 2; ++t) {
 #pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const int rib = 32 * t + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-                        const float sv = s_meta[wave][0][rib];
-                        const float c = (Q.sq * sv) * static_cast<float>(acc[t][uu][r]);
-                        if (valid && c >= thr) {
+                for (int r = 0; r < 16; ++r) {
+                    const int rib = 32 * t + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                    const float sv = s_meta[wave][0][rib];   // NaN for invisible rows
+#pragma unroll
+                    for (int uu = 0; uu < NQS; ++uu) {
+                        if (sv * static_cast<float>(acc[t][uu][r]) >= thq[uu]) {
+                            const ScanQ& Q = s_q[32 * (u0 + uu) + (lane & 31)];
                             float lo, hi;
                             pair_interval(Q, sv, s_meta[wave][1][rib], s_meta[wave][2][rib],
                                           acc[t][uu][r], gamma, lo, hi);
-                            if (hi >= Q.tau && (!Q.has_cert || lo <= Q.s_cert)) mk |= 1u << (16 * t + r);
+                            if (hi >= Q.tau && (!Q.has_cert || lo <= Q.s_cert))
+                                mask[uu] |= 1u << (16 * t + r);
                         }
                     }
                 }
-                mask[uu] = mk;
-                const int mine = __popc(mk);
+            }
+#pragma unroll
+            for (int uu = 0; uu < NQS; ++uu) {
+                const int mine = __popc(mask[uu]);
                 other[uu] = __shfl_xor(mine, 32, 64);
                 if (lane < 32) s_wcnt[wave][32 * uu + lane] = mine + other[uu];
             }
@@ -454,7 +472,7 @@ __global__ __launch_bounds__(256, 1) void k_scan_mfma_wide(
                 int nb = 0;
                 if (tot > room) {
                     const int need = tot - room;
-                    const int64_t cap = sq[b].cand_cap;
+                    const int64_t cap = s_q[b].cand_cap;
                     const int64_t per = cap / (16 * static_cast<int64_t>(gridDim.x));
                     const int chunk = static_cast<int>(per < 1 ? 1 : per > kMaxChunk ? kMaxChunk : per);
                     const int take = need > chunk ? need : chunk;
@@ -474,7 +492,7 @@ __global__ __launch_bounds__(256, 1) void k_scan_mfma_wide(
                 for (int uu = 0; uu < NQS; ++uu) {
                     if (!mask[uu]) continue;
                     const int ql = 32 * uu + (lane & 31);
-                    const ScanQ Q = sq[32 * u0 + ql];
+                    const ScanQ& Q = s_q[32 * u0 + ql];
                     const int old = s_old[ql], room = s_room[ql], nb = s_new[ql];
                     int j = s_wcnt[wave][ql] + ((lane >= 32) ? other[uu] : 0);
 #pragma unroll
@@ -533,18 +551,12 @@ static void mfma_pass(const IndexView& ix, const uint64_t* vis, int64_t nblocks,
                            gamma, o);
     } else if (NQT >= 4) {
         constexpr int W = NQT >= 4 ? NQT : 4;
+        // two workgroups per CU (256 registers per lane each): one's epilogue
+        // and barriers overlap the other's MFMA work
         const int64_t groups = (nblocks + 3) / 4;
-        const uint32_t g = static_cast<uint32_t>(std::min<int64_t>(groups, cu_count()));
+        const uint32_t g = static_cast<uint32_t>(std::min<int64_t>(groups, 2 * cu_count()));
         const int nsteps = ix.nchunk / 2;
-        if (nsteps % 8 == 0)
-            hipLaunchKernelGGL((k_scan_mfma_wide<W, 8>), dim3(g), dim3(256), 0, stream, ix.codes,
-                               ix.scale, ix.vnorm, ix.enorm, vis, nblocks, ix.nchunk, qfrag, sq, nq,
-                               gamma, o);
-        else if (nsteps % 4 == 0)
-            hipLaunchKernelGGL((k_scan_mfma_wide<W, 4>), dim3(g), dim3(256), 0, stream, ix.codes,
-                               ix.scale, ix.vnorm, ix.enorm, vis, nblocks, ix.nchunk, qfrag, sq, nq,
-                               gamma, o);
-        else if (nsteps % 2 == 0)
+        if (nsteps % 2 == 0)
             hipLaunchKernelGGL((k_scan_mfma_wide<W, 2>), dim3(g), dim3(256), 0, stream, ix.codes,
                                ix.scale, ix.vnorm, ix.enorm, vis, nblocks, ix.nchunk, qfrag, sq, nq,
                                gamma, o);
