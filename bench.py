@@ -16,12 +16,24 @@ queries (value = queries/s); batches of 1 (distinct queries of the 200-query
 single-request set, one per step) and 64 are timed in the same run and
 reported under ``per_batch``.
 
-``roofline`` is for the dominant kernel, the full interval scan of the
-headline batch: algorithmic bytes per launch, N (d + 12) + 8 N / 64, divided by
-its average launch time measured with HIP events on the library's stream.
+Kernel times come from HIP events the library records on its own stream
+around each kernel class of every scan round, inside the timed region.
+``kernels`` lists every class with its algorithmic bytes and rate:
+  * scan variants: N (d + 12) + 8 N / 64 bytes per launch (codes, three
+    per-row floats, visibility bits), independent of the batch;
+  * rescore: (4 d + 20) bytes per candidate (its float32 row, the candidate's
+    row / lo / hi, the key written);
+and ``roofline`` is the class with the most time in the headline batch
+(HBM-bound: achieved GB/s against 8 TB/s), ``roofline_scan`` the dominant
+scan variant.  ``traffic`` is filled from the committed PMC summary of that
+kernel (FETCH_SIZE + WRITE_SIZE per launch, scaled by the same counters on a
+plain device copy) when its source is unchanged since, else null.
 ``cpu_baseline`` times the CPU oracle (exhaustive float64 dense ranking, brute
 force sparse ranking, exact complete-list RRF) on a few queries of the
 headline batch and checks their Top-20.
+
+``--copy-calibration MB`` only runs a device-to-device copy of MB MiB ten
+times (the reference kernel for the PMC byte counters) and exits.
 """
 from __future__ import annotations
 
@@ -56,7 +68,59 @@ def parse():
     ap.add_argument("--range-size", type=int, default=4096)
     ap.add_argument("--cpu-queries", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MB")
     return ap.parse_args()
+
+
+# committed PMC summaries: kernel class -> (file, sources whose hash it records)
+TRAFFIC_FILES = {
+    "rescore": ("profiles/k_rescore_passage_b256_traffic.txt", ["paper_2608_07152_amd/csrc/pvs_rank.hip"]),
+    "k_scan_mfma<8>": ("profiles/k_scan_mfma_wide_passage_b256_traffic.txt",
+                       ["paper_2608_07152_amd/csrc/pvs_scan.hip"]),
+    "k_scan_gemv<1>": ("profiles/k_scan_gemv1_passage_b1_traffic.txt",
+                       ["paper_2608_07152_amd/csrc/pvs_scan.hip"]),
+}
+
+
+def sources_sha(paths):
+    import hashlib
+    h = hashlib.sha256()
+    for p in paths:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def traffic_for(kernel):
+    """HBM bytes per launch from the committed PMC summary, or None when
+    there is none or the kernel's source changed since it was taken."""
+    if kernel not in TRAFFIC_FILES:
+        return None
+    path, srcs = TRAFFIC_FILES[kernel]
+    full = os.path.join(ROOT, path)
+    if not os.path.exists(full):
+        return None
+    vals = {}
+    with open(full) as f:
+        for line in f:
+            if ":" in line:
+                k, v = line.split(":", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("source_sha256") != sources_sha(srcs) or "traffic_bytes_per_launch" not in vals:
+        return None
+    return float(vals["traffic_bytes_per_launch"])
+
+
+def copy_calibration(mb):
+    import torch
+    n = mb * (1 << 20) // 4
+    a = torch.ones(n, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    for _ in range(10):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n, "copies": 10}), flush=True)
 
 
 def cpu_baseline(x, post, q, qs, K, wts, n_queries):
@@ -83,6 +147,17 @@ def cpu_baseline(x, post, q, qs, K, wts, n_queries):
     return out, el, blas
 
 
+def roofline_of(name, k):
+    """HBM roofline of one kernel class over the timed region."""
+    launches = max(1, k["launches"])
+    avg_ms = k["ms"] / launches
+    bpl = k["bytes"] / launches
+    achieved = bpl / (avg_ms * 1e-3) / 1e9 if avg_ms > 0 else 0.0
+    return {"bound": "hbm", "kernel": name, "achieved": achieved, "peak": HBM_PEAK_GBS,
+            "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic_for(name),
+            "avg_launch_ms": avg_ms, "launches": k["launches"], "bytes_per_launch": bpl}
+
+
 def query_set_for(w, batch):
     if w.name != "passage":
         return "default"
@@ -95,6 +170,9 @@ def main():
         print("bench.py: this build runs on one GPU; --gpus N with N > 1 is not supported",
               file=sys.stderr)
         sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
     import numpy as np
     import torch
 
@@ -179,6 +257,21 @@ def main():
         achieved = bpl / (avg_ms * 1e-3) / 1e9 if avg_ms > 0 else 0.0
         variants = {eahr.pvs_profile.VARIANTS[i]: {"ms": vms[i], "launches": prof["variant_launches"][i]}
                     for i in range(len(vms)) if prof["variant_launches"][i]}
+        # every kernel class with its algorithmic bytes
+        kernels = {}
+        for i, name in enumerate(eahr.pvs_profile.VARIANTS):
+            if prof["variant_launches"][i]:
+                ms, n = vms[i], prof["variant_launches"][i]
+                kernels[name] = {"ms": ms, "launches": n, "bytes": prof["variant_bytes"][i],
+                                 "gbs": prof["variant_bytes"][i] / (ms * 1e-3) / 1e9 if ms > 0 else 0.0}
+        if prof["scan_rounds"]:
+            rb = prof["rescore_rows"] * (4 * w.d + 20)
+            ms = prof["rescore_ms"]
+            kernels["rescore"] = {"ms": ms, "launches": prof["scan_rounds"], "bytes": rb,
+                                  "gbs": rb / (ms * 1e-3) / 1e9 if ms > 0 else 0.0}
+        dom = max(kernels, key=lambda k: kernels[k]["ms"])
+        kernels["sort_pack"] = {"ms": prof["sort_ms"], "launches": prof["scan_rounds"]}
+        kernels["sample_select"] = {"ms": prof["sample_ms"], "launches": prof["scan_rounds"]}
         stats = [s for r in res for s in r[3]]
         dd = np.array([s["dense_depth"] for s in stats])
         out = {
@@ -187,6 +280,7 @@ def main():
             "scan_kernel": eahr.pvs_profile.VARIANTS[v],
             "scan_gbs": achieved, "scan_frac": achieved / HBM_PEAK_GBS, "scan_avg_launch_ms": avg_ms,
             "scan_launches": launches, "scan_bytes_per_launch": bpl, "scan_variants": variants,
+            "kernels": kernels, "dominant": dom,
             "kernel_ms": {"scan": prof["scan_ms"], "sample_select": prof["sample_ms"],
                           "rescore": prof["rescore_ms"], "sort_pack": prof["sort_ms"]},
             "rescored_rows": prof["rescore_rows"],
@@ -220,11 +314,8 @@ def main():
         "config": {"workload": f"{w.name} N={w.n} d={w.d} batch={args.batch} K={K} k=60 "
                                f"weights={wts[0]}:{wts[1]}",
                    "global_batch": args.batch, "parallelism": "single GPU"},
-        "roofline": {"bound": "hbm", "kernel": head["scan_kernel"], "achieved": head["scan_gbs"],
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": head["scan_frac"],
-                     "traffic": None, "avg_launch_ms": head["scan_avg_launch_ms"],
-                     "launches": head["scan_launches"],
-                     "bytes_per_launch": head["scan_bytes_per_launch"]},
+        "roofline": roofline_of(head["dominant"], head["kernels"][head["dominant"]]),
+        "roofline_scan": roofline_of(head["scan_kernel"], head["kernels"][head["scan_kernel"]]),
         "per_batch": per_batch,
     }
     if not args.no_cpu_baseline:
