@@ -398,7 +398,16 @@ static void free_buffers(ScanBuffers& b) {
 }
 
 // Per-query scan buffers for nq queries and samples of sample_ld rows.
-// counts layout: [cand nq][cert nq][fail nq][offs nq + 1]
+// counts layout: [total nq][cert nq][fail nq][offs nq + 1][need nq], then
+// from sub_counts_at(nq) the append counters of the candidate sub-regions,
+// nq * kSub of them, kCntStride ints apart.  h_counts mirrors the first
+// 5 nq + 1 entries.
+static size_t host_counts(int32_t nq) { return 5 * static_cast<size_t>(nq) + 1; }
+static size_t sub_counts_at(int32_t nq) { return (host_counts(nq) + 63) / 64 * 64; }
+static size_t all_counts(int32_t nq) {
+    return sub_counts_at(nq) + static_cast<size_t>(nq) * pvs::kSub * pvs::kCntStride;
+}
+
 static int ensure_query_buffers(pvs_state* st, int32_t nq, int64_t sample_ld) {
     if (nq <= st->buf_nq && sample_ld <= st->buf_sample) return EAHR_OK;
     nq = std::max(nq, st->buf_nq);
@@ -414,15 +423,14 @@ static int ensure_query_buffers(pvs_state* st, int32_t nq, int64_t sample_ld) {
     st->h_scanq = nullptr;
     st->h_counts = nullptr;
     EAHR_TRY(dev_alloc(&st->scanq, nq));
-    EAHR_TRY(dev_alloc(&st->counts, 4 * static_cast<size_t>(nq) + 1));
+    EAHR_TRY(dev_alloc(&st->counts, all_counts(nq)));
     EAHR_TRY(dev_alloc(&st->sample_lo, static_cast<size_t>(nq) * sample_ld));
     EAHR_TRY(dev_alloc(&st->sample_hi, static_cast<size_t>(nq) * sample_ld));
     int8_t* f;
     EAHR_TRY(dev_alloc(&f, static_cast<size_t>(st->ix->dp / 32) * 8 * 64 * 16));
     st->qfrag = f;
     HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&st->h_scanq), nq * sizeof(ScanQ)));
-    HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&st->h_counts),
-                          (4 * static_cast<size_t>(nq) + 1) * sizeof(int32_t)));
+    HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&st->h_counts), host_counts(nq) * sizeof(int32_t)));
     st->buf_nq = nq;
     st->buf_sample = sample_ld;
     return EAHR_OK;
@@ -748,20 +756,24 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     //    Queries past the pool limit wait for the next round (kept in todo).
     int64_t total = 0;
     int32_t run = 0;
+    const int64_t max_sub = round_up(st->n_rows, 64);
     for (; run < nq; ++run) {
         ScanQ& sq = st->h_scanq[run];
         const auto& Q = st->q[todo[run]];
         // exact count when the sample saw every block, plus room for the
         // unused tails of per-workgroup slices (at most cap / 16)
-        int64_t cap = (stride == 1)
+        const int64_t cap = (stride == 1)
                           ? static_cast<int64_t>(sq.sample_hits) + sq.sample_hits / 8 + 64
                           : static_cast<int64_t>(std::ceil(sq.sample_hits / frac * pvs::kCapSlack)) + pvs::kCapPad;
-        cap = std::max(cap, Q.cap_hint);
-        cap = std::min<int64_t>(std::max<int64_t>(cap, 1), st->n_rows);
-        if (run > 0 && total + cap > pvs::kPoolMax) break;
+        // per sub-region, with room for an uneven split
+        int64_t sub = (cap + pvs::kSub - 1) / pvs::kSub;
+        sub += sub / 4 + 16;
+        sub = std::max(sub, Q.cap_hint);
+        sub = std::min(sub, max_sub);
+        if (run > 0 && total + sub * pvs::kSub > pvs::kPoolMax) break;
         sq.cand_off = total;
-        sq.cand_cap = cap;
-        total += cap;
+        sq.cand_cap = sub;
+        total += sub * pvs::kSub;
     }
     std::vector<int32_t> later(todo.begin() + run, todo.end());
     todo.resize(run);
@@ -772,32 +784,36 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     int32_t* d_cert = st->counts + nq;
     int32_t* d_fail = st->counts + 2 * nq;
     int32_t* d_offs = st->counts + 3 * nq;
-    HIP_TRY(hipMemsetAsync(st->counts, 0, (4 * static_cast<size_t>(nq) + 1) * sizeof(int32_t), s));
+    int32_t* d_need = st->counts + 4 * nq + 1;
+    int32_t* d_sub = st->counts + sub_counts_at(nq);
+    HIP_TRY(hipMemsetAsync(st->counts, 0, all_counts(nq) * sizeof(int32_t), s));
     pvs::ScanOut mo;
     mo.cand_row = st->cand_row;
     mo.cand_lo = st->cand_lo;
     mo.cand_hi = st->cand_hi;
-    mo.cand_cnt = d_cand;
+    mo.cand_cnt = d_sub;
     EAHR_TRY(mark(2));
     scan(false, mo, nq);
     EAHR_TRY(mark(3));
+    pvs::launch_cand_totals(d_sub, st->scanq, nq, d_cand, d_need, s);
     HIP_TRY(hipGetLastError());
-    HIP_TRY(hipMemcpyAsync(st->h_counts, d_cand, nq * sizeof(int32_t), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipMemcpyAsync(st->h_counts, st->counts, host_counts(nq) * sizeof(int32_t),
+                           hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
+    const std::vector<int32_t> need(st->h_counts + 4 * nq + 1, st->h_counts + 5 * nq + 1);
     st->stats.scans += 1;
     st->stats.sample_scans += 1;
     st->stats.rows_scanned += nblocks * 64;
     st->stats.bytes_scanned += st->n_rows * (static_cast<int64_t>(ix->d) + 12) + nblocks * 8;
 
     // 3. rescore, order and pack the certified ranks
-    std::vector<int32_t> cand(st->h_counts, st->h_counts + nq);
+    std::vector<int32_t> cand(st->h_counts, st->h_counts + nq);   // kept candidates
     int64_t max_cnt = 0, kept = 0;
     for (int32_t i = 0; i < nq; ++i) {
-        const int64_t c = std::min<int64_t>(cand[i], st->h_scanq[i].cand_cap);
-        max_cnt = std::max(max_cnt, c);
-        kept += c;
+        max_cnt = std::max<int64_t>(max_cnt, cand[i]);
+        kept += cand[i];
     }
-    pvs::launch_rescore(v, st->qrows, st->scanq, nq, st->cand_row, st->cand_lo, st->cand_hi, d_cand,
+    pvs::launch_rescore(v, st->qrows, st->scanq, nq, st->cand_row, st->cand_lo, st->cand_hi, d_sub,
                         max_cnt, st->keys, d_cert, d_fail, s);
     EAHR_TRY(mark(4));
     uint64_t* sorted = pvs::launch_segmented_sort(st->keys, st->keys_tmp, d_cand, st->scanq, nq, max_cnt, s);
@@ -848,7 +864,7 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     std::vector<uint8_t> usable(nq, 0);
     for (int32_t i = 0; i < nq; ++i) {
         auto& Q = st->q[todo[i]];
-        usable[i] = !h_fail[i] && cand[i] <= st->h_scanq[i].cand_cap;
+        usable[i] = !h_fail[i] && need[i] <= st->h_scanq[i].cand_cap;
         old_size[i] = static_cast<int64_t>(Q.cache_id.size());
         if (usable[i]) {
             Q.cache_id.resize(old_size[i] + h_cert[i]);
@@ -874,8 +890,8 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
             Q.failed = true;
             continue;
         }
-        if (cand[i] > st->h_scanq[i].cand_cap) {   // region overflowed: redo with room for all
-            Q.cap_hint = static_cast<int64_t>(cand[i]) + cand[i] / 4 + 256;
+        if (need[i] > st->h_scanq[i].cand_cap) {   // a sub-region overflowed: redo with room for all
+            Q.cap_hint = static_cast<int64_t>(need[i]) + need[i] / 4 + 64;
             keep.push_back(b);
             continue;
         }

@@ -12,6 +12,12 @@ constexpr int kSortTile = 2048;    // keys sorted per workgroup in LDS
 constexpr int kMaxGemvQueries = 8; // queries per GEMV scan pass
 constexpr int kMaxMfmaQueries = 256;  // queries per MFMA scan pass (8 tiles of 32)
 constexpr int kMaxChunk = 256;     // largest slice of a candidate region one workgroup reserves
+// A query's candidate region is split into kSub sub-regions, each with its
+// own append counter; the code block (or workgroup) picks the sub-region
+// from its index, so concurrent appends of one query hit kSub different
+// counters instead of one.  Counters sit kCntStride ints (64 bytes) apart.
+constexpr int kSub = 64;
+constexpr int kCntStride = 16;
 
 // Per scanning query, uploaded before every scan.  All fields are read
 // uniformly by a wavefront (scalar loads).
@@ -30,7 +36,7 @@ struct ScanQ {
     float wmax;        // upper bound of E + G over every row of the index
     int32_t sample_hits;  // sampled eligible rows with hi >= tau (select pass)
     int64_t cand_off;  // first slot of this query's candidate region
-    int64_t cand_cap;  // slots in the region
+    int64_t cand_cap;  // slots in each of its kSub sub-regions
 };
 static_assert(sizeof(ScanQ) == 64, "ScanQ layout");
 
@@ -55,11 +61,11 @@ void launch_quantize(const float* src, int64_t nrows, int32_t d, int64_t src_str
 
 // Outputs of a scan pass.  Sample pass: lower and upper bounds of every
 // (query, row) pair of the sampled blocks, row-major [query][sample_ld],
-// -inf / -inf for ineligible rows.  Main pass: candidates of query b go to
-// slots cand_off .. cand_off + cand_cap - 1 of its ScanQ; cand_cnt[b] counts
-// every slot handed out, including those past the region.  A slot may hold
-// the sentinel row -1 (part of a reserved slice left unused), which is no
-// candidate.
+// -inf / -inf for ineligible rows.  Main pass: the candidates query b appends
+// to sub-region s go to slots cand_off + s * cand_cap + j, j < cand_cap, and
+// cand_cnt[(b * kSub + s) * kCntStride] counts every slot of sub-region s
+// handed out, including those past its end.  A slot may hold the sentinel
+// row -1 (part of a reserved slice left unused), which is no candidate.
 struct ScanOut {
     float* sample_lo = nullptr;
     float* sample_hi = nullptr;
@@ -87,13 +93,22 @@ int mfma_tiles_for(int32_t nq);
 void launch_select(const float* sample_lo, const float* sample_hi, int64_t n, int64_t ld,
                    ScanQ* sq, int32_t nq, hipStream_t stream);
 
+// Per query: total[b] = sum over sub-regions of min(count, cand_cap) (the
+// candidates kept), need[b] = the largest sub-region count (a sub-region
+// overflowed when need[b] > cand_cap).
+void launch_cand_totals(const int32_t* sub_cnt, const ScanQ* sq, int32_t nq, int32_t* total,
+                        int32_t* need, hipStream_t stream);
+
+// Rescoring reads the kept candidates of every sub-region of a query in
+// sub-region order and writes their keys densely: key i of query b goes to
+// keys[cand_off + i], i < total[b].
 void launch_rescore(const IndexView& ix, const float* qrows, const ScanQ* sq, int32_t nq,
                     const int32_t* cand_row, const float* cand_lo, const float* cand_hi,
-                    const int32_t* cand_cnt, int64_t max_cnt, uint64_t* keys, int32_t* cert_cnt,
+                    const int32_t* sub_cnt, int64_t max_cnt, uint64_t* keys, int32_t* cert_cnt,
                     int32_t* fail, hipStream_t stream);
 
-// Sorts every query's candidate keys (its region, min(cnt, cap) entries)
-// ascending; returns the buffer holding the result (keys or tmp).
+// Sorts every query's candidate keys (cnt[b] keys from cand_off) ascending;
+// returns the buffer holding the result (keys or tmp).
 uint64_t* launch_segmented_sort(uint64_t* keys, uint64_t* tmp, const int32_t* cnt,
                                 const ScanQ* sq, int32_t nq, int64_t max_cnt, hipStream_t stream);
 

@@ -11,20 +11,39 @@
 
 namespace pvs {
 
-// One wavefront per candidate; grid.y = query.
+// One wavefront per candidate; grid.y = query.  Candidate i of the query
+// (sub-region order) lives in sub-region s with first[s] <= i < last[s]:
+// lane s holds first[s] and last[s] (a prefix sum of the kept counts), and a
+// ballot finds s.
 template <int J>
 __global__ __launch_bounds__(256) void k_rescore(
     const float4* __restrict__ rows, int32_t df4, const float4* __restrict__ qrows,
     const ScanQ* __restrict__ sq, const int32_t* __restrict__ cand_row,
     const float* __restrict__ cand_lo, const float* __restrict__ cand_hi,
-    const int32_t* __restrict__ cand_cnt, uint64_t* __restrict__ keys,
+    const int32_t* __restrict__ sub_cnt, uint64_t* __restrict__ keys,
     int32_t* __restrict__ cert_cnt, int32_t* __restrict__ fail) {
+    static_assert(kSub == 64, "one lane per sub-region");
     const int lane = threadIdx.x & 63;
     const int b = blockIdx.y;
     const ScanQ Q = sq[b];
     float4 qv[J];
     load_query_row<J>(qrows, Q.qi, df4, lane, qv);
-    const int64_t n = min(static_cast<int64_t>(cand_cnt[b]), Q.cand_cap);
+    const int c = sub_cnt[(b * kSub + lane) * kCntStride];
+    const int kept = static_cast<int>(c < Q.cand_cap ? c : Q.cand_cap);
+    int last = kept;
+    for (int off = 1; off < 64; off <<= 1) {
+        const int t = __shfl_up(last, off, 64);
+        if (lane >= off) last += t;
+    }
+    const int first = last - kept;
+    const int64_t n = __builtin_amdgcn_readlane(last, 63);
+    // slot of candidate i (uniform across the wavefront)
+    auto slot_of = [&](int64_t i) -> int64_t {
+        const uint64_t m = __ballot(first <= i && i < last);
+        const int s = __ffsll(static_cast<unsigned long long>(m)) - 1;
+        const int f = __builtin_amdgcn_readlane(first, s);
+        return Q.cand_off + static_cast<int64_t>(s) * Q.cand_cap + (i - f);
+    };
     int local_cert = 0;
     // R candidates per wavefront iteration keep R * J 16-byte loads in flight
     constexpr int R = (J <= 4) ? 4 : 1;
@@ -33,11 +52,13 @@ __global__ __launch_bounds__(256) void k_rescore(
     const int64_t stride = static_cast<int64_t>(gridDim.x) * 4 * R;
     for (int64_t i0 = wave * R; i0 < n; i0 += stride) {
         int32_t row[R];
+        int64_t src[R];
         float4 v[R][J];
 #pragma unroll
         for (int k = 0; k < R; ++k) {
             const int64_t i = i0 + k;
-            row[k] = (i < n) ? cand_row[Q.cand_off + i] : -1;
+            src[k] = (i < n) ? slot_of(i) : 0;
+            row[k] = (i < n) ? cand_row[src[k]] : -1;
             const float4* rp = rows + static_cast<int64_t>(row[k] < 0 ? 0 : row[k]) * df4;
 #pragma unroll
             for (int t = 0; t < J; ++t) {
@@ -68,8 +89,8 @@ __global__ __launch_bounds__(256) void k_rescore(
             const float s = acc;
             if (lane == 0) {
                 const int64_t at = Q.cand_off + i0 + k;
-                const float lo = cand_lo[at];
-                const float hi = cand_hi[at];
+                const float lo = cand_lo[src[k]];
+                const float hi = cand_hi[src[k]];
                 if (!(lo <= s && s <= hi)) fail[b] = 1;
                 const bool dropped =
                     Q.has_cert && (s > Q.s_cert || (s == Q.s_cert && row[k] <= Q.id_cert));
@@ -86,7 +107,7 @@ __global__ __launch_bounds__(256) void k_rescore(
 template <int J>
 static void rescore_j(const IndexView& ix, const float* qrows, const ScanQ* sq, int32_t nq,
                       const int32_t* cand_row, const float* cand_lo, const float* cand_hi,
-                      const int32_t* cand_cnt, int64_t max_cnt, uint64_t* keys, int32_t* cert_cnt,
+                      const int32_t* sub_cnt, int64_t max_cnt, uint64_t* keys, int32_t* cert_cnt,
                       int32_t* fail, hipStream_t stream) {
     int64_t gx = (max_cnt + 3) / 4;
     if (gx > 4096) gx = 4096;
@@ -94,17 +115,17 @@ static void rescore_j(const IndexView& ix, const float* qrows, const ScanQ* sq, 
     hipLaunchKernelGGL((k_rescore<J>), dim3(static_cast<uint32_t>(gx), nq), dim3(256), 0, stream,
                        reinterpret_cast<const float4*>(ix.rows), ix.df / 4,
                        reinterpret_cast<const float4*>(qrows), sq, cand_row, cand_lo, cand_hi,
-                       cand_cnt, keys, cert_cnt, fail);
+                       sub_cnt, keys, cert_cnt, fail);
 }
 
 void launch_rescore(const IndexView& ix, const float* qrows, const ScanQ* sq, int32_t nq,
                     const int32_t* cand_row, const float* cand_lo, const float* cand_hi,
-                    const int32_t* cand_cnt, int64_t max_cnt, uint64_t* keys, int32_t* cert_cnt,
+                    const int32_t* sub_cnt, int64_t max_cnt, uint64_t* keys, int32_t* cert_cnt,
                     int32_t* fail, hipStream_t stream) {
     if (nq <= 0 || max_cnt <= 0) return;
 #define PVS_RS(N)                                                                              \
     case N:                                                                                    \
-        rescore_j<N>(ix, qrows, sq, nq, cand_row, cand_lo, cand_hi, cand_cnt, max_cnt, keys,   \
+        rescore_j<N>(ix, qrows, sq, nq, cand_row, cand_lo, cand_hi, sub_cnt, max_cnt, keys,    \
                      cert_cnt, fail, stream);                                                  \
         break;
     switch (row_chunks(ix.df)) {
@@ -129,7 +150,7 @@ __global__ __launch_bounds__(256) void k_sort_tiles(uint64_t* __restrict__ keys,
                                                     const ScanQ* __restrict__ sq) {
     __shared__ uint64_t s[kSortTile];
     const int b = blockIdx.y;
-    const int64_t n = min(static_cast<int64_t>(cnt[b]), sq[b].cand_cap);
+    const int64_t n = cnt[b];
     const int64_t base = static_cast<int64_t>(blockIdx.x) * kSortTile;
     if (base >= n) return;
     uint64_t* k = keys + sq[b].cand_off + base;
@@ -164,7 +185,7 @@ __global__ __launch_bounds__(256) void k_merge(const uint64_t* __restrict__ src,
                                                const int32_t* __restrict__ cnt,
                                                const ScanQ* __restrict__ sq, int64_t run) {
     const int b = blockIdx.y;
-    const int64_t n = min(static_cast<int64_t>(cnt[b]), sq[b].cand_cap);
+    const int64_t n = cnt[b];
     const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
     if (i >= n) return;
     const uint64_t* s = src + sq[b].cand_off;

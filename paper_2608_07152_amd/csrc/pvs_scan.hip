@@ -16,7 +16,7 @@ namespace pvs {
 // ------------------------------------------------------------------- GEMV
 // One wavefront per 64-row block (lane = row); QB queries per pass, their
 // codes read through scalar loads.  Appends use one atomic per wavefront and
-// query (ballot + prefix count).
+// query (ballot + prefix count) on the counter of sub-region blk % kSub.
 template <int QB, bool SAMPLE>
 __global__ __launch_bounds__(256) void k_scan_gemv(
     const uint4* __restrict__ codes, const float* __restrict__ scale,
@@ -71,14 +71,16 @@ __global__ __launch_bounds__(256) void k_scan_gemv(
             const bool take = elig && hi >= Q.tau;
             const uint64_t mask = __ballot(take);
             if (mask) {
+                const int sub = static_cast<int>(blk & (kSub - 1));
                 const int leader = __ffsll(static_cast<unsigned long long>(mask)) - 1;
                 int base = 0;
-                if (lane == leader) base = atomicAdd(&o.cand_cnt[b], __popcll(mask));
+                if (lane == leader)
+                    base = atomicAdd(&o.cand_cnt[(b * kSub + sub) * kCntStride], __popcll(mask));
                 base = __shfl(base, leader, 64);
                 if (take) {
                     const int64_t pos = base + __popcll(mask & ((1ull << lane) - 1ull));
                     if (pos < Q.cand_cap) {
-                        const int64_t at = Q.cand_off + pos;
+                        const int64_t at = Q.cand_off + sub * Q.cand_cap + pos;
                         o.cand_row[at] = static_cast<int32_t>(row);
                         o.cand_lo[at] = lo;
                         o.cand_hi[at] = hi;
@@ -110,7 +112,7 @@ static ScanOut shift_out(const ScanOut& o, int32_t q0) {
     ScanOut s = o;
     if (s.sample_lo) s.sample_lo += q0 * o.sample_ld;
     if (s.sample_hi) s.sample_hi += q0 * o.sample_ld;
-    if (s.cand_cnt) s.cand_cnt += q0;
+    if (s.cand_cnt) s.cand_cnt += static_cast<int64_t>(q0) * kSub * kCntStride;
     return s;
 }
 
@@ -234,7 +236,6 @@ __global__ __launch_bounds__(256) void k_scan_mfma(
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int rib = 32 * t + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-                    const int64_t row = blk * 64 + rib;
                     float lo, hi;
                     pair_interval(Q, svr[t][r], vnr[t][r], enr[t][r], acc[t][uu][r], gamma, lo, hi);
                     const bool elig = ((vbits >> rib) & 1ull) && (!Q.has_cert || lo <= Q.s_cert);
@@ -252,7 +253,6 @@ __global__ __launch_bounds__(256) void k_scan_mfma(
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const int rib = 32 * t + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-                const int64_t row = blk * 64 + rib;
                 const float sv = svr[t][r];
                 const float c = (Q.sq * sv) * static_cast<float>(acc[t][uu][r]);
                 if (valid && c >= thr && ((vbits >> rib) & 1ull)) {
@@ -264,8 +264,10 @@ __global__ __launch_bounds__(256) void k_scan_mfma(
         }
         const int mine = __popc(mask);
         const int other = __shfl_xor(mine, 32, 64);
+        const int sub = static_cast<int>(blk & (kSub - 1));
         int base = 0;
-        if (lane < 32 && mine + other > 0) base = atomicAdd(&o.cand_cnt[b], mine + other);
+        if (lane < 32 && mine + other > 0)
+            base = atomicAdd(&o.cand_cnt[(b * kSub + sub) * kCntStride], mine + other);
         base = __shfl(base, lane & 31, 64);
         if (!mask) continue;
         int64_t pos = base + ((lane >= 32) ? other : 0);
@@ -279,7 +281,7 @@ __global__ __launch_bounds__(256) void k_scan_mfma(
                 if (pos < Q.cand_cap) {
                     float lo, hi;
                     pair_interval(Q, svr[t][r], vnr[t][r], enr[t][r], acc[t][uu][r], gamma, lo, hi);
-                    const int64_t at = Q.cand_off + pos;
+                    const int64_t at = Q.cand_off + sub * Q.cand_cap + pos;
                     o.cand_row[at] = static_cast<int32_t>(row);
                     o.cand_lo[at] = lo;
                     o.cand_hi[at] = hi;
@@ -305,10 +307,10 @@ __global__ __launch_bounds__(256) void k_scan_mfma(
 // per-block bound of E + G (from the block's largest norms) gives a centre
 // threshold below which no row of the block can reach tau; invisible rows
 // carry a NaN scale so they fail it.  Candidates are appended through chunks
-// of each query's region that the workgroup reserves with one global atomic
-// per chunk (per-wave atomics on B hot counters serialise); slots of a chunk
-// left unused at the end hold the sentinel row -1, which the region's count
-// includes and rescoring skips.
+// of sub-region blockIdx.x % kSub of each query's region that the workgroup
+// reserves with one global atomic per chunk; slots of a chunk left unused at
+// the end hold the sentinel row -1, which the sub-region's count includes and
+// rescoring skips.
 template <int NQT, int PA>
 __global__ __launch_bounds__(256, 2) void k_scan_mfma_wide(
     const uint4* __restrict__ codes, const float* __restrict__ scale,
@@ -327,6 +329,9 @@ __global__ __launch_bounds__(256, 2) void k_scan_mfma_wide(
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
+    const int sub = static_cast<int>(blockIdx.x & (kSub - 1));
+    // workgroups sharing one sub-region
+    const int64_t wg_per_sub = (static_cast<int64_t>(gridDim.x) + kSub - 1) / kSub;
     for (int b = tid; b < NQT * 32; b += 256) {
         s_pos[b] = s_end[b] = 0;
         if (b < nq) s_q[b] = sq[b];
@@ -473,10 +478,10 @@ __global__ __launch_bounds__(256, 2) void k_scan_mfma_wide(
                 if (tot > room) {
                     const int need = tot - room;
                     const int64_t cap = s_q[b].cand_cap;
-                    const int64_t per = cap / (16 * static_cast<int64_t>(gridDim.x));
+                    const int64_t per = cap / (16 * wg_per_sub);
                     const int chunk = static_cast<int>(per < 1 ? 1 : per > kMaxChunk ? kMaxChunk : per);
                     const int take = need > chunk ? need : chunk;
-                    nb = atomicAdd(&o.cand_cnt[b], take);
+                    nb = atomicAdd(&o.cand_cnt[(b * kSub + sub) * kCntStride], take);
                     s_pos[b] = nb + need;
                     s_end[b] = nb + take;
                 } else {
@@ -507,7 +512,7 @@ __global__ __launch_bounds__(256, 2) void k_scan_mfma_wide(
                                 float lo, hi;
                                 pair_interval(Q, s_meta[wave][0][rib], s_meta[wave][1][rib],
                                               s_meta[wave][2][rib], acc[t][uu][r], gamma, lo, hi);
-                                const int64_t at = Q.cand_off + pos;
+                                const int64_t at = Q.cand_off + sub * Q.cand_cap + pos;
                                 o.cand_row[at] = static_cast<int32_t>(row);
                                 o.cand_lo[at] = lo;
                                 o.cand_hi[at] = hi;
@@ -524,7 +529,7 @@ __global__ __launch_bounds__(256, 2) void k_scan_mfma_wide(
     for (int b = tid; b < NQT * 32 && b < nq; b += 256) {
         const ScanQ Q = sq[b];
         const int64_t e = s_end[b] < Q.cand_cap ? s_end[b] : Q.cand_cap;
-        for (int64_t p = s_pos[b]; p < e; ++p) o.cand_row[Q.cand_off + p] = -1;
+        for (int64_t p = s_pos[b]; p < e; ++p) o.cand_row[Q.cand_off + sub * Q.cand_cap + p] = -1;
     }
 }
 
@@ -601,6 +606,35 @@ void launch_scan_mfma(const IndexView& ix, const uint64_t* vis, int64_t nblocks,
         }
 #undef PVS_MFMA_CASE
     }
+}
+
+// ------------------------------------------------------ candidate totals
+// One wavefront per query, lane s reads the counter of sub-region s.
+__global__ __launch_bounds__(64) void k_cand_totals(const int32_t* __restrict__ sub_cnt,
+                                                    const ScanQ* __restrict__ sq,
+                                                    int32_t* __restrict__ total,
+                                                    int32_t* __restrict__ need) {
+    static_assert(kSub == 64, "one lane per sub-region");
+    const int b = blockIdx.x;
+    const int lane = threadIdx.x;
+    const int c = sub_cnt[(b * kSub + lane) * kCntStride];
+    const int64_t cap = sq[b].cand_cap;
+    int kept = static_cast<int>(c < cap ? c : cap);
+    int mx = c;
+    for (int off = 32; off > 0; off >>= 1) {
+        kept += __shfl_xor(kept, off, 64);
+        mx = max(mx, __shfl_xor(mx, off, 64));
+    }
+    if (lane == 0) {
+        total[b] = kept;
+        need[b] = mx;
+    }
+}
+
+void launch_cand_totals(const int32_t* sub_cnt, const ScanQ* sq, int32_t nq, int32_t* total,
+                        int32_t* need, hipStream_t stream) {
+    if (nq <= 0) return;
+    hipLaunchKernelGGL(k_cand_totals, dim3(nq), dim3(64), 0, stream, sub_cnt, sq, total, need);
 }
 
 // ------------------------------------------------------------ threshold
