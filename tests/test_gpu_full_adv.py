@@ -1,0 +1,73 @@
+"""Parity on anti-correlated lists at full size: N = 2,000,000 rows of
+d = 768, 100 queries whose sparse ranking reverses the dense one (the
+controlled rank streams of Sec. 3.4 / 4.2 with real channels).  Neither list
+can be cut short (Sec. 2.2), so every query exhausts both, and pvs_next must
+emit the complete exact 2M-entry dense ranking (Sec. 2.1, 2.3.1)."""
+import time
+
+import numpy as np
+import pytest
+
+from paper_2608_07152_amd import datagen
+
+from full_common import K, check_query, load_library, note
+from gpu_helpers import check_dense_prefix, row_norms64, scores64
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def E():
+    return load_library()
+
+
+@pytest.fixture(scope="module")
+def adv(E):
+    t = time.time()
+    w = datagen.workload("adv")
+    x, _ = datagen.corpus(w)
+    q, _ = datagen.queries(w)
+    post, qs = datagen.adversarial_postings(w, x, q)
+    idx = E.pvs_build(x)
+    pbm = E.pbm_build(post.term_ptr, post.doc, post.impact, w.n, 4096)
+    vn = row_norms64(x)
+    note(f"adversarial set up in {time.time() - t:.1f}s")
+    yield w, x, vn, q, post, qs, idx, pbm
+    idx.free()
+    pbm.free()
+
+
+def test_adversarial_topk_exhausts_both_lists(E, adv):
+    w, x, vn, q, post, qs, idx, pbm = adv
+    t = time.time()
+    ids, cnt, stt, stats = E.eahr_topk(idx, pbm, q, qs, K=K)
+    note(f"adversarial eahr_topk on {len(q)} queries: {time.time() - t:.2f}s")
+    assert np.all(stt == 0) and np.all(cnt == K)
+    for s in stats:
+        assert s["dense_status"] == E.LIST_EXHAUSTED and s["sparse_status"] == E.LIST_EXHAUSTED
+        assert s["dense_depth"] == w.n and s["sparse_depth"] == w.n
+    for b in (0, 99):
+        check_query(E, idx, x, vn, post, q[b], qs[b], ids[b], stats[b], (1, 1))
+
+
+def test_adversarial_complete_dense_ranking(E, adv):
+    """The complete 2M-entry ranking, in one call and split over calls
+    (bit-identical), against the oracle's full sort."""
+    w, x, vn, q, post, qs, idx, pbm = adv
+    for b in (17, 64):
+        s64 = scores64(q[b], x)
+        st = E.pvs_open(idx, q[b:b + 1])
+        ids, scs, cnt, stt = E.pvs_next(st, w.n)
+        st.close()
+        assert cnt[0] == w.n and stt[0] == E.LIST_EXHAUSTED
+        check_dense_prefix(q[b], x, ids[0], scs[0], s64=s64, vn=vn)
+        st2 = E.pvs_open(idx, q[b:b + 1])
+        parts, scores = [], []
+        for m in (1000, 300_000, w.n):
+            i2, s2, c2, t2 = E.pvs_next(st2, m)
+            parts.append(i2[0, :c2[0]])
+            scores.append(s2[0, :c2[0]])
+        st2.close()
+        assert t2[0] == E.LIST_EXHAUSTED
+        assert np.array_equal(np.concatenate(parts), ids[0])
+        assert np.array_equal(np.concatenate(scores), scs[0])
