@@ -7,6 +7,8 @@
 #include <atomic>
 #include <chrono>
 #include <cstdint>
+#include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <memory>
 #include <new>
@@ -42,6 +44,17 @@ using ::eahr::parallel_for;
 // share of its queries still to finish).
 constexpr int64_t kFillMaxDepth = int64_t(1) << 17;
 constexpr int64_t kFillBudget = int64_t(1) << 25;
+
+// EAHR_TRACE=1 prints one line per depth round of eahr_topk to stderr: the
+// depth, the lists it advances, and the wall time of the dense channel
+// (including work-ahead), the sparse channel and certification.
+bool trace_on() {
+    static const bool on = [] {
+        const char* p = std::getenv("EAHR_TRACE");
+        return p && *p && *p != '0';
+    }();
+    return on;
+}
 
 double ms_since(std::chrono::steady_clock::time_point t0) {
     return std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
@@ -134,6 +147,8 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
             if (dact[b]) m = std::max<int64_t>(m, depth - static_cast<int64_t>(F[b].L[0].size()));
         }
         if (m > (1LL << 30)) m = 1LL << 30;
+        const auto t_round = std::chrono::steady_clock::now();
+        double r_dense = 0, r_sparse = 0;
         // sparse channel on worker threads while the dense channel runs on the GPU
         std::thread sparse_thread;
         std::atomic<bool> sparse_done{false};
@@ -150,7 +165,8 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
                                         sscores[b].data(), &scnt[b], &ssts[b]);
                 sparse_finished.fetch_add(1, std::memory_order_relaxed);
             });
-            t_sparse += ms_since(t0);
+            r_sparse = ms_since(t0);
+            t_sparse += r_sparse;
             sparse_done.store(true, std::memory_order_release);
         };
         bool any_sparse = false;
@@ -191,7 +207,8 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
                     fill_ranks += added;
                 }
             }
-            t_dense += ms_since(t0);
+            r_dense = ms_since(t0);
+            t_dense += r_dense;
         }
         if (sparse_thread.joinable()) sparse_thread.join();
         EAHR_TRY(dense_rc);
@@ -224,10 +241,29 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
                     sstat[b] = EAHR_LIST_EXHAUSTED;
                 }
             }
+            if (F[b].dup) {   // a channel repeated an id: its list is not a ranking
+                failed[b] = 1;
+                return;
+            }
             rounds[b] += 1;
             F[b].certify();
         });
-        t_fuse += ms_since(t0);
+        const double r_fuse = ms_since(t0);
+        t_fuse += r_fuse;
+        if (trace_on()) {
+            int64_t nd = 0, ns = 0, open_q = 0;
+            for (int32_t b = 0; b < B; ++b) {
+                nd += dact[b];
+                ns += sact[b];
+                open_q += !F[b].resolved && !failed[b];
+            }
+            std::fprintf(stderr,
+                         "eahr round depth=%lld dense_q=%lld sparse_q=%lld dense_ms=%.2f sparse_ms=%.2f "
+                         "certify_ms=%.2f round_ms=%.2f unresolved_after=%lld\n",
+                         static_cast<long long>(depth), static_cast<long long>(nd),
+                         static_cast<long long>(ns), r_dense, r_sparse, r_fuse, ms_since(t_round),
+                         static_cast<long long>(open_q));
+        }
         depth = (depth > (INT64_MAX / ep.growth)) ? INT64_MAX : depth * ep.growth;
     }
     if (prof) pvs_profile_add_host(t_dense, t_sparse, t_fuse);
@@ -285,6 +321,7 @@ extern "C" int eahr_fuse_lists(const int64_t* list_d, int64_t n_d, const int64_t
             if (upto > have) f.append(i, lists[i] + have, upto - have);
             if (static_cast<int64_t>(f.L[i].size()) == lens[i]) f.L[i].open = false;
         }
+        if (f.dup) EAHR_FAIL(EAHR_E_INVALID, "eahr_fuse_lists: a list repeats an id");
         rounds += 1;
         f.certify();
         if (step > 0) depth += step;

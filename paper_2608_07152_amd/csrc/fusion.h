@@ -20,7 +20,8 @@
 // id, so the ranks of a round are radix-sorted and merge-joined against the
 // other list to find items seen by both; a union-find over list positions
 // ("next live single-list position") skips items that became both-seen or
-// fixed in amortised constant time.  Ids must lie in [0, 2^31).
+// fixed in amortised constant time.  Ids must lie in [0, 2^31) and be
+// distinct inside a list (a repeat sets dup).
 #pragma once
 #include <algorithm>
 #include <cstdint>
@@ -61,26 +62,35 @@ inline bool precedes(const Frac& a, int64_t x, const Frac& b, int64_t y) {
     return c > 0 || (c == 0 && x < y);
 }
 
-// Ascending sort of (id << 32 | rank) keys by id (ids < 2^31, distinct).
+// Ascending sort of (id << 32 | rank) keys by id (ids < 2^31): least-
+// significant-digit radix sort on the id bytes (256 scatter targets stay in
+// cache), skipping bytes equal in every id; short runs use a comparison sort.
 inline void sort_by_id(std::vector<uint64_t>& a, std::vector<uint64_t>& tmp) {
     const size_t n = a.size();
-    if (n < 4096) {
+    if (n < 1024) {
         std::sort(a.begin(), a.end());
         return;
     }
     tmp.resize(n);
-    std::vector<uint32_t> cnt(65536);
-    for (int pass = 0; pass < 2; ++pass) {
-        const int shift = 32 + 16 * pass;
-        std::fill(cnt.begin(), cnt.end(), 0u);
-        for (size_t i = 0; i < n; ++i) ++cnt[(a[i] >> shift) & 0xffff];
+    uint32_t cnt[4][256] = {};
+    for (size_t i = 0; i < n; ++i) {
+        const uint32_t id = static_cast<uint32_t>(a[i] >> 32);
+        ++cnt[0][id & 0xff];
+        ++cnt[1][(id >> 8) & 0xff];
+        ++cnt[2][(id >> 16) & 0xff];
+        ++cnt[3][id >> 24];
+    }
+    for (int d = 0; d < 4; ++d) {
+        const int shift = 32 + 8 * d;
+        uint32_t* c = cnt[d];
+        if (c[(a[0] >> shift) & 0xff] == n) continue;   // one digit value
         uint32_t sum = 0;
-        for (auto& c : cnt) {
-            const uint32_t t = c;
-            c = sum;
+        for (int v = 0; v < 256; ++v) {
+            const uint32_t t = c[v];
+            c[v] = sum;
             sum += t;
         }
-        for (size_t i = 0; i < n; ++i) tmp[cnt[(a[i] >> shift) & 0xffff]++] = a[i];
+        for (size_t i = 0; i < n; ++i) tmp[c[(a[i] >> shift) & 0xff]++] = a[i];
         a.swap(tmp);
     }
 }
@@ -150,11 +160,13 @@ struct Fusion {
     std::vector<Scored> both;   // binary heap of unfixed both-seen items
     std::vector<int64_t> A;     // fixed prefix
     bool resolved = false;
+    bool dup = false;           // an id repeated inside one list
     std::vector<uint64_t> batch, tmp, merged;
 
     bool fixed(int64_t x) const { return std::find(A.begin(), A.end(), x) != A.end(); }
 
-    // Append n ranks to list i (ids must be new to the list).
+    // Append n ranks to list i (ids must be new to the list, else dup is set
+    // and the bookkeeping is no longer meaningful).
     void append(int i, const int64_t* ids, int64_t n) {
         if (n <= 0) return;
         List& me = L[i];
@@ -203,6 +215,9 @@ struct Fusion {
         merged.resize(me.by_id.size() + batch.size());
         std::merge(me.by_id.begin(), me.by_id.end(), batch.begin(), batch.end(), merged.begin());
         me.by_id.swap(merged);
+        // a repeated id sits next to its twin in id order
+        for (size_t k = 1; k < me.by_id.size() && !dup; ++k)
+            dup = (me.by_id[k] >> 32) == (me.by_id[k - 1] >> 32);
     }
 
     int64_t single_from(int i, int64_t p) {

@@ -15,7 +15,6 @@
 #include <cstring>
 #include <memory>
 #include <new>
-#include <queue>
 #include <vector>
 
 #include "common.h"
@@ -87,15 +86,6 @@ extern "C" int pbm_debug_set_blockmax(pbm_index* ix, int32_t term, int64_t range
     EAHR_FAIL(EAHR_E_INVALID, "pbm_debug_set_blockmax: term has no postings in range");
 }
 
-// entry of `term` for `range`, or -1
-static int64_t find_entry(const pbm_index* ix, int32_t term, int64_t range) {
-    const int64_t* b = ix->bm_range.data() + ix->bm_ptr[term];
-    const int64_t* e = ix->bm_range.data() + ix->bm_ptr[term + 1];
-    const int64_t* it = std::lower_bound(b, e, range);
-    if (it == e || *it != range) return -1;
-    return it - ix->bm_range.data();
-}
-
 extern "C" int pbm_open(const pbm_index* ix, const eahr_sparse_query* q, pbm_state** out) {
     if (!out) EAHR_FAIL(EAHR_E_INVALID, "pbm_open: out is NULL");
     *out = nullptr;
@@ -120,15 +110,24 @@ extern "C" int pbm_open(const pbm_index* ix, const eahr_sparse_query* q, pbm_sta
         st->terms.push_back(p.first);
         st->w.push_back(p.second);
     }
-    // H(R) in ascending term order over the ranges any query term touches
-    std::vector<float> H(static_cast<size_t>(ix->n_ranges), 0.0f);
-    std::vector<uint8_t> touched(static_cast<size_t>(ix->n_ranges), 0);
+    // H(R) in ascending term order over the ranges any query term touches;
+    // each term's block-max entry per range is tabulated for expansion
+    const int64_t nr = ix->n_ranges;
+    std::vector<float> H(static_cast<size_t>(nr), 0.0f);
+    std::vector<uint8_t> touched(static_cast<size_t>(nr), 0);
     std::vector<int64_t> list;
+    try {
+        st->ent.assign(st->terms.size() * static_cast<size_t>(nr), -1);
+    } catch (const std::bad_alloc&) {
+        EAHR_FAIL(EAHR_E_OOM, "pbm_open: host allocation");
+    }
     for (size_t i = 0; i < st->terms.size(); ++i) {
         const int32_t t = st->terms[i];
         const float w = st->w[i];
+        int64_t* ent = st->ent.data() + i * static_cast<size_t>(nr);
         for (int64_t e = ix->bm_ptr[t]; e < ix->bm_ptr[t + 1]; ++e) {
             const int64_t r = ix->bm_range[e];
+            ent[r] = e;
             const float c = w * ix->bm_max[e];
             H[r] = H[r] + c;
             if (!touched[r]) {
@@ -138,7 +137,10 @@ extern "C" int pbm_open(const pbm_index* ix, const eahr_sparse_query* q, pbm_sta
         }
     }
     for (int64_t r : list)
-        if (H[r] > 0.0f) st->ranges.push(pbm_state::Range{H[r], r});
+        if (H[r] > 0.0f) st->order.push_back(pbm_state::Range{H[r], r});
+    std::sort(st->order.begin(), st->order.end(), [](const pbm_state::Range& a, const pbm_state::Range& b) {
+        return a.H > b.H || (a.H == b.H && a.r < b.r);
+    });
     *out = st.release();
     return EAHR_OK;
 }
@@ -160,9 +162,10 @@ static inline float unord32(uint32_t k) {
 static inline uint64_t item_key(float s, int64_t id) {
     return (static_cast<uint64_t>(~ord32(s + 0.0f)) << 32) | static_cast<uint64_t>(id);
 }
+static inline bool ranges_left(const pbm_state* st) { return st->next < st->order.size(); }
 static inline uint64_t bound_key(const pbm_state* st) {
-    if (st->ranges.empty()) return ~0ull;
-    const auto& R = st->ranges.top();
+    if (!ranges_left(st)) return ~0ull;
+    const auto& R = st->order[st->next];
     return (static_cast<uint64_t>(~ord32(R.H)) << 32) | static_cast<uint64_t>(R.r * st->ix->range_size);
 }
 
@@ -180,7 +183,7 @@ static bool expand(pbm_state* st, const pbm_state::Range& R) {
     st->touched.clear();
     for (size_t i = 0; i < st->terms.size(); ++i) {
         const int32_t t = st->terms[i];
-        const int64_t e = find_entry(ix, t, R.r);
+        const int64_t e = st->ent[i * static_cast<size_t>(ix->n_ranges) + R.r];
         if (e < 0) continue;
         const int64_t p_end = (e + 1 < ix->bm_ptr[t + 1]) ? ix->bm_off[e + 1] : ix->term_ptr[t + 1];
         const float w = st->w[i];
@@ -206,6 +209,64 @@ static bool expand(pbm_state* st, const pbm_state::Range& R) {
     return ok;
 }
 
+// Ascending sort of 64-bit keys: least-significant-digit radix sort with
+// 8-bit digits (256 scatter targets stay in cache), skipping digits that are
+// equal in every key (the high bits of the identifiers); short runs use a
+// comparison sort.
+static void sort_keys(std::vector<uint64_t>& a) {
+    const size_t n = a.size();
+    if (n < 1024) {
+        std::sort(a.begin(), a.end());
+        return;
+    }
+    // scratch reused by every state sorted on this thread
+    thread_local std::vector<uint64_t> tmp;
+    thread_local std::vector<uint32_t> cnt;
+    if (tmp.size() < n) tmp.resize(n);
+    cnt.assign(8 * 256, 0u);
+    for (size_t i = 0; i < n; ++i) {
+        const uint64_t k = a[i];
+        for (int d = 0; d < 8; ++d) ++cnt[d * 256 + ((k >> (8 * d)) & 0xff)];
+    }
+    for (int d = 0; d < 8; ++d) {
+        uint32_t* c = cnt.data() + d * 256;
+        if (c[(a[0] >> (8 * d)) & 0xff] == n) continue;   // one digit value
+        uint32_t sum = 0;
+        for (int v = 0; v < 256; ++v) {
+            const uint32_t t = c[v];
+            c[v] = sum;
+            sum += t;
+        }
+        uint64_t* out = tmp.data();
+        for (size_t i = 0; i < n; ++i) out[c[(a[i] >> (8 * d)) & 0xff]++] = a[i];
+        std::copy(out, out + n, a.begin());
+    }
+}
+
+// Expansion visits ranges in bound order, i.e. at scattered addresses:
+// prefetch the block-max offsets of the range two ahead and the postings of
+// the range one ahead.
+static inline void prefetch_ahead(const pbm_state* st) {
+    const pbm_index* ix = st->ix;
+    const size_t nr = static_cast<size_t>(ix->n_ranges);
+    for (size_t ahead = 1; ahead <= 2; ++ahead) {
+        const size_t j = st->next + ahead;
+        if (j >= st->order.size()) return;
+        const int64_t r = st->order[j].r;
+        for (size_t i = 0; i < st->terms.size(); ++i) {
+            const int64_t e = st->ent[i * nr + r];
+            if (e < 0) continue;
+            if (ahead == 2) {
+                __builtin_prefetch(&ix->bm_off[e]);
+            } else {
+                const int64_t p = ix->bm_off[e];
+                __builtin_prefetch(&ix->docs[p]);
+                __builtin_prefetch(&ix->imp[p]);
+            }
+        }
+    }
+}
+
 // Refill the ready run with at least `want` publishable items when the
 // remaining ranges allow: expand ranges in bound order until enough pooled
 // items precede the next range's bound (counted whenever the pool has grown
@@ -216,7 +277,7 @@ static bool refill(pbm_state* st, size_t want) {
     st->ready_pos = 0;
     size_t checked = 0;
     for (;;) {
-        if (st->ranges.empty()) break;
+        if (!ranges_left(st)) break;
         if (st->pool.size() >= want && st->pool.size() >= checked + checked / 2) {
             const uint64_t bk = bound_key(st);
             size_t n = 0;
@@ -224,8 +285,8 @@ static bool refill(pbm_state* st, size_t want) {
             if (n >= want) break;
             checked = st->pool.size();
         }
-        const auto R = st->ranges.top();
-        st->ranges.pop();
+        prefetch_ahead(st);
+        const auto R = st->order[st->next++];
         st->ranges_expanded += 1;
         if (!expand(st, R)) return false;
     }
@@ -233,7 +294,7 @@ static bool refill(pbm_state* st, size_t want) {
     auto mid = std::partition(st->pool.begin(), st->pool.end(), [bk](uint64_t k) { return k < bk; });
     st->ready.assign(st->pool.begin(), mid);
     st->pool.erase(st->pool.begin(), mid);
-    std::sort(st->ready.begin(), st->ready.end());
+    sort_keys(st->ready);
     return true;
 }
 
@@ -251,7 +312,7 @@ extern "C" int pbm_next(pbm_state* st, int32_t m, int64_t* ids, float* scores, i
                 ++n;
                 continue;
             }
-            if (st->ranges.empty() && st->pool.empty()) break;   // list complete
+            if (!ranges_left(st) && st->pool.empty()) break;   // list complete
             if (!refill(st, static_cast<size_t>(m - n))) {
                 st->failed = true;
                 n = 0;
@@ -262,7 +323,7 @@ extern "C" int pbm_next(pbm_state* st, int32_t m, int64_t* ids, float* scores, i
     st->emitted += n;
     *count = n;
     if (st->failed) *status = EAHR_LIST_FAILED;
-    else if (st->ranges.empty() && st->pool.empty() && st->ready_pos >= st->ready.size())
+    else if (!ranges_left(st) && st->pool.empty() && st->ready_pos >= st->ready.size())
         *status = EAHR_LIST_EXHAUSTED;
     else *status = EAHR_LIST_OPEN;
     return EAHR_OK;

@@ -1,7 +1,6 @@
 // Host structures of the Posting Block-Max sparse channel.
 #pragma once
 #include <cstdint>
-#include <queue>
 #include <vector>
 
 #include "eahr.h"
@@ -26,15 +25,16 @@ struct pbm_state {
         float H;
         int64_t r;
     };
-    struct RangeOrder {   // max-heap on (H desc, first id asc)
-        bool operator()(const Range& a, const Range& b) const {
-            return a.H < b.H || (a.H == b.H && a.r > b.r);
-        }
-    };
     const pbm_index* ix = nullptr;
     std::vector<int32_t> terms;   // ascending term ids with nonzero weight
     std::vector<float> w;
-    std::priority_queue<Range, std::vector<Range>, RangeOrder> ranges;
+    // Ranges with H(R) > 0 in expansion order (H desc, first id asc); H(R)
+    // is fixed at open, so the order is sorted once.  order[next..] are the
+    // unexpanded ranges.
+    std::vector<Range> order;
+    size_t next = 0;
+    // ent[i * n_ranges + r]: block-max entry of terms[i] for range r, or -1
+    std::vector<int64_t> ent;
     // Scored items as keys (~ord(S) << 32 | id): ascending keys are
     // (S desc, id asc), and an item precedes range R's bound exactly when its
     // key is below (~ord(H(R)) << 32 | first id of R).

@@ -99,6 +99,30 @@ def test_fuse_lists_weight_two_to_one():
         assert list(got) == rrf.rrf_topk([a, b], [2, 1], 60, 20)
 
 
+def test_fuse_lists_rejects_a_repeated_id():
+    """A list that repeats an id is not a ranking (Sec. 2.1: each retriever
+    ranks a set of distinct items)."""
+    with pytest.raises(eahr.EahrError) as ei:
+        eahr.eahr_fuse_lists(np.array([3, 1, 3, 0]), np.array([1, 0, 2]), K=2, depth0=2)
+    assert ei.value.code == eahr.EAHR_E_INVALID
+
+
+def test_fuse_lists_large_prefixes_equal_complete_rrf():
+    """Deep prefixes (several table growths of the id bookkeeping): partially
+    overlapping permutations of 200,000 ids."""
+    rng = np.random.default_rng(5)
+    n = 200_000
+    a = rng.permutation(n)
+    b = a.copy()
+    blk = 5000
+    for s0 in range(0, n, blk):
+        b[s0:s0 + blk] = rng.permutation(b[s0:s0 + blk])
+    b = np.concatenate([b[n // 2:], b[:n // 2]])
+    for wts in ((1, 1), (2, 1)):
+        got, st = eahr.eahr_fuse_lists(a, b, K=20, w_dense=wts[0], w_sparse=wts[1])
+        assert list(got) == rrf.rrf_topk([a, b], list(wts), 60, 20)
+
+
 def test_sparse_only_topk_through_eahr_topk():
     # the dense channel is not touched when its weight is 0 (no GPU needed)
     w = datagen.workload("tiny", n=5000)
