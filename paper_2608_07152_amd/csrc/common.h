@@ -7,6 +7,10 @@
 
 namespace eahr {
 void set_error(const char* fmt, ...) __attribute__((format(printf, 1, 2)));
+
+// EAHR_TRACE=1 (environment) turns on per-round timing lines on stderr: one
+// per depth round of eahr_topk and one per scan round of the dense channel.
+bool trace_on();
 }
 
 #define EAHR_FAIL(code, ...)           \

@@ -8,7 +8,6 @@
 #include <chrono>
 #include <cstdint>
 #include <cstdio>
-#include <cstdlib>
 #include <cstring>
 #include <memory>
 #include <new>
@@ -44,17 +43,6 @@ using ::eahr::parallel_for;
 // share of its queries still to finish).
 constexpr int64_t kFillMaxDepth = int64_t(1) << 17;
 constexpr int64_t kFillBudget = int64_t(1) << 25;
-
-// EAHR_TRACE=1 prints one line per depth round of eahr_topk to stderr: the
-// depth, the lists it advances, and the wall time of the dense channel
-// (including work-ahead), the sparse channel and certification.
-bool trace_on() {
-    static const bool on = [] {
-        const char* p = std::getenv("EAHR_TRACE");
-        return p && *p && *p != '0';
-    }();
-    return on;
-}
 
 double ms_since(std::chrono::steady_clock::time_point t0) {
     return std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
@@ -250,7 +238,7 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
         });
         const double r_fuse = ms_since(t0);
         t_fuse += r_fuse;
-        if (trace_on()) {
+        if (::eahr::trace_on()) {
             int64_t nd = 0, ns = 0, open_q = 0;
             for (int32_t b = 0; b < B; ++b) {
                 nd += dact[b];

@@ -1,6 +1,7 @@
-// Thread-local last-error message of libeahr.
+// Thread-local last-error message of libeahr, and the trace switch.
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 
 #include "common.h"
 
@@ -14,6 +15,14 @@ void set_error(const char* fmt, ...) {
     va_start(ap, fmt);
     std::vsnprintf(g_err, sizeof(g_err), fmt, ap);
     va_end(ap);
+}
+
+bool trace_on() {
+    static const bool on = [] {
+        const char* p = std::getenv("EAHR_TRACE");
+        return p && *p && *p != '0';
+    }();
+    return on;
 }
 }  // namespace eahr
 

@@ -11,8 +11,10 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <chrono>
 #include <cmath>
 #include <cstdint>
+#include <cstdio>
 #include <cstdlib>
 #include <cstring>
 #include <limits>
@@ -660,6 +662,7 @@ extern "C" int pvs_scores(const pvs_state* st, int32_t b, const int64_t* rows, i
 }
 
 // ============================================================== scan driver
+static inline int32_t key_id(uint64_t key) { return static_cast<int32_t>(key & 0xffffffffu); }
 static inline float key_score(uint64_t key) {
     const uint32_t k = ~static_cast<uint32_t>(key >> 32);
     const uint32_t bits = (k & 0x80000000u) ? (k & 0x7fffffffu) : ~k;
@@ -675,8 +678,8 @@ static int64_t lower_overlap(const pvs_state* st, int32_t b) {
     if (!Q.has_cert) return 0;
     const double lim = static_cast<double>(Q.s_cert) + 2.0 * Q.wmax;
     int64_t a = 0;
-    for (int64_t i = static_cast<int64_t>(Q.cache_score.size()) - 1; i >= 0; --i) {
-        if (Q.cache_score[i] > lim) break;
+    for (int64_t i = static_cast<int64_t>(Q.cache.size()) - 1; i >= 0; --i) {
+        if (key_score(Q.cache[i]) > lim) break;
         ++a;
     }
     return a;
@@ -711,13 +714,13 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
         const int32_t b = todo[i];
         auto& Q = st->q[b];
         ScanQ sq = make_scanq(st, b);
-        const int64_t have = static_cast<int64_t>(Q.cache_score.size());
+        const int64_t have = static_cast<int64_t>(Q.cache.size());
         const int64_t avail = have - Q.emitted;
         const int64_t need = std::max<int64_t>(1, m - avail);
         const int64_t spec = std::min(pvs::kSpecFactor * (Q.emitted + m) - have, pvs::kSpecBudget / nq);
         const int64_t target = std::max({need, mmin, spec}) + lower_overlap(st, b);
         double k = (stride == 1) ? static_cast<double>(target)
-                                 : std::max(4.0, std::ceil(2.0 * target * frac));
+                                 : std::max(4.0, std::ceil(pvs::kSampleMargin * target * frac));
         for (int r = 0; r < Q.retries; ++r) k *= 4.0;
         sq.k = static_cast<int32_t>(std::min(k, 2.0e9));
         st->h_scanq[i] = sq;
@@ -737,6 +740,10 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
         else pvs::launch_scan(v, st->vis, nblocks, st->qcodes, st->scanq, n, ix->gamma, sample, o, s);
     };
 
+    const bool trace = ::eahr::trace_on();
+    using clk = std::chrono::steady_clock;
+    clk::time_point tp[6];
+    tp[0] = clk::now();
     // 1. threshold and candidate estimate from the sampled blocks
     HIP_TRY(hipMemcpyAsync(st->scanq, st->h_scanq, nq * sizeof(ScanQ), hipMemcpyHostToDevice, s));
     pvs::ScanOut so;
@@ -746,11 +753,12 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     so.sample_stride = stride;
     EAHR_TRY(mark(0));
     scan(true, so, nq);
-    pvs::launch_select(st->sample_lo, st->sample_hi, sample_ld, sample_ld, st->scanq, nq, s);
+    pvs::launch_select(st->sample_lo, st->sample_hi, sample_ld, sample_ld, stride > 1, st->scanq, nq, s);
     EAHR_TRY(mark(1));
     HIP_TRY(hipGetLastError());
     HIP_TRY(hipMemcpyAsync(st->h_scanq, st->scanq, nq * sizeof(ScanQ), hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
+    tp[1] = clk::now();
 
     // 2. candidate regions: the sample saw every block when stride == 1.
     //    Queries past the pool limit wait for the next round (kept in todo).
@@ -800,6 +808,7 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     HIP_TRY(hipMemcpyAsync(st->h_counts, st->counts, host_counts(nq) * sizeof(int32_t),
                            hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
+    tp[2] = clk::now();
     const std::vector<int32_t> need(st->h_counts + 4 * nq + 1, st->h_counts + 5 * nq + 1);
     st->stats.scans += 1;
     st->stats.sample_scans += 1;
@@ -824,12 +833,14 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     HIP_TRY(hipMemcpyAsync(st->h_counts + nq, d_cert, (3 * static_cast<size_t>(nq) + 1) * sizeof(int32_t),
                            hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
+    tp[3] = clk::now();
     const int32_t* h_cert = st->h_counts + nq;
     const int32_t* h_fail = st->h_counts + 2 * nq;
     const int32_t* h_offs = st->h_counts + 3 * nq;
     if (h_offs[nq] > 0)
         HIP_TRY(hipMemcpy(st->h_packed, st->packed, static_cast<size_t>(h_offs[nq]) * sizeof(uint64_t),
                           hipMemcpyDeviceToHost));
+    tp[4] = clk::now();
     if (prof) {
         float t[4];
         HIP_TRY(hipEventElapsedTime(&t[0], st->ev[0], st->ev[1]));
@@ -859,29 +870,28 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
         g_prof.scan_rounds += 1;
     }
 
-    // decode the certified keys of every query into its cache (in parallel)
-    std::vector<int64_t> old_size(nq, 0);
+    // append the certified keys of every query to its cache (in parallel)
     std::vector<uint8_t> usable(nq, 0);
-    for (int32_t i = 0; i < nq; ++i) {
-        auto& Q = st->q[todo[i]];
+    for (int32_t i = 0; i < nq; ++i)
         usable[i] = !h_fail[i] && need[i] <= st->h_scanq[i].cand_cap;
-        old_size[i] = static_cast<int64_t>(Q.cache_id.size());
-        if (usable[i]) {
-            Q.cache_id.resize(old_size[i] + h_cert[i]);
-            Q.cache_score.resize(old_size[i] + h_cert[i]);
-        }
-    }
     eahr::parallel_for(nq, eahr::host_threads(), [&](int64_t i) {
-        if (!usable[i]) return;
-        auto& Q = st->q[todo[i]];
+        if (!usable[i] || h_cert[i] == 0) return;
         const uint64_t* kp = st->h_packed + h_offs[i];
-        int32_t* id = Q.cache_id.data() + old_size[i];
-        float* sc = Q.cache_score.data() + old_size[i];
-        for (int64_t j = 0; j < h_cert[i]; ++j) {
-            id[j] = static_cast<int32_t>(kp[j] & 0xffffffffu);
-            sc[j] = key_score(kp[j]);
-        }
+        auto& c = st->q[todo[i]].cache;
+        c.insert(c.end(), kp, kp + h_cert[i]);
     });
+    if (trace) {
+        tp[5] = clk::now();
+        auto ms = [&](int a, int b) { return std::chrono::duration<double, std::milli>(tp[b] - tp[a]).count(); };
+        int64_t certified = 0;
+        for (int32_t i = 0; i < nq; ++i) certified += h_cert[i];
+        std::fprintf(stderr,
+                     "pvs scan_round queries=%d path=%s stride=%lld pool=%lld kept=%lld certified=%lld "
+                     "sample_ms=%.2f scan_ms=%.2f rank_ms=%.2f copy_ms=%.2f decode_ms=%.2f\n",
+                     nq, mfma ? "mfma" : "gemv", static_cast<long long>(stride),
+                     static_cast<long long>(total), static_cast<long long>(kept),
+                     static_cast<long long>(certified), ms(0, 1), ms(1, 2), ms(2, 3), ms(3, 4), ms(4, 5));
+    }
     std::vector<int32_t> keep;
     for (int32_t i = 0; i < nq; ++i) {
         const int32_t b = todo[i];
@@ -901,11 +911,11 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
         st->stats.certified += c;
         if (c > 0) {
             Q.has_cert = true;
-            Q.s_cert = Q.cache_score.back();
-            Q.id_cert = Q.cache_id.back();
+            Q.s_cert = key_score(Q.cache.back());
+            Q.id_cert = key_id(Q.cache.back());
         }
-        const int64_t avail = static_cast<int64_t>(Q.cache_score.size()) - Q.emitted;
-        if (static_cast<int64_t>(Q.cache_score.size()) >= st->n_vis) {
+        const int64_t avail = static_cast<int64_t>(Q.cache.size()) - Q.emitted;
+        if (static_cast<int64_t>(Q.cache.size()) >= st->n_vis) {
             Q.cert_exhausted = true;
             Q.retries = 0;
         } else if (avail >= m) {
@@ -931,7 +941,7 @@ extern "C" int pvs_next(pvs_state* st, int32_t m, const uint8_t* active, int64_t
         if (active && !active[b]) continue;
         auto& Q = st->q[b];
         if (Q.failed || Q.cert_exhausted) continue;
-        const int64_t avail = static_cast<int64_t>(Q.cache_score.size()) - Q.emitted;
+        const int64_t avail = static_cast<int64_t>(Q.cache.size()) - Q.emitted;
         if (avail < m) todo.push_back(b);
     }
     for (int guard = 0; !todo.empty(); ++guard) {
@@ -946,11 +956,12 @@ extern "C" int pvs_next(pvs_state* st, int32_t m, const uint8_t* active, int64_t
             status[b] = EAHR_LIST_FAILED;
             continue;
         }
-        const int64_t avail = static_cast<int64_t>(Q.cache_score.size()) - Q.emitted;
+        const int64_t avail = static_cast<int64_t>(Q.cache.size()) - Q.emitted;
         const int64_t take = std::min<int64_t>(m, avail);
+        const uint64_t* kp = Q.cache.data() + Q.emitted;
         for (int64_t j = 0; j < take; ++j) {
-            ids[static_cast<int64_t>(b) * m + j] = Q.cache_id[Q.emitted + j];
-            scores[static_cast<int64_t>(b) * m + j] = Q.cache_score[Q.emitted + j];
+            ids[static_cast<int64_t>(b) * m + j] = key_id(kp[j]);
+            scores[static_cast<int64_t>(b) * m + j] = key_score(kp[j]);
         }
         Q.emitted += take;
         st->stats.emitted += take;
@@ -967,9 +978,9 @@ int pvs_fill(pvs_state* st, int64_t depth, const uint8_t* active, int64_t* added
     for (int32_t b = 0; b < st->B; ++b) {
         if (active && !active[b]) continue;
         const auto& Q = st->q[b];
-        before += static_cast<int64_t>(Q.cache_score.size());
+        before += static_cast<int64_t>(Q.cache.size());
         if (Q.failed || Q.cert_exhausted) continue;
-        if (static_cast<int64_t>(Q.cache_score.size()) >= depth) continue;
+        if (static_cast<int64_t>(Q.cache.size()) >= depth) continue;
         todo.push_back(b);
         m = std::max<int64_t>(m, depth - Q.emitted);
     }
@@ -981,7 +992,7 @@ int pvs_fill(pvs_state* st, int64_t depth, const uint8_t* active, int64_t* added
     if (added) {
         int64_t after = 0;
         for (int32_t b = 0; b < st->B; ++b)
-            if (!active || active[b]) after += static_cast<int64_t>(st->q[b].cache_score.size());
+            if (!active || active[b]) after += static_cast<int64_t>(st->q[b].cache.size());
         *added = after - before;
     }
     return EAHR_OK;

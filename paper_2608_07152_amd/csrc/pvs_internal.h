@@ -11,7 +11,12 @@
 namespace pvs {
 // Threshold estimation samples every stride-th code block, with the stride
 // the largest power of two that keeps at least this many blocks sampled.
+// With stride 1 tau is the target-th largest lower bound, so at least the
+// target is certified.  With a larger stride tau is taken from the sampled
+// interval midpoints (close to the scores, so the rows certified, s >= tau,
+// number about the target scaled by the stride) with this relative margin.
 constexpr int64_t kSampleBlocks = 2048;
+constexpr double kSampleMargin = 1.25;
 // Smallest candidate pool allocated for a scan, and the largest pool one scan
 // round may use (queries beyond it wait for the next round).
 constexpr int64_t kMinCap = 4096;
@@ -108,8 +113,9 @@ struct pvs_state {
         bool has_cert = false;          // a rank has been certified
         float s_cert = 0.0f;            // key (s_cert, id_cert) of the last certified rank
         int32_t id_cert = -1;
-        std::vector<int32_t> cache_id;  // certified ranks in order
-        std::vector<float> cache_score;
+        // certified ranks in order, as their sort keys (~mono(s32) << 32 | id);
+        // ids and scores are decoded only when emitted
+        std::vector<uint64_t> cache;
         int64_t emitted = 0;            // ranks returned by pvs_next
         bool failed = false;
         bool cert_exhausted = false;    // every visible row certified

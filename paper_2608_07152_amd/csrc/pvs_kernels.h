@@ -88,10 +88,11 @@ void launch_scan_mfma(const IndexView& ix, const uint64_t* vis, int64_t nblocks,
                       const ScanOut& o, void* frag, hipStream_t stream);
 int mfma_tiles_for(int32_t nq);
 
-// tau = k-th largest finite sampled lower bound; sample_hits = sampled pairs
-// with hi >= tau (both written into sq).
+// tau = k-th largest finite sampled lower bound (or, with midpoint, sampled
+// interval midpoint); sample_hits = sampled pairs with hi >= tau (both
+// written into sq).
 void launch_select(const float* sample_lo, const float* sample_hi, int64_t n, int64_t ld,
-                   ScanQ* sq, int32_t nq, hipStream_t stream);
+                   bool midpoint, ScanQ* sq, int32_t nq, hipStream_t stream);
 
 // Per query: total[b] = sum over sub-regions of min(count, cand_cap) (the
 // candidates kept), need[b] = the largest sub-region count (a sub-region

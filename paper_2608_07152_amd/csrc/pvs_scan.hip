@@ -638,12 +638,19 @@ void launch_cand_totals(const int32_t* sub_cnt, const ScanQ* sq, int32_t nq, int
 }
 
 // ------------------------------------------------------------ threshold
-// One workgroup per query: tau = the k-th largest finite sampled lower bound
-// (radix select over order-preserving keys, 8 bits per pass), -inf when fewer
-// than k are finite; then sample_hits = sampled pairs with hi >= tau.
+// One workgroup per query: tau = the k-th largest finite value among the
+// sampled lower bounds (midpoint == 0) or the sampled interval midpoints
+// (lo + hi) / 2 (midpoint == 1), by radix select over order-preserving keys,
+// 8 bits per pass; -inf when fewer than k are finite.  Then sample_hits =
+// sampled pairs with hi >= tau.
+__device__ __forceinline__ float select_value(const float* x, const float* y, int64_t i, int midpoint) {
+    const float lo = x[i];
+    return (midpoint && lo != -INFINITY) ? 0.5f * lo + 0.5f * y[i] : lo;
+}
+
 __global__ __launch_bounds__(1024) void k_select(const float* __restrict__ sample_lo,
                                                  const float* __restrict__ sample_hi, int64_t n,
-                                                 int64_t ld, ScanQ* __restrict__ sq) {
+                                                 int64_t ld, int midpoint, ScanQ* __restrict__ sq) {
     __shared__ uint32_t hist[256];
     __shared__ uint32_t s_digit;
     __shared__ uint32_t s_rest;
@@ -673,7 +680,7 @@ __global__ __launch_bounds__(1024) void k_select(const float* __restrict__ sampl
             for (int i = threadIdx.x; i < 256; i += blockDim.x) hist[i] = 0;
             __syncthreads();
             for (int64_t i = threadIdx.x; i < n; i += blockDim.x) {
-                const float v = x[i];
+                const float v = select_value(x, y, i, midpoint);
                 if (v == -INFINITY) continue;
                 const uint32_t key = mono32(v);
                 if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
@@ -710,9 +717,10 @@ __global__ __launch_bounds__(1024) void k_select(const float* __restrict__ sampl
 }
 
 void launch_select(const float* sample_lo, const float* sample_hi, int64_t n, int64_t ld,
-                   ScanQ* sq, int32_t nq, hipStream_t stream) {
+                   bool midpoint, ScanQ* sq, int32_t nq, hipStream_t stream) {
     if (nq <= 0) return;
-    hipLaunchKernelGGL(k_select, dim3(nq), dim3(1024), 0, stream, sample_lo, sample_hi, n, ld, sq);
+    hipLaunchKernelGGL(k_select, dim3(nq), dim3(1024), 0, stream, sample_lo, sample_hi, n, ld,
+                       midpoint ? 1 : 0, sq);
 }
 
 }  // namespace pvs
