@@ -41,8 +41,9 @@ constexpr int64_t kTargetBudget = 8192;
 constexpr int64_t kSpecFactor = 8;
 constexpr int64_t kSpecBudget = int64_t(1) << 20;
 // Scans of at least this many queries use the Int8 MFMA kernel; smaller ones
-// the dot4 GEMV kernel.  EAHR_SCAN_PATH=gemv|mfma forces one path (testing).
-constexpr int32_t kMfmaMinQueries = 4;
+// the dot4 GEMV kernel, which streams the codes at the HBM rate for up to 8
+// queries in one pass.  EAHR_SCAN_PATH=gemv|mfma forces one path (testing).
+constexpr int32_t kMfmaMinQueries = 9;
 enum class ScanPath { Auto, Gemv, Mfma };
 }  // namespace pvs
 

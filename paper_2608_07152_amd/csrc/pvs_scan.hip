@@ -576,9 +576,12 @@ static void mfma_pass(const IndexView& ix, const uint64_t* vis, int64_t nblocks,
     }
 }
 
+// Query tiles of an MFMA pass: one tile up to 32 queries, else the wide
+// kernel with 4 or 8 tiles (33-64 queries also take 4 tiles: the wide
+// kernel streams the codes faster than the two-tile kernel computes).
 int mfma_tiles_for(int32_t nq) {
     const int t = (nq + 31) / 32;
-    return t <= 1 ? 1 : t <= 2 ? 2 : t <= 4 ? 4 : 8;
+    return t <= 1 ? 1 : t <= 4 ? 4 : 8;
 }
 
 void launch_scan_mfma(const IndexView& ix, const uint64_t* vis, int64_t nblocks,
