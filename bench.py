@@ -77,6 +77,8 @@ TRAFFIC_FILES = {
     "rescore": ("profiles/k_rescore_passage_b256_traffic.txt", ["paper_2608_07152_amd/csrc/pvs_rank.hip"]),
     "k_scan_mfma<8>": ("profiles/k_scan_mfma_wide_passage_b256_traffic.txt",
                        ["paper_2608_07152_amd/csrc/pvs_scan.hip"]),
+    "k_scan_mfma<4>": ("profiles/k_scan_mfma_wide4_passage_b256_traffic.txt",
+                       ["paper_2608_07152_amd/csrc/pvs_scan.hip"]),
     "k_scan_gemv<1>": ("profiles/k_scan_gemv1_passage_b1_traffic.txt",
                        ["paper_2608_07152_amd/csrc/pvs_scan.hip"]),
 }
