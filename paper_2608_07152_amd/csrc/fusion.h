@@ -22,6 +22,11 @@
 // ("next live single-list position") skips items that became both-seen or
 // fixed in amortised constant time.  Ids must lie in [0, 2^31) and be
 // distinct inside a list (a repeat sets dup).
+//
+// Once one list is closed (read to its end) nothing joins against the other
+// list's id order any more: appends to the open list then test membership in
+// the closed list with a bitmap over ids (and look up the rank in its id
+// order only for the items it holds), and repeats with a second bitmap.
 #pragma once
 #include <algorithm>
 #include <cstdint>
@@ -148,9 +153,12 @@ struct Fusion {
         }
         void kill(int64_t p) { alive[p >> 6] &= ~(1ull << (p & 63)); }
         void grow(int64_t n_new) {   // new positions start live
-            const int64_t p0 = size();
-            alive.resize(static_cast<size_t>((p0 + n_new + 63) >> 6), 0);
-            for (int64_t p = p0; p < p0 + n_new; ++p) alive[p >> 6] |= 1ull << (p & 63);
+            const int64_t p0 = size(), p1 = p0 + n_new;
+            alive.resize(static_cast<size_t>((p1 + 63) >> 6), 0);
+            int64_t p = p0;
+            for (; p < p1 && (p & 63); ++p) alive[p >> 6] |= 1ull << (p & 63);
+            for (; p + 64 <= p1; p += 64) alive[p >> 6] = ~0ull;
+            for (; p < p1; ++p) alive[p >> 6] |= 1ull << (p & 63);
         }
         int64_t size() const { return static_cast<int64_t>(ids.size()); }
     };
@@ -162,6 +170,35 @@ struct Fusion {
     bool resolved = false;
     bool dup = false;           // an id repeated inside one list
     std::vector<uint64_t> batch, tmp, merged;
+    // closed-list mode: seen[i] has bit x set when list i holds id x
+    bool bitmaps = false;
+    std::vector<uint64_t> seen[2];
+
+    static bool test_bit(const std::vector<uint64_t>& b, int64_t x) {
+        const size_t w = static_cast<size_t>(x >> 6);
+        return w < b.size() && ((b[w] >> (x & 63)) & 1ull);
+    }
+    // sets bit x, returns whether it was already set
+    static bool set_bit(std::vector<uint64_t>& b, int64_t x) {
+        const size_t w = static_cast<size_t>(x >> 6);
+        if (w >= b.size()) b.resize(std::max(w + 1, b.size() * 2), 0);
+        const uint64_t m = 1ull << (x & 63);
+        const bool had = (b[w] & m) != 0;
+        b[w] |= m;
+        return had;
+    }
+    void enter_bitmap_mode() {
+        for (int i = 0; i < 2; ++i)
+            for (int64_t x : L[i].ids) set_bit(seen[i], x);
+        bitmaps = true;
+    }
+    // rank (1-based) of id x in list i, from its id order; x must be in it
+    int64_t rank_of(int i, int64_t x) const {
+        const auto& v = L[i].by_id;
+        const uint64_t key = static_cast<uint64_t>(x) << 32;
+        const auto it = std::lower_bound(v.begin(), v.end(), key);
+        return static_cast<int64_t>(*it & 0xffffffffu);
+    }
 
     bool fixed(int64_t x) const { return std::find(A.begin(), A.end(), x) != A.end(); }
 
@@ -169,6 +206,10 @@ struct Fusion {
     // and the bookkeeping is no longer meaningful).
     void append(int i, const int64_t* ids, int64_t n) {
         if (n <= 0) return;
+        if (!L[1 - i].open) {
+            append_closed_other(i, ids, n);
+            return;
+        }
         List& me = L[i];
         List& other = L[1 - i];
         const int64_t p0 = me.size();
@@ -212,12 +253,61 @@ struct Fusion {
             for (size_t k = heap0 + 1; k <= both.size(); ++k)
                 std::push_heap(both.begin(), both.begin() + k, HeapLess{P});
         }
+        // merge into the id order; a repeated id meets its twin here
+        for (size_t k = 1; k < batch.size(); ++k) dup |= (batch[k] >> 32) == (batch[k - 1] >> 32);
         merged.resize(me.by_id.size() + batch.size());
-        std::merge(me.by_id.begin(), me.by_id.end(), batch.begin(), batch.end(), merged.begin());
+        {
+            const uint64_t* x = me.by_id.data();
+            const uint64_t* xe = x + me.by_id.size();
+            const uint64_t* y = batch.data();
+            const uint64_t* ye = y + batch.size();
+            uint64_t* out = merged.data();
+            bool eq = false;
+            while (x < xe && y < ye) {
+                eq |= (*x >> 32) == (*y >> 32);
+                *out++ = (*y < *x) ? *y++ : *x++;
+            }
+            out = std::copy(x, xe, out);
+            std::copy(y, ye, out);
+            dup |= eq;
+        }
         me.by_id.swap(merged);
-        // a repeated id sits next to its twin in id order
-        for (size_t k = 1; k < me.by_id.size() && !dup; ++k)
-            dup = (me.by_id[k] >> 32) == (me.by_id[k - 1] >> 32);
+    }
+
+    // Append to list i while the other list is closed (see the file header).
+    void append_closed_other(int i, const int64_t* ids, int64_t n) {
+        if (!bitmaps) enter_bitmap_mode();
+        List& me = L[i];
+        List& other = L[1 - i];
+        const int64_t p0 = me.size();
+        me.grow(n);
+        me.ids.insert(me.ids.end(), ids, ids + n);
+        const size_t heap0 = both.size();
+        for (int64_t j = 0; j < n; ++j) {
+            const int64_t x = ids[j];
+            const int64_t rank = p0 + j + 1;
+            if (set_bit(seen[i], x)) {
+                dup = true;
+                me.kill(rank - 1);
+                continue;
+            }
+            if (!test_bit(seen[1 - i], x)) continue;
+            const int64_t ro = rank_of(1 - i, x);
+            me.kill(rank - 1);
+            other.kill(ro - 1);
+            if (!fixed(x)) {
+                const int64_t r0 = (i == 0) ? rank : ro, r1 = (i == 0) ? ro : rank;
+                both.push_back(Scored{g_double(*P, 0, r0) + g_double(*P, 1, r1),
+                                      static_cast<int32_t>(r0), static_cast<int32_t>(r1), x});
+            }
+        }
+        const size_t added = both.size() - heap0;
+        if (added > heap0 / 8) {
+            std::make_heap(both.begin(), both.end(), HeapLess{P});
+        } else {
+            for (size_t k = heap0 + 1; k <= both.size(); ++k)
+                std::push_heap(both.begin(), both.begin() + k, HeapLess{P});
+        }
     }
 
     int64_t single_from(int i, int64_t p) {

@@ -948,26 +948,31 @@ extern "C" int pvs_next(pvs_state* st, int32_t m, const uint8_t* active, int64_t
         if (guard > 200) EAHR_FAIL(EAHR_E_HIP, "pvs_next: scan loop did not converge");
         EAHR_TRY(scan_round(st, todo, m));
     }
-    for (int32_t b = 0; b < B; ++b) {
-        if (active && !active[b]) continue;
+    // decode the emitted ranks of every query (in parallel)
+    std::vector<int64_t> took(B, 0);
+    eahr::parallel_for(B, eahr::host_threads(), [&](int64_t b) {
+        if (active && !active[b]) return;
         auto& Q = st->q[b];
         if (Q.failed) {
             count[b] = 0;
             status[b] = EAHR_LIST_FAILED;
-            continue;
+            return;
         }
         const int64_t avail = static_cast<int64_t>(Q.cache.size()) - Q.emitted;
         const int64_t take = std::min<int64_t>(m, avail);
         const uint64_t* kp = Q.cache.data() + Q.emitted;
+        int64_t* oi = ids + b * static_cast<int64_t>(m);
+        float* os = scores + b * static_cast<int64_t>(m);
         for (int64_t j = 0; j < take; ++j) {
-            ids[static_cast<int64_t>(b) * m + j] = key_id(kp[j]);
-            scores[static_cast<int64_t>(b) * m + j] = key_score(kp[j]);
+            oi[j] = key_id(kp[j]);
+            os[j] = key_score(kp[j]);
         }
         Q.emitted += take;
-        st->stats.emitted += take;
+        took[b] = take;
         count[b] = static_cast<int32_t>(take);
         status[b] = (Q.emitted >= st->n_vis) ? EAHR_LIST_EXHAUSTED : EAHR_LIST_OPEN;
-    }
+    });
+    for (int32_t b = 0; b < B; ++b) st->stats.emitted += took[b];
     return EAHR_OK;
 }
 

@@ -107,6 +107,24 @@ def test_fuse_lists_rejects_a_repeated_id():
     assert ei.value.code == eahr.EAHR_E_INVALID
 
 
+@pytest.mark.parametrize("seed", range(6))
+def test_fuse_lists_one_list_closed_early(seed):
+    """The sparse list ends long before the dense one: later dense ranks are
+    joined against the closed list by id bitmap (Sec. 2.2 exhaustion: a closed
+    list contributes its complete ranking)."""
+    rng = np.random.default_rng(100 + seed)
+    n = 20000
+    a = rng.permutation(n)
+    b = rng.choice(n, size=int(rng.integers(30, 300)), replace=False)
+    for wts in ((1, 1), (2, 1), (1, 2)):
+        got, st = eahr.eahr_fuse_lists(a, b, K=20, w_dense=wts[0], w_sparse=wts[1])
+        assert list(got) == rrf.rrf_topk([a, b], list(wts), 60, 20)
+    # a repeat in the open list after the other closed is still rejected
+    bad = np.concatenate([a[:5000], a[100:101], a[5000:]])
+    with pytest.raises(eahr.EahrError):
+        eahr.eahr_fuse_lists(bad, b[:40], K=20, depth0=20)
+
+
 def test_fuse_lists_large_prefixes_equal_complete_rrf():
     """Deep prefixes (several table growths of the id bookkeeping): partially
     overlapping permutations of 200,000 ids."""
