@@ -10,6 +10,7 @@
 #include <cstdio>
 #include <cstring>
 #include <memory>
+#include <mutex>
 #include <new>
 #include <thread>
 #include <vector>
@@ -61,6 +62,36 @@ struct RawBuf {   // uninitialised growable host buffer
     }
 };
 
+// Per-call buffers of eahr_topk (fusion states, the rounds' dense and sparse
+// ranks), kept between calls so that their memory is reused rather than
+// faulted in again; concurrent calls each take their own.
+struct TopkWork {
+    std::vector<Fusion> F;
+    RawBuf<int64_t> dids;
+    RawBuf<float> dscores;
+    std::vector<std::vector<int64_t>> sids;
+    std::vector<std::vector<float>> sscores;
+};
+
+std::mutex g_work_mu;
+std::vector<std::unique_ptr<TopkWork>> g_work;
+
+struct WorkLease {
+    std::unique_ptr<TopkWork> w;
+    WorkLease() {
+        std::lock_guard<std::mutex> lk(g_work_mu);
+        if (!g_work.empty()) {
+            w = std::move(g_work.back());
+            g_work.pop_back();
+        }
+        if (!w) w.reset(new TopkWork());
+    }
+    ~WorkLease() {
+        std::lock_guard<std::mutex> lk(g_work_mu);
+        if (g_work.size() < 4) g_work.push_back(std::move(w));
+    }
+};
+
 }  // namespace
 
 extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index* sparse,
@@ -80,7 +111,11 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
     const bool prof = pvs_profile_on();
     double t_dense = 0, t_sparse = 0, t_fuse = 0;
 
-    std::vector<Fusion> F(B);
+    WorkLease lease;
+    TopkWork& W = *lease.w;
+    if (W.F.size() < static_cast<size_t>(B)) W.F.resize(B);
+    for (int32_t b = 0; b < B; ++b) W.F[b].reset();
+    Fusion* F = W.F.data();
     std::vector<int32_t> dstat(B, EAHR_LIST_EXHAUSTED), sstat(B, EAHR_LIST_EXHAUSTED);
     std::vector<int32_t> rounds(B, 0);
     std::vector<uint8_t> failed(B, 0);
@@ -106,12 +141,16 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
         cl.sp.assign(B, nullptr);
         for (int32_t b = 0; b < B; ++b) EAHR_TRY(pbm_open(sparse, &q_sparse[b], &cl.sp[b]));
     }
-    RawBuf<int64_t> dids;
-    RawBuf<float> dscores;
+    RawBuf<int64_t>& dids = W.dids;
+    RawBuf<float>& dscores = W.dscores;
     std::vector<int32_t> dcnt(B, 0), dsts(B);
     std::vector<uint8_t> dact(B, 0);
-    std::vector<std::vector<int64_t>> sids(B);
-    std::vector<std::vector<float>> sscores(B);
+    if (W.sids.size() < static_cast<size_t>(B)) {
+        W.sids.resize(B);
+        W.sscores.resize(B);
+    }
+    auto& sids = W.sids;
+    auto& sscores = W.sscores;
     std::vector<int32_t> scnt(B, 0), ssts(B, EAHR_LIST_OPEN);
     std::vector<uint8_t> sact(B, 0);
     std::vector<int> sparse_rc(B, EAHR_OK);

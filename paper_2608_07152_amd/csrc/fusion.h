@@ -202,6 +202,23 @@ struct Fusion {
 
     bool fixed(int64_t x) const { return std::find(A.begin(), A.end(), x) != A.end(); }
 
+    // Back to an empty fusion with both lists open, keeping the memory.
+    void reset() {
+        for (auto& l : L) {
+            l.ids.clear();
+            l.by_id.clear();
+            l.alive.clear();
+            l.open = true;
+            l.cursor = 0;
+        }
+        both.clear();
+        A.clear();
+        resolved = false;
+        dup = false;
+        bitmaps = false;
+        for (auto& b : seen) std::fill(b.begin(), b.end(), 0ull);
+    }
+
     // Append n ranks to list i (ids must be new to the list, else dup is set
     // and the bookkeeping is no longer meaningful).
     void append(int i, const int64_t* ids, int64_t n) {

@@ -73,6 +73,10 @@ extern "C" int pbm_build(const int64_t* term_ptr, int32_t vocab, const int32_t* 
     return EAHR_OK;
 }
 
+pbm_index::~pbm_index() {
+    for (pbm_state* st : free_states) delete st;
+}
+
 extern "C" void pbm_free(pbm_index* ix) { delete ix; }
 
 extern "C" int pbm_debug_set_blockmax(pbm_index* ix, int32_t term, int64_t range, float value) {
@@ -91,8 +95,17 @@ extern "C" int pbm_open(const pbm_index* ix, const eahr_sparse_query* q, pbm_sta
     *out = nullptr;
     if (!ix || !q || q->n_terms < 0 || (q->n_terms > 0 && (!q->terms || !q->weights)))
         EAHR_FAIL(EAHR_E_INVALID, "pbm_open: bad arguments");
-    std::unique_ptr<pbm_state> st(new (std::nothrow) pbm_state());
+    std::unique_ptr<pbm_state> st;
+    {
+        std::lock_guard<std::mutex> lk(ix->free_mu);
+        if (!ix->free_states.empty()) {
+            st.reset(ix->free_states.back());
+            ix->free_states.pop_back();
+        }
+    }
+    if (!st) st.reset(new (std::nothrow) pbm_state());
     if (!st) EAHR_FAIL(EAHR_E_OOM, "pbm_open: host allocation");
+    st->reset();
     st->ix = ix;
     std::vector<std::pair<int32_t, float>> tw;
     for (int32_t i = 0; i < q->n_terms; ++i) {
@@ -329,4 +342,17 @@ extern "C" int pbm_next(pbm_state* st, int32_t m, int64_t* ids, float* scores, i
     return EAHR_OK;
 }
 
-extern "C" void pbm_close(pbm_state* st) { delete st; }
+// Closed states go back to their index for reuse (up to this many).
+constexpr size_t kFreeStates = 1024;
+
+extern "C" void pbm_close(pbm_state* st) {
+    if (!st) return;
+    if (st->ix) {
+        std::lock_guard<std::mutex> lk(st->ix->free_mu);
+        if (st->ix->free_states.size() < kFreeStates) {
+            st->ix->free_states.push_back(st);
+            return;
+        }
+    }
+    delete st;
+}

@@ -1,6 +1,7 @@
 // Host structures of the Posting Block-Max sparse channel.
 #pragma once
 #include <cstdint>
+#include <mutex>
 #include <vector>
 
 #include "eahr.h"
@@ -18,6 +19,11 @@ struct pbm_index {
     std::vector<int64_t> bm_range;   // range number
     std::vector<float> bm_max;       // m_t(R)
     std::vector<int64_t> bm_off;     // first posting of the term inside the range
+    // closed states kept for reuse by later pbm_open calls (their vectors
+    // keep their memory)
+    mutable std::mutex free_mu;
+    mutable std::vector<struct pbm_state*> free_states;
+    ~pbm_index();
 };
 
 struct pbm_state {
@@ -48,4 +54,20 @@ struct pbm_state {
     int64_t ranges_expanded = 0;
     int64_t postings_visited = 0;
     bool failed = false;
+
+    // empty state for another query, keeping the memory
+    void reset() {
+        terms.clear();
+        w.clear();
+        order.clear();
+        next = 0;
+        pool.clear();
+        ready.clear();
+        ready_pos = 0;
+        touched.clear();   // acc and seen are all zero after every expansion
+        emitted = 0;
+        ranges_expanded = 0;
+        postings_visited = 0;
+        failed = false;
+    }
 };

@@ -354,13 +354,27 @@ static void adopt_buffers(pvs_state* st, ScanBuffers& b) {
 #define PVS_MOVE_IN(f) st->f = b.f;
     PVS_BUFFER_FIELDS(PVS_MOVE_IN)
 #undef PVS_MOVE_IN
+    st->recycled.swap(b.caches);
     b = ScanBuffers{};
 }
+
+// Caches kept for the next state, at most this many bytes in all: reusing
+// their memory spares the page faults of fresh allocations.
+constexpr size_t kRecycleBytes = size_t(2) << 30;
 
 static void donate_buffers(pvs_state* st, ScanBuffers& b) {
 #define PVS_MOVE_OUT(f) b.f = st->f;
     PVS_BUFFER_FIELDS(PVS_MOVE_OUT)
 #undef PVS_MOVE_OUT
+    b.caches.clear();
+    size_t kept = 0;
+    for (auto& Q : st->q) {
+        const size_t bytes = Q.cache.capacity() * sizeof(uint64_t);
+        if (kept + bytes > kRecycleBytes) break;
+        kept += bytes;
+        Q.cache.clear();
+        b.caches.push_back(std::move(Q.cache));
+    }
     st->buf_nq = 0;
     st->buf_sample = 0;
     st->pool_cap = 0;
@@ -528,6 +542,9 @@ extern "C" int pvs_open(const pvs_index* ix, int64_t epoch, const float* q, int3
     dev_free(tmp);
     if (fl[0]) EAHR_FAIL(EAHR_E_NONFINITE, "pvs_open: non-finite value in a query");
     st->q.resize(B);
+    for (size_t b = 0; b < st->recycled.size() && b < static_cast<size_t>(B); ++b)
+        st->q[b].cache.swap(st->recycled[b]);
+    st->recycled.clear();
     const double NV = ix->nv_max, NEV = ix->nev_max, g = ix->gamma;
     for (int32_t b = 0; b < B; ++b) {
         auto& Q = st->q[b];

@@ -80,6 +80,8 @@ struct ScanBuffers {
     int32_t* h_counts = nullptr;
     uint64_t* h_packed = nullptr;
     int64_t h_packed_cap = 0;
+    // certified-rank caches of the closed state (emptied, capacity kept)
+    std::vector<std::vector<uint64_t>> caches;
 };
 
 struct pvs_index {
@@ -133,6 +135,7 @@ struct pvs_state {
     float *qscale = nullptr, *qnorm = nullptr, *qenorm = nullptr, *qhnorm = nullptr;
     uint32_t* qflags = nullptr;
     std::vector<Query> q;
+    std::vector<std::vector<uint64_t>> recycled;   // caches adopted from the index
     pvs_counters stats{};
     // per-query scan buffers, sized for buf_nq queries and buf_sample rows
     int32_t buf_nq = 0;
