@@ -141,6 +141,7 @@ typedef struct {
     double variant_ms[12];
     int64_t variant_launches[12];
     int64_t variant_bytes[12];
+    int64_t rescore_certified;   /* candidates certified by rescoring (keys written) */
 } pvs_profile;
 
 int pvs_profile_enable(int32_t on);   /* also clears the accumulators */

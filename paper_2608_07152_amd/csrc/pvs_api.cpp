@@ -414,11 +414,11 @@ static void free_buffers(ScanBuffers& b) {
 }
 
 // Per-query scan buffers for nq queries and samples of sample_ld rows.
-// counts layout: [total nq][cert nq][fail nq][offs nq + 1][need nq], then
-// from sub_counts_at(nq) the append counters of the candidate sub-regions,
-// nq * kSub of them, kCntStride ints apart.  h_counts mirrors the first
-// 5 nq + 1 entries.
-static size_t host_counts(int32_t nq) { return 5 * static_cast<size_t>(nq) + 1; }
+// counts layout: [total nq][cert nq][fail nq][offs nq + 1][need nq]
+// [rescore chunk base nq + 1], then from sub_counts_at(nq) the append
+// counters of the candidate sub-regions, nq * kSub of them, kCntStride ints
+// apart.  h_counts mirrors the first 6 nq + 2 entries.
+static size_t host_counts(int32_t nq) { return 6 * static_cast<size_t>(nq) + 2; }
 static size_t sub_counts_at(int32_t nq) { return (host_counts(nq) + 63) / 64 * 64; }
 static size_t all_counts(int32_t nq) {
     return sub_counts_at(nq) + static_cast<size_t>(nq) * pvs::kSub * pvs::kCntStride;
@@ -810,6 +810,7 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     int32_t* d_fail = st->counts + 2 * nq;
     int32_t* d_offs = st->counts + 3 * nq;
     int32_t* d_need = st->counts + 4 * nq + 1;
+    int32_t* d_cbase = st->counts + 5 * nq + 1;
     int32_t* d_sub = st->counts + sub_counts_at(nq);
     HIP_TRY(hipMemsetAsync(st->counts, 0, all_counts(nq) * sizeof(int32_t), s));
     pvs::ScanOut mo;
@@ -834,16 +835,20 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
 
     // 3. rescore, order and pack the certified ranks
     std::vector<int32_t> cand(st->h_counts, st->h_counts + nq);   // kept candidates
-    int64_t max_cnt = 0, kept = 0;
-    for (int32_t i = 0; i < nq; ++i) {
-        max_cnt = std::max<int64_t>(max_cnt, cand[i]);
-        kept += cand[i];
-    }
-    pvs::launch_rescore(v, st->qrows, st->scanq, nq, st->cand_row, st->cand_lo, st->cand_hi, d_sub,
-                        max_cnt, st->keys, d_cert, d_fail, s);
+    int64_t kept = 0;
+    for (int32_t i = 0; i < nq; ++i) kept += cand[i];
+    const int64_t chunks = pvs::rescore_chunks(cand.data(), nq);
+    pvs::launch_rescore(v, st->qrows, st->scanq, nq, d_cand, d_cbase, chunks, st->cand_row,
+                        st->cand_lo, st->cand_hi, d_sub, st->keys, d_cert, d_fail, s);
     EAHR_TRY(mark(4));
-    uint64_t* sorted = pvs::launch_segmented_sort(st->keys, st->keys_tmp, d_cand, st->scanq, nq, max_cnt, s);
-    pvs::launch_pack(sorted, d_cert, st->scanq, nq, max_cnt, d_offs, st->packed, s);
+    // only the certified keys are ordered
+    HIP_TRY(hipMemcpyAsync(st->h_counts + nq, d_cert, nq * sizeof(int32_t), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    int64_t max_cert = 0;
+    for (int32_t i = 0; i < nq; ++i) max_cert = std::max<int64_t>(max_cert, st->h_counts[nq + i]);
+    EAHR_TRY(mark(6));
+    uint64_t* sorted = pvs::launch_segmented_sort(st->keys, st->keys_tmp, d_cert, st->scanq, nq, max_cert, s);
+    pvs::launch_pack(sorted, d_cert, st->scanq, nq, max_cert, d_offs, st->packed, s);
     EAHR_TRY(mark(5));
     HIP_TRY(hipGetLastError());
     EAHR_TRY(ensure_host_packed(st, kept));
@@ -863,7 +868,7 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
         HIP_TRY(hipEventElapsedTime(&t[0], st->ev[0], st->ev[1]));
         HIP_TRY(hipEventElapsedTime(&t[1], st->ev[2], st->ev[3]));
         HIP_TRY(hipEventElapsedTime(&t[2], st->ev[3], st->ev[4]));
-        HIP_TRY(hipEventElapsedTime(&t[3], st->ev[4], st->ev[5]));
+        HIP_TRY(hipEventElapsedTime(&t[3], st->ev[6], st->ev[5]));
         std::lock_guard<std::mutex> lk(g_prof_mu);
         g_prof.sample_ms += t[0];
         g_prof.scan_ms += t[1];
@@ -883,6 +888,7 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
         g_prof.variant_bytes[v] += launches * pass_bytes;
         g_prof.rescore_ms += t[2];
         g_prof.rescore_rows += kept;
+        for (int32_t i = 0; i < nq; ++i) g_prof.rescore_certified += h_cert[i];
         g_prof.sort_ms += t[3];
         g_prof.scan_rounds += 1;
     }

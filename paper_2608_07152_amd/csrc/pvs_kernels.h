@@ -101,12 +101,17 @@ void launch_cand_totals(const int32_t* sub_cnt, const ScanQ* sq, int32_t nq, int
                         int32_t* need, hipStream_t stream);
 
 // Rescoring reads the kept candidates of every sub-region of a query in
-// sub-region order and writes their keys densely: key i of query b goes to
-// keys[cand_off + i], i < total[b].
+// sub-region order (total[b] of them, chunked by rescore_chunks) and appends
+// the keys of the certified ones at keys[cand_off + j], j < cert_cnt[b]
+// (cert_cnt zeroed by the caller; order of appends unspecified).  cbase is
+// device scratch of nq + 1 ints; chunks = rescore_chunks of the host copy of
+// total.
+int64_t rescore_chunks(const int32_t* total, int32_t nq);
 void launch_rescore(const IndexView& ix, const float* qrows, const ScanQ* sq, int32_t nq,
+                    const int32_t* total, int32_t* cbase, int64_t chunks,
                     const int32_t* cand_row, const float* cand_lo, const float* cand_hi,
-                    const int32_t* sub_cnt, int64_t max_cnt, uint64_t* keys, int32_t* cert_cnt,
-                    int32_t* fail, hipStream_t stream);
+                    const int32_t* sub_cnt, uint64_t* keys, int32_t* cert_cnt, int32_t* fail,
+                    hipStream_t stream);
 
 // Sorts every query's candidate keys (cnt[b] keys from cand_off) ascending;
 // returns the buffer holding the result (keys or tmp).

@@ -1,33 +1,64 @@
 // Candidate rescoring, ordering and packing of the PVS dense channel.
 //
 // Every candidate gets its authoritative float32 score (row_score, one fixed
-// order), is checked against its interval (App. A.1: a score outside it fails
-// the request), and receives a 64-bit sort key.  A scan with threshold tau
-// certifies exactly the candidates with s32 >= tau whose key follows the last
-// certified key; their keys are (~mono(s32) << 32 | row), so ascending keys
-// are (score descending, id ascending).  Other candidates get (~0 << 32 | row)
-// and sort after every certified one.  Keys are unique inside a query.
+// order) and is checked against its interval (App. A.1: a score outside it
+// fails the request).  A scan with threshold tau certifies exactly the
+// candidates with s32 >= tau whose key follows the last certified key; their
+// keys (~mono(s32) << 32 | row) are appended to the query's key region, so
+// ascending keys are (score descending, id ascending).  Keys are unique
+// inside a query; the segmented sort orders each query's certified keys.
 #include "pvs_device.h"
 
 namespace pvs {
 
-// One wavefront per candidate; grid.y = query.  Candidate i of the query
-// (sub-region order) lives in sub-region s with first[s] <= i < last[s]:
-// lane s holds first[s] and last[s] (a prefix sum of the kept counts), and a
-// ballot finds s.
+// Candidates of a scan round are cut into chunks of kRescoreChunk per query;
+// cbase[b] is the first chunk of query b (exclusive prefix over the queries).
+constexpr int kRescoreChunk = 256;
+
+__global__ __launch_bounds__(64) void k_chunk_base(const int32_t* __restrict__ total, int32_t nq,
+                                                   int32_t* __restrict__ cbase) {
+    if (threadIdx.x == 0) {
+        int32_t acc = 0;
+        for (int b = 0; b < nq; ++b) {
+            cbase[b] = acc;
+            acc += (total[b] + kRescoreChunk - 1) / kRescoreChunk;
+        }
+        cbase[nq] = acc;
+    }
+}
+
+// One workgroup per chunk, one wavefront per quarter of it, R candidates in
+// flight per wavefront (one candidate per wavefront pass: lane l holds
+// elements 256 t + 4 l + i of the row, the fixed order of row_score).
+// Candidate i of a query (sub-region order) lives in sub-region s with
+// first[s] <= i < last[s]: lane s holds first[s] and last[s] (a prefix sum of
+// the kept counts), and a ballot finds s.  Only certified candidates produce
+// a key: s32 >= tau and the key (~mono(s32) << 32 | row) after the last
+// certified key; a wavefront collects its keys in lanes 0.. and appends them
+// to the query's key region with one atomic.
 template <int J>
 __global__ __launch_bounds__(256) void k_rescore(
     const float4* __restrict__ rows, int32_t df4, const float4* __restrict__ qrows,
-    const ScanQ* __restrict__ sq, const int32_t* __restrict__ cand_row,
-    const float* __restrict__ cand_lo, const float* __restrict__ cand_hi,
-    const int32_t* __restrict__ sub_cnt, uint64_t* __restrict__ keys,
-    int32_t* __restrict__ cert_cnt, int32_t* __restrict__ fail) {
+    const ScanQ* __restrict__ sq, int32_t nq, const int32_t* __restrict__ cbase,
+    const int32_t* __restrict__ cand_row, const float* __restrict__ cand_lo,
+    const float* __restrict__ cand_hi, const int32_t* __restrict__ sub_cnt,
+    uint64_t* __restrict__ keys, int32_t* __restrict__ cert_cnt, int32_t* __restrict__ fail) {
     static_assert(kSub == 64, "one lane per sub-region");
+    constexpr int PER_WAVE = kRescoreChunk / 4;
+    static_assert(PER_WAVE <= 64, "one key per lane");
     const int lane = threadIdx.x & 63;
-    const int b = blockIdx.y;
+    const int wave = threadIdx.x >> 6;
+    // the query of this chunk: the last b with cbase[b] <= chunk (that query
+    // has chunks, as cbase[b + 1] > chunk)
+    const int x = blockIdx.x;
+    int blo = 0, bhi = nq;
+    while (bhi - blo > 1) {
+        const int mid = (blo + bhi) >> 1;
+        if (cbase[mid] <= x) blo = mid;
+        else bhi = mid;
+    }
+    const int b = blo;
     const ScanQ Q = sq[b];
-    float4 qv[J];
-    load_query_row<J>(qrows, Q.qi, df4, lane, qv);
     const int c = sub_cnt[(b * kSub + lane) * kCntStride];
     const int kept = static_cast<int>(c < Q.cand_cap ? c : Q.cand_cap);
     int last = kept;
@@ -37,6 +68,11 @@ __global__ __launch_bounds__(256) void k_rescore(
     }
     const int first = last - kept;
     const int64_t n = __builtin_amdgcn_readlane(last, 63);
+    const int64_t i_begin = static_cast<int64_t>(x - cbase[b]) * kRescoreChunk + wave * PER_WAVE;
+    const int64_t i_end = (i_begin + PER_WAVE < n) ? i_begin + PER_WAVE : n;
+    if (i_begin >= i_end) return;
+    float4 qv[J];
+    load_query_row<J>(qrows, Q.qi, df4, lane, qv);
     // slot of candidate i (uniform across the wavefront)
     auto slot_of = [&](int64_t i) -> int64_t {
         const uint64_t m = __ballot(first <= i && i < last);
@@ -44,21 +80,19 @@ __global__ __launch_bounds__(256) void k_rescore(
         const int f = __builtin_amdgcn_readlane(first, s);
         return Q.cand_off + static_cast<int64_t>(s) * Q.cand_cap + (i - f);
     };
-    int local_cert = 0;
-    // R candidates per wavefront iteration keep R * J 16-byte loads in flight
     constexpr int R = (J <= 4) ? 4 : 1;
-    const int64_t wave = __builtin_amdgcn_readfirstlane(
-        static_cast<int>(blockIdx.x * 4 + (threadIdx.x >> 6)));
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * 4 * R;
-    for (int64_t i0 = wave * R; i0 < n; i0 += stride) {
+    uint64_t mykey = 0;
+    int nk = 0;          // certified keys collected (lanes 0 .. nk - 1)
+    bool bad = false;
+    for (int64_t i0 = i_begin; i0 < i_end; i0 += R) {
         int32_t row[R];
         int64_t src[R];
         float4 v[R][J];
 #pragma unroll
         for (int k = 0; k < R; ++k) {
             const int64_t i = i0 + k;
-            src[k] = (i < n) ? slot_of(i) : 0;
-            row[k] = (i < n) ? cand_row[src[k]] : -1;
+            src[k] = (i < i_end) ? slot_of(i) : 0;
+            row[k] = (i < i_end) ? cand_row[src[k]] : -1;
             const float4* rp = rows + static_cast<int64_t>(row[k] < 0 ? 0 : row[k]) * df4;
 #pragma unroll
             for (int t = 0; t < J; ++t) {
@@ -68,12 +102,7 @@ __global__ __launch_bounds__(256) void k_rescore(
         }
 #pragma unroll
         for (int k = 0; k < R; ++k) {
-            if (i0 + k >= n) break;
-            if (row[k] < 0) {   // sentinel slot: a unique key after every real one
-                if (lane == 0)
-                    keys[Q.cand_off + i0 + k] = ~0ull - static_cast<uint64_t>(i0 + k);
-                continue;
-            }
+            if (row[k] < 0) continue;   // past the chunk, or a sentinel slot
             // same accumulation order as row_score: (t, x, y, z, w), then the butterfly
             float acc = 0.0f;
 #pragma unroll
@@ -86,47 +115,56 @@ __global__ __launch_bounds__(256) void k_rescore(
                 }
             }
             for (int off = 32; off > 0; off >>= 1) acc = acc + __shfl_xor(acc, off, 64);
-            const float s = acc;
-            if (lane == 0) {
-                const int64_t at = Q.cand_off + i0 + k;
-                const float lo = cand_lo[src[k]];
-                const float hi = cand_hi[src[k]];
-                if (!(lo <= s && s <= hi)) fail[b] = 1;
-                const bool dropped =
-                    Q.has_cert && (s > Q.s_cert || (s == Q.s_cert && row[k] <= Q.id_cert));
-                const bool cert = !dropped && s >= Q.tau;
-                const uint64_t hiw = cert ? static_cast<uint64_t>(~mono32(s)) : 0xffffffffull;
-                keys[at] = (hiw << 32) | static_cast<uint32_t>(row[k]);
-                local_cert += cert;
+            const float s = acc;   // identical in every lane
+            const float lo = cand_lo[src[k]];
+            const float hi = cand_hi[src[k]];
+            bad |= !(lo <= s && s <= hi);
+            const bool dropped =
+                Q.has_cert && (s > Q.s_cert || (s == Q.s_cert && row[k] <= Q.id_cert));
+            if (!dropped && s >= Q.tau) {
+                if (lane == nk)
+                    mykey = (static_cast<uint64_t>(~mono32(s)) << 32) | static_cast<uint32_t>(row[k]);
+                ++nk;
             }
         }
     }
-    if (lane == 0 && local_cert) atomicAdd(&cert_cnt[b], local_cert);
+    if (bad && lane == 0) fail[b] = 1;
+    if (nk == 0) return;
+    int base = 0;
+    if (lane == 0) base = atomicAdd(&cert_cnt[b], nk);
+    base = __shfl(base, 0, 64);
+    if (lane < nk) keys[Q.cand_off + base + lane] = mykey;
 }
 
 template <int J>
 static void rescore_j(const IndexView& ix, const float* qrows, const ScanQ* sq, int32_t nq,
-                      const int32_t* cand_row, const float* cand_lo, const float* cand_hi,
-                      const int32_t* sub_cnt, int64_t max_cnt, uint64_t* keys, int32_t* cert_cnt,
-                      int32_t* fail, hipStream_t stream) {
-    int64_t gx = (max_cnt + 3) / 4;
-    if (gx > 4096) gx = 4096;
-    if (gx < 1) gx = 1;
-    hipLaunchKernelGGL((k_rescore<J>), dim3(static_cast<uint32_t>(gx), nq), dim3(256), 0, stream,
+                      const int32_t* cbase, int64_t chunks, const int32_t* cand_row,
+                      const float* cand_lo, const float* cand_hi, const int32_t* sub_cnt,
+                      uint64_t* keys, int32_t* cert_cnt, int32_t* fail, hipStream_t stream) {
+    hipLaunchKernelGGL((k_rescore<J>), dim3(static_cast<uint32_t>(chunks)), dim3(256), 0, stream,
                        reinterpret_cast<const float4*>(ix.rows), ix.df / 4,
-                       reinterpret_cast<const float4*>(qrows), sq, cand_row, cand_lo, cand_hi,
-                       sub_cnt, keys, cert_cnt, fail);
+                       reinterpret_cast<const float4*>(qrows), sq, nq, cbase, cand_row, cand_lo,
+                       cand_hi, sub_cnt, keys, cert_cnt, fail);
+}
+
+int64_t rescore_chunks(const int32_t* total, int32_t nq) {
+    int64_t c = 0;
+    for (int32_t b = 0; b < nq; ++b) c += (total[b] + kRescoreChunk - 1) / kRescoreChunk;
+    return c;
 }
 
 void launch_rescore(const IndexView& ix, const float* qrows, const ScanQ* sq, int32_t nq,
+                    const int32_t* total, int32_t* cbase, int64_t chunks,
                     const int32_t* cand_row, const float* cand_lo, const float* cand_hi,
-                    const int32_t* sub_cnt, int64_t max_cnt, uint64_t* keys, int32_t* cert_cnt,
-                    int32_t* fail, hipStream_t stream) {
-    if (nq <= 0 || max_cnt <= 0) return;
+                    const int32_t* sub_cnt, uint64_t* keys, int32_t* cert_cnt, int32_t* fail,
+                    hipStream_t stream) {
+    if (nq <= 0) return;
+    hipLaunchKernelGGL(k_chunk_base, dim3(1), dim3(64), 0, stream, total, nq, cbase);
+    if (chunks <= 0) return;
 #define PVS_RS(N)                                                                              \
     case N:                                                                                    \
-        rescore_j<N>(ix, qrows, sq, nq, cand_row, cand_lo, cand_hi, sub_cnt, max_cnt, keys,    \
-                     cert_cnt, fail, stream);                                                  \
+        rescore_j<N>(ix, qrows, sq, nq, cbase, chunks, cand_row, cand_lo, cand_hi, sub_cnt,    \
+                     keys, cert_cnt, fail, stream);                                            \
         break;
     switch (row_chunks(ix.df)) {
         PVS_RS(1)
