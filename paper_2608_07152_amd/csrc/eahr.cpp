@@ -19,6 +19,7 @@
 #include "eahr.h"
 #include "fusion.h"
 #include "host_parallel.h"
+#include "pbm_internal.h"
 #include "pvs_internal.h"
 
 namespace {
@@ -154,6 +155,20 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
     std::vector<int32_t> scnt(B, 0), ssts(B, EAHR_LIST_OPEN);
     std::vector<uint8_t> sact(B, 0);
     std::vector<int> sparse_rc(B, EAHR_OK);
+    // sparse work order: the queries with the most postings first, so that
+    // the last ones a round waits for are short (their first call scores
+    // about their postings)
+    std::vector<int32_t> sorder(B);
+    for (int32_t b = 0; b < B; ++b) sorder[b] = b;
+    std::vector<int64_t> cost(B, 1);
+    if (use_sparse) {
+        for (int32_t b = 0; b < B; ++b)
+            for (int32_t i = 0; i < q_sparse[b].n_terms; ++i) {
+                const int32_t t = q_sparse[b].terms[i];
+                if (t >= 0 && t < sparse->vocab) cost[b] += sparse->term_ptr[t + 1] - sparse->term_ptr[t];
+            }
+        std::stable_sort(sorder.begin(), sorder.end(), [&](int32_t a, int32_t c) { return cost[a] > cost[c]; });
+    }
     int64_t depth = ep.depth0;
     double fill_ms = 0.0;            // measured cost of dense work-ahead
     int64_t fill_ranks = 0;
@@ -179,18 +194,22 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
         // sparse channel on worker threads while the dense channel runs on the GPU
         std::thread sparse_thread;
         std::atomic<bool> sparse_done{false};
-        std::atomic<int64_t> sparse_finished{0};
+        std::atomic<int64_t> sparse_cost_done{0};   // postings of the queries finished
+        int64_t sparse_cost = 0;
+        for (int32_t b = 0; b < B; ++b)
+            if (sact[b]) sparse_cost += cost[b];
         const auto t_sparse0 = std::chrono::steady_clock::now();
         auto sparse_work = [&]() {
             const auto t0 = std::chrono::steady_clock::now();
-            parallel_for(B, std::max(1, threads - 1), [&](int64_t b) {
+            parallel_for(B, std::max(1, threads - 1), [&](int64_t i) {
+                const int32_t b = sorder[i];
                 if (!sact[b]) return;
                 const int64_t need = std::min<int64_t>(depth - static_cast<int64_t>(F[b].L[1].size()), 1LL << 30);
                 sids[b].resize(static_cast<size_t>(need));
                 sscores[b].resize(static_cast<size_t>(need));
                 sparse_rc[b] = pbm_next(cl.sp[b], static_cast<int32_t>(need), sids[b].data(),
                                         sscores[b].data(), &scnt[b], &ssts[b]);
-                sparse_finished.fetch_add(1, std::memory_order_relaxed);
+                sparse_cost_done.fetch_add(cost[b], std::memory_order_relaxed);
             });
             r_sparse = ms_since(t0);
             t_sparse += r_sparse;
@@ -208,20 +227,18 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
             // While the sparse channel is still busy, certify the dense ranks
             // of the next depths ahead (they are served from the cache later;
             // the output does not depend on it).
-            int64_t nd = 0, ns = 0;
-            for (int32_t b = 0; b < B; ++b) {
-                nd += dact[b];
-                ns += sact[b];
-            }
+            int64_t nd = 0;
+            for (int32_t b = 0; b < B; ++b) nd += dact[b];
             const int64_t cap = std::min<int64_t>(kFillMaxDepth, kFillBudget / std::max<int64_t>(nd, 1));
             int64_t ahead = depth;
             while (dense_rc == EAHR_OK && sparse_thread.joinable() && ahead <= cap / ep.growth &&
                    !sparse_done.load(std::memory_order_acquire)) {
-                // remaining sparse time: from the finished share, or (none
-                // finished yet) at least the time it has run so far
-                const int64_t fin = sparse_finished.load(std::memory_order_relaxed);
+                // remaining sparse time: from the share of postings of the
+                // finished queries (a first call scores about its postings),
+                // or (none finished yet) at least the time it has run so far
+                const int64_t fin = sparse_cost_done.load(std::memory_order_relaxed);
                 const double run = ms_since(t_sparse0);
-                const double left = fin > 0 ? run * static_cast<double>(ns - fin) / fin : run;
+                const double left = fin > 0 ? run * static_cast<double>(sparse_cost - fin) / fin : run;
                 const double rate = fill_ranks > 0 ? fill_ms / static_cast<double>(fill_ranks) : 0.0;
                 const double est = rate * static_cast<double>((ahead * ep.growth - ahead) * nd);
                 if (est > left) break;
@@ -233,6 +250,13 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
                     fill_ms += ms_since(tf);
                     fill_ranks += added;
                 }
+                if (::eahr::trace_on())
+                    std::fprintf(stderr,
+                                 "eahr fill depth=%lld sparse_postings_done=%lld/%lld sparse_left_ms=%.2f "
+                                 "est_ms=%.2f added=%lld fill_ms=%.2f\n",
+                                 static_cast<long long>(ahead), static_cast<long long>(fin),
+                                 static_cast<long long>(sparse_cost), left, est,
+                                 static_cast<long long>(added), ms_since(tf));
             }
             r_dense = ms_since(t0);
             t_dense += r_dense;

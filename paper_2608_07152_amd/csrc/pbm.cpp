@@ -256,28 +256,47 @@ static void sort_keys(std::vector<uint64_t>& a) {
     }
 }
 
-// Expansion visits ranges in bound order, i.e. at scattered addresses:
-// prefetch the block-max offsets of the range two ahead and the postings of
-// the range one ahead.
-static inline void prefetch_ahead(const pbm_state* st) {
-    const pbm_index* ix = st->ix;
-    const size_t nr = static_cast<size_t>(ix->n_ranges);
-    for (size_t ahead = 1; ahead <= 2; ++ahead) {
-        const size_t j = st->next + ahead;
-        if (j >= st->order.size()) return;
-        const int64_t r = st->order[j].r;
-        for (size_t i = 0; i < st->terms.size(); ++i) {
-            const int64_t e = st->ent[i * nr + r];
-            if (e < 0) continue;
-            if (ahead == 2) {
-                __builtin_prefetch(&ix->bm_off[e]);
-            } else {
-                const int64_t p = ix->bm_off[e];
-                __builtin_prefetch(&ix->docs[p]);
-                __builtin_prefetch(&ix->imp[p]);
-            }
+// Ranges are expanded in batches: the next `batch` ranges of the bound order,
+// visited in id order so that each term's postings are read front to back.
+// Expanding a range beyond the ones the stopping rule needs only adds work;
+// publication still waits for the bound of the first unexpanded range.  The
+// batch doubles (kBatchMin .. kBatchMax) while a refill goes on.
+constexpr size_t kBatchMin = 8;
+constexpr size_t kBatchMax = 1024;
+
+// Move the publishable pool items (keys below the bound key bk) to the
+// ready run, sorted.  When far more are publishable than wanted, only the
+// smallest keys go (at least kPublishMin and 4 * want, cut at a boundary of
+// the top 16 key bits found from one histogram pass): they are still the
+// smallest keys of everything unpublished, and the rest stay pooled for a
+// later refill, so a query whose every range had to be expanded does not
+// sort its whole scored set up front.
+constexpr size_t kPublishMin = 65536;
+
+static void publish(pbm_state* st, uint64_t bk, size_t want) {
+    auto& pool = st->pool;
+    const auto mid = std::partition(pool.begin(), pool.end(), [bk](uint64_t k) { return k < bk; });
+    const size_t np = static_cast<size_t>(mid - pool.begin());
+    const size_t take = std::max(kPublishMin, 4 * want);
+    auto cut_end = mid;
+    if (np > take + take / 2) {
+        thread_local std::vector<uint32_t> hist;
+        hist.assign(65536, 0u);
+        for (auto it = pool.begin(); it != mid; ++it) ++hist[*it >> 48];
+        size_t cum = 0;
+        uint32_t cut = 0;
+        for (; cut < 65535; ++cut) {
+            cum += hist[cut];
+            if (cum >= take) break;
+        }
+        if (cut < 65535) {
+            const uint64_t lim = static_cast<uint64_t>(cut + 1) << 48;
+            cut_end = std::partition(pool.begin(), mid, [lim](uint64_t k) { return k < lim; });
         }
     }
+    st->ready.assign(pool.begin(), cut_end);
+    pool.erase(pool.begin(), cut_end);
+    sort_keys(st->ready);
 }
 
 // Refill the ready run with at least `want` publishable items when the
@@ -289,6 +308,8 @@ static bool refill(pbm_state* st, size_t want) {
     st->ready.clear();
     st->ready_pos = 0;
     size_t checked = 0;
+    size_t batch = kBatchMin;
+    std::vector<pbm_state::Range>& run = st->batch;
     for (;;) {
         if (!ranges_left(st)) break;
         if (st->pool.size() >= want && st->pool.size() >= checked + checked / 2) {
@@ -298,16 +319,18 @@ static bool refill(pbm_state* st, size_t want) {
             if (n >= want) break;
             checked = st->pool.size();
         }
-        prefetch_ahead(st);
-        const auto R = st->order[st->next++];
-        st->ranges_expanded += 1;
-        if (!expand(st, R)) return false;
+        const size_t take = std::min(batch, st->order.size() - st->next);
+        run.assign(st->order.begin() + st->next, st->order.begin() + st->next + take);
+        st->next += take;
+        std::sort(run.begin(), run.end(),
+                  [](const pbm_state::Range& a, const pbm_state::Range& b) { return a.r < b.r; });
+        for (const auto& R : run) {
+            st->ranges_expanded += 1;
+            if (!expand(st, R)) return false;
+        }
+        batch = std::min(batch * 2, kBatchMax);
     }
-    const uint64_t bk = bound_key(st);
-    auto mid = std::partition(st->pool.begin(), st->pool.end(), [bk](uint64_t k) { return k < bk; });
-    st->ready.assign(st->pool.begin(), mid);
-    st->pool.erase(st->pool.begin(), mid);
-    sort_keys(st->ready);
+    publish(st, bound_key(st), want);
     return true;
 }
 

@@ -39,6 +39,7 @@ struct pbm_state {
     // unexpanded ranges.
     std::vector<Range> order;
     size_t next = 0;
+    std::vector<Range> batch;     // ranges of the current expansion batch
     // ent[i * n_ranges + r]: block-max entry of terms[i] for range r, or -1
     std::vector<int64_t> ent;
     // Scored items as keys (~ord(S) << 32 | id): ascending keys are

@@ -96,3 +96,38 @@ def test_pbm_rejects_bad_postings():
         eahr.pbm_build(np.array([0, 1]), np.array([0], np.int32), np.array([-1.0], np.float32), 5, 2)
     with pytest.raises(eahr.EahrError):
         eahr.pbm_build(np.array([0, 1]), np.array([0], np.int32), np.array([np.inf], np.float32), 5, 2)
+
+
+def test_pbm_common_term_partial_publication():
+    """A term in most documents makes every range worth expanding, so far
+    more items become publishable than a request wants; they are published
+    in runs of the smallest keys.  The complete ranking, read in doubling
+    requests and in one request, equals the brute-force ranking."""
+    rng = np.random.default_rng(11)
+    n = 300_000
+    common = np.sort(rng.choice(n, size=250_000, replace=False)).astype(np.int32)
+    rare1 = np.sort(rng.choice(n, size=3_000, replace=False)).astype(np.int32)
+    rare2 = np.sort(rng.choice(n, size=5_000, replace=False)).astype(np.int32)
+    docs = np.concatenate([common, rare1, rare2])
+    imp = np.concatenate([rng.uniform(0.01, 0.05, len(common)), rng.uniform(1, 9, len(rare1)),
+                          rng.uniform(1, 9, len(rare2))]).astype(np.float32)
+    # a few exact ties across the common term
+    imp[:1000] = np.float32(0.03)
+    term_ptr = np.array([0, len(common), len(common) + len(rare1), len(docs)], dtype=np.int64)
+    post = datagen.Postings(3, term_ptr, docs, imp)
+    terms = np.array([0, 1, 2], np.int32)
+    wts = np.ones(3, np.float32)
+    want_ids, want_s = _oracle_ranking(post, n, terms, wts)
+    idx = eahr.pbm_build(term_ptr, docs, imp, n, 4096)
+    st = eahr.pbm_open(idx, terms, wts)
+    got_i, got_s, m, status = [], [], 20, eahr.LIST_OPEN
+    while status != eahr.LIST_EXHAUSTED:
+        ids, sc, status = eahr.pbm_next(st, m)
+        got_i.append(ids)
+        got_s.append(sc)
+        m *= 2
+    assert np.array_equal(np.concatenate(got_i), want_ids)
+    assert np.array_equal(np.concatenate(got_s), want_s)
+    st1 = eahr.pbm_open(idx, terms, wts)
+    ids, sc, status = eahr.pbm_next(st1, n + 1)
+    assert status == eahr.LIST_EXHAUSTED and np.array_equal(ids, want_ids)
