@@ -38,8 +38,12 @@ constexpr int64_t kTargetBudget = 8192;
 // kSpecBudget ranks per scan shared by its queries.  Rescoring a row costs
 // about 1/1000 of streaming the codes once, so over-certifying is cheap next
 // to an extra scan.
+// A scan certifies at least kSpecFloor ranks per query (within the same
+// budget): a round of a batch scan costs about as much as rescoring a few
+// thousand ranks per query, so shallow requests are served ahead.
 constexpr int64_t kSpecFactor = 8;
 constexpr int64_t kSpecBudget = int64_t(1) << 20;
+constexpr int64_t kSpecFloor = 4096;
 // Scans of at least this many queries use the Int8 MFMA kernel; smaller ones
 // the dot4 GEMV kernel, which streams the codes at the HBM rate for up to 8
 // queries in one pass.  EAHR_SCAN_PATH=gemv|mfma forces one path (testing).
