@@ -326,9 +326,7 @@ void pvs_state::release_scan_buffers() {
     dev_free(sample_lo);
     dev_free(sample_hi);
     dev_free(qfrag);
-    dev_free(cand_row);
-    dev_free(cand_lo);
-    dev_free(cand_hi);
+    dev_free(cand);
     dev_free(keys);
     dev_free(keys_tmp);
     dev_free(packed);
@@ -347,7 +345,7 @@ void pvs_state::release_scan_buffers() {
 // Move the scan buffers between a state and an index's spare slot.
 #define PVS_BUFFER_FIELDS(X)                                                                 \
     X(buf_nq) X(buf_sample) X(scanq) X(counts) X(sample_lo) X(sample_hi) X(qfrag) X(pool_cap) \
-    X(cand_row) X(cand_lo) X(cand_hi) X(keys) X(keys_tmp) X(packed) X(h_scanq) X(h_counts)    \
+    X(cand) X(keys) X(keys_tmp) X(packed) X(h_scanq) X(h_counts)    \
     X(h_packed) X(h_packed_cap)
 
 static void adopt_buffers(pvs_state* st, ScanBuffers& b) {
@@ -384,9 +382,7 @@ static void donate_buffers(pvs_state* st, ScanBuffers& b) {
     st->sample_lo = nullptr;
     st->sample_hi = nullptr;
     st->qfrag = nullptr;
-    st->cand_row = nullptr;
-    st->cand_lo = nullptr;
-    st->cand_hi = nullptr;
+    st->cand = nullptr;
     st->keys = nullptr;
     st->keys_tmp = nullptr;
     st->packed = nullptr;
@@ -401,9 +397,7 @@ static void free_buffers(ScanBuffers& b) {
     dev_free(b.sample_lo);
     dev_free(b.sample_hi);
     dev_free(b.qfrag);
-    dev_free(b.cand_row);
-    dev_free(b.cand_lo);
-    dev_free(b.cand_hi);
+    dev_free(b.cand);
     dev_free(b.keys);
     dev_free(b.keys_tmp);
     dev_free(b.packed);
@@ -457,17 +451,13 @@ static int ensure_pool(pvs_state* st, int64_t slots) {
     if (slots <= st->pool_cap) return EAHR_OK;
     slots = std::max<int64_t>(slots + slots / 4, pvs::kMinCap);
     HIP_TRY(hipStreamSynchronize(st->ix->stream));
-    dev_free(st->cand_row);
-    dev_free(st->cand_lo);
-    dev_free(st->cand_hi);
+    dev_free(st->cand);
     dev_free(st->keys);
     dev_free(st->keys_tmp);
     dev_free(st->packed);
     st->pool_cap = 0;
     const size_t n = static_cast<size_t>(slots);
-    EAHR_TRY(dev_alloc(&st->cand_row, n));
-    EAHR_TRY(dev_alloc(&st->cand_lo, n));
-    EAHR_TRY(dev_alloc(&st->cand_hi, n));
+    EAHR_TRY(dev_alloc(&st->cand, n));
     EAHR_TRY(dev_alloc(&st->keys, n));
     EAHR_TRY(dev_alloc(&st->keys_tmp, n));
     EAHR_TRY(dev_alloc(&st->packed, n));
@@ -815,9 +805,7 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     int32_t* d_sub = st->counts + sub_counts_at(nq);
     HIP_TRY(hipMemsetAsync(st->counts, 0, all_counts(nq) * sizeof(int32_t), s));
     pvs::ScanOut mo;
-    mo.cand_row = st->cand_row;
-    mo.cand_lo = st->cand_lo;
-    mo.cand_hi = st->cand_hi;
+    mo.cand = st->cand;
     mo.cand_cnt = d_sub;
     EAHR_TRY(mark(2));
     scan(false, mo, nq);
@@ -839,8 +827,8 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     int64_t kept = 0;
     for (int32_t i = 0; i < nq; ++i) kept += cand[i];
     const int64_t chunks = pvs::rescore_chunks(cand.data(), nq);
-    pvs::launch_rescore(v, st->qrows, st->scanq, nq, d_cand, d_cbase, chunks, st->cand_row,
-                        st->cand_lo, st->cand_hi, d_sub, st->keys, d_cert, d_fail, s);
+    pvs::launch_rescore(v, st->qrows, st->scanq, nq, d_cand, d_cbase, chunks, st->cand, ix->gamma,
+                        d_sub, st->keys, d_cert, d_fail, s);
     EAHR_TRY(mark(4));
     // only the certified keys are ordered
     HIP_TRY(hipMemcpyAsync(st->h_counts + nq, d_cert, nq * sizeof(int32_t), hipMemcpyDeviceToHost, s));

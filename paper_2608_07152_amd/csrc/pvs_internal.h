@@ -74,9 +74,7 @@ struct ScanBuffers {
     float* sample_hi = nullptr;
     void* qfrag = nullptr;
     int64_t pool_cap = 0;
-    int32_t* cand_row = nullptr;
-    float* cand_lo = nullptr;
-    float* cand_hi = nullptr;
+    uint2* cand = nullptr;          // (row, integer dot) per candidate slot
     uint64_t* keys = nullptr;
     uint64_t* keys_tmp = nullptr;
     uint64_t* packed = nullptr;
@@ -151,9 +149,7 @@ struct pvs_state {
     void* qfrag = nullptr;             // query codes in MFMA operand order
     // candidate pool (pool_cap slots) split into per-query regions per scan
     int64_t pool_cap = 0;
-    int32_t* cand_row = nullptr;
-    float* cand_lo = nullptr;
-    float* cand_hi = nullptr;
+    uint2* cand = nullptr;
     uint64_t* keys = nullptr;
     uint64_t* keys_tmp = nullptr;
     uint64_t* packed = nullptr;

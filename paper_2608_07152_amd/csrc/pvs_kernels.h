@@ -64,16 +64,16 @@ void launch_quantize(const float* src, int64_t nrows, int32_t d, int64_t src_str
 // -inf / -inf for ineligible rows.  Main pass: the candidates query b appends
 // to sub-region s go to slots cand_off + s * cand_cap + j, j < cand_cap, and
 // cand_cnt[(b * kSub + s) * kCntStride] counts every slot of sub-region s
-// handed out, including those past its end.  A slot may hold the sentinel
-// row -1 (part of a reserved slice left unused), which is no candidate.
+// handed out, including those past its end.  A slot holds the candidate's row
+// and its exact integer dot product (from which rescoring recomputes the
+// interval), or the sentinel row 0xffffffff (part of a reserved slice left
+// unused), which is no candidate.
 struct ScanOut {
     float* sample_lo = nullptr;
     float* sample_hi = nullptr;
     int64_t sample_ld = 0;
     int64_t sample_stride = 1;   // sampled blocks are multiples of this
-    int32_t* cand_row = nullptr;
-    float* cand_lo = nullptr;
-    float* cand_hi = nullptr;
+    uint2* cand = nullptr;   // (row, integer dot); row 0xffffffff marks a sentinel slot
     int32_t* cand_cnt = nullptr;
 };
 
@@ -109,9 +109,8 @@ void launch_cand_totals(const int32_t* sub_cnt, const ScanQ* sq, int32_t nq, int
 int64_t rescore_chunks(const int32_t* total, int32_t nq);
 void launch_rescore(const IndexView& ix, const float* qrows, const ScanQ* sq, int32_t nq,
                     const int32_t* total, int32_t* cbase, int64_t chunks,
-                    const int32_t* cand_row, const float* cand_lo, const float* cand_hi,
-                    const int32_t* sub_cnt, uint64_t* keys, int32_t* cert_cnt, int32_t* fail,
-                    hipStream_t stream);
+                    const uint2* cand, float gamma, const int32_t* sub_cnt, uint64_t* keys,
+                    int32_t* cert_cnt, int32_t* fail, hipStream_t stream);
 
 // Sorts every query's candidate keys (cnt[b] keys from cand_off) ascending;
 // returns the buffer holding the result (keys or tmp).

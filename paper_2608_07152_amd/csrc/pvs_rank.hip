@@ -2,7 +2,8 @@
 //
 // Every candidate gets its authoritative float32 score (row_score, one fixed
 // order) and is checked against its interval (App. A.1: a score outside it
-// fails the request).  A scan with threshold tau certifies exactly the
+// fails the request), recomputed here from the integer dot product the scan
+// recorded with the same arithmetic as the scan's, so identical to it.  A scan with threshold tau certifies exactly the
 // candidates with s32 >= tau whose key follows the last certified key; their
 // keys (~mono(s32) << 32 | row) are appended to the query's key region, so
 // ascending keys are (score descending, id ascending).  Keys are unique
@@ -40,9 +41,10 @@ template <int J>
 __global__ __launch_bounds__(256) void k_rescore(
     const float4* __restrict__ rows, int32_t df4, const float4* __restrict__ qrows,
     const ScanQ* __restrict__ sq, int32_t nq, const int32_t* __restrict__ cbase,
-    const int32_t* __restrict__ cand_row, const float* __restrict__ cand_lo,
-    const float* __restrict__ cand_hi, const int32_t* __restrict__ sub_cnt,
-    uint64_t* __restrict__ keys, int32_t* __restrict__ cert_cnt, int32_t* __restrict__ fail) {
+    const uint2* __restrict__ cand, const float* __restrict__ scale,
+    const float* __restrict__ vnorm, const float* __restrict__ enorm, float gamma,
+    const int32_t* __restrict__ sub_cnt, uint64_t* __restrict__ keys,
+    int32_t* __restrict__ cert_cnt, int32_t* __restrict__ fail) {
     static_assert(kSub == 64, "one lane per sub-region");
     constexpr int PER_WAVE = kRescoreChunk / 4;
     static_assert(PER_WAVE <= 64, "one key per lane");
@@ -86,14 +88,20 @@ __global__ __launch_bounds__(256) void k_rescore(
     bool bad = false;
     for (int64_t i0 = i_begin; i0 < i_end; i0 += R) {
         int32_t row[R];
-        int64_t src[R];
+        int32_t dot[R];
+        float sv[R], nv[R], nev[R];
         float4 v[R][J];
 #pragma unroll
         for (int k = 0; k < R; ++k) {
             const int64_t i = i0 + k;
-            src[k] = (i < i_end) ? slot_of(i) : 0;
-            row[k] = (i < i_end) ? cand_row[src[k]] : -1;
-            const float4* rp = rows + static_cast<int64_t>(row[k] < 0 ? 0 : row[k]) * df4;
+            const uint2 rec = (i < i_end) ? cand[slot_of(i)] : make_uint2(0xffffffffu, 0u);
+            row[k] = static_cast<int32_t>(rec.x);   // -1 past the chunk or for a sentinel
+            dot[k] = static_cast<int32_t>(rec.y);
+            const int64_t r = row[k] < 0 ? 0 : row[k];
+            sv[k] = scale[r];
+            nv[k] = vnorm[r];
+            nev[k] = enorm[r];
+            const float4* rp = rows + r * df4;
 #pragma unroll
             for (int t = 0; t < J; ++t) {
                 const int idx = 64 * t + lane;
@@ -116,8 +124,8 @@ __global__ __launch_bounds__(256) void k_rescore(
             }
             for (int off = 32; off > 0; off >>= 1) acc = acc + __shfl_xor(acc, off, 64);
             const float s = acc;   // identical in every lane
-            const float lo = cand_lo[src[k]];
-            const float hi = cand_hi[src[k]];
+            float lo, hi;
+            pair_interval(Q, sv[k], nv[k], nev[k], dot[k], gamma, lo, hi);
             bad |= !(lo <= s && s <= hi);
             const bool dropped =
                 Q.has_cert && (s > Q.s_cert || (s == Q.s_cert && row[k] <= Q.id_cert));
@@ -138,13 +146,13 @@ __global__ __launch_bounds__(256) void k_rescore(
 
 template <int J>
 static void rescore_j(const IndexView& ix, const float* qrows, const ScanQ* sq, int32_t nq,
-                      const int32_t* cbase, int64_t chunks, const int32_t* cand_row,
-                      const float* cand_lo, const float* cand_hi, const int32_t* sub_cnt,
-                      uint64_t* keys, int32_t* cert_cnt, int32_t* fail, hipStream_t stream) {
+                      const int32_t* cbase, int64_t chunks, const uint2* cand, float gamma,
+                      const int32_t* sub_cnt, uint64_t* keys, int32_t* cert_cnt, int32_t* fail,
+                      hipStream_t stream) {
     hipLaunchKernelGGL((k_rescore<J>), dim3(static_cast<uint32_t>(chunks)), dim3(256), 0, stream,
                        reinterpret_cast<const float4*>(ix.rows), ix.df / 4,
-                       reinterpret_cast<const float4*>(qrows), sq, nq, cbase, cand_row, cand_lo,
-                       cand_hi, sub_cnt, keys, cert_cnt, fail);
+                       reinterpret_cast<const float4*>(qrows), sq, nq, cbase, cand, ix.scale,
+                       ix.vnorm, ix.enorm, gamma, sub_cnt, keys, cert_cnt, fail);
 }
 
 int64_t rescore_chunks(const int32_t* total, int32_t nq) {
@@ -155,16 +163,15 @@ int64_t rescore_chunks(const int32_t* total, int32_t nq) {
 
 void launch_rescore(const IndexView& ix, const float* qrows, const ScanQ* sq, int32_t nq,
                     const int32_t* total, int32_t* cbase, int64_t chunks,
-                    const int32_t* cand_row, const float* cand_lo, const float* cand_hi,
-                    const int32_t* sub_cnt, uint64_t* keys, int32_t* cert_cnt, int32_t* fail,
-                    hipStream_t stream) {
+                    const uint2* cand, float gamma, const int32_t* sub_cnt, uint64_t* keys,
+                    int32_t* cert_cnt, int32_t* fail, hipStream_t stream) {
     if (nq <= 0) return;
     hipLaunchKernelGGL(k_chunk_base, dim3(1), dim3(64), 0, stream, total, nq, cbase);
     if (chunks <= 0) return;
 #define PVS_RS(N)                                                                              \
     case N:                                                                                    \
-        rescore_j<N>(ix, qrows, sq, nq, cbase, chunks, cand_row, cand_lo, cand_hi, sub_cnt,    \
-                     keys, cert_cnt, fail, stream);                                            \
+        rescore_j<N>(ix, qrows, sq, nq, cbase, chunks, cand, gamma, sub_cnt, keys, cert_cnt,  \
+                     fail, stream);                                                            \
         break;
     switch (row_chunks(ix.df)) {
         PVS_RS(1)

@@ -81,9 +81,7 @@ __global__ __launch_bounds__(256) void k_scan_gemv(
                     const int64_t pos = base + __popcll(mask & ((1ull << lane) - 1ull));
                     if (pos < Q.cand_cap) {
                         const int64_t at = Q.cand_off + sub * Q.cand_cap + pos;
-                        o.cand_row[at] = static_cast<int32_t>(row);
-                        o.cand_lo[at] = lo;
-                        o.cand_hi[at] = hi;
+                        o.cand[at] = make_uint2(static_cast<uint32_t>(row), static_cast<uint32_t>(acc[b]));
                     }
                 }
             }
@@ -279,12 +277,8 @@ __global__ __launch_bounds__(256) void k_scan_mfma(
                 const int rib = 32 * t + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
                 const int64_t row = blk * 64 + rib;
                 if (pos < Q.cand_cap) {
-                    float lo, hi;
-                    pair_interval(Q, svr[t][r], vnr[t][r], enr[t][r], acc[t][uu][r], gamma, lo, hi);
                     const int64_t at = Q.cand_off + sub * Q.cand_cap + pos;
-                    o.cand_row[at] = static_cast<int32_t>(row);
-                    o.cand_lo[at] = lo;
-                    o.cand_hi[at] = hi;
+                    o.cand[at] = make_uint2(static_cast<uint32_t>(row), static_cast<uint32_t>(acc[t][uu][r]));
                 }
                 ++pos;
             }
@@ -509,13 +503,9 @@ __global__ __launch_bounds__(256, 2) void k_scan_mfma_wide(
                             const int64_t row = blk * 64 + rib;
                             const int64_t pos = (j < room) ? old + j : nb + (j - room);
                             if (pos < Q.cand_cap) {
-                                float lo, hi;
-                                pair_interval(Q, s_meta[wave][0][rib], s_meta[wave][1][rib],
-                                              s_meta[wave][2][rib], acc[t][uu][r], gamma, lo, hi);
                                 const int64_t at = Q.cand_off + sub * Q.cand_cap + pos;
-                                o.cand_row[at] = static_cast<int32_t>(row);
-                                o.cand_lo[at] = lo;
-                                o.cand_hi[at] = hi;
+                                o.cand[at] = make_uint2(static_cast<uint32_t>(row),
+                                                        static_cast<uint32_t>(acc[t][uu][r]));
                             }
                             ++j;
                         }
@@ -529,7 +519,7 @@ __global__ __launch_bounds__(256, 2) void k_scan_mfma_wide(
     for (int b = tid; b < NQT * 32 && b < nq; b += 256) {
         const ScanQ Q = sq[b];
         const int64_t e = s_end[b] < Q.cand_cap ? s_end[b] : Q.cand_cap;
-        for (int64_t p = s_pos[b]; p < e; ++p) o.cand_row[Q.cand_off + sub * Q.cand_cap + p] = -1;
+        for (int64_t p = s_pos[b]; p < e; ++p) o.cand[Q.cand_off + sub * Q.cand_cap + p] = make_uint2(0xffffffffu, 0u);
     }
 }
 
