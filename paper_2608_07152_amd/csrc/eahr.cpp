@@ -12,6 +12,7 @@
 #include <memory>
 #include <mutex>
 #include <new>
+#include <string>
 #include <thread>
 #include <vector>
 
@@ -108,6 +109,7 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
     if (use_dense && (!dense || !q_dense)) EAHR_FAIL(EAHR_E_INVALID, "eahr_topk: dense channel missing");
     if (use_sparse && (!sparse || !q_sparse)) EAHR_FAIL(EAHR_E_INVALID, "eahr_topk: sparse channel missing");
     const Params P{ep.K, ep.k_rrf, {ep.w_dense, ep.w_sparse}};
+    const auto t_call = std::chrono::steady_clock::now();
     const int threads = host_threads();
     const bool prof = pvs_profile_on();
     double t_dense = 0, t_sparse = 0, t_fuse = 0;
@@ -137,11 +139,16 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
                 if (s) pbm_close(s);
         }
     } cl;
+    const auto t_open = std::chrono::steady_clock::now();
     if (use_dense) EAHR_TRY(pvs_open(dense, epoch, q_dense, B, q_ptr_kind, &cl.st));
+    const double open_dense_ms = ms_since(t_open);
+    // sparse states are opened by the sparse workers, at a query's first
+    // call; the queries are checked here
     if (use_sparse) {
+        for (int32_t b = 0; b < B; ++b) EAHR_TRY(pbm_check_query(sparse, &q_sparse[b]));
         cl.sp.assign(B, nullptr);
-        for (int32_t b = 0; b < B; ++b) EAHR_TRY(pbm_open(sparse, &q_sparse[b], &cl.sp[b]));
     }
+    if (::eahr::trace_on()) std::fprintf(stderr, "eahr open dense_ms=%.2f\n", open_dense_ms);
     RawBuf<int64_t>& dids = W.dids;
     RawBuf<float>& dscores = W.dscores;
     std::vector<int32_t> dcnt(B, 0), dsts(B);
@@ -155,6 +162,15 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
     std::vector<int32_t> scnt(B, 0), ssts(B, EAHR_LIST_OPEN);
     std::vector<uint8_t> sact(B, 0);
     std::vector<int> sparse_rc(B, EAHR_OK);
+    // error messages are per thread: a sparse worker's first one is carried
+    // back to the caller
+    std::mutex sparse_err_mu;
+    std::string sparse_err;
+    auto note_sparse_error = [&](int rc) {
+        if (rc == EAHR_OK) return;
+        std::lock_guard<std::mutex> lk(sparse_err_mu);
+        if (sparse_err.empty()) sparse_err = eahr_last_error();
+    };
     // sparse work order: the queries with the most postings first, so that
     // the last ones a round waits for are short (their first call scores
     // about their postings)
@@ -204,11 +220,20 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
             parallel_for(B, std::max(1, threads - 1), [&](int64_t i) {
                 const int32_t b = sorder[i];
                 if (!sact[b]) return;
+                if (!cl.sp[b]) {
+                    sparse_rc[b] = pbm_open(sparse, &q_sparse[b], &cl.sp[b]);
+                    if (sparse_rc[b] != EAHR_OK) {
+                        note_sparse_error(sparse_rc[b]);
+                        sparse_cost_done.fetch_add(cost[b], std::memory_order_relaxed);
+                        return;
+                    }
+                }
                 const int64_t need = std::min<int64_t>(depth - static_cast<int64_t>(F[b].L[1].size()), 1LL << 30);
                 sids[b].resize(static_cast<size_t>(need));
                 sscores[b].resize(static_cast<size_t>(need));
                 sparse_rc[b] = pbm_next(cl.sp[b], static_cast<int32_t>(need), sids[b].data(),
                                         sscores[b].data(), &scnt[b], &ssts[b]);
+                note_sparse_error(sparse_rc[b]);
                 sparse_cost_done.fetch_add(cost[b], std::memory_order_relaxed);
             });
             r_sparse = ms_since(t0);
@@ -263,7 +288,11 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
         }
         if (sparse_thread.joinable()) sparse_thread.join();
         EAHR_TRY(dense_rc);
-        for (int32_t b = 0; b < B; ++b) EAHR_TRY(sparse_rc[b]);
+        for (int32_t b = 0; b < B; ++b)
+            if (sparse_rc[b] != EAHR_OK) {
+                ::eahr::set_error("%s", sparse_err.c_str());
+                return sparse_rc[b];
+            }
         // merge this round's ranks and certify, one query per task
         const auto t0 = std::chrono::steady_clock::now();
         parallel_for(B, threads, [&](int64_t b) {
@@ -318,6 +347,18 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
         depth = (depth > (INT64_MAX / ep.growth)) ? INT64_MAX : depth * ep.growth;
     }
     if (prof) pvs_profile_add_host(t_dense, t_sparse, t_fuse);
+    if (::eahr::trace_on()) {
+        const auto tc = std::chrono::steady_clock::now();
+        if (cl.st) pvs_close(cl.st);
+        cl.st = nullptr;
+        const double cd = ms_since(tc);
+        for (auto*& sp : cl.sp) {
+            if (sp) pbm_close(sp);
+            sp = nullptr;
+        }
+        std::fprintf(stderr, "eahr close dense_ms=%.2f sparse_ms=%.2f call_ms=%.2f\n", cd,
+                     ms_since(tc) - cd, ms_since(t_call));
+    }
     bool any_failed = false;
     for (int32_t b = 0; b < B; ++b) {
         const auto& f = F[b];

@@ -90,11 +90,25 @@ extern "C" int pbm_debug_set_blockmax(pbm_index* ix, int32_t term, int64_t range
     EAHR_FAIL(EAHR_E_INVALID, "pbm_debug_set_blockmax: term has no postings in range");
 }
 
+int pbm_check_query(const pbm_index* ix, const eahr_sparse_query* q) {
+    if (!ix || !q || q->n_terms < 0 || (q->n_terms > 0 && (!q->terms || !q->weights)))
+        EAHR_FAIL(EAHR_E_INVALID, "pbm_open: bad arguments");
+    for (int32_t i = 0; i < q->n_terms; ++i) {
+        const int32_t t = q->terms[i];
+        const float w = q->weights[i];
+        if (t < 0 || t >= ix->vocab) EAHR_FAIL(EAHR_E_INVALID, "pbm_open: term id out of range");
+        if (!std::isfinite(w) || w < 0.0f) EAHR_FAIL(EAHR_E_INVALID, "pbm_open: weight must be finite and >= 0");
+    }
+    std::vector<int32_t> t(q->terms, q->terms + q->n_terms);
+    std::sort(t.begin(), t.end());
+    if (std::adjacent_find(t.begin(), t.end()) != t.end()) EAHR_FAIL(EAHR_E_INVALID, "pbm_open: duplicate term");
+    return EAHR_OK;
+}
+
 extern "C" int pbm_open(const pbm_index* ix, const eahr_sparse_query* q, pbm_state** out) {
     if (!out) EAHR_FAIL(EAHR_E_INVALID, "pbm_open: out is NULL");
     *out = nullptr;
-    if (!ix || !q || q->n_terms < 0 || (q->n_terms > 0 && (!q->terms || !q->weights)))
-        EAHR_FAIL(EAHR_E_INVALID, "pbm_open: bad arguments");
+    EAHR_TRY(pbm_check_query(ix, q));
     std::unique_ptr<pbm_state> st;
     {
         std::lock_guard<std::mutex> lk(ix->free_mu);
@@ -108,16 +122,8 @@ extern "C" int pbm_open(const pbm_index* ix, const eahr_sparse_query* q, pbm_sta
     st->reset();
     st->ix = ix;
     std::vector<std::pair<int32_t, float>> tw;
-    for (int32_t i = 0; i < q->n_terms; ++i) {
-        const int32_t t = q->terms[i];
-        const float w = q->weights[i];
-        if (t < 0 || t >= ix->vocab) EAHR_FAIL(EAHR_E_INVALID, "pbm_open: term id out of range");
-        if (!std::isfinite(w) || w < 0.0f) EAHR_FAIL(EAHR_E_INVALID, "pbm_open: weight must be finite and >= 0");
-        tw.emplace_back(t, w);
-    }
+    for (int32_t i = 0; i < q->n_terms; ++i) tw.emplace_back(q->terms[i], q->weights[i]);
     std::sort(tw.begin(), tw.end());
-    for (size_t i = 1; i < tw.size(); ++i)
-        if (tw[i].first == tw[i - 1].first) EAHR_FAIL(EAHR_E_INVALID, "pbm_open: duplicate term");
     for (auto& p : tw) {
         if (p.second == 0.0f) continue;   // a zero weight contributes exactly 0
         st->terms.push_back(p.first);

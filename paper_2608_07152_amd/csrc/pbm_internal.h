@@ -26,6 +26,11 @@ struct pbm_index {
     ~pbm_index();
 };
 
+// Checks a query against the index (term ids in range, weights finite and
+// non-negative, no term twice) as pbm_open does; EAHR_OK or the error code
+// with the message set.
+int pbm_check_query(const pbm_index* ix, const eahr_sparse_query* q);
+
 struct pbm_state {
     struct Range {
         float H;
