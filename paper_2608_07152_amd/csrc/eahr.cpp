@@ -293,8 +293,12 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
                 ::eahr::set_error("%s", sparse_err.c_str());
                 return sparse_rc[b];
             }
-        // merge this round's ranks and certify, one query per task
+        // merge this round's ranks and certify, one query per task; a long
+        // append may use the threads left over by few queries
         const auto t0 = std::chrono::steady_clock::now();
+        int64_t busy = 0;
+        for (int32_t b = 0; b < B; ++b) busy += !F[b].resolved && !failed[b] && (dact[b] || sact[b]);
+        for (int32_t b = 0; b < B; ++b) F[b].threads = std::max<int>(1, threads / std::max<int64_t>(busy, 1));
         parallel_for(B, threads, [&](int64_t b) {
             if (F[b].resolved || failed[b]) return;
             if (dact[b]) {
@@ -399,6 +403,7 @@ extern "C" int eahr_fuse_lists(const int64_t* list_d, int64_t n_d, const int64_t
     const Params P{ep.K, ep.k_rrf, {ep.w_dense, ep.w_sparse}};
     Fusion f;
     f.P = &P;
+    f.threads = host_threads();
     const int64_t* lists[2] = {list_d, list_s};
     const int64_t lens[2] = {n_d, n_s};
     for (int i = 0; i < 2; ++i) f.L[i].open = P.w[i] > 0 && lens[i] > 0;

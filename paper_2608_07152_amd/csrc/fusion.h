@@ -18,19 +18,23 @@
 //
 // Bookkeeping without per-item hashing: each list keeps its prefix sorted by
 // id, so the ranks of a round are radix-sorted and merge-joined against the
-// other list to find items seen by both; a union-find over list positions
-// ("next live single-list position") skips items that became both-seen or
-// fixed in amortised constant time.  Ids must lie in [0, 2^31) and be
-// distinct inside a list (a repeat sets dup).
+// other list to find items seen by both; a bitmap of live positions per list
+// skips items that became both-seen or fixed a word at a time.  Ids must lie
+// in [0, 2^31) and be distinct inside a list (a repeat sets dup).
 //
 // Once one list is closed (read to its end) nothing joins against the other
 // list's id order any more: appends to the open list then test membership in
 // the closed list with a bitmap over ids (and look up the rank in its id
-// order only for the items it holds), and repeats with a second bitmap.
+// order only for the items it holds), and repeats with a second bitmap.  A
+// long such append is split over `threads` host threads (atomic bit updates;
+// the both-seen items are collected per part, and the heap order does not
+// depend on their insertion order because (F, id) is a total order).
 #pragma once
 #include <algorithm>
 #include <cstdint>
 #include <vector>
+
+#include "host_parallel.h"
 
 namespace eahr {
 
@@ -163,7 +167,12 @@ struct Fusion {
         int64_t size() const { return static_cast<int64_t>(ids.size()); }
     };
 
+    // appends of at least this many ranks while the other list is closed are
+    // split over up to `threads` host threads
+    static constexpr int64_t kParallelAppend = int64_t(1) << 16;
+
     const Params* P = nullptr;
+    int threads = 1;
     List L[2];
     std::vector<Scored> both;   // binary heap of unfixed both-seen items
     std::vector<int64_t> A;     // fixed prefix
@@ -291,31 +300,74 @@ struct Fusion {
         me.by_id.swap(merged);
     }
 
-    // Append to list i while the other list is closed (see the file header).
-    void append_closed_other(int i, const int64_t* ids, int64_t n) {
-        if (!bitmaps) enter_bitmap_mode();
+    // Ranks p0 + j + 1 (j in [j0, j1)) of list i while the other list is
+    // closed: repeats set the flag, both-seen items go to out.  Atomic bit
+    // updates when parts of one append run concurrently.
+    template <bool Atomic>
+    void closed_part(int i, const int64_t* ids, int64_t p0, int64_t j0, int64_t j1,
+                     std::vector<Scored>& out, bool& rep) {
         List& me = L[i];
         List& other = L[1 - i];
-        const int64_t p0 = me.size();
-        me.grow(n);
-        me.ids.insert(me.ids.end(), ids, ids + n);
-        const size_t heap0 = both.size();
-        for (int64_t j = 0; j < n; ++j) {
+        auto clear_bit = [](std::vector<uint64_t>& b, int64_t p) {
+            const uint64_t m = ~(1ull << (p & 63));
+            if (Atomic) __atomic_fetch_and(&b[static_cast<size_t>(p >> 6)], m, __ATOMIC_RELAXED);
+            else b[static_cast<size_t>(p >> 6)] &= m;
+        };
+        uint64_t* mine = seen[i].data();
+        for (int64_t j = j0; j < j1; ++j) {
             const int64_t x = ids[j];
             const int64_t rank = p0 + j + 1;
-            if (set_bit(seen[i], x)) {
-                dup = true;
-                me.kill(rank - 1);
+            const uint64_t m = 1ull << (x & 63);
+            const bool had = Atomic ? (__atomic_fetch_or(&mine[x >> 6], m, __ATOMIC_RELAXED) & m) != 0
+                                    : (mine[x >> 6] & m) != 0;
+            if (!Atomic) mine[x >> 6] |= m;
+            if (had) {
+                rep = true;
+                clear_bit(me.alive, rank - 1);
                 continue;
             }
             if (!test_bit(seen[1 - i], x)) continue;
             const int64_t ro = rank_of(1 - i, x);
-            me.kill(rank - 1);
-            other.kill(ro - 1);
+            clear_bit(me.alive, rank - 1);
+            clear_bit(other.alive, ro - 1);
             if (!fixed(x)) {
                 const int64_t r0 = (i == 0) ? rank : ro, r1 = (i == 0) ? ro : rank;
-                both.push_back(Scored{g_double(*P, 0, r0) + g_double(*P, 1, r1),
-                                      static_cast<int32_t>(r0), static_cast<int32_t>(r1), x});
+                out.push_back(Scored{g_double(*P, 0, r0) + g_double(*P, 1, r1),
+                                     static_cast<int32_t>(r0), static_cast<int32_t>(r1), x});
+            }
+        }
+    }
+
+    // Append to list i while the other list is closed (see the file header).
+    void append_closed_other(int i, const int64_t* ids, int64_t n) {
+        if (!bitmaps) enter_bitmap_mode();
+        List& me = L[i];
+        const int64_t p0 = me.size();
+        me.grow(n);
+        me.ids.insert(me.ids.end(), ids, ids + n);
+        const size_t heap0 = both.size();
+        int64_t xmax = 0;
+        for (int64_t j = 0; j < n; ++j) xmax = std::max(xmax, ids[j]);
+        const size_t words = static_cast<size_t>(xmax >> 6) + 1;
+        if (seen[i].size() < words) seen[i].resize(std::max(words, seen[i].size() * 2), 0);
+        const int parts = (threads > 1 && n >= kParallelAppend)
+                        ? static_cast<int>(std::min<int64_t>(threads, n / (kParallelAppend / 4)))
+                        : 1;
+        if (parts <= 1) {
+            bool rep = false;
+            closed_part<false>(i, ids, p0, 0, n, both, rep);
+            dup |= rep;
+        } else {
+            std::vector<std::vector<Scored>> found(static_cast<size_t>(parts));
+            std::vector<uint8_t> rep(static_cast<size_t>(parts), 0);
+            parallel_for(parts, parts, [&](int64_t t) {
+                bool r = false;
+                closed_part<true>(i, ids, p0, n * t / parts, n * (t + 1) / parts, found[t], r);
+                rep[t] = r;
+            });
+            for (int t = 0; t < parts; ++t) {
+                dup |= rep[t] != 0;
+                both.insert(both.end(), found[t].begin(), found[t].end());
             }
         }
         const size_t added = both.size() - heap0;

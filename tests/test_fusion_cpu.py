@@ -125,6 +125,24 @@ def test_fuse_lists_one_list_closed_early(seed):
         eahr.eahr_fuse_lists(bad, b[:40], K=20, depth0=20)
 
 
+def test_fuse_lists_deep_reads_after_the_other_list_closed():
+    """The sparse list holds ids from the tail of the dense list, so the dense
+    list is read far past the point where the sparse list closed; appends of
+    that size are split over several host threads.  A repeat deep in the open
+    list is still rejected."""
+    rng = np.random.default_rng(11)
+    n = 600_000
+    a = rng.permutation(n)
+    b = rng.permutation(a[n - 200_000:])[:3000]
+    for wts in ((1, 1), (2, 1)):
+        got, st = eahr.eahr_fuse_lists(a, b, K=20, w_dense=wts[0], w_sparse=wts[1])
+        assert list(got) == rrf.rrf_topk([a, b], list(wts), 60, 20)
+        assert st["dense_depth"] > 300_000
+    bad = np.concatenate([a[:400_000], a[350_000:350_001], a[400_000:]])
+    with pytest.raises(eahr.EahrError):
+        eahr.eahr_fuse_lists(bad, b, K=20)
+
+
 def test_fuse_lists_large_prefixes_equal_complete_rrf():
     """Deep prefixes (several table growths of the id bookkeeping): partially
     overlapping permutations of 200,000 ids."""
