@@ -21,9 +21,10 @@ around each kernel class of every scan round, inside the timed region.
 ``kernels`` lists every class with its algorithmic bytes and rate:
   * scan variants: N (d + 12) + 8 N / 64 bytes per launch (codes, three
     per-row floats, visibility bits), independent of the batch;
-  * rescore: (4 d + 20) bytes per candidate (its float32 row, its 8-byte
-    (row, integer dot) record, the three per-row floats its interval is
-    recomputed from) plus 8 bytes per certified candidate (its key);
+  * rescore: (4 d + 12) bytes per row load (a float32 row and the three
+    per-row floats its intervals are recomputed from; one load serves the
+    adjacent records of one row) plus 16 bytes per candidate pair (its
+    (row, query, integer dot) record) and 8 per certified pair (its key);
 and ``roofline`` is the class with the most time in the headline batch
 (HBM-bound: achieved GB/s against 8 TB/s), ``roofline_scan`` the dominant
 scan variant.  ``traffic`` is filled from the committed PMC summary of that
@@ -268,7 +269,8 @@ def main():
                 kernels[name] = {"ms": ms, "launches": n, "bytes": prof["variant_bytes"][i],
                                  "gbs": prof["variant_bytes"][i] / (ms * 1e-3) / 1e9 if ms > 0 else 0.0}
         if prof["scan_rounds"]:
-            rb = prof["rescore_rows"] * (4 * w.d + 20) + prof["rescore_certified"] * 8
+            rb = (prof["rescore_row_reads"] * (4 * w.d + 12) + prof["rescore_rows"] * 16
+                  + prof["rescore_certified"] * 8)
             ms = prof["rescore_ms"]
             kernels["rescore"] = {"ms": ms, "launches": prof["scan_rounds"], "bytes": rb,
                                   "gbs": rb / (ms * 1e-3) / 1e9 if ms > 0 else 0.0}
@@ -286,7 +288,7 @@ def main():
             "kernels": kernels, "dominant": dom,
             "kernel_ms": {"scan": prof["scan_ms"], "sample_select": prof["sample_ms"],
                           "rescore": prof["rescore_ms"], "sort_pack": prof["sort_ms"]},
-            "rescored_rows": prof["rescore_rows"],
+            "rescored_pairs": prof["rescore_rows"], "rescore_row_reads": prof["rescore_row_reads"],
             "host_ms": {"dense_calls": prof["host_dense_ms"], "sparse_rounds": prof["host_sparse_ms"],
                         "certify": prof["host_fuse_ms"]},
             "dense_depth": {"mean": float(dd.mean()), "median": float(np.median(dd)), "max": int(dd.max())},

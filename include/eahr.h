@@ -109,10 +109,12 @@ typedef struct {
     int64_t sample_scans;    /* threshold-estimation passes over sampled rows  */
     int64_t rows_scanned;    /* visible-or-not rows streamed by full scans     */
     int64_t bytes_scanned;   /* code + metadata bytes streamed by full scans   */
-    int64_t candidates;      /* rows rescored in float32                       */
+    int64_t candidates;      /* (query, row) pairs rescored in float32         */
     int64_t certified;       /* ranks certified by scans                       */
     int64_t emitted;         /* ranks returned by pvs_next                     */
     int64_t rescans;         /* scans repeated with a lower threshold          */
+    int64_t overflows;       /* query scans repeated because the candidate pool
+                              * or the query's key region was too small       */
 } pvs_counters;
 
 int pvs_stats(const pvs_state* st, pvs_counters* out);
@@ -128,7 +130,7 @@ typedef struct {
     int64_t scan_bytes;      /* algorithmic bytes those launches streamed    */
     double sample_ms;        /* threshold sampling + selection               */
     double rescore_ms;       /* float32 rescoring of candidates              */
-    int64_t rescore_rows;
+    int64_t rescore_rows;    /* candidate pairs rescored                     */
     double sort_ms;          /* candidate sort and packing                   */
     int64_t scan_rounds;
     int64_t mfma_launches;   /* scan launches that used the Int8 MFMA kernel */
@@ -142,6 +144,8 @@ typedef struct {
     int64_t variant_launches[12];
     int64_t variant_bytes[12];
     int64_t rescore_certified;   /* candidates certified by rescoring (keys written) */
+    int64_t rescore_row_reads;   /* row loads of rescoring: one per run of pairs of one
+                                  * row inside a wavefront's share */
 } pvs_profile;
 
 int pvs_profile_enable(int32_t on);   /* also clears the accumulators */

@@ -326,7 +326,7 @@ void pvs_state::release_scan_buffers() {
     dev_free(sample_lo);
     dev_free(sample_hi);
     dev_free(qfrag);
-    dev_free(cand);
+    dev_free(pairs);
     dev_free(keys);
     dev_free(keys_tmp);
     dev_free(packed);
@@ -345,7 +345,7 @@ void pvs_state::release_scan_buffers() {
 // Move the scan buffers between a state and an index's spare slot.
 #define PVS_BUFFER_FIELDS(X)                                                                 \
     X(buf_nq) X(buf_sample) X(scanq) X(counts) X(sample_lo) X(sample_hi) X(qfrag) X(pool_cap) \
-    X(cand) X(keys) X(keys_tmp) X(packed) X(h_scanq) X(h_counts)    \
+    X(pairs) X(keys) X(keys_tmp) X(packed) X(h_scanq) X(h_counts)    \
     X(h_packed) X(h_packed_cap)
 
 static void adopt_buffers(pvs_state* st, ScanBuffers& b) {
@@ -382,7 +382,7 @@ static void donate_buffers(pvs_state* st, ScanBuffers& b) {
     st->sample_lo = nullptr;
     st->sample_hi = nullptr;
     st->qfrag = nullptr;
-    st->cand = nullptr;
+    st->pairs = nullptr;
     st->keys = nullptr;
     st->keys_tmp = nullptr;
     st->packed = nullptr;
@@ -397,7 +397,7 @@ static void free_buffers(ScanBuffers& b) {
     dev_free(b.sample_lo);
     dev_free(b.sample_hi);
     dev_free(b.qfrag);
-    dev_free(b.cand);
+    dev_free(b.pairs);
     dev_free(b.keys);
     dev_free(b.keys_tmp);
     dev_free(b.packed);
@@ -408,14 +408,14 @@ static void free_buffers(ScanBuffers& b) {
 }
 
 // Per-query scan buffers for nq queries and samples of sample_ld rows.
-// counts layout: [total nq][cert nq][fail nq][offs nq + 1][need nq]
-// [rescore chunk base nq + 1], then from sub_counts_at(nq) the append
-// counters of the candidate sub-regions, nq * kSub of them, kCntStride ints
-// apart.  h_counts mirrors the first 6 nq + 2 entries.
-static size_t host_counts(int32_t nq) { return 6 * static_cast<size_t>(nq) + 2; }
-static size_t sub_counts_at(int32_t nq) { return (host_counts(nq) + 63) / 64 * 64; }
+// counts layout: [cert nq][fail nq][offs nq + 1][row reads 1]
+// [rescore chunk base kSub + 1], then from pair_counts_at(nq) the kSub append
+// counters of the pair pool, kCntStride ints apart.  h_counts mirrors it.
+static size_t pair_counts_at(int32_t nq) {
+    return (3 * static_cast<size_t>(nq) + 2 + pvs::kSub + 1 + 63) / 64 * 64;
+}
 static size_t all_counts(int32_t nq) {
-    return sub_counts_at(nq) + static_cast<size_t>(nq) * pvs::kSub * pvs::kCntStride;
+    return pair_counts_at(nq) + static_cast<size_t>(pvs::kSub) * pvs::kCntStride;
 }
 
 static int ensure_query_buffers(pvs_state* st, int32_t nq, int64_t sample_ld) {
@@ -440,24 +440,24 @@ static int ensure_query_buffers(pvs_state* st, int32_t nq, int64_t sample_ld) {
     EAHR_TRY(dev_alloc(&f, static_cast<size_t>(st->ix->dp / 32) * 8 * 64 * 16));
     st->qfrag = f;
     HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&st->h_scanq), nq * sizeof(ScanQ)));
-    HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&st->h_counts), host_counts(nq) * sizeof(int32_t)));
+    HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&st->h_counts), all_counts(nq) * sizeof(int32_t)));
     st->buf_nq = nq;
     st->buf_sample = sample_ld;
     return EAHR_OK;
 }
 
-// Candidate pool of `slots` entries shared by the regions of one scan.
+// Pair pool and key regions of `slots` entries for one scan.
 static int ensure_pool(pvs_state* st, int64_t slots) {
     if (slots <= st->pool_cap) return EAHR_OK;
     slots = std::max<int64_t>(slots + slots / 4, pvs::kMinCap);
     HIP_TRY(hipStreamSynchronize(st->ix->stream));
-    dev_free(st->cand);
+    dev_free(st->pairs);
     dev_free(st->keys);
     dev_free(st->keys_tmp);
     dev_free(st->packed);
     st->pool_cap = 0;
     const size_t n = static_cast<size_t>(slots);
-    EAHR_TRY(dev_alloc(&st->cand, n));
+    EAHR_TRY(dev_alloc(&st->pairs, n));
     EAHR_TRY(dev_alloc(&st->keys, n));
     EAHR_TRY(dev_alloc(&st->keys_tmp, n));
     EAHR_TRY(dev_alloc(&st->packed, n));
@@ -494,6 +494,7 @@ extern "C" int pvs_open(const pvs_index* ix, int64_t epoch, const float* q, int3
         if (std::strcmp(p, "gemv") == 0) st->path = pvs::ScanPath::Gemv;
         else if (std::strcmp(p, "mfma") == 0) st->path = pvs::ScanPath::Mfma;
     }
+    if (const char* p = std::getenv("EAHR_CAP_SHRINK")) st->cap_shrink = std::max(1L, std::atol(p));
     st->n_rows = ix->snaps[epoch].rows;
     st->n_vis = ix->snaps[epoch].visible;
     st->vis = ix->snaps[epoch].vis;
@@ -784,9 +785,13 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
         // per sub-region, with room for an uneven split
         int64_t sub = (cap + pvs::kSub - 1) / pvs::kSub;
         sub += sub / 4 + 16;
+        if (Q.cap_hint == 0 && st->cap_shrink > 1) sub = std::max<int64_t>(1, sub / st->cap_shrink);
         sub = std::max(sub, Q.cap_hint);
         sub = std::min(sub, max_sub);
         if (run > 0 && total + sub * pvs::kSub > pvs::kPoolMax) break;
+        // a pool counter must not wrap: at most (blocks / kSub + 32) * 64 rows
+        // of one sub-region times the queries
+        if (run > 0 && (nblocks + 2048) * (run + 1) >= (int64_t(1) << 31)) break;
         sq.cand_off = total;
         sq.cand_cap = sub;
         total += sub * pvs::kSub;
@@ -796,58 +801,76 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     nq = run;
     EAHR_TRY(ensure_pool(st, total));
     HIP_TRY(hipMemcpyAsync(st->scanq, st->h_scanq, nq * sizeof(ScanQ), hipMemcpyHostToDevice, s));
-    int32_t* d_cand = st->counts;
-    int32_t* d_cert = st->counts + nq;
-    int32_t* d_fail = st->counts + 2 * nq;
-    int32_t* d_offs = st->counts + 3 * nq;
-    int32_t* d_need = st->counts + 4 * nq + 1;
-    int32_t* d_cbase = st->counts + 5 * nq + 1;
-    int32_t* d_sub = st->counts + sub_counts_at(nq);
+    int32_t* d_cert = st->counts;
+    int32_t* d_fail = st->counts + nq;
+    int32_t* d_offs = st->counts + 2 * nq;
+    int32_t* d_reads = st->counts + 3 * nq + 1;
+    int32_t* d_cbase = st->counts + 3 * nq + 2;
+    int32_t* d_pcnt = st->counts + pair_counts_at(nq);
+    const int32_t* h_pcnt = st->h_counts + pair_counts_at(nq);
+    const int64_t pair_sub = total / pvs::kSub;
     HIP_TRY(hipMemsetAsync(st->counts, 0, all_counts(nq) * sizeof(int32_t), s));
     pvs::ScanOut mo;
-    mo.cand = st->cand;
-    mo.cand_cnt = d_sub;
+    mo.pairs = st->pairs;
+    mo.pair_sub = pair_sub;
+    mo.pair_cnt = d_pcnt;
     EAHR_TRY(mark(2));
     scan(false, mo, nq);
     EAHR_TRY(mark(3));
-    pvs::launch_cand_totals(d_sub, st->scanq, nq, d_cand, d_need, s);
     HIP_TRY(hipGetLastError());
-    HIP_TRY(hipMemcpyAsync(st->h_counts, st->counts, host_counts(nq) * sizeof(int32_t),
+    HIP_TRY(hipMemcpyAsync(st->h_counts + pair_counts_at(nq), d_pcnt,
+                           static_cast<size_t>(pvs::kSub) * pvs::kCntStride * sizeof(int32_t),
                            hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
     tp[2] = clk::now();
-    const std::vector<int32_t> need(st->h_counts + 4 * nq + 1, st->h_counts + 5 * nq + 1);
+    int64_t kept = 0, fullest = 0;   // records kept; the fullest sub-region's count
+    for (int i = 0; i < pvs::kSub; ++i) {
+        const int64_t c = h_pcnt[i * pvs::kCntStride];
+        kept += std::min(c, pair_sub);
+        fullest = std::max(fullest, c);
+    }
+    const bool pool_over = fullest > pair_sub;   // records were dropped
     st->stats.scans += 1;
     st->stats.sample_scans += 1;
     st->stats.rows_scanned += nblocks * 64;
     st->stats.bytes_scanned += st->n_rows * (static_cast<int64_t>(ix->d) + 12) + nblocks * 8;
 
     // 3. rescore, order and pack the certified ranks
-    std::vector<int32_t> cand(st->h_counts, st->h_counts + nq);   // kept candidates
-    int64_t kept = 0;
-    for (int32_t i = 0; i < nq; ++i) kept += cand[i];
-    const int64_t chunks = pvs::rescore_chunks(cand.data(), nq);
-    pvs::launch_rescore(v, st->qrows, st->scanq, nq, d_cand, d_cbase, chunks, st->cand, ix->gamma,
-                        d_sub, st->keys, d_cert, d_fail, s);
+    const int64_t chunks = pvs::rescore_chunks(h_pcnt, pair_sub);
+    pvs::launch_rescore(v, st->qrows, st->scanq, d_pcnt, st->pairs, pair_sub, d_cbase, chunks,
+                        ix->gamma, st->keys, d_cert, d_fail, d_reads, s);
     EAHR_TRY(mark(4));
-    // only the certified keys are ordered
-    HIP_TRY(hipMemcpyAsync(st->h_counts + nq, d_cert, nq * sizeof(int32_t), hipMemcpyDeviceToHost, s));
+    // only the certified keys are ordered; a query whose key region overflowed
+    // (it is scanned again) keeps the region's worth
+    HIP_TRY(hipMemcpyAsync(st->h_counts, d_cert, nq * sizeof(int32_t), hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
+    const std::vector<int32_t> cert_all(st->h_counts, st->h_counts + nq);
     int64_t max_cert = 0;
-    for (int32_t i = 0; i < nq; ++i) max_cert = std::max<int64_t>(max_cert, st->h_counts[nq + i]);
+    bool clamped = false;
+    for (int32_t i = 0; i < nq; ++i) {
+        const int64_t region = pvs::kSub * st->h_scanq[i].cand_cap;
+        if (st->h_counts[i] > region) {
+            st->h_counts[i] = static_cast<int32_t>(region);
+            clamped = true;
+        }
+        max_cert = std::max<int64_t>(max_cert, st->h_counts[i]);
+    }
+    if (clamped)
+        HIP_TRY(hipMemcpyAsync(d_cert, st->h_counts, nq * sizeof(int32_t), hipMemcpyHostToDevice, s));
     EAHR_TRY(mark(6));
     uint64_t* sorted = pvs::launch_segmented_sort(st->keys, st->keys_tmp, d_cert, st->scanq, nq, max_cert, s);
     pvs::launch_pack(sorted, d_cert, st->scanq, nq, max_cert, d_offs, st->packed, s);
     EAHR_TRY(mark(5));
     HIP_TRY(hipGetLastError());
     EAHR_TRY(ensure_host_packed(st, kept));
-    HIP_TRY(hipMemcpyAsync(st->h_counts + nq, d_cert, (3 * static_cast<size_t>(nq) + 1) * sizeof(int32_t),
+    HIP_TRY(hipMemcpyAsync(st->h_counts, st->counts, (3 * static_cast<size_t>(nq) + 2) * sizeof(int32_t),
                            hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
     tp[3] = clk::now();
-    const int32_t* h_cert = st->h_counts + nq;
-    const int32_t* h_fail = st->h_counts + 2 * nq;
-    const int32_t* h_offs = st->h_counts + 3 * nq;
+    const int32_t* h_cert = st->h_counts;
+    const int32_t* h_fail = st->h_counts + nq;
+    const int32_t* h_offs = st->h_counts + 2 * nq;
+    const int64_t row_reads = st->h_counts[3 * nq + 1];
     if (h_offs[nq] > 0)
         HIP_TRY(hipMemcpy(st->h_packed, st->packed, static_cast<size_t>(h_offs[nq]) * sizeof(uint64_t),
                           hipMemcpyDeviceToHost));
@@ -877,6 +900,7 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
         g_prof.variant_bytes[v] += launches * pass_bytes;
         g_prof.rescore_ms += t[2];
         g_prof.rescore_rows += kept;
+        g_prof.rescore_row_reads += row_reads;
         for (int32_t i = 0; i < nq; ++i) g_prof.rescore_certified += h_cert[i];
         g_prof.sort_ms += t[3];
         g_prof.scan_rounds += 1;
@@ -885,7 +909,7 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     // append the certified keys of every query to its cache (in parallel)
     std::vector<uint8_t> usable(nq, 0);
     for (int32_t i = 0; i < nq; ++i)
-        usable[i] = !h_fail[i] && need[i] <= st->h_scanq[i].cand_cap;
+        usable[i] = !h_fail[i] && !pool_over && cert_all[i] == h_cert[i];
     eahr::parallel_for(nq, eahr::host_threads(), [&](int64_t i) {
         if (!usable[i] || h_cert[i] == 0) return;
         const uint64_t* kp = st->h_packed + h_offs[i];
@@ -904,6 +928,7 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
                      static_cast<long long>(total), static_cast<long long>(kept),
                      static_cast<long long>(certified), ms(0, 1), ms(1, 2), ms(2, 3), ms(3, 4), ms(4, 5));
     }
+    if (!pool_over) st->stats.candidates += kept;
     std::vector<int32_t> keep;
     for (int32_t i = 0; i < nq; ++i) {
         const int32_t b = todo[i];
@@ -912,13 +937,22 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
             Q.failed = true;
             continue;
         }
-        if (need[i] > st->h_scanq[i].cand_cap) {   // a sub-region overflowed: redo with room for all
-            Q.cap_hint = static_cast<int64_t>(need[i]) + need[i] / 4 + 64;
+        const int64_t cap = st->h_scanq[i].cand_cap;
+        if (pool_over) {   // records were dropped: every query again, with a larger pool
+            const double grow = static_cast<double>(fullest) / static_cast<double>(pair_sub);
+            Q.cap_hint = std::max(Q.cap_hint, static_cast<int64_t>(std::ceil(cap * grow * 1.25)) + 16);
+            st->stats.overflows += 1;
+            keep.push_back(b);
+            continue;
+        }
+        if (cert_all[i] != h_cert[i]) {   // its key region overflowed: again with room for all
+            const int64_t per = (cert_all[i] + pvs::kSub - 1) / pvs::kSub;
+            Q.cap_hint = per + per / 4 + 16;
+            st->stats.overflows += 1;
             keep.push_back(b);
             continue;
         }
         Q.cap_hint = 0;
-        st->stats.candidates += cand[i];
         const int64_t c = h_cert[i];
         st->stats.certified += c;
         if (c > 0) {

@@ -74,7 +74,7 @@ struct ScanBuffers {
     float* sample_hi = nullptr;
     void* qfrag = nullptr;
     int64_t pool_cap = 0;
-    uint2* cand = nullptr;          // (row, integer dot) per candidate slot
+    uint4* pairs = nullptr;         // candidate pair records of a scan (pool)
     uint64_t* keys = nullptr;
     uint64_t* keys_tmp = nullptr;
     uint64_t* packed = nullptr;
@@ -149,11 +149,14 @@ struct pvs_state {
     void* qfrag = nullptr;             // query codes in MFMA operand order
     // candidate pool (pool_cap slots) split into per-query regions per scan
     int64_t pool_cap = 0;
-    uint2* cand = nullptr;
+    uint4* pairs = nullptr;
     uint64_t* keys = nullptr;
     uint64_t* keys_tmp = nullptr;
     uint64_t* packed = nullptr;
     pvs::ScanPath path = pvs::ScanPath::Auto;
+    // test knob: first-attempt key regions and pool divided by this, so that
+    // the overflow and rescan paths run (results do not change)
+    int64_t cap_shrink = 1;
     hipEvent_t ev[7] = {};             // profiling events (created on first use)
     pvs::ScanQ* h_scanq = nullptr;     // pinned host mirrors
     int32_t* h_counts = nullptr;

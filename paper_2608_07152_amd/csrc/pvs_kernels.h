@@ -11,11 +11,10 @@ constexpr int kMaxDim = 4096;      // 127^2 * 4096 < 2^31 and a_m < 1
 constexpr int kSortTile = 2048;    // keys sorted per workgroup in LDS
 constexpr int kMaxGemvQueries = 8; // queries per GEMV scan pass
 constexpr int kMaxMfmaQueries = 256;  // queries per MFMA scan pass (8 tiles of 32)
-constexpr int kMaxChunk = 256;     // largest slice of a candidate region one workgroup reserves
-// A query's candidate region is split into kSub sub-regions, each with its
+// The candidate pool of a scan is split into kSub sub-regions, each with its
 // own append counter; the code block (or workgroup) picks the sub-region
-// from its index, so concurrent appends of one query hit kSub different
-// counters instead of one.  Counters sit kCntStride ints (64 bytes) apart.
+// from its index, so concurrent appends hit kSub different counters instead
+// of one.  Counters sit kCntStride ints (64 bytes) apart.
 constexpr int kSub = 64;
 constexpr int kCntStride = 16;
 
@@ -35,8 +34,8 @@ struct ScanQ {
     float neq;         // ||e_q||_2 rounded up
     float wmax;        // upper bound of E + G over every row of the index
     int32_t sample_hits;  // sampled eligible rows with hi >= tau (select pass)
-    int64_t cand_off;  // first slot of this query's candidate region
-    int64_t cand_cap;  // slots in each of its kSub sub-regions
+    int64_t cand_off;  // first slot of this query's key region
+    int64_t cand_cap;  // its key region holds kSub * cand_cap keys
 };
 static_assert(sizeof(ScanQ) == 64, "ScanQ layout");
 
@@ -61,20 +60,25 @@ void launch_quantize(const float* src, int64_t nrows, int32_t d, int64_t src_str
 
 // Outputs of a scan pass.  Sample pass: lower and upper bounds of every
 // (query, row) pair of the sampled blocks, row-major [query][sample_ld],
-// -inf / -inf for ineligible rows.  Main pass: the candidates query b appends
-// to sub-region s go to slots cand_off + s * cand_cap + j, j < cand_cap, and
-// cand_cnt[(b * kSub + s) * kCntStride] counts every slot of sub-region s
-// handed out, including those past its end.  A slot holds the candidate's row
-// and its exact integer dot product (from which rescoring recomputes the
-// interval), or the sentinel row 0xffffffff (part of a reserved slice left
-// unused), which is no candidate.
+// -inf / -inf for ineligible rows.  Main pass: every candidate pair (hi >= tau)
+// becomes one record (row, index of the query in the scan, exact integer dot
+// product, 0).  A wavefront reserves all records of its block (or of its
+// block and half of the query tiles, in the wide MFMA kernel) with one atomic
+// on the counter of sub-region s = block or workgroup index % kSub,
+// pair_cnt[s * kCntStride], and writes them at pairs[s * pair_sub + j] for
+// j < pair_sub; the counter counts every record handed out, also past the
+// sub-region's end (the pool overflowed).  A wavefront writes the records of
+// one row next to each other, so rescoring reads the row once for all of
+// them.
 struct ScanOut {
     float* sample_lo = nullptr;
     float* sample_hi = nullptr;
     int64_t sample_ld = 0;
     int64_t sample_stride = 1;   // sampled blocks are multiples of this
-    uint2* cand = nullptr;   // (row, integer dot); row 0xffffffff marks a sentinel slot
-    int32_t* cand_cnt = nullptr;
+    uint4* pairs = nullptr;
+    int64_t pair_sub = 0;        // records per sub-region
+    int32_t* pair_cnt = nullptr;
+    int32_t qbase = 0;           // scan index of the pass's first query
 };
 
 void launch_scan(const IndexView& ix, const uint64_t* vis, int64_t nblocks, const int8_t* qcodes,
@@ -94,23 +98,21 @@ int mfma_tiles_for(int32_t nq);
 void launch_select(const float* sample_lo, const float* sample_hi, int64_t n, int64_t ld,
                    bool midpoint, ScanQ* sq, int32_t nq, hipStream_t stream);
 
-// Per query: total[b] = sum over sub-regions of min(count, cand_cap) (the
-// candidates kept), need[b] = the largest sub-region count (a sub-region
-// overflowed when need[b] > cand_cap).
-void launch_cand_totals(const int32_t* sub_cnt, const ScanQ* sq, int32_t nq, int32_t* total,
-                        int32_t* need, hipStream_t stream);
-
-// Rescoring reads the kept candidates of every sub-region of a query in
-// sub-region order (total[b] of them, chunked by rescore_chunks) and appends
-// the keys of the certified ones at keys[cand_off + j], j < cert_cnt[b]
-// (cert_cnt zeroed by the caller; order of appends unspecified).  cbase is
-// device scratch of nq + 1 ints; chunks = rescore_chunks of the host copy of
-// total.
-int64_t rescore_chunks(const int32_t* total, int32_t nq);
-void launch_rescore(const IndexView& ix, const float* qrows, const ScanQ* sq, int32_t nq,
-                    const int32_t* total, int32_t* cbase, int64_t chunks,
-                    const uint2* cand, float gamma, const int32_t* sub_cnt, uint64_t* keys,
-                    int32_t* cert_cnt, int32_t* fail, hipStream_t stream);
+// Rescoring reads the kept records of every sub-region of the pool (at most
+// pair_sub each, in chunks of kRescoreChunk; chunks = rescore_chunks of the
+// host copy of the counters), computes each pair's float32 score and checks
+// it against its interval, and appends the keys of the certified pairs of
+// query b at keys[cand_off + j], j < min(cert_cnt[b], kSub * cand_cap)
+// (cert_cnt zeroed by the caller counts them all; order of appends
+// unspecified).  cbase is device scratch of kSub + 1 ints; row_reads (one
+// int, zeroed by the caller) receives the number of row loads, one per run of
+// records of one row inside a wavefront's share.
+constexpr int kRescoreChunk = 256;
+int64_t rescore_chunks(const int32_t* pair_cnt, int64_t pair_sub);
+void launch_rescore(const IndexView& ix, const float* qrows, const ScanQ* sq,
+                    const int32_t* pair_cnt, const uint4* pairs, int64_t pair_sub,
+                    int32_t* cbase, int64_t chunks, float gamma, uint64_t* keys,
+                    int32_t* cert_cnt, int32_t* fail, int32_t* row_reads, hipStream_t stream);
 
 // Sorts every query's candidate keys (cnt[b] keys from cand_off) ascending;
 // returns the buffer holding the result (keys or tmp).

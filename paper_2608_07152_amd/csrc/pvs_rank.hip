@@ -1,177 +1,187 @@
 // Candidate rescoring, ordering and packing of the PVS dense channel.
 //
-// Every candidate gets its authoritative float32 score (row_score, one fixed
-// order) and is checked against its interval (App. A.1: a score outside it
-// fails the request), recomputed here from the integer dot product the scan
-// recorded with the same arithmetic as the scan's, so identical to it.  A scan with threshold tau certifies exactly the
-// candidates with s32 >= tau whose key follows the last certified key; their
-// keys (~mono(s32) << 32 | row) are appended to the query's key region, so
-// ascending keys are (score descending, id ascending).  Keys are unique
-// inside a query; the segmented sort orders each query's certified keys.
+// Every candidate pair gets its authoritative float32 score (row_score's
+// fixed order) and is checked against its interval (App. A.1: a score
+// outside it fails the request), recomputed from the integer dot product the
+// scan recorded with the scan's own arithmetic, so identical to it.  A scan
+// with threshold tau certifies exactly the candidates with s32 >= tau whose
+// key follows the last certified key; their keys (~mono(s32) << 32 | row) are
+// appended to the query's key region, so ascending keys are (score
+// descending, id ascending).  Keys are unique inside a query; the segmented
+// sort orders each query's certified keys.
+#include <algorithm>
+
 #include "pvs_device.h"
 
 namespace pvs {
 
-// Candidates of a scan round are cut into chunks of kRescoreChunk per query;
-// cbase[b] is the first chunk of query b (exclusive prefix over the queries).
-constexpr int kRescoreChunk = 256;
-
-__global__ __launch_bounds__(64) void k_chunk_base(const int32_t* __restrict__ total, int32_t nq,
-                                                   int32_t* __restrict__ cbase) {
+// Records of a scan round are cut into chunks of kRescoreChunk per pool
+// sub-region; cbase[s] is the first chunk of sub-region s (exclusive prefix).
+__global__ __launch_bounds__(64) void k_chunk_base(const int32_t* __restrict__ pair_cnt,
+                                                   int64_t pair_sub, int32_t* __restrict__ cbase) {
     if (threadIdx.x == 0) {
         int32_t acc = 0;
-        for (int b = 0; b < nq; ++b) {
-            cbase[b] = acc;
-            acc += (total[b] + kRescoreChunk - 1) / kRescoreChunk;
+        for (int s = 0; s < kSub; ++s) {
+            cbase[s] = acc;
+            const int64_t n = pair_cnt[s * kCntStride] < pair_sub ? pair_cnt[s * kCntStride] : pair_sub;
+            acc += static_cast<int32_t>((n + kRescoreChunk - 1) / kRescoreChunk);
         }
-        cbase[nq] = acc;
+        cbase[kSub] = acc;
     }
 }
 
-// One workgroup per chunk, one wavefront per quarter of it, R candidates in
-// flight per wavefront (one candidate per wavefront pass: lane l holds
-// elements 256 t + 4 l + i of the row, the fixed order of row_score).
-// Candidate i of a query (sub-region order) lives in sub-region s with
-// first[s] <= i < last[s]: lane s holds first[s] and last[s] (a prefix sum of
-// the kept counts), and a ballot finds s.  Only certified candidates produce
-// a key: s32 >= tau and the key (~mono(s32) << 32 | row) after the last
-// certified key; a wavefront collects its keys in lanes 0.. and appends them
-// to the query's key region with one atomic.
+// One workgroup per chunk, one wavefront per quarter of it.  Lane j holds the
+// wavefront's record j; the records are then taken R at a time, each by the
+// whole wavefront (lane l holds elements 256 t + 4 l + i of the row and of
+// the query, the fixed order of row_score).  Records of one row are adjacent,
+// so after the first of them the row comes from cache.  A certified pair's
+// key stays in the lane of its record; at the end the keys of each query are
+// appended to its region with one atomic.
 template <int J>
 __global__ __launch_bounds__(256) void k_rescore(
     const float4* __restrict__ rows, int32_t df4, const float4* __restrict__ qrows,
-    const ScanQ* __restrict__ sq, int32_t nq, const int32_t* __restrict__ cbase,
-    const uint2* __restrict__ cand, const float* __restrict__ scale,
-    const float* __restrict__ vnorm, const float* __restrict__ enorm, float gamma,
-    const int32_t* __restrict__ sub_cnt, uint64_t* __restrict__ keys,
-    int32_t* __restrict__ cert_cnt, int32_t* __restrict__ fail) {
-    static_assert(kSub == 64, "one lane per sub-region");
+    const ScanQ* __restrict__ sq, const int32_t* __restrict__ cbase,
+    const int32_t* __restrict__ pair_cnt, const uint4* __restrict__ pairs, int64_t pair_sub,
+    const float* __restrict__ scale, const float* __restrict__ vnorm,
+    const float* __restrict__ enorm, float gamma, uint64_t* __restrict__ keys,
+    int32_t* __restrict__ cert_cnt, int32_t* __restrict__ fail, int32_t* __restrict__ row_reads) {
     constexpr int PER_WAVE = kRescoreChunk / 4;
-    static_assert(PER_WAVE <= 64, "one key per lane");
+    static_assert(PER_WAVE == 64, "one record per lane");
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    // the query of this chunk: the last b with cbase[b] <= chunk (that query
-    // has chunks, as cbase[b + 1] > chunk)
+    // the sub-region of this chunk: the last s with cbase[s] <= chunk
     const int x = blockIdx.x;
-    int blo = 0, bhi = nq;
-    while (bhi - blo > 1) {
-        const int mid = (blo + bhi) >> 1;
-        if (cbase[mid] <= x) blo = mid;
-        else bhi = mid;
+    int slo = 0, shi = kSub;
+    while (shi - slo > 1) {
+        const int mid = (slo + shi) >> 1;
+        if (cbase[mid] <= x) slo = mid;
+        else shi = mid;
     }
-    const int b = blo;
-    const ScanQ Q = sq[b];
-    const int c = sub_cnt[(b * kSub + lane) * kCntStride];
-    const int kept = static_cast<int>(c < Q.cand_cap ? c : Q.cand_cap);
-    int last = kept;
-    for (int off = 1; off < 64; off <<= 1) {
-        const int t = __shfl_up(last, off, 64);
-        if (lane >= off) last += t;
-    }
-    const int first = last - kept;
-    const int64_t n = __builtin_amdgcn_readlane(last, 63);
-    const int64_t i_begin = static_cast<int64_t>(x - cbase[b]) * kRescoreChunk + wave * PER_WAVE;
-    const int64_t i_end = (i_begin + PER_WAVE < n) ? i_begin + PER_WAVE : n;
-    if (i_begin >= i_end) return;
-    float4 qv[J];
-    load_query_row<J>(qrows, Q.qi, df4, lane, qv);
-    // slot of candidate i (uniform across the wavefront)
-    auto slot_of = [&](int64_t i) -> int64_t {
-        const uint64_t m = __ballot(first <= i && i < last);
-        const int s = __ffsll(static_cast<unsigned long long>(m)) - 1;
-        const int f = __builtin_amdgcn_readlane(first, s);
-        return Q.cand_off + static_cast<int64_t>(s) * Q.cand_cap + (i - f);
-    };
+    const int s = slo;
+    const int64_t cnt = pair_cnt[s * kCntStride];
+    const int64_t n_s = cnt < pair_sub ? cnt : pair_sub;
+    const int64_t i0 = static_cast<int64_t>(x - cbase[s]) * kRescoreChunk + wave * PER_WAVE;
+    const int n = static_cast<int>(n_s - i0 < PER_WAVE ? n_s - i0 : PER_WAVE);
+    if (n <= 0) return;
+    const uint4 rec = (lane < n) ? pairs[s * pair_sub + i0 + lane] : make_uint4(0u, 0u, 0u, 0u);
     constexpr int R = (J <= 4) ? 4 : 1;
     uint64_t mykey = 0;
-    int nk = 0;          // certified keys collected (lanes 0 .. nk - 1)
-    bool bad = false;
-    for (int64_t i0 = i_begin; i0 < i_end; i0 += R) {
-        int32_t row[R];
-        int32_t dot[R];
+    int myb = -1;          // query of this lane's certified record
+    int reads = 0;
+    uint32_t prev = 0xffffffffu;
+    for (int k0 = 0; k0 < n; k0 += R) {
+        int32_t row[R], b[R], dot[R];
         float sv[R], nv[R], nev[R];
-        float4 v[R][J];
+        float4 v[R][J], qv[R][J];
 #pragma unroll
         for (int k = 0; k < R; ++k) {
-            const int64_t i = i0 + k;
-            const uint2 rec = (i < i_end) ? cand[slot_of(i)] : make_uint2(0xffffffffu, 0u);
-            row[k] = static_cast<int32_t>(rec.x);   // -1 past the chunk or for a sentinel
-            dot[k] = static_cast<int32_t>(rec.y);
+            const int j = k0 + k < n ? k0 + k : n - 1;
+            const bool ok = k0 + k < n;
+            row[k] = ok ? static_cast<int32_t>(__builtin_amdgcn_readlane(rec.x, j)) : -1;
+            b[k] = static_cast<int32_t>(__builtin_amdgcn_readlane(rec.y, j));
+            dot[k] = static_cast<int32_t>(__builtin_amdgcn_readlane(rec.z, j));
             const int64_t r = row[k] < 0 ? 0 : row[k];
             sv[k] = scale[r];
             nv[k] = vnorm[r];
             nev[k] = enorm[r];
             const float4* rp = rows + r * df4;
+            const float4* qp = qrows + static_cast<int64_t>(sq[b[k]].qi) * df4;
 #pragma unroll
             for (int t = 0; t < J; ++t) {
                 const int idx = 64 * t + lane;
-                v[k][t] = (row[k] >= 0 && idx < df4) ? rp[idx] : make_float4(0, 0, 0, 0);
+                const bool in = row[k] >= 0 && idx < df4;
+                v[k][t] = in ? rp[idx] : make_float4(0, 0, 0, 0);
+                qv[k][t] = in ? qp[idx] : make_float4(0, 0, 0, 0);
             }
         }
 #pragma unroll
         for (int k = 0; k < R; ++k) {
-            if (row[k] < 0) continue;   // past the chunk, or a sentinel slot
+            if (row[k] < 0) continue;   // past the wavefront's records
+            reads += static_cast<uint32_t>(row[k]) != prev;
+            prev = static_cast<uint32_t>(row[k]);
             // same accumulation order as row_score: (t, x, y, z, w), then the butterfly
             float acc = 0.0f;
 #pragma unroll
             for (int t = 0; t < J; ++t) {
                 if (64 * t + lane < df4) {
-                    acc = fmaf(qv[t].x, v[k][t].x, acc);
-                    acc = fmaf(qv[t].y, v[k][t].y, acc);
-                    acc = fmaf(qv[t].z, v[k][t].z, acc);
-                    acc = fmaf(qv[t].w, v[k][t].w, acc);
+                    acc = fmaf(qv[k][t].x, v[k][t].x, acc);
+                    acc = fmaf(qv[k][t].y, v[k][t].y, acc);
+                    acc = fmaf(qv[k][t].z, v[k][t].z, acc);
+                    acc = fmaf(qv[k][t].w, v[k][t].w, acc);
                 }
             }
             for (int off = 32; off > 0; off >>= 1) acc = acc + __shfl_xor(acc, off, 64);
-            const float s = acc;   // identical in every lane
+            const float sc = acc;   // identical in every lane
+            const ScanQ& Q = sq[b[k]];
             float lo, hi;
             pair_interval(Q, sv[k], nv[k], nev[k], dot[k], gamma, lo, hi);
-            bad |= !(lo <= s && s <= hi);
+            if (!(lo <= sc && sc <= hi) && lane == 0) fail[b[k]] = 1;
             const bool dropped =
-                Q.has_cert && (s > Q.s_cert || (s == Q.s_cert && row[k] <= Q.id_cert));
-            if (!dropped && s >= Q.tau) {
-                if (lane == nk)
-                    mykey = (static_cast<uint64_t>(~mono32(s)) << 32) | static_cast<uint32_t>(row[k]);
-                ++nk;
+                Q.has_cert && (sc > Q.s_cert || (sc == Q.s_cert && row[k] <= Q.id_cert));
+            if (!dropped && sc >= Q.tau && lane == k0 + k) {
+                mykey = (static_cast<uint64_t>(~mono32(sc)) << 32) | static_cast<uint32_t>(row[k]);
+                myb = b[k];
             }
         }
     }
-    if (bad && lane == 0) fail[b] = 1;
-    if (nk == 0) return;
+    if (lane == 0) atomicAdd(row_reads, reads);
+    // group the certified lanes by query (one pass per distinct query, ALU
+    // only), then the first lane of each group appends the group with one
+    // atomic, all groups in the same instruction
+    uint64_t todo = __ballot(myb >= 0);
+    if (!todo) return;
+    int leader = 0, rank = 0, size = 0;
+    while (todo) {
+        const int l0 = __ffsll(static_cast<unsigned long long>(todo)) - 1;
+        const int b0 = __builtin_amdgcn_readlane(myb, l0);
+        const uint64_t grp = __ballot(myb == b0);
+        if (myb == b0) {
+            leader = l0;
+            rank = __popcll(grp & ((1ull << lane) - 1ull));
+            size = __popcll(grp);
+        }
+        todo &= ~grp;
+    }
     int base = 0;
-    if (lane == 0) base = atomicAdd(&cert_cnt[b], nk);
-    base = __shfl(base, 0, 64);
-    if (lane < nk) keys[Q.cand_off + base + lane] = mykey;
+    if (myb >= 0 && lane == leader) base = atomicAdd(&cert_cnt[myb], size);
+    base = __shfl(base, leader, 64);
+    if (myb < 0) return;
+    const int64_t pos = static_cast<int64_t>(base) + rank;
+    const ScanQ& Q = sq[myb];
+    if (pos < kSub * Q.cand_cap) keys[Q.cand_off + pos] = mykey;
 }
 
 template <int J>
-static void rescore_j(const IndexView& ix, const float* qrows, const ScanQ* sq, int32_t nq,
-                      const int32_t* cbase, int64_t chunks, const uint2* cand, float gamma,
-                      const int32_t* sub_cnt, uint64_t* keys, int32_t* cert_cnt, int32_t* fail,
-                      hipStream_t stream) {
+static void rescore_j(const IndexView& ix, const float* qrows, const ScanQ* sq,
+                      const int32_t* cbase, int64_t chunks, const int32_t* pair_cnt,
+                      const uint4* pairs, int64_t pair_sub, float gamma, uint64_t* keys,
+                      int32_t* cert_cnt, int32_t* fail, int32_t* row_reads, hipStream_t stream) {
     hipLaunchKernelGGL((k_rescore<J>), dim3(static_cast<uint32_t>(chunks)), dim3(256), 0, stream,
                        reinterpret_cast<const float4*>(ix.rows), ix.df / 4,
-                       reinterpret_cast<const float4*>(qrows), sq, nq, cbase, cand, ix.scale,
-                       ix.vnorm, ix.enorm, gamma, sub_cnt, keys, cert_cnt, fail);
+                       reinterpret_cast<const float4*>(qrows), sq, cbase, pair_cnt, pairs,
+                       pair_sub, ix.scale, ix.vnorm, ix.enorm, gamma, keys, cert_cnt, fail,
+                       row_reads);
 }
 
-int64_t rescore_chunks(const int32_t* total, int32_t nq) {
+int64_t rescore_chunks(const int32_t* pair_cnt, int64_t pair_sub) {
     int64_t c = 0;
-    for (int32_t b = 0; b < nq; ++b) c += (total[b] + kRescoreChunk - 1) / kRescoreChunk;
+    for (int s = 0; s < kSub; ++s) {
+        const int64_t n = std::min<int64_t>(pair_cnt[s * kCntStride], pair_sub);
+        c += (n + kRescoreChunk - 1) / kRescoreChunk;
+    }
     return c;
 }
 
-void launch_rescore(const IndexView& ix, const float* qrows, const ScanQ* sq, int32_t nq,
-                    const int32_t* total, int32_t* cbase, int64_t chunks,
-                    const uint2* cand, float gamma, const int32_t* sub_cnt, uint64_t* keys,
-                    int32_t* cert_cnt, int32_t* fail, hipStream_t stream) {
-    if (nq <= 0) return;
-    hipLaunchKernelGGL(k_chunk_base, dim3(1), dim3(64), 0, stream, total, nq, cbase);
+void launch_rescore(const IndexView& ix, const float* qrows, const ScanQ* sq,
+                    const int32_t* pair_cnt, const uint4* pairs, int64_t pair_sub,
+                    int32_t* cbase, int64_t chunks, float gamma, uint64_t* keys,
+                    int32_t* cert_cnt, int32_t* fail, int32_t* row_reads, hipStream_t stream) {
+    hipLaunchKernelGGL(k_chunk_base, dim3(1), dim3(64), 0, stream, pair_cnt, pair_sub, cbase);
     if (chunks <= 0) return;
 #define PVS_RS(N)                                                                              \
     case N:                                                                                    \
-        rescore_j<N>(ix, qrows, sq, nq, cbase, chunks, cand, gamma, sub_cnt, keys, cert_cnt,  \
-                     fail, stream);                                                            \
+        rescore_j<N>(ix, qrows, sq, cbase, chunks, pair_cnt, pairs, pair_sub, gamma, keys,     \
+                     cert_cnt, fail, row_reads, stream);                                       \
         break;
     switch (row_chunks(ix.df)) {
         PVS_RS(1)

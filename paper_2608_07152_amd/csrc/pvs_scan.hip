@@ -15,8 +15,9 @@ namespace pvs {
 
 // ------------------------------------------------------------------- GEMV
 // One wavefront per 64-row block (lane = row); QB queries per pass, their
-// codes read through scalar loads.  Appends use one atomic per wavefront and
-// query (ballot + prefix count) on the counter of sub-region blk % kSub.
+// codes read through scalar loads.  The block's records (lane order, then
+// query order) take one atomic per wavefront on the counter of sub-region
+// blk % kSub.
 template <int QB, bool SAMPLE>
 __global__ __launch_bounds__(256) void k_scan_gemv(
     const uint4* __restrict__ codes, const float* __restrict__ scale,
@@ -57,6 +58,7 @@ __global__ __launch_bounds__(256) void k_scan_gemv(
             acc[b] = a;
         }
     }
+    uint32_t take = 0;   // bit b: the pair (query b, this row) is a candidate
 #pragma unroll
     for (int b = 0; b < QB; ++b) {
         const ScanQ Q = sq[b];
@@ -67,24 +69,33 @@ __global__ __launch_bounds__(256) void k_scan_gemv(
             const int64_t i = b * o.sample_ld + w * 64 + lane;
             o.sample_lo[i] = elig ? lo : -INFINITY;
             o.sample_hi[i] = elig ? hi : -INFINITY;
-        } else {
-            const bool take = elig && hi >= Q.tau;
-            const uint64_t mask = __ballot(take);
-            if (mask) {
-                const int sub = static_cast<int>(blk & (kSub - 1));
-                const int leader = __ffsll(static_cast<unsigned long long>(mask)) - 1;
-                int base = 0;
-                if (lane == leader)
-                    base = atomicAdd(&o.cand_cnt[(b * kSub + sub) * kCntStride], __popcll(mask));
-                base = __shfl(base, leader, 64);
-                if (take) {
-                    const int64_t pos = base + __popcll(mask & ((1ull << lane) - 1ull));
-                    if (pos < Q.cand_cap) {
-                        const int64_t at = Q.cand_off + sub * Q.cand_cap + pos;
-                        o.cand[at] = make_uint2(static_cast<uint32_t>(row), static_cast<uint32_t>(acc[b]));
-                    }
-                }
-            }
+        } else if (elig && hi >= Q.tau) {
+            take |= 1u << b;
+        }
+    }
+    if (SAMPLE) return;
+    // records in (row, query) order: exclusive prefix of the per-lane counts
+    const int mine = __popc(take);
+    int incl = mine;
+    for (int off = 1; off < 64; off <<= 1) {
+        const int t = __shfl_up(incl, off, 64);
+        if (lane >= off) incl += t;
+    }
+    const int total = __shfl(incl, 63, 64);
+    if (total == 0) return;
+    const int sub = static_cast<int>(blk & (kSub - 1));
+    int base = 0;
+    if (lane == 0) base = atomicAdd(&o.pair_cnt[sub * kCntStride], total);
+    base = __shfl(base, 0, 64);
+    uint4* dst = o.pairs + sub * o.pair_sub;
+    int64_t p = static_cast<int64_t>(base) + (incl - mine);
+#pragma unroll
+    for (int b = 0; b < QB; ++b) {
+        if ((take >> b) & 1u) {
+            if (p < o.pair_sub)
+                dst[p] = make_uint4(static_cast<uint32_t>(row), static_cast<uint32_t>(o.qbase + b),
+                                    static_cast<uint32_t>(acc[b]), 0u);
+            ++p;
         }
     }
 }
@@ -110,7 +121,7 @@ static ScanOut shift_out(const ScanOut& o, int32_t q0) {
     ScanOut s = o;
     if (s.sample_lo) s.sample_lo += q0 * o.sample_ld;
     if (s.sample_hi) s.sample_hi += q0 * o.sample_ld;
-    if (s.cand_cnt) s.cand_cnt += static_cast<int64_t>(q0) * kSub * kCntStride;
+    s.qbase = o.qbase + q0;
     return s;
 }
 
@@ -150,6 +161,67 @@ void launch_scan(const IndexView& ix, const uint64_t* vis, int64_t nblocks, cons
 // therefore 32 consecutive rows of one code chunk: two contiguous 512-byte
 // runs of the chunk-major block layout.
 
+// Records of the candidate pairs of one block and NQS query tiles (q0 is the
+// scan index of the first tile's first query): bit 16 t + r of mask[uu] in
+// lane l marks the pair of query q0 + 32 uu + l % 32 and the row of
+// accumulator element r of acc[t][uu].  One atomic reserves the wavefront's
+// records; they are written row by row (rows in (t, r, l / 32) order, each
+// row's queries ascending), so the records of one row are adjacent.
+template <int NQS>
+__device__ __forceinline__ void emit_pairs(const uint32_t (&mask)[NQS], const v16i (&acc)[2][NQS],
+                                           int64_t blk, int lane, int32_t q0, int sub,
+                                           const ScanOut& o) {
+    int mine = 0;
+#pragma unroll
+    for (int uu = 0; uu < NQS; ++uu) mine += __popc(mask[uu]);
+    for (int off = 32; off > 0; off >>= 1) mine += __shfl_xor(mine, off, 64);
+    if (mine == 0) return;
+    int base = 0;
+    if (lane == 0) base = atomicAdd(&o.pair_cnt[sub * kCntStride], mine);
+    // 32-bit positions and rows: the host keeps every counter and row id
+    // below 2^31
+    int run = __builtin_amdgcn_readfirstlane(base);
+    const int cap = static_cast<int>(o.pair_sub);
+    uint4* dst = o.pairs + sub * o.pair_sub;
+    const uint32_t below = (1u << (lane & 31)) - 1u;
+    const bool upper = lane >= 32;
+    uint32_t row0 = static_cast<uint32_t>(blk * 64) + 4 * (lane >> 5);
+    uint32_t qid = static_cast<uint32_t>(q0 + (lane & 31));
+    // opaque here, so the 32 row numbers derived from row0 are formed at
+    // their stores instead of being hoisted out of the caller's loops (where
+    // they would stay live across the K loop)
+    asm volatile("" : "+v"(row0), "+v"(qid));
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int bit = 16 * t + r;
+            int ca = 0, cb = 0;
+#pragma unroll
+            for (int uu = 0; uu < NQS; ++uu) {
+                const uint64_t bal = __ballot((mask[uu] >> bit) & 1u);
+                ca += __popc(static_cast<uint32_t>(bal));
+                cb += __popc(static_cast<uint32_t>(bal >> 32));
+            }
+            if (ca + cb == 0) continue;
+            int at = run + (upper ? ca : 0);
+#pragma unroll
+            for (int uu = 0; uu < NQS; ++uu) {
+                const uint64_t bal = __ballot((mask[uu] >> bit) & 1u);
+                const uint32_t m = upper ? static_cast<uint32_t>(bal >> 32) : static_cast<uint32_t>(bal);
+                if ((mask[uu] >> bit) & 1u) {
+                    const int p = at + __popc(m & below);
+                    if (p < cap)
+                        dst[p] = make_uint4(row0 + 32 * t + 8 * (r >> 2) + (r & 3), qid + 32 * uu,
+                                            static_cast<uint32_t>(acc[t][uu][r]), 0u);
+                }
+                at += __popc(m);
+            }
+            run += ca + cb;
+        }
+    }
+}
+
 // Query codes of one pass in MFMA B-fragment order:
 // frag[(s * nqt + u) * 64 + lane] = 16 code bytes of query 32 u + lane % 32,
 // bytes 32 s + 16 (lane / 32) .. +15; queries past nq are zero.
@@ -172,7 +244,7 @@ __global__ __launch_bounds__(64) void k_qfrag(const int8_t* __restrict__ qcodes,
 // the block's codes from L2).  Epilogue per query tile: lane l owns query
 // 32 u + l % 32 and 32 of the block's rows; the centre-score pre-test skips
 // the exact interval for rows that cannot reach tau; survivors of lanes l and
-// l ^ 32 (same query) reserve their slots with one atomic.
+// l ^ 32 (same query) become records through emit_pairs.
 template <int NQT, bool SAMPLE>
 __global__ __launch_bounds__(256) void k_scan_mfma(
     const uint4* __restrict__ codes, const float* __restrict__ scale,
@@ -221,12 +293,14 @@ __global__ __launch_bounds__(256) void k_scan_mfma(
             acc[1][u] = __builtin_amdgcn_mfma_i32_32x32x32_i8(va1, vb, acc[1][u], 0, 0, 0);
         }
     }
+    uint32_t mask[NQS];   // candidate bits (16 t + r) of each tile
 #pragma unroll
     for (int uu = 0; uu < NQS; ++uu) {
         const int u = u0 + uu;
         const int b = 32 * u + (lane & 31);
         const bool valid = b < nq;
         const ScanQ Q = sq[valid ? b : 0];
+        mask[uu] = 0;
         if (SAMPLE) {
             if (!valid) continue;
 #pragma unroll
@@ -245,7 +319,6 @@ __global__ __launch_bounds__(256) void k_scan_mfma(
             continue;
         }
         const float thr = center_threshold(Q);
-        uint32_t mask = 0;
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
 #pragma unroll
@@ -256,34 +329,13 @@ __global__ __launch_bounds__(256) void k_scan_mfma(
                 if (valid && c >= thr && ((vbits >> rib) & 1ull)) {
                     float lo, hi;
                     pair_interval(Q, sv, vnr[t][r], enr[t][r], acc[t][uu][r], gamma, lo, hi);
-                    if (hi >= Q.tau && (!Q.has_cert || lo <= Q.s_cert)) mask |= 1u << (16 * t + r);
+                    if (hi >= Q.tau && (!Q.has_cert || lo <= Q.s_cert)) mask[uu] |= 1u << (16 * t + r);
                 }
-            }
-        }
-        const int mine = __popc(mask);
-        const int other = __shfl_xor(mine, 32, 64);
-        const int sub = static_cast<int>(blk & (kSub - 1));
-        int base = 0;
-        if (lane < 32 && mine + other > 0)
-            base = atomicAdd(&o.cand_cnt[(b * kSub + sub) * kCntStride], mine + other);
-        base = __shfl(base, lane & 31, 64);
-        if (!mask) continue;
-        int64_t pos = base + ((lane >= 32) ? other : 0);
-#pragma unroll
-        for (int t = 0; t < 2; ++t) {
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                if (!((mask >> (16 * t + r)) & 1u)) continue;
-                const int rib = 32 * t + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-                const int64_t row = blk * 64 + rib;
-                if (pos < Q.cand_cap) {
-                    const int64_t at = Q.cand_off + sub * Q.cand_cap + pos;
-                    o.cand[at] = make_uint2(static_cast<uint32_t>(row), static_cast<uint32_t>(acc[t][uu][r]));
-                }
-                ++pos;
             }
         }
     }
+    if (!SAMPLE)
+        emit_pairs<NQS>(mask, acc, blk, lane, o.qbase + 32 * u0, static_cast<int>(blk & (kSub - 1)), o);
     }
 }
 
@@ -300,11 +352,9 @@ __global__ __launch_bounds__(256) void k_scan_mfma(
 // Epilogue: lane l owns query 32 u + l % 32 and 32 of the block's rows.  A
 // per-block bound of E + G (from the block's largest norms) gives a centre
 // threshold below which no row of the block can reach tau; invisible rows
-// carry a NaN scale so they fail it.  Candidates are appended through chunks
-// of sub-region blockIdx.x % kSub of each query's region that the workgroup
-// reserves with one global atomic per chunk; slots of a chunk left unused at
-// the end hold the sentinel row -1, which the sub-region's count includes and
-// rescoring skips.
+// carry a NaN scale so they fail it.  Each wavefront writes the records of
+// its block and half through emit_pairs into sub-region blk % kSub (blocks,
+// not workgroups, spread the records evenly over the sub-regions).
 template <int NQT, int PA>
 __global__ __launch_bounds__(256, 2) void k_scan_mfma_wide(
     const uint4* __restrict__ codes, const float* __restrict__ scale,
@@ -316,20 +366,10 @@ __global__ __launch_bounds__(256, 2) void k_scan_mfma_wide(
     __shared__ v4i bsm[2][PA][NQS * 64];       // B fragments of two stages
     __shared__ float s_meta[4][3][64];         // scale (NaN if invisible), norm, error norm
     __shared__ ScanQ s_q[NQT * 32];            // the scanning queries
-    __shared__ int32_t s_wcnt[4][NQS * 32];    // per wave counts, then offsets
-    __shared__ int32_t s_pos[NQT * 32];        // next free slot of each query's chunk
-    __shared__ int32_t s_end[NQT * 32];        // end of that chunk
-    __shared__ int32_t s_old[NQS * 32], s_room[NQS * 32], s_new[NQS * 32];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int sub = static_cast<int>(blockIdx.x & (kSub - 1));
-    // workgroups sharing one sub-region
-    const int64_t wg_per_sub = (static_cast<int64_t>(gridDim.x) + kSub - 1) / kSub;
-    for (int b = tid; b < NQT * 32; b += 256) {
-        s_pos[b] = s_end[b] = 0;
-        if (b < nq) s_q[b] = sq[b];
-    }
+    for (int b = tid; b < nq && b < NQT * 32; b += 256) s_q[b] = sq[b];
     __syncthreads();
     const int nsteps = nchunk >> 1;            // a multiple of PA
     const int64_t ngroups = (nblocks + 3) / 4;
@@ -417,7 +457,6 @@ __global__ __launch_bounds__(256, 2) void k_scan_mfma_wide(
             // margin that covers the rounding of both products), and only
             // pairs that pass it evaluate the exact interval.
             uint32_t mask[NQS];
-            int other[NQS];
             float thq[NQS];
 #pragma unroll
             for (int uu = 0; uu < NQS; ++uu) {
@@ -448,78 +487,14 @@ __global__ __launch_bounds__(256, 2) void k_scan_mfma_wide(
                     }
                 }
             }
-#pragma unroll
-            for (int uu = 0; uu < NQS; ++uu) {
-                const int mine = __popc(mask[uu]);
-                other[uu] = __shfl_xor(mine, 32, 64);
-                if (lane < 32) s_wcnt[wave][32 * uu + lane] = mine + other[uu];
-            }
-            __syncthreads();
-            // one thread per query: wave offsets, and a new chunk of the
-            // query's region when the current one is too small
-            if (tid < NQS * 32) {
-                const int b = 32 * u0 + tid;
-                int tot = 0;
-#pragma unroll
-                for (int w = 0; w < 4; ++w) {
-                    const int c = s_wcnt[w][tid];
-                    s_wcnt[w][tid] = tot;
-                    tot += c;
-                }
-                const int old = s_pos[b];
-                const int room = s_end[b] - old;
-                int nb = 0;
-                if (tot > room) {
-                    const int need = tot - room;
-                    const int64_t cap = s_q[b].cand_cap;
-                    const int64_t per = cap / (16 * wg_per_sub);
-                    const int chunk = static_cast<int>(per < 1 ? 1 : per > kMaxChunk ? kMaxChunk : per);
-                    const int take = need > chunk ? need : chunk;
-                    nb = atomicAdd(&o.cand_cnt[(b * kSub + sub) * kCntStride], take);
-                    s_pos[b] = nb + need;
-                    s_end[b] = nb + take;
-                } else {
-                    s_pos[b] = old + tot;
-                }
-                s_old[tid] = old;
-                s_room[tid] = room;
-                s_new[tid] = nb;
-            }
-            __syncthreads();
-            if (have) {
-#pragma unroll
-                for (int uu = 0; uu < NQS; ++uu) {
-                    if (!mask[uu]) continue;
-                    const int ql = 32 * uu + (lane & 31);
-                    const ScanQ& Q = s_q[32 * u0 + ql];
-                    const int old = s_old[ql], room = s_room[ql], nb = s_new[ql];
-                    int j = s_wcnt[wave][ql] + ((lane >= 32) ? other[uu] : 0);
-#pragma unroll
-                    for (int t = 0; t < 2; ++t) {
-#pragma unroll
-                        for (int r = 0; r < 16; ++r) {
-                            if (!((mask[uu] >> (16 * t + r)) & 1u)) continue;
-                            const int rib = 32 * t + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-                            const int64_t row = blk * 64 + rib;
-                            const int64_t pos = (j < room) ? old + j : nb + (j - room);
-                            if (pos < Q.cand_cap) {
-                                const int64_t at = Q.cand_off + sub * Q.cand_cap + pos;
-                                o.cand[at] = make_uint2(static_cast<uint32_t>(row),
-                                                        static_cast<uint32_t>(acc[t][uu][r]));
-                            }
-                            ++j;
-                        }
-                    }
-                }
-            }
-            __syncthreads();   // bsm, the metadata and the chunk tables are reused next
+            // no code motion across the epilogue (the next half's loads would
+            // raise the register pressure past 256)
+            __builtin_amdgcn_sched_barrier(0);
+            if (have)
+                emit_pairs<NQS>(mask, acc, blk, lane, o.qbase + 32 * u0, static_cast<int>(blk & (kSub - 1)), o);
+            __builtin_amdgcn_sched_barrier(0);
+            __syncthreads();   // bsm and the metadata are reused next
         }
-    }
-    // unused tails of this workgroup's chunks become sentinel rows (-1)
-    for (int b = tid; b < NQT * 32 && b < nq; b += 256) {
-        const ScanQ Q = sq[b];
-        const int64_t e = s_end[b] < Q.cand_cap ? s_end[b] : Q.cand_cap;
-        for (int64_t p = s_pos[b]; p < e; ++p) o.cand[Q.cand_off + sub * Q.cand_cap + p] = make_uint2(0xffffffffu, 0u);
     }
 }
 
@@ -599,35 +574,6 @@ void launch_scan_mfma(const IndexView& ix, const uint64_t* vis, int64_t nblocks,
         }
 #undef PVS_MFMA_CASE
     }
-}
-
-// ------------------------------------------------------ candidate totals
-// One wavefront per query, lane s reads the counter of sub-region s.
-__global__ __launch_bounds__(64) void k_cand_totals(const int32_t* __restrict__ sub_cnt,
-                                                    const ScanQ* __restrict__ sq,
-                                                    int32_t* __restrict__ total,
-                                                    int32_t* __restrict__ need) {
-    static_assert(kSub == 64, "one lane per sub-region");
-    const int b = blockIdx.x;
-    const int lane = threadIdx.x;
-    const int c = sub_cnt[(b * kSub + lane) * kCntStride];
-    const int64_t cap = sq[b].cand_cap;
-    int kept = static_cast<int>(c < cap ? c : cap);
-    int mx = c;
-    for (int off = 32; off > 0; off >>= 1) {
-        kept += __shfl_xor(kept, off, 64);
-        mx = max(mx, __shfl_xor(mx, off, 64));
-    }
-    if (lane == 0) {
-        total[b] = kept;
-        need[b] = mx;
-    }
-}
-
-void launch_cand_totals(const int32_t* sub_cnt, const ScanQ* sq, int32_t nq, int32_t* total,
-                        int32_t* need, hipStream_t stream) {
-    if (nq <= 0) return;
-    hipLaunchKernelGGL(k_cand_totals, dim3(nq), dim3(64), 0, stream, sub_cnt, sq, total, need);
 }
 
 // ------------------------------------------------------------ threshold

@@ -62,7 +62,8 @@ class eahr_query_stats(C.Structure):
 
 class pvs_counters(C.Structure):
     _fields_ = [(n, C.c_int64) for n in ("scans", "sample_scans", "rows_scanned", "bytes_scanned",
-                                          "candidates", "certified", "emitted", "rescans")]
+                                          "candidates", "certified", "emitted", "rescans",
+                                          "overflows")]
 
     def as_dict(self):
         return {f: getattr(self, f) for f, _ in self._fields_}
@@ -75,7 +76,8 @@ class pvs_profile(C.Structure):
                 ("mfma_launches", C.c_int64), ("host_dense_ms", C.c_double),
                 ("host_sparse_ms", C.c_double), ("host_fuse_ms", C.c_double),
                 ("variant_ms", C.c_double * 12), ("variant_launches", C.c_int64 * 12),
-                ("variant_bytes", C.c_int64 * 12), ("rescore_certified", C.c_int64)]
+                ("variant_bytes", C.c_int64 * 12), ("rescore_certified", C.c_int64),
+                ("rescore_row_reads", C.c_int64)]
 
     VARIANTS = [f"k_scan_gemv<{q}>" for q in range(1, 9)] + \
         [f"k_scan_mfma<{t}>" for t in (1, 2, 4, 8)]

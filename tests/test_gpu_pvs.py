@@ -274,6 +274,24 @@ def test_mfma_and_gemv_scans_agree(E, tiny, tiny_index, monkeypatch, B):
         check_dense_prefix(qb[b], x, ia[b], sa[b])
 
 
+@pytest.mark.parametrize("path", ["gemv", "mfma"])
+def test_overflowing_pools_are_scanned_again(E, tiny, tiny_index, monkeypatch, path):
+    """Key regions and the candidate pool sized far too small on the first
+    attempt (a test knob): the records past a sub-region's end are dropped,
+    every query is scanned again with room, and the ranks are bit-equal to an
+    unconstrained run."""
+    w, x, q = tiny
+    qb, _ = datagen.queries(datagen.workload("tiny"), count=70)
+    ref = _open_with_path(E, tiny_index, qb, path, monkeypatch)
+    ir, sr, _ = _drain(E, ref, [20, 300])
+    monkeypatch.setenv("EAHR_CAP_SHRINK", "64")
+    st = _open_with_path(E, tiny_index, qb, path, monkeypatch)
+    monkeypatch.delenv("EAHR_CAP_SHRINK")
+    ig, sg, _ = _drain(E, st, [20, 300])
+    assert ig == ir and sg == sr
+    assert E.pvs_stats(st)["overflows"] > 0 and E.pvs_stats(ref)["overflows"] == 0
+
+
 def test_single_hip_runtime_in_process(E):
     import re
     maps = open("/proc/self/maps").read()
