@@ -222,6 +222,73 @@ __device__ __forceinline__ void emit_pairs(const uint32_t (&mask)[NQS], const v1
     }
 }
 
+// Records of a block for 8 query tiles computed in two halves: the first
+// half's candidate bits m0 (tiles 0-3) with their dot products saved in
+// LDS (sd, this lane's from sd[j], in (t, r, tile) order), the second half's
+// bits m1 (tiles 4-7) with acc.  One atomic; each row's records (all 8 tiles)
+// are adjacent, as in emit_pairs.
+__device__ __forceinline__ void emit_pairs_joined(const uint32_t (&m0)[4], const int32_t* sd, int j,
+                                                  const uint32_t (&m1)[4], const v16i (&acc)[2][4],
+                                                  int64_t blk, int lane, int32_t q0, int sub,
+                                                  const ScanOut& o) {
+    int mine = 0;
+#pragma unroll
+    for (int uu = 0; uu < 4; ++uu) mine += __popc(m0[uu]) + __popc(m1[uu]);
+    for (int off = 32; off > 0; off >>= 1) mine += __shfl_xor(mine, off, 64);
+    if (mine == 0) return;
+    int base = 0;
+    if (lane == 0) base = atomicAdd(&o.pair_cnt[sub * kCntStride], mine);
+    int run = __builtin_amdgcn_readfirstlane(base);
+    const int cap = static_cast<int>(o.pair_sub);
+    uint4* dst = o.pairs + sub * o.pair_sub;
+    const uint32_t below = (1u << (lane & 31)) - 1u;
+    const bool upper = lane >= 32;
+    uint32_t row0 = static_cast<uint32_t>(blk * 64) + 4 * (lane >> 5);
+    uint32_t qid = static_cast<uint32_t>(q0 + (lane & 31));
+    asm volatile("" : "+v"(row0), "+v"(qid));   // as in emit_pairs
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int bit = 16 * t + r;
+            int ca = 0, cb = 0;
+#pragma unroll
+            for (int uu = 0; uu < 4; ++uu) {
+                const uint64_t b0 = __ballot((m0[uu] >> bit) & 1u);
+                const uint64_t b1 = __ballot((m1[uu] >> bit) & 1u);
+                ca += __popc(static_cast<uint32_t>(b0)) + __popc(static_cast<uint32_t>(b1));
+                cb += __popc(static_cast<uint32_t>(b0 >> 32)) + __popc(static_cast<uint32_t>(b1 >> 32));
+            }
+            if (ca + cb == 0) continue;
+            int at = run + (upper ? ca : 0);
+            const uint32_t row = row0 + 32 * t + 8 * (r >> 2) + (r & 3);
+#pragma unroll
+            for (int uu = 0; uu < 4; ++uu) {
+                const uint64_t bal = __ballot((m0[uu] >> bit) & 1u);
+                const uint32_t m = upper ? static_cast<uint32_t>(bal >> 32) : static_cast<uint32_t>(bal);
+                if ((m0[uu] >> bit) & 1u) {
+                    const int p = at + __popc(m & below);
+                    const int32_t dot = sd[j++];
+                    if (p < cap) dst[p] = make_uint4(row, qid + 32 * uu, static_cast<uint32_t>(dot), 0u);
+                }
+                at += __popc(m);
+            }
+#pragma unroll
+            for (int uu = 0; uu < 4; ++uu) {
+                const uint64_t bal = __ballot((m1[uu] >> bit) & 1u);
+                const uint32_t m = upper ? static_cast<uint32_t>(bal >> 32) : static_cast<uint32_t>(bal);
+                if ((m1[uu] >> bit) & 1u) {
+                    const int p = at + __popc(m & below);
+                    if (p < cap)
+                        dst[p] = make_uint4(row, qid + 32 * (4 + uu), static_cast<uint32_t>(acc[t][uu][r]), 0u);
+                }
+                at += __popc(m);
+            }
+            run += ca + cb;
+        }
+    }
+}
+
 // Query codes of one pass in MFMA B-fragment order:
 // frag[(s * nqt + u) * 64 + lane] = 16 code bytes of query 32 u + lane % 32,
 // bytes 32 s + 16 (lane / 32) .. +15; queries past nq are zero.
@@ -366,6 +433,10 @@ __global__ __launch_bounds__(256, 2) void k_scan_mfma_wide(
     __shared__ v4i bsm[2][PA][NQS * 64];       // B fragments of two stages
     __shared__ float s_meta[4][3][64];         // scale (NaN if invisible), norm, error norm
     __shared__ ScanQ s_q[NQT * 32];            // the scanning queries
+    // 8 tiles: dot products of the first half's candidates, written with the
+    // second half's (at most kSavedDots per wavefront, else written at once)
+    constexpr int kSavedDots = 512;
+    __shared__ int32_t s_dots[4][NQT == 8 ? kSavedDots : 1];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
@@ -388,6 +459,8 @@ __global__ __launch_bounds__(256, 2) void k_scan_mfma_wide(
             nvb = wave_max(v ? nv : 0.0f);
             nevb = wave_max(v ? nev : 0.0f);
         }
+        uint32_t mask0[NQS] = {};   // first half's candidates kept for the joined write
+        int j0 = 0;                 // this lane's first saved dot product
 #pragma unroll 1
         for (int u0 = 0; u0 < NQT; u0 += NQS) {
             v16i acc[2][NQS];
@@ -490,8 +563,38 @@ __global__ __launch_bounds__(256, 2) void k_scan_mfma_wide(
             // no code motion across the epilogue (the next half's loads would
             // raise the register pressure past 256)
             __builtin_amdgcn_sched_barrier(0);
-            if (have)
-                emit_pairs<NQS>(mask, acc, blk, lane, o.qbase + 32 * u0, static_cast<int>(blk & (kSub - 1)), o);
+            const int sub = static_cast<int>(blk & (kSub - 1));
+            if (have && NQT == 8 && u0 == 0) {
+                // first of two halves: save the dot products of its candidates
+                // (lane order, then (t, r, tile)) to write them with the second
+                int cnt = 0;
+#pragma unroll
+                for (int uu = 0; uu < NQS; ++uu) cnt += __popc(mask[uu]);
+                int incl = cnt;
+                for (int off = 1; off < 64; off <<= 1) {
+                    const int v = __shfl_up(incl, off, 64);
+                    if (lane >= off) incl += v;
+                }
+                if (__shfl(incl, 63, 64) > kSavedDots) {
+                    emit_pairs<NQS>(mask, acc, blk, lane, o.qbase, sub, o);
+                } else {
+                    int j = incl - cnt;
+                    j0 = j;
+#pragma unroll
+                    for (int t = 0; t < 2; ++t)
+#pragma unroll
+                        for (int r = 0; r < 16; ++r)
+#pragma unroll
+                            for (int uu = 0; uu < NQS; ++uu)
+                                if ((mask[uu] >> (16 * t + r)) & 1u) s_dots[wave][j++] = acc[t][uu][r];
+#pragma unroll
+                    for (int uu = 0; uu < NQS; ++uu) mask0[uu] = mask[uu];
+                }
+            } else if (have && NQT == 8) {
+                emit_pairs_joined(mask0, s_dots[wave], j0, mask, acc, blk, lane, o.qbase, sub, o);
+            } else if (have) {
+                emit_pairs<NQS>(mask, acc, blk, lane, o.qbase + 32 * u0, sub, o);
+            }
             __builtin_amdgcn_sched_barrier(0);
             __syncthreads();   // bsm and the metadata are reused next
         }
