@@ -408,14 +408,18 @@ static void free_buffers(ScanBuffers& b) {
 }
 
 // Per-query scan buffers for nq queries and samples of sample_ld rows.
-// counts layout: [cert nq][fail nq][offs nq + 1][row reads 1]
+// counts layout: [cert nq][fail nq][offs nq + 1][unused 1]
 // [rescore chunk base kSub + 1], then from pair_counts_at(nq) the kSub append
-// counters of the pair pool, kCntStride ints apart.  h_counts mirrors it.
+// counters of the pair pool and from reads_counts_at(nq) the kSub row-load
+// counters of rescoring, kCntStride ints apart.  h_counts mirrors it.
 static size_t pair_counts_at(int32_t nq) {
     return (3 * static_cast<size_t>(nq) + 2 + pvs::kSub + 1 + 63) / 64 * 64;
 }
-static size_t all_counts(int32_t nq) {
+static size_t reads_counts_at(int32_t nq) {
     return pair_counts_at(nq) + static_cast<size_t>(pvs::kSub) * pvs::kCntStride;
+}
+static size_t all_counts(int32_t nq) {
+    return reads_counts_at(nq) + static_cast<size_t>(pvs::kSub) * pvs::kCntStride;
 }
 
 static int ensure_query_buffers(pvs_state* st, int32_t nq, int64_t sample_ld) {
@@ -804,7 +808,7 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     int32_t* d_cert = st->counts;
     int32_t* d_fail = st->counts + nq;
     int32_t* d_offs = st->counts + 2 * nq;
-    int32_t* d_reads = st->counts + 3 * nq + 1;
+    int32_t* d_reads = st->counts + reads_counts_at(nq);
     int32_t* d_cbase = st->counts + 3 * nq + 2;
     int32_t* d_pcnt = st->counts + pair_counts_at(nq);
     const int32_t* h_pcnt = st->h_counts + pair_counts_at(nq);
@@ -865,12 +869,18 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     EAHR_TRY(ensure_host_packed(st, kept));
     HIP_TRY(hipMemcpyAsync(st->h_counts, st->counts, (3 * static_cast<size_t>(nq) + 2) * sizeof(int32_t),
                            hipMemcpyDeviceToHost, s));
+    if (prof)
+        HIP_TRY(hipMemcpyAsync(st->h_counts + reads_counts_at(nq), d_reads,
+                               static_cast<size_t>(pvs::kSub) * pvs::kCntStride * sizeof(int32_t),
+                               hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
     tp[3] = clk::now();
     const int32_t* h_cert = st->h_counts;
     const int32_t* h_fail = st->h_counts + nq;
     const int32_t* h_offs = st->h_counts + 2 * nq;
-    const int64_t row_reads = st->h_counts[3 * nq + 1];
+    int64_t row_reads = 0;
+    if (prof)
+        for (int i = 0; i < pvs::kSub; ++i) row_reads += st->h_counts[reads_counts_at(nq) + i * pvs::kCntStride];
     if (h_offs[nq] > 0)
         HIP_TRY(hipMemcpy(st->h_packed, st->packed, static_cast<size_t>(h_offs[nq]) * sizeof(uint64_t),
                           hipMemcpyDeviceToHost));

@@ -104,9 +104,9 @@ void launch_select(const float* sample_lo, const float* sample_hi, int64_t n, in
 // it against its interval, and appends the keys of the certified pairs of
 // query b at keys[cand_off + j], j < min(cert_cnt[b], kSub * cand_cap)
 // (cert_cnt zeroed by the caller counts them all; order of appends
-// unspecified).  cbase is device scratch of kSub + 1 ints; row_reads (one
-// int, zeroed by the caller) receives the number of row loads, one per run of
-// records of one row inside a wavefront's share.
+// unspecified).  cbase is device scratch of kSub + 1 ints; the kSub counters
+// row_reads[s * kCntStride] (zeroed by the caller) sum to the number of row
+// loads, one per run of records of one row inside a wavefront's share.
 constexpr int kRescoreChunk = 256;
 int64_t rescore_chunks(const int32_t* pair_cnt, int64_t pair_sub);
 void launch_rescore(const IndexView& ix, const float* qrows, const ScanQ* sq,

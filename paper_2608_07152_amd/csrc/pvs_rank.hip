@@ -31,12 +31,14 @@ __global__ __launch_bounds__(64) void k_chunk_base(const int32_t* __restrict__ p
 }
 
 // One workgroup per chunk, one wavefront per quarter of it.  Lane j holds the
-// wavefront's record j; the records are then taken R at a time, each by the
-// whole wavefront (lane l holds elements 256 t + 4 l + i of the row and of
-// the query, the fixed order of row_score).  Records of one row are adjacent,
-// so after the first of them the row comes from cache.  A certified pair's
-// key stays in the lane of its record; at the end the keys of each query are
-// appended to its region with one atomic.
+// wavefront's record j and everything about it that does not need the score:
+// its interval (the scan's arithmetic on the same inputs, so identical to the
+// scan's), its query's threshold and last certified key.  The records are then
+// scored R at a time, each by the whole wavefront (lane l holds elements
+// 256 t + 4 l + i of the row and of the query, the fixed order of row_score);
+// the lane of the record judges the score.  Records of one row are adjacent,
+// so after the first of them the row comes from cache.  At the end the keys
+// of each query are appended to its region with one atomic.
 template <int J>
 __global__ __launch_bounds__(256) void k_rescore(
     const float4* __restrict__ rows, int32_t df4, const float4* __restrict__ qrows,
@@ -63,29 +65,34 @@ __global__ __launch_bounds__(256) void k_rescore(
     const int64_t i0 = static_cast<int64_t>(x - cbase[s]) * kRescoreChunk + wave * PER_WAVE;
     const int n = static_cast<int>(n_s - i0 < PER_WAVE ? n_s - i0 : PER_WAVE);
     if (n <= 0) return;
-    const uint4 rec = (lane < n) ? pairs[s * pair_sub + i0 + lane] : make_uint4(0u, 0u, 0u, 0u);
+    // this lane's record
+    const bool mine = lane < n;
+    const uint4 rec = mine ? pairs[s * pair_sub + i0 + lane] : make_uint4(0u, 0u, 0u, 0u);
+    const int32_t my_row = static_cast<int32_t>(rec.x);
+    const int32_t my_b = static_cast<int32_t>(rec.y);
+    const ScanQ& MQ = sq[my_b];
+    const int32_t my_qi = MQ.qi;
+    float my_lo, my_hi;
+    pair_interval(MQ, scale[my_row], vnorm[my_row], enorm[my_row], static_cast<int32_t>(rec.z), gamma,
+                  my_lo, my_hi);
+    const float my_tau = MQ.tau, my_scert = MQ.s_cert;
+    const int32_t my_idcert = MQ.id_cert;
+    const bool my_hascert = MQ.has_cert != 0;
     constexpr int R = (J <= 4) ? 4 : 1;
     uint64_t mykey = 0;
-    int myb = -1;          // query of this lane's certified record
+    bool cert = false, bad = false;
     int reads = 0;
     uint32_t prev = 0xffffffffu;
     for (int k0 = 0; k0 < n; k0 += R) {
-        int32_t row[R], b[R], dot[R];
-        float sv[R], nv[R], nev[R];
+        int32_t row[R];
         float4 v[R][J], qv[R][J];
 #pragma unroll
         for (int k = 0; k < R; ++k) {
             const int j = k0 + k < n ? k0 + k : n - 1;
-            const bool ok = k0 + k < n;
-            row[k] = ok ? static_cast<int32_t>(__builtin_amdgcn_readlane(rec.x, j)) : -1;
-            b[k] = static_cast<int32_t>(__builtin_amdgcn_readlane(rec.y, j));
-            dot[k] = static_cast<int32_t>(__builtin_amdgcn_readlane(rec.z, j));
-            const int64_t r = row[k] < 0 ? 0 : row[k];
-            sv[k] = scale[r];
-            nv[k] = vnorm[r];
-            nev[k] = enorm[r];
-            const float4* rp = rows + r * df4;
-            const float4* qp = qrows + static_cast<int64_t>(sq[b[k]].qi) * df4;
+            row[k] = k0 + k < n ? __builtin_amdgcn_readlane(my_row, j) : -1;
+            const int32_t qi = __builtin_amdgcn_readlane(my_qi, j);
+            const float4* rp = rows + static_cast<int64_t>(row[k] < 0 ? 0 : row[k]) * df4;
+            const float4* qp = qrows + static_cast<int64_t>(qi) * df4;
 #pragma unroll
             for (int t = 0; t < J; ++t) {
                 const int idx = 64 * t + lane;
@@ -112,23 +119,25 @@ __global__ __launch_bounds__(256) void k_rescore(
             }
             for (int off = 32; off > 0; off >>= 1) acc = acc + __shfl_xor(acc, off, 64);
             const float sc = acc;   // identical in every lane
-            const ScanQ& Q = sq[b[k]];
-            float lo, hi;
-            pair_interval(Q, sv[k], nv[k], nev[k], dot[k], gamma, lo, hi);
-            if (!(lo <= sc && sc <= hi) && lane == 0) fail[b[k]] = 1;
-            const bool dropped =
-                Q.has_cert && (sc > Q.s_cert || (sc == Q.s_cert && row[k] <= Q.id_cert));
-            if (!dropped && sc >= Q.tau && lane == k0 + k) {
-                mykey = (static_cast<uint64_t>(~mono32(sc)) << 32) | static_cast<uint32_t>(row[k]);
-                myb = b[k];
+            if (lane == k0 + k) {
+                bad = !(my_lo <= sc && sc <= my_hi);
+                const bool dropped =
+                    my_hascert && (sc > my_scert || (sc == my_scert && row[k] <= my_idcert));
+                if (!dropped && sc >= my_tau) {
+                    mykey = (static_cast<uint64_t>(~mono32(sc)) << 32) | static_cast<uint32_t>(row[k]);
+                    cert = true;
+                }
             }
         }
     }
-    if (lane == 0) atomicAdd(row_reads, reads);
+    // one of kSub counters (one address for every wavefront would serialise)
+    if (lane == 0) atomicAdd(&row_reads[(blockIdx.x & (kSub - 1)) * kCntStride], reads);
+    if (bad) fail[my_b] = 1;
     // group the certified lanes by query (one pass per distinct query, ALU
     // only), then the first lane of each group appends the group with one
     // atomic, all groups in the same instruction
-    uint64_t todo = __ballot(myb >= 0);
+    const int myb = cert ? my_b : -1;
+    uint64_t todo = __ballot(cert);
     if (!todo) return;
     int leader = 0, rank = 0, size = 0;
     while (todo) {
@@ -143,12 +152,11 @@ __global__ __launch_bounds__(256) void k_rescore(
         todo &= ~grp;
     }
     int base = 0;
-    if (myb >= 0 && lane == leader) base = atomicAdd(&cert_cnt[myb], size);
+    if (cert && lane == leader) base = atomicAdd(&cert_cnt[myb], size);
     base = __shfl(base, leader, 64);
-    if (myb < 0) return;
+    if (!cert) return;
     const int64_t pos = static_cast<int64_t>(base) + rank;
-    const ScanQ& Q = sq[myb];
-    if (pos < kSub * Q.cand_cap) keys[Q.cand_off + pos] = mykey;
+    if (pos < kSub * MQ.cand_cap) keys[MQ.cand_off + pos] = mykey;
 }
 
 template <int J>
