@@ -37,7 +37,7 @@ __global__ __launch_bounds__(64) void k_chunk_base(const int32_t* __restrict__ p
 // scored R at a time, each by the whole wavefront (lane l holds elements
 // 256 t + 4 l + i of the row and of the query, the fixed order of row_score);
 // the lane of the record judges the score.  Records of one row are adjacent,
-// so after the first of them the row comes from cache.  At the end the keys
+// so the row is loaded once for them.  At the end the keys
 // of each query are appended to its region with one atomic.
 template <int J>
 __global__ __launch_bounds__(256) void k_rescore(
@@ -82,39 +82,64 @@ __global__ __launch_bounds__(256) void k_rescore(
     uint64_t mykey = 0;
     bool cert = false, bad = false;
     int reads = 0;
-    uint32_t prev = 0xffffffffu;
+    // the row and the query row of the previous record stay in registers:
+    // a record with the same row (adjacent records) or the same query (a
+    // single-query scan) loads nothing new for it
+    float4 vc[J], qc[J];
+    int32_t rowc = -1, qic = -1;
     for (int k0 = 0; k0 < n; k0 += R) {
-        int32_t row[R];
+        int32_t row[R], qi[R];
+        bool newrow[R], newq[R];
         float4 v[R][J], qv[R][J];
 #pragma unroll
         for (int k = 0; k < R; ++k) {
             const int j = k0 + k < n ? k0 + k : n - 1;
             row[k] = k0 + k < n ? __builtin_amdgcn_readlane(my_row, j) : -1;
-            const int32_t qi = __builtin_amdgcn_readlane(my_qi, j);
+            qi[k] = __builtin_amdgcn_readlane(my_qi, j);
+            const int32_t pr = k == 0 ? rowc : row[k - 1];
+            const int32_t pq = k == 0 ? qic : qi[k - 1];
+            newrow[k] = row[k] >= 0 && row[k] != pr;
+            newq[k] = row[k] >= 0 && qi[k] != pq;
             const float4* rp = rows + static_cast<int64_t>(row[k] < 0 ? 0 : row[k]) * df4;
-            const float4* qp = qrows + static_cast<int64_t>(qi) * df4;
+            const float4* qp = qrows + static_cast<int64_t>(qi[k]) * df4;
+            if (newrow[k]) {
 #pragma unroll
-            for (int t = 0; t < J; ++t) {
-                const int idx = 64 * t + lane;
-                const bool in = row[k] >= 0 && idx < df4;
-                v[k][t] = in ? rp[idx] : make_float4(0, 0, 0, 0);
-                qv[k][t] = in ? qp[idx] : make_float4(0, 0, 0, 0);
+                for (int t = 0; t < J; ++t) {
+                    const int idx = 64 * t + lane;
+                    v[k][t] = idx < df4 ? rp[idx] : make_float4(0, 0, 0, 0);
+                }
+            }
+            if (newq[k]) {
+#pragma unroll
+                for (int t = 0; t < J; ++t) {
+                    const int idx = 64 * t + lane;
+                    qv[k][t] = idx < df4 ? qp[idx] : make_float4(0, 0, 0, 0);
+                }
             }
         }
 #pragma unroll
         for (int k = 0; k < R; ++k) {
             if (row[k] < 0) continue;   // past the wavefront's records
-            reads += static_cast<uint32_t>(row[k]) != prev;
-            prev = static_cast<uint32_t>(row[k]);
+            if (newrow[k]) {
+                ++reads;
+#pragma unroll
+                for (int t = 0; t < J; ++t) vc[t] = v[k][t];
+                rowc = row[k];
+            }
+            if (newq[k]) {
+#pragma unroll
+                for (int t = 0; t < J; ++t) qc[t] = qv[k][t];
+                qic = qi[k];
+            }
             // same accumulation order as row_score: (t, x, y, z, w), then the butterfly
             float acc = 0.0f;
 #pragma unroll
             for (int t = 0; t < J; ++t) {
                 if (64 * t + lane < df4) {
-                    acc = fmaf(qv[k][t].x, v[k][t].x, acc);
-                    acc = fmaf(qv[k][t].y, v[k][t].y, acc);
-                    acc = fmaf(qv[k][t].z, v[k][t].z, acc);
-                    acc = fmaf(qv[k][t].w, v[k][t].w, acc);
+                    acc = fmaf(qc[t].x, vc[t].x, acc);
+                    acc = fmaf(qc[t].y, vc[t].y, acc);
+                    acc = fmaf(qc[t].z, vc[t].z, acc);
+                    acc = fmaf(qc[t].w, vc[t].w, acc);
                 }
             }
             for (int off = 32; off > 0; off >>= 1) acc = acc + __shfl_xor(acc, off, 64);
