@@ -293,13 +293,14 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
                 ::eahr::set_error("%s", sparse_err.c_str());
                 return sparse_rc[b];
             }
-        // merge this round's ranks and certify, one query per task; a long
-        // append may use the threads left over by few queries
+        // merge this round's ranks and certify
         const auto t0 = std::chrono::steady_clock::now();
         int64_t busy = 0;
         for (int32_t b = 0; b < B; ++b) busy += !F[b].resolved && !failed[b] && (dact[b] || sact[b]);
+        // one query per task; a long append of one of few queries takes the
+        // threads the others leave
         for (int32_t b = 0; b < B; ++b) F[b].threads = std::max<int>(1, threads / std::max<int64_t>(busy, 1));
-        parallel_for(B, threads, [&](int64_t b) {
+        auto certify_one = [&](int64_t b) {
             if (F[b].resolved || failed[b]) return;
             if (dact[b]) {
                 if (dsts[b] == EAHR_LIST_FAILED) {
@@ -331,7 +332,8 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
             }
             rounds[b] += 1;
             F[b].certify();
-        });
+        };
+        parallel_for(B, threads, certify_one);
         const double r_fuse = ms_since(t0);
         t_fuse += r_fuse;
         if (::eahr::trace_on()) {

@@ -25,10 +25,13 @@
 // Once one list is closed (read to its end) nothing joins against the other
 // list's id order any more: appends to the open list then test membership in
 // the closed list with a bitmap over ids (and look up the rank in its id
-// order only for the items it holds), and repeats with a second bitmap.  A
-// long such append is split over `threads` host threads (atomic bit updates;
-// the both-seen items are collected per part, and the heap order does not
-// depend on their insertion order because (F, id) is a total order).
+// order only for the items it holds), and repeats with a second bitmap.
+//
+// A long append (either kind) is split over `threads` host threads: the sort
+// by id digit by digit, the joins and merges over ranges of ids (equal ids
+// fall into one range), bits cleared atomically; the both-seen items are
+// collected per range, and the heap order does not depend on their insertion
+// order because (F, id) is a total order.
 #pragma once
 #include <algorithm>
 #include <cstdint>
@@ -104,6 +107,40 @@ inline void sort_by_id(std::vector<uint64_t>& a, std::vector<uint64_t>& tmp) {
     }
 }
 
+// sort_by_id over `parts` host threads: per digit, each part counts its
+// slice, then scatters it (stable) at offsets ordered by (digit, part).
+inline void sort_by_id_parallel(std::vector<uint64_t>& a, std::vector<uint64_t>& tmp, int parts) {
+    const size_t n = a.size();
+    tmp.resize(n);
+    std::vector<uint32_t> cnt(static_cast<size_t>(parts) * 256);
+    for (int d = 0; d < 4; ++d) {
+        const int shift = 32 + 8 * d;
+        std::fill(cnt.begin(), cnt.end(), 0u);
+        parallel_for(parts, parts, [&](int64_t t) {
+            uint32_t* c = cnt.data() + t * 256;
+            for (size_t i = n * t / parts, e = n * (t + 1) / parts; i < e; ++i) ++c[(a[i] >> shift) & 0xff];
+        });
+        uint32_t sum = 0;
+        bool one = false;
+        for (int v = 0; v < 256; ++v) {
+            uint32_t tot = 0;
+            for (int t = 0; t < parts; ++t) {
+                const uint32_t c = cnt[t * 256 + v];
+                cnt[t * 256 + v] = sum + tot;
+                tot += c;
+            }
+            one |= tot == n;
+            sum += tot;
+        }
+        if (one) continue;   // one digit value
+        parallel_for(parts, parts, [&](int64_t t) {
+            uint32_t* c = cnt.data() + t * 256;
+            for (size_t i = n * t / parts, e = n * (t + 1) / parts; i < e; ++i) tmp[c[(a[i] >> shift) & 0xff]++] = a[i];
+        });
+        a.swap(tmp);
+    }
+}
+
 // A both-seen item: its ranks define F exactly; f is F in float64 (relative
 // error below 2^-50), used to order items whose values are far apart.
 struct Scored {
@@ -167,8 +204,8 @@ struct Fusion {
         int64_t size() const { return static_cast<int64_t>(ids.size()); }
     };
 
-    // appends of at least this many ranks while the other list is closed are
-    // split over up to `threads` host threads
+    // appends of at least this many ranks are split over up to `threads`
+    // host threads
     static constexpr int64_t kParallelAppend = int64_t(1) << 16;
 
     const Params* P = nullptr;
@@ -244,32 +281,91 @@ struct Fusion {
         batch.resize(static_cast<size_t>(n));
         for (int64_t j = 0; j < n; ++j)
             batch[j] = (static_cast<uint64_t>(ids[j]) << 32) | static_cast<uint64_t>(p0 + j + 1);
-        sort_by_id(batch, tmp);
+        const int parts = (threads > 1 && n >= kParallelAppend)
+                        ? static_cast<int>(std::min<int64_t>(threads, n / (kParallelAppend / 4)))
+                        : 1;
+        if (parts > 1) sort_by_id_parallel(batch, tmp, parts);
+        else sort_by_id(batch, tmp);
+        // Parts of the id range: part t holds the ids from splitter t on (the
+        // id of batch[n t / parts]) in the batch, the other list's id order
+        // and this list's id order alike, so equal ids meet inside one part.
+        const auto& ob = other.by_id;
+        std::vector<size_t> sa(parts + 1), sb(parts + 1), sm(parts + 1);
+        sa[0] = sb[0] = sm[0] = 0;
+        sa[parts] = batch.size();
+        sb[parts] = ob.size();
+        sm[parts] = me.by_id.size();
+        for (int t = 1; t < parts; ++t) {
+            const uint64_t key = batch[static_cast<size_t>(n) * t / parts] & ~0xffffffffull;
+            sa[t] = std::lower_bound(batch.begin(), batch.end(), key) - batch.begin();
+            sb[t] = std::lower_bound(ob.begin(), ob.end(), key) - ob.begin();
+            sm[t] = std::lower_bound(me.by_id.begin(), me.by_id.end(), key) - me.by_id.begin();
+        }
         // merge-join with the other list: items now seen by both
         const size_t heap0 = both.size();
-        size_t a = 0, b = 0;
-        const auto& ob = other.by_id;
-        while (a < batch.size() && b < ob.size()) {
-            const uint64_t xa = batch[a] >> 32, xb = ob[b] >> 32;
-            if (xa < xb) {
-                ++a;
-            } else if (xb < xa) {
-                ++b;
-            } else {
-                const int64_t ri = static_cast<int64_t>(batch[a] & 0xffffffffu);
-                const int64_t rj = static_cast<int64_t>(ob[b] & 0xffffffffu);
-                me.kill(ri - 1);
-                other.kill(rj - 1);
-                const int64_t x = static_cast<int64_t>(xa);
-                if (!fixed(x)) {
-                    const int64_t r0 = (i == 0) ? ri : rj, r1 = (i == 0) ? rj : ri;
-                    both.push_back(Scored{g_double(*P, 0, r0) + g_double(*P, 1, r1),
-                                          static_cast<int32_t>(r0), static_cast<int32_t>(r1), x});
+        std::vector<std::vector<Scored>> found(parts > 1 ? parts : 0);
+        auto join = [&](size_t a, size_t ae, size_t b, size_t be, std::vector<Scored>& out, bool atomic) {
+            while (a < ae && b < be) {
+                const uint64_t xa = batch[a] >> 32, xb = ob[b] >> 32;
+                if (xa < xb) {
+                    ++a;
+                } else if (xb < xa) {
+                    ++b;
+                } else {
+                    const int64_t ri = static_cast<int64_t>(batch[a] & 0xffffffffu);
+                    const int64_t rj = static_cast<int64_t>(ob[b] & 0xffffffffu);
+                    if (atomic) {
+                        __atomic_fetch_and(&me.alive[(ri - 1) >> 6], ~(1ull << ((ri - 1) & 63)), __ATOMIC_RELAXED);
+                        __atomic_fetch_and(&other.alive[(rj - 1) >> 6], ~(1ull << ((rj - 1) & 63)), __ATOMIC_RELAXED);
+                    } else {
+                        me.kill(ri - 1);
+                        other.kill(rj - 1);
+                    }
+                    const int64_t x = static_cast<int64_t>(xa);
+                    if (!fixed(x)) {
+                        const int64_t r0 = (i == 0) ? ri : rj, r1 = (i == 0) ? rj : ri;
+                        out.push_back(Scored{g_double(*P, 0, r0) + g_double(*P, 1, r1),
+                                             static_cast<int32_t>(r0), static_cast<int32_t>(r1), x});
+                    }
+                    ++a;
+                    ++b;
                 }
-                ++a;
-                ++b;
+            }
+        };
+        // merge into the id order; a repeated id meets its twin here (or,
+        // inside the batch, its neighbour)
+        merged.resize(me.by_id.size() + batch.size());
+        auto merge = [&](size_t x0, size_t x1, size_t y0, size_t y1) -> bool {
+            bool eq = false;
+            for (size_t k = y0 + 1; k < y1; ++k) eq |= (batch[k] >> 32) == (batch[k - 1] >> 32);
+            const uint64_t* x = me.by_id.data() + x0;
+            const uint64_t* xe = me.by_id.data() + x1;
+            const uint64_t* y = batch.data() + y0;
+            const uint64_t* ye = batch.data() + y1;
+            uint64_t* out = merged.data() + x0 + y0;
+            while (x < xe && y < ye) {
+                eq |= (*x >> 32) == (*y >> 32);
+                *out++ = (*y < *x) ? *y++ : *x++;
+            }
+            out = std::copy(x, xe, out);
+            std::copy(y, ye, out);
+            return eq;
+        };
+        if (parts == 1) {
+            join(0, batch.size(), 0, ob.size(), both, false);
+            dup |= merge(0, me.by_id.size(), 0, batch.size());
+        } else {
+            std::vector<uint8_t> eq(parts, 0);
+            parallel_for(parts, parts, [&](int64_t t) {
+                join(sa[t], sa[t + 1], sb[t], sb[t + 1], found[t], true);
+                eq[t] = merge(sm[t], sm[t + 1], sa[t], sa[t + 1]);
+            });
+            for (int t = 0; t < parts; ++t) {
+                dup |= eq[t] != 0;
+                both.insert(both.end(), found[t].begin(), found[t].end());
             }
         }
+        me.by_id.swap(merged);
         // restore the heap: one push per new item, or a linear rebuild when
         // the round added many
         const size_t added = both.size() - heap0;
@@ -279,25 +375,6 @@ struct Fusion {
             for (size_t k = heap0 + 1; k <= both.size(); ++k)
                 std::push_heap(both.begin(), both.begin() + k, HeapLess{P});
         }
-        // merge into the id order; a repeated id meets its twin here
-        for (size_t k = 1; k < batch.size(); ++k) dup |= (batch[k] >> 32) == (batch[k - 1] >> 32);
-        merged.resize(me.by_id.size() + batch.size());
-        {
-            const uint64_t* x = me.by_id.data();
-            const uint64_t* xe = x + me.by_id.size();
-            const uint64_t* y = batch.data();
-            const uint64_t* ye = y + batch.size();
-            uint64_t* out = merged.data();
-            bool eq = false;
-            while (x < xe && y < ye) {
-                eq |= (*x >> 32) == (*y >> 32);
-                *out++ = (*y < *x) ? *y++ : *x++;
-            }
-            out = std::copy(x, xe, out);
-            std::copy(y, ye, out);
-            dup |= eq;
-        }
-        me.by_id.swap(merged);
     }
 
     // Ranks p0 + j + 1 (j in [j0, j1)) of list i while the other list is

@@ -17,75 +17,99 @@ inline int host_threads() {
     return static_cast<int>(std::min(n, 16u));
 }
 
-// Persistent worker threads for parallel_for: one job at a time; a caller
-// that finds the pool busy (another thread's job) is told so and uses its
-// own threads instead.
+// Persistent worker threads shared by every parallel_for of the process.
+// A call posts a job (items [0, n), at most `extra` helpers) and works on it
+// itself; idle workers join open jobs.  Calls may run concurrently and may
+// nest (a job's item may post a job): a caller only ever waits for items
+// that are already running, so every wait ends.
 class WorkerPool {
 public:
     static WorkerPool& get() {
         static WorkerPool pool(host_threads() - 1);
         return pool;
     }
-    // Runs work() on the caller and up to `extra` workers; false when busy.
-    bool run(int extra, const std::function<void()>& work) {
-        bool idle = false;
-        if (!busy_.compare_exchange_strong(idle, true, std::memory_order_acquire)) return false;
-        extra = std::max(0, std::min<int>(extra, static_cast<int>(workers_.size())));
+
+    void run(int64_t n, int extra, const std::function<void(int64_t)>& f) {
+        Job job;
+        job.f = &f;
+        job.n = n;
+        job.helpers = std::max(0, extra);
+        if (job.helpers > 0 && !workers_.empty()) {
+            {
+                std::lock_guard<std::mutex> lk(mu_);
+                jobs_.push_back(&job);
+            }
+            cv_.notify_all();
+        }
+        work_on(job);
         {
+            // no new helper may join once the job is withdrawn
             std::lock_guard<std::mutex> lk(mu_);
-            fn_ = &work;
-            want_ = extra;
-            pending_ = extra;
-            ++gen_;
+            jobs_.erase(std::remove(jobs_.begin(), jobs_.end(), &job), jobs_.end());
         }
-        if (extra > 0) cv_.notify_all();
-        work();
-        {
-            std::unique_lock<std::mutex> lk(mu_);
-            done_.wait(lk, [&] { return pending_ == 0; });
-            fn_ = nullptr;
-        }
-        busy_.store(false, std::memory_order_release);
-        return true;
+        std::unique_lock<std::mutex> lk(job.mu);
+        job.cv.wait(lk, [&] { return job.active == 0; });
     }
+
     ~WorkerPool() {
         {
             std::lock_guard<std::mutex> lk(mu_);
             stop_ = true;
-            ++gen_;
         }
         cv_.notify_all();
         for (auto& t : workers_) t.join();
     }
 
 private:
+    struct Job {
+        const std::function<void(int64_t)>* f = nullptr;
+        int64_t n = 0;
+        int helpers = 0;                    // helpers still allowed to join
+        std::atomic<int64_t> next{0};
+        std::mutex mu;
+        std::condition_variable cv;
+        int active = 0;                     // helpers inside work_on
+    };
+
     explicit WorkerPool(int n) {
-        for (int i = 0; i < n; ++i) workers_.emplace_back([this, i] { loop(i); });
+        for (int i = 0; i < n; ++i) workers_.emplace_back([this] { loop(); });
     }
-    void loop(int id) {
-        uint64_t seen = 0;
+
+    static void work_on(Job& job) {
+        for (int64_t i = job.next.fetch_add(1); i < job.n; i = job.next.fetch_add(1)) (*job.f)(i);
+    }
+
+    void loop() {
         for (;;) {
-            const std::function<void()>* f = nullptr;
+            Job* job = nullptr;
             {
                 std::unique_lock<std::mutex> lk(mu_);
-                cv_.wait(lk, [&] { return stop_ || gen_ != seen; });
+                // the job is picked inside the wait: items are taken without
+                // the pool lock, so a second look could find none left
+                cv_.wait(lk, [&] {
+                    if (stop_) return true;
+                    for (Job* j : jobs_)
+                        if (j->helpers > 0 && j->next.load(std::memory_order_relaxed) < j->n) {
+                            job = j;
+                            return true;
+                        }
+                    return false;
+                });
                 if (stop_) return;
-                seen = gen_;
-                if (id >= want_) continue;   // not needed for this job
-                f = fn_;
+                --job->helpers;
+                std::lock_guard<std::mutex> jl(job->mu);   // registered before the pool lock is released
+                ++job->active;
             }
-            (*f)();
-            std::lock_guard<std::mutex> lk(mu_);
-            if (--pending_ == 0) done_.notify_one();
+            work_on(*job);
+            std::lock_guard<std::mutex> jl(job->mu);
+            if (--job->active == 0) job->cv.notify_all();
         }
     }
-    std::atomic<bool> busy_{false};         // a job is running (nested calls see it too)
+
     std::mutex mu_;
-    std::condition_variable cv_, done_;
+    std::condition_variable cv_;
+    std::vector<Job*> jobs_;
     std::vector<std::thread> workers_;
-    const std::function<void()>* fn_ = nullptr;
-    uint64_t gen_ = 0;
-    int want_ = 0, pending_ = 0;
     bool stop_ = false;
 };
 
@@ -97,17 +121,9 @@ void parallel_for(int64_t n, int threads, F&& f) {
         for (int64_t i = 0; i < n; ++i) f(i);
         return;
     }
-    std::atomic<int64_t> next{0};
-    const std::function<void()> work = [&]() {
-        for (int64_t i = next.fetch_add(1); i < n; i = next.fetch_add(1)) f(i);
-    };
+    const std::function<void(int64_t)> work = [&](int64_t i) { f(i); };
     const int extra = static_cast<int>(std::min<int64_t>(threads, n)) - 1;
-    if (WorkerPool::get().run(extra, work)) return;
-    std::vector<std::thread> pool;
-    pool.reserve(extra);
-    for (int t = 0; t < extra; ++t) pool.emplace_back(work);
-    work();
-    for (auto& t : pool) t.join();
+    WorkerPool::get().run(n, extra, work);
 }
 
 }  // namespace eahr

@@ -143,6 +143,55 @@ def test_fuse_lists_deep_reads_after_the_other_list_closed():
         eahr.eahr_fuse_lists(bad, b, K=20)
 
 
+def test_fuse_lists_deep_reads_with_both_lists_open():
+    """Two long partially overlapping lists read deep while both stay open:
+    appends of that size sort, join and merge over several host threads.  A
+    repeat deep in one list is still rejected."""
+    rng = np.random.default_rng(12)
+    n = 700_000
+    a = rng.permutation(n)
+    b = a.copy()
+    for s0 in range(0, n, 50_000):
+        b[s0:s0 + 50_000] = rng.permutation(b[s0:s0 + 50_000])
+    b = np.concatenate([b[300_000:], b[:300_000]])
+    for wts in ((1, 1), (2, 1)):
+        got, st = eahr.eahr_fuse_lists(a, b, K=20, w_dense=wts[0], w_sparse=wts[1])
+        assert list(got) == rrf.rrf_topk([a, b], list(wts), 60, 20)
+        assert st["dense_depth"] > 200_000 and st["sparse_status"] == eahr.LIST_OPEN
+    bad = np.concatenate([a[:250_000], a[200_000:200_001], a[250_000:]])
+    with pytest.raises(eahr.EahrError):
+        eahr.eahr_fuse_lists(bad, b, K=20)
+
+
+def test_fuse_lists_concurrent_calls():
+    """Several host threads call the fusion at once, each with appends long
+    enough to be split over the shared worker threads (nested and concurrent
+    use of the pool); every call returns its own exact result."""
+    import threading
+    rng = np.random.default_rng(13)
+    cases = []
+    for _ in range(4):
+        n = 300_000
+        a = rng.permutation(n)
+        b = a.copy()
+        for s0 in range(0, n, 30_000):
+            b[s0:s0 + 30_000] = rng.permutation(b[s0:s0 + 30_000])
+        b = np.concatenate([b[100_000:], b[:100_000]])
+        cases.append((a, b))
+    want = [rrf.rrf_topk([a, b], [1, 1], 60, 20) for a, b in cases]
+    got = [None] * len(cases)
+
+    def run(i):
+        got[i] = list(eahr.eahr_fuse_lists(*cases[i], K=20)[0])
+
+    ts = [threading.Thread(target=run, args=(i,)) for i in range(len(cases))]
+    for t in ts:
+        t.start()
+    for t in ts:
+        t.join()
+    assert got == want
+
+
 def test_fuse_lists_large_prefixes_equal_complete_rrf():
     """Deep prefixes (several table growths of the id bookkeeping): partially
     overlapping permutations of 200,000 ids."""
