@@ -34,11 +34,11 @@ __global__ __launch_bounds__(64) void k_chunk_base(const int32_t* __restrict__ p
 // wavefront's record j and everything about it that does not need the score:
 // its interval (the scan's arithmetic on the same inputs, so identical to the
 // scan's), its query's threshold and last certified key.  The records are then
-// scored R at a time, each by the whole wavefront (lane l holds elements
-// 256 t + 4 l + i of the row and of the query, the fixed order of row_score);
-// the lane of the record judges the score.  Records of one row are adjacent,
-// so the row is loaded once for them.  At the end the keys
-// of each query are appended to its region with one atomic.
+// scored one after another, each by the whole wavefront (lane l holds
+// elements 256 t + 4 l + i of the row and of the query, the fixed order of
+// row_score); the lane of the record judges the score.  Records of one row
+// are adjacent, so the row is loaded once for them.  At the end the keys of
+// each query are appended to its region with one atomic.
 template <int J>
 __global__ __launch_bounds__(256) void k_rescore(
     const float4* __restrict__ rows, int32_t df4, const float4* __restrict__ qrows,
@@ -78,80 +78,57 @@ __global__ __launch_bounds__(256) void k_rescore(
     const float my_tau = MQ.tau, my_scert = MQ.s_cert;
     const int32_t my_idcert = MQ.id_cert;
     const bool my_hascert = MQ.has_cert != 0;
-    constexpr int R = (J <= 4) ? 4 : 1;
     uint64_t mykey = 0;
     bool cert = false, bad = false;
     int reads = 0;
-    // the row and the query row of the previous record stay in registers:
-    // a record with the same row (adjacent records) or the same query (a
-    // single-query scan) loads nothing new for it
+    // One record at a time, its row and query row kept in registers for the
+    // next record: adjacent records of one row (or one query) load nothing
+    // new.  Few registers (about 64) buy the occupancy that hides the gather
+    // latency; keeping several records in flight per wavefront measured
+    // slower (15 % at 4 in flight, more beyond).
     float4 vc[J], qc[J];
     int32_t rowc = -1, qic = -1;
-    for (int k0 = 0; k0 < n; k0 += R) {
-        int32_t row[R], qi[R];
-        bool newrow[R], newq[R];
-        float4 v[R][J], qv[R][J];
-#pragma unroll
-        for (int k = 0; k < R; ++k) {
-            const int j = k0 + k < n ? k0 + k : n - 1;
-            row[k] = k0 + k < n ? __builtin_amdgcn_readlane(my_row, j) : -1;
-            qi[k] = __builtin_amdgcn_readlane(my_qi, j);
-            const int32_t pr = k == 0 ? rowc : row[k - 1];
-            const int32_t pq = k == 0 ? qic : qi[k - 1];
-            newrow[k] = row[k] >= 0 && row[k] != pr;
-            newq[k] = row[k] >= 0 && qi[k] != pq;
-            const float4* rp = rows + static_cast<int64_t>(row[k] < 0 ? 0 : row[k]) * df4;
-            const float4* qp = qrows + static_cast<int64_t>(qi[k]) * df4;
-            if (newrow[k]) {
-#pragma unroll
-                for (int t = 0; t < J; ++t) {
-                    const int idx = 64 * t + lane;
-                    v[k][t] = idx < df4 ? rp[idx] : make_float4(0, 0, 0, 0);
-                }
-            }
-            if (newq[k]) {
-#pragma unroll
-                for (int t = 0; t < J; ++t) {
-                    const int idx = 64 * t + lane;
-                    qv[k][t] = idx < df4 ? qp[idx] : make_float4(0, 0, 0, 0);
-                }
-            }
-        }
-#pragma unroll
-        for (int k = 0; k < R; ++k) {
-            if (row[k] < 0) continue;   // past the wavefront's records
-            if (newrow[k]) {
-                ++reads;
-#pragma unroll
-                for (int t = 0; t < J; ++t) vc[t] = v[k][t];
-                rowc = row[k];
-            }
-            if (newq[k]) {
-#pragma unroll
-                for (int t = 0; t < J; ++t) qc[t] = qv[k][t];
-                qic = qi[k];
-            }
-            // same accumulation order as row_score: (t, x, y, z, w), then the butterfly
-            float acc = 0.0f;
+    for (int k = 0; k < n; ++k) {
+        const int32_t row = __builtin_amdgcn_readlane(my_row, k);
+        const int32_t qi = __builtin_amdgcn_readlane(my_qi, k);
+        if (row != rowc) {
+            const float4* rp = rows + static_cast<int64_t>(row) * df4;
 #pragma unroll
             for (int t = 0; t < J; ++t) {
-                if (64 * t + lane < df4) {
-                    acc = fmaf(qc[t].x, vc[t].x, acc);
-                    acc = fmaf(qc[t].y, vc[t].y, acc);
-                    acc = fmaf(qc[t].z, vc[t].z, acc);
-                    acc = fmaf(qc[t].w, vc[t].w, acc);
-                }
+                const int idx = 64 * t + lane;
+                vc[t] = idx < df4 ? rp[idx] : make_float4(0, 0, 0, 0);
             }
-            for (int off = 32; off > 0; off >>= 1) acc = acc + __shfl_xor(acc, off, 64);
-            const float sc = acc;   // identical in every lane
-            if (lane == k0 + k) {
-                bad = !(my_lo <= sc && sc <= my_hi);
-                const bool dropped =
-                    my_hascert && (sc > my_scert || (sc == my_scert && row[k] <= my_idcert));
-                if (!dropped && sc >= my_tau) {
-                    mykey = (static_cast<uint64_t>(~mono32(sc)) << 32) | static_cast<uint32_t>(row[k]);
-                    cert = true;
-                }
+            rowc = row;
+            ++reads;
+        }
+        if (qi != qic) {
+            const float4* qp = qrows + static_cast<int64_t>(qi) * df4;
+#pragma unroll
+            for (int t = 0; t < J; ++t) {
+                const int idx = 64 * t + lane;
+                qc[t] = idx < df4 ? qp[idx] : make_float4(0, 0, 0, 0);
+            }
+            qic = qi;
+        }
+        // same accumulation order as row_score: (t, x, y, z, w), then the butterfly
+        float acc = 0.0f;
+#pragma unroll
+        for (int t = 0; t < J; ++t) {
+            if (64 * t + lane < df4) {
+                acc = fmaf(qc[t].x, vc[t].x, acc);
+                acc = fmaf(qc[t].y, vc[t].y, acc);
+                acc = fmaf(qc[t].z, vc[t].z, acc);
+                acc = fmaf(qc[t].w, vc[t].w, acc);
+            }
+        }
+        for (int off = 32; off > 0; off >>= 1) acc = acc + __shfl_xor(acc, off, 64);
+        const float sc = acc;   // identical in every lane
+        if (lane == k) {
+            bad = !(my_lo <= sc && sc <= my_hi);
+            const bool dropped = my_hascert && (sc > my_scert || (sc == my_scert && row <= my_idcert));
+            if (!dropped && sc >= my_tau) {
+                mykey = (static_cast<uint64_t>(~mono32(sc)) << 32) | static_cast<uint32_t>(row);
+                cert = true;
             }
         }
     }
