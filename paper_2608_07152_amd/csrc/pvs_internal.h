@@ -37,12 +37,14 @@ constexpr int64_t kTargetBudget = 8192;
 // up to kSpecFactor times the depth reached after the request, within
 // kSpecBudget ranks per scan shared by its queries.  Rescoring a row costs
 // about 1/1000 of streaming the codes once, so over-certifying is cheap next
-// to an extra scan.
+// to an extra scan.  Measured on 8.8M x 768 (queries/s at batch 256 / 1 / 64):
+// factor 8 and 2^20 ranks 1,860 / 90 / 1,085; 8 and 2^22 2,355 / 106 / 1,128;
+// 16 and 2^22 2,338 / 117 / 1,241; 2^23 and 2^24 are slower again.
 // A scan certifies at least kSpecFloor ranks per query (within the same
 // budget): a round of a batch scan costs about as much as rescoring a few
 // thousand ranks per query, so shallow requests are served ahead.
-constexpr int64_t kSpecFactor = 8;
-constexpr int64_t kSpecBudget = int64_t(1) << 20;
+constexpr int64_t kSpecFactor = 16;
+constexpr int64_t kSpecBudget = int64_t(1) << 22;
 constexpr int64_t kSpecFloor = 4096;
 // Scans of at least this many queries use the Int8 MFMA kernel; smaller ones
 // the dot4 GEMV kernel, which streams the codes at the HBM rate for up to 8
