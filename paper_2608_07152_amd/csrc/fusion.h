@@ -76,7 +76,8 @@ inline bool precedes(const Frac& a, int64_t x, const Frac& b, int64_t y) {
 
 // Ascending sort of (id << 32 | rank) keys by id (ids < 2^31): least-
 // significant-digit radix sort on the id bytes (256 scatter targets stay in
-// cache), skipping bytes equal in every id; short runs use a comparison sort.
+// cache; 12-bit digits, one pass fewer for ids below 2^24, measured slower),
+// skipping bytes equal in every id; short runs use a comparison sort.
 inline void sort_by_id(std::vector<uint64_t>& a, std::vector<uint64_t>& tmp) {
     const size_t n = a.size();
     if (n < 1024) {
@@ -305,12 +306,13 @@ struct Fusion {
         const size_t heap0 = both.size();
         std::vector<std::vector<Scored>> found(parts > 1 ? parts : 0);
         auto join = [&](size_t a, size_t ae, size_t b, size_t be, std::vector<Scored>& out, bool atomic) {
+            // ids interleave at random: the advance is branch-free, only a
+            // match (rarer) branches
             while (a < ae && b < be) {
                 const uint64_t xa = batch[a] >> 32, xb = ob[b] >> 32;
-                if (xa < xb) {
-                    ++a;
-                } else if (xb < xa) {
-                    ++b;
+                if (xa != xb) {
+                    a += xa < xb;
+                    b += xb < xa;
                 } else {
                     const int64_t ri = static_cast<int64_t>(batch[a] & 0xffffffffu);
                     const int64_t rj = static_cast<int64_t>(ob[b] & 0xffffffffu);
@@ -343,9 +345,13 @@ struct Fusion {
             const uint64_t* y = batch.data() + y0;
             const uint64_t* ye = batch.data() + y1;
             uint64_t* out = merged.data() + x0 + y0;
-            while (x < xe && y < ye) {
-                eq |= (*x >> 32) == (*y >> 32);
-                *out++ = (*y < *x) ? *y++ : *x++;
+            while (x < xe && y < ye) {   // branch-free: the order of x and y is random
+                const uint64_t vx = *x, vy = *y;
+                eq |= (vx >> 32) == (vy >> 32);
+                const bool ty = vy < vx;
+                *out++ = ty ? vy : vx;
+                y += ty;
+                x += !ty;
             }
             out = std::copy(x, xe, out);
             std::copy(y, ye, out);
