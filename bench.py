@@ -70,6 +70,9 @@ def parse():
     ap.add_argument("--range-size", type=int, default=4096)
     ap.add_argument("--cpu-queries", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-ablation", action="store_true",
+                    help="skip the rank-generator ablation (global-scale scalar quantisation vs PVS)")
+    ap.add_argument("--ablation-queries", type=int, default=20)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MB")
     return ap.parse_args()
 
@@ -166,6 +169,87 @@ def query_set_for(w, batch):
     if w.name != "passage":
         return "default"
     return {64: "b64", 256: "b256"}.get(batch, "single")
+
+
+def generator_ablation(eahr, torch, x, idx, pbm, qdev, sparse_q, w, K, wts, nq, batch):
+    """Rank-generator ablation (Sec. 4.4, Table 4-1): the same eahr_topk with
+    the dense generator replaced by global-scale scalar-quantisation intervals.
+    Single requests are timed in pairs (order alternating, 1 warm-up + 3 runs
+    each, median per query) and compared by the geometric mean of the
+    per-query latency ratios; the batch is timed for 1 warm-up + 2 steps each.
+    f32 evaluations are the rescored (query, row) pairs of each call."""
+    import numpy as np
+    log("ablation: building the global-scale index")
+    t = time.perf_counter()
+    gidx = eahr.pvs_build_quant(x, "global")
+    torch.cuda.synchronize()
+    log(f"ablation: global-scale index built in {time.perf_counter() - t:.1f}s")
+    gens = {"pvs": idx, "scalar": gidx}
+
+    def call(ix, a, b):
+        eahr.pvs_profile_enable(True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        r = eahr.eahr_topk(ix, pbm, a, b, K=K, w_dense=wts[0], w_sparse=wts[1])
+        torch.cuda.synchronize()
+        el = time.perf_counter() - t0
+        pairs = eahr.pvs_profile_read()["rescore_rows"]
+        eahr.pvs_profile_enable(False)
+        return el, pairs, r
+
+    name1 = query_set_for(w, 1)
+    qd, qs = qdev[name1], sparse_q[name1]
+    nq = min(nq, qd.shape[0])
+    lat = {g: [] for g in gens}
+    evals = {g: [] for g in gens}
+    same = 0
+    for i in range(nq):
+        a, b = qd[i:i + 1], qs[i:i + 1]
+        order = list(gens) if i % 2 == 0 else list(gens)[::-1]
+        times = {g: [] for g in gens}
+        ids = {}
+        for rep in range(4):
+            for g in order:
+                el, pairs, r = call(gens[g], a, b)
+                if rep:
+                    times[g].append(el)
+                else:
+                    evals[g].append(pairs)
+                    ids[g] = r[0][0, :r[1][0]].tolist()
+        same += ids["pvs"] == ids["scalar"]
+        for g in gens:
+            lat[g].append(float(np.median(times[g])))
+    ratio = float(np.exp(np.mean(np.log(np.array(lat["scalar"]) / np.array(lat["pvs"])))))
+    single = {
+        "queries": nq, "scalar_over_pvs_latency_gmean": ratio,
+        "median_ms": {g: float(np.median(lat[g]) * 1e3) for g in gens},
+        "f32_evals_median": {g: float(np.median(evals[g])) for g in gens},
+        "f32_evals_reduction": 1.0 - float(np.median(evals["pvs"])) / max(1.0, float(np.median(evals["scalar"]))),
+        "topk_identical": same,
+    }
+    log(f"ablation: single requests scalar/pvs = {ratio:.3f}, f32 evals "
+        f"{single['f32_evals_median']['pvs']:.0f} vs {single['f32_evals_median']['scalar']:.0f}")
+    nameb = query_set_for(w, batch)
+    a, b = qdev[nameb][:batch], sparse_q[nameb][:batch]
+    bt = {}
+    for g in gens:
+        call(gens[g], a, b)
+        runs = [call(gens[g], a, b) for _ in range(2)]
+        bt[g] = {"ms_per_step": float(np.mean([r[0] for r in runs]) * 1e3),
+                 "f32_evals_per_step": float(np.mean([r[1] for r in runs])),
+                 "ids": runs[0][2][0]}
+    batched = {
+        "batch": batch,
+        "scalar_over_pvs_latency": bt["scalar"]["ms_per_step"] / bt["pvs"]["ms_per_step"],
+        "ms_per_step": {g: bt[g]["ms_per_step"] for g in gens},
+        "f32_evals_per_step": {g: bt[g]["f32_evals_per_step"] for g in gens},
+        "topk_identical": bool(np.array_equal(bt["pvs"]["ids"], bt["scalar"]["ids"])),
+    }
+    log(f"ablation: batch {batch} scalar/pvs = {batched['scalar_over_pvs_latency']:.3f}")
+    eahr.pvs_free(gidx)
+    torch.cuda.synchronize()
+    return {"alternative": "scalar-quantisation intervals (one global scale)", "reference": "pvs",
+            "single_requests": single, "batch": batched}
 
 
 def main():
@@ -303,6 +387,11 @@ def main():
     for cfg in configs[1:]:
         per_batch.append(run_config(*cfg)[0])
 
+    ablation = None
+    if not args.no_ablation:
+        ablation = generator_ablation(eahr, torch, x, idx, pbm, qdev, sparse_q, w, K, wts,
+                                      args.ablation_queries, args.batch)
+
     line = {
         "metric": "exact Top-20 EAHR queries/s at 8.8Mx768 (PVS scan HBM GB/s in roofline)",
         "value": head["queries_per_s"],
@@ -323,6 +412,8 @@ def main():
         "roofline_scan": roofline_of(head["scan_kernel"], head["kernels"][head["scan_kernel"]]),
         "per_batch": per_batch,
     }
+    if ablation is not None:
+        line["ablation"] = ablation
     if not args.no_cpu_baseline:
         bsz = configs[0][0]
         name = query_set_for(w, bsz)

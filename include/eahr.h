@@ -65,6 +65,23 @@ typedef struct pbm_state pbm_state;
 int pvs_build(const float* corpus, int64_t n, int32_t d, int32_t ptr_kind,
               void* stream, pvs_index** out);
 
+/* Quantisation modes of pvs_build_quant. */
+enum { EAHR_QUANT_PER_VECTOR = 0, EAHR_QUANT_GLOBAL = 1 };
+
+/* pvs_build_quant -- pvs_build with a choice of scale: EAHR_QUANT_PER_VECTOR
+ * is pvs_build (one scale per row, Sec. 2.3.1); EAHR_QUANT_GLOBAL gives every
+ * row one shared scale s = fl32(max |x| / 127) over the corpus (1 for an
+ * all-zero corpus), the scalar-quantisation interval generator that Sec. 3.5
+ * and Sec. 4.4 (Table 4-1) compare PVS with.  Codes, norms, intervals,
+ * rescoring and the pvs_next contract are otherwise identical, so the two
+ * modes rank identically and differ only in how many pairs are rescored.
+ * The shared scale is fixed by the first non-empty pvs_build_quant or
+ * pvs_insert; later inserts reuse it, and their codes clip at +-127 (the
+ * error norm is computed from the clipped codes, so intervals stay valid).
+ * Errors: those of pvs_build, and EAHR_E_INVALID for an unknown mode. */
+int pvs_build_quant(const float* corpus, int64_t n, int32_t d, int32_t ptr_kind,
+                    void* stream, int32_t quant, pvs_index** out);
+
 /* pvs_insert -- append n_new rows (quantised on insert); their ids are
  * *first_id .. *first_id + n_new - 1.  They are visible in the live state and
  * in epochs taken afterwards, never in earlier epochs. */

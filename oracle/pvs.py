@@ -87,6 +87,42 @@ def quantize(v32: np.ndarray) -> Encoded:
     return Encoded(s, z, norm, enorm, hnorm)
 
 
+def quantize_global(v32: np.ndarray, scale=None) -> Encoded:
+    """Scalar quantisation with one scale shared by every row: the interval
+    generator Sec. 3.5 and Sec. 4.4 (Table 4-1) compare PVS with.
+
+    Reading: the shared scale is the per-vector rule applied to the whole
+    matrix, s = fl32(max_ij |v_ij| / 127) (1 if every entry is zero, the
+    smallest positive float32 if the quotient underflows); codes, norms and
+    intervals are then those of Sec. 2.3.1 with s_v = s for every row.  A
+    given ``scale`` (rows inserted after the scale was fixed) is used as is,
+    and codes that would exceed 127 in magnitude are clipped.
+    """
+    v = np.atleast_2d(np.asarray(v32, dtype=np.float32))
+    if not np.all(np.isfinite(v)):
+        raise ValueError("non-finite input")
+    if scale is None:
+        mu = F32(np.max(np.abs(v))) if v.size else F32(0)
+        sc = F32(mu / F32(127))
+        if mu > 0 and sc == 0:
+            sc = TINY32
+        if mu == 0:
+            sc = F32(1)
+    else:
+        sc = F32(scale)
+    n = v.shape[0]
+    s = np.full(n, sc, dtype=np.float32)
+    x = (v / sc).astype(np.float32)                      # correctly rounded f32 divide
+    z = np.clip(round_half_away(x), -127, 127).astype(np.int8)
+    v64 = v.astype(np.float64)
+    vh64 = np.float64(sc) * z.astype(np.float64)         # exact products
+    e64 = v64 - vh64
+    norm = up32(np.sqrt(np.sum(v64 * v64, axis=1)))
+    enorm = up32(np.sqrt(np.sum(e64 * e64, axis=1)))
+    hnorm = up32(np.sqrt(np.sum(vh64 * vh64, axis=1)))
+    return Encoded(s, z, norm, enorm, hnorm)
+
+
 def gamma(m: int) -> np.float32:
     """Smallest float32 >= a_m / (1 - a_m) with a_m = (8m + 64) eps (App. A.1)."""
     a = (8 * m + 64) * EPS32

@@ -145,11 +145,48 @@ static int index_grow(pvs_index* ix, int64_t need_rows) {
     return EAHR_OK;
 }
 
+// The shared scale of a global-scale index: fl32(max |x| / 127) over the n
+// rows given (its first non-empty build or insert), 1 if they are all zero,
+// the smallest positive float32 if the quotient underflows (the per-row rule
+// applied to the whole matrix).
+static int global_scale_of(pvs_index* ix, const float* src, int64_t n, bool dev, float* out) {
+    hipStream_t s = ix->stream;
+    HIP_TRY(hipMemsetAsync(ix->flags, 0, 4 * sizeof(uint32_t), s));
+    const int64_t chunk = 65536;
+    for (int64_t r = 0; r < n; r += chunk) {
+        const int64_t k = std::min(chunk, n - r);
+        const float* p = src + r * ix->d;
+        if (!dev) {
+            if (!ix->staging) EAHR_TRY(dev_alloc(&ix->staging, static_cast<size_t>(chunk) * ix->d));
+            HIP_TRY(hipMemcpyAsync(ix->staging, p, static_cast<size_t>(k) * ix->d * sizeof(float),
+                                   hipMemcpyHostToDevice, s));
+            p = ix->staging;
+        }
+        pvs::launch_maxabs(p, k * ix->d, ix->flags, s);
+        HIP_TRY(hipGetLastError());
+        if (!dev) HIP_TRY(hipStreamSynchronize(s));   // staging buffer is reused
+    }
+    uint32_t fl[4];
+    HIP_TRY(hipMemcpyAsync(fl, ix->flags, sizeof(fl), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    if (fl[0]) EAHR_FAIL(EAHR_E_NONFINITE, "non-finite value in corpus rows");
+    float mu;
+    std::memcpy(&mu, &fl[3], 4);
+    float sc = mu / 127.0f;
+    if (mu > 0.0f && sc == 0.0f) sc = std::numeric_limits<float>::denorm_min();
+    if (mu == 0.0f) sc = 1.0f;
+    *out = sc;
+    return EAHR_OK;
+}
+
 // Quantise n rows (host or device) into rows [row0, row0 + n) of the index.
 static int index_quantize(pvs_index* ix, const float* src, int64_t n, int32_t ptr_kind, int64_t row0) {
     hipStream_t s = ix->stream;
-    HIP_TRY(hipMemsetAsync(ix->flags, 0, 4 * sizeof(uint32_t), s));
     const bool dev = (ptr_kind == EAHR_PTR_DEVICE);
+    if (ix->quant == EAHR_QUANT_GLOBAL && ix->global_s == 0.0f && n > 0)
+        EAHR_TRY(global_scale_of(ix, src, n, dev, &ix->global_s));
+    const float fixed_s = (ix->quant == EAHR_QUANT_GLOBAL) ? ix->global_s : 0.0f;
+    HIP_TRY(hipMemsetAsync(ix->flags, 0, 4 * sizeof(uint32_t), s));
     const int64_t chunk = 65536;
     for (int64_t r = 0; r < n; r += chunk) {
         const int64_t k = std::min(chunk, n - r);
@@ -161,7 +198,7 @@ static int index_quantize(pvs_index* ix, const float* src, int64_t n, int32_t pt
             p = ix->staging;
         }
         pvs::launch_quantize(p, k, ix->d, ix->d, row0 + r, true, ix->codes, ix->dp, ix->scale,
-                             ix->vnorm, ix->enorm, nullptr, ix->frows, ix->df, ix->flags, s);
+                             ix->vnorm, ix->enorm, nullptr, ix->frows, ix->df, fixed_s, ix->flags, s);
         HIP_TRY(hipGetLastError());
         if (!dev) HIP_TRY(hipStreamSynchronize(s));   // staging buffer is reused
     }
@@ -200,8 +237,15 @@ static int take_snapshot(pvs_index* ix, int64_t* epoch) {
 
 extern "C" int pvs_build(const float* corpus, int64_t n, int32_t d, int32_t ptr_kind, void* stream,
                          pvs_index** out) {
+    return pvs_build_quant(corpus, n, d, ptr_kind, stream, EAHR_QUANT_PER_VECTOR, out);
+}
+
+extern "C" int pvs_build_quant(const float* corpus, int64_t n, int32_t d, int32_t ptr_kind,
+                               void* stream, int32_t quant, pvs_index** out) {
     if (!out) EAHR_FAIL(EAHR_E_INVALID, "pvs_build: out is NULL");
     *out = nullptr;
+    if (quant != EAHR_QUANT_PER_VECTOR && quant != EAHR_QUANT_GLOBAL)
+        EAHR_FAIL(EAHR_E_INVALID, "pvs_build: unknown quantisation mode %d", quant);
     if (n < 0 || d <= 0 || (n > 0 && !corpus)) EAHR_FAIL(EAHR_E_INVALID, "pvs_build: bad arguments");
     if (d > pvs::kMaxDim) EAHR_FAIL(EAHR_E_RANGE, "pvs_build: d=%d exceeds %d", d, pvs::kMaxDim);
     if (n >= (1LL << 31) - 64) EAHR_FAIL(EAHR_E_RANGE, "pvs_build: too many rows");
@@ -216,6 +260,7 @@ extern "C" int pvs_build(const float* corpus, int64_t n, int32_t d, int32_t ptr_
     ix->df = static_cast<int32_t>(round_up(d, 4));
     ix->nchunk = ix->dp / 16;
     ix->gamma = gamma_of(d);
+    ix->quant = quant;
     EAHR_TRY(dev_alloc(&ix->flags, 4));
     EAHR_TRY(index_grow(ix.get(), std::max<int64_t>(n, 64)));
     if (n > 0) {
@@ -524,7 +569,7 @@ extern "C" int pvs_open(const pvs_index* ix, int64_t epoch, const float* q, int3
         src = tmp;
     }
     pvs::launch_quantize(src, B, ix->d, ix->d, 0, false, st->qcodes, ix->dp, st->qscale, st->qnorm,
-                         st->qenorm, st->qhnorm, st->qrows, ix->df, st->qflags, s);
+                         st->qenorm, st->qhnorm, st->qrows, ix->df, 0.0f, st->qflags, s);
     HIP_TRY(hipGetLastError());
     std::vector<float> sc(B), nq(B), ne(B), nh(B);
     uint32_t fl[4];

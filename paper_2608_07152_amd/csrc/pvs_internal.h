@@ -108,6 +108,8 @@ struct pvs_index {
     float* staging = nullptr;  // host->device staging for quantisation
     float nv_max = 0.0f, nev_max = 0.0f;
     float gamma = 0.0f;
+    int32_t quant = EAHR_QUANT_PER_VECTOR;   // per-vector scales, or one shared scale
+    float global_s = 0.0f;                   // the shared scale once fixed (global mode)
     std::vector<Snapshot> snaps;
     mutable ScanBuffers spare;   // buffers of the last closed state
     mutable bool has_spare = false;

@@ -56,7 +56,9 @@ struct IndexView {
 void launch_quantize(const float* src, int64_t nrows, int32_t d, int64_t src_stride,
                      int64_t row0, bool tiled, int8_t* codes, int32_t dp, float* scale,
                      float* vnorm, float* enorm, float* hnorm, float* rows, int32_t df,
-                     uint32_t* flags, hipStream_t stream);
+                     float fixed_s, uint32_t* flags, hipStream_t stream);
+// Largest |x| of count floats into flags[3] (float bits), non-finite into flags[0].
+void launch_maxabs(const float* src, int64_t count, uint32_t* flags, hipStream_t stream);
 
 // Outputs of a scan pass.  Sample pass: lower and upper bounds of every
 // (query, row) pair of the sampled blocks, row-major [query][sample_ld],

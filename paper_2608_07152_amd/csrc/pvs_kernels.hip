@@ -13,7 +13,7 @@ __global__ __launch_bounds__(256) void k_quantize(
     const float* __restrict__ src, int64_t nrows, int32_t d, int64_t src_stride, int64_t row0,
     int tiled, int8_t* __restrict__ codes, int32_t dp, float* __restrict__ scale,
     float* __restrict__ vnorm, float* __restrict__ enorm, float* __restrict__ hnorm,
-    float* __restrict__ rows, int32_t df, uint32_t* __restrict__ flags) {
+    float* __restrict__ rows, int32_t df, float fixed_s, uint32_t* __restrict__ flags) {
     const int lane = threadIdx.x & 63;
     const int64_t r = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
     if (r >= nrows) return;
@@ -30,6 +30,7 @@ __global__ __launch_bounds__(256) void k_quantize(
     float s = mu / 127.0f;
     if (mu > 0.0f && s == 0.0f) s = __uint_as_float(1u);
     if (mu == 0.0f) s = 1.0f;
+    if (fixed_s > 0.0f) s = fixed_s;   // one scale for every row (global scalar quantisation)
     const int64_t R = row0 + r;
     const int nchunk = dp / 16;
     double n2 = 0.0, e2 = 0.0, h2 = 0.0;
@@ -78,13 +79,40 @@ __global__ __launch_bounds__(256) void k_quantize(
 
 void launch_quantize(const float* src, int64_t nrows, int32_t d, int64_t src_stride, int64_t row0,
                      bool tiled, int8_t* codes, int32_t dp, float* scale, float* vnorm,
-                     float* enorm, float* hnorm, float* rows, int32_t df, uint32_t* flags,
-                     hipStream_t stream) {
+                     float* enorm, float* hnorm, float* rows, int32_t df, float fixed_s,
+                     uint32_t* flags, hipStream_t stream) {
     if (nrows <= 0) return;
     const int64_t grid = (nrows + 3) / 4;
     hipLaunchKernelGGL(k_quantize, dim3(static_cast<uint32_t>(grid)), dim3(256), 0, stream, src,
                        nrows, d, src_stride, row0, tiled ? 1 : 0, codes, dp, scale, vnorm, enorm,
-                       hnorm, rows, df, flags);
+                       hnorm, rows, df, fixed_s, flags);
+}
+
+// Largest |x| over count floats (atomic max of the float's bits into flags[3],
+// valid for non-negative floats) and a non-finite flag in flags[0].
+__global__ __launch_bounds__(256) void k_maxabs(const float* __restrict__ src, int64_t count,
+                                                uint32_t* __restrict__ flags) {
+    float mu = 0.0f;
+    bool bad = false;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < count; i += stride) {
+        const float x = src[i];
+        bad |= !isfinite(x);
+        mu = fmaxf(mu, fabsf(x));
+    }
+    mu = wave_max(mu);
+    const bool any_bad = __any(bad);
+    if ((threadIdx.x & 63) == 0) {
+        if (any_bad) atomicOr(&flags[0], 1u);
+        atomicMax(&flags[3], __float_as_uint(mu));
+    }
+}
+
+void launch_maxabs(const float* src, int64_t count, uint32_t* flags, hipStream_t stream) {
+    if (count <= 0) return;
+    const int64_t blocks = std::min<int64_t>((count + 255) / 256, 4096);
+    hipLaunchKernelGGL(k_maxabs, dim3(static_cast<uint32_t>(blocks)), dim3(256), 0, stream, src,
+                       count, flags);
 }
 
 // ----------------------------------------------------------- debug paths

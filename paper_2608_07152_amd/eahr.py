@@ -97,6 +97,7 @@ _i64p, _i32p, _u8p, _i8p = C.POINTER(C.c_int64), C.POINTER(C.c_int32), C.POINTER
 # name -> (restype, argtypes); mirrors include/eahr.h
 SIGNATURES = {
     "pvs_build": (C.c_int, [_P, _i64, _i32, _i32, _P, C.POINTER(_P)]),
+    "pvs_build_quant": (C.c_int, [_P, _i64, _i32, _i32, _P, _i32, C.POINTER(_P)]),
     "pvs_insert": (C.c_int, [_P, _P, _i64, _i32, _i64p]),
     "pvs_delete": (C.c_int, [_P, _i64p, _i64]),
     "pvs_snapshot": (C.c_int, [_P, _i64p]),
@@ -262,6 +263,19 @@ def pvs_build(corpus, stream=None) -> PvsIndex:
     n, d = shape
     h = C.c_void_p()
     _check(load().pvs_build(p, n, d, kind, _stream_ptr(stream), C.byref(h)))
+    return PvsIndex(h, d)
+
+
+QUANT_MODES = {"per_vector": 0, "global": 1}
+
+
+def pvs_build_quant(corpus, quant: str = "per_vector", stream=None) -> PvsIndex:
+    """pvs_build with a choice of scale: "per_vector" (PVS) or "global" (one
+    scale shared by every row, the scalar-quantisation generator)."""
+    p, kind, keep, shape = _array_arg(corpus)
+    n, d = shape
+    h = C.c_void_p()
+    _check(load().pvs_build_quant(p, n, d, kind, _stream_ptr(stream), QUANT_MODES[quant], C.byref(h)))
     return PvsIndex(h, d)
 
 

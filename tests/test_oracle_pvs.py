@@ -234,3 +234,75 @@ def test_interval_widens_with_guard():
     width = iv.hi.astype(np.float64) - iv.lo.astype(np.float64)
     assert np.all(width >= 2 * (iv.E.astype(np.float64) + iv.G.astype(np.float64)))
     assert np.all(iv.G > 0)
+
+
+# ---------------------------------------------------------------------------
+# Global-scale scalar quantisation (the alternative generator of Sec. 4.4)
+
+def test_global_scale_reduces_to_per_vector_when_row_maxima_agree():
+    # every row has the same largest magnitude, so the shared scale is each
+    # row's own scale and the two encoders must agree exactly
+    rng = np.random.default_rng(11)
+    x = rng.uniform(-0.9, 0.9, (50, 64)).astype(np.float32)
+    x[np.arange(50), rng.integers(0, 64, 50)] = np.where(rng.random(50) < 0.5, F32(-1.25), F32(1.25))
+    g, p = pvs.quantize_global(x), pvs.quantize(x)
+    for f in ("s", "z", "norm", "enorm", "hnorm"):
+        assert np.array_equal(getattr(g, f), getattr(p, f)), f
+
+
+def test_global_scale_is_the_largest_row_scale():
+    # f32 division by 127 is monotone, so fl32(max|v| / 127) equals the
+    # largest per-row scale of the nonzero rows
+    w = datagen.workload("tiny", n=300)
+    x, _ = datagen.corpus(w)
+    assert pvs.quantize_global(x).s[0] == pvs.quantize(x).s.max()
+
+
+def test_global_scale_dyadic_closed_form():
+    # max |entry| = 127 * 2^-6 and every entry a multiple of 2^-6: the scale
+    # is 2^-6, the codes are the multipliers and the residual is zero
+    rng = np.random.default_rng(3)
+    k = rng.integers(-127, 128, (20, 32))
+    k[4, 7] = 127
+    x = (k * 2.0 ** -6).astype(np.float32)
+    e = pvs.quantize_global(x)
+    assert np.all(e.s == F32(2.0 ** -6))
+    assert np.array_equal(e.z.astype(np.int64), k)
+    assert np.all(e.enorm == 0)
+
+
+def test_global_codes_are_nearest_integers_and_residual_bounded():
+    rng = np.random.default_rng(8)
+    x = rng.standard_normal((40, 48)).astype(np.float32)
+    e = pvs.quantize_global(x)
+    s = e.s[0]
+    for i in range(0, 40, 3):
+        for j in range(0, 48, 5):
+            assert int(e.z[i, j]) == _nearest_int_brute(F32(x[i, j] / s))
+    resid = np.abs(x.astype(np.float64) - np.float64(s) * e.z.astype(np.float64))
+    # |v - s z| <= s/2 up to the rounding of the f32 quotient
+    assert np.all(resid <= np.float64(s) * (0.5 + 2.0 ** -20))
+
+
+def test_global_zero_matrix_and_clipping_with_a_fixed_scale():
+    e = pvs.quantize_global(np.zeros((3, 8), dtype=np.float32))
+    assert np.all(e.s == F32(1)) and not np.any(e.z)
+    # rows inserted after the scale was fixed: codes clip at +-127 and the
+    # residual norm accounts for what was clipped
+    x = np.array([[1.0, -3.0, 0.5]], dtype=np.float32)
+    e = pvs.quantize_global(x, scale=F32(1.0 / 127))
+    assert list(e.z[0]) == [127, -127, 64]
+    r = x.astype(np.float64)[0] - np.float64(F32(1.0 / 127)) * e.z[0].astype(np.float64)
+    assert e.enorm[0] >= np.sqrt(np.sum(r * r))
+
+
+@pytest.mark.parametrize("clip", [False, True])
+def test_global_intervals_contain_exact_scores(clip):
+    w = datagen.workload("tiny", n=400)
+    x, _ = datagen.corpus(w)
+    q, _ = datagen.queries(w, count=5)
+    ve = pvs.quantize_global(x, scale=(pvs.quantize_global(x).s[0] * F32(0.5)) if clip else None)
+    iv = pvs.intervals(pvs.quantize(q), ve, w.d)
+    s64 = q.astype(np.float64) @ x.astype(np.float64).T
+    assert np.all(iv.lo <= s64) and np.all(s64 <= iv.hi)
+    assert np.all(np.abs(s64 - iv.c.astype(np.float64)) <= iv.E.astype(np.float64) * (1 + 1e-6))
