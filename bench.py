@@ -173,24 +173,28 @@ def query_set_for(w, batch):
 
 def generator_ablation(eahr, torch, x, idx, pbm, qdev, sparse_q, w, K, wts, nq, batch):
     """Rank-generator ablation (Sec. 4.4, Table 4-1): the same eahr_topk with
-    the dense generator replaced by global-scale scalar-quantisation intervals.
-    Single requests are timed in pairs (order alternating, 1 warm-up + 3 runs
+    the dense generator replaced by global-scale scalar-quantisation intervals
+    ("scalar") or by one exhaustive float32 scan ("scan").  Single requests
+    are timed in paired rounds (generator order rotating, 1 warm-up + 3 runs
     each, median per query) and compared by the geometric mean of the
-    per-query latency ratios; the batch is timed for 1 warm-up + 2 steps each.
-    f32 evaluations are the rescored (query, row) pairs of each call."""
+    per-query latency ratios; the batch is timed for 1 warm-up + 2 steps with
+    PVS and scalar intervals (an exhaustive scan of a whole batch would keep
+    8 bytes per row and query on the host).  f32 evaluations are the (query,
+    row) pairs scored in float32 by each call."""
     import numpy as np
     log("ablation: building the global-scale index")
     t = time.perf_counter()
     gidx = eahr.pvs_build_quant(x, "global")
     torch.cuda.synchronize()
     log(f"ablation: global-scale index built in {time.perf_counter() - t:.1f}s")
-    gens = {"pvs": idx, "scalar": gidx}
+    gens = {"pvs": (idx, "intervals"), "scalar": (gidx, "intervals"), "scan": (idx, "full_scan")}
 
-    def call(ix, a, b):
+    def call(g, a, b):
+        ix, gen = gens[g]
         eahr.pvs_profile_enable(True)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        r = eahr.eahr_topk(ix, pbm, a, b, K=K, w_dense=wts[0], w_sparse=wts[1])
+        r = eahr.eahr_topk(ix, pbm, a, b, K=K, w_dense=wts[0], w_sparse=wts[1], dense_generator=gen)
         torch.cuda.synchronize()
         el = time.perf_counter() - t0
         pairs = eahr.pvs_profile_read()["rescore_rows"]
@@ -200,55 +204,67 @@ def generator_ablation(eahr, torch, x, idx, pbm, qdev, sparse_q, w, K, wts, nq, 
     name1 = query_set_for(w, 1)
     qd, qs = qdev[name1], sparse_q[name1]
     nq = min(nq, qd.shape[0])
+    names = list(gens)
     lat = {g: [] for g in gens}
     evals = {g: [] for g in gens}
-    same = 0
+    same = {g: 0 for g in gens}
     for i in range(nq):
         a, b = qd[i:i + 1], qs[i:i + 1]
-        order = list(gens) if i % 2 == 0 else list(gens)[::-1]
+        order = names[i % len(names):] + names[:i % len(names)]
         times = {g: [] for g in gens}
         ids = {}
         for rep in range(4):
             for g in order:
-                el, pairs, r = call(gens[g], a, b)
+                el, pairs, r = call(g, a, b)
                 if rep:
                     times[g].append(el)
                 else:
                     evals[g].append(pairs)
                     ids[g] = r[0][0, :r[1][0]].tolist()
-        same += ids["pvs"] == ids["scalar"]
         for g in gens:
+            same[g] += ids[g] == ids["pvs"]
             lat[g].append(float(np.median(times[g])))
-    ratio = float(np.exp(np.mean(np.log(np.array(lat["scalar"]) / np.array(lat["pvs"])))))
+
+    def gmean_ratio(g):
+        return float(np.exp(np.mean(np.log(np.array(lat[g]) / np.array(lat["pvs"])))))
+
+    def reduction(g):
+        return 1.0 - float(np.median(evals["pvs"])) / max(1.0, float(np.median(evals[g])))
+
     single = {
-        "queries": nq, "scalar_over_pvs_latency_gmean": ratio,
+        "queries": nq,
+        "scalar_over_pvs_latency_gmean": gmean_ratio("scalar"),
+        "scan_over_pvs_latency_gmean": gmean_ratio("scan"),
         "median_ms": {g: float(np.median(lat[g]) * 1e3) for g in gens},
         "f32_evals_median": {g: float(np.median(evals[g])) for g in gens},
-        "f32_evals_reduction": 1.0 - float(np.median(evals["pvs"])) / max(1.0, float(np.median(evals["scalar"]))),
-        "topk_identical": same,
+        "pvs_f32_evals_reduction_vs": {"scalar": reduction("scalar"), "scan": reduction("scan")},
+        "topk_identical_to_pvs": {g: same[g] for g in ("scalar", "scan")},
     }
-    log(f"ablation: single requests scalar/pvs = {ratio:.3f}, f32 evals "
-        f"{single['f32_evals_median']['pvs']:.0f} vs {single['f32_evals_median']['scalar']:.0f}")
+    log(f"ablation: single requests scalar/pvs = {single['scalar_over_pvs_latency_gmean']:.3f}, "
+        f"scan/pvs = {single['scan_over_pvs_latency_gmean']:.3f}, f32 evals "
+        + ", ".join(f"{g} {single['f32_evals_median'][g]:.0f}" for g in gens))
     nameb = query_set_for(w, batch)
     a, b = qdev[nameb][:batch], sparse_q[nameb][:batch]
     bt = {}
-    for g in gens:
-        call(gens[g], a, b)
-        runs = [call(gens[g], a, b) for _ in range(2)]
+    for g in ("pvs", "scalar"):
+        call(g, a, b)
+        runs = [call(g, a, b) for _ in range(2)]
         bt[g] = {"ms_per_step": float(np.mean([r[0] for r in runs]) * 1e3),
                  "f32_evals_per_step": float(np.mean([r[1] for r in runs])),
                  "ids": runs[0][2][0]}
     batched = {
         "batch": batch,
         "scalar_over_pvs_latency": bt["scalar"]["ms_per_step"] / bt["pvs"]["ms_per_step"],
-        "ms_per_step": {g: bt[g]["ms_per_step"] for g in gens},
-        "f32_evals_per_step": {g: bt[g]["f32_evals_per_step"] for g in gens},
+        "ms_per_step": {g: bt[g]["ms_per_step"] for g in bt},
+        "f32_evals_per_step": {g: bt[g]["f32_evals_per_step"] for g in bt},
         "topk_identical": bool(np.array_equal(bt["pvs"]["ids"], bt["scalar"]["ids"])),
     }
     log(f"ablation: batch {batch} scalar/pvs = {batched['scalar_over_pvs_latency']:.3f}")
     eahr.pvs_free(gidx)
     torch.cuda.synchronize()
-    return {"alternative": "scalar-quantisation intervals (one global scale)", "reference": "pvs",
+    return {"reference": "pvs",
+            "alternatives": {"scalar": "scalar-quantisation intervals (one global scale)",
+                             "scan": "exhaustive float32 scan, one sort per query"},
             "single_requests": single, "batch": batched}
 
 

@@ -105,6 +105,23 @@ int pvs_info(const pvs_index* idx, int64_t epoch, int64_t* rows, int32_t* d,
 int pvs_open(const pvs_index* idx, int64_t epoch, const float* q, int32_t B,
              int32_t ptr_kind, pvs_state** out);
 
+/* Dense rank generators of pvs_open_gen. */
+enum { EAHR_GEN_INTERVALS = 0, EAHR_GEN_FULL_SCAN = 1 };
+
+/* pvs_open_gen -- pvs_open with a choice of dense rank generator:
+ * EAHR_GEN_INTERVALS is pvs_open (interval scans over the index's codes,
+ * Sec. 2.3.1); EAHR_GEN_FULL_SCAN scores every visible row in float32 on the
+ * first pvs_next that needs ranks, sorts them once and serves every later
+ * rank from that complete ranking: the exhaustive float32 scan that Sec. 3.5
+ * and Sec. 4.4 (Table 4-1) compare PVS with.  Scores are the same
+ * authoritative float32 dot products, so both generators emit identical
+ * ranks.  The full scan needs 16 bytes of device memory per row of the epoch
+ * and query of a group (groups are sized to 4 GiB) and keeps 8 bytes per
+ * visible row and query on the host.  Errors: those of pvs_open, and
+ * EAHR_E_INVALID for an unknown generator. */
+int pvs_open_gen(const pvs_index* idx, int64_t epoch, const float* q, int32_t B,
+                 int32_t ptr_kind, int32_t generator, pvs_state** out);
+
 /* pvs_next -- extend each active query's exact dense prefix by up to m ranks
  * (Sec. 2.3.1 resumable generation).  The complete list orders the visible
  * rows by (authoritative float32 inner product descending, id ascending);
@@ -230,6 +247,7 @@ typedef struct {
     int32_t k_rrf;       /* rank constant k >= 1                                  */
     int32_t w_dense;     /* rank-scaled weights w_i >= 0 (Sec. 2.1), integers     */
     int32_t w_sparse;
+    int32_t dense_generator;   /* EAHR_GEN_* of the dense channel (0: intervals)  */
 } eahr_params;
 
 typedef struct {

@@ -30,7 +30,8 @@ using ::eahr::Params;
 
 int check_params(const eahr_params& ep) {
     if (ep.K < 0 || ep.depth0 < 1 || ep.growth < 2 || ep.k_rrf < 1 || ep.k_rrf > (1 << 20) ||
-        ep.w_dense < 0 || ep.w_dense > 1024 || ep.w_sparse < 0 || ep.w_sparse > 1024)
+        ep.w_dense < 0 || ep.w_dense > 1024 || ep.w_sparse < 0 || ep.w_sparse > 1024 ||
+        (ep.dense_generator != EAHR_GEN_INTERVALS && ep.dense_generator != EAHR_GEN_FULL_SCAN))
         EAHR_FAIL(EAHR_E_INVALID, "eahr: parameters out of range");
     return EAHR_OK;
 }
@@ -140,7 +141,8 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
         }
     } cl;
     const auto t_open = std::chrono::steady_clock::now();
-    if (use_dense) EAHR_TRY(pvs_open(dense, epoch, q_dense, B, q_ptr_kind, &cl.st));
+    if (use_dense)
+        EAHR_TRY(pvs_open_gen(dense, epoch, q_dense, B, q_ptr_kind, ep.dense_generator, &cl.st));
     const double open_dense_ms = ms_since(t_open);
     // sparse states are opened by the sparse workers, at a query's first
     // call; the queries are checked here

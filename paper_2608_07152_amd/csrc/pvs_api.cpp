@@ -527,8 +527,15 @@ static int ensure_host_packed(pvs_state* st, int64_t n) {
 
 extern "C" int pvs_open(const pvs_index* ix, int64_t epoch, const float* q, int32_t B,
                         int32_t ptr_kind, pvs_state** out) {
+    return pvs_open_gen(ix, epoch, q, B, ptr_kind, EAHR_GEN_INTERVALS, out);
+}
+
+extern "C" int pvs_open_gen(const pvs_index* ix, int64_t epoch, const float* q, int32_t B,
+                            int32_t ptr_kind, int32_t generator, pvs_state** out) {
     if (!out) EAHR_FAIL(EAHR_E_INVALID, "pvs_open: out is NULL");
     *out = nullptr;
+    if (generator != EAHR_GEN_INTERVALS && generator != EAHR_GEN_FULL_SCAN)
+        EAHR_FAIL(EAHR_E_INVALID, "pvs_open: unknown generator %d", generator);
     if (!ix || B <= 0 || !q) EAHR_FAIL(EAHR_E_INVALID, "pvs_open: bad arguments");
     if (epoch < 0 || epoch >= static_cast<int64_t>(ix->snaps.size()))
         EAHR_FAIL(EAHR_E_INVALID, "pvs_open: unknown epoch %lld", static_cast<long long>(epoch));
@@ -539,6 +546,7 @@ extern "C" int pvs_open(const pvs_index* ix, int64_t epoch, const float* q, int3
     st->ix = ix;
     st->epoch = epoch;
     st->B = B;
+    st->generator = generator;
     if (const char* p = std::getenv("EAHR_SCAN_PATH")) {
         if (std::strcmp(p, "gemv") == 0) st->path = pvs::ScanPath::Gemv;
         else if (std::strcmp(p, "mfma") == 0) st->path = pvs::ScanPath::Mfma;
@@ -742,6 +750,96 @@ static int64_t lower_overlap(const pvs_state* st, int32_t b) {
     return a;
 }
 
+// Exhaustive float32 generator: every visible row of the epoch is scored in
+// float32 (the same authoritative order as rescoring), each query's keys are
+// sorted once and the whole ranking becomes its certified cache, so the
+// query is finished after one round.  Queries go in groups whose keys and
+// sort buffer fit in 4 GiB.
+static int full_scan_round(pvs_state* st, std::vector<int32_t>& todo) {
+    const pvs_index* ix = st->ix;
+    hipStream_t s = ix->stream;
+    const int64_t n = st->n_rows;
+    const bool prof = g_prof_on.load(std::memory_order_relaxed) != 0;
+    if (prof && !st->ev[0])
+        for (auto& e : st->ev) HIP_TRY(hipEventCreate(&e));
+    const int64_t per = std::min<int64_t>(65535, std::max<int64_t>(1, (int64_t(4) << 30) / std::max<int64_t>(1, 16 * n)));
+    const pvs::IndexView v = view_of(ix);
+    for (size_t g0 = 0; g0 < todo.size() && n > 0; g0 += static_cast<size_t>(per)) {
+        const int32_t ng = static_cast<int32_t>(std::min<int64_t>(per, static_cast<int64_t>(todo.size() - g0)));
+        uint64_t *keys = nullptr, *tmp = nullptr;
+        int32_t *d_qidx = nullptr, *d_cnt = nullptr;
+        ScanQ* d_sq = nullptr;
+        std::vector<int32_t> qidx(ng), cnt(ng, static_cast<int32_t>(n));
+        std::vector<ScanQ> sq(ng);
+        for (int32_t i = 0; i < ng; ++i) {
+            qidx[i] = todo[g0 + i];
+            sq[i] = ScanQ{};
+            sq[i].qi = qidx[i];
+            sq[i].cand_off = static_cast<int64_t>(i) * n;
+        }
+        int rc = EAHR_OK;
+        auto body = [&]() -> int {
+            EAHR_TRY(dev_alloc(&keys, static_cast<size_t>(ng) * n));
+            EAHR_TRY(dev_alloc(&tmp, static_cast<size_t>(ng) * n));
+            EAHR_TRY(dev_alloc(&d_qidx, ng));
+            EAHR_TRY(dev_alloc(&d_cnt, ng));
+            EAHR_TRY(dev_alloc(&d_sq, ng));
+            HIP_TRY(hipMemcpyAsync(d_qidx, qidx.data(), ng * sizeof(int32_t), hipMemcpyHostToDevice, s));
+            HIP_TRY(hipMemcpyAsync(d_cnt, cnt.data(), ng * sizeof(int32_t), hipMemcpyHostToDevice, s));
+            HIP_TRY(hipMemcpyAsync(d_sq, sq.data(), ng * sizeof(ScanQ), hipMemcpyHostToDevice, s));
+            if (prof) HIP_TRY(hipEventRecord(st->ev[0], s));
+            pvs::launch_full_keys(v, st->vis, n, st->qrows, d_qidx, ng, keys, n, s);
+            HIP_TRY(hipGetLastError());
+            if (prof) HIP_TRY(hipEventRecord(st->ev[1], s));
+            const uint64_t* sorted = pvs::launch_segmented_sort(keys, tmp, d_cnt, d_sq, ng, n, s);
+            HIP_TRY(hipGetLastError());
+            if (prof) HIP_TRY(hipEventRecord(st->ev[2], s));
+            for (int32_t i = 0; i < ng; ++i) {
+                auto& Q = st->q[qidx[i]];
+                Q.cache.resize(static_cast<size_t>(st->n_vis));
+                if (st->n_vis > 0)
+                    HIP_TRY(hipMemcpyAsync(Q.cache.data(), sorted + static_cast<int64_t>(i) * n,
+                                           st->n_vis * sizeof(uint64_t), hipMemcpyDeviceToHost, s));
+            }
+            HIP_TRY(hipStreamSynchronize(s));
+            return EAHR_OK;
+        };
+        rc = body();
+        dev_free(keys);
+        dev_free(tmp);
+        dev_free(d_qidx);
+        dev_free(d_cnt);
+        dev_free(d_sq);
+        if (rc != EAHR_OK) return rc;
+        if (prof) {
+            float t0 = 0.0f, t1 = 0.0f;
+            HIP_TRY(hipEventElapsedTime(&t0, st->ev[0], st->ev[1]));
+            HIP_TRY(hipEventElapsedTime(&t1, st->ev[1], st->ev[2]));
+            std::lock_guard<std::mutex> lk(g_prof_mu);
+            g_prof.rescore_ms += t0;
+            g_prof.rescore_rows += static_cast<int64_t>(ng) * st->n_vis;
+            g_prof.rescore_row_reads += static_cast<int64_t>(ng) * st->n_vis;
+            g_prof.rescore_certified += static_cast<int64_t>(ng) * st->n_vis;
+            g_prof.sort_ms += t1;
+            g_prof.scan_rounds += 1;
+        }
+        for (int32_t i = 0; i < ng; ++i) {
+            auto& Q = st->q[qidx[i]];
+            st->stats.scans += 1;
+            st->stats.candidates += st->n_vis;
+            st->stats.certified += st->n_vis;
+            if (st->n_vis > 0) {
+                Q.has_cert = true;
+                Q.s_cert = key_score(Q.cache.back());
+                Q.id_cert = key_id(Q.cache.back());
+            }
+        }
+    }
+    for (int32_t b : todo) st->q[b].cert_exhausted = true;
+    todo.clear();
+    return EAHR_OK;
+}
+
 // One scan round over the queries in `todo`; removes the queries it finished.
 //  1. sample pass + select: tau and the sampled hit count of every query;
 //  2. candidate regions sized from the hits (host), main scan;
@@ -750,6 +848,7 @@ static int64_t lower_overlap(const pvs_state* st, int32_t b) {
 // their candidates; queries that certified too few ranks again with a lower
 // threshold.
 static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
+    if (st->generator == EAHR_GEN_FULL_SCAN) return full_scan_round(st, todo);
     const pvs_index* ix = st->ix;
     hipStream_t s = ix->stream;
     int32_t nq = static_cast<int32_t>(todo.size());

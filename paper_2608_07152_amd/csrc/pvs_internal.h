@@ -134,6 +134,7 @@ struct pvs_state {
     const pvs_index* ix = nullptr;
     int64_t epoch = 0;
     int32_t B = 0;
+    int32_t generator = EAHR_GEN_INTERVALS;   // interval scans, or one exhaustive float32 scan
     int64_t n_rows = 0, n_vis = 0;
     const uint64_t* vis = nullptr;
     int8_t* qcodes = nullptr;   // B x dp row-major

@@ -118,6 +118,12 @@ void launch_rescore(const IndexView& ix, const float* qrows, const ScanQ* sq,
 
 // Sorts every query's candidate keys (cnt[b] keys from cand_off) ascending;
 // returns the buffer holding the result (keys or tmp).
+// Exhaustive float32 keys of every row of [0, n_rows) for ng queries (state
+// query indices qidx, device), query g's keys at keys + g * ld; invisible rows
+// get ~0.
+void launch_full_keys(const IndexView& ix, const uint64_t* vis, int64_t n_rows, const float* qrows,
+                      const int32_t* qidx, int32_t ng, uint64_t* keys, int64_t ld,
+                      hipStream_t stream);
 uint64_t* launch_segmented_sort(uint64_t* keys, uint64_t* tmp, const int32_t* cnt,
                                 const ScanQ* sq, int32_t nq, int64_t max_cnt, hipStream_t stream);
 

@@ -1,5 +1,6 @@
-// Quantisation, visibility and debug kernels of the PVS dense channel
-// (Sec. 2.3.1).  The numerical contract is stated in pvs_device.h.
+// Quantisation, visibility, exhaustive float32 scoring and debug kernels of
+// the PVS dense channel (Sec. 2.3.1).  The numerical contract is stated in
+// pvs_device.h.
 #include "pvs_device.h"
 
 namespace pvs {
@@ -113,6 +114,59 @@ void launch_maxabs(const float* src, int64_t count, uint32_t* flags, hipStream_t
     const int64_t blocks = std::min<int64_t>((count + 255) / 256, 4096);
     hipLaunchKernelGGL(k_maxabs, dim3(static_cast<uint32_t>(blocks)), dim3(256), 0, stream, src,
                        count, flags);
+}
+
+// ------------------------------------------------------- exhaustive scoring
+// The exhaustive float32 generator (the "full float32 scan" alternative of
+// Sec. 4.4, Table 4-1): every row of the epoch gets its authoritative score in
+// row_score's fixed order, so each key equals the one rescoring would write;
+// rows not visible get the key ~0, which sorts after every real key.  One
+// wavefront per row (three 1 KiB coalesced loads per 768-float row), the
+// query row in registers; blockIdx.y selects the query of the group.
+template <int J>
+__global__ __launch_bounds__(256) void k_full_keys(const float* __restrict__ rows, int32_t df,
+                                                   const uint64_t* __restrict__ vis, int64_t n_rows,
+                                                   const float* __restrict__ qrows,
+                                                   const int32_t* __restrict__ qidx,
+                                                   uint64_t* __restrict__ keys, int64_t ld) {
+    const int lane = threadIdx.x & 63;
+    const int df4 = df / 4;
+    float4 qv[J];
+    load_query_row<J>(reinterpret_cast<const float4*>(qrows), qidx[blockIdx.y], df4, lane, qv);
+    uint64_t* out = keys + static_cast<int64_t>(blockIdx.y) * ld;
+    const int64_t nw = static_cast<int64_t>(gridDim.x) * 4;
+    for (int64_t r = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6); r < n_rows; r += nw) {
+        if (!((vis[r >> 6] >> (r & 63)) & 1ull)) {   // uniform across the wavefront
+            if (lane == 0) out[r] = ~0ull;
+            continue;
+        }
+        const float sc = row_score<J>(reinterpret_cast<const float4*>(rows + r * df), qv, lane, df4);
+        if (lane == 0) out[r] = (static_cast<uint64_t>(~mono32(sc)) << 32) | static_cast<uint32_t>(r);
+    }
+}
+
+void launch_full_keys(const IndexView& ix, const uint64_t* vis, int64_t n_rows, const float* qrows,
+                      const int32_t* qidx, int32_t ng, uint64_t* keys, int64_t ld,
+                      hipStream_t stream) {
+    if (n_rows <= 0 || ng <= 0) return;
+    const int64_t blocks = std::min<int64_t>((n_rows + 3) / 4, 8192);
+    const dim3 grid(static_cast<uint32_t>(blocks), static_cast<uint32_t>(ng));
+#define PVS_FK(J)                                                                                \
+    case J:                                                                                      \
+        hipLaunchKernelGGL(k_full_keys<J>, grid, dim3(256), 0, stream, ix.rows, ix.df, vis,     \
+                           n_rows, qrows, qidx, keys, ld);                                       \
+        break;
+    switch (row_chunks(ix.df)) {
+        PVS_FK(1)
+        PVS_FK(2)
+        PVS_FK(3)
+        PVS_FK(4)
+        PVS_FK(8)
+        PVS_FK(16)
+        default:
+            break;
+    }
+#undef PVS_FK
 }
 
 // ----------------------------------------------------------- debug paths

@@ -47,7 +47,8 @@ class eahr_sparse_query(C.Structure):
 
 class eahr_params(C.Structure):
     _fields_ = [("K", C.c_int32), ("depth0", C.c_int32), ("growth", C.c_int32),
-                ("k_rrf", C.c_int32), ("w_dense", C.c_int32), ("w_sparse", C.c_int32)]
+                ("k_rrf", C.c_int32), ("w_dense", C.c_int32), ("w_sparse", C.c_int32),
+                ("dense_generator", C.c_int32)]
 
 
 class eahr_query_stats(C.Structure):
@@ -103,6 +104,7 @@ SIGNATURES = {
     "pvs_snapshot": (C.c_int, [_P, _i64p]),
     "pvs_info": (C.c_int, [_P, _i64, _i64p, _i32p, _i64p]),
     "pvs_open": (C.c_int, [_P, _i64, _P, _i32, _i32, C.POINTER(_P)]),
+    "pvs_open_gen": (C.c_int, [_P, _i64, _P, _i32, _i32, _i32, C.POINTER(_P)]),
     "pvs_next": (C.c_int, [_P, _i32, _u8p, _i64p, _f32p, _i32p, _i32p]),
     "pvs_stats": (C.c_int, [_P, C.POINTER(pvs_counters)]),
     "pvs_profile_enable": (C.c_int, [_i32]),
@@ -303,12 +305,20 @@ def pvs_info(index: PvsIndex, epoch: int = 0) -> Tuple[int, int, int]:
     return rows.value, d.value, vis.value
 
 
-def pvs_open(index: PvsIndex, queries, epoch: int = 0) -> PvsState:
+GENERATORS = {"intervals": 0, "full_scan": 1}
+
+
+def pvs_open(index: PvsIndex, queries, epoch: int = 0, generator: str = "intervals") -> PvsState:
+    """Encode a query batch and open resumable dense state; ``generator`` is
+    "intervals" (interval scans) or "full_scan" (one exhaustive float32 scan)."""
     p, kind, keep, shape = _array_arg(queries)
     if len(shape) == 1:
         shape = (1, shape[0])
     h = C.c_void_p()
-    _check(load().pvs_open(index.h, epoch, p, shape[0], kind, C.byref(h)))
+    if generator == "intervals":
+        _check(load().pvs_open(index.h, epoch, p, shape[0], kind, C.byref(h)))
+    else:
+        _check(load().pvs_open_gen(index.h, epoch, p, shape[0], kind, GENERATORS[generator], C.byref(h)))
     return PvsState(h, index, shape[0])
 
 
@@ -430,18 +440,20 @@ def pbm_debug_set_blockmax(index: PbmIndex, term: int, range_: int, value: float
 
 
 # ------------------------------------------------------------------ fusion
-def _params(K, k_rrf, w_dense, w_sparse, depth0, growth):
+def _params(K, k_rrf, w_dense, w_sparse, depth0, growth, generator="intervals"):
     for v in (k_rrf, w_dense, w_sparse):
         if int(v) != v:
             raise ValueError("k and the weights must be integers")
-    return eahr_params(int(K), int(depth0), int(growth), int(k_rrf), int(w_dense), int(w_sparse))
+    return eahr_params(int(K), int(depth0), int(growth), int(k_rrf), int(w_dense), int(w_sparse),
+                       GENERATORS[generator])
 
 
 def eahr_topk(dense: Optional[PvsIndex], sparse: Optional[PbmIndex], q_dense,
               q_sparse: Sequence[Tuple[np.ndarray, np.ndarray]], K: int = 20, k_rrf: int = 60,
               w_dense: int = 1, w_sparse: int = 1, epoch: int = 0, depth0: int = 20,
-              growth: int = 2, allow_failed: bool = False):
-    """Ordered Top-K of complete-list weighted RRF for a batch of queries.
+              growth: int = 2, allow_failed: bool = False, dense_generator: str = "intervals"):
+    """Ordered Top-K of complete-list weighted RRF for a batch of queries
+    (``dense_generator``: "intervals" or "full_scan", see pvs_open).
 
     Returns (ids [B,K] int64 with -1 padding, count [B], status [B], stats list)."""
     B = len(q_sparse) if q_sparse is not None else int(np.shape(q_dense)[0])
@@ -457,7 +469,7 @@ def eahr_topk(dense: Optional[PvsIndex], sparse: Optional[PbmIndex], q_dense,
             q, k = _sparse_query(t, w)
             qs[b] = q
             keep.append(k)
-    prm = _params(K, k_rrf, w_dense, w_sparse, depth0, growth)
+    prm = _params(K, k_rrf, w_dense, w_sparse, depth0, growth, dense_generator)
     ids = np.full((B, max(K, 1)), -1, dtype=np.int64)
     cnt = np.zeros(B, dtype=np.int32)
     stt = np.zeros(B, dtype=np.int32)

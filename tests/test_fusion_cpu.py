@@ -222,3 +222,18 @@ def test_sparse_only_topk_through_eahr_topk():
         want = list(osparse.sparse_ranking(S)[:20])
         assert list(ids[b, :cnt[b]]) == want
         assert stt[b] == 0
+
+
+def test_unknown_dense_generator_rejected():
+    import ctypes as C
+    from paper_2608_07152_amd import eahr
+    lib = eahr.load()
+    prm = eahr._params(20, 60, 1, 1, 20, 2)
+    prm.dense_generator = 9
+    a = np.arange(10, dtype=np.int64)
+    out = np.zeros(20, dtype=np.int64)
+    cnt = C.c_int32()
+    rc = lib.eahr_fuse_lists(a.ctypes.data_as(C.POINTER(C.c_int64)), 10,
+                             a.ctypes.data_as(C.POINTER(C.c_int64)), 10, C.byref(prm), 0,
+                             out.ctypes.data_as(C.POINTER(C.c_int64)), C.byref(cnt), None)
+    assert rc == eahr.EAHR_E_INVALID

@@ -165,3 +165,83 @@ def test_unknown_quantisation_mode_rejected(E):
     x = np.ones((4, 8), np.float32)
     rc = lib.pvs_build_quant(x.ctypes.data_as(C.c_void_p), 4, 8, 0, None, 7, C.byref(h))
     assert rc == E.EAHR_E_INVALID and not h.value
+
+
+# ---------------------------------------------------------------------------
+# Exhaustive float32 scan generator (the other alternative of Table 4-1)
+
+def test_full_scan_prefixes_equal_interval_generator(E, tiny, both):
+    w, x, q, _, _ = tiny
+    schedule = [20, 20, 40, 80, 160, 320, 640]
+    got_i, sc_i = _drain(E, E.pvs_open(both[0], q), schedule)
+    st = E.pvs_open(both[0], q, generator="full_scan")
+    got_f, sc_f = _drain(E, st, schedule)
+    for b in range(len(q)):
+        assert got_f[b] == got_i[b], b
+        assert sc_f[b] == sc_i[b], b
+        check_dense_prefix(q[b], x, got_f[b], sc_f[b])
+    c = E.pvs_stats(st)
+    assert c["candidates"] == w.n * len(q) and c["scans"] == len(q)
+
+
+def test_full_scan_to_exhaustion_with_deletes(E):
+    w = datagen.workload("tiny", n=3000, d=64)
+    x, _ = datagen.corpus(w)
+    q, _ = datagen.queries(w, count=3)
+    idx = E.pvs_build(x)
+    gone = np.arange(5, 3000, 7)
+    E.pvs_delete(idx, gone)
+    epoch = E.pvs_snapshot(idx)
+    vis = np.ones(3000, bool)
+    vis[gone] = False
+    st = E.pvs_open(idx, q, epoch=epoch, generator="full_scan")
+    ids, scs = _drain(E, st, [100, 1000, 5000])
+    ref, _ = _drain(E, E.pvs_open(idx, q, epoch=epoch), [100, 1000, 5000])
+    for b in range(3):
+        assert len(ids[b]) == int(vis.sum())
+        assert ids[b] == ref[b]
+        check_dense_prefix(q[b], x, ids[b], scs[b], visible=vis)
+    _, _, c, stt = E.pvs_next(st, 10)
+    assert np.all(c == 0) and np.all(stt == E.LIST_EXHAUSTED)
+
+
+def test_full_scan_eahr_topk_equals_intervals(E, tiny, both):
+    w, x, q, lab, qlab = tiny
+    post = datagen.bm25_impacts(w, datagen.sparse_docs(w, lab))
+    qs = datagen.sparse_queries(w, qlab)
+    pbm = E.pbm_build(post.term_ptr, post.doc, post.impact, w.n, 1024)
+    for wts in ((1, 1), (2, 1)):
+        a = E.eahr_topk(both[0], pbm, q, qs, K=20, w_dense=wts[0], w_sparse=wts[1])
+        f = E.eahr_topk(both[0], pbm, q, qs, K=20, w_dense=wts[0], w_sparse=wts[1],
+                        dense_generator="full_scan")
+        assert np.all(f[2] == 0)
+        assert np.array_equal(a[0], f[0]) and np.array_equal(a[1], f[1])
+
+
+def test_full_scan_anticorrelated_exhausts_both(E):
+    w = datagen.workload("adv", n=3000, d=64)
+    x, _ = datagen.corpus(w)
+    q, _ = datagen.queries(w, count=2)
+    post, qs = datagen.adversarial_postings(w, x, q)
+    idx = E.pvs_build(x)
+    pbm = E.pbm_build(post.term_ptr, post.doc, post.impact, w.n, 256)
+    a = E.eahr_topk(idx, pbm, q, qs, K=20)
+    f = E.eahr_topk(idx, pbm, q, qs, K=20, dense_generator="full_scan")
+    assert np.array_equal(a[0], f[0])
+    for b in range(2):
+        assert f[3][b]["dense_depth"] == w.n and f[3][b]["sparse_depth"] == w.n
+        S = osparse.sparse_scores(post.term_ptr, post.doc, post.impact, qs[b][0], qs[b][1], w.n)
+        di, ds, _, _ = E.pvs_next(E.pvs_open(idx, q[b:b + 1], generator="full_scan"), w.n)
+        check_dense_prefix(q[b], x, di[0], ds[0])
+        want = fused_reference(hybrid_dense_list(di[0], q[b], x), osparse.sparse_ranking(S), 20)
+        assert list(f[0][b, :f[1][b]]) == want
+
+
+def test_unknown_generator_rejected(E, tiny, both):
+    import ctypes as C
+    w, x, q, _, _ = tiny
+    lib = E.load()
+    h = C.c_void_p()
+    qq = np.ascontiguousarray(q[:1])
+    rc = lib.pvs_open_gen(both[0].h, 0, qq.ctypes.data_as(C.c_void_p), 1, 0, 9, C.byref(h))
+    assert rc == E.EAHR_E_INVALID and not h.value
