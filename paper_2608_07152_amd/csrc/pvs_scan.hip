@@ -624,7 +624,15 @@ static void mfma_pass(const IndexView& ix, const uint64_t* vis, int64_t nblocks,
         const int64_t groups = (nblocks + 3) / 4;
         const uint32_t g = static_cast<uint32_t>(std::min<int64_t>(groups, 2 * cu_count()));
         const int nsteps = ix.nchunk / 2;
-        if (nsteps % 2 == 0)
+        // four tiles: a four-step stage (243 registers, no spills) keeps twice
+        // the code fragments in flight per wavefront and halves the barriers;
+        // eight tiles would spill at that depth
+        constexpr int PA_DEEP = (W == 4) ? 4 : 2;
+        if (PA_DEEP == 4 && nsteps % 4 == 0)
+            hipLaunchKernelGGL((k_scan_mfma_wide<W, PA_DEEP>), dim3(g), dim3(256), 0, stream, ix.codes,
+                               ix.scale, ix.vnorm, ix.enorm, vis, nblocks, ix.nchunk, qfrag, sq, nq,
+                               gamma, o);
+        else if (nsteps % 2 == 0)
             hipLaunchKernelGGL((k_scan_mfma_wide<W, 2>), dim3(g), dim3(256), 0, stream, ix.codes,
                                ix.scale, ix.vnorm, ix.enorm, vis, nblocks, ix.nchunk, qfrag, sq, nq,
                                gamma, o);
