@@ -204,6 +204,45 @@ int pvs_scores(const pvs_state* st, int32_t b, const int64_t* rows, int64_t n,
 void pvs_close(pvs_state* st);
 void pvs_free(pvs_index* idx);
 
+/* ------------------------------------------- hierarchical merging (dense) */
+
+/* Hierarchical merging of exact dense rankings (Sec. 2.4).  A Segment is a
+ * pvs_index whose rows stand for global item ids; a Shard merges the
+ * rankings of its Segments, and a request merges its Shards, each by (score
+ * descending, global id ascending), into one resumable ranking with the
+ * pvs_next contract.  An item held by more than one Segment is emitted once
+ * when its copies agree on score and version; otherwise the query's merged
+ * list is Failed (sticky), as it is when a Segment's list fails. */
+typedef struct pvs_merge pvs_merge;
+
+/* pvs_merge_open -- open a Shard over n_segs Segments for B queries.
+ *   segs[s]      the Segment's index; epochs[s] its snapshot (NULL: all 0).
+ *   gids[s]      host array, one global id >= 0 per row of the snapshot,
+ *                strictly ascending (so the Segment's own id order is the
+ *                global one); copied.
+ *   versions[s]  host array of per-row versions, or NULL (all 0); versions
+ *                may be NULL.  Copied.
+ *   q            B x d float32 queries (host or device, ptr_kind).
+ * Errors: EAHR_E_INVALID for null arguments or ids that are negative or
+ * not ascending; those of pvs_open. */
+int pvs_merge_open(const pvs_index* const* segs, const int64_t* epochs,
+                   const int64_t* const* gids, const int64_t* const* versions,
+                   int32_t n_segs, const float* q, int32_t B, int32_t ptr_kind,
+                   pvs_merge** out);
+
+/* pvs_merge_shards -- the request-level merge over n_shards Shards opened by
+ * pvs_merge_open on the same B queries and not read yet.  The request takes
+ * ownership of the Shards: close only the returned handle. */
+int pvs_merge_shards(pvs_merge** shards, int32_t n_shards, pvs_merge** out);
+
+/* pvs_merge_next -- next m merged ranks per active query; ids are global
+ * ids.  Same count/status contract as pvs_next. */
+int pvs_merge_next(pvs_merge* mg, int32_t m, const uint8_t* active, int64_t* ids,
+                   float* scores, int32_t* count, int32_t* status);
+
+/* pvs_merge_close -- release a merge (and, for a request, its Shards). */
+void pvs_merge_close(pvs_merge* mg);
+
 /* ------------------------------------------------------------ PBM (sparse) */
 
 /* pbm_build -- Posting Block-Max index over term-major postings (Sec. 2.3.2).

@@ -19,7 +19,7 @@ OUT = os.path.join(HERE, "libeahr.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 
 HIP_SOURCES = ["pvs_kernels.hip", "pvs_scan.hip", "pvs_rank.hip"]
-HOST_SOURCES = ["pvs_api.cpp", "pbm.cpp", "eahr.cpp", "errors.cpp"]
+HOST_SOURCES = ["pvs_api.cpp", "pvs_merge.cpp", "pbm.cpp", "eahr.cpp", "errors.cpp"]
 
 ROCM_INCLUDE = os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "include")
 ARCH = os.environ.get("EAHR_OFFLOAD_ARCH", "gfx950")

@@ -105,6 +105,11 @@ SIGNATURES = {
     "pvs_info": (C.c_int, [_P, _i64, _i64p, _i32p, _i64p]),
     "pvs_open": (C.c_int, [_P, _i64, _P, _i32, _i32, C.POINTER(_P)]),
     "pvs_open_gen": (C.c_int, [_P, _i64, _P, _i32, _i32, _i32, C.POINTER(_P)]),
+    "pvs_merge_open": (C.c_int, [C.POINTER(_P), _i64p, C.POINTER(_i64p), C.POINTER(_i64p), _i32, _P,
+                                 _i32, _i32, C.POINTER(_P)]),
+    "pvs_merge_shards": (C.c_int, [C.POINTER(_P), _i32, C.POINTER(_P)]),
+    "pvs_merge_next": (C.c_int, [_P, _i32, _u8p, _i64p, _f32p, _i32p, _i32p]),
+    "pvs_merge_close": (None, [_P]),
     "pvs_next": (C.c_int, [_P, _i32, _u8p, _i64p, _f32p, _i32p, _i32p]),
     "pvs_stats": (C.c_int, [_P, C.POINTER(pvs_counters)]),
     "pvs_profile_enable": (C.c_int, [_i32]),
@@ -225,6 +230,27 @@ class PvsState:
             pass
 
 
+class PvsMerge:
+    """A merged dense ranking (a Shard over Segments, or a request over
+    Shards); keeps its indexes alive."""
+
+    def __init__(self, handle, keep, B: int):
+        self.h = handle
+        self.keep = keep
+        self.B = B
+
+    def close(self):
+        if self.h:
+            load().pvs_merge_close(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
 class PbmIndex:
     def __init__(self, handle):
         self.h = handle
@@ -336,6 +362,59 @@ def pvs_next(state: PvsState, m: int, active: Optional[Sequence[bool]] = None):
     _check(load().pvs_next(state.h, m, _ptr(act, C.c_uint8) if act is not None else None,
                            _ptr(ids, C.c_int64), _ptr(sc, C.c_float), _ptr(cnt, C.c_int32),
                            _ptr(stt, C.c_int32)))
+    return ids[:, :m], sc[:, :m], cnt, stt
+
+
+def pvs_merge_open(segments: Sequence[PvsIndex], gids, queries, versions=None, epochs=None) -> PvsMerge:
+    """A Shard over Segments: segments[s] with its row -> global id map
+    gids[s] (strictly ascending) and optional per-row versions."""
+    n = len(segments)
+    p, kind, keep, shape = _array_arg(queries)
+    if len(shape) == 1:
+        shape = (1, shape[0])
+    segs = (_P * n)(*[sg.h for sg in segments])
+    g = [np.ascontiguousarray(x, dtype=np.int64) for x in gids]
+    gp = (_i64p * n)(*[_ptr(x, C.c_int64) for x in g])
+    v = None
+    vp = None
+    if versions is not None:
+        v = [None if x is None else np.ascontiguousarray(x, dtype=np.int64) for x in versions]
+        vp = (_i64p * n)(*[(_ptr(x, C.c_int64) if x is not None else None) for x in v])
+    e = None
+    if epochs is not None:
+        e = np.ascontiguousarray(epochs, dtype=np.int64)
+    h = C.c_void_p()
+    _check(load().pvs_merge_open(segs, _ptr(e, C.c_int64) if e is not None else None, gp, vp, n, p,
+                                 shape[0], kind, C.byref(h)))
+    return PvsMerge(h, list(segments), shape[0])
+
+
+def pvs_merge_shards(shards: Sequence[PvsMerge]) -> PvsMerge:
+    """The request-level merge over Shards; takes ownership of them."""
+    n = len(shards)
+    arr = (_P * n)(*[s.h for s in shards])
+    h = C.c_void_p()
+    _check(load().pvs_merge_shards(arr, n, C.byref(h)))
+    keep = []
+    for s in shards:
+        keep.append(s.keep)
+        s.h = None          # owned by the request-level merge now
+    return PvsMerge(h, keep, shards[0].B)
+
+
+def pvs_merge_next(mg: PvsMerge, m: int, active: Optional[Sequence[bool]] = None):
+    """Next m merged ranks per query: (global ids [B,m], scores [B,m], count, status)."""
+    B = mg.B
+    ids = np.full((B, max(m, 1)), -1, dtype=np.int64)
+    sc = np.zeros((B, max(m, 1)), dtype=np.float32)
+    cnt = np.zeros(B, dtype=np.int32)
+    stt = np.zeros(B, dtype=np.int32)
+    act = None
+    if active is not None:
+        act = np.ascontiguousarray(np.asarray(active, dtype=np.uint8))
+    _check(load().pvs_merge_next(mg.h, m, _ptr(act, C.c_uint8) if act is not None else None,
+                                 _ptr(ids, C.c_int64), _ptr(sc, C.c_float), _ptr(cnt, C.c_int32),
+                                 _ptr(stt, C.c_int32)))
     return ids[:, :m], sc[:, :m], cnt, stt
 
 

@@ -1,0 +1,130 @@
+"""GPU parity of hierarchical merging (Sec. 2.4): Segment rankings merged in a
+Shard and Shard rankings merged per request must give the exact ranking of
+the union, identical to one index over all items, and must fail a query
+whose copies of an item disagree."""
+import numpy as np
+import pytest
+
+from paper_2608_07152_amd import datagen
+
+from gpu_helpers import check_dense_prefix
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def E():
+    from paper_2608_07152_amd import eahr
+    eahr.load()
+    return eahr
+
+
+@pytest.fixture(scope="module")
+def tiny(E):
+    w = datagen.workload("tiny", n=6000, d=96)
+    x, _ = datagen.corpus(w)
+    q, _ = datagen.queries(w, count=6)
+    return w, x, q
+
+
+def _drain(E, mg, schedule, nxt):
+    ids = [[] for _ in range(mg.B)]
+    scs = [[] for _ in range(mg.B)]
+    last = None
+    for m in schedule:
+        i, s, c, stt = nxt(mg, m)
+        for b in range(mg.B):
+            assert c[b] == m or stt[b] != E.LIST_OPEN
+            ids[b].extend(i[b, :c[b]].tolist())
+            scs[b].extend(s[b, :c[b]].tolist())
+        last = stt
+    return ids, scs, last
+
+
+def _segments(E, x, parts):
+    """Segments of the rows in `parts` (lists of global ids, ascending)."""
+    return [E.pvs_build(x[np.asarray(p)]) for p in parts], [np.asarray(p, np.int64) for p in parts]
+
+
+def test_shard_of_segments_equals_one_index(E, tiny):
+    w, x, q = tiny
+    parts = [np.arange(s, w.n, 3) for s in range(3)]          # interleaved ids
+    segs, gids = _segments(E, x, parts)
+    mg = E.pvs_merge_open(segs, gids, q)
+    sched = [20, 40, 200, 1000]
+    got, sc, stt = _drain(E, mg, sched, E.pvs_merge_next)
+    ref, rsc, _ = _drain(E, E.pvs_open(E.pvs_build(x), q), sched, E.pvs_next)
+    for b in range(len(q)):
+        assert got[b] == ref[b], b
+        assert sc[b] == rsc[b], b
+        check_dense_prefix(q[b], x, got[b], sc[b])
+    assert np.all(stt == E.LIST_OPEN)
+
+
+def test_request_over_shards_equals_one_index(E, tiny):
+    w, x, q = tiny
+    ids = np.arange(w.n)
+    parts = [ids[ids < 1500], ids[(ids >= 1500) & (ids % 2 == 0)], ids[(ids >= 1500) & (ids % 2 == 1)]]
+    segs, gids = _segments(E, x, parts)
+    shard_a = E.pvs_merge_open(segs[:2], gids[:2], q)
+    shard_b = E.pvs_merge_open(segs[2:], gids[2:], q)
+    req = E.pvs_merge_shards([shard_a, shard_b])
+    sched = [20, 20, 500, 3000]
+    got, sc, _ = _drain(E, req, sched, E.pvs_merge_next)
+    ref, rsc, _ = _drain(E, E.pvs_open(E.pvs_build(x), q), sched, E.pvs_next)
+    for b in range(len(q)):
+        assert got[b] == ref[b] and sc[b] == rsc[b], b
+
+
+def test_merge_to_exhaustion_with_snapshots(E):
+    w = datagen.workload("tiny", n=900, d=64)
+    x, _ = datagen.corpus(w)
+    q, _ = datagen.queries(w, count=3)
+    parts = [np.arange(0, 900, 2), np.arange(1, 900, 2)]
+    segs, gids = _segments(E, x, parts)
+    E.pvs_delete(segs[1], np.arange(0, 450, 5))            # local rows of segment 1
+    ep1 = E.pvs_snapshot(segs[1])
+    vis = np.ones(900, bool)
+    vis[gids[1][np.arange(0, 450, 5)]] = False
+    mg = E.pvs_merge_open(segs, gids, q, epochs=[0, ep1])
+    got, sc, stt = _drain(E, mg, [100, 5000], E.pvs_merge_next)
+    assert np.all(stt == E.LIST_EXHAUSTED)
+    for b in range(3):
+        assert len(got[b]) == int(vis.sum())
+        check_dense_prefix(q[b], x, got[b], sc[b], visible=vis)
+    _, _, c, stt = E.pvs_merge_next(mg, 10)
+    assert np.all(c == 0) and np.all(stt == E.LIST_EXHAUSTED)
+
+
+@pytest.mark.parametrize("case", ["consistent", "version", "score"])
+def test_copies_in_two_segments(E, case):
+    w = datagen.workload("tiny", n=400, d=64)
+    x, _ = datagen.corpus(w)
+    q, _ = datagen.queries(w, count=2)
+    a_ids = np.arange(0, 300)
+    b_ids = np.arange(250, 400)                              # 250..299 held by both
+    xb = x[b_ids].copy()
+    vb = np.zeros(len(b_ids), np.int64)
+    if case == "version":
+        vb[10] = 1                                           # item 260: another version
+    if case == "score":
+        xb[10] = x[(260 + 7) % 400]                          # item 260: another vector
+    segs = [E.pvs_build(x[a_ids]), E.pvs_build(xb)]
+    mg = E.pvs_merge_open(segs, [a_ids, b_ids], q, versions=[np.zeros(300, np.int64), vb])
+    got, sc, stt = _drain(E, mg, [50, 1000], E.pvs_merge_next)
+    if case == "consistent":
+        assert np.all(stt == E.LIST_EXHAUSTED)
+        for b in range(2):
+            assert sorted(got[b]) == list(range(400))        # each item once
+            check_dense_prefix(q[b], x, got[b], sc[b])
+    else:
+        assert np.all(stt == E.LIST_FAILED)                  # read to the end: the conflict is met
+        _, _, c, stt2 = E.pvs_merge_next(mg, 5)
+        assert np.all(c == 0) and np.all(stt2 == E.LIST_FAILED)   # sticky
+
+
+def test_merge_rejects_unordered_ids(E, tiny):
+    w, x, q = tiny
+    seg = E.pvs_build(x[:10])
+    with pytest.raises(Exception):
+        E.pvs_merge_open([seg], [np.array([0, 1, 2, 3, 4, 6, 5, 7, 8, 9])], q)
