@@ -1,0 +1,85 @@
+"""The authoritative float32 score follows one fixed order (reading R6 of the
+dense channel): lane l of a wavefront accumulates q_j * v_j with a fused
+multiply-add over j = 256 t + 4 l + i in (t, i) order, then the 64 lane sums
+are combined by an xor butterfly (offsets 32, 16, .., 1).  This test
+recomputes that order on the CPU with exactly rounded float32 operations and
+requires the GPU's scores (pvs_scores, and the ranks pvs_next emits) to
+match bit for bit."""
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from paper_2608_07152_amd import datagen
+
+pytestmark = pytest.mark.gpu
+
+F32 = np.float32
+
+
+def _round32(fr: Fraction) -> np.float32:
+    """Float32 nearest to an exact rational, ties to even."""
+    f = F32(float(fr))
+    cands = [np.nextafter(f, F32(-np.inf)), f, np.nextafter(f, F32(np.inf))]
+    return min(cands, key=lambda c: (abs(Fraction(float(c)) - fr),
+                                     int(np.array(c, F32).view(np.int32)) & 1))
+
+
+def _fma32(a, b, c) -> np.float32:
+    return _round32(Fraction(float(a)) * Fraction(float(b)) + Fraction(float(c)))
+
+
+def _add32(a, b) -> np.float32:
+    return _round32(Fraction(float(a)) + Fraction(float(b)))
+
+
+def r6_score(q: np.ndarray, v: np.ndarray) -> np.float32:
+    d = len(q)
+    df = (d + 3) // 4 * 4
+    qp = np.zeros(df, F32)
+    vp = np.zeros(df, F32)
+    qp[:d] = q
+    vp[:d] = v
+    df4 = df // 4
+    lanes = []
+    for lane in range(64):
+        acc = F32(0)
+        t = 0
+        while 64 * t + lane < df4:
+            for i in range(4):
+                j = 256 * t + 4 * lane + i
+                acc = _fma32(qp[j], vp[j], acc)
+            t += 1
+        lanes.append(acc)
+    for off in (32, 16, 8, 4, 2, 1):
+        lanes = [_add32(lanes[l], lanes[l ^ off]) for l in range(64)]
+    return lanes[0]
+
+
+@pytest.fixture(scope="module")
+def E():
+    from paper_2608_07152_amd import eahr
+    eahr.load()
+    return eahr
+
+
+@pytest.mark.parametrize("d", [100, 128, 768])
+def test_scores_follow_the_fixed_order_bit_for_bit(E, d):
+    w = datagen.workload("tiny", n=300, d=d)
+    x, _ = datagen.corpus(w)
+    q, _ = datagen.queries(w, count=2)
+    idx = E.pvs_build(x)
+    st = E.pvs_open(idx, q)
+    rng = np.random.default_rng(d)
+    rows = np.sort(rng.choice(w.n, size=6, replace=False))
+    for b in range(2):
+        got = E.pvs_scores(st, b, rows)
+        for k, r in enumerate(rows):
+            want = r6_score(q[b], x[r])
+            assert np.array(got[k], F32).view(np.int32) == np.array(want, F32).view(np.int32), (b, r)
+    # the ranks pvs_next emits carry the same scores (rescoring's own code)
+    ids, sc, cnt, _ = E.pvs_next(st, 5)
+    for b in range(2):
+        for k in range(cnt[b]):
+            want = r6_score(q[b], x[ids[b, k]])
+            assert np.array(sc[b, k], F32).view(np.int32) == np.array(want, F32).view(np.int32)
