@@ -217,7 +217,7 @@ typedef struct pvs_merge pvs_merge;
 
 /* pvs_merge_open -- open a Shard over n_segs Segments for B queries.
  *   segs[s]      the Segment's index; epochs[s] its snapshot (NULL: all 0).
- *   gids[s]      host array, one global id >= 0 per row of the snapshot,
+ *   gids[s]      host array, one global id in [0, 2^31 - 1) per row of the snapshot,
  *                strictly ascending (so the Segment's own id order is the
  *                global one); copied.
  *   versions[s]  host array of per-row versions, or NULL (all 0); versions
@@ -315,6 +315,17 @@ int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index* sparse,
               const eahr_sparse_query* q_sparse, int32_t B, const eahr_params* params,
               int64_t* out_ids, int32_t* out_count, int32_t* out_status,
               eahr_query_stats* stats);
+
+/* eahr_topk_merged -- eahr_topk whose dense channel is a merged ranking
+ * (pvs_merge_open / pvs_merge_shards, opened on the same B queries and not
+ * read yet; it stays the caller's to close and is read on by this call).
+ * Sparse document ids must be the merge's global ids.  The dense channel
+ * uses interval scans (params->dense_generator must be EAHR_GEN_INTERVALS).
+ * Outputs and errors as eahr_topk. */
+int eahr_topk_merged(pvs_merge* dense, const pbm_index* sparse,
+                     const eahr_sparse_query* q_sparse, int32_t B, const eahr_params* params,
+                     int64_t* out_ids, int32_t* out_count, int32_t* out_status,
+                     eahr_query_stats* stats);
 
 /* eahr_fuse_lists -- the same fusion over two complete rankings given as host
  * arrays of distinct ids (e.g. controlled rank streams, Sec. 3.4).  Both lists

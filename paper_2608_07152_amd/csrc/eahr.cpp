@@ -97,17 +97,21 @@ struct WorkLease {
 
 }  // namespace
 
-extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index* sparse,
-                         const float* q_dense, int32_t q_ptr_kind,
-                         const eahr_sparse_query* q_sparse, int32_t B, const eahr_params* params,
-                         int64_t* out_ids, int32_t* out_count, int32_t* out_status,
-                         eahr_query_stats* stats) {
+// The dense channel is either a pvs_state opened here on `dense` or, when
+// `merged` is given, a caller-opened merged ranking (Segments / Shards).
+static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
+                     const pbm_index* sparse, const float* q_dense, int32_t q_ptr_kind,
+                     const eahr_sparse_query* q_sparse, int32_t B, const eahr_params* params,
+                     int64_t* out_ids, int32_t* out_count, int32_t* out_status,
+                     eahr_query_stats* stats) {
     if (!params || B <= 0 || !out_ids || !out_count || !out_status)
         EAHR_FAIL(EAHR_E_INVALID, "eahr_topk: bad arguments");
     const eahr_params& ep = *params;
     EAHR_TRY(check_params(ep));
     const bool use_dense = ep.w_dense > 0, use_sparse = ep.w_sparse > 0;
-    if (use_dense && (!dense || !q_dense)) EAHR_FAIL(EAHR_E_INVALID, "eahr_topk: dense channel missing");
+    if (use_dense && !merged && (!dense || !q_dense)) EAHR_FAIL(EAHR_E_INVALID, "eahr_topk: dense channel missing");
+    if (use_dense && merged && eahr_merge_batch(merged) != B)
+        EAHR_FAIL(EAHR_E_INVALID, "eahr_topk_merged: the merge was opened for another batch size");
     if (use_sparse && (!sparse || !q_sparse)) EAHR_FAIL(EAHR_E_INVALID, "eahr_topk: sparse channel missing");
     const Params P{ep.K, ep.k_rrf, {ep.w_dense, ep.w_sparse}};
     const auto t_call = std::chrono::steady_clock::now();
@@ -141,7 +145,7 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
         }
     } cl;
     const auto t_open = std::chrono::steady_clock::now();
-    if (use_dense)
+    if (use_dense && !merged)
         EAHR_TRY(pvs_open_gen(dense, epoch, q_dense, B, q_ptr_kind, ep.dense_generator, &cl.st));
     const double open_dense_ms = ms_since(t_open);
     // sparse states are opened by the sparse workers, at a query's first
@@ -250,7 +254,10 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
             const auto t0 = std::chrono::steady_clock::now();
             int64_t* ids = dids.get(static_cast<size_t>(B) * m);
             float* sc = dscores.get(static_cast<size_t>(B) * m);
-            dense_rc = pvs_next(cl.st, static_cast<int32_t>(m), dact.data(), ids, sc, dcnt.data(), dsts.data());
+            dense_rc = merged ? pvs_merge_next(merged, static_cast<int32_t>(m), dact.data(), ids, sc,
+                                               dcnt.data(), dsts.data())
+                              : pvs_next(cl.st, static_cast<int32_t>(m), dact.data(), ids, sc,
+                                         dcnt.data(), dsts.data());
             // While the sparse channel is still busy, certify the dense ranks
             // of the next depths ahead (they are served from the cache later;
             // the output does not depend on it).
@@ -258,7 +265,7 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
             for (int32_t b = 0; b < B; ++b) nd += dact[b];
             const int64_t cap = std::min<int64_t>(kFillMaxDepth, kFillBudget / std::max<int64_t>(nd, 1));
             int64_t ahead = depth;
-            while (dense_rc == EAHR_OK && sparse_thread.joinable() && ahead <= cap / ep.growth &&
+            while (dense_rc == EAHR_OK && !merged && sparse_thread.joinable() && ahead <= cap / ep.growth &&
                    !sparse_done.load(std::memory_order_acquire)) {
                 // remaining sparse time: from the share of postings of the
                 // finished queries (a first call scores about its postings),
@@ -389,6 +396,27 @@ extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index*
     }
     if (any_failed) EAHR_FAIL(EAHR_E_FAILED, "eahr_topk: a ranked list failed");
     return EAHR_OK;
+}
+
+extern "C" int eahr_topk(const pvs_index* dense, int64_t epoch, const pbm_index* sparse,
+                         const float* q_dense, int32_t q_ptr_kind,
+                         const eahr_sparse_query* q_sparse, int32_t B, const eahr_params* params,
+                         int64_t* out_ids, int32_t* out_count, int32_t* out_status,
+                         eahr_query_stats* stats) {
+    return topk_impl(dense, epoch, nullptr, sparse, q_dense, q_ptr_kind, q_sparse, B, params, out_ids,
+                     out_count, out_status, stats);
+}
+
+extern "C" int eahr_topk_merged(pvs_merge* dense, const pbm_index* sparse,
+                                const eahr_sparse_query* q_sparse, int32_t B,
+                                const eahr_params* params, int64_t* out_ids, int32_t* out_count,
+                                int32_t* out_status, eahr_query_stats* stats) {
+    if (params && params->w_dense > 0 && !dense)
+        EAHR_FAIL(EAHR_E_INVALID, "eahr_topk_merged: dense channel missing");
+    if (params && params->dense_generator != EAHR_GEN_INTERVALS)
+        EAHR_FAIL(EAHR_E_INVALID, "eahr_topk_merged: the merged channel uses interval scans");
+    return topk_impl(nullptr, 0, dense, sparse, nullptr, EAHR_PTR_HOST, q_sparse, B, params, out_ids,
+                     out_count, out_status, stats);
 }
 
 extern "C" int eahr_fuse_lists(const int64_t* list_d, int64_t n_d, const int64_t* list_s,

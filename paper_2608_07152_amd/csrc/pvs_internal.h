@@ -59,6 +59,8 @@ enum class ScanPath { Auto, Gemv, Mfma };
 // sparse channel of a round is still running, so the GPU works ahead.
 // `added` (optional) receives the number of ranks certified by the call.
 int pvs_fill(pvs_state* st, int64_t depth, const uint8_t* active, int64_t* added);
+// Batch size a merged ranking was opened for (pvs_merge.cpp).
+int32_t eahr_merge_batch(const pvs_merge* mg);
 
 // Process-wide profile hooks used by the host fusion (pvs_profile_enable).
 bool pvs_profile_on();

@@ -23,6 +23,7 @@
 #include <vector>
 
 #include "common.h"
+#include "pvs_internal.h"
 
 namespace {
 
@@ -275,7 +276,8 @@ extern "C" int pvs_merge_open(const pvs_index* const* segs, const int64_t* epoch
         auto& S = mg->src[s];
         S.gid.assign(gids[s], gids[s] + erows);
         for (int64_t r = 0; r < erows; ++r) {
-            if (S.gid[r] < 0) EAHR_FAIL(EAHR_E_INVALID, "pvs_merge_open: negative global id");
+            if (S.gid[r] < 0 || S.gid[r] >= (1LL << 31) - 1)
+                EAHR_FAIL(EAHR_E_INVALID, "pvs_merge_open: global id outside [0, 2^31 - 1)");
             if (r > 0 && S.gid[r] <= S.gid[r - 1])
                 EAHR_FAIL(EAHR_E_INVALID, "pvs_merge_open: segment %d ids not strictly ascending", s);
         }
@@ -343,3 +345,5 @@ extern "C" int pvs_merge_next(pvs_merge* mg, int32_t m, const uint8_t* active, i
 }
 
 extern "C" void pvs_merge_close(pvs_merge* mg) { delete mg; }
+
+int32_t eahr_merge_batch(const pvs_merge* mg) { return mg ? mg->B : 0; }

@@ -129,6 +129,8 @@ SIGNATURES = {
     "eahr_topk": (C.c_int, [_P, _i64, _P, _P, _i32, C.POINTER(eahr_sparse_query), _i32,
                             C.POINTER(eahr_params), _i64p, _i32p, _i32p,
                             C.POINTER(eahr_query_stats)]),
+    "eahr_topk_merged": (C.c_int, [_P, _P, C.POINTER(eahr_sparse_query), _i32, C.POINTER(eahr_params),
+                                   _i64p, _i32p, _i32p, C.POINTER(eahr_query_stats)]),
     "eahr_fuse_lists": (C.c_int, [_i64p, _i64, _i64p, _i64, C.POINTER(eahr_params), _i32, _i64p,
                                   _i32p, C.POINTER(eahr_query_stats)]),
     "eahr_last_error": (C.c_char_p, []),
@@ -556,6 +558,31 @@ def eahr_topk(dense: Optional[PvsIndex], sparse: Optional[PbmIndex], q_dense,
     rc = load().eahr_topk(dense.h if dense is not None else None, epoch,
                           sparse.h if sparse is not None else None, p, kind, qs, B, C.byref(prm),
                           _ptr(ids, C.c_int64), _ptr(cnt, C.c_int32), _ptr(stt, C.c_int32), stats)
+    if not (rc == EAHR_E_FAILED and allow_failed):
+        _check(rc)
+    return ids[:, :K], cnt, stt, [s.as_dict() for s in stats]
+
+
+def eahr_topk_merged(dense: Optional[PvsMerge], sparse: Optional[PbmIndex],
+                     q_sparse: Sequence[Tuple[np.ndarray, np.ndarray]], B: int, K: int = 20,
+                     k_rrf: int = 60, w_dense: int = 1, w_sparse: int = 1, depth0: int = 20,
+                     growth: int = 2, allow_failed: bool = False):
+    """eahr_topk over a merged dense ranking (pvs_merge_open / pvs_merge_shards)."""
+    qs = (eahr_sparse_query * B)()
+    keep = []
+    if q_sparse is not None:
+        for b, (t, w) in enumerate(q_sparse):
+            q, k = _sparse_query(t, w)
+            qs[b] = q
+            keep.append(k)
+    prm = _params(K, k_rrf, w_dense, w_sparse, depth0, growth)
+    ids = np.full((B, max(K, 1)), -1, dtype=np.int64)
+    cnt = np.zeros(B, dtype=np.int32)
+    stt = np.zeros(B, dtype=np.int32)
+    stats = (eahr_query_stats * B)()
+    rc = load().eahr_topk_merged(dense.h if dense is not None else None,
+                                 sparse.h if sparse is not None else None, qs, B, C.byref(prm),
+                                 _ptr(ids, C.c_int64), _ptr(cnt, C.c_int32), _ptr(stt, C.c_int32), stats)
     if not (rc == EAHR_E_FAILED and allow_failed):
         _check(rc)
     return ids[:, :K], cnt, stt, [s.as_dict() for s in stats]

@@ -128,3 +128,31 @@ def test_merge_rejects_unordered_ids(E, tiny):
     seg = E.pvs_build(x[:10])
     with pytest.raises(Exception):
         E.pvs_merge_open([seg], [np.array([0, 1, 2, 3, 4, 6, 5, 7, 8, 9])], q)
+
+
+@pytest.mark.parametrize("wts", [(1, 1), (2, 1)])
+def test_eahr_topk_over_merged_segments(E, wts):
+    from oracle import sparse as osparse
+    from gpu_helpers import fused_reference, hybrid_dense_list
+    w = datagen.workload("tiny")
+    x, lab = datagen.corpus(w)
+    q, qlab = datagen.queries(w)
+    post = datagen.bm25_impacts(w, datagen.sparse_docs(w, lab))
+    qs = datagen.sparse_queries(w, qlab)
+    pbm = E.pbm_build(post.term_ptr, post.doc, post.impact, w.n, 1024)
+    ids = np.arange(w.n)
+    parts = [ids[ids % 4 == r] for r in range(4)]
+    segs, gids = _segments(E, x, parts)
+    req = E.pvs_merge_shards([E.pvs_merge_open(segs[:2], gids[:2], q), E.pvs_merge_open(segs[2:], gids[2:], q)])
+    got, cnt, stt, stats = E.eahr_topk_merged(req, pbm, qs, len(q), K=20, w_dense=wts[0], w_sparse=wts[1])
+    ref, rcnt, _, _ = E.eahr_topk(E.pvs_build(x), pbm, q, qs, K=20, w_dense=wts[0], w_sparse=wts[1])
+    assert np.all(stt == 0)
+    assert np.array_equal(got, ref) and np.array_equal(cnt, rcnt)
+    one = E.pvs_build(x)
+    for b in range(len(q)):
+        D = stats[b]["dense_depth"]
+        di, ds, _, _ = E.pvs_next(E.pvs_open(one, q[b:b + 1]), max(D, 1))
+        check_dense_prefix(q[b], x, di[0, :D], ds[0, :D])
+        S = osparse.sparse_scores(post.term_ptr, post.doc, post.impact, qs[b][0], qs[b][1], w.n)
+        want = fused_reference(hybrid_dense_list(di[0, :D], q[b], x), osparse.sparse_ranking(S), 20, 60, wts)
+        assert list(got[b, :cnt[b]]) == want, b
