@@ -287,7 +287,19 @@ typedef struct {
     int32_t w_dense;     /* rank-scaled weights w_i >= 0 (Sec. 2.1), integers     */
     int32_t w_sparse;
     int32_t dense_generator;   /* EAHR_GEN_* of the dense channel (0: intervals)  */
+    int32_t schedule;          /* EAHR_SCHED_*: depth doubling (0) or the frozen
+                                * scheduler of Sec. 3.5 (1); the result is the same */
 } eahr_params;
+
+/* Depth schedules of eahr_params.schedule.  EAHR_SCHED_DOUBLING: every Open
+ * list advances to depth0 * growth^j per round.  EAHR_SCHED_FROZEN (Sec. 3.5):
+ * one list per step, at most 16 ranks, the one with the larger weighted-RRF
+ * contribution at its next unread rank (ties: dense) unless the other was
+ * skipped 16 steps in a row; certification after every step through the
+ * first 4K ranks of cumulative access, then after a further 1/8 of the
+ * access (64 to 1,024 ranks), and at once when a list is read to its end.
+ * eahr_fuse_lists ignores its step argument under the frozen schedule. */
+enum { EAHR_SCHED_DOUBLING = 0, EAHR_SCHED_FROZEN = 1 };
 
 typedef struct {
     int64_t dense_depth;    /* d_i: ranks read from each list        */

@@ -22,6 +22,7 @@
 #include "host_parallel.h"
 #include "pbm_internal.h"
 #include "pvs_internal.h"
+#include "schedule.h"
 
 namespace {
 
@@ -31,7 +32,8 @@ using ::eahr::Params;
 int check_params(const eahr_params& ep) {
     if (ep.K < 0 || ep.depth0 < 1 || ep.growth < 2 || ep.k_rrf < 1 || ep.k_rrf > (1 << 20) ||
         ep.w_dense < 0 || ep.w_dense > 1024 || ep.w_sparse < 0 || ep.w_sparse > 1024 ||
-        (ep.dense_generator != EAHR_GEN_INTERVALS && ep.dense_generator != EAHR_GEN_FULL_SCAN))
+        (ep.dense_generator != EAHR_GEN_INTERVALS && ep.dense_generator != EAHR_GEN_FULL_SCAN) ||
+        (ep.schedule != EAHR_SCHED_DOUBLING && ep.schedule != EAHR_SCHED_FROZEN))
         EAHR_FAIL(EAHR_E_INVALID, "eahr: parameters out of range");
     return EAHR_OK;
 }
@@ -191,10 +193,117 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
             }
         std::stable_sort(sorder.begin(), sorder.end(), [&](int32_t a, int32_t c) { return cost[a] > cost[c]; });
     }
+    if (ep.schedule == EAHR_SCHED_FROZEN) {
+        // Frozen scheduler: ranks are read ahead into per-query pending
+        // buffers (dense batched, sparse per query), and every check appends
+        // exactly the ranks the schedule has reached and certifies.
+        const int64_t H = ::eahr::FrozenSchedule::kHorizon;
+        std::vector<::eahr::FrozenSchedule> Sch(B);
+        std::vector<std::vector<int64_t>> pend[2];
+        std::vector<int64_t> head[2];
+        std::vector<uint8_t> exh[2];
+        for (int i = 0; i < 2; ++i) {
+            pend[i].assign(B, {});
+            head[i].assign(B, 0);
+            exh[i].assign(B, 0);
+        }
+        auto live = [&](int32_t b) { return !F[b].resolved && !failed[b]; };
+        auto have = [&](int i, int32_t b) { return static_cast<int64_t>(pend[i][b].size()) - head[i][b]; };
+        for (;;) {
+            bool any = false;
+            for (int32_t b = 0; b < B; ++b) any |= live(b);
+            if (!any) break;
+            const auto t0 = std::chrono::steady_clock::now();
+            if (use_dense) {
+                int64_t m = 0;
+                for (int32_t b = 0; b < B; ++b) {
+                    dact[b] = live(b) && !exh[0][b] && have(0, b) < H;
+                    if (dact[b]) m = std::max<int64_t>(m, 2 * H - have(0, b));
+                }
+                if (m > 0) {
+                    int64_t* ids = dids.get(static_cast<size_t>(B) * m);
+                    float* sc = dscores.get(static_cast<size_t>(B) * m);
+                    EAHR_TRY(pvs_next(cl.st, static_cast<int32_t>(m), dact.data(), ids, sc, dcnt.data(),
+                                      dsts.data()));
+                    for (int32_t b = 0; b < B; ++b) {
+                        if (!dact[b]) continue;
+                        if (dsts[b] == EAHR_LIST_FAILED) {
+                            failed[b] = 1;
+                            dstat[b] = EAHR_LIST_FAILED;
+                            continue;
+                        }
+                        const int64_t* p = ids + static_cast<size_t>(b) * m;
+                        pend[0][b].insert(pend[0][b].end(), p, p + dcnt[b]);
+                        if (dsts[b] == EAHR_LIST_EXHAUSTED) exh[0][b] = 1;
+                    }
+                }
+            }
+            t_dense += ms_since(t0);
+            const auto t1 = std::chrono::steady_clock::now();
+            if (use_sparse) {
+                parallel_for(B, threads, [&](int64_t b) {
+                    if (!live(static_cast<int32_t>(b)) || exh[1][b] || have(1, b) >= H) return;
+                    if (!cl.sp[b]) {
+                        sparse_rc[b] = pbm_open(sparse, &q_sparse[b], &cl.sp[b]);
+                        if (sparse_rc[b] != EAHR_OK) return;
+                    }
+                    const int64_t need = 2 * H - have(1, b);
+                    sids[b].resize(static_cast<size_t>(need));
+                    sscores[b].resize(static_cast<size_t>(need));
+                    sparse_rc[b] = pbm_next(cl.sp[b], static_cast<int32_t>(need), sids[b].data(),
+                                            sscores[b].data(), &scnt[b], &ssts[b]);
+                    if (sparse_rc[b] != EAHR_OK) return;
+                    if (ssts[b] == EAHR_LIST_FAILED) {
+                        failed[b] = 1;
+                        sstat[b] = EAHR_LIST_FAILED;
+                        return;
+                    }
+                    pend[1][b].insert(pend[1][b].end(), sids[b].begin(), sids[b].begin() + scnt[b]);
+                    if (ssts[b] == EAHR_LIST_EXHAUSTED) exh[1][b] = 1;
+                });
+                for (int32_t b = 0; b < B; ++b) EAHR_TRY(sparse_rc[b]);
+            }
+            t_sparse += ms_since(t1);
+            const auto t2 = std::chrono::steady_clock::now();
+            parallel_for(B, threads, [&](int64_t bb) {
+                const int32_t b = static_cast<int32_t>(bb);
+                if (!live(b)) return;
+                auto& S = Sch[b];
+                const int64_t avail[2] = {S.d[0] + have(0, b), S.d[1] + have(1, b)};
+                const bool done[2] = {exh[0][b] != 0, exh[1][b] != 0};
+                const bool use[2] = {use_dense, use_sparse};
+                S.advance(P, avail, done, use);
+                for (int i = 0; i < 2; ++i) {
+                    const int64_t n = S.d[i] - static_cast<int64_t>(F[b].L[i].size());
+                    if (n > 0) {
+                        F[b].append(i, pend[i][b].data() + head[i][b], n);
+                        head[i][b] += n;
+                    }
+                    if (done[i] && S.d[i] == avail[i] && F[b].L[i].open) {
+                        F[b].L[i].open = false;
+                        (i == 0 ? dstat : sstat)[b] = EAHR_LIST_EXHAUSTED;
+                    }
+                    if (head[i][b] > (1 << 16) && 2 * head[i][b] > static_cast<int64_t>(pend[i][b].size())) {
+                        pend[i][b].erase(pend[i][b].begin(), pend[i][b].begin() + head[i][b]);
+                        head[i][b] = 0;
+                    }
+                }
+                if (F[b].dup) {
+                    failed[b] = 1;
+                    return;
+                }
+                rounds[b] += 1;
+                F[b].certify();
+                // both lists complete and still unresolved: not rankings
+                if (!F[b].resolved && !F[b].L[0].open && !F[b].L[1].open) failed[b] = 1;
+            });
+            t_fuse += ms_since(t2);
+        }
+    }
     int64_t depth = ep.depth0;
     double fill_ms = 0.0;            // measured cost of dense work-ahead
     int64_t fill_ranks = 0;
-    for (;;) {
+    for (bool doubling = ep.schedule == EAHR_SCHED_DOUBLING; doubling;) {
         bool any = false;
         for (int32_t b = 0; b < B; ++b) any |= !F[b].resolved && !failed[b];
         if (!any) break;
@@ -441,6 +550,25 @@ extern "C" int eahr_fuse_lists(const int64_t* list_d, int64_t n_d, const int64_t
     for (int i = 0; i < 2; ++i) f.L[i].open = P.w[i] > 0 && lens[i] > 0;
     if (ep.K == 0) f.resolved = true;
     int32_t rounds = 0;
+    if (ep.schedule == EAHR_SCHED_FROZEN) {
+        ::eahr::FrozenSchedule S;
+        const bool use[2] = {f.L[0].open, f.L[1].open};
+        const int64_t avail[2] = {use[0] ? lens[0] : 0, use[1] ? lens[1] : 0};
+        const bool done[2] = {true, true};
+        while (!f.resolved) {
+            const bool stepped = S.advance(P, avail, done, use);
+            for (int i = 0; i < 2; ++i) {
+                const int64_t have = static_cast<int64_t>(f.L[i].size());
+                if (S.d[i] > have) f.append(i, lists[i] + have, S.d[i] - have);
+                if (f.L[i].open && static_cast<int64_t>(f.L[i].size()) == avail[i]) f.L[i].open = false;
+            }
+            if (f.dup) EAHR_FAIL(EAHR_E_INVALID, "eahr_fuse_lists: a list repeats an id");
+            rounds += 1;
+            f.certify();
+            if (!f.resolved && !stepped)
+                EAHR_FAIL(EAHR_E_INVALID, "eahr_fuse_lists: lists hold duplicate ids");
+        }
+    }
     int64_t depth = step > 0 ? step : ep.depth0;
     while (!f.resolved) {
         for (int i = 0; i < 2; ++i) {

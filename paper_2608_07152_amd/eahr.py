@@ -48,7 +48,7 @@ class eahr_sparse_query(C.Structure):
 class eahr_params(C.Structure):
     _fields_ = [("K", C.c_int32), ("depth0", C.c_int32), ("growth", C.c_int32),
                 ("k_rrf", C.c_int32), ("w_dense", C.c_int32), ("w_sparse", C.c_int32),
-                ("dense_generator", C.c_int32)]
+                ("dense_generator", C.c_int32), ("schedule", C.c_int32)]
 
 
 class eahr_query_stats(C.Structure):
@@ -521,18 +521,22 @@ def pbm_debug_set_blockmax(index: PbmIndex, term: int, range_: int, value: float
 
 
 # ------------------------------------------------------------------ fusion
-def _params(K, k_rrf, w_dense, w_sparse, depth0, growth, generator="intervals"):
+SCHEDULES = {"doubling": 0, "frozen": 1}
+
+
+def _params(K, k_rrf, w_dense, w_sparse, depth0, growth, generator="intervals", schedule="doubling"):
     for v in (k_rrf, w_dense, w_sparse):
         if int(v) != v:
             raise ValueError("k and the weights must be integers")
     return eahr_params(int(K), int(depth0), int(growth), int(k_rrf), int(w_dense), int(w_sparse),
-                       GENERATORS[generator])
+                       GENERATORS[generator], SCHEDULES[schedule])
 
 
 def eahr_topk(dense: Optional[PvsIndex], sparse: Optional[PbmIndex], q_dense,
               q_sparse: Sequence[Tuple[np.ndarray, np.ndarray]], K: int = 20, k_rrf: int = 60,
               w_dense: int = 1, w_sparse: int = 1, epoch: int = 0, depth0: int = 20,
-              growth: int = 2, allow_failed: bool = False, dense_generator: str = "intervals"):
+              growth: int = 2, allow_failed: bool = False, dense_generator: str = "intervals",
+              schedule: str = "doubling"):
     """Ordered Top-K of complete-list weighted RRF for a batch of queries
     (``dense_generator``: "intervals" or "full_scan", see pvs_open).
 
@@ -550,7 +554,7 @@ def eahr_topk(dense: Optional[PvsIndex], sparse: Optional[PbmIndex], q_dense,
             q, k = _sparse_query(t, w)
             qs[b] = q
             keep.append(k)
-    prm = _params(K, k_rrf, w_dense, w_sparse, depth0, growth, dense_generator)
+    prm = _params(K, k_rrf, w_dense, w_sparse, depth0, growth, dense_generator, schedule)
     ids = np.full((B, max(K, 1)), -1, dtype=np.int64)
     cnt = np.zeros(B, dtype=np.int32)
     stt = np.zeros(B, dtype=np.int32)
@@ -589,11 +593,12 @@ def eahr_topk_merged(dense: Optional[PvsMerge], sparse: Optional[PbmIndex],
 
 
 def eahr_fuse_lists(list_d, list_s, K: int = 20, k_rrf: int = 60, w_dense: int = 1,
-                    w_sparse: int = 1, step: int = 0, depth0: int = 20, growth: int = 2):
+                    w_sparse: int = 1, step: int = 0, depth0: int = 20, growth: int = 2,
+                    schedule: str = "doubling"):
     """Fusion over two complete host rankings; returns (top ids, stats dict)."""
     a = np.ascontiguousarray(list_d, dtype=np.int64)
     b = np.ascontiguousarray(list_s, dtype=np.int64)
-    prm = _params(K, k_rrf, w_dense, w_sparse, depth0, growth)
+    prm = _params(K, k_rrf, w_dense, w_sparse, depth0, growth, schedule=schedule)
     out = np.full(max(K, 1), -1, dtype=np.int64)
     cnt = C.c_int32()
     st = eahr_query_stats()
