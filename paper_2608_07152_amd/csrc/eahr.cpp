@@ -524,6 +524,8 @@ extern "C" int eahr_topk_merged(pvs_merge* dense, const pbm_index* sparse,
         EAHR_FAIL(EAHR_E_INVALID, "eahr_topk_merged: dense channel missing");
     if (params && params->dense_generator != EAHR_GEN_INTERVALS)
         EAHR_FAIL(EAHR_E_INVALID, "eahr_topk_merged: the merged channel uses interval scans");
+    if (params && params->w_dense > 0 && !eahr_merge_unread(dense))
+        EAHR_FAIL(EAHR_E_INVALID, "eahr_topk_merged: the merge has already been read");
     return topk_impl(nullptr, 0, dense, sparse, nullptr, EAHR_PTR_HOST, q_sparse, B, params, out_ids,
                      out_count, out_status, stats);
 }

@@ -61,6 +61,8 @@ enum class ScanPath { Auto, Gemv, Mfma };
 int pvs_fill(pvs_state* st, int64_t depth, const uint8_t* active, int64_t* added);
 // Batch size a merged ranking was opened for (pvs_merge.cpp).
 int32_t eahr_merge_batch(const pvs_merge* mg);
+// No rank of the merge has been returned yet (and no query failed).
+bool eahr_merge_unread(const pvs_merge* mg);
 
 // Process-wide profile hooks used by the host fusion (pvs_profile_enable).
 bool pvs_profile_on();

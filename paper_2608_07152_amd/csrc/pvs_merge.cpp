@@ -347,3 +347,10 @@ extern "C" int pvs_merge_next(pvs_merge* mg, int32_t m, const uint8_t* active, i
 extern "C" void pvs_merge_close(pvs_merge* mg) { delete mg; }
 
 int32_t eahr_merge_batch(const pvs_merge* mg) { return mg ? mg->B : 0; }
+
+bool eahr_merge_unread(const pvs_merge* mg) {
+    if (!mg) return false;
+    for (const auto& q : mg->q)
+        if (q.emitted > 0 || q.failed) return false;
+    return true;
+}

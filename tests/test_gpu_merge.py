@@ -156,3 +156,13 @@ def test_eahr_topk_over_merged_segments(E, wts):
         S = osparse.sparse_scores(post.term_ptr, post.doc, post.impact, qs[b][0], qs[b][1], w.n)
         want = fused_reference(hybrid_dense_list(di[0, :D], q[b], x), osparse.sparse_ranking(S), 20, 60, wts)
         assert list(got[b, :cnt[b]]) == want, b
+
+
+def test_eahr_topk_merged_rejects_a_read_merge(E, tiny):
+    w, x, q = tiny
+    parts = [np.arange(0, w.n, 2), np.arange(1, w.n, 2)]
+    segs, gids = _segments(E, x, parts)
+    mg = E.pvs_merge_open(segs, gids, q)
+    E.pvs_merge_next(mg, 5)
+    with pytest.raises(Exception):
+        E.eahr_topk_merged(mg, None, None, len(q), K=20, w_dense=1, w_sparse=0)
