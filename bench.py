@@ -174,7 +174,9 @@ def query_set_for(w, batch):
 def generator_ablation(eahr, torch, x, idx, pbm, qdev, sparse_q, w, K, wts, nq, batch):
     """Rank-generator ablation (Sec. 4.4, Table 4-1): the same eahr_topk with
     the dense generator replaced by global-scale scalar-quantisation intervals
-    ("scalar") or by one exhaustive float32 scan ("scan").  Single requests
+    ("scalar") or by one exhaustive float32 scan ("scan"), or the sparse
+    generator replaced by the complete exact sparse ranking
+    ("sparse_complete").  Single requests
     are timed in paired rounds (generator order rotating, 1 warm-up + 3 runs
     each, median per query) and compared by the geometric mean of the
     per-query latency ratios; the batch is timed for 1 warm-up + 2 steps with
@@ -187,14 +189,16 @@ def generator_ablation(eahr, torch, x, idx, pbm, qdev, sparse_q, w, K, wts, nq, 
     gidx = eahr.pvs_build_quant(x, "global")
     torch.cuda.synchronize()
     log(f"ablation: global-scale index built in {time.perf_counter() - t:.1f}s")
-    gens = {"pvs": (idx, "intervals"), "scalar": (gidx, "intervals"), "scan": (idx, "full_scan")}
+    gens = {"pvs": (idx, "intervals", "pbm"), "scalar": (gidx, "intervals", "pbm"),
+            "scan": (idx, "full_scan", "pbm"), "sparse_complete": (idx, "intervals", "complete")}
 
     def call(g, a, b):
-        ix, gen = gens[g]
+        ix, gen, sgen = gens[g]
         eahr.pvs_profile_enable(True)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        r = eahr.eahr_topk(ix, pbm, a, b, K=K, w_dense=wts[0], w_sparse=wts[1], dense_generator=gen)
+        r = eahr.eahr_topk(ix, pbm, a, b, K=K, w_dense=wts[0], w_sparse=wts[1], dense_generator=gen,
+                           sparse_generator=sgen)
         torch.cuda.synchronize()
         el = time.perf_counter() - t0
         pairs = eahr.pvs_profile_read()["rescore_rows"]
@@ -235,18 +239,20 @@ def generator_ablation(eahr, torch, x, idx, pbm, qdev, sparse_q, w, K, wts, nq, 
         "queries": nq,
         "scalar_over_pvs_latency_gmean": gmean_ratio("scalar"),
         "scan_over_pvs_latency_gmean": gmean_ratio("scan"),
+        "sparse_complete_over_pbm_latency_gmean": gmean_ratio("sparse_complete"),
         "median_ms": {g: float(np.median(lat[g]) * 1e3) for g in gens},
         "f32_evals_median": {g: float(np.median(evals[g])) for g in gens},
         "pvs_f32_evals_reduction_vs": {"scalar": reduction("scalar"), "scan": reduction("scan")},
-        "topk_identical_to_pvs": {g: same[g] for g in ("scalar", "scan")},
+        "topk_identical_to_pvs": {g: same[g] for g in ("scalar", "scan", "sparse_complete")},
     }
     log(f"ablation: single requests scalar/pvs = {single['scalar_over_pvs_latency_gmean']:.3f}, "
-        f"scan/pvs = {single['scan_over_pvs_latency_gmean']:.3f}, f32 evals "
+        f"scan/pvs = {single['scan_over_pvs_latency_gmean']:.3f}, "
+        f"sparse complete/pbm = {single['sparse_complete_over_pbm_latency_gmean']:.3f}, f32 evals "
         + ", ".join(f"{g} {single['f32_evals_median'][g]:.0f}" for g in gens))
     nameb = query_set_for(w, batch)
     a, b = qdev[nameb][:batch], sparse_q[nameb][:batch]
     bt = {}
-    for g in ("pvs", "scalar"):
+    for g in ("pvs", "scalar", "sparse_complete"):
         call(g, a, b)
         runs = [call(g, a, b) for _ in range(2)]
         bt[g] = {"ms_per_step": float(np.mean([r[0] for r in runs]) * 1e3),
@@ -255,16 +261,19 @@ def generator_ablation(eahr, torch, x, idx, pbm, qdev, sparse_q, w, K, wts, nq, 
     batched = {
         "batch": batch,
         "scalar_over_pvs_latency": bt["scalar"]["ms_per_step"] / bt["pvs"]["ms_per_step"],
+        "sparse_complete_over_pbm_latency": bt["sparse_complete"]["ms_per_step"] / bt["pvs"]["ms_per_step"],
         "ms_per_step": {g: bt[g]["ms_per_step"] for g in bt},
         "f32_evals_per_step": {g: bt[g]["f32_evals_per_step"] for g in bt},
-        "topk_identical": bool(np.array_equal(bt["pvs"]["ids"], bt["scalar"]["ids"])),
+        "topk_identical": bool(np.array_equal(bt["pvs"]["ids"], bt["scalar"]["ids"]) and
+                               np.array_equal(bt["pvs"]["ids"], bt["sparse_complete"]["ids"])),
     }
     log(f"ablation: batch {batch} scalar/pvs = {batched['scalar_over_pvs_latency']:.3f}")
     eahr.pvs_free(gidx)
     torch.cuda.synchronize()
     return {"reference": "pvs",
             "alternatives": {"scalar": "scalar-quantisation intervals (one global scale)",
-                             "scan": "exhaustive float32 scan, one sort per query"},
+                             "scan": "exhaustive float32 scan, one sort per query",
+                             "sparse_complete": "complete exact sparse ranking (PBM replaced)"},
             "single_requests": single, "batch": batched}
 
 

@@ -271,6 +271,20 @@ int pbm_next(pbm_state* st, int32_t m, int64_t* ids, float* scores, int32_t* cou
              int32_t* status);
 void pbm_close(pbm_state* st);
 
+/* Sparse rank generators of pbm_open_gen. */
+enum { EAHR_SPARSE_PBM = 0, EAHR_SPARSE_COMPLETE = 1 };
+
+/* pbm_open_gen -- pbm_open with a choice of generator: EAHR_SPARSE_PBM is
+ * pbm_open (ranges expanded in bound order, ranks published when no
+ * unexpanded range can precede them, Sec. 2.3.2); EAHR_SPARSE_COMPLETE scores
+ * every document of every range with a positive bound at the first pbm_next
+ * and sorts them once: the complete exact sparse ranking that Sec. 3.5 and
+ * Sec. 4.4 (Table 4-1) compare PBM with.  Both give identical rankings and
+ * scores.  Errors: those of pbm_open, and EAHR_E_INVALID for an unknown
+ * generator. */
+int pbm_open_gen(const pbm_index* idx, const eahr_sparse_query* q, int32_t generator,
+                 pbm_state** out);
+
 /* pbm_debug_set_blockmax -- test hook: overwrite m_t(R) of one (term, range)
  * entry so that a later pbm_open sees metadata that no longer covers its
  * postings; pbm_next then reports EAHR_LIST_FAILED (App. A.2).  Returns
@@ -289,6 +303,7 @@ typedef struct {
     int32_t dense_generator;   /* EAHR_GEN_* of the dense channel (0: intervals)  */
     int32_t schedule;          /* EAHR_SCHED_*: depth doubling (0) or the frozen
                                 * scheduler of Sec. 3.5 (1); the result is the same */
+    int32_t sparse_generator;  /* EAHR_SPARSE_* of the sparse channel (0: PBM)     */
 } eahr_params;
 
 /* Depth schedules of eahr_params.schedule.  EAHR_SCHED_DOUBLING: every Open

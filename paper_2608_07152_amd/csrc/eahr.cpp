@@ -33,7 +33,8 @@ int check_params(const eahr_params& ep) {
     if (ep.K < 0 || ep.depth0 < 1 || ep.growth < 2 || ep.k_rrf < 1 || ep.k_rrf > (1 << 20) ||
         ep.w_dense < 0 || ep.w_dense > 1024 || ep.w_sparse < 0 || ep.w_sparse > 1024 ||
         (ep.dense_generator != EAHR_GEN_INTERVALS && ep.dense_generator != EAHR_GEN_FULL_SCAN) ||
-        (ep.schedule != EAHR_SCHED_DOUBLING && ep.schedule != EAHR_SCHED_FROZEN))
+        (ep.schedule != EAHR_SCHED_DOUBLING && ep.schedule != EAHR_SCHED_FROZEN) ||
+        (ep.sparse_generator != EAHR_SPARSE_PBM && ep.sparse_generator != EAHR_SPARSE_COMPLETE))
         EAHR_FAIL(EAHR_E_INVALID, "eahr: parameters out of range");
     return EAHR_OK;
 }
@@ -244,7 +245,7 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
                 parallel_for(B, threads, [&](int64_t b) {
                     if (!live(static_cast<int32_t>(b)) || exh[1][b] || have(1, b) >= H) return;
                     if (!cl.sp[b]) {
-                        sparse_rc[b] = pbm_open(sparse, &q_sparse[b], &cl.sp[b]);
+                        sparse_rc[b] = pbm_open_gen(sparse, &q_sparse[b], ep.sparse_generator, &cl.sp[b]);
                         if (sparse_rc[b] != EAHR_OK) return;
                     }
                     const int64_t need = 2 * H - have(1, b);
@@ -336,7 +337,7 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
                 const int32_t b = sorder[i];
                 if (!sact[b]) return;
                 if (!cl.sp[b]) {
-                    sparse_rc[b] = pbm_open(sparse, &q_sparse[b], &cl.sp[b]);
+                    sparse_rc[b] = pbm_open_gen(sparse, &q_sparse[b], ep.sparse_generator, &cl.sp[b]);
                     if (sparse_rc[b] != EAHR_OK) {
                         note_sparse_error(sparse_rc[b]);
                         sparse_cost_done.fetch_add(cost[b], std::memory_order_relaxed);

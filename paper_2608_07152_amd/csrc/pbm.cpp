@@ -106,8 +106,15 @@ int pbm_check_query(const pbm_index* ix, const eahr_sparse_query* q) {
 }
 
 extern "C" int pbm_open(const pbm_index* ix, const eahr_sparse_query* q, pbm_state** out) {
+    return pbm_open_gen(ix, q, EAHR_SPARSE_PBM, out);
+}
+
+extern "C" int pbm_open_gen(const pbm_index* ix, const eahr_sparse_query* q, int32_t generator,
+                            pbm_state** out) {
     if (!out) EAHR_FAIL(EAHR_E_INVALID, "pbm_open: out is NULL");
     *out = nullptr;
+    if (generator != EAHR_SPARSE_PBM && generator != EAHR_SPARSE_COMPLETE)
+        EAHR_FAIL(EAHR_E_INVALID, "pbm_open: unknown sparse generator %d", generator);
     EAHR_TRY(pbm_check_query(ix, q));
     std::unique_ptr<pbm_state> st;
     {
@@ -121,6 +128,7 @@ extern "C" int pbm_open(const pbm_index* ix, const eahr_sparse_query* q, pbm_sta
     if (!st) EAHR_FAIL(EAHR_E_OOM, "pbm_open: host allocation");
     st->reset();
     st->ix = ix;
+    st->complete = (generator == EAHR_SPARSE_COMPLETE);
     std::vector<std::pair<int32_t, float>> tw;
     for (int32_t i = 0; i < q->n_terms; ++i) tw.emplace_back(q->terms[i], q->weights[i]);
     std::sort(tw.begin(), tw.end());
@@ -345,6 +353,25 @@ extern "C" int pbm_next(pbm_state* st, int32_t m, int64_t* ids, float* scores, i
     if (!st || m < 0 || (m > 0 && (!ids || !scores)) || !count || !status)
         EAHR_FAIL(EAHR_E_INVALID, "pbm_next: bad arguments");
     int32_t n = 0;
+    if (!st->failed && st->complete && !st->complete_done) {
+        // complete generator: score every document of every range with a
+        // positive bound (ascending ranges), then one sort of all of them
+        st->complete_done = true;
+        std::vector<pbm_state::Range> all(st->order.begin(), st->order.end());
+        std::sort(all.begin(), all.end(),
+                  [](const pbm_state::Range& a, const pbm_state::Range& b) { return a.r < b.r; });
+        for (const auto& R : all) {
+            st->ranges_expanded += 1;
+            if (!expand(st, R)) st->failed = true;
+        }
+        st->next = st->order.size();
+        if (!st->failed) {
+            sort_keys(st->pool);
+            st->ready.swap(st->pool);
+            st->ready_pos = 0;
+        }
+        st->pool.clear();
+    }
     if (!st->failed) {
         while (n < m) {
             if (st->ready_pos < st->ready.size()) {

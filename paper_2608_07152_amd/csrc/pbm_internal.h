@@ -60,6 +60,8 @@ struct pbm_state {
     int64_t ranges_expanded = 0;
     int64_t postings_visited = 0;
     bool failed = false;
+    bool complete = false;        // complete generator: rank everything at the first call
+    bool complete_done = false;
 
     // empty state for another query, keeping the memory
     void reset() {
@@ -75,5 +77,7 @@ struct pbm_state {
         ranges_expanded = 0;
         postings_visited = 0;
         failed = false;
+        complete = false;
+        complete_done = false;
     }
 };

@@ -48,7 +48,8 @@ class eahr_sparse_query(C.Structure):
 class eahr_params(C.Structure):
     _fields_ = [("K", C.c_int32), ("depth0", C.c_int32), ("growth", C.c_int32),
                 ("k_rrf", C.c_int32), ("w_dense", C.c_int32), ("w_sparse", C.c_int32),
-                ("dense_generator", C.c_int32), ("schedule", C.c_int32)]
+                ("dense_generator", C.c_int32), ("schedule", C.c_int32),
+                ("sparse_generator", C.c_int32)]
 
 
 class eahr_query_stats(C.Structure):
@@ -123,6 +124,7 @@ SIGNATURES = {
     "pbm_build": (C.c_int, [_i64p, _i32, _i32p, _f32p, _i64, _i32, C.POINTER(_P)]),
     "pbm_free": (None, [_P]),
     "pbm_open": (C.c_int, [_P, C.POINTER(eahr_sparse_query), C.POINTER(_P)]),
+    "pbm_open_gen": (C.c_int, [_P, C.POINTER(eahr_sparse_query), _i32, C.POINTER(_P)]),
     "pbm_next": (C.c_int, [_P, _i32, _i64p, _f32p, _i32p, _i32p]),
     "pbm_close": (None, [_P]),
     "pbm_debug_set_blockmax": (C.c_int, [_P, _i32, _i64, C.c_float]),
@@ -492,10 +494,16 @@ def _sparse_query(terms, weights):
     return q, (t, w)
 
 
-def pbm_open(index: PbmIndex, terms, weights) -> PbmState:
+def pbm_open(index: PbmIndex, terms, weights, generator: str = "pbm") -> PbmState:
+    """Resumable exact sparse ranking of one query; ``generator`` is "pbm"
+    (Posting Block-Max) or "complete" (every document scored and sorted at the
+    first call)."""
     q, keep = _sparse_query(terms, weights)
     h = C.c_void_p()
-    _check(load().pbm_open(index.h, C.byref(q), C.byref(h)))
+    if generator == "pbm":
+        _check(load().pbm_open(index.h, C.byref(q), C.byref(h)))
+    else:
+        _check(load().pbm_open_gen(index.h, C.byref(q), SPARSE_GENERATORS[generator], C.byref(h)))
     return PbmState(h, index)
 
 
@@ -522,21 +530,23 @@ def pbm_debug_set_blockmax(index: PbmIndex, term: int, range_: int, value: float
 
 # ------------------------------------------------------------------ fusion
 SCHEDULES = {"doubling": 0, "frozen": 1}
+SPARSE_GENERATORS = {"pbm": 0, "complete": 1}
 
 
-def _params(K, k_rrf, w_dense, w_sparse, depth0, growth, generator="intervals", schedule="doubling"):
+def _params(K, k_rrf, w_dense, w_sparse, depth0, growth, generator="intervals", schedule="doubling",
+            sparse_generator="pbm"):
     for v in (k_rrf, w_dense, w_sparse):
         if int(v) != v:
             raise ValueError("k and the weights must be integers")
     return eahr_params(int(K), int(depth0), int(growth), int(k_rrf), int(w_dense), int(w_sparse),
-                       GENERATORS[generator], SCHEDULES[schedule])
+                       GENERATORS[generator], SCHEDULES[schedule], SPARSE_GENERATORS[sparse_generator])
 
 
 def eahr_topk(dense: Optional[PvsIndex], sparse: Optional[PbmIndex], q_dense,
               q_sparse: Sequence[Tuple[np.ndarray, np.ndarray]], K: int = 20, k_rrf: int = 60,
               w_dense: int = 1, w_sparse: int = 1, epoch: int = 0, depth0: int = 20,
               growth: int = 2, allow_failed: bool = False, dense_generator: str = "intervals",
-              schedule: str = "doubling"):
+              schedule: str = "doubling", sparse_generator: str = "pbm"):
     """Ordered Top-K of complete-list weighted RRF for a batch of queries
     (``dense_generator``: "intervals" or "full_scan", see pvs_open).
 
@@ -554,7 +564,7 @@ def eahr_topk(dense: Optional[PvsIndex], sparse: Optional[PbmIndex], q_dense,
             q, k = _sparse_query(t, w)
             qs[b] = q
             keep.append(k)
-    prm = _params(K, k_rrf, w_dense, w_sparse, depth0, growth, dense_generator, schedule)
+    prm = _params(K, k_rrf, w_dense, w_sparse, depth0, growth, dense_generator, schedule, sparse_generator)
     ids = np.full((B, max(K, 1)), -1, dtype=np.int64)
     cnt = np.zeros(B, dtype=np.int32)
     stt = np.zeros(B, dtype=np.int32)

@@ -131,3 +131,54 @@ def test_pbm_common_term_partial_publication():
     st1 = eahr.pbm_open(idx, terms, wts)
     ids, sc, status = eahr.pbm_next(st1, n + 1)
     assert status == eahr.LIST_EXHAUSTED and np.array_equal(ids, want_ids)
+
+
+# ---------------------------------------------------------------------------
+# Complete exact sparse ranking (the alternative generator of Sec. 4.4)
+
+@pytest.mark.parametrize("range_size", [7, 4096])
+def test_complete_generator_equals_oracle_and_pbm(tiny_sparse, range_size):
+    w, post, qs = tiny_sparse
+    idx = eahr.pbm_build(post.term_ptr, post.doc, post.impact, w.n, range_size)
+    for terms, wts in qs:
+        want_ids, want_s = _oracle_ranking(post, w.n, terms, wts)
+        got = []
+        gs = []
+        st = eahr.pbm_open(idx, terms, wts, generator="complete")
+        for m in (1, 19, 0, 300, 10 ** 6):
+            ids, sc, status = eahr.pbm_next(st, m)
+            assert len(ids) == m or status == eahr.LIST_EXHAUSTED
+            got.extend(ids)
+            gs.extend(sc)
+        assert status == eahr.LIST_EXHAUSTED
+        assert np.array_equal(np.array(got), want_ids)
+        assert np.array_equal(np.array(gs, np.float32), want_s)
+
+
+def test_complete_generator_reports_metadata_failure(tiny_sparse):
+    # the complete generator expands every range, so a block-max entry below
+    # its postings fails the list at the first call (App. A.2)
+    w, post, qs = tiny_sparse
+    idx = eahr.pbm_build(post.term_ptr, post.doc, post.impact, w.n, 64)
+    terms, wts = qs[1]          # the case of test_pbm_uncovered_blockmax_fails
+    t = int(terms[0])
+    r = int(post.doc[post.term_ptr[t]]) // 64
+    eahr.pbm_debug_set_blockmax(idx, t, r, 0.0)
+    st = eahr.pbm_open(idx, terms, wts, generator="complete")
+    ids, _, status = eahr.pbm_next(st, 10)
+    assert status == eahr.LIST_FAILED and len(ids) == 0
+
+
+def test_sparse_only_topk_with_complete_generator():
+    w = datagen.workload("tiny", n=5000)
+    _, lab = datagen.corpus(w)
+    post = datagen.bm25_impacts(w, datagen.sparse_docs(w, lab))
+    _, qlab = datagen.queries(w, count=5)
+    qs = datagen.sparse_queries(w, qlab)
+    idx = eahr.pbm_build(post.term_ptr, post.doc, post.impact, w.n, 512)
+    a = eahr.eahr_topk(None, idx, None, qs, K=20, w_dense=0, w_sparse=1)
+    c = eahr.eahr_topk(None, idx, None, qs, K=20, w_dense=0, w_sparse=1, sparse_generator="complete")
+    f = eahr.eahr_topk(None, idx, None, qs, K=20, w_dense=0, w_sparse=1, sparse_generator="complete",
+                       schedule="frozen")
+    assert np.array_equal(a[0], c[0]) and np.array_equal(a[1], c[1])
+    assert np.array_equal(a[0], f[0])
