@@ -64,7 +64,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="passage")
     ap.add_argument("--batch", type=int, default=256, help="queries per eahr_topk call (headline)")
-    ap.add_argument("--extra", default="1:20,64:3", help="extra batch:steps configurations")
+    ap.add_argument("--extra", default="1:200,64:3", help="extra batch:steps configurations")
     ap.add_argument("--n", type=int, default=None, help="override corpus rows (quick runs only)")
     ap.add_argument("--weights", default="1:1")
     ap.add_argument("--range-size", type=int, default=4096)
@@ -354,9 +354,12 @@ def main():
         torch.cuda.synchronize()
         t = time.perf_counter()
         res = []
+        step_ms = []
         for i in range(steps):
             a, b = batch_at(warmup + i)
+            t_step = time.perf_counter()   # eahr_topk returns host results: the step is complete
             res.append(eahr.eahr_topk(idx, pbm, a, b, K=K, w_dense=wts[0], w_sparse=wts[1]))
+            step_ms.append((time.perf_counter() - t_step) * 1e3)
         torch.cuda.synchronize()
         el = time.perf_counter() - t
         prof = eahr.pvs_profile_read()
@@ -401,6 +404,12 @@ def main():
             "host_ms": {"dense_calls": prof["host_dense_ms"], "sparse_rounds": prof["host_sparse_ms"],
                         "certify": prof["host_fuse_ms"]},
             "dense_depth": {"mean": float(dd.mean()), "median": float(np.median(dd)), "max": int(dd.max())},
+            # per-call latency (per query when the batch is 1), Sec. 3.5 reports p50/p95/p99
+            "latency_ms": {"p50": float(np.percentile(step_ms, 50)), "p95": float(np.percentile(step_ms, 95)),
+                           "p99": float(np.percentile(step_ms, 99)), "max": float(np.max(step_ms))},
+            # read ratio d_i / n_i: dense n_i = the visible rows; sparse only where the list was read to its end
+            "dense_read_ratio": {"median": float(np.median(dd) / w.n), "max": float(dd.max() / w.n)},
+            "sparse_exhausted": int(sum(s["sparse_len"] >= 0 for s in stats)),
             "sparse_depth_mean": float(np.mean([s["sparse_depth"] for s in stats])),
             "failed": int(sum(int(np.sum(r[2] != 0)) for r in res)),
         }
