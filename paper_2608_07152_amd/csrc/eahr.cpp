@@ -246,14 +246,20 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
                     if (!live(static_cast<int32_t>(b)) || exh[1][b] || have(1, b) >= H) return;
                     if (!cl.sp[b]) {
                         sparse_rc[b] = pbm_open_gen(sparse, &q_sparse[b], ep.sparse_generator, &cl.sp[b]);
-                        if (sparse_rc[b] != EAHR_OK) return;
+                        if (sparse_rc[b] != EAHR_OK) {
+                            note_sparse_error(sparse_rc[b]);
+                            return;
+                        }
                     }
                     const int64_t need = 2 * H - have(1, b);
                     sids[b].resize(static_cast<size_t>(need));
                     sscores[b].resize(static_cast<size_t>(need));
                     sparse_rc[b] = pbm_next(cl.sp[b], static_cast<int32_t>(need), sids[b].data(),
                                             sscores[b].data(), &scnt[b], &ssts[b]);
-                    if (sparse_rc[b] != EAHR_OK) return;
+                    if (sparse_rc[b] != EAHR_OK) {
+                        note_sparse_error(sparse_rc[b]);
+                        return;
+                    }
                     if (ssts[b] == EAHR_LIST_FAILED) {
                         failed[b] = 1;
                         sstat[b] = EAHR_LIST_FAILED;
@@ -262,7 +268,11 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
                     pend[1][b].insert(pend[1][b].end(), sids[b].begin(), sids[b].begin() + scnt[b]);
                     if (ssts[b] == EAHR_LIST_EXHAUSTED) exh[1][b] = 1;
                 });
-                for (int32_t b = 0; b < B; ++b) EAHR_TRY(sparse_rc[b]);
+                for (int32_t b = 0; b < B; ++b)
+                    if (sparse_rc[b] != EAHR_OK) {
+                        ::eahr::set_error("%s", sparse_err.c_str());
+                        return sparse_rc[b];
+                    }
             }
             t_sparse += ms_since(t1);
             const auto t2 = std::chrono::steady_clock::now();
