@@ -97,3 +97,31 @@ def test_passage_b64_matches_oracle(E, passage):
     assert np.all(stt == 0) and np.all(cnt == K)
     for b in (5, 63):
         check_query(E, idx, x, vn, post, q[b], qs[b], ids[b], stats[b], (1, 1))
+
+
+def test_passage_alternative_generators_match_oracle(E, passage):
+    # the rank-generator ablation (Sec. 4.4) at full size: scalar intervals
+    # with one global scale, the exhaustive float32 scan and the complete
+    # sparse ranking give the Top-20 of PVS + PBM, and that Top-20 is the
+    # oracle's for sampled queries
+    w, x, vn, post, sets, idx, pbm, s64cache = passage
+    q, qs = sets["single"]
+    t = time.time()
+    gidx = E.pvs_build_quant(x, "global")
+    note(f"global-scale index built in {time.time() - t:.1f}s")
+    ref = E.eahr_topk(idx, pbm, q[:8], qs[:8], K=K)
+    alts = {
+        "scalar": E.eahr_topk(gidx, pbm, q[:8], qs[:8], K=K),
+        "scan": E.eahr_topk(idx, pbm, q[:2], qs[:2], K=K, dense_generator="full_scan"),
+        "sparse_complete": E.eahr_topk(idx, pbm, q[:8], qs[:8], K=K, sparse_generator="complete"),
+    }
+    for name, r in alts.items():
+        n = r[0].shape[0]
+        assert np.all(r[2] == 0), name
+        assert np.array_equal(r[0], ref[0][:n]) and np.array_equal(r[1], ref[1][:n]), name
+    for b in (0, 5):
+        key = ("single", b)
+        s64cache[key] = check_query(E, idx, x, vn, post, q[b], qs[b], ref[0][b], ref[3][b], (1, 1),
+                                    s64=s64cache.get(key))
+    gidx.free()
+    note("alternative generators checked")
