@@ -280,7 +280,7 @@ def generator_ablation(eahr, torch, x, idx, pbm, qdev, sparse_q, w, K, wts, nq, 
 def main():
     args = parse()
     if args.gpus != 1:
-        print("bench.py: this build runs on one GPU; --gpus N with N > 1 is not supported",
+        print("bench.py: the library runs on one GPU; --gpus N with N > 1 is not supported",
               file=sys.stderr)
         sys.exit(2)
     if args.copy_calibration:
