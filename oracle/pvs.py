@@ -24,9 +24,15 @@ Readings where the paper is silent (each also listed in the design notes):
   a_m = (8m + 64) * 2^-23 (numerator and denominator are exact in float32).
 
 Parity: pinned by closed forms (zero vector, scaled basis vectors, exact
-half-way ties), brute-force nearest-integer search, exact-rational checks of
-gamma and of outward rounding, tightness of the residual bound, and
-containment of exact scores.
+half-way ties, dyadic inputs), brute-force nearest-integer and nearest-scale
+search, the bracket of gamma, tightness of the residual bound, containment
+of exact and float32 scores, and an exact-rational recomputation of c, E, G
+and both endpoints from the raw vectors (each within its stated number of
+float32 roundings, the endpoints exactly one ulp outward), which rejects
+planted mistakes in the guard (a dropped ||q|| ||v|| term, a_m in place of
+gamma_m, ||q_hat|| in place of ||q||, no outward step, a wrong endpoint).
+This module is test infrastructure: only the tests, the smoke check and the
+CPU baseline of the benchmark use it.
 """
 from __future__ import annotations
 
