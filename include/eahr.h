@@ -133,7 +133,10 @@ int pvs_open_gen(const pvs_index* idx, int64_t epoch, const float* q, int32_t B,
  *   status  B: EAHR_LIST_* after the call.  Failed is sticky: it is set when a
  *           rescored score lies outside its interval (App. A.1); such a query
  *           returns count 0 from then on.
- * Returns EAHR_OK even when some queries failed (see status). */
+ * Returns EAHR_OK even when some queries failed (see status).
+ * Test hook: with the environment variable EAHR_TEST_FAIL_QUERY=b set when a
+ * state is opened, rescoring judges query b's scores against a zero-width
+ * interval around c, so that query fails through this containment check. */
 int pvs_next(pvs_state* st, int32_t m, const uint8_t* active, int64_t* ids,
              float* scores, int32_t* count, int32_t* status);
 
@@ -210,9 +213,13 @@ void pvs_free(pvs_index* idx);
  * pvs_index whose rows stand for global item ids; a Shard merges the
  * rankings of its Segments, and a request merges its Shards, each by (score
  * descending, global id ascending), into one resumable ranking with the
- * pvs_next contract.  An item held by more than one Segment is emitted once
- * when its copies agree on score and version; otherwise the query's merged
- * list is Failed (sticky), as it is when a Segment's list fails. */
+ * pvs_next contract.  An item visible in more than one Segment is emitted
+ * once when its copies agree on score and version.  Copies that disagree
+ * invalidate the request whatever depth it reaches, so they are compared
+ * when the merge is opened (pvs_merge_open within a Shard, pvs_merge_shards
+ * across Shards): a version conflict fails every query, a score conflict the
+ * queries it occurs for, and such a query's merged list is Failed (sticky)
+ * from its first pvs_merge_next, as it is when a Segment's list fails. */
 typedef struct pvs_merge pvs_merge;
 
 /* pvs_merge_open -- open a Shard over n_segs Segments for B queries.

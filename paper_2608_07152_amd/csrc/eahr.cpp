@@ -481,6 +481,15 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
         }
         depth = (depth > (INT64_MAX / ep.growth)) ? INT64_MAX : depth * ep.growth;
     }
+    // a rescored score outside its interval fails its query even when the
+    // failure came from work-ahead that no pvs_next has reported yet
+    // (App. A.1: PVS fails the request)
+    if (cl.st)
+        for (int32_t b = 0; b < B; ++b)
+            if (!failed[b] && pvs_query_failed(cl.st, b)) {
+                failed[b] = 1;
+                dstat[b] = EAHR_LIST_FAILED;
+            }
     if (prof) pvs_profile_add_host(t_dense, t_sparse, t_fuse);
     if (::eahr::trace_on()) {
         const auto tc = std::chrono::steady_clock::now();

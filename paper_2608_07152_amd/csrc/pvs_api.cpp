@@ -552,6 +552,7 @@ extern "C" int pvs_open_gen(const pvs_index* ix, int64_t epoch, const float* q, 
         else if (std::strcmp(p, "mfma") == 0) st->path = pvs::ScanPath::Mfma;
     }
     if (const char* p = std::getenv("EAHR_CAP_SHRINK")) st->cap_shrink = std::max(1L, std::atol(p));
+    if (const char* p = std::getenv("EAHR_TEST_FAIL_QUERY")) st->test_fail_qi = static_cast<int32_t>(std::atol(p));
     st->n_rows = ix->snaps[epoch].rows;
     st->n_vis = ix->snaps[epoch].visible;
     st->vis = ix->snaps[epoch].vis;
@@ -986,7 +987,7 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     // 3. rescore, order and pack the certified ranks
     const int64_t chunks = pvs::rescore_chunks(h_pcnt, pair_sub);
     pvs::launch_rescore(v, st->qrows, st->scanq, d_pcnt, st->pairs, pair_sub, d_cbase, chunks,
-                        ix->gamma, st->keys, d_cert, d_fail, d_reads, s);
+                        ix->gamma, st->keys, d_cert, d_fail, d_reads, st->test_fail_qi, s);
     EAHR_TRY(mark(4));
     // only the certified keys are ordered; a query whose key region overflowed
     // (it is scanned again) keeps the region's worth
@@ -1201,6 +1202,10 @@ int pvs_fill(pvs_state* st, int64_t depth, const uint8_t* active, int64_t* added
         *added = after - before;
     }
     return EAHR_OK;
+}
+
+bool pvs_query_failed(const pvs_state* st, int32_t b) {
+    return st && b >= 0 && b < st->B && st->q[b].failed;
 }
 
 extern "C" int pvs_stats(const pvs_state* st, pvs_counters* out) {

@@ -59,6 +59,9 @@ enum class ScanPath { Auto, Gemv, Mfma };
 // sparse channel of a round is still running, so the GPU works ahead.
 // `added` (optional) receives the number of ranks certified by the call.
 int pvs_fill(pvs_state* st, int64_t depth, const uint8_t* active, int64_t* added);
+// Whether query b of a state has failed (a rescored score outside its
+// interval), also in work-ahead that pvs_next has not reported yet.
+bool pvs_query_failed(const pvs_state* st, int32_t b);
 // Batch size a merged ranking was opened for (pvs_merge.cpp).
 int32_t eahr_merge_batch(const pvs_merge* mg);
 // No rank of the merge has been returned yet (and no query failed).
@@ -166,6 +169,10 @@ struct pvs_state {
     // test knob: first-attempt key regions and pool divided by this, so that
     // the overflow and rescan paths run (results do not change)
     int64_t cap_shrink = 1;
+    // test knob (EAHR_TEST_FAIL_QUERY): this query's rescoring judges its
+    // scores against a zero-width interval, so its list fails through the
+    // normal containment check (App. A.1); -1: off
+    int32_t test_fail_qi = -1;
     hipEvent_t ev[7] = {};             // profiling events (created on first use)
     pvs::ScanQ* h_scanq = nullptr;     // pinned host mirrors
     int32_t* h_counts = nullptr;

@@ -11,9 +11,14 @@
 // every source that is still Open has a buffered head, so no unread rank of
 // any source can precede it.
 //
-// An item held by several sources (an id that occurs in more than one id
-// map) may be emitted once: a later copy with the same score and version is
-// dropped, any other copy fails the query (sticky), as does a failed source.
+// An item held by several sources (an id visible in more than one of them)
+// is emitted once: a later copy with the same score and version is dropped.
+// Copies that disagree invalidate the request whatever depth it reaches
+// (Sec. 2.4), so they are found when a merge is opened: every id visible in
+// more than one source is compared across its copies (versions for all
+// queries, authoritative scores per query), and each query with a
+// disagreeing copy is Failed from the start (sticky), as is a query whose
+// source fails.
 #include <algorithm>
 #include <cstdint>
 #include <cstring>
@@ -30,6 +35,15 @@ namespace {
 struct Item {
     int64_t id;
     float score;
+    int64_t version;
+};
+
+// A visible copy of an item: its global id, the Segment state holding it,
+// its row there and its version.
+struct Copy {
+    int64_t gid;
+    pvs_state* st;
+    int64_t row;
     int64_t version;
 };
 
@@ -55,8 +69,8 @@ struct pvs_merge {
     };
     int32_t B = 0;
     std::vector<Source> src;
-    std::vector<int64_t> ids_sorted;           // every global id of every source (for the parent)
-    std::unordered_map<int64_t, int> shared;   // ids held by more than one source
+    std::vector<Copy> copies;                  // every visible copy below this merge, by gid
+    std::unordered_map<int64_t, int> shared;   // ids visible in more than one source
     struct Query {
         bool failed = false;
         bool has_last = false;
@@ -78,18 +92,67 @@ pvs_merge::~pvs_merge() {
 
 namespace {
 
-// Ids held by more than one of the sorted id lists.
-void find_shared(pvs_merge* mg, std::vector<std::vector<int64_t>>& lists) {
-    std::vector<int64_t> all;
-    size_t total = 0;
-    for (auto& l : lists) total += l.size();
-    all.reserve(total);
-    for (auto& l : lists) all.insert(all.end(), l.begin(), l.end());
-    std::sort(all.begin(), all.end());
-    for (size_t i = 1; i < all.size(); ++i)
-        if (all[i] == all[i - 1]) mg->shared[all[i]] = 1;
-    mg->ids_sorted.swap(all);
-    mg->ids_sorted.erase(std::unique(mg->ids_sorted.begin(), mg->ids_sorted.end()), mg->ids_sorted.end());
+// Sorts the visible copies of every source of mg (already in mg->copies) by
+// global id, records the ids visible in more than one copy and fails up
+// front every query for which two copies of one id disagree: a different
+// version fails every query, a different authoritative float32 score the
+// query it differs for (the copies are scored with pvs_scores, the same
+// arithmetic that ranks them).
+int find_conflicts(pvs_merge* mg) {
+    auto& cp = mg->copies;
+    std::stable_sort(cp.begin(), cp.end(), [](const Copy& a, const Copy& b) { return a.gid < b.gid; });
+    std::vector<std::pair<size_t, size_t>> runs;   // [first, last) of ids with several copies
+    for (size_t i = 0; i < cp.size();) {
+        size_t j = i + 1;
+        while (j < cp.size() && cp[j].gid == cp[i].gid) ++j;
+        if (j - i > 1) {
+            runs.emplace_back(i, j);
+            mg->shared[cp[i].gid] = 1;
+        }
+        i = j;
+    }
+    if (runs.empty()) return EAHR_OK;
+    bool version_conflict = false;
+    for (const auto& r : runs)
+        for (size_t k = r.first + 1; k < r.second; ++k) version_conflict |= cp[k].version != cp[r.first].version;
+    if (version_conflict) {
+        for (auto& Q : mg->q) Q.failed = true;
+        return EAHR_OK;
+    }
+    // scores of every shared copy, per query: one pvs_scores call per
+    // (Segment state, query) over that state's shared rows
+    std::vector<pvs_state*> states;
+    for (const auto& r : runs)
+        for (size_t k = r.first; k < r.second; ++k) states.push_back(cp[k].st);
+    std::sort(states.begin(), states.end());
+    states.erase(std::unique(states.begin(), states.end()), states.end());
+    std::vector<std::vector<int64_t>> rows(states.size());
+    std::vector<size_t> slot(cp.size(), 0);   // copy k -> its index in its state's row list
+    for (const auto& r : runs)
+        for (size_t k = r.first; k < r.second; ++k) {
+            const size_t s = std::lower_bound(states.begin(), states.end(), cp[k].st) - states.begin();
+            slot[k] = rows[s].size();
+            rows[s].push_back(cp[k].row);
+        }
+    std::vector<std::vector<float>> sc(states.size());
+    for (int32_t b = 0; b < mg->B; ++b) {
+        if (mg->q[b].failed) continue;
+        for (size_t s = 0; s < states.size(); ++s) {
+            sc[s].resize(rows[s].size());
+            EAHR_TRY(pvs_scores(states[s], b, rows[s].data(), static_cast<int64_t>(rows[s].size()),
+                                sc[s].data()));
+        }
+        auto score_of = [&](size_t k) {
+            const size_t s = std::lower_bound(states.begin(), states.end(), cp[k].st) - states.begin();
+            return sc[s][slot[k]];
+        };
+        for (const auto& r : runs) {
+            const float s0 = score_of(r.first);
+            for (size_t k = r.first + 1; k < r.second; ++k)
+                if (!(score_of(k) == s0)) mg->q[b].failed = true;
+        }
+    }
+    return EAHR_OK;
 }
 
 int merge_next_items(pvs_merge* mg, int32_t m, const uint8_t* active, std::vector<std::vector<Item>>& out,
@@ -264,7 +327,6 @@ extern "C" int pvs_merge_open(const pvs_index* const* segs, const int64_t* epoch
     if (!mg) EAHR_FAIL(EAHR_E_OOM, "pvs_merge_open: host allocation");
     mg->B = B;
     mg->src.resize(n_segs);
-    std::vector<std::vector<int64_t>> lists(n_segs);
     for (int32_t s = 0; s < n_segs; ++s) {
         if (!segs[s] || !gids[s]) EAHR_FAIL(EAHR_E_INVALID, "pvs_merge_open: segment %d is NULL", s);
         int64_t rows = 0, vis = 0;
@@ -282,13 +344,22 @@ extern "C" int pvs_merge_open(const pvs_index* const* segs, const int64_t* epoch
                 EAHR_FAIL(EAHR_E_INVALID, "pvs_merge_open: segment %d ids not strictly ascending", s);
         }
         if (versions && versions[s]) S.version.assign(versions[s], versions[s] + erows);
-        lists[s] = S.gid;
     }
-    find_shared(mg.get(), lists);
     init_sources(mg.get());
     for (int32_t s = 0; s < n_segs; ++s)
         EAHR_TRY(pvs_open_gen(segs[s], epochs ? epochs[s] : 0, q, B, ptr_kind, EAHR_GEN_INTERVALS,
                               &mg->src[s].st));
+    // the visible rows of every Segment's snapshot
+    for (int32_t s = 0; s < n_segs; ++s) {
+        const auto& S = mg->src[s];
+        const auto& sn = segs[s]->snaps[epochs ? epochs[s] : 0];
+        std::vector<uint64_t> vis(static_cast<size_t>(std::max<int64_t>(1, (sn.rows + 63) / 64)));
+        HIP_TRY(hipMemcpy(vis.data(), sn.vis, vis.size() * sizeof(uint64_t), hipMemcpyDeviceToHost));
+        for (int64_t r = 0; r < sn.rows; ++r)
+            if ((vis[r >> 6] >> (r & 63)) & 1ull)
+                mg->copies.push_back(Copy{S.gid[r], S.st, r, S.version.empty() ? 0 : S.version[r]});
+    }
+    EAHR_TRY(find_conflicts(mg.get()));
     *out = mg.release();
     return EAHR_OK;
 }
@@ -311,13 +382,15 @@ extern "C" int pvs_merge_shards(pvs_merge** shards, int32_t n_shards, pvs_merge*
     if (!mg) EAHR_FAIL(EAHR_E_OOM, "pvs_merge_shards: host allocation");
     mg->B = B;
     mg->src.resize(n_shards);
-    std::vector<std::vector<int64_t>> lists(n_shards);
-    for (int32_t s = 0; s < n_shards; ++s) {
-        mg->src[s].child = shards[s];
-        lists[s] = shards[s]->ids_sorted;
-    }
-    find_shared(mg.get(), lists);
+    for (int32_t s = 0; s < n_shards; ++s) mg->src[s].child = shards[s];
     init_sources(mg.get());
+    // copies across Shards (each Shard has already compared its own)
+    for (int32_t s = 0; s < n_shards; ++s) {
+        const auto& c = shards[s]->copies;
+        mg->copies.insert(mg->copies.end(), c.begin(), c.end());
+    }
+    EAHR_TRY(find_conflicts(mg.get()));
+    for (int32_t s = 0; s < n_shards; ++s) std::vector<Copy>().swap(shards[s]->copies);
     mg->owns_children = true;   // the shards now belong to the request-level merge
     *out = mg.release();
     return EAHR_OK;
@@ -351,6 +424,6 @@ int32_t eahr_merge_batch(const pvs_merge* mg) { return mg ? mg->B : 0; }
 bool eahr_merge_unread(const pvs_merge* mg) {
     if (!mg) return false;
     for (const auto& q : mg->q)
-        if (q.emitted > 0 || q.failed) return false;
+        if (q.emitted > 0) return false;
     return true;
 }

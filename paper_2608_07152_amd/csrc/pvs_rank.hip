@@ -46,7 +46,8 @@ __global__ __launch_bounds__(256) void k_rescore(
     const int32_t* __restrict__ pair_cnt, const uint4* __restrict__ pairs, int64_t pair_sub,
     const float* __restrict__ scale, const float* __restrict__ vnorm,
     const float* __restrict__ enorm, float gamma, uint64_t* __restrict__ keys,
-    int32_t* __restrict__ cert_cnt, int32_t* __restrict__ fail, int32_t* __restrict__ row_reads) {
+    int32_t* __restrict__ cert_cnt, int32_t* __restrict__ fail, int32_t* __restrict__ row_reads,
+    int32_t fail_qi) {
     constexpr int PER_WAVE = kRescoreChunk / 4;
     static_assert(PER_WAVE == 64, "one record per lane");
     const int lane = threadIdx.x & 63;
@@ -75,6 +76,13 @@ __global__ __launch_bounds__(256) void k_rescore(
     float my_lo, my_hi;
     pair_interval(MQ, scale[my_row], vnorm[my_row], enorm[my_row], static_cast<int32_t>(rec.z), gamma,
                   my_lo, my_hi);
+    if (my_qi == fail_qi) {
+        // failure injection (tests only): the judged interval of this query
+        // shrinks to the ulps around c, so its scores fall outside it
+        const float c = (MQ.sq * scale[my_row]) * static_cast<float>(static_cast<int32_t>(rec.z));
+        my_lo = next_down(c);
+        my_hi = next_up(c);
+    }
     const float my_tau = MQ.tau, my_scert = MQ.s_cert;
     const int32_t my_idcert = MQ.id_cert;
     const bool my_hascert = MQ.has_cert != 0;
@@ -165,12 +173,13 @@ template <int J>
 static void rescore_j(const IndexView& ix, const float* qrows, const ScanQ* sq,
                       const int32_t* cbase, int64_t chunks, const int32_t* pair_cnt,
                       const uint4* pairs, int64_t pair_sub, float gamma, uint64_t* keys,
-                      int32_t* cert_cnt, int32_t* fail, int32_t* row_reads, hipStream_t stream) {
+                      int32_t* cert_cnt, int32_t* fail, int32_t* row_reads, int32_t fail_qi,
+                      hipStream_t stream) {
     hipLaunchKernelGGL((k_rescore<J>), dim3(static_cast<uint32_t>(chunks)), dim3(256), 0, stream,
                        reinterpret_cast<const float4*>(ix.rows), ix.df / 4,
                        reinterpret_cast<const float4*>(qrows), sq, cbase, pair_cnt, pairs,
                        pair_sub, ix.scale, ix.vnorm, ix.enorm, gamma, keys, cert_cnt, fail,
-                       row_reads);
+                       row_reads, fail_qi);
 }
 
 int64_t rescore_chunks(const int32_t* pair_cnt, int64_t pair_sub) {
@@ -185,13 +194,14 @@ int64_t rescore_chunks(const int32_t* pair_cnt, int64_t pair_sub) {
 void launch_rescore(const IndexView& ix, const float* qrows, const ScanQ* sq,
                     const int32_t* pair_cnt, const uint4* pairs, int64_t pair_sub,
                     int32_t* cbase, int64_t chunks, float gamma, uint64_t* keys,
-                    int32_t* cert_cnt, int32_t* fail, int32_t* row_reads, hipStream_t stream) {
+                    int32_t* cert_cnt, int32_t* fail, int32_t* row_reads, int32_t fail_qi,
+                    hipStream_t stream) {
     hipLaunchKernelGGL(k_chunk_base, dim3(1), dim3(64), 0, stream, pair_cnt, pair_sub, cbase);
     if (chunks <= 0) return;
 #define PVS_RS(N)                                                                              \
     case N:                                                                                    \
         rescore_j<N>(ix, qrows, sq, cbase, chunks, pair_cnt, pairs, pair_sub, gamma, keys,     \
-                     cert_cnt, fail, row_reads, stream);                                       \
+                     cert_cnt, fail, row_reads, fail_qi, stream);                              \
         break;
     switch (row_chunks(ix.df)) {
         PVS_RS(1)

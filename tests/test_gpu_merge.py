@@ -5,6 +5,7 @@ whose copies of an item disagree."""
 import numpy as np
 import pytest
 
+from oracle import dense as odense
 from paper_2608_07152_amd import datagen
 
 from gpu_helpers import check_dense_prefix
@@ -118,9 +119,59 @@ def test_copies_in_two_segments(E, case):
             assert sorted(got[b]) == list(range(400))        # each item once
             check_dense_prefix(q[b], x, got[b], sc[b])
     else:
-        assert np.all(stt == E.LIST_FAILED)                  # read to the end: the conflict is met
+        assert np.all(stt == E.LIST_FAILED)
         _, _, c, stt2 = E.pvs_merge_next(mg, 5)
         assert np.all(c == 0) and np.all(stt2 == E.LIST_FAILED)   # sticky
+        # the conflict is found when the merge is opened, not when it is read
+        mg2 = E.pvs_merge_open(segs, [a_ids, b_ids], q, versions=[np.zeros(300, np.int64), vb])
+        _, _, c, stt3 = E.pvs_merge_next(mg2, 1)
+        assert np.all(c == 0) and np.all(stt3 == E.LIST_FAILED)
+
+
+@pytest.mark.parametrize("case", ["version", "score"])
+def test_deep_conflict_fails_a_shallow_request(E, case):
+    # Sec. 2.4: conflicting copies invalidate the request, and the depth a
+    # request reads must not change its result, so a conflict far below the
+    # Top-20 still fails it (Shard level and request level alike)
+    w = datagen.workload("tiny", n=2000, d=64)
+    x, _ = datagen.corpus(w)
+    q, _ = datagen.queries(w, count=3)
+    a_ids, b_ids = np.arange(0, 1500), np.arange(1400, 2000)      # 1400..1499 in both
+    s64 = q[0].astype(np.float64) @ x.astype(np.float64).T
+    rank = np.empty(w.n, np.int64)
+    rank[np.lexsort((np.arange(w.n), -s64))] = np.arange(w.n)
+    deep = 1400 + int(np.argmax(rank[1400:1500]))                # deepest shared item for query 0
+    assert rank[deep] > 1000
+    xb = x[b_ids].copy()
+    vb = np.zeros(len(b_ids), np.int64)
+    if case == "version":
+        vb[deep - 1400] = 7
+    else:
+        xb[deep - 1400] = x[deep] * np.float32(1.0 + 2.0 ** -8)   # another score for every query
+    segs = [E.pvs_build(x[a_ids]), E.pvs_build(xb)]
+    vers = [np.zeros(len(a_ids), np.int64), vb]
+    mg = E.pvs_merge_open(segs, [a_ids, b_ids], q, versions=vers)
+    got, cnt, stt, stats = E.eahr_topk_merged(mg, None, None, len(q), K=20, w_dense=1, w_sparse=0,
+                                              allow_failed=True)
+    assert np.all(stt == E.LIST_FAILED) and np.all(cnt == 0)
+    with pytest.raises(E.EahrError) as ei:
+        E.eahr_topk_merged(E.pvs_merge_open(segs, [a_ids, b_ids], q, versions=vers), None, None,
+                           len(q), K=20, w_dense=1, w_sparse=0)
+    assert ei.value.code == E.EAHR_E_FAILED
+    # across Shards: each Shard holds one copy
+    req = E.pvs_merge_shards([E.pvs_merge_open(segs[:1], [a_ids], q, versions=vers[:1]),
+                              E.pvs_merge_open(segs[1:], [b_ids], q, versions=vers[1:])])
+    _, _, c, st2 = E.pvs_merge_next(req, 20)
+    assert np.all(c == 0) and np.all(st2 == E.LIST_FAILED)
+    # the same Segments without the conflicting copy resolve normally
+    keep = b_ids != deep
+    ok = E.pvs_merge_open([segs[0], E.pvs_build(xb[keep])], [a_ids, b_ids[keep]], q)
+    got, cnt, stt, _ = E.eahr_topk_merged(ok, None, None, len(q), K=20, w_dense=1, w_sparse=0)
+    assert np.all(stt == 0) and np.all(cnt == 20)
+    ref, rcnt, _, _ = E.eahr_topk(E.pvs_build(x), None, q, None, K=20, w_dense=1, w_sparse=0)
+    assert np.array_equal(got, ref)
+    for b in range(len(q)):
+        assert list(got[b]) == odense.dense_ranking(q[b], x)[:20].tolist()
 
 
 def test_merge_rejects_unordered_ids(E, tiny):
