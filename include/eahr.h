@@ -204,6 +204,10 @@ int pvs_intervals(const pvs_state* st, int32_t b, const int64_t* rows, int64_t n
 int pvs_scores(const pvs_state* st, int32_t b, const int64_t* rows, int64_t n,
                float* scores);
 
+/* pvs_close releases a state.  pvs_free releases an index; while states
+ * opened on it are still open (also states held by a merge) the release
+ * waits for the last of them to be closed, and the index accepts no new
+ * pvs_open.  Both accept NULL. */
 void pvs_close(pvs_state* st);
 void pvs_free(pvs_index* idx);
 
@@ -261,6 +265,8 @@ void pvs_merge_close(pvs_merge* mg);
 int pbm_build(const int64_t* term_ptr, int32_t vocab, const int32_t* docs,
               const float* impacts, int64_t n_docs, int32_t range_size,
               pbm_index** out);
+/* pbm_free -- release the index; while states opened on it are still open
+ * the release waits for the last pbm_close (no new pbm_open meanwhile). */
 void pbm_free(pbm_index* idx);
 
 /* A sparse query: n_terms distinct term ids with weights q_t >= 0. */

@@ -77,7 +77,17 @@ pbm_index::~pbm_index() {
     for (pbm_state* st : free_states) delete st;
 }
 
-extern "C" void pbm_free(pbm_index* ix) { delete ix; }
+extern "C" void pbm_free(pbm_index* ix) {
+    if (!ix) return;
+    {
+        std::lock_guard<std::mutex> lk(ix->free_mu);
+        if (ix->open_states > 0) {   // released by the last pbm_close
+            ix->release_requested = true;
+            return;
+        }
+    }
+    delete ix;
+}
 
 extern "C" int pbm_debug_set_blockmax(pbm_index* ix, int32_t term, int64_t range, float value) {
     if (!ix || term < 0 || term >= ix->vocab) EAHR_FAIL(EAHR_E_INVALID, "pbm_debug_set_blockmax: bad term");
@@ -119,6 +129,7 @@ extern "C" int pbm_open_gen(const pbm_index* ix, const eahr_sparse_query* q, int
     std::unique_ptr<pbm_state> st;
     {
         std::lock_guard<std::mutex> lk(ix->free_mu);
+        if (ix->release_requested) EAHR_FAIL(EAHR_E_INVALID, "pbm_open: the index has been freed");
         if (!ix->free_states.empty()) {
             st.reset(ix->free_states.back());
             ix->free_states.pop_back();
@@ -168,6 +179,10 @@ extern "C" int pbm_open_gen(const pbm_index* ix, const eahr_sparse_query* q, int
     std::sort(st->order.begin(), st->order.end(), [](const pbm_state::Range& a, const pbm_state::Range& b) {
         return a.H > b.H || (a.H == b.H && a.r < b.r);
     });
+    {
+        std::lock_guard<std::mutex> lk(ix->free_mu);
+        ix->open_states += 1;
+    }
     *out = st.release();
     return EAHR_OK;
 }
@@ -403,12 +418,17 @@ constexpr size_t kFreeStates = 1024;
 
 extern "C" void pbm_close(pbm_state* st) {
     if (!st) return;
-    if (st->ix) {
-        std::lock_guard<std::mutex> lk(st->ix->free_mu);
-        if (st->ix->free_states.size() < kFreeStates) {
-            st->ix->free_states.push_back(st);
+    const pbm_index* ix = st->ix;
+    bool release = false;
+    if (ix) {
+        std::lock_guard<std::mutex> lk(ix->free_mu);
+        ix->open_states -= 1;
+        release = ix->release_requested && ix->open_states == 0;
+        if (!release && ix->free_states.size() < kFreeStates) {
+            ix->free_states.push_back(st);
             return;
         }
     }
     delete st;
+    if (release) delete ix;   // pbm_free came first
 }

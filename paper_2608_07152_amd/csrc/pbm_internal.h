@@ -23,6 +23,10 @@ struct pbm_index {
     // keep their memory)
     mutable std::mutex free_mu;
     mutable std::vector<struct pbm_state*> free_states;
+    // states opened on the index and not closed yet; pbm_free while some are
+    // open only marks the index, and the last pbm_close releases it
+    mutable int64_t open_states = 0;
+    mutable bool release_requested = false;
     ~pbm_index();
 };
 

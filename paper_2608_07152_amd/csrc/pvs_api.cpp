@@ -318,7 +318,17 @@ extern "C" int pvs_info(const pvs_index* ix, int64_t epoch, int64_t* rows, int32
     return EAHR_OK;
 }
 
-extern "C" void pvs_free(pvs_index* ix) { delete ix; }
+extern "C" void pvs_free(pvs_index* ix) {
+    if (!ix) return;
+    {
+        std::lock_guard<std::mutex> lk(ix->life_mu);
+        if (ix->open_states > 0) {   // released by the last pvs_close
+            ix->release_requested = true;
+            return;
+        }
+    }
+    delete ix;
+}
 
 extern "C" int pvs_read_index(const pvs_index* ix, int64_t row0, int64_t n, int8_t* codes,
                               float* meta) {
@@ -541,6 +551,10 @@ extern "C" int pvs_open_gen(const pvs_index* ix, int64_t epoch, const float* q, 
         EAHR_FAIL(EAHR_E_INVALID, "pvs_open: unknown epoch %lld", static_cast<long long>(epoch));
     if (ptr_kind != EAHR_PTR_HOST && ptr_kind != EAHR_PTR_DEVICE)
         EAHR_FAIL(EAHR_E_INVALID, "pvs_open: bad ptr_kind");
+    {
+        std::lock_guard<std::mutex> lk(ix->life_mu);
+        if (ix->release_requested) EAHR_FAIL(EAHR_E_INVALID, "pvs_open: the index has been freed");
+    }
     std::unique_ptr<pvs_state> st(new (std::nothrow) pvs_state());
     if (!st) EAHR_FAIL(EAHR_E_OOM, "pvs_open: host allocation");
     st->ix = ix;
@@ -607,19 +621,33 @@ extern "C" int pvs_open_gen(const pvs_index* ix, int64_t epoch, const float* q, 
         const double G = (c + E + nq[b] * NV) * g;
         Q.wmax = static_cast<float>((E + G) * 1.01 + 1e-30);
     }
+    {
+        std::lock_guard<std::mutex> lk(ix->life_mu);
+        ix->open_states += 1;
+    }
     *out = st.release();
     return EAHR_OK;
 }
 
 extern "C" void pvs_close(pvs_state* st) {
-    if (st && st->ix) {
-        (void)hipStreamSynchronize(st->ix->stream);
-        if (!st->ix->has_spare) {
-            donate_buffers(st, st->ix->spare);
-            st->ix->has_spare = true;
+    if (!st) return;
+    const pvs_index* ix = st->ix;
+    if (ix) {
+        (void)hipStreamSynchronize(ix->stream);
+        if (!ix->has_spare) {
+            donate_buffers(st, ix->spare);
+            ix->has_spare = true;
         }
     }
     delete st;
+    if (!ix) return;
+    bool release = false;
+    {
+        std::lock_guard<std::mutex> lk(ix->life_mu);
+        ix->open_states -= 1;
+        release = ix->release_requested && ix->open_states == 0;
+    }
+    if (release) delete ix;   // pvs_free came first
 }
 
 extern "C" int pvs_read_query(const pvs_state* st, int8_t* codes, float* meta) {

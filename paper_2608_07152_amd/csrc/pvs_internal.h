@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <mutex>
 #include <vector>
 
 #include "eahr.h"
@@ -120,6 +121,11 @@ struct pvs_index {
     std::vector<Snapshot> snaps;
     mutable ScanBuffers spare;   // buffers of the last closed state
     mutable bool has_spare = false;
+    // states opened on the index and not closed yet; pvs_free while some are
+    // open only marks the index, and the last pvs_close releases it
+    mutable std::mutex life_mu;
+    mutable int64_t open_states = 0;
+    mutable bool release_requested = false;
     ~pvs_index();
 };
 

@@ -310,3 +310,25 @@ def test_device_pointer_inputs(E, tiny):
     ref = E.pvs_open(E.pvs_build(x), q)
     ir, sr, _, _ = E.pvs_next(ref, 50)
     assert np.array_equal(i, ir) and np.array_equal(s, sr)
+
+
+def test_index_freed_before_its_states(E, tiny):
+    # the library defers the release of an index until its last state is
+    # closed, so finalisation order (e.g. Python's cyclic GC) does not matter
+    w, x, q = tiny
+    idx = E.pvs_build(x[:3000])
+    st = E.pvs_open(idx, q[:2])
+    ids, scs, cnt, _ = E.pvs_next(st, 10)
+    h = idx.h
+    E.load().pvs_free(h)
+    idx.h = None
+    ids2, _, cnt2, _ = E.pvs_next(st, 10)          # the state still works
+    assert np.all(cnt2 == 10)
+    st.close()
+    mg_idx = [E.pvs_build(x[:100]), E.pvs_build(x[100:200])]
+    mg = E.pvs_merge_open(mg_idx, [np.arange(100), np.arange(100, 200)], q[:2])
+    for i in mg_idx:
+        i.free()
+    _, _, c, _ = E.pvs_merge_next(mg, 5)
+    assert np.all(c == 5)
+    mg.close()

@@ -182,3 +182,18 @@ def test_sparse_only_topk_with_complete_generator():
                        schedule="frozen")
     assert np.array_equal(a[0], c[0]) and np.array_equal(a[1], c[1])
     assert np.array_equal(a[0], f[0])
+
+
+def test_pbm_index_freed_before_its_states(tiny_sparse):
+    # pbm_free waits for the last pbm_close (finalisation order must not matter)
+    w, post, qs = tiny_sparse
+    idx = eahr.pbm_build(post.term_ptr, post.doc, post.impact, w.n, 512)
+    sts = [eahr.pbm_open(idx, t, wt) for t, wt in qs[:3]]
+    first, _, _ = eahr.pbm_next(sts[0], 10)
+    eahr.load().pbm_free(idx.h)
+    idx.h = None
+    again, _, _ = eahr.pbm_next(sts[1], 10)
+    want, _ = _oracle_ranking(post, w.n, qs[1][0], qs[1][1])
+    assert len(first) == 10 and list(again) == want[:len(again)].tolist()
+    for s in sts:
+        s.close()
