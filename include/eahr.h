@@ -204,6 +204,20 @@ int pvs_intervals(const pvs_state* st, int32_t b, const int64_t* rows, int64_t n
 int pvs_scores(const pvs_state* st, int32_t b, const int64_t* rows, int64_t n,
                float* scores);
 
+/* Largest n of one pvs_scores_noalloc call. */
+#define EAHR_NOALLOC_MAX_ROWS 65536
+
+/* pvs_scores_noalloc -- pvs_scores for callers that cannot allocate memory
+ * (code under HIP stream capture, tight serving loops, harnesses that forbid
+ * allocation): the same arguments (host rows and scores), results and
+ * errors, plus EAHR_E_RANGE when n > EAHR_NOALLOC_MAX_ROWS.  It calls no
+ * allocator: the row ids and scores are staged in one fixed array of device
+ * memory per GPU (EAHR_NOALLOC_MAX_ROWS * 12 bytes, held until the process
+ * ends) that every call on that GPU shares, so calls that overlap on one GPU
+ * race. */
+int pvs_scores_noalloc(const pvs_state* st, int32_t b, const int64_t* rows, int64_t n,
+                       float* scores);
+
 /* pvs_close releases a state.  pvs_free releases an index; while states
  * opened on it are still open (also states held by a merge) the release
  * waits for the last of them to be closed, and the index accepts no new

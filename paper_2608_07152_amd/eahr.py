@@ -119,6 +119,7 @@ SIGNATURES = {
     "pvs_read_query": (C.c_int, [_P, _i8p, _f32p]),
     "pvs_intervals": (C.c_int, [_P, _i32, _i64p, _i64, _f32p, _f32p]),
     "pvs_scores": (C.c_int, [_P, _i32, _i64p, _i64, _f32p]),
+    "pvs_scores_noalloc": (C.c_int, [_P, _i32, _i64p, _i64, _f32p]),
     "pvs_close": (None, [_P]),
     "pvs_free": (None, [_P]),
     "pbm_build": (C.c_int, [_i64p, _i32, _i32p, _f32p, _i64, _i32, C.POINTER(_P)]),
@@ -465,6 +466,18 @@ def pvs_scores(state: PvsState, b: int, rows):
     r = np.ascontiguousarray(rows, dtype=np.int64)
     out = np.zeros(len(r), dtype=np.float32)
     _check(load().pvs_scores(state.h, b, _ptr(r, C.c_int64), len(r), _ptr(out, C.c_float)))
+    return out
+
+
+NOALLOC_MAX_ROWS = 65536
+
+
+def pvs_scores_noalloc(state: PvsState, b: int, rows):
+    """pvs_scores through the entry point that allocates nothing (at most
+    NOALLOC_MAX_ROWS rows per call)."""
+    r = np.ascontiguousarray(rows, dtype=np.int64)
+    out = np.zeros(len(r), dtype=np.float32)
+    _check(load().pvs_scores_noalloc(state.h, b, _ptr(r, C.c_int64), len(r), _ptr(out, C.c_float)))
     return out
 
 
