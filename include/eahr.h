@@ -391,6 +391,19 @@ int eahr_fuse_lists(const int64_t* list_d, int64_t n_d, const int64_t* list_s,
                     int64_t n_s, const eahr_params* params, int32_t step,
                     int64_t* out_ids, int32_t* out_count, eahr_query_stats* stats);
 
+/* eahr_set_rank_observer -- register fn (process-wide; NULL clears) to see
+ * every rank eahr_topk and eahr_topk_merged read from their channels, for
+ * tests and tracing.  fn is called on the thread that called eahr_topk,
+ * after each read and before the read ranks are certified: `list` is 0
+ * (dense) or 1 (sparse), `first` the 0-based position of the first of the n
+ * ranks in the query's list, ids and scores the ranks themselves (valid
+ * during the call only).  Reads of a query that failed or was already
+ * resolved are not reported.  The observer adds no work to the channels
+ * and cannot change a result. */
+typedef void (*eahr_rank_observer)(void* user, int32_t query, int32_t list, int64_t first,
+                                   const int64_t* ids, const float* scores, int64_t n);
+int eahr_set_rank_observer(eahr_rank_observer fn, void* user);
+
 /* Last error message of the calling thread (static storage, never NULL). */
 const char* eahr_last_error(void);
 

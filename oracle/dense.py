@@ -26,12 +26,17 @@ def scores64(q: np.ndarray, v: np.ndarray) -> np.ndarray:
 
 
 def rank_order(scores: np.ndarray, ids: Optional[np.ndarray] = None) -> np.ndarray:
-    """Ids sorted by (score descending, id ascending).  -0.0 equals +0.0."""
+    """Ids sorted by (score descending, id ascending).  -0.0 equals +0.0.
+
+    Two stable sorts: by id, then by descending score, which keeps the id
+    order among equal scores."""
     s = np.asarray(scores, dtype=np.float64) + 0.0   # maps -0.0 to +0.0
     if ids is None:
         ids = np.arange(len(s), dtype=np.int64)
-    order = np.lexsort((ids, -s))
-    return np.asarray(ids)[order]
+    ids = np.asarray(ids)
+    by_id = np.argsort(ids, kind="stable")
+    by_score = np.argsort(-s[by_id], kind="stable")
+    return ids[by_id[by_score]]
 
 
 def dense_ranking(q: np.ndarray, v: np.ndarray, visible: Optional[np.ndarray] = None

@@ -82,6 +82,11 @@ struct TopkWork {
 std::mutex g_work_mu;
 std::vector<std::unique_ptr<TopkWork>> g_work;
 
+// eahr_set_rank_observer
+std::mutex g_obs_mu;
+eahr_rank_observer g_obs = nullptr;
+void* g_obs_user = nullptr;
+
 struct WorkLease {
     std::unique_ptr<TopkWork> w;
     WorkLease() {
@@ -119,6 +124,21 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
     const Params P{ep.K, ep.k_rrf, {ep.w_dense, ep.w_sparse}};
     const auto t_call = std::chrono::steady_clock::now();
     const int threads = host_threads();
+    eahr_rank_observer obs = nullptr;
+    void* obs_user = nullptr;
+    {
+        std::lock_guard<std::mutex> lk(g_obs_mu);
+        obs = g_obs;
+        obs_user = g_obs_user;
+    }
+    std::vector<int64_t> nobs[2];   // ranks passed to the observer per list and query
+    nobs[0].assign(B, 0);
+    nobs[1].assign(B, 0);
+    auto observe = [&](int32_t b, int list, const int64_t* ids, const float* sc, int64_t n) {
+        if (!obs || n <= 0) return;
+        obs(obs_user, b, list, nobs[list][b], ids, sc, n);
+        nobs[list][b] += n;
+    };
     const bool prof = pvs_profile_on();
     double t_dense = 0, t_sparse = 0, t_fuse = 0;
 
@@ -130,8 +150,19 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
     std::vector<int32_t> dstat(B, EAHR_LIST_EXHAUSTED), sstat(B, EAHR_LIST_EXHAUSTED);
     std::vector<int32_t> rounds(B, 0);
     std::vector<uint8_t> failed(B, 0);
+    // id range of the channels (ids are dense rows and sparse documents),
+    // which lets deep queries switch the fusion to direct rank arrays
+    int64_t universe = 0;
+    if (use_dense && !merged) {
+        int64_t rows = 0;
+        EAHR_TRY(pvs_info(dense, epoch, &rows, nullptr, nullptr));
+        universe = rows;
+    }
+    if (use_sparse) universe = std::max<int64_t>(universe, sparse->n_docs);
+    if (merged) universe = 0;   // global ids of a merge have no known range
     for (int32_t b = 0; b < B; ++b) {
         F[b].P = &P;
+        F[b].universe = universe;
         F[b].L[0].open = use_dense;
         F[b].L[1].open = use_sparse;
         if (use_dense) dstat[b] = EAHR_LIST_OPEN;
@@ -234,6 +265,7 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
                             continue;
                         }
                         const int64_t* p = ids + static_cast<size_t>(b) * m;
+                        observe(b, 0, p, sc + static_cast<size_t>(b) * m, dcnt[b]);
                         pend[0][b].insert(pend[0][b].end(), p, p + dcnt[b]);
                         if (dsts[b] == EAHR_LIST_EXHAUSTED) exh[0][b] = 1;
                     }
@@ -242,6 +274,7 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
             t_dense += ms_since(t0);
             const auto t1 = std::chrono::steady_clock::now();
             if (use_sparse) {
+                std::vector<uint8_t> sread(B, 0);
                 parallel_for(B, threads, [&](int64_t b) {
                     if (!live(static_cast<int32_t>(b)) || exh[1][b] || have(1, b) >= H) return;
                     if (!cl.sp[b]) {
@@ -266,8 +299,11 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
                         return;
                     }
                     pend[1][b].insert(pend[1][b].end(), sids[b].begin(), sids[b].begin() + scnt[b]);
+                    sread[b] = 1;
                     if (ssts[b] == EAHR_LIST_EXHAUSTED) exh[1][b] = 1;
                 });
+                for (int32_t b = 0; b < B; ++b)
+                    if (sread[b]) observe(b, 1, sids[b].data(), sscores[b].data(), scnt[b]);
                 for (int32_t b = 0; b < B; ++b)
                     if (sparse_rc[b] != EAHR_OK) {
                         ::eahr::set_error("%s", sparse_err.c_str());
@@ -422,6 +458,15 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
                 ::eahr::set_error("%s", sparse_err.c_str());
                 return sparse_rc[b];
             }
+        if (obs)
+            for (int32_t b = 0; b < B; ++b) {
+                if (F[b].resolved || failed[b]) continue;
+                if (dact[b] && dsts[b] != EAHR_LIST_FAILED)
+                    observe(b, 0, dids.p.get() + static_cast<size_t>(b) * m,
+                            dscores.p.get() + static_cast<size_t>(b) * m, dcnt[b]);
+                if (sact[b] && ssts[b] != EAHR_LIST_FAILED)
+                    observe(b, 1, sids[b].data(), sscores[b].data(), scnt[b]);
+            }
         // merge this round's ranks and certify
         const auto t0 = std::chrono::steady_clock::now();
         int64_t busy = 0;
@@ -550,6 +595,13 @@ extern "C" int eahr_topk_merged(pvs_merge* dense, const pbm_index* sparse,
                      out_count, out_status, stats);
 }
 
+extern "C" int eahr_set_rank_observer(eahr_rank_observer fn, void* user) {
+    std::lock_guard<std::mutex> lk(g_obs_mu);
+    g_obs = fn;
+    g_obs_user = user;
+    return EAHR_OK;
+}
+
 extern "C" int eahr_fuse_lists(const int64_t* list_d, int64_t n_d, const int64_t* list_s,
                                int64_t n_s, const eahr_params* params, int32_t step,
                                int64_t* out_ids, int32_t* out_count, eahr_query_stats* stats) {
@@ -567,6 +619,8 @@ extern "C" int eahr_fuse_lists(const int64_t* list_d, int64_t n_d, const int64_t
     Fusion f;
     f.P = &P;
     f.threads = host_threads();
+    for (int64_t j = 0; j < n_d; ++j) f.universe = std::max(f.universe, list_d[j] + 1);
+    for (int64_t j = 0; j < n_s; ++j) f.universe = std::max(f.universe, list_s[j] + 1);
     const int64_t* lists[2] = {list_d, list_s};
     const int64_t lens[2] = {n_d, n_s};
     for (int i = 0; i < 2; ++i) f.L[i].open = P.w[i] > 0 && lens[i] > 0;

@@ -27,6 +27,13 @@
 // the closed list with a bitmap over ids (and look up the rank in its id
 // order only for the items it holds), and repeats with a second bitmap.
 //
+// Once the lists together hold at least 1/16 of the id range [0, universe)
+// (when the caller knows it), both lists switch to direct rank arrays
+// indexed by id: an append then costs O(ranks appended) whatever the depth,
+// where a merge into the id order costs O(depth).  This keeps schedules that
+// append few ranks at a time to deep lists (checks every 16 ranks, the
+// frozen scheduler) linear in the depth reached.
+//
 // A long append (either kind) is split over `threads` host threads: the sort
 // by id digit by digit, the joins and merges over ranges of ids (equal ids
 // fall into one range), bits cleared atomically; the both-seen items are
@@ -220,6 +227,12 @@ struct Fusion {
     // closed-list mode: seen[i] has bit x set when list i holds id x
     bool bitmaps = false;
     std::vector<uint64_t> seen[2];
+    // direct mode: pos[i][x] is the 1-based rank of id x in list i (0: not
+    // in it); entered once the lists hold universe / kDirectShare ranks
+    static constexpr int64_t kDirectShare = 16;
+    int64_t universe = 0;       // ids lie in [0, universe); 0: not known
+    bool direct = false;
+    std::vector<int32_t> pos[2];
 
     static bool test_bit(const std::vector<uint64_t>& b, int64_t x) {
         const size_t w = static_cast<size_t>(x >> 6);
@@ -264,12 +277,124 @@ struct Fusion {
         dup = false;
         bitmaps = false;
         for (auto& b : seen) std::fill(b.begin(), b.end(), 0ull);
+        direct = false;
+        universe = 0;
+        for (auto& p : pos) std::vector<int32_t>().swap(p);   // only deep queries need them
+    }
+
+    void enter_direct_mode() {
+        for (int i = 0; i < 2; ++i)
+            for (int64_t x : L[i].ids) universe = std::max(universe, x + 1);
+        for (int i = 0; i < 2; ++i) {
+            pos[i].assign(static_cast<size_t>(universe), 0);
+            for (int64_t p = 0; p < L[i].size(); ++p) {
+                int32_t& r = pos[i][static_cast<size_t>(L[i].ids[p])];
+                if (r) dup = true;
+                else r = static_cast<int32_t>(p + 1);
+            }
+        }
+        direct = true;
+    }
+
+    // Ranks p0 + j + 1 (j in [j0, j1)) of list i in direct mode: repeats set
+    // the flag, both-seen items go to out.  Atomic updates when parts of one
+    // append run concurrently (the other list is not written meanwhile).
+    template <bool Atomic>
+    void direct_part(int i, const int64_t* ids, int64_t p0, int64_t j0, int64_t j1,
+                     std::vector<Scored>& out, bool& rep) {
+        List& me = L[i];
+        List& other = L[1 - i];
+        auto clear_bit = [](std::vector<uint64_t>& b, int64_t p) {
+            const uint64_t m = ~(1ull << (p & 63));
+            if (Atomic) __atomic_fetch_and(&b[static_cast<size_t>(p >> 6)], m, __ATOMIC_RELAXED);
+            else b[static_cast<size_t>(p >> 6)] &= m;
+        };
+        int32_t* mine = pos[i].data();
+        const int32_t* theirs = pos[1 - i].data();
+        for (int64_t j = j0; j < j1; ++j) {
+            const int64_t x = ids[j];
+            const int64_t rank = p0 + j + 1;
+            int32_t prev;
+            if (Atomic) {
+                prev = __atomic_exchange_n(&mine[x], static_cast<int32_t>(rank), __ATOMIC_RELAXED);
+            } else {
+                prev = mine[x];
+                if (!prev) mine[x] = static_cast<int32_t>(rank);
+            }
+            if (prev) {
+                rep = true;
+                clear_bit(me.alive, rank - 1);
+                continue;
+            }
+            const int64_t ro = theirs[x];
+            if (!ro) continue;
+            clear_bit(me.alive, rank - 1);
+            clear_bit(other.alive, ro - 1);
+            if (!fixed(x)) {
+                const int64_t r0 = (i == 0) ? rank : ro, r1 = (i == 0) ? ro : rank;
+                out.push_back(Scored{g_double(*P, 0, r0) + g_double(*P, 1, r1),
+                                     static_cast<int32_t>(r0), static_cast<int32_t>(r1), x});
+            }
+        }
+    }
+
+    void append_direct(int i, const int64_t* ids, int64_t n) {
+        List& me = L[i];
+        const int64_t p0 = me.size();
+        me.grow(n);
+        me.ids.insert(me.ids.end(), ids, ids + n);
+        int64_t xmax = -1;
+        for (int64_t j = 0; j < n; ++j) xmax = std::max(xmax, ids[j]);
+        if (xmax >= universe) {   // an id beyond the announced range
+            universe = xmax + 1;
+            for (auto& p : pos) p.resize(static_cast<size_t>(universe), 0);
+        }
+        const size_t heap0 = both.size();
+        const int parts = (threads > 1 && n >= kParallelAppend)
+                        ? static_cast<int>(std::min<int64_t>(threads, n / (kParallelAppend / 4)))
+                        : 1;
+        if (parts <= 1) {
+            bool rep = false;
+            direct_part<false>(i, ids, p0, 0, n, both, rep);
+            dup |= rep;
+        } else {
+            std::vector<std::vector<Scored>> found(static_cast<size_t>(parts));
+            std::vector<uint8_t> rep(static_cast<size_t>(parts), 0);
+            parallel_for(parts, parts, [&](int64_t t) {
+                bool r = false;
+                direct_part<true>(i, ids, p0, n * t / parts, n * (t + 1) / parts, found[t], r);
+                rep[t] = r;
+            });
+            for (int t = 0; t < parts; ++t) {
+                dup |= rep[t] != 0;
+                both.insert(both.end(), found[t].begin(), found[t].end());
+            }
+        }
+        restore_heap(heap0);
+    }
+
+    // Heap order after items were pushed behind position heap0: one push per
+    // new item, or a linear rebuild when many were added.
+    void restore_heap(size_t heap0) {
+        const size_t added = both.size() - heap0;
+        if (added > heap0 / 8) {
+            std::make_heap(both.begin(), both.end(), HeapLess{P});
+        } else {
+            for (size_t k = heap0 + 1; k <= both.size(); ++k)
+                std::push_heap(both.begin(), both.begin() + k, HeapLess{P});
+        }
     }
 
     // Append n ranks to list i (ids must be new to the list, else dup is set
     // and the bookkeeping is no longer meaningful).
     void append(int i, const int64_t* ids, int64_t n) {
         if (n <= 0) return;
+        if (!direct && universe > 0 && (L[0].size() + L[1].size() + n) * kDirectShare >= universe)
+            enter_direct_mode();
+        if (direct) {
+            append_direct(i, ids, n);
+            return;
+        }
         if (!L[1 - i].open) {
             append_closed_other(i, ids, n);
             return;
@@ -372,15 +497,7 @@ struct Fusion {
             }
         }
         me.by_id.swap(merged);
-        // restore the heap: one push per new item, or a linear rebuild when
-        // the round added many
-        const size_t added = both.size() - heap0;
-        if (added > heap0 / 8) {
-            std::make_heap(both.begin(), both.end(), HeapLess{P});
-        } else {
-            for (size_t k = heap0 + 1; k <= both.size(); ++k)
-                std::push_heap(both.begin(), both.begin() + k, HeapLess{P});
-        }
+        restore_heap(heap0);
     }
 
     // Ranks p0 + j + 1 (j in [j0, j1)) of list i while the other list is
@@ -453,13 +570,7 @@ struct Fusion {
                 both.insert(both.end(), found[t].begin(), found[t].end());
             }
         }
-        const size_t added = both.size() - heap0;
-        if (added > heap0 / 8) {
-            std::make_heap(both.begin(), both.end(), HeapLess{P});
-        } else {
-            for (size_t k = heap0 + 1; k <= both.size(); ++k)
-                std::push_heap(both.begin(), both.begin() + k, HeapLess{P});
-        }
+        restore_heap(heap0);
     }
 
     int64_t single_from(int i, int64_t p) {

@@ -97,6 +97,10 @@ _i32, _i64, _f32p = C.c_int32, C.c_int64, C.POINTER(C.c_float)
 _i64p, _i32p, _u8p, _i8p = C.POINTER(C.c_int64), C.POINTER(C.c_int32), C.POINTER(C.c_uint8), C.POINTER(C.c_int8)
 
 # name -> (restype, argtypes); mirrors include/eahr.h
+# eahr_rank_observer (include/eahr.h)
+RANK_OBSERVER = C.CFUNCTYPE(None, C.c_void_p, C.c_int32, C.c_int32, C.c_int64,
+                            C.POINTER(C.c_int64), C.POINTER(C.c_float), C.c_int64)
+
 SIGNATURES = {
     "pvs_build": (C.c_int, [_P, _i64, _i32, _i32, _P, C.POINTER(_P)]),
     "pvs_build_quant": (C.c_int, [_P, _i64, _i32, _i32, _P, _i32, C.POINTER(_P)]),
@@ -119,6 +123,7 @@ SIGNATURES = {
     "pvs_read_query": (C.c_int, [_P, _i8p, _f32p]),
     "pvs_intervals": (C.c_int, [_P, _i32, _i64p, _i64, _f32p, _f32p]),
     "pvs_scores": (C.c_int, [_P, _i32, _i64p, _i64, _f32p]),
+    "eahr_set_rank_observer": (C.c_int, [RANK_OBSERVER, _P]),
     "pvs_scores_noalloc": (C.c_int, [_P, _i32, _i64p, _i64, _f32p]),
     "pvs_close": (None, [_P]),
     "pvs_free": (None, [_P]),
@@ -629,6 +634,47 @@ def eahr_fuse_lists(list_d, list_s, K: int = 20, k_rrf: int = 60, w_dense: int =
                                   C.byref(prm), step, _ptr(out, C.c_int64), C.byref(cnt),
                                   C.byref(st)))
     return out[:cnt.value], st.as_dict()
+
+
+class RankRecorder:
+    """Context manager around eahr_set_rank_observer: records every rank the
+    fusion reads, per (query, list), as (ids, scores) arrays.
+
+        with RankRecorder() as rec:
+            eahr_topk(...)
+        ids, scores = rec.ranks(b, 0)      # dense ranks read for query b
+    """
+
+    def __init__(self):
+        self._parts = {}
+        self._cb = RANK_OBSERVER(self._record)
+
+    def _record(self, user, query, lst, first, ids, scores, n):
+        key = (int(query), int(lst))
+        parts = self._parts.setdefault(key, [])
+        have = sum(len(p[0]) for p in parts)
+        assert first == have, (key, first, have)
+        parts.append((np.ctypeslib.as_array(ids, shape=(n,)).copy(),
+                      np.ctypeslib.as_array(scores, shape=(n,)).copy()))
+
+    def __enter__(self):
+        _check(load().eahr_set_rank_observer(self._cb, None))
+        return self
+
+    def __exit__(self, *exc):
+        load().eahr_set_rank_observer(RANK_OBSERVER(), None)
+        return False
+
+    def ranks(self, query: int, lst: int):
+        parts = self._parts.get((query, lst), [])
+        if not parts:
+            return np.zeros(0, np.int64), np.zeros(0, np.float32)
+        return (np.concatenate([p[0] for p in parts]), np.concatenate([p[1] for p in parts]))
+
+
+def eahr_set_rank_observer(fn, user=None) -> None:
+    """Register a RANK_OBSERVER (or None to clear); keep fn referenced."""
+    _check(load().eahr_set_rank_observer(fn if fn is not None else RANK_OBSERVER(), user))
 
 
 def exported_symbols() -> List[str]:

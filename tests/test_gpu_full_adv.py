@@ -10,8 +10,9 @@ import pytest
 
 from paper_2608_07152_amd import datagen
 
-from full_common import K, check_query, load_library, note
-from gpu_helpers import check_dense_prefix, row_norms64, scores64
+from full_common import K, load_library, note
+from gpu_helpers import (check_dense_prefix, check_fusion_run, for_each_parallel, full_order,
+                         row_norms64, score_matrix, scores64)
 
 pytestmark = pytest.mark.gpu
 
@@ -37,17 +38,33 @@ def adv(E):
     pbm.free()
 
 
-def test_adversarial_topk_exhausts_both_lists(E, adv):
+def test_adversarial_every_query_exhausts_both_lists(E, adv):
+    """All 100 queries: both lists run to exhaustion, the complete 2M-entry
+    dense ranking the fusion read is the oracle's, the complete sparse
+    ranking is the reversal, and the Top-20 is the complete-list RRF."""
     w, x, vn, q, post, qs, idx, pbm = adv
     t = time.time()
-    ids, cnt, stt, stats = E.eahr_topk(idx, pbm, q, qs, K=K)
+    with E.RankRecorder() as rec:
+        ids, cnt, stt, stats = E.eahr_topk(idx, pbm, q, qs, K=K)
     note(f"adversarial eahr_topk on {len(q)} queries: {time.time() - t:.2f}s")
     assert np.all(stt == 0) and np.all(cnt == K)
     for s in stats:
         assert s["dense_status"] == E.LIST_EXHAUSTED and s["sparse_status"] == E.LIST_EXHAUSTED
         assert s["dense_depth"] == w.n and s["sparse_depth"] == w.n
-    for b in (0, 99):
-        check_query(E, idx, x, vn, post, q[b], qs[b], ids[b], stats[b], (1, 1))
+    t = time.time()
+    S = score_matrix(q, x)
+
+    def one(b):
+        full = full_order(S[b])
+        dense = rec.ranks(b, 0)
+        check_fusion_run(q[b], x, vn, post, qs[b], ids[b], cnt[b], stats[b], dense, rec.ranks(b, 1),
+                         (1, 1), S[b], full=full, K=K)
+        # exhaustion leaves no room for near-tie slack at the ends: the
+        # complete list read is a permutation of every row
+        assert np.array_equal(np.sort(dense[0]), np.arange(w.n))
+
+    for_each_parallel(one, range(len(q)))
+    note(f"adversarial: every query checked in {time.time() - t:.1f}s")
 
 
 def test_adversarial_complete_dense_ranking(E, adv):

@@ -197,3 +197,23 @@ def test_pbm_index_freed_before_its_states(tiny_sparse):
     assert len(first) == 10 and list(again) == want[:len(again)].tolist()
     for s in sts:
         s.close()
+
+
+@pytest.mark.parametrize("schedule", ["doubling", "frozen"])
+def test_rank_observer_sees_the_ranks_read(tiny_sparse, schedule):
+    # the observer reports every rank a fusion reads, in list order, and
+    # does not change the result (sparse-only fusion runs on the host)
+    w, post, qs = tiny_sparse
+    idx = eahr.pbm_build(post.term_ptr, post.doc, post.impact, w.n, 512)
+    plain = eahr.eahr_topk(None, idx, None, qs, K=20, w_dense=0, w_sparse=1, schedule=schedule)
+    with eahr.RankRecorder() as rec:
+        got = eahr.eahr_topk(None, idx, None, qs, K=20, w_dense=0, w_sparse=1, schedule=schedule)
+    after = eahr.eahr_topk(None, idx, None, qs, K=20, w_dense=0, w_sparse=1, schedule=schedule)
+    assert np.array_equal(plain[0], got[0]) and np.array_equal(plain[0], after[0])
+    for b, (t, wt) in enumerate(qs):
+        ids, scores = rec.ranks(b, 1)
+        want, wscores = _oracle_ranking(post, w.n, t, wt)
+        assert len(ids) >= got[3][b]["sparse_depth"] > 0
+        assert np.array_equal(ids, want[:len(ids)])
+        assert np.array_equal(scores.view(np.int32), wscores[:len(ids)].view(np.int32))
+        assert len(rec.ranks(b, 0)[0]) == 0
