@@ -73,6 +73,8 @@ def parse():
     ap.add_argument("--no-ablation", action="store_true",
                     help="skip the rank-generator ablation (global-scale scalar quantisation vs PVS)")
     ap.add_argument("--ablation-queries", type=int, default=20)
+    ap.add_argument("--no-streams", action="store_true",
+                    help="skip the controlled rank-stream experiment (host only)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MB")
     return ap.parse_args()
 
@@ -277,6 +279,38 @@ def generator_ablation(eahr, torch, x, idx, pbm, qdev, sparse_q, w, K, wts, nq, 
             "single_requests": single, "batch": batched}
 
 
+def controlled_streams(eahr, datagen, K=20, check_every=16):
+    """The controlled rank streams of Sec. 3.4 through eahr_fuse_lists: 3
+    sizes x 5 relationships x 3 seeds, both lists advancing together with a
+    check every 16 ranks.  Per instance: the first checkpoint at which the
+    ordered Top-20 is fixed, the read ratio (that depth / n) and whether a
+    list was read to its end (Sec. 4.2 reports the same three)."""
+    import numpy as np
+    out = {}
+    t0 = time.perf_counter()
+    for rel in datagen.STREAM_RELATIONS:
+        inst = []
+        for n in datagen.STREAM_SIZES:
+            for seed in datagen.STREAM_SEEDS:
+                a, b = datagen.controlled_streams(rel, n, seed)
+                t = time.perf_counter()
+                _, st = eahr.eahr_fuse_lists(a, b, K=K, step=check_every)
+                el = time.perf_counter() - t
+                d = max(st["dense_depth"], st["sparse_depth"])
+                inst.append({"n": n, "seed": seed, "first_resolved_depth": d, "read_ratio": d / n,
+                             "exhausted": st["dense_status"] == eahr.LIST_EXHAUSTED
+                             or st["sparse_status"] == eahr.LIST_EXHAUSTED,
+                             "fuse_ms": el * 1e3})
+        d = [i["first_resolved_depth"] for i in inst]
+        r = [i["read_ratio"] for i in inst]
+        out[rel] = {"median_depth": float(np.median(d)), "read_ratio_min": min(r), "read_ratio_max": max(r),
+                    "exhausted": sum(i["exhausted"] for i in inst), "instances": inst}
+        log(f"streams {rel}: median depth {np.median(d):.0f}, read ratio {min(r):.4f}-{max(r):.4f}, "
+            f"exhausted {out[rel]['exhausted']}/{len(inst)}")
+    out["seconds"] = time.perf_counter() - t0
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -448,6 +482,8 @@ def main():
     }
     if ablation is not None:
         line["ablation"] = ablation
+    if not args.no_streams:
+        line["controlled_streams"] = controlled_streams(eahr, datagen)
     if not args.no_cpu_baseline:
         bsz = configs[0][0]
         name = query_set_for(w, bsz)

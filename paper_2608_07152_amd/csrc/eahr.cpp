@@ -621,6 +621,9 @@ extern "C" int eahr_fuse_lists(const int64_t* list_d, int64_t n_d, const int64_t
     f.threads = host_threads();
     for (int64_t j = 0; j < n_d; ++j) f.universe = std::max(f.universe, list_d[j] + 1);
     for (int64_t j = 0; j < n_s; ++j) f.universe = std::max(f.universe, list_s[j] + 1);
+    // both lists are given whole, so their id range is exact: direct rank
+    // arrays from the start keep small steps linear in the depth
+    f.enter_direct_mode();
     const int64_t* lists[2] = {list_d, list_s};
     const int64_t lens[2] = {n_d, n_s};
     for (int i = 0; i < 2; ++i) f.L[i].open = P.w[i] > 0 && lens[i] > 0;

@@ -472,3 +472,47 @@ def temporal_docs(w: Workload, labels_all: np.ndarray, base_n: int) -> SparseDoc
         parts.append(_draw_docs(w, lab, S_TEMPORAL_DOCS, c, topics, zipf))
         offs.append(base_n + c * CHUNK_ROWS)
     return _merge_chunks(w.vocab, parts, len(labels_all), offs)
+
+
+# --------------------------------------------------------------------------
+# controlled rank streams (Sec. 3.4)
+# --------------------------------------------------------------------------
+STREAM_SIZES = (100_000, 1_000_000, 5_000_000)
+STREAM_SEEDS = (1729, 2027, 65537)
+STREAM_RELATIONS = ("correlated", "partial", "independent", "anti", "all_tied")
+
+
+def controlled_streams(relation: str, n: int, seed: int) -> Tuple[np.ndarray, np.ndarray]:
+    """Two complete rankings of the ids 0..n-1 with a given relationship:
+    the first list is a random permutation (except all-tied); the second
+    permutes it inside contiguous blocks of 32 ("correlated"), takes 500
+    random items of the first list's top 1,000 and the 500 items that follow
+    that top 1,000 in the first list, shuffled, as its own top 1,000, followed
+    by the other items in the first list's order ("partial"), is an
+    independent permutation ("independent") or the
+    reversed first list ("anti").  All-tied: every item scores the same in
+    both lists, so both are identifier order."""
+    rng = np.random.default_rng(seed)
+    if relation == "all_tied":
+        ids = np.arange(n, dtype=np.int64)
+        return ids, ids.copy()
+    a = rng.permutation(n).astype(np.int64)
+    if relation == "correlated":
+        order = np.lexsort((rng.random(n), np.arange(n) // 32))
+        b = a[order]
+    elif relation == "partial":
+        top = min(1000, n)
+        half = top // 2
+        inside = rng.choice(a[:top], size=half, replace=False)
+        outside = a[top:top + (top - half)]
+        head = rng.permutation(np.concatenate([inside, outside]))
+        used = np.zeros(n, dtype=bool)
+        used[head] = True
+        b = np.concatenate([head, a[~used[a]]])
+    elif relation == "independent":
+        b = rng.permutation(n).astype(np.int64)
+    elif relation == "anti":
+        b = a[::-1].copy()
+    else:
+        raise ValueError(f"unknown stream relation {relation!r}")
+    return a, b.astype(np.int64)

@@ -56,28 +56,48 @@ def test_fuse_lists_stops_where_reference_first_resolves(seed):
     assert list(got) == A
 
 
-def test_fuse_lists_controlled_correlated_streams():
+@pytest.mark.parametrize("relation", list(datagen.STREAM_RELATIONS))
+def test_controlled_stream_instances(relation):
+    # the controlled rank streams of Sec. 3.4 (3 sizes x 3 seeds per
+    # relation, both lists advancing together, a check every 16 ranks):
+    # correlated and all-tied streams first resolve at depth 32 at every
+    # size, anti-correlated streams exhaust both lists (Sec. 4.2, pinned in
+    # tests/golden), and every fused Top-20 is the complete-list RRF
     g = json.load(open(os.path.join(GOLDEN, "e5_controlled_streams.json")))
-    want = g["outcomes"]["correlated_32_block_permutation"]["first_resolved_depth"]
-    for n in g["sizes"]:
-        for seed in g["seeds"]:
-            rng = np.random.default_rng(seed)
-            a = rng.permutation(n)
-            order = np.lexsort((rng.random(n), np.arange(n) // g["block"]))
-            b = a[order]
+    assert list(datagen.STREAM_SIZES) == g["sizes"] and list(datagen.STREAM_SEEDS) == g["seeds"]
+    for n in datagen.STREAM_SIZES:
+        for seed in datagen.STREAM_SEEDS:
+            a, b = datagen.controlled_streams(relation, n, seed)
             got, st = eahr.eahr_fuse_lists(a, b, K=g["K"], step=g["check_every"])
-            assert st["dense_depth"] == want and st["sparse_depth"] == want
-            assert list(got) == rrf.rrf_topk([a, b], [1, 1], 60, g["K"])
+            if relation in ("correlated", "all_tied"):
+                want = g["outcomes"]["correlated_32_block_permutation"]["first_resolved_depth"]
+                assert st["dense_depth"] == want and st["sparse_depth"] == want
+            if relation == "anti":
+                assert st["dense_status"] == eahr.LIST_EXHAUSTED and st["sparse_status"] == eahr.LIST_EXHAUSTED
+                assert st["dense_depth"] == n and st["sparse_depth"] == n
+            else:
+                assert st["dense_status"] == eahr.LIST_OPEN and st["sparse_status"] == eahr.LIST_OPEN
+            assert st["dense_depth"] == st["sparse_depth"] and st["dense_depth"] % g["check_every"] == 0 \
+                or st["dense_depth"] == n
+            assert list(got) == rrf.rrf_topk([a, b], [1, 1], 60, g["K"]), (relation, n, seed)
 
 
-def test_fuse_lists_anticorrelated_streams_exhaust_both():
-    for n, seed in ((100_000, 1729), (30_000, 2027)):
-        rng = np.random.default_rng(seed)
-        a = rng.permutation(n)
-        got, st = eahr.eahr_fuse_lists(a, a[::-1], K=20, step=16)
-        assert st["dense_status"] == eahr.LIST_EXHAUSTED and st["sparse_status"] == eahr.LIST_EXHAUSTED
-        assert st["dense_depth"] == n and st["sparse_depth"] == n
-        assert list(got) == rrf.rrf_topk([a, a[::-1]], [1, 1], 60, 20)
+def test_controlled_stream_generator_shapes():
+    n = 5000
+    for rel in datagen.STREAM_RELATIONS:
+        a, b = datagen.controlled_streams(rel, n, 1729)
+        assert sorted(a.tolist()) == list(range(n)) == sorted(b.tolist())
+    a, b = datagen.controlled_streams("correlated", n, 1729)
+    assert all(set(a[i:i + 32]) == set(b[i:i + 32]) for i in range(0, n, 32))
+    a, b = datagen.controlled_streams("partial", n, 1729)
+    assert len(set(a[:1000]) & set(b[:1000])) == 500
+    assert set(b[:1000]) - set(a[:1000]) == set(a[1000:1500])
+    rest = [x for x in a if x not in set(b[:1000])]
+    assert list(b[1000:]) == rest
+    a, b = datagen.controlled_streams("anti", n, 1729)
+    assert np.array_equal(b, a[::-1])
+    a, b = datagen.controlled_streams("all_tied", n, 1729)
+    assert np.array_equal(a, np.arange(n)) and np.array_equal(b, np.arange(n))
 
 
 def test_fuse_lists_no_padding_and_zero_weight():
