@@ -73,6 +73,9 @@ def parse():
     ap.add_argument("--no-ablation", action="store_true",
                     help="skip the rank-generator ablation (global-scale scalar quantisation vs PVS)")
     ap.add_argument("--ablation-queries", type=int, default=20)
+    ap.add_argument("--configs", default="weights21,mid,adv,temporal",
+                    help="further configurations (comma-separated): weights21 (the passage batch at "
+                         "weights 2:1), mid, adv, temporal; empty for none")
     ap.add_argument("--no-streams", action="store_true",
                     help="skip the controlled rank-stream experiment (host only)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MB")
@@ -132,8 +135,88 @@ def copy_calibration(mb):
     print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n, "copies": 10}), flush=True)
 
 
-def cpu_baseline(x, post, q, qs, K, wts, n_queries):
-    """Time the oracle on the first n_queries of the batch."""
+def step_summary(eahr, prof, res, d, n_visible, bsz, steps, el, step_ms):
+    """Throughput, kernel classes with their algorithmic bytes, and the
+    per-query work counters of a timed series of eahr_topk calls."""
+    import numpy as np
+    # dominant scan kernel variant = most total scan time
+    vms = prof["variant_ms"]
+    v = max(range(len(vms)), key=lambda i: vms[i])
+    launches = max(1, prof["variant_launches"][v])
+    avg_ms = vms[v] / launches
+    bpl = prof["variant_bytes"][v] / launches
+    achieved = bpl / (avg_ms * 1e-3) / 1e9 if avg_ms > 0 else 0.0
+    variants = {eahr.pvs_profile.VARIANTS[i]: {"ms": vms[i], "launches": prof["variant_launches"][i]}
+                for i in range(len(vms)) if prof["variant_launches"][i]}
+    # every kernel class with its algorithmic bytes
+    kernels = {}
+    for i, name in enumerate(eahr.pvs_profile.VARIANTS):
+        if prof["variant_launches"][i]:
+            ms, n = vms[i], prof["variant_launches"][i]
+            kernels[name] = {"ms": ms, "launches": n, "bytes": prof["variant_bytes"][i],
+                             "gbs": prof["variant_bytes"][i] / (ms * 1e-3) / 1e9 if ms > 0 else 0.0}
+    if prof["scan_rounds"]:
+        rb = (prof["rescore_row_reads"] * (4 * d + 12) + prof["rescore_rows"] * 16
+              + prof["rescore_certified"] * 8)
+        ms = prof["rescore_ms"]
+        kernels["rescore"] = {"ms": ms, "launches": prof["scan_rounds"], "bytes": rb,
+                              "gbs": rb / (ms * 1e-3) / 1e9 if ms > 0 else 0.0}
+    dom = max(kernels, key=lambda k: kernels[k]["ms"])
+    kernels["sort_pack"] = {"ms": prof["sort_ms"], "launches": prof["scan_rounds"]}
+    kernels["sample_select"] = {"ms": prof["sample_ms"], "launches": prof["scan_rounds"]}
+    stats = [s for r in res for s in r[3]]
+    dd = np.array([s["dense_depth"] for s in stats])
+    kms = prof["scan_ms"] + prof["sample_ms"] + prof["rescore_ms"] + prof["sort_ms"]
+    return {
+        "batch": bsz, "steps": steps, "queries_per_s": steps * bsz / el,
+        "ms_per_step": el / steps * 1e3,
+        "scan_kernel": eahr.pvs_profile.VARIANTS[v],
+        "scan_gbs": achieved, "scan_frac": achieved / HBM_PEAK_GBS, "scan_avg_launch_ms": avg_ms,
+        "scan_launches": launches, "scan_bytes_per_launch": bpl, "scan_variants": variants,
+        "kernels": kernels, "dominant": dom,
+        "kernel_ms": {"scan": prof["scan_ms"], "sample_select": prof["sample_ms"],
+                      "rescore": prof["rescore_ms"], "sort_pack": prof["sort_ms"]},
+        # share of the wall time the GPU spent in the dense channel's kernels
+        "gpu_busy_frac": kms / (el * 1e3) if el > 0 else 0.0,
+        "rescored_pairs": prof["rescore_rows"], "rescore_row_reads": prof["rescore_row_reads"],
+        "host_ms": {"dense_calls": prof["host_dense_ms"], "sparse_rounds": prof["host_sparse_ms"],
+                    "certify": prof["host_fuse_ms"]},
+        "dense_depth": {"mean": float(dd.mean()), "median": float(np.median(dd)), "max": int(dd.max())},
+        # per-call latency (per query when the batch is 1), Sec. 3.5 reports p50/p95/p99
+        "latency_ms": {"p50": float(np.percentile(step_ms, 50)), "p95": float(np.percentile(step_ms, 95)),
+                       "p99": float(np.percentile(step_ms, 99)), "max": float(np.max(step_ms))},
+        # read ratio d_i / n_i: dense n_i = the visible rows; sparse only where the list was read to its end
+        "dense_read_ratio": {"median": float(np.median(dd) / n_visible), "max": float(dd.max() / n_visible)},
+        "sparse_exhausted": int(sum(s["sparse_len"] >= 0 for s in stats)),
+        "sparse_depth_mean": float(np.mean([s["sparse_depth"] for s in stats])),
+        # work counters of Sec. 3.5 per query (medians)
+        "dense_f32_evals_median": float(np.median([s["dense_evals"] for s in stats])),
+        "sparse_postings_median": float(np.median([s["sparse_postings"] for s in stats])),
+        "sparse_scored_median": float(np.median([s["sparse_scored"] for s in stats])),
+        "failed": int(sum(int(np.sum(r[2] != 0)) for r in res)),
+    }
+
+
+def cpu_host_info():
+    """Usable host cores and the CPU model (the oracle baseline's machine)."""
+    cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return cores, model
+
+
+def cpu_baseline(x, post, q, qs, K, wts, n_queries, visible=None):
+    """Time the oracle (exhaustive float64 dense ranking streamed in 1M-row
+    chunks, brute-force sparse scores, exact complete-list RRF) on the first
+    n_queries of a batch; returns the Top-K lists, seconds and the threads the
+    oracle's float64 products ran on."""
     import numpy as np
     from oracle import dense as odense
     from oracle import rrf as orrf
@@ -146,14 +229,125 @@ def cpu_baseline(x, post, q, qs, K, wts, n_queries):
     out = []
     t = time.perf_counter()
     step = 1 << 20
+    ids = np.arange(len(x), dtype=np.int64)
+    if visible is not None:
+        ids = ids[visible]
     for b in range(n_queries):
         s64 = np.concatenate([odense.scores64(q[b], x[r:r + step]) for r in range(0, len(x), step)])
-        dense_list = odense.rank_order(s64)
-        S = osparse.sparse_scores(post.term_ptr, post.doc, post.impact, qs[b][0], qs[b][1], len(x))
+        dense_list = odense.rank_order(s64[ids], ids)
+        S = osparse.sparse_scores(post.term_ptr, post.doc, post.impact, qs[b][0], qs[b][1], len(x),
+                                  visible)
         sparse_list = osparse.sparse_ranking(S)
         out.append(orrf.rrf_topk([dense_list, sparse_list], list(wts), 60, K))
     el = time.perf_counter() - t
     return out, el, blas
+
+
+def cpu_baseline_entry(n, el, threads, what):
+    cores, model = cpu_host_info()
+    return {"value": n / el, "unit": "queries/s", "cores": threads, "host_cores": cores,
+            "cpu_model": model, "kind": "oracle", "seconds": el, "sample": what}
+
+
+def bench_workload(name, eahr, torch, datagen, K, steps, warmup, cpu_queries, wts=(1, 1)):
+    """One further configuration of the workload table: its own corpus,
+    index and query batch (one eahr_topk call per step on all its queries),
+    kernel rooflines, work counters, and the oracle on a few queries (timed
+    as a CPU baseline and compared with the GPU's Top-K)."""
+    import numpy as np
+    t0 = time.perf_counter()
+    w = datagen.workload(name)
+    x, lab = datagen.corpus(w)
+    q, qlab = datagen.queries(w)
+    epochs = [(0, None)]
+    if name == "temporal":
+        steps_ = list(datagen.temporal_steps(w, w.n))
+        x = np.concatenate([x] + [st.insert_rows for st in steps_])
+        lab = np.concatenate([lab] + [st.insert_labels for st in steps_])
+        docs = datagen.temporal_docs(w, lab, w.n)
+    elif not w.adversarial:
+        docs = datagen.sparse_docs(w, lab)
+    idx = eahr.pvs_build(x[:w.n])
+    if name == "temporal":
+        vis = np.zeros(len(x), dtype=bool)
+        vis[:w.n] = True
+        epochs = [(0, vis.copy())]
+        rows = w.n
+        for st in steps_:
+            eahr.pvs_delete(idx, st.delete_ids)
+            eahr.pvs_insert(idx, st.insert_rows)
+            vis[st.delete_ids] = False
+            vis[rows:rows + len(st.insert_rows)] = True
+            rows += len(st.insert_rows)
+            epochs.append((eahr.pvs_snapshot(idx), vis.copy()))
+    if w.adversarial:
+        post, qs = datagen.adversarial_postings(w, x, q)
+        posts = [post]
+    elif name == "temporal":
+        qs = datagen.sparse_queries(w, qlab)
+        posts = [datagen.bm25_impacts(w, docs, v) for _, v in epochs]
+    else:
+        qs = datagen.sparse_queries(w, qlab)
+        posts = [datagen.bm25_impacts(w, docs)]
+    pbms = [eahr.pbm_build(p.term_ptr, p.doc, p.impact, len(x), 4096) for p in posts]
+    qd = torch.from_numpy(q).cuda()
+    torch.cuda.synchronize()
+    log(f"{name}: set up in {time.perf_counter() - t0:.1f}s ({len(x)} rows, {len(q)} queries)")
+    # temporal: warm up on S0, then one timed step per snapshot S1..S5
+    runs = [(e, pbms[i]) for i, (e, _) in enumerate(epochs)] if name == "temporal" else None
+
+    def call(i):
+        if runs is not None:
+            e, pb = runs[i]
+            return eahr.eahr_topk(idx, pb, qd, qs, K=K, w_dense=wts[0], w_sparse=wts[1], epoch=e)
+        return eahr.eahr_topk(idx, pbms[0], qd, qs, K=K, w_dense=wts[0], w_sparse=wts[1])
+
+    if runs is not None:
+        warm, timed = [0], list(range(1, len(runs)))
+    else:
+        warm, timed = [0] * warmup, [0] * steps
+    for i in warm:
+        call(i)
+    eahr.pvs_profile_enable(True)
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    res, step_ms = [], []
+    for i in timed:
+        ts = time.perf_counter()
+        res.append(call(i))
+        step_ms.append((time.perf_counter() - ts) * 1e3)
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t
+    prof = eahr.pvs_profile_read()
+    eahr.pvs_profile_enable(False)
+    n_vis = float(np.mean([eahr.pvs_info(idx, e)[2] for e, _ in (epochs[1:] if runs else epochs)]))
+    out = step_summary(eahr, prof, res, w.d, n_vis, len(q), len(timed), el, step_ms)
+    out["workload"] = (f"{name} N={w.n} d={w.d} centers={w.centers} queries={len(q)} K={K} k=60 "
+                       f"weights={wts[0]}:{wts[1]}" + (" snapshots S1-S5 (one step each)"
+                                                         if runs else ""))
+    out["roofline"] = roofline_of(out["dominant"], out["kernels"][out["dominant"]])
+    out["roofline_scan"] = roofline_of(out["scan_kernel"], out["kernels"][out["scan_kernel"]])
+    log(f"{name}: {out['queries_per_s']:.1f} q/s, dominant {out['dominant']} "
+        f"{out['roofline']['frac']:.2f} of HBM, scan {out['scan_kernel']} {out['scan_frac']:.2f}")
+    if cpu_queries > 0:
+        last_e, last_vis = (epochs[-1] if runs else epochs[0])
+        post = posts[-1]
+        want, cel, threads = cpu_baseline(x, post, q, qs, K, wts, cpu_queries, last_vis)
+        ids, cnt, _, _ = res[-1]
+        match = sum(list(ids[b, :cnt[b]]) == want[b] for b in range(cpu_queries))
+        out["cpu_baseline"] = cpu_baseline_entry(
+            cpu_queries, cel, threads,
+            f"{cpu_queries} queries of the batch" + (" on snapshot S5" if runs else "")
+            + " over every visible row (exhaustive fp64 dense sort, brute-force sparse, exact RRF)")
+        out["oracle_check"] = {"queries": cpu_queries, "top20_equal": int(match)}
+        log(f"{name}: cpu oracle {cel:.1f}s, {match}/{cpu_queries} Top-20 equal")
+    for pb in pbms:
+        eahr.pbm_free(pb)
+    eahr.pvs_free(idx)
+    del qd
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return out
 
 
 def roofline_of(name, k):
@@ -370,7 +564,8 @@ def main():
     qdev = {name: torch.from_numpy(q).cuda() for name, (q, _) in qsets.items()}
     torch.cuda.synchronize()
 
-    def run_config(bsz, steps, warmup):
+    def run_config(bsz, steps, warmup, weights=None):
+        wts_ = weights or wts
         name = query_set_for(w, bsz)
         qd, qs = qdev[name], sparse_q[name]
         pool = qd.shape[0]
@@ -383,7 +578,7 @@ def main():
 
         for i in range(warmup):
             a, b = batch_at(i)
-            eahr.eahr_topk(idx, pbm, a, b, K=K, w_dense=wts[0], w_sparse=wts[1])
+            eahr.eahr_topk(idx, pbm, a, b, K=K, w_dense=wts_[0], w_sparse=wts_[1])
         eahr.pvs_profile_enable(True)
         torch.cuda.synchronize()
         t = time.perf_counter()
@@ -392,62 +587,14 @@ def main():
         for i in range(steps):
             a, b = batch_at(warmup + i)
             t_step = time.perf_counter()   # eahr_topk returns host results: the step is complete
-            res.append(eahr.eahr_topk(idx, pbm, a, b, K=K, w_dense=wts[0], w_sparse=wts[1]))
+            res.append(eahr.eahr_topk(idx, pbm, a, b, K=K, w_dense=wts_[0], w_sparse=wts_[1]))
             step_ms.append((time.perf_counter() - t_step) * 1e3)
         torch.cuda.synchronize()
         el = time.perf_counter() - t
         prof = eahr.pvs_profile_read()
         eahr.pvs_profile_enable(False)
-        # dominant scan kernel variant = most total scan time
-        vms = prof["variant_ms"]
-        v = max(range(len(vms)), key=lambda i: vms[i])
-        launches = max(1, prof["variant_launches"][v])
-        avg_ms = vms[v] / launches
-        bpl = prof["variant_bytes"][v] / launches
-        achieved = bpl / (avg_ms * 1e-3) / 1e9 if avg_ms > 0 else 0.0
-        variants = {eahr.pvs_profile.VARIANTS[i]: {"ms": vms[i], "launches": prof["variant_launches"][i]}
-                    for i in range(len(vms)) if prof["variant_launches"][i]}
-        # every kernel class with its algorithmic bytes
-        kernels = {}
-        for i, name in enumerate(eahr.pvs_profile.VARIANTS):
-            if prof["variant_launches"][i]:
-                ms, n = vms[i], prof["variant_launches"][i]
-                kernels[name] = {"ms": ms, "launches": n, "bytes": prof["variant_bytes"][i],
-                                 "gbs": prof["variant_bytes"][i] / (ms * 1e-3) / 1e9 if ms > 0 else 0.0}
-        if prof["scan_rounds"]:
-            rb = (prof["rescore_row_reads"] * (4 * w.d + 12) + prof["rescore_rows"] * 16
-                  + prof["rescore_certified"] * 8)
-            ms = prof["rescore_ms"]
-            kernels["rescore"] = {"ms": ms, "launches": prof["scan_rounds"], "bytes": rb,
-                                  "gbs": rb / (ms * 1e-3) / 1e9 if ms > 0 else 0.0}
-        dom = max(kernels, key=lambda k: kernels[k]["ms"])
-        kernels["sort_pack"] = {"ms": prof["sort_ms"], "launches": prof["scan_rounds"]}
-        kernels["sample_select"] = {"ms": prof["sample_ms"], "launches": prof["scan_rounds"]}
-        stats = [s for r in res for s in r[3]]
-        dd = np.array([s["dense_depth"] for s in stats])
-        out = {
-            "batch": bsz, "steps": steps, "queries_per_s": steps * bsz / el,
-            "ms_per_step": el / steps * 1e3,
-            "scan_kernel": eahr.pvs_profile.VARIANTS[v],
-            "scan_gbs": achieved, "scan_frac": achieved / HBM_PEAK_GBS, "scan_avg_launch_ms": avg_ms,
-            "scan_launches": launches, "scan_bytes_per_launch": bpl, "scan_variants": variants,
-            "kernels": kernels, "dominant": dom,
-            "kernel_ms": {"scan": prof["scan_ms"], "sample_select": prof["sample_ms"],
-                          "rescore": prof["rescore_ms"], "sort_pack": prof["sort_ms"]},
-            "rescored_pairs": prof["rescore_rows"], "rescore_row_reads": prof["rescore_row_reads"],
-            "host_ms": {"dense_calls": prof["host_dense_ms"], "sparse_rounds": prof["host_sparse_ms"],
-                        "certify": prof["host_fuse_ms"]},
-            "dense_depth": {"mean": float(dd.mean()), "median": float(np.median(dd)), "max": int(dd.max())},
-            # per-call latency (per query when the batch is 1), Sec. 3.5 reports p50/p95/p99
-            "latency_ms": {"p50": float(np.percentile(step_ms, 50)), "p95": float(np.percentile(step_ms, 95)),
-                           "p99": float(np.percentile(step_ms, 99)), "max": float(np.max(step_ms))},
-            # read ratio d_i / n_i: dense n_i = the visible rows; sparse only where the list was read to its end
-            "dense_read_ratio": {"median": float(np.median(dd) / w.n), "max": float(dd.max() / w.n)},
-            "sparse_exhausted": int(sum(s["sparse_len"] >= 0 for s in stats)),
-            "sparse_depth_mean": float(np.mean([s["sparse_depth"] for s in stats])),
-            "failed": int(sum(int(np.sum(r[2] != 0)) for r in res)),
-        }
-        log(f"batch {bsz}: {out['queries_per_s']:.1f} q/s, scan {achieved:.0f} GB/s")
+        out = step_summary(eahr, prof, res, w.d, w.n, bsz, steps, el, step_ms)
+        log(f"batch {bsz}: {out['queries_per_s']:.1f} q/s, scan {out['scan_gbs']:.0f} GB/s")
         return out, res
 
     head, head_res = run_config(*configs[0])
@@ -459,6 +606,20 @@ def main():
     if not args.no_ablation:
         ablation = generator_ablation(eahr, torch, x, idx, pbm, qdev, sparse_q, w, K, wts,
                                       args.ablation_queries, args.batch)
+    cfg_names = [c for c in args.configs.split(",") if c]
+    further = {}
+    if "weights21" in cfg_names and w.name == "passage":
+        o, r21 = run_config(args.batch, args.steps, args.warmup, weights=(2, 1))
+        o["workload"] = f"passage N={w.n} d={w.d} batch={args.batch} K={K} k=60 weights=2:1"
+        o["roofline"] = roofline_of(o["dominant"], o["kernels"][o["dominant"]])
+        o["roofline_scan"] = roofline_of(o["scan_kernel"], o["kernels"][o["scan_kernel"]])
+        if not args.no_cpu_baseline:
+            name = query_set_for(w, args.batch)
+            want, cel, threads = cpu_baseline(x, post, qsets[name][0], sparse_q[name], K, (2, 1), 1)
+            ids, cnt, _, _ = r21[0]
+            o["cpu_baseline"] = cpu_baseline_entry(1, cel, threads, "1 query of the batch over the full corpus")
+            o["oracle_check"] = {"queries": 1, "top20_equal": int(list(ids[0, :cnt[0]]) == want[0])}
+        further["passage_2to1"] = o
 
     line = {
         "metric": "exact Top-20 EAHR queries/s at 8.8Mx768 (PVS scan HBM GB/s in roofline)",
@@ -491,15 +652,28 @@ def main():
         qs = sparse_q[name]
         nqc = min(args.cpu_queries, bsz)
         log(f"cpu oracle on {nqc} queries")
-        want, cel, cores = cpu_baseline(x, post, q, qs, K, wts, nqc)
+        want, cel, threads = cpu_baseline(x, post, q, qs, K, wts, nqc)
         ids, cnt, _, _ = head_res[0]
         match = sum(list(ids[b, :cnt[b]]) == want[b] for b in range(nqc))
-        line["cpu_baseline"] = {"value": nqc / cel, "unit": "queries/s", "cores": cores,
-                                "kind": "oracle",
-                                "sample": f"{nqc} queries of the headline batch over the full corpus "
-                                          f"(exhaustive fp64 dense sort, brute-force sparse, exact RRF)"}
+        line["cpu_baseline"] = cpu_baseline_entry(
+            nqc, cel, threads, f"{nqc} queries of the headline batch over the full corpus "
+                               f"(exhaustive fp64 dense sort, brute-force sparse, exact RRF)")
         line["oracle_check"] = {"queries": nqc, "top20_equal": int(match)}
         log(f"cpu oracle {cel:.1f}s, {match}/{nqc} Top-20 equal")
+    others = [c for c in cfg_names if c in ("mid", "adv", "temporal")]
+    if others:
+        # the passage data is no longer needed
+        eahr.pvs_free(idx)
+        eahr.pbm_free(pbm)
+        del x, post, qdev
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        for c in others:
+            st = {"mid": (args.steps, args.warmup), "adv": (2, 1), "temporal": (5, 1)}[c]
+            further[c] = bench_workload(c, eahr, torch, datagen, K, st[0], st[1],
+                                        0 if args.no_cpu_baseline else 1)
+    if further:
+        line["configs"] = further
     print(json.dumps(line), flush=True)
 
 

@@ -352,6 +352,10 @@ typedef struct {
     int32_t sparse_status;
     int32_t rounds;         /* depth rounds taken                    */
     int32_t resolved;       /* 1 when the ordered Top-K was fixed    */
+    /* work counters of Sec. 3.5 (0 for a merged dense channel) */
+    int64_t dense_evals;     /* (query, item) pairs scored in float32  */
+    int64_t sparse_postings; /* postings read by the sparse channel    */
+    int64_t sparse_scored;   /* sparse items given an exact score      */
 } eahr_query_stats;
 
 /* eahr_topk -- the ordered Top-K of complete-list weighted RRF (Sec. 2.1) for

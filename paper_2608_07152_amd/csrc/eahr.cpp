@@ -150,16 +150,21 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
     std::vector<int32_t> dstat(B, EAHR_LIST_EXHAUSTED), sstat(B, EAHR_LIST_EXHAUSTED);
     std::vector<int32_t> rounds(B, 0);
     std::vector<uint8_t> failed(B, 0);
-    // id range of the channels (ids are dense rows and sparse documents),
-    // which lets deep queries switch the fusion to direct rank arrays
+    // Under the frozen scheduler appends stay small (at most a check's gap)
+    // while lists grow deep, so deep queries switch the fusion to direct rank
+    // arrays over the channels' id range (dense rows, sparse documents).
+    // Depth doubling appends as many ranks as a list already holds, so its
+    // merges into the id order cost O(depth) in all and the arrays (8 bytes
+    // per id of the range) would cost more than they save.
     int64_t universe = 0;
-    if (use_dense && !merged) {
-        int64_t rows = 0;
-        EAHR_TRY(pvs_info(dense, epoch, &rows, nullptr, nullptr));
-        universe = rows;
+    if (ep.schedule == EAHR_SCHED_FROZEN && !merged) {
+        if (use_dense) {
+            int64_t rows = 0;
+            EAHR_TRY(pvs_info(dense, epoch, &rows, nullptr, nullptr));
+            universe = rows;
+        }
+        if (use_sparse) universe = std::max<int64_t>(universe, sparse->n_docs);
     }
-    if (use_sparse) universe = std::max<int64_t>(universe, sparse->n_docs);
-    if (merged) universe = 0;   // global ids of a merge have no known range
     for (int32_t b = 0; b < B; ++b) {
         F[b].P = &P;
         F[b].universe = universe;
@@ -536,6 +541,14 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
                 dstat[b] = EAHR_LIST_FAILED;
             }
     if (prof) pvs_profile_add_host(t_dense, t_sparse, t_fuse);
+    std::vector<int64_t> d_evals(B, 0), s_posts(B, 0), s_scored(B, 0);
+    for (int32_t b = 0; b < B; ++b) {
+        if (cl.st) d_evals[b] = pvs_query_evals(cl.st, b);
+        if (!cl.sp.empty() && cl.sp[b]) {
+            s_posts[b] = cl.sp[b]->postings_visited;
+            s_scored[b] = cl.sp[b]->items_scored;
+        }
+    }
     if (::eahr::trace_on()) {
         const auto tc = std::chrono::steady_clock::now();
         if (cl.st) pvs_close(cl.st);
@@ -566,6 +579,9 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
             s.sparse_status = sstat[b];
             s.rounds = rounds[b];
             s.resolved = f.resolved ? 1 : 0;
+            s.dense_evals = d_evals[b];
+            s.sparse_postings = s_posts[b];
+            s.sparse_scored = s_scored[b];
         }
     }
     if (any_failed) EAHR_FAIL(EAHR_E_FAILED, "eahr_topk: a ranked list failed");
@@ -679,6 +695,9 @@ extern "C" int eahr_fuse_lists(const int64_t* list_d, int64_t n_d, const int64_t
         stats->sparse_status = f.L[1].open ? EAHR_LIST_OPEN : EAHR_LIST_EXHAUSTED;
         stats->rounds = rounds;
         stats->resolved = f.resolved ? 1 : 0;
+        stats->dense_evals = 0;
+        stats->sparse_postings = 0;
+        stats->sparse_scored = 0;
     }
     return EAHR_OK;
 }

@@ -241,6 +241,7 @@ static bool expand(pbm_state* st, const pbm_state::Range& R) {
         }
     }
     bool ok = true;
+    st->items_scored += static_cast<int64_t>(st->touched.size());
     for (int32_t off : st->touched) {
         const float s = st->acc[off];
         if (s > R.H) ok = false;

@@ -63,6 +63,7 @@ struct pbm_state {
     int64_t emitted = 0;
     int64_t ranges_expanded = 0;
     int64_t postings_visited = 0;
+    int64_t items_scored = 0;     // documents given an exact score S(x)
     bool failed = false;
     bool complete = false;        // complete generator: rank everything at the first call
     bool complete_done = false;
@@ -80,6 +81,7 @@ struct pbm_state {
         emitted = 0;
         ranges_expanded = 0;
         postings_visited = 0;
+        items_scored = 0;
         failed = false;
         complete = false;
         complete_done = false;

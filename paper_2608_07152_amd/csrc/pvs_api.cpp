@@ -465,16 +465,20 @@ static void free_buffers(ScanBuffers& b) {
 // Per-query scan buffers for nq queries and samples of sample_ld rows.
 // counts layout: [cert nq][fail nq][offs nq + 1][unused 1]
 // [rescore chunk base kSub + 1], then from pair_counts_at(nq) the kSub append
-// counters of the pair pool and from reads_counts_at(nq) the kSub row-load
-// counters of rescoring, kCntStride ints apart.  h_counts mirrors it.
+// counters of the pair pool, from reads_counts_at(nq) the kSub row-load
+// counters of rescoring, kCntStride ints apart, and from evals_counts_at(nq)
+// the records of each query.  h_counts mirrors it.
 static size_t pair_counts_at(int32_t nq) {
     return (3 * static_cast<size_t>(nq) + 2 + pvs::kSub + 1 + 63) / 64 * 64;
 }
 static size_t reads_counts_at(int32_t nq) {
     return pair_counts_at(nq) + static_cast<size_t>(pvs::kSub) * pvs::kCntStride;
 }
-static size_t all_counts(int32_t nq) {
+static size_t evals_counts_at(int32_t nq) {
     return reads_counts_at(nq) + static_cast<size_t>(pvs::kSub) * pvs::kCntStride;
+}
+static size_t all_counts(int32_t nq) {
+    return evals_counts_at(nq) + static_cast<size_t>(nq);
 }
 
 static int ensure_query_buffers(pvs_state* st, int32_t nq, int64_t sample_ld) {
@@ -854,6 +858,7 @@ static int full_scan_round(pvs_state* st, std::vector<int32_t>& todo) {
         }
         for (int32_t i = 0; i < ng; ++i) {
             auto& Q = st->q[qidx[i]];
+            Q.evals += st->n_vis;
             st->stats.scans += 1;
             st->stats.candidates += st->n_vis;
             st->stats.certified += st->n_vis;
@@ -991,12 +996,15 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     mo.pairs = st->pairs;
     mo.pair_sub = pair_sub;
     mo.pair_cnt = d_pcnt;
+    mo.q_evals = st->counts + evals_counts_at(nq);
     EAHR_TRY(mark(2));
     scan(false, mo, nq);
     EAHR_TRY(mark(3));
     HIP_TRY(hipGetLastError());
     HIP_TRY(hipMemcpyAsync(st->h_counts + pair_counts_at(nq), d_pcnt,
                            static_cast<size_t>(pvs::kSub) * pvs::kCntStride * sizeof(int32_t),
+                           hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipMemcpyAsync(st->h_counts + evals_counts_at(nq), mo.q_evals, nq * sizeof(int32_t),
                            hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
     tp[2] = clk::now();
@@ -1011,6 +1019,35 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     st->stats.sample_scans += 1;
     st->stats.rows_scanned += nblocks * 64;
     st->stats.bytes_scanned += st->n_rows * (static_cast<int64_t>(ix->d) + 12) + nblocks * 8;
+    if (pool_over) {
+        // records were dropped: nothing of this scan is used, so nothing is
+        // rescored, and every query scans again with room for all of its
+        // candidates
+        const double grow = static_cast<double>(fullest) / static_cast<double>(pair_sub);
+        std::vector<int32_t> again;
+        for (int32_t i = 0; i < nq; ++i) {
+            auto& Q = st->q[todo[i]];
+            const int64_t cap = st->h_scanq[i].cand_cap;
+            Q.cap_hint = std::max(Q.cap_hint, static_cast<int64_t>(std::ceil(cap * grow * 1.25)) + 16);
+            st->stats.overflows += 1;
+            again.push_back(todo[i]);
+        }
+        if (prof) {
+            float t[2];
+            HIP_TRY(hipEventElapsedTime(&t[0], st->ev[0], st->ev[1]));
+            HIP_TRY(hipEventElapsedTime(&t[1], st->ev[2], st->ev[3]));
+            std::lock_guard<std::mutex> lk(g_prof_mu);
+            g_prof.sample_ms += t[0];
+            g_prof.scan_ms += t[1];
+        }
+        again.insert(again.end(), later.begin(), later.end());
+        todo.swap(again);
+        return EAHR_OK;
+    }
+    {
+        const int32_t* ev = st->h_counts + evals_counts_at(nq);
+        for (int32_t i = 0; i < nq; ++i) st->q[todo[i]].evals += ev[i];
+    }
 
     // 3. rescore, order and pack the certified ranks
     const int64_t chunks = pvs::rescore_chunks(h_pcnt, pair_sub);
@@ -1092,7 +1129,7 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     // append the certified keys of every query to its cache (in parallel)
     std::vector<uint8_t> usable(nq, 0);
     for (int32_t i = 0; i < nq; ++i)
-        usable[i] = !h_fail[i] && !pool_over && cert_all[i] == h_cert[i];
+        usable[i] = !h_fail[i] && cert_all[i] == h_cert[i];
     eahr::parallel_for(nq, eahr::host_threads(), [&](int64_t i) {
         if (!usable[i] || h_cert[i] == 0) return;
         const uint64_t* kp = st->h_packed + h_offs[i];
@@ -1111,21 +1148,13 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
                      static_cast<long long>(total), static_cast<long long>(kept),
                      static_cast<long long>(certified), ms(0, 1), ms(1, 2), ms(2, 3), ms(3, 4), ms(4, 5));
     }
-    if (!pool_over) st->stats.candidates += kept;
+    st->stats.candidates += kept;
     std::vector<int32_t> keep;
     for (int32_t i = 0; i < nq; ++i) {
         const int32_t b = todo[i];
         auto& Q = st->q[b];
         if (h_fail[i]) {
             Q.failed = true;
-            continue;
-        }
-        const int64_t cap = st->h_scanq[i].cand_cap;
-        if (pool_over) {   // records were dropped: every query again, with a larger pool
-            const double grow = static_cast<double>(fullest) / static_cast<double>(pair_sub);
-            Q.cap_hint = std::max(Q.cap_hint, static_cast<int64_t>(std::ceil(cap * grow * 1.25)) + 16);
-            st->stats.overflows += 1;
-            keep.push_back(b);
             continue;
         }
         if (cert_all[i] != h_cert[i]) {   // its key region overflowed: again with room for all
@@ -1234,6 +1263,10 @@ int pvs_fill(pvs_state* st, int64_t depth, const uint8_t* active, int64_t* added
 
 bool pvs_query_failed(const pvs_state* st, int32_t b) {
     return st && b >= 0 && b < st->B && st->q[b].failed;
+}
+
+int64_t pvs_query_evals(const pvs_state* st, int32_t b) {
+    return (st && b >= 0 && b < st->B) ? st->q[b].evals : 0;
 }
 
 extern "C" int pvs_stats(const pvs_state* st, pvs_counters* out) {

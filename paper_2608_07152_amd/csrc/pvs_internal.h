@@ -63,6 +63,8 @@ int pvs_fill(pvs_state* st, int64_t depth, const uint8_t* active, int64_t* added
 // Whether query b of a state has failed (a rescored score outside its
 // interval), also in work-ahead that pvs_next has not reported yet.
 bool pvs_query_failed(const pvs_state* st, int32_t b);
+// (query, row) pairs of query b scored in float32 so far.
+int64_t pvs_query_evals(const pvs_state* st, int32_t b);
 // Batch size a merged ranking was opened for (pvs_merge.cpp).
 int32_t eahr_merge_batch(const pvs_merge* mg);
 // No rank of the merge has been returned yet (and no query failed).
@@ -143,6 +145,7 @@ struct pvs_state {
         bool cert_exhausted = false;    // every visible row certified
         int retries = 0;                // consecutive scans that certified too few
         int64_t cap_hint = 0;           // candidate capacity needed by the last overflow
+        int64_t evals = 0;              // (query, row) pairs rescored in float32
     };
     const pvs_index* ix = nullptr;
     int64_t epoch = 0;

@@ -80,6 +80,10 @@ struct ScanOut {
     uint4* pairs = nullptr;
     int64_t pair_sub = 0;        // records per sub-region
     int32_t* pair_cnt = nullptr;
+    // main pass: q_evals[i] (zeroed by the caller) counts the records of the
+    // query with scan index i, i.e. the float32 evaluations its rescoring
+    // will make when the pool did not overflow
+    int32_t* q_evals = nullptr;
     int32_t qbase = 0;           // scan index of the pass's first query
 };
 

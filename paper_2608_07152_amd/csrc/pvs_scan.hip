@@ -83,6 +83,11 @@ __global__ __launch_bounds__(256) void k_scan_gemv(
     }
     const int total = __shfl(incl, 63, 64);
     if (total == 0) return;
+#pragma unroll
+    for (int b = 0; b < QB; ++b) {
+        const int c = __popcll(__ballot((take >> b) & 1u));
+        if (lane == 0 && c) atomicAdd(&o.q_evals[o.qbase + b], c);
+    }
     const int sub = static_cast<int>(blk & (kSub - 1));
     int base = 0;
     if (lane == 0) base = atomicAdd(&o.pair_cnt[sub * kCntStride], total);
@@ -401,8 +406,15 @@ __global__ __launch_bounds__(256) void k_scan_mfma(
             }
         }
     }
-    if (!SAMPLE)
+    if (!SAMPLE) {
+#pragma unroll
+        for (int uu = 0; uu < NQS; ++uu) {   // records per query (lanes l and l ^ 32 share one)
+            int c = __popc(mask[uu]);
+            c += __shfl_xor(c, 32, 64);
+            if (lane < 32 && c) atomicAdd(&o.q_evals[o.qbase + 32 * (u0 + uu) + lane], c);
+        }
         emit_pairs<NQS>(mask, acc, blk, lane, o.qbase + 32 * u0, static_cast<int>(blk & (kSub - 1)), o);
+    }
     }
 }
 
@@ -437,10 +449,12 @@ __global__ __launch_bounds__(256, 2) void k_scan_mfma_wide(
     // second half's (at most kSavedDots per wavefront, else written at once)
     constexpr int kSavedDots = 512;
     __shared__ int32_t s_dots[4][NQT == 8 ? kSavedDots : 1];
+    __shared__ int32_t s_evals[NQT * 32];      // records per query of this workgroup
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
     for (int b = tid; b < nq && b < NQT * 32; b += 256) s_q[b] = sq[b];
+    for (int b = tid; b < NQT * 32; b += 256) s_evals[b] = 0;
     __syncthreads();
     const int nsteps = nchunk >> 1;            // a multiple of PA
     const int64_t ngroups = (nblocks + 3) / 4;
@@ -558,6 +572,12 @@ __global__ __launch_bounds__(256, 2) void k_scan_mfma_wide(
             // no code motion across the epilogue (the next half's loads would
             // raise the register pressure past 256)
             __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int uu = 0; uu < NQS; ++uu) {   // records per query (lanes l and l ^ 32 share one)
+                int c = __popc(mask[uu]);
+                c += __shfl_xor(c, 32, 64);
+                if (lane < 32 && c) atomicAdd(&s_evals[32 * (u0 + uu) + lane], c);
+            }
             const int sub = static_cast<int>(blk & (kSub - 1));
             if (have && NQT == 8 && u0 == 0) {
                 // first of two halves: save the dot products of its candidates
@@ -594,6 +614,8 @@ __global__ __launch_bounds__(256, 2) void k_scan_mfma_wide(
             __syncthreads();   // bsm and the metadata are reused next
         }
     }
+    for (int b = tid; b < nq && b < NQT * 32; b += 256)
+        if (s_evals[b]) atomicAdd(&o.q_evals[o.qbase + b], s_evals[b]);
 }
 
 static int cu_count() {

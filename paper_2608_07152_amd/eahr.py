@@ -56,7 +56,9 @@ class eahr_query_stats(C.Structure):
     _fields_ = [("dense_depth", C.c_int64), ("sparse_depth", C.c_int64),
                 ("dense_len", C.c_int64), ("sparse_len", C.c_int64),
                 ("dense_status", C.c_int32), ("sparse_status", C.c_int32),
-                ("rounds", C.c_int32), ("resolved", C.c_int32)]
+                ("rounds", C.c_int32), ("resolved", C.c_int32),
+                ("dense_evals", C.c_int64), ("sparse_postings", C.c_int64),
+                ("sparse_scored", C.c_int64)]
 
     def as_dict(self):
         return {f: getattr(self, f) for f, _ in self._fields_}

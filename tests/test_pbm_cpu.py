@@ -217,3 +217,19 @@ def test_rank_observer_sees_the_ranks_read(tiny_sparse, schedule):
         assert np.array_equal(ids, want[:len(ids)])
         assert np.array_equal(scores.view(np.int32), wscores[:len(ids)].view(np.int32))
         assert len(rec.ranks(b, 0)[0]) == 0
+
+
+def test_sparse_work_counters(tiny_sparse):
+    # the complete generator reads every posting of the query terms once and
+    # scores every document carrying one; PBM stops earlier
+    w, post, qs = tiny_sparse
+    idx = eahr.pbm_build(post.term_ptr, post.doc, post.impact, w.n, 256)
+    _, _, _, full = eahr.eahr_topk(None, idx, None, qs, K=20, w_dense=0, w_sparse=1,
+                                   sparse_generator="complete")
+    _, _, _, pbm = eahr.eahr_topk(None, idx, None, qs, K=20, w_dense=0, w_sparse=1)
+    for b, (t, _) in enumerate(qs):
+        n_post = sum(int(post.term_ptr[x + 1] - post.term_ptr[x]) for x in t)
+        docs = np.unique(np.concatenate([post.doc[post.term_ptr[x]:post.term_ptr[x + 1]] for x in t]))
+        assert full[b]["sparse_postings"] == n_post and full[b]["sparse_scored"] == len(docs)
+        assert 0 < pbm[b]["sparse_postings"] <= n_post and 0 < pbm[b]["sparse_scored"] <= len(docs)
+        assert full[b]["dense_evals"] == 0 == pbm[b]["dense_evals"]
