@@ -478,7 +478,7 @@ static size_t evals_counts_at(int32_t nq) {
     return reads_counts_at(nq) + static_cast<size_t>(pvs::kSub) * pvs::kCntStride;
 }
 static size_t all_counts(int32_t nq) {
-    return evals_counts_at(nq) + static_cast<size_t>(nq);
+    return evals_counts_at(nq) + static_cast<size_t>(pvs::kSub) * nq;
 }
 
 static int ensure_query_buffers(pvs_state* st, int32_t nq, int64_t sample_ld) {
@@ -997,6 +997,7 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     mo.pair_sub = pair_sub;
     mo.pair_cnt = d_pcnt;
     mo.q_evals = st->counts + evals_counts_at(nq);
+    mo.q_ld = nq;
     EAHR_TRY(mark(2));
     scan(false, mo, nq);
     EAHR_TRY(mark(3));
@@ -1004,8 +1005,8 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     HIP_TRY(hipMemcpyAsync(st->h_counts + pair_counts_at(nq), d_pcnt,
                            static_cast<size_t>(pvs::kSub) * pvs::kCntStride * sizeof(int32_t),
                            hipMemcpyDeviceToHost, s));
-    HIP_TRY(hipMemcpyAsync(st->h_counts + evals_counts_at(nq), mo.q_evals, nq * sizeof(int32_t),
-                           hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipMemcpyAsync(st->h_counts + evals_counts_at(nq), mo.q_evals,
+                           static_cast<size_t>(pvs::kSub) * nq * sizeof(int32_t), hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
     tp[2] = clk::now();
     int64_t kept = 0, fullest = 0;   // records kept; the fullest sub-region's count
@@ -1046,7 +1047,8 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     }
     {
         const int32_t* ev = st->h_counts + evals_counts_at(nq);
-        for (int32_t i = 0; i < nq; ++i) st->q[todo[i]].evals += ev[i];
+        for (int c = 0; c < pvs::kSub; ++c)
+            for (int32_t i = 0; i < nq; ++i) st->q[todo[i]].evals += ev[c * nq + i];
     }
 
     // 3. rescore, order and pack the certified ranks

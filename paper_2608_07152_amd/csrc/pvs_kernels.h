@@ -80,10 +80,13 @@ struct ScanOut {
     uint4* pairs = nullptr;
     int64_t pair_sub = 0;        // records per sub-region
     int32_t* pair_cnt = nullptr;
-    // main pass: q_evals[i] (zeroed by the caller) counts the records of the
-    // query with scan index i, i.e. the float32 evaluations its rescoring
-    // will make when the pool did not overflow
+    // main pass: q_evals[s * q_ld + i] (zeroed by the caller), summed over
+    // the kSub copies s, counts the records of the query with scan index i,
+    // i.e. the float32 evaluations its rescoring will make when the pool did
+    // not overflow (a block or workgroup adds to copy s = its index % kSub,
+    // so the atomics of concurrent blocks spread over kSub addresses)
     int32_t* q_evals = nullptr;
+    int32_t q_ld = 0;
     int32_t qbase = 0;           // scan index of the pass's first query
 };
 

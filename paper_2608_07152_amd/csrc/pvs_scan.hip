@@ -8,6 +8,9 @@
 // Two kernels compute the same integers: a dot4 GEMV for a few queries and an
 // Int8 MFMA contraction for batches.
 #include <algorithm>
+#include <atomic>
+#include <cstdlib>
+#include <cstring>
 
 #include "pvs_device.h"
 
@@ -86,7 +89,7 @@ __global__ __launch_bounds__(256) void k_scan_gemv(
 #pragma unroll
     for (int b = 0; b < QB; ++b) {
         const int c = __popcll(__ballot((take >> b) & 1u));
-        if (lane == 0 && c) atomicAdd(&o.q_evals[o.qbase + b], c);
+        if (lane == 0 && c) atomicAdd(&o.q_evals[(blk & (kSub - 1)) * o.q_ld + o.qbase + b], c);
     }
     const int sub = static_cast<int>(blk & (kSub - 1));
     int base = 0;
@@ -411,7 +414,8 @@ __global__ __launch_bounds__(256) void k_scan_mfma(
         for (int uu = 0; uu < NQS; ++uu) {   // records per query (lanes l and l ^ 32 share one)
             int c = __popc(mask[uu]);
             c += __shfl_xor(c, 32, 64);
-            if (lane < 32 && c) atomicAdd(&o.q_evals[o.qbase + 32 * (u0 + uu) + lane], c);
+            if (lane < 32 && c)
+                atomicAdd(&o.q_evals[(blk & (kSub - 1)) * o.q_ld + o.qbase + 32 * (u0 + uu) + lane], c);
         }
         emit_pairs<NQS>(mask, acc, blk, lane, o.qbase + 32 * u0, static_cast<int>(blk & (kSub - 1)), o);
     }
@@ -615,7 +619,285 @@ __global__ __launch_bounds__(256, 2) void k_scan_mfma_wide(
         }
     }
     for (int b = tid; b < nq && b < NQT * 32; b += 256)
-        if (s_evals[b]) atomicAdd(&o.q_evals[o.qbase + b], s_evals[b]);
+        if (s_evals[b]) atomicAdd(&o.q_evals[(blockIdx.x & (kSub - 1)) * o.q_ld + o.qbase + b], s_evals[b]);
+}
+
+// ------------------------------------------------ single-pass MFMA scan, LDS queries
+// Query batches of up to 32 NQT queries in one pass over the codes.  A
+// workgroup of 8 wavefronts (two per SIMD) holds the query fragments of the
+// first NQT - NG tiles for every K step in LDS for the whole kernel; the
+// last NG tiles are read from global memory (L2-resident, shared by every
+// workgroup) two steps ahead.  Each wavefront takes one 32-row half of a
+// 64-row code block at a time and computes all NQT tiles for it (NQT
+// accumulators of 32 x 32), its code fragments streaming into a register
+// ring P steps deep that runs on into the next half-block, so the epilogue
+// of one half-block overlaps the loads of the next and the other
+// wavefront's MFMAs.  Vector memory loads complete in issue order for the
+// wait counters, so every load is issued at least two steps before the
+// step that waits for it.
+//
+// Epilogue: a per-half-block integer pre-test.  For query b a row can be a
+// candidate only where c = (s_q s_v) dot >= thr_b (block_threshold over the
+// half-block's largest norms); with s_v in [s_lo, s_hi] over its visible
+// rows that needs dot >= (thr_b / s_q) / s_hi (thr_b >= 0) or
+// (thr_b / s_q) / s_lo (thr_b < 0), loosened by a relative margin and one
+// unit (dot_bound).  A lane compares the largest of its 16 accumulators of
+// a tile with that bound, and only where it passes are the exact intervals
+// of its pairs computed.
+struct QFields {          // the fields of a scanning query the epilogue reads
+    float tau, s_cert, sq, nq, nqh, neq, wmax;
+    int32_t has_cert;
+};
+
+__device__ __forceinline__ float wave_min(float v) {
+    for (int off = 32; off > 0; off >>= 1) v = fminf(v, __shfl_xor(v, off, 64));
+    return v;
+}
+
+// Smallest integer dot product with which a row can pass scaled_threshold x
+// (fl(s_v * dot) >= x, s_v in [s_lo, s_hi]); INT32_MIN passes every row,
+// INT32_MAX none.
+__device__ __forceinline__ int32_t dot_bound(float x, float s_lo, float s_hi) {
+    if (!(x > -INFINITY)) return INT32_MIN;
+    const float xl = x - fabsf(x) * 0x1p-22f - 0x1p-120f;   // then s_v * dot >= xl
+    const float y = (xl >= 0.0f) ? xl / s_hi : xl / s_lo;
+    if (!(y > -2.0e9f)) return INT32_MIN;
+    if (!(y < 2.0e9f)) return INT32_MAX;
+    return static_cast<int32_t>(floorf(y - fabsf(y) * 0x1p-20f)) - 1;
+}
+
+// Records of one 32-row half-block h of block blk (lane l: query q0 + 32 uu
+// + l % 32, rows 8 (r / 4) + 4 (l / 32) + r % 4 of the half), written row by
+// row as in emit_pairs.
+template <int NQT>
+__device__ __forceinline__ void emit_half(const uint32_t (&mask)[NQT], const v16i (&acc)[NQT],
+                                          int64_t blk, int h, int lane, int32_t q0, int sub,
+                                          const ScanOut& o) {
+    int mine = 0;
+#pragma unroll
+    for (int uu = 0; uu < NQT; ++uu) mine += __popc(mask[uu]);
+    for (int off = 32; off > 0; off >>= 1) mine += __shfl_xor(mine, off, 64);
+    if (mine == 0) return;
+    int base = 0;
+    if (lane == 0) base = atomicAdd(&o.pair_cnt[sub * kCntStride], mine);
+    int run = __builtin_amdgcn_readfirstlane(base);
+    const int cap = static_cast<int>(o.pair_sub);
+    uint4* dst = o.pairs + sub * o.pair_sub;
+    const uint32_t below = (1u << (lane & 31)) - 1u;
+    const bool upper = lane >= 32;
+    uint32_t row0 = static_cast<uint32_t>(blk * 64 + 32 * h) + 4 * (lane >> 5);
+    uint32_t qid = static_cast<uint32_t>(q0 + (lane & 31));
+    asm volatile("" : "+v"(row0), "+v"(qid));   // as in emit_pairs
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        int ca = 0, cb = 0;
+#pragma unroll
+        for (int uu = 0; uu < NQT; ++uu) {
+            const uint64_t bal = __ballot((mask[uu] >> r) & 1u);
+            ca += __popc(static_cast<uint32_t>(bal));
+            cb += __popc(static_cast<uint32_t>(bal >> 32));
+        }
+        if (ca + cb == 0) continue;
+        int at = run + (upper ? ca : 0);
+#pragma unroll
+        for (int uu = 0; uu < NQT; ++uu) {
+            const uint64_t bal = __ballot((mask[uu] >> r) & 1u);
+            const uint32_t m = upper ? static_cast<uint32_t>(bal >> 32) : static_cast<uint32_t>(bal);
+            if ((mask[uu] >> r) & 1u) {
+                const int p = at + __popc(m & below);
+                if (p < cap)
+                    dst[p] = make_uint4(row0 + 8 * (r >> 2) + (r & 3), qid + 32 * uu,
+                                        static_cast<uint32_t>(acc[uu][r]), 0u);
+            }
+            at += __popc(m);
+        }
+        run += ca + cb;
+    }
+}
+
+template <int NQT, int NG, int NS, int P>
+__global__ __launch_bounds__(512, 1) void k_scan_mfma_r1(
+    const uint4* __restrict__ codes, const float* __restrict__ scale,
+    const float* __restrict__ vnorm, const float* __restrict__ enorm,
+    const uint64_t* __restrict__ vis, int64_t nblocks, int32_t nchunk,
+    const v4i* __restrict__ qfrag, const ScanQ* __restrict__ sq, int32_t nq, float gamma,
+    ScanOut o) {
+    constexpr int W = 8;
+    constexpr int NL = NQT - NG;            // tiles whose fragments stay in LDS
+    static_assert(P >= 2 && P <= NS, "ring depth");
+    extern __shared__ __align__(16) unsigned char lds[];
+    v4i* bsm = reinterpret_cast<v4i*>(lds);                                    // [NS][NL][64]
+    QFields* s_qf = reinterpret_cast<QFields*>(lds + static_cast<size_t>(NS) * NL * 1024);
+    float* s_meta = reinterpret_cast<float*>(s_qf + NQT * 32);                 // [W][3][32]
+    int32_t* s_evals = reinterpret_cast<int32_t*>(s_meta + W * 3 * 32);        // [NQT * 32]
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: scalar block indices
+    for (int i = tid; i < NS * NL * 64; i += 64 * W) {
+        const int s = i / (NL * 64), rest = i % (NL * 64);
+        bsm[i] = qfrag[s * NQT * 64 + rest];        // tiles 0 .. NL - 1 of step s
+    }
+    for (int b = tid; b < NQT * 32; b += 64 * W) {
+        QFields f{};
+        f.tau = INFINITY;
+        if (b < nq) {
+            const ScanQ& Q = sq[b];
+            f = QFields{Q.tau, Q.s_cert, Q.sq, Q.nq, Q.nqh, Q.neq, Q.wmax, Q.has_cert};
+        }
+        s_qf[b] = f;
+        s_evals[b] = 0;
+    }
+    __syncthreads();
+    float* meta = s_meta + wave * 96;
+    const int64_t nhalves = 2 * nblocks;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * W;
+    int64_t hb = static_cast<int64_t>(blockIdx.x) * W + wave;
+    const __amdgpu_buffer_rsrc_t qrs =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<v4i*>(qfrag), 0, 0x7fffffff, 0x00020000);
+    const int32_t qf_off = lane * 16;
+    const int32_t code_off = ((lane >> 5) * 64 + (lane & 31)) * 16;
+    auto half_rsrc = [&](int64_t x) {   // codes of half-block x (32 rows of block x / 2)
+        return __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint4*>(codes + (x >> 1) * nchunk * 64 + 32 * (x & 1)), 0, 0x7fffffff, 0x00020000);
+    };
+    v4i a[P];                     // ring: slot s % P holds step s
+    v4i g[2][NG > 0 ? NG : 1];    // global tiles, two steps ahead
+    auto load_a = [&](__amdgpu_buffer_rsrc_t rs, int s, v4i& dst) {
+        dst = __builtin_amdgcn_raw_buffer_load_b128(rs, code_off, s * 2048, 0);
+    };
+    auto load_g = [&](int s, v4i (&dst)[NG > 0 ? NG : 1]) {
+#pragma unroll
+        for (int j = 0; j < NG; ++j)
+            dst[j] = __builtin_amdgcn_raw_buffer_load_b128(qrs, qf_off, (s * NQT + NL + j) * 1024, 0);
+    };
+    float sv0 = 0.0f, nv0 = 0.0f, nev0 = 0.0f;
+    uint32_t vbits = 0;
+    auto load_meta = [&](int64_t x) {
+        const int64_t row = (x >> 1) * 64 + 32 * (x & 1) + (lane & 31);
+        sv0 = scale[row];
+        nv0 = vnorm[row];
+        nev0 = enorm[row];
+        vbits = static_cast<uint32_t>(vis[x >> 1] >> (32 * (x & 1)));
+    };
+    if (hb < nhalves) {
+        load_meta(hb);
+        const __amdgpu_buffer_rsrc_t rs = half_rsrc(hb);
+#pragma unroll
+        for (int p = 0; p < P; ++p) load_a(rs, p, a[p]);
+        if (NG > 0) {
+            load_g(0, g[0]);
+            load_g(1, g[1]);
+        }
+    }
+    for (; hb < nhalves; hb += stride) {
+        const int64_t nxt = hb + stride;
+        const bool more = nxt < nhalves;
+        const __amdgpu_buffer_rsrc_t rs_cur = half_rsrc(hb);
+        const __amdgpu_buffer_rsrc_t rs_nxt = half_rsrc(more ? nxt : hb);
+        // this half-block's metadata (invisible rows carry a NaN scale)
+        const bool visible = (vbits >> (lane & 31)) & 1u;
+        if (lane < 32) {
+            meta[lane] = visible ? sv0 : __builtin_nanf("");
+            meta[32 + lane] = nv0;
+            meta[64 + lane] = nev0;
+        }
+        const float nvb = wave_max(visible ? nv0 : 0.0f);
+        const float nevb = wave_max(visible ? nev0 : 0.0f);
+        const float s_hi = wave_max(visible ? sv0 : 0.0f);
+        const float s_lo = wave_min(visible ? sv0 : INFINITY);
+        v16i acc[NQT];
+#pragma unroll
+        for (int u = 0; u < NQT; ++u) acc[u] = v16i{};
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+            const int p = s % P;
+#pragma unroll
+            for (int u = 0; u < NL; ++u) {
+                const v4i vb = bsm[(s * NL + u) * 64 + lane];
+                acc[u] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[p], vb, acc[u], 0, 0, 0);
+            }
+#pragma unroll
+            for (int j = 0; j < NG; ++j)
+                acc[NL + j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[p], g[s & 1][j], acc[NL + j], 0, 0, 0);
+            // refills: global tiles of step s + 2 (or of the next
+            // half-block's first steps), then the ring slot
+            if (NG > 0) {
+                if (s + 2 < NS) load_g(s + 2, g[s & 1]);
+                else if (more) load_g(s + 2 - NS, g[s & 1]);
+            }
+            if (s + P < NS) load_a(rs_cur, s + P, a[p]);
+            else if (more) load_a(rs_nxt, s + P - NS, a[p]);
+            __builtin_amdgcn_sched_barrier(0);   // keep each step's loads in its step
+        }
+        if (more) load_meta(nxt);
+        // epilogue: the scale of each of the lane's 16 rows (NaN: invisible)
+        // in registers; per tile a pre-test s_v * dot >= thq (thq from the
+        // half-block's largest norms, with a margin for the rounding of
+        // both products), exact intervals only for the pairs that pass
+        float svr[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) svr[r] = meta[8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)];
+        constexpr bool kNormsInRegs = NQT <= 4;
+        float nvr[kNormsInRegs ? 16 : 1], nevr[kNormsInRegs ? 16 : 1];
+        if constexpr (kNormsInRegs) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int rih = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                nvr[r] = meta[32 + rih];
+                nevr[r] = meta[64 + rih];
+            }
+        }
+        uint32_t mask[NQT];
+#pragma unroll
+        for (int uu = 0; uu < NQT; ++uu) {
+            mask[uu] = 0;
+            const int b = 32 * uu + (lane & 31);
+            const QFields f = s_qf[b];
+            ScanQ Q{};
+            Q.tau = f.tau;
+            Q.sq = f.sq;
+            Q.nq = f.nq;
+            Q.nqh = f.nqh;
+            Q.neq = f.neq;
+            Q.wmax = f.wmax;
+            const bool valid = b < nq && s_hi > 0.0f;
+            const float thq = valid ? scaled_threshold(block_threshold(Q, nvb, nevb, gamma), Q.sq) : INFINITY;
+            uint32_t pm = 0;
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                if (svr[r] * static_cast<float>(acc[uu][r]) >= thq) pm |= 1u << r;
+            if (pm) {
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    if (!((pm >> r) & 1u)) continue;
+                    const int rih = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                    float nv, nev;
+                    if constexpr (kNormsInRegs) {
+                        nv = nvr[r];
+                        nev = nevr[r];
+                    } else {
+                        nv = meta[32 + rih];
+                        nev = meta[64 + rih];
+                    }
+                    float lo, hi;
+                    pair_interval(Q, svr[r], nv, nev, acc[uu][r], gamma, lo, hi);
+                    if (hi >= f.tau && (!f.has_cert || lo <= f.s_cert)) mask[uu] |= 1u << r;
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);   // one tile's values live at a time
+        }
+#pragma unroll
+        for (int uu = 0; uu < NQT; ++uu) {   // records per query (lanes l and l ^ 32 share one)
+            int c = __popc(mask[uu]);
+            c += __shfl_xor(c, 32, 64);
+            if (lane < 32 && c) atomicAdd(&s_evals[32 * uu + lane], c);
+        }
+        emit_half<NQT>(mask, acc, hb >> 1, static_cast<int>(hb & 1), lane, o.qbase,
+                       static_cast<int>((hb >> 1) & (kSub - 1)), o);
+    }
+    __syncthreads();
+    for (int b = tid; b < nq && b < NQT * 32; b += 64 * W)
+        if (s_evals[b]) atomicAdd(&o.q_evals[(blockIdx.x & (kSub - 1)) * o.q_ld + o.qbase + b], s_evals[b]);
 }
 
 static int cu_count() {
@@ -629,12 +911,50 @@ static int cu_count() {
     return n;
 }
 
+// The single-pass kernel for an index of NS K steps (its loop is unrolled
+// for them); false when the index has another step count or the kernel
+// cannot get its LDS.  EAHR_MFMA_KERNEL=wide (testing) keeps the older
+// kernel.
+template <int NQT, int NG, int NS, int P>
+static bool r1_launch(const IndexView& ix, const uint64_t* vis, int64_t nblocks, const v4i* qfrag,
+                      const ScanQ* sq, int32_t nq, float gamma, const ScanOut& o, hipStream_t stream) {
+    if (ix.nchunk / 2 != NS) return false;
+    if (const char* e = std::getenv("EAHR_MFMA_KERNEL"))
+        if (std::strcmp(e, "wide") == 0) return false;
+    constexpr size_t lds = static_cast<size_t>(NS) * (NQT - NG) * 1024 + NQT * 32 * sizeof(QFields) +
+                           8 * 96 * sizeof(float) + NQT * 32 * sizeof(int32_t);
+    static std::atomic<int> ready{0};   // 1: LDS attribute set, -1: refused
+    if (ready.load() == 0) {
+        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_scan_mfma_r1<NQT, NG, NS, P>),
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+        ready.store(e == hipSuccess ? 1 : -1);
+        if (e != hipSuccess) (void)hipGetLastError();
+    }
+    if (ready.load() < 0) return false;
+    const int64_t groups = (2 * nblocks + 7) / 8;
+    const uint32_t g = static_cast<uint32_t>(std::min<int64_t>(groups, cu_count()));
+    hipLaunchKernelGGL((k_scan_mfma_r1<NQT, NG, NS, P>), dim3(g), dim3(512), lds, stream, ix.codes, ix.scale,
+                       ix.vnorm, ix.enorm, vis, nblocks, ix.nchunk, qfrag, sq, nq, gamma, o);
+    return true;
+}
+
 template <int NQT>
 static void mfma_pass(const IndexView& ix, const uint64_t* vis, int64_t nblocks, const v4i* qfrag,
                       const ScanQ* sq, int32_t nq, float gamma, bool sample, const ScanOut& o,
                       hipStream_t stream) {
     const int64_t waves = sample ? (nblocks + o.sample_stride - 1) / o.sample_stride : nblocks;
     const uint32_t grid = static_cast<uint32_t>((waves + 3) / 4);
+    if constexpr (NQT == 8) {
+        // 256 queries, d = 768: six tiles in LDS, two from L2; d = 384: all in LDS
+        if (!sample && (r1_launch<8, 2, 24, 6>(ix, vis, nblocks, qfrag, sq, nq, gamma, o, stream) ||
+                        r1_launch<8, 0, 12, 6>(ix, vis, nblocks, qfrag, sq, nq, gamma, o, stream)))
+            return;
+    }
+    if constexpr (NQT == 4) {
+        if (!sample && (r1_launch<4, 0, 24, 8>(ix, vis, nblocks, qfrag, sq, nq, gamma, o, stream) ||
+                        r1_launch<4, 0, 12, 6>(ix, vis, nblocks, qfrag, sq, nq, gamma, o, stream)))
+            return;
+    }
     if (sample) {
         hipLaunchKernelGGL((k_scan_mfma<NQT, true>), dim3(grid), dim3(256), 0, stream, ix.codes,
                            ix.scale, ix.vnorm, ix.enorm, vis, nblocks, ix.nchunk, qfrag, sq, nq,

@@ -332,3 +332,53 @@ def test_index_freed_before_its_states(E, tiny):
     _, _, c, _ = E.pvs_merge_next(mg, 5)
     assert np.all(c == 5)
     mg.close()
+
+
+@pytest.fixture(scope="module", params=[384, 768], ids=["d384", "d768"])
+def wide_d(request, E):
+    # dimensions with an unrolled single-pass MFMA kernel (12 and 24 K steps);
+    # 37,000 rows: several blocks per workgroup and a ragged last block
+    w = datagen.workload("tiny", n=37_000, d=request.param, centers=64)
+    x, _ = datagen.corpus(w)
+    return w, x, E.pvs_build(x)
+
+
+@pytest.mark.parametrize("B", [40, 130, 256, 300])
+def test_single_pass_mfma_scan_agrees(E, wide_d, monkeypatch, B):
+    """The single-pass MFMA scan (query fragments resident in LDS, 4 or 8
+    tiles, two of them from L2 at d = 768), the older wide MFMA kernel and
+    the dot4 GEMV scan produce the same ranks and scores, bit for bit, and
+    the prefixes are the oracle's."""
+    w, x, idx = wide_d
+    qb, _ = datagen.queries(w, count=B)
+    runs = {}
+    for kern in ("lds", "wide"):
+        if kern == "wide":
+            monkeypatch.setenv("EAHR_MFMA_KERNEL", "wide")
+        st = _open_with_path(E, idx, qb, "mfma", monkeypatch)
+        runs[kern] = _drain(E, st, [20, 500])[:2]
+        monkeypatch.delenv("EAHR_MFMA_KERNEL", raising=False)
+    g = _open_with_path(E, idx, qb, "gemv", monkeypatch)
+    runs["gemv"] = _drain(E, g, [20, 500])[:2]
+    assert runs["lds"] == runs["wide"] == runs["gemv"]
+    ia, sa = runs["lds"]
+    for b in range(0, B, max(1, B // 5)):
+        check_dense_prefix(qb[b], x, ia[b], sa[b])
+
+
+def test_single_pass_mfma_scan_with_deletes(E, monkeypatch):
+    w = datagen.workload("tiny", n=9_000, d=768, centers=16)
+    x, _ = datagen.corpus(w)
+    idx = E.pvs_build(x)
+    rng = np.random.default_rng(3)
+    dels = np.sort(rng.choice(w.n, 1500, replace=False))
+    E.pvs_delete(idx, dels)
+    e1 = E.pvs_snapshot(idx)
+    visible = np.ones(w.n, bool)
+    visible[dels] = False
+    qb, _ = datagen.queries(w, count=200)
+    # invisible rows inside blocks and half-blocks (epoch 1)
+    a = E.pvs_open(idx, qb, epoch=e1)
+    ia, sa, _ = _drain(E, a, [20, 400])
+    for b in range(0, 200, 37):
+        check_dense_prefix(qb[b], x, ia[b], sa[b], visible)
