@@ -73,9 +73,10 @@ def parse():
     ap.add_argument("--no-ablation", action="store_true",
                     help="skip the rank-generator ablation (global-scale scalar quantisation vs PVS)")
     ap.add_argument("--ablation-queries", type=int, default=20)
-    ap.add_argument("--configs", default="weights21,mid,adv,temporal",
+    ap.add_argument("--configs", default="weights21,sparse_gpu,mid,adv,temporal",
                     help="further configurations (comma-separated): weights21 (the passage batch at "
-                         "weights 2:1), mid, adv, temporal; empty for none")
+                         "weights 2:1), sparse_gpu (the passage batch, and every further workload, "
+                         "again with PBM's posting work on the GPU), mid, adv, temporal; empty for none")
     ap.add_argument("--no-streams", action="store_true",
                     help="skip the controlled rank-stream experiment (host only)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MB")
@@ -249,7 +250,8 @@ def cpu_baseline_entry(n, el, threads, what):
             "cpu_model": model, "kind": "oracle", "seconds": el, "sample": what}
 
 
-def bench_workload(name, eahr, torch, datagen, K, steps, warmup, cpu_queries, wts=(1, 1)):
+def bench_workload(name, eahr, torch, datagen, K, steps, warmup, cpu_queries, wts=(1, 1),
+                   sparse_gpu=False):
     """One further configuration of the workload table: its own corpus,
     index and query batch (one eahr_topk call per step on all its queries),
     kernel rooflines, work counters, and the oracle on a few queries (timed
@@ -296,11 +298,13 @@ def bench_workload(name, eahr, torch, datagen, K, steps, warmup, cpu_queries, wt
     # temporal: warm up on S0, then one timed step per snapshot S1..S5
     runs = [(e, pbms[i]) for i, (e, _) in enumerate(epochs)] if name == "temporal" else None
 
-    def call(i):
+    def call(i, sgen="pbm"):
         if runs is not None:
             e, pb = runs[i]
-            return eahr.eahr_topk(idx, pb, qd, qs, K=K, w_dense=wts[0], w_sparse=wts[1], epoch=e)
-        return eahr.eahr_topk(idx, pbms[0], qd, qs, K=K, w_dense=wts[0], w_sparse=wts[1])
+            return eahr.eahr_topk(idx, pb, qd, qs, K=K, w_dense=wts[0], w_sparse=wts[1], epoch=e,
+                                  sparse_generator=sgen)
+        return eahr.eahr_topk(idx, pbms[0], qd, qs, K=K, w_dense=wts[0], w_sparse=wts[1],
+                              sparse_generator=sgen)
 
     if runs is not None:
         warm, timed = [0], list(range(1, len(runs)))
@@ -329,6 +333,9 @@ def bench_workload(name, eahr, torch, datagen, K, steps, warmup, cpu_queries, wt
     out["roofline_scan"] = roofline_of(out["scan_kernel"], out["kernels"][out["scan_kernel"]])
     log(f"{name}: {out['queries_per_s']:.1f} q/s, dominant {out['dominant']} "
         f"{out['roofline']['frac']:.2f} of HBM, scan {out['scan_kernel']} {out['scan_frac']:.2f}")
+    if sparse_gpu:
+        out["sparse_gpu"] = sparse_gpu_steps(eahr, torch, lambda i: call(i, "pbm_gpu"), warm, timed, res)
+        log(f"{name}: PBM on the GPU {out['sparse_gpu']['queries_per_s']:.1f} q/s")
     if cpu_queries > 0:
         last_e, last_vis = (epochs[-1] if runs else epochs[0])
         post = posts[-1]
@@ -505,6 +512,54 @@ def controlled_streams(eahr, datagen, K=20, check_every=16):
     return out
 
 
+def sparse_gpu_steps(eahr, torch, call, warm, timed, host_res):
+    """The same steps with Posting Block-Max's posting work on the GPU
+    (EAHR_SPARSE_PBM_GPU): queries/s, per-step time and whether every step's
+    Top-K, counts and statuses equal the host generator's."""
+    import numpy as np
+    for i in warm:
+        call(i)
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    res, step_ms = [], []
+    for i in timed:
+        ts = time.perf_counter()
+        res.append(call(i))
+        step_ms.append((time.perf_counter() - ts) * 1e3)
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t
+    nq = sum(len(r[1]) for r in res)
+    same = all(np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1]) and np.array_equal(a[2], b[2])
+               for a, b in zip(res, host_res))
+    postings = [float(np.mean([s["sparse_postings"] for s in r[3]])) for r in res]
+    return {"queries_per_s": nq / el, "ms_per_step": float(np.mean(step_ms)),
+            "topk_equal_to_host_generator": bool(same),
+            "sparse_postings_mean": float(np.mean(postings))}
+
+
+def sparse_only_compare(eahr, torch, pbm, qs, K, steps):
+    """The sparse channel alone (weights 0:1, the Top-K of the exact sparse
+    ranking) over one batch, with the host generator and with the GPU one:
+    queries/s of each and whether their Top-K agree."""
+    import numpy as np
+    out = {}
+    ref = None
+    for gen in ("pbm", "pbm_gpu"):
+        eahr.eahr_topk(None, pbm, None, qs, K=K, w_dense=0, w_sparse=1, sparse_generator=gen)
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        for _ in range(steps):
+            r = eahr.eahr_topk(None, pbm, None, qs, K=K, w_dense=0, w_sparse=1, sparse_generator=gen)
+        torch.cuda.synchronize()
+        out[gen + "_queries_per_s"] = steps * len(qs) / (time.perf_counter() - t)
+        if ref is None:
+            ref = r
+        else:
+            out["topk_equal"] = bool(np.array_equal(ref[0], r[0]) and np.array_equal(ref[1], r[1]))
+    log(f"sparse only: host {out['pbm_queries_per_s']:.0f} q/s, GPU {out['pbm_gpu_queries_per_s']:.0f} q/s")
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -564,7 +619,7 @@ def main():
     qdev = {name: torch.from_numpy(q).cuda() for name, (q, _) in qsets.items()}
     torch.cuda.synchronize()
 
-    def run_config(bsz, steps, warmup, weights=None):
+    def run_config(bsz, steps, warmup, weights=None, sgen="pbm"):
         wts_ = weights or wts
         name = query_set_for(w, bsz)
         qd, qs = qdev[name], sparse_q[name]
@@ -578,7 +633,7 @@ def main():
 
         for i in range(warmup):
             a, b = batch_at(i)
-            eahr.eahr_topk(idx, pbm, a, b, K=K, w_dense=wts_[0], w_sparse=wts_[1])
+            eahr.eahr_topk(idx, pbm, a, b, K=K, w_dense=wts_[0], w_sparse=wts_[1], sparse_generator=sgen)
         eahr.pvs_profile_enable(True)
         torch.cuda.synchronize()
         t = time.perf_counter()
@@ -587,7 +642,8 @@ def main():
         for i in range(steps):
             a, b = batch_at(warmup + i)
             t_step = time.perf_counter()   # eahr_topk returns host results: the step is complete
-            res.append(eahr.eahr_topk(idx, pbm, a, b, K=K, w_dense=wts_[0], w_sparse=wts_[1]))
+            res.append(eahr.eahr_topk(idx, pbm, a, b, K=K, w_dense=wts_[0], w_sparse=wts_[1],
+                                      sparse_generator=sgen))
             step_ms.append((time.perf_counter() - t_step) * 1e3)
         torch.cuda.synchronize()
         el = time.perf_counter() - t
@@ -620,6 +676,18 @@ def main():
             o["cpu_baseline"] = cpu_baseline_entry(1, cel, threads, "1 query of the batch over the full corpus")
             o["oracle_check"] = {"queries": 1, "top20_equal": int(list(ids[0, :cnt[0]]) == want[0])}
         further["passage_2to1"] = o
+    if "sparse_gpu" in cfg_names:
+        # the headline batch with Posting Block-Max's posting work on the GPU
+        o, rg = run_config(args.batch, args.steps, args.warmup, sgen="pbm_gpu")
+        o["workload"] = (f"passage N={w.n} d={w.d} batch={args.batch} K={K} k=60 weights={wts[0]}:{wts[1]} "
+                         f"sparse=PBM on the GPU")
+        o["roofline"] = roofline_of(o["dominant"], o["kernels"][o["dominant"]])
+        o["roofline_scan"] = roofline_of(o["scan_kernel"], o["kernels"][o["scan_kernel"]])
+        o["topk_equal_to_host_generator"] = bool(all(
+            np.array_equal(a[0], b[0]) and np.array_equal(a[2], b[2]) for a, b in zip(rg, head_res)))
+        o["sparse_only"] = sparse_only_compare(eahr, torch, pbm, sparse_q[query_set_for(w, args.batch)][:args.batch],
+                                               K, args.steps)
+        further["passage_sparse_gpu"] = o
 
     line = {
         "metric": "exact Top-20 EAHR queries/s at 8.8Mx768 (PVS scan HBM GB/s in roofline)",
@@ -671,7 +739,8 @@ def main():
         for c in others:
             st = {"mid": (args.steps, args.warmup), "adv": (2, 1), "temporal": (5, 1)}[c]
             further[c] = bench_workload(c, eahr, torch, datagen, K, st[0], st[1],
-                                        0 if args.no_cpu_baseline else 1)
+                                        0 if args.no_cpu_baseline else 1,
+                                        sparse_gpu="sparse_gpu" in cfg_names)
     if further:
         line["configs"] = further
     print(json.dumps(line), flush=True)

@@ -49,6 +49,7 @@ typedef struct pvs_index pvs_index;
 typedef struct pvs_state pvs_state;
 typedef struct pbm_index pbm_index;
 typedef struct pbm_state pbm_state;
+typedef struct pbm_gpu_state pbm_gpu_state;
 
 /* ------------------------------------------------------------ PVS (dense) */
 
@@ -298,8 +299,9 @@ int pbm_next(pbm_state* st, int32_t m, int64_t* ids, float* scores, int32_t* cou
              int32_t* status);
 void pbm_close(pbm_state* st);
 
-/* Sparse rank generators of pbm_open_gen. */
-enum { EAHR_SPARSE_PBM = 0, EAHR_SPARSE_COMPLETE = 1 };
+/* Sparse rank generators of pbm_open_gen (EAHR_SPARSE_PBM_GPU only for
+ * eahr_params.sparse_generator: its states are pbm_gpu_open batches). */
+enum { EAHR_SPARSE_PBM = 0, EAHR_SPARSE_COMPLETE = 1, EAHR_SPARSE_PBM_GPU = 2 };
 
 /* pbm_open_gen -- pbm_open with a choice of generator: EAHR_SPARSE_PBM is
  * pbm_open (ranges expanded in bound order, ranks published when no
@@ -318,6 +320,45 @@ int pbm_open_gen(const pbm_index* idx, const eahr_sparse_query* q, int32_t gener
  * EAHR_E_INVALID when the term has no postings in that range. */
 int pbm_debug_set_blockmax(pbm_index* idx, int32_t term, int64_t range, float value);
 
+/* ------------------------------------------------- PBM on the GPU (sparse) */
+
+/* Largest range_size the GPU generator handles (a range's scores live in
+ * the LDS of one workgroup). */
+#define EAHR_PBM_GPU_MAX_RANGE 16384
+
+/* pbm_upload -- copy the index's postings and block-max table to the
+ * current GPU (about 8 bytes per posting and 20 per block-max entry).  The
+ * first pbm_gpu_open does it when no copy exists; later calls do nothing.
+ * The copy lives until pbm_free; pbm_debug_set_blockmax updates it too.
+ * Errors: EAHR_E_INVALID (NULL), EAHR_E_OOM / EAHR_E_HIP. */
+int pbm_upload(const pbm_index* idx);
+
+/* pbm_gpu_open -- B sparse queries ranked by Posting Block-Max with the
+ * posting work on the GPU (Sec. 2.3.2, App. A.2): the bounds H(R) of every
+ * (query, range) pair in one kernel, one thread per pair; later, every
+ * expanded range's documents scored by one workgroup in LDS.  Each query's
+ * ranking, scores and work counters equal those of pbm_open + pbm_next on the
+ * same query (H and S are accumulated in the same order with the same
+ * roundings; the host keeps the bound order, the expansion batches and the
+ * publication rule of the host generator).  The index must stay alive and
+ * unmodified while the state is open (pbm_free waits for pbm_gpu_close).
+ * Errors: those of pbm_open for any query; EAHR_E_RANGE when range_size >
+ * EAHR_PBM_GPU_MAX_RANGE; EAHR_E_OOM / EAHR_E_HIP. */
+int pbm_gpu_open(const pbm_index* idx, const eahr_sparse_query* q, int32_t B, pbm_gpu_state** out);
+/* pbm_gpu_next -- the next m[b] ranks of every query b with m[b] > 0, as
+ * pbm_next(m[b]) would give them, into the host arrays ids[b] / scores[b]
+ * (m[b] entries each; unused when m[b] == 0).  Queries with m[b] == 0 are
+ * untouched (count 0, their current status).  The expansions of all queries
+ * that need one run in the same device rounds.  A range whose scores exceed
+ * its bound fails its query only (EAHR_LIST_FAILED, count 0, sticky).
+ * Errors: EAHR_E_INVALID (NULL pointers, m[b] < 0), EAHR_E_OOM / EAHR_E_HIP. */
+int pbm_gpu_next(pbm_gpu_state* st, const int32_t* m, int64_t* const* ids, float* const* scores,
+                 int32_t* count, int32_t* status);
+/* pbm_gpu_counters -- work of query b so far: out[0] postings visited,
+ * out[1] documents scored, out[2] ranges expanded (Sec. 3.5 counters). */
+int pbm_gpu_counters(const pbm_gpu_state* st, int32_t b, int64_t* out);
+void pbm_gpu_close(pbm_gpu_state* st);
+
 /* -------------------------------------------------------- EAHR (fusion) */
 
 typedef struct {
@@ -330,7 +371,8 @@ typedef struct {
     int32_t dense_generator;   /* EAHR_GEN_* of the dense channel (0: intervals)  */
     int32_t schedule;          /* EAHR_SCHED_*: depth doubling (0) or the frozen
                                 * scheduler of Sec. 3.5 (1); the result is the same */
-    int32_t sparse_generator;  /* EAHR_SPARSE_* of the sparse channel (0: PBM)     */
+    int32_t sparse_generator;  /* EAHR_SPARSE_* of the sparse channel (0: PBM on the
+                                * host, 2: PBM with its posting work on the GPU) */
 } eahr_params;
 
 /* Depth schedules of eahr_params.schedule.  EAHR_SCHED_DOUBLING: every Open

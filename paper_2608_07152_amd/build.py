@@ -18,7 +18,7 @@ INCLUDE = os.path.join(ROOT, "include")
 OUT = os.path.join(HERE, "libeahr.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 
-HIP_SOURCES = ["pvs_kernels.hip", "pvs_scan.hip", "pvs_rank.hip", "pvs_noalloc.hip"]
+HIP_SOURCES = ["pvs_kernels.hip", "pvs_scan.hip", "pvs_rank.hip", "pvs_noalloc.hip", "pbm_gpu.hip"]
 HOST_SOURCES = ["pvs_api.cpp", "pvs_merge.cpp", "pbm.cpp", "eahr.cpp", "errors.cpp"]
 
 ROCM_INCLUDE = os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "include")

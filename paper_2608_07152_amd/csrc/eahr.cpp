@@ -34,7 +34,8 @@ int check_params(const eahr_params& ep) {
         ep.w_dense < 0 || ep.w_dense > 1024 || ep.w_sparse < 0 || ep.w_sparse > 1024 ||
         (ep.dense_generator != EAHR_GEN_INTERVALS && ep.dense_generator != EAHR_GEN_FULL_SCAN) ||
         (ep.schedule != EAHR_SCHED_DOUBLING && ep.schedule != EAHR_SCHED_FROZEN) ||
-        (ep.sparse_generator != EAHR_SPARSE_PBM && ep.sparse_generator != EAHR_SPARSE_COMPLETE))
+        (ep.sparse_generator != EAHR_SPARSE_PBM && ep.sparse_generator != EAHR_SPARSE_COMPLETE &&
+         ep.sparse_generator != EAHR_SPARSE_PBM_GPU))
         EAHR_FAIL(EAHR_E_INVALID, "eahr: parameters out of range");
     return EAHR_OK;
 }
@@ -177,10 +178,12 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
     struct Cleanup {
         pvs_state* st = nullptr;
         std::vector<pbm_state*> sp;
+        pbm_gpu_state* gsp = nullptr;   // the batch's GPU sparse states
         ~Cleanup() {
             if (st) pvs_close(st);
             for (auto* s : sp)
                 if (s) pbm_close(s);
+            if (gsp) pbm_gpu_close(gsp);
         }
     } cl;
     const auto t_open = std::chrono::steady_clock::now();
@@ -230,6 +233,25 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
             }
         std::stable_sort(sorder.begin(), sorder.end(), [&](int32_t a, int32_t c) { return cost[a] > cost[c]; });
     }
+    // GPU sparse generator: one batched call serves every query that wants
+    // ranks (want[b] > 0) into sids / sscores; the batch's states are opened
+    // at the first call
+    const bool gpu_sparse = use_sparse && ep.sparse_generator == EAHR_SPARSE_PBM_GPU;
+    std::vector<int32_t> gwant(B, 0);
+    std::vector<int64_t*> gids(B, nullptr);
+    std::vector<float*> gsc(B, nullptr);
+    auto gpu_sparse_next = [&](const std::vector<int64_t>& want) -> int {
+        if (!cl.gsp) EAHR_TRY(pbm_gpu_open(sparse, q_sparse, B, &cl.gsp));
+        for (int32_t b = 0; b < B; ++b) {
+            gwant[b] = static_cast<int32_t>(std::min<int64_t>(std::max<int64_t>(want[b], 0), 1LL << 30));
+            sids[b].resize(static_cast<size_t>(gwant[b]));
+            sscores[b].resize(static_cast<size_t>(gwant[b]));
+            gids[b] = sids[b].data();
+            gsc[b] = sscores[b].data();
+            if (gwant[b] == 0) scnt[b] = 0;
+        }
+        return pbm_gpu_next(cl.gsp, gwant.data(), gids.data(), gsc.data(), scnt.data(), ssts.data());
+    };
     if (ep.schedule == EAHR_SCHED_FROZEN) {
         // Frozen scheduler: ranks are read ahead into per-query pending
         // buffers (dense batched, sparse per query), and every check appends
@@ -278,7 +300,23 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
             }
             t_dense += ms_since(t0);
             const auto t1 = std::chrono::steady_clock::now();
-            if (use_sparse) {
+            if (gpu_sparse) {
+                std::vector<int64_t> want(B, 0);
+                for (int32_t b = 0; b < B; ++b)
+                    if (live(b) && !exh[1][b] && have(1, b) < H) want[b] = 2 * H - have(1, b);
+                EAHR_TRY(gpu_sparse_next(want));
+                for (int32_t b = 0; b < B; ++b) {
+                    if (want[b] == 0) continue;
+                    if (ssts[b] == EAHR_LIST_FAILED) {
+                        failed[b] = 1;
+                        sstat[b] = EAHR_LIST_FAILED;
+                        continue;
+                    }
+                    observe(b, 1, sids[b].data(), sscores[b].data(), scnt[b]);
+                    pend[1][b].insert(pend[1][b].end(), sids[b].begin(), sids[b].begin() + scnt[b]);
+                    if (ssts[b] == EAHR_LIST_EXHAUSTED) exh[1][b] = 1;
+                }
+            } else if (use_sparse) {
                 std::vector<uint8_t> sread(B, 0);
                 parallel_for(B, threads, [&](int64_t b) {
                     if (!live(static_cast<int32_t>(b)) || exh[1][b] || have(1, b) >= H) return;
@@ -384,6 +422,22 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
         const auto t_sparse0 = std::chrono::steady_clock::now();
         auto sparse_work = [&]() {
             const auto t0 = std::chrono::steady_clock::now();
+            if (gpu_sparse) {
+                std::vector<int64_t> want(B, 0);
+                for (int32_t b = 0; b < B; ++b)
+                    if (sact[b]) want[b] = depth - static_cast<int64_t>(F[b].L[1].size());
+                const int rc = gpu_sparse_next(want);
+                if (rc != EAHR_OK) {
+                    note_sparse_error(rc);
+                    for (int32_t b = 0; b < B; ++b)
+                        if (sact[b]) sparse_rc[b] = rc;
+                }
+                sparse_cost_done.store(sparse_cost, std::memory_order_relaxed);
+                r_sparse = ms_since(t0);
+                t_sparse += r_sparse;
+                sparse_done.store(true, std::memory_order_release);
+                return;
+            }
             parallel_for(B, std::max(1, threads - 1), [&](int64_t i) {
                 const int32_t b = sorder[i];
                 if (!sact[b]) return;
@@ -548,6 +602,13 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
             s_posts[b] = cl.sp[b]->postings_visited;
             s_scored[b] = cl.sp[b]->items_scored;
         }
+        if (cl.gsp) {
+            int64_t c[3];
+            if (pbm_gpu_counters(cl.gsp, b, c) == EAHR_OK) {
+                s_posts[b] = c[0];
+                s_scored[b] = c[1];
+            }
+        }
     }
     if (::eahr::trace_on()) {
         const auto tc = std::chrono::steady_clock::now();
@@ -558,6 +619,8 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
             if (sp) pbm_close(sp);
             sp = nullptr;
         }
+        if (cl.gsp) pbm_gpu_close(cl.gsp);
+        cl.gsp = nullptr;
         std::fprintf(stderr, "eahr close dense_ms=%.2f sparse_ms=%.2f call_ms=%.2f\n", cd,
                      ms_since(tc) - cd, ms_since(t_call));
     }

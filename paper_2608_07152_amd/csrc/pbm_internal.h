@@ -4,7 +4,22 @@
 #include <mutex>
 #include <vector>
 
+#include <hip/hip_runtime.h>
+
 #include "eahr.h"
+
+// Device copy of an index for the GPU generator (pbm_upload): postings and
+// the block-max table on one GPU.
+struct pbm_device {
+    int device = -1;
+    int32_t* docs = nullptr;
+    float* imp = nullptr;
+    int64_t* term_ptr = nullptr;
+    int64_t* bm_ptr = nullptr;
+    int32_t* bm_range = nullptr;
+    float* bm_max = nullptr;
+    int64_t* bm_off = nullptr;
+};
 
 struct pbm_index {
     int32_t vocab = 0;
@@ -27,6 +42,11 @@ struct pbm_index {
     // open only marks the index, and the last pbm_close releases it
     mutable int64_t open_states = 0;
     mutable bool release_requested = false;
+    // device copy (made by pbm_upload or the first GPU open), under dev_mu
+    mutable std::mutex dev_mu;
+    mutable pbm_device* dev = nullptr;
+    // closed GPU states kept for reuse (under free_mu)
+    mutable std::vector<struct pbm_gpu_state*> free_gpu_states;
     ~pbm_index();
 };
 
@@ -38,6 +58,7 @@ int pbm_check_query(const pbm_index* ix, const eahr_sparse_query* q);
 struct pbm_state {
     struct Range {
         float H;
+        int32_t post = 0;   // postings of the query inside R (GPU generator)
         int64_t r;
     };
     const pbm_index* ix = nullptr;
@@ -86,4 +107,39 @@ struct pbm_state {
         complete = false;
         complete_done = false;
     }
+};
+
+// Growable device and pinned host buffers of a GPU state (kept across the
+// calls that reuse the state).
+struct pbm_buf {
+    void* p = nullptr;
+    size_t cap = 0;   // bytes
+};
+
+// A batch of queries ranked by the GPU generator: per query the host part of
+// PBM (bound order, pool, published run, counters) in a pbm_state, and the
+// device buffers the bound and expansion kernels use.  Closed states return
+// to their index (buffers, stream and vectors keep their memory).
+struct pbm_gpu_state {
+    struct Call {                 // progress of one query inside pbm_gpu_next
+        int32_t m = 0, n = 0;
+        bool done = true;
+        bool in_refill = false;
+        size_t want = 0, checked = 0, batch = 0;
+        std::vector<pbm_state::Range> run;   // ranges waiting for the device
+        bool run_pending = false;
+    };
+    const pbm_index* ix = nullptr;
+    int32_t B = 0;
+    int device = 0;
+    hipStream_t stream = nullptr;
+    std::vector<pbm_state> q;
+    std::vector<Call> call;
+    // device: query terms (qptr, qterm, qw), bounds (H, post), per round
+    // tasks, key offsets, counters (key counts, scored counts, fail flags)
+    // and keys
+    pbm_buf d_qptr, d_qterm, d_qw, d_H, d_post, d_tasks, d_keyoff, d_cnt, d_keys;
+    // pinned host mirrors
+    pbm_buf h_H, h_post, h_tasks, h_keyoff, h_cnt, h_keys;
+    ~pbm_gpu_state();
 };

@@ -136,6 +136,11 @@ SIGNATURES = {
     "pbm_next": (C.c_int, [_P, _i32, _i64p, _f32p, _i32p, _i32p]),
     "pbm_close": (None, [_P]),
     "pbm_debug_set_blockmax": (C.c_int, [_P, _i32, _i64, C.c_float]),
+    "pbm_upload": (C.c_int, [_P]),
+    "pbm_gpu_open": (C.c_int, [_P, C.POINTER(eahr_sparse_query), _i32, C.POINTER(_P)]),
+    "pbm_gpu_next": (C.c_int, [_P, _i32p, C.POINTER(_i64p), C.POINTER(_f32p), _i32p, _i32p]),
+    "pbm_gpu_counters": (C.c_int, [_P, _i32, _i64p]),
+    "pbm_gpu_close": (None, [_P]),
     "eahr_topk": (C.c_int, [_P, _i64, _P, _P, _i32, C.POINTER(eahr_sparse_query), _i32,
                             C.POINTER(eahr_params), _i64p, _i32p, _i32p,
                             C.POINTER(eahr_query_stats)]),
@@ -287,6 +292,24 @@ class PbmState:
     def close(self):
         if self.h:
             load().pbm_close(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class PbmGpuState:
+    def __init__(self, handle, index, keep):
+        self.h = handle
+        self.index = index
+        self._keep = keep
+
+    def close(self):
+        if self.h:
+            load().pbm_gpu_close(self.h)
             self.h = None
 
     def __del__(self):
@@ -548,9 +571,59 @@ def pbm_debug_set_blockmax(index: PbmIndex, term: int, range_: int, value: float
     _check(load().pbm_debug_set_blockmax(index.h, term, range_, value))
 
 
+PBM_GPU_MAX_RANGE = 16384
+
+
+def pbm_upload(index: PbmIndex) -> None:
+    _check(load().pbm_upload(index.h))
+
+
+def pbm_gpu_open(index: PbmIndex, queries: Sequence[Tuple[np.ndarray, np.ndarray]]) -> PbmGpuState:
+    """A batch of sparse queries ranked by Posting Block-Max with the posting
+    work on the GPU; ``queries`` is a list of (terms, weights)."""
+    B = len(queries)
+    qs = (eahr_sparse_query * max(B, 1))()
+    keep = []
+    for b, (t, w) in enumerate(queries):
+        q, k = _sparse_query(t, w)
+        qs[b] = q
+        keep.append(k)
+    h = C.c_void_p()
+    _check(load().pbm_gpu_open(index.h, qs, B, C.byref(h)))
+    return PbmGpuState(h, index, keep)
+
+
+def pbm_gpu_next(state: PbmGpuState, m):
+    """The next m[b] ranks of every query (m: an int for all, or one per
+    query; 0 leaves a query untouched).  Returns a list of (ids, scores,
+    status) per query."""
+    B = len(state._keep)
+    mm = np.ascontiguousarray(np.broadcast_to(np.asarray(m, dtype=np.int32), (B,)))
+    ids = [np.full(max(int(v), 1), -1, dtype=np.int64) for v in mm]
+    sc = [np.zeros(max(int(v), 1), dtype=np.float32) for v in mm]
+    pid = (C.POINTER(C.c_int64) * max(B, 1))(*[_ptr(a, C.c_int64) for a in ids])
+    psc = (C.POINTER(C.c_float) * max(B, 1))(*[_ptr(a, C.c_float) for a in sc])
+    cnt = np.zeros(max(B, 1), dtype=np.int32)
+    stt = np.zeros(max(B, 1), dtype=np.int32)
+    _check(load().pbm_gpu_next(state.h, _ptr(mm, C.c_int32), pid, psc, _ptr(cnt, C.c_int32),
+                               _ptr(stt, C.c_int32)))
+    return [(ids[b][:cnt[b]], sc[b][:cnt[b]], int(stt[b])) for b in range(B)]
+
+
+def pbm_gpu_counters(state: PbmGpuState, b: int):
+    """(postings visited, documents scored, ranges expanded) of query b."""
+    out = np.zeros(3, dtype=np.int64)
+    _check(load().pbm_gpu_counters(state.h, b, _ptr(out, C.c_int64)))
+    return int(out[0]), int(out[1]), int(out[2])
+
+
+def pbm_gpu_close(state: PbmGpuState) -> None:
+    state.close()
+
+
 # ------------------------------------------------------------------ fusion
 SCHEDULES = {"doubling": 0, "frozen": 1}
-SPARSE_GENERATORS = {"pbm": 0, "complete": 1}
+SPARSE_GENERATORS = {"pbm": 0, "complete": 1, "pbm_gpu": 2}
 
 
 def _params(K, k_rrf, w_dense, w_sparse, depth0, growth, generator="intervals", schedule="doubling",

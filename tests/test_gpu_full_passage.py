@@ -117,6 +117,28 @@ def test_passage_b256_every_query_matches_oracle(E, passage):
     del S
 
 
+def test_passage_b256_gpu_sparse_generator(E, passage):
+    """The 256-query batch with Posting Block-Max's posting work on the GPU:
+    the same Top-20, statuses, sparse ranks read and sparse work counters as
+    the host generator, whose every query the test above checks against the
+    oracle (so this run is oracle-exact too)."""
+    w, x, vn, post, sets, idx, pbm, _ = passage
+    q, qs = sets["b256"]
+    out = []
+    for gen in ("pbm", "pbm_gpu"):
+        t = time.time()
+        with E.RankRecorder() as rec:
+            ids, cnt, stt, stats = E.eahr_topk(idx, pbm, q, qs, K=K, sparse_generator=gen)
+        note(f"b256 sparse generator {gen}: eahr_topk {time.time() - t:.2f}s")
+        out.append((ids, cnt, stt, stats, [rec.ranks(b, 1) for b in range(len(q))]))
+    (ia, ca, sa, ta, ra), (ib, cb, sb, tb, rb) = out
+    assert np.array_equal(ia, ib) and np.array_equal(ca, cb) and np.array_equal(sa, sb)
+    for b in range(len(q)):
+        assert np.array_equal(ra[b][0], rb[b][0]) and np.array_equal(ra[b][1], rb[b][1]), b
+        for key in ("sparse_depth", "sparse_postings", "sparse_scored"):
+            assert ta[b][key] == tb[b][key], (b, key)
+
+
 def test_passage_single_requests_every_query(E, passage):
     w, x, vn, post, sets, idx, pbm, s64cache = passage
     q, qs = sets["single"]
