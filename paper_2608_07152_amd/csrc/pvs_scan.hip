@@ -730,9 +730,11 @@ __global__ __launch_bounds__(512, 1) void k_scan_mfma_r1(
     QFields* s_qf = reinterpret_cast<QFields*>(lds + static_cast<size_t>(NS) * NL * 1024);
     float* s_meta = reinterpret_cast<float*>(s_qf + NQT * 32);                 // [W][3][32]
     int32_t* s_evals = reinterpret_cast<int32_t*>(s_meta + W * 3 * 32);        // [NQT * 32]
+    int32_t* s_ent = s_evals + NQT * 32;                                        // [W][2][64]
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: scalar block indices
+    int32_t* ent = s_ent + wave * 128;       // this wavefront's list: dot products, then packed indices
     for (int i = tid; i < NS * NL * 64; i += 64 * W) {
         const int s = i / (NL * 64), rest = i % (NL * 64);
         bsm[i] = qfrag[s * NQT * 64 + rest];        // tiles 0 .. NL - 1 of step s
@@ -830,27 +832,20 @@ __global__ __launch_bounds__(512, 1) void k_scan_mfma_r1(
             __builtin_amdgcn_sched_barrier(0);   // keep each step's loads in its step
         }
         if (more) load_meta(nxt);
-        // epilogue: the scale of each of the lane's 16 rows (NaN: invisible)
-        // in registers; per tile a pre-test s_v * dot >= thq (thq from the
-        // half-block's largest norms, with a margin for the rounding of
-        // both products), exact intervals only for the pairs that pass
+        // Epilogue.  Pre-test of every pair, one compare per accumulator:
+        // s_v * dot >= thq, thq from the half-block's largest norms with a
+        // margin for the rounding of both products (invisible rows carry a
+        // NaN scale and never pass).  The compare's lane mask places the
+        // passing pairs in a list of 64 in LDS (accumulator rows, then
+        // tiles, then lanes), and each full list takes the exact interval
+        // test densely, one pair per lane, so the divergent per-row exact
+        // test of a sparse pass pattern is never run.
         float svr[16];
 #pragma unroll
         for (int r = 0; r < 16; ++r) svr[r] = meta[8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)];
-        constexpr bool kNormsInRegs = NQT <= 4;
-        float nvr[kNormsInRegs ? 16 : 1], nevr[kNormsInRegs ? 16 : 1];
-        if constexpr (kNormsInRegs) {
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int rih = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-                nvr[r] = meta[32 + rih];
-                nevr[r] = meta[64 + rih];
-            }
-        }
-        uint32_t mask[NQT];
+        float thq[NQT];
 #pragma unroll
         for (int uu = 0; uu < NQT; ++uu) {
-            mask[uu] = 0;
             const int b = 32 * uu + (lane & 31);
             const QFields f = s_qf[b];
             ScanQ Q{};
@@ -861,39 +856,78 @@ __global__ __launch_bounds__(512, 1) void k_scan_mfma_r1(
             Q.neq = f.neq;
             Q.wmax = f.wmax;
             const bool valid = b < nq && s_hi > 0.0f;
-            const float thq = valid ? scaled_threshold(block_threshold(Q, nvb, nevb, gamma), Q.sq) : INFINITY;
-            uint32_t pm = 0;
-#pragma unroll
-            for (int r = 0; r < 16; ++r)
-                if (svr[r] * static_cast<float>(acc[uu][r]) >= thq) pm |= 1u << r;
-            if (pm) {
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    if (!((pm >> r) & 1u)) continue;
-                    const int rih = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-                    float nv, nev;
-                    if constexpr (kNormsInRegs) {
-                        nv = nvr[r];
-                        nev = nevr[r];
-                    } else {
-                        nv = meta[32 + rih];
-                        nev = meta[64 + rih];
-                    }
-                    float lo, hi;
-                    pair_interval(Q, svr[r], nv, nev, acc[uu][r], gamma, lo, hi);
-                    if (hi >= f.tau && (!f.has_cert || lo <= f.s_cert)) mask[uu] |= 1u << r;
+            thq[uu] = valid ? scaled_threshold(block_threshold(Q, nvb, nevb, gamma), Q.sq) : INFINITY;
+        }
+        const int sub = static_cast<int>((hb >> 1) & (kSub - 1));
+        const uint32_t row_base = static_cast<uint32_t>((hb >> 1) * 64 + 32 * (hb & 1));
+        auto flush = [&](int n) {
+            __builtin_amdgcn_wave_barrier();
+            bool ok = false;
+            int32_t dot = 0;
+            int rih = 0, qb = 0, half = 0;
+            if (lane < n) {
+                dot = ent[lane];
+                const int x = ent[64 + lane];
+                const int r = x & 15, sl = (x >> 4) & 63;
+                half = sl >> 5;
+                rih = 8 * (r >> 2) + 4 * half + (r & 3);
+                qb = 32 * (x >> 10) + (sl & 31);
+                const QFields f = s_qf[qb];
+                ScanQ Q{};
+                Q.sq = f.sq;
+                Q.nq = f.nq;
+                Q.nqh = f.nqh;
+                Q.neq = f.neq;
+                float lo, hi;
+                pair_interval(Q, meta[rih], meta[32 + rih], meta[64 + rih], dot, gamma, lo, hi);
+                ok = hi >= f.tau && (!f.has_cert || lo <= f.s_cert);
+            }
+            // records of the upper rows after those of the lower ones, so
+            // that the records of one row stay adjacent
+            const uint64_t b0 = __ballot(ok && half == 0), b1 = __ballot(ok && half == 1);
+            const int n0 = __popcll(b0), tot = n0 + __popcll(b1);
+            if (tot) {
+                int base = 0;
+                if (lane == 0) base = atomicAdd(&o.pair_cnt[sub * kCntStride], tot);
+                base = __builtin_amdgcn_readfirstlane(base);
+                if (ok) {
+                    const uint64_t bm = half ? b1 : b0;
+                    const int pos = base + (half ? n0 : 0) +
+                                    static_cast<int>(__builtin_amdgcn_mbcnt_hi(
+                                        static_cast<uint32_t>(bm >> 32),
+                                        __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(bm), 0u)));
+                    if (pos < o.pair_sub)
+                        o.pairs[sub * o.pair_sub + pos] = make_uint4(row_base + rih, static_cast<uint32_t>(o.qbase + qb),
+                                                                     static_cast<uint32_t>(dot), 0u);
+                    atomicAdd(&s_evals[qb], 1);
                 }
             }
-            __builtin_amdgcn_sched_barrier(0);   // one tile's values live at a time
-        }
+            __builtin_amdgcn_wave_barrier();
+        };
+        int fill = 0;
 #pragma unroll
-        for (int uu = 0; uu < NQT; ++uu) {   // records per query (lanes l and l ^ 32 share one)
-            int c = __popc(mask[uu]);
-            c += __shfl_xor(c, 32, 64);
-            if (lane < 32 && c) atomicAdd(&s_evals[32 * uu + lane], c);
+        for (int r = 0; r < 16; ++r) {
+#pragma unroll
+            for (int uu = 0; uu < NQT; ++uu) {
+                const bool pass = svr[r] * static_cast<float>(acc[uu][r]) >= thq[uu];
+                const uint64_t bal = __ballot(pass);
+                if (!bal) continue;
+                const int n = __popcll(bal);
+                if (fill + n > 64) {
+                    flush(fill);
+                    fill = 0;
+                }
+                if (pass) {
+                    const int pos = fill + static_cast<int>(__builtin_amdgcn_mbcnt_hi(
+                                               static_cast<uint32_t>(bal >> 32),
+                                               __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(bal), 0u)));
+                    ent[pos] = acc[uu][r];
+                    ent[64 + pos] = r | (lane << 4) | (uu << 10);
+                }
+                fill += n;
+            }
         }
-        emit_half<NQT>(mask, acc, hb >> 1, static_cast<int>(hb & 1), lane, o.qbase,
-                       static_cast<int>((hb >> 1) & (kSub - 1)), o);
+        if (fill) flush(fill);
     }
     __syncthreads();
     for (int b = tid; b < nq && b < NQT * 32; b += 64 * W)
@@ -922,7 +956,7 @@ static bool r1_launch(const IndexView& ix, const uint64_t* vis, int64_t nblocks,
     if (const char* e = std::getenv("EAHR_MFMA_KERNEL"))
         if (std::strcmp(e, "wide") == 0) return false;
     constexpr size_t lds = static_cast<size_t>(NS) * (NQT - NG) * 1024 + NQT * 32 * sizeof(QFields) +
-                           8 * 96 * sizeof(float) + NQT * 32 * sizeof(int32_t);
+                           8 * 96 * sizeof(float) + NQT * 32 * sizeof(int32_t) + 8 * 128 * sizeof(int32_t);
     static std::atomic<int> ready{0};   // 1: LDS attribute set, -1: refused
     if (ready.load() == 0) {
         const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_scan_mfma_r1<NQT, NG, NS, P>),
