@@ -12,14 +12,18 @@
 //      E = ||e_q|| * ||v|| + ||q_hat|| * ||e_v||
 //      G = ((|c| + E) + ||q|| * ||v||) * gamma_m
 //      lo = down(c - (E + G)),  hi = up(c + (E + G))   (one ulp outward)
-//  * authoritative float32 score: lane l of a wavefront accumulates
-//    q_j * v_j with fmaf over j = 256 t + 4 l + i in (t, i) order, then the
-//    64 lane sums are combined by an xor butterfly (offsets 32, 16, .., 1).
-//    Every path that reports a score uses row_score below.
+//  * authoritative float32 score: a group of 16 lanes scores one row.  Lane
+//    j of the group takes the float4 chunks c = 16 t + j (t = 0, 1, .. while
+//    c < df / 4) of the row and of the query and accumulates their products
+//    with fmaf in (t, x, y, z, w) order; the 16 lane sums are then added as a
+//    balanced pairwise tree: partners j ^ 1, then j ^ 2, j ^ 4, j ^ 8.
+//    Every path that reports a score uses group_dot / group_score_seg below.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
+
+#include <utility>
 
 #include "pvs_kernels.h"
 
@@ -120,41 +124,92 @@ __device__ __forceinline__ float scaled_threshold(float thr, float sq) {
     return (r > -INFINITY && r < INFINITY) ? r : -INFINITY;
 }
 
-// Authoritative float32 score of one row (fixed order, see the file header).
-template <int J>
-__device__ __forceinline__ float row_score(const float4* __restrict__ rp, const float4 (&qv)[J],
-                                           int lane, int df4) {
+// Sum of the 16 lanes of every row of the wavefront as a pairwise tree:
+// partners j ^ 1 and j ^ 2 (quad permutations), then the lane mirrored
+// within 8 and within 16 lanes, which after the earlier steps hold the same
+// values as j ^ 4 and j ^ 8.  Float addition is commutative, so both
+// partners of a pair compute the same bits and every lane of the row ends
+// with the row's sum.
+__device__ __forceinline__ float sum16(float a) {
+    a = a + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(a), 0xB1, 0xF, 0xF, false));
+    a = a + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(a), 0x4E, 0xF, 0xF, false));
+    a = a + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(a), 0x141, 0xF, 0xF, false));
+    a = a + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(a), 0x140, 0xF, 0xF, false));
+    return a;
+}
+
+// Lane I of every row of 16 lanes, broadcast to its row.
+template <int I>
+__device__ __forceinline__ int32_t bcast16(int32_t x) {
+    return __builtin_amdgcn_update_dpp(0, x, 0x150 + I, 0xF, 0xF, false);
+}
+
+// f(integral_constant<int, I>) for I = 0 .. N - 1 (compile-time indices).
+template <typename F, int... Is>
+__device__ __forceinline__ void static_for(F&& f, std::integer_sequence<int, Is...>) {
+    (f(std::integral_constant<int, Is>{}), ...);
+}
+
+// Chunks per lane of a 16-lane group for a row of df floats, rounded to the
+// instantiated sizes; 0 for rows longer than 16 * kSegChunks chunks, which
+// are scored in segments.  FULL instantiations are for df / 4 == 16 * J.
+constexpr int kSegChunks = 16;
+inline int group_chunks(int df) {
+    const int j = (df / 4 + 15) / 16;
+    return j <= 1 ? 1 : j <= 2 ? 2 : j <= 3 ? 3 : j <= 4 ? 4 : j <= 6 ? 6 : j <= 8 ? 8 : j <= 12 ? 12 : j <= 16 ? 16 : 0;
+}
+
+// The chunks of lane j of a group (zeros past the row's end).
+template <int J, bool FULL>
+__device__ __forceinline__ void load_chunks(const float4* __restrict__ base, int j, int df4, float4 (&dst)[J]) {
+#pragma unroll
+    for (int t = 0; t < J; ++t) {
+        const int c = 16 * t + j;
+        dst[t] = (FULL || c < df4) ? base[c] : make_float4(0, 0, 0, 0);
+    }
+}
+
+// Authoritative score of a row held by a group (its chunks in v, the
+// query's in q), in the fixed order of the file header.
+template <int J, bool FULL>
+__device__ __forceinline__ float group_dot(const float4 (&v)[J], const float4 (&q)[J], int j, int df4) {
     float acc = 0.0f;
 #pragma unroll
     for (int t = 0; t < J; ++t) {
-        const int idx = 64 * t + lane;
-        if (idx < df4) {
-            const float4 v = rp[idx];
-            acc = fmaf(qv[t].x, v.x, acc);
-            acc = fmaf(qv[t].y, v.y, acc);
-            acc = fmaf(qv[t].z, v.z, acc);
-            acc = fmaf(qv[t].w, v.w, acc);
+        if (FULL || 16 * t + j < df4) {
+            acc = fmaf(q[t].x, v[t].x, acc);
+            acc = fmaf(q[t].y, v[t].y, acc);
+            acc = fmaf(q[t].z, v[t].z, acc);
+            acc = fmaf(q[t].w, v[t].w, acc);
         }
     }
-    for (int off = 32; off > 0; off >>= 1) acc = acc + __shfl_xor(acc, off, 64);
-    return acc;
+    return sum16(acc);
 }
 
-template <int J>
-__device__ __forceinline__ void load_query_row(const float4* __restrict__ qrows, int32_t qi,
-                                               int df4, int lane, float4 (&qv)[J]) {
+// The same score for rows longer than 16 * kSegChunks chunks: segments of
+// kSegChunks chunks per lane, loaded and accumulated one after another.
+__device__ __forceinline__ float group_score_seg(const float4* __restrict__ rp, const float4* __restrict__ qp,
+                                                 int j, int df4) {
+    float acc = 0.0f;
+    for (int c0 = 0; c0 < df4; c0 += 16 * kSegChunks) {
+        float4 v[kSegChunks], q[kSegChunks];
 #pragma unroll
-    for (int t = 0; t < J; ++t) {
-        const int idx = 64 * t + lane;
-        qv[t] = (idx < df4) ? qrows[static_cast<int64_t>(qi) * df4 + idx] : make_float4(0, 0, 0, 0);
+        for (int t = 0; t < kSegChunks; ++t) {
+            const int c = c0 + 16 * t + j;
+            v[t] = c < df4 ? rp[c] : make_float4(0, 0, 0, 0);
+            q[t] = c < df4 ? qp[c] : make_float4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int t = 0; t < kSegChunks; ++t) {
+            if (c0 + 16 * t + j < df4) {
+                acc = fmaf(q[t].x, v[t].x, acc);
+                acc = fmaf(q[t].y, v[t].y, acc);
+                acc = fmaf(q[t].z, v[t].z, acc);
+                acc = fmaf(q[t].w, v[t].w, acc);
+            }
+        }
     }
-}
-
-// Number of float4 chunks per lane for a row of df floats, rounded to the
-// instantiated sizes.
-inline int row_chunks(int df) {
-    const int j = (df / 4 + 63) / 64;
-    return j <= 1 ? 1 : j <= 2 ? 2 : j <= 3 ? 3 : j <= 4 ? 4 : j <= 8 ? 8 : 16;
+    return sum16(acc);
 }
 
 }  // namespace pvs

@@ -119,53 +119,82 @@ void launch_maxabs(const float* src, int64_t count, uint32_t* flags, hipStream_t
 // ------------------------------------------------------- exhaustive scoring
 // The exhaustive float32 generator (the "full float32 scan" alternative of
 // Sec. 4.4, Table 4-1): every row of the epoch gets its authoritative score in
-// row_score's fixed order, so each key equals the one rescoring would write;
-// rows not visible get the key ~0, which sorts after every real key.  One
-// wavefront per row (three 1 KiB coalesced loads per 768-float row), the
-// query row in registers; blockIdx.y selects the query of the group.
-template <int J>
+// the fixed order of group_dot, so each key equals the one rescoring would
+// write; rows not visible get the key ~0, which sorts after every real key.
+// One 16-lane group per row (four rows per wavefront, 256 contiguous bytes
+// per group and load), the query row in registers; blockIdx.y selects the
+// query of the group.
+template <int J, bool FULL>
 __global__ __launch_bounds__(256) void k_full_keys(const float* __restrict__ rows, int32_t df,
                                                    const uint64_t* __restrict__ vis, int64_t n_rows,
                                                    const float* __restrict__ qrows,
                                                    const int32_t* __restrict__ qidx,
                                                    uint64_t* __restrict__ keys, int64_t ld) {
-    const int lane = threadIdx.x & 63;
+    const int j = threadIdx.x & 15;
     const int df4 = df / 4;
-    float4 qv[J];
-    load_query_row<J>(reinterpret_cast<const float4*>(qrows), qidx[blockIdx.y], df4, lane, qv);
+    const float4* qp = reinterpret_cast<const float4*>(qrows) + static_cast<int64_t>(qidx[blockIdx.y]) * df4;
+    float4 q[J > 0 ? J : 1];
+    if constexpr (J > 0) load_chunks<J, FULL>(qp, j, df4, q);
     uint64_t* out = keys + static_cast<int64_t>(blockIdx.y) * ld;
-    const int64_t nw = static_cast<int64_t>(gridDim.x) * 4;
-    for (int64_t r = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6); r < n_rows; r += nw) {
-        if (!((vis[r >> 6] >> (r & 63)) & 1ull)) {   // uniform across the wavefront
-            if (lane == 0) out[r] = ~0ull;
+    const int64_t ng = static_cast<int64_t>(gridDim.x) * 16;
+    for (int64_t r = static_cast<int64_t>(blockIdx.x) * 16 + (threadIdx.x >> 4); r < n_rows; r += ng) {
+        if (!((vis[r >> 6] >> (r & 63)) & 1ull)) {   // the same in every lane of the group
+            if (j == 0) out[r] = ~0ull;
             continue;
         }
-        const float sc = row_score<J>(reinterpret_cast<const float4*>(rows + r * df), qv, lane, df4);
-        if (lane == 0) out[r] = (static_cast<uint64_t>(~mono32(sc)) << 32) | static_cast<uint32_t>(r);
+        const float4* rp = reinterpret_cast<const float4*>(rows + r * df);
+        float sc;
+        if constexpr (J > 0) {
+            float4 v[J];
+            load_chunks<J, FULL>(rp, j, df4, v);
+            sc = group_dot<J, FULL>(v, q, j, df4);
+        } else {
+            sc = group_score_seg(rp, qp, j, df4);
+        }
+        if (j == 0) out[r] = (static_cast<uint64_t>(~mono32(sc)) << 32) | static_cast<uint32_t>(r);
     }
 }
+
+// Instantiations of a group kernel for the chunk count of df floats.
+#define PVS_GROUP_SWITCH(df, CASE)                 \
+    do {                                           \
+        const int J_ = group_chunks(df);           \
+        const bool full_ = J_ > 0 && (df) / 4 == 16 * J_; \
+        switch (J_) {                              \
+            CASE(1)                                \
+            CASE(2)                                \
+            CASE(3)                                \
+            CASE(4)                                \
+            CASE(6)                                \
+            CASE(8)                                \
+            CASE(12)                               \
+            CASE(16)                               \
+            default:                               \
+                CASE_SEG();                        \
+                break;                             \
+        }                                          \
+    } while (0)
 
 void launch_full_keys(const IndexView& ix, const uint64_t* vis, int64_t n_rows, const float* qrows,
                       const int32_t* qidx, int32_t ng, uint64_t* keys, int64_t ld,
                       hipStream_t stream) {
     if (n_rows <= 0 || ng <= 0) return;
-    const int64_t blocks = std::min<int64_t>((n_rows + 3) / 4, 8192);
+    const int64_t blocks = std::min<int64_t>((n_rows + 15) / 16, 8192);
     const dim3 grid(static_cast<uint32_t>(blocks), static_cast<uint32_t>(ng));
-#define PVS_FK(J)                                                                                \
-    case J:                                                                                      \
-        hipLaunchKernelGGL(k_full_keys<J>, grid, dim3(256), 0, stream, ix.rows, ix.df, vis,     \
-                           n_rows, qrows, qidx, keys, ld);                                       \
+#define PVS_FK(N)                                                                                  \
+    case N:                                                                                        \
+        if (full_)                                                                                 \
+            hipLaunchKernelGGL((k_full_keys<N, true>), grid, dim3(256), 0, stream, ix.rows, ix.df, vis, \
+                               n_rows, qrows, qidx, keys, ld);                                     \
+        else                                                                                       \
+            hipLaunchKernelGGL((k_full_keys<N, false>), grid, dim3(256), 0, stream, ix.rows, ix.df, \
+                               vis, n_rows, qrows, qidx, keys, ld);                                \
         break;
-    switch (row_chunks(ix.df)) {
-        PVS_FK(1)
-        PVS_FK(2)
-        PVS_FK(3)
-        PVS_FK(4)
-        PVS_FK(8)
-        PVS_FK(16)
-        default:
-            break;
-    }
+#define CASE_SEG()                                                                                 \
+    hipLaunchKernelGGL((k_full_keys<0, false>), grid, dim3(256), 0, stream, ix.rows, ix.df, vis,   \
+                       n_rows, qrows, qidx, keys, ld)
+    PVS_GROUP_SWITCH(ix.df, PVS_FK);
+#undef CASE_SEG
 #undef PVS_FK
 }
 
@@ -212,45 +241,52 @@ void launch_intervals(const IndexView& ix, const int8_t* qcodes, const ScanQ* sq
                        rows, n, lo, hi);
 }
 
-// Authoritative scores of one query against listed rows.
-template <int J>
+// Authoritative scores of one query against listed rows: one 16-lane group
+// per row, in the fixed order of group_dot.
+template <int J, bool FULL>
 __global__ __launch_bounds__(256) void k_scores(const float4* __restrict__ rows, int32_t df4,
                                                 const float4* __restrict__ qrows, int32_t qi,
                                                 const int64_t* __restrict__ ids, int64_t n,
                                                 float* __restrict__ out) {
-    const int lane = threadIdx.x & 63;
-    float4 qv[J];
-    load_query_row<J>(qrows, qi, df4, lane, qv);
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6); i < n;
-         i += static_cast<int64_t>(gridDim.x) * 4) {
-        const float s = row_score<J>(rows + ids[i] * df4, qv, lane, df4);
-        if (lane == 0) out[i] = s;
+    const int j = threadIdx.x & 15;
+    const float4* qp = qrows + static_cast<int64_t>(qi) * df4;
+    float4 q[J > 0 ? J : 1];
+    if constexpr (J > 0) load_chunks<J, FULL>(qp, j, df4, q);
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * 16 + (threadIdx.x >> 4); i < n;
+         i += static_cast<int64_t>(gridDim.x) * 16) {
+        const float4* rp = rows + ids[i] * df4;
+        float s;
+        if constexpr (J > 0) {
+            float4 v[J];
+            load_chunks<J, FULL>(rp, j, df4, v);
+            s = group_dot<J, FULL>(v, q, j, df4);
+        } else {
+            s = group_score_seg(rp, qp, j, df4);
+        }
+        if (j == 0) out[i] = s;
     }
 }
 
 void launch_scores(const IndexView& ix, const float* qrows, int32_t qi, const int64_t* rows,
                    int64_t n, float* out, hipStream_t stream) {
     if (n <= 0) return;
-    int64_t g = (n + 3) / 4;
+    int64_t g = (n + 15) / 16;
     if (g > 65536) g = 65536;
     const float4* r4 = reinterpret_cast<const float4*>(ix.rows);
     const float4* q4 = reinterpret_cast<const float4*>(qrows);
     const dim3 grid(static_cast<uint32_t>(g));
-#define PVS_SC(N)                                                                                 \
-    case N:                                                                                       \
-        hipLaunchKernelGGL(k_scores<N>, grid, dim3(256), 0, stream, r4, ix.df / 4, q4, qi, rows, \
-                           n, out);                                                               \
+    const int32_t df4 = ix.df / 4;
+#define PVS_SC(N)                                                                                  \
+    case N:                                                                                        \
+        if (full_)                                                                                 \
+            hipLaunchKernelGGL((k_scores<N, true>), grid, dim3(256), 0, stream, r4, df4, q4, qi, rows, n, out); \
+        else                                                                                       \
+            hipLaunchKernelGGL((k_scores<N, false>), grid, dim3(256), 0, stream, r4, df4, q4, qi, rows, n, out); \
         break;
-    switch (row_chunks(ix.df)) {
-        PVS_SC(1)
-        PVS_SC(2)
-        PVS_SC(3)
-        PVS_SC(4)
-        PVS_SC(8)
-        PVS_SC(16)
-        default:
-            break;
-    }
+#define CASE_SEG() \
+    hipLaunchKernelGGL((k_scores<0, false>), grid, dim3(256), 0, stream, r4, df4, q4, qi, rows, n, out)
+    PVS_GROUP_SWITCH(ix.df, PVS_SC);
+#undef CASE_SEG
 #undef PVS_SC
 }
 

@@ -1,7 +1,7 @@
 // Candidate rescoring, ordering and packing of the PVS dense channel.
 //
-// Every candidate pair gets its authoritative float32 score (row_score's
-// fixed order) and is checked against its interval (App. A.1: a score
+// Every candidate pair gets its authoritative float32 score (the fixed
+// order of group_dot) and is checked against its interval (App. A.1: a score
 // outside it fails the request), recomputed from the integer dot product the
 // scan recorded with the scan's own arithmetic, so identical to it.  A scan
 // with threshold tau certifies exactly the candidates with s32 >= tau whose
@@ -33,13 +33,15 @@ __global__ __launch_bounds__(64) void k_chunk_base(const int32_t* __restrict__ p
 // One workgroup per chunk, one wavefront per quarter of it.  Lane j holds the
 // wavefront's record j and everything about it that does not need the score:
 // its interval (the scan's arithmetic on the same inputs, so identical to the
-// scan's), its query's threshold and last certified key.  The records are then
-// scored one after another, each by the whole wavefront (lane l holds
-// elements 256 t + 4 l + i of the row and of the query, the fixed order of
-// row_score); the lane of the record judges the score.  Records of one row
-// are adjacent, so the row is loaded once for them.  At the end the keys of
-// each query are appended to its region with one atomic.
-template <int J>
+// scan's), its query's threshold and last certified key.  Each 16-lane group
+// g then scores records 16 g .. 16 g + 15 one after another (the group's
+// lanes hold the record's row and query row in the fixed order of the
+// authoritative score, so four records are scored at once), and the record's
+// own lane judges its score.  Records of one row are adjacent, so a group
+// loads the row once for them; likewise the query row.  At the end the keys
+// of each query are appended to its region with one atomic.
+// J: chunks per lane (0: rows scored in segments); FULL: df / 4 == 16 J.
+template <int J, bool FULL>
 __global__ __launch_bounds__(256) void k_rescore(
     const float4* __restrict__ rows, int32_t df4, const float4* __restrict__ qrows,
     const ScanQ* __restrict__ sq, const int32_t* __restrict__ cbase,
@@ -88,58 +90,47 @@ __global__ __launch_bounds__(256) void k_rescore(
     const bool my_hascert = MQ.has_cert != 0;
     uint64_t mykey = 0;
     bool cert = false, bad = false;
-    int reads = 0;
-    // One record at a time, its row and query row kept in registers for the
-    // next record: adjacent records of one row (or one query) load nothing
-    // new.  Few registers (about 64) buy the occupancy that hides the gather
-    // latency; keeping several records in flight per wavefront measured
-    // slower (15 % at 4 in flight, more beyond).
-    float4 vc[J], qc[J];
-    int32_t rowc = -1, qic = -1;
-    for (int k = 0; k < n; ++k) {
-        const int32_t row = __builtin_amdgcn_readlane(my_row, k);
-        const int32_t qi = __builtin_amdgcn_readlane(my_qi, k);
-        if (row != rowc) {
-            const float4* rp = rows + static_cast<int64_t>(row) * df4;
-#pragma unroll
-            for (int t = 0; t < J; ++t) {
-                const int idx = 64 * t + lane;
-                vc[t] = idx < df4 ? rp[idx] : make_float4(0, 0, 0, 0);
+    const int g = lane >> 4, j = lane & 15;
+    float4 v[J > 0 ? J : 1], q[J > 0 ? J : 1];
+    int32_t prow = -1, pqi = -1;
+    int reads = 0;   // row loads of this lane's group
+    static_for(
+        [&](auto I_) {
+            constexpr int i = decltype(I_)::value;
+            // the group's record i, held by lane 16 g + i
+            const int32_t row = bcast16<i>(my_row);
+            const int32_t qi = bcast16<i>(my_qi);
+            if (16 * g + i < n) {   // the same in every lane of the group
+                float sc;
+                if constexpr (J > 0) {
+                    if (row != prow) {
+                        load_chunks<J, FULL>(rows + static_cast<int64_t>(row) * df4, j, df4, v);
+                        prow = row;
+                        ++reads;
+                    }
+                    if (qi != pqi) {
+                        load_chunks<J, FULL>(qrows + static_cast<int64_t>(qi) * df4, j, df4, q);
+                        pqi = qi;
+                    }
+                    sc = group_dot<J, FULL>(v, q, j, df4);
+                } else {
+                    sc = group_score_seg(rows + static_cast<int64_t>(row) * df4,
+                                         qrows + static_cast<int64_t>(qi) * df4, j, df4);
+                    ++reads;
+                }
+                if (j == i) {
+                    bad = !(my_lo <= sc && sc <= my_hi);
+                    const bool dropped = my_hascert && (sc > my_scert || (sc == my_scert && row <= my_idcert));
+                    if (!dropped && sc >= my_tau) {
+                        mykey = (static_cast<uint64_t>(~mono32(sc)) << 32) | static_cast<uint32_t>(row);
+                        cert = true;
+                    }
+                }
             }
-            rowc = row;
-            ++reads;
-        }
-        if (qi != qic) {
-            const float4* qp = qrows + static_cast<int64_t>(qi) * df4;
-#pragma unroll
-            for (int t = 0; t < J; ++t) {
-                const int idx = 64 * t + lane;
-                qc[t] = idx < df4 ? qp[idx] : make_float4(0, 0, 0, 0);
-            }
-            qic = qi;
-        }
-        // same accumulation order as row_score: (t, x, y, z, w), then the butterfly
-        float acc = 0.0f;
-#pragma unroll
-        for (int t = 0; t < J; ++t) {
-            if (64 * t + lane < df4) {
-                acc = fmaf(qc[t].x, vc[t].x, acc);
-                acc = fmaf(qc[t].y, vc[t].y, acc);
-                acc = fmaf(qc[t].z, vc[t].z, acc);
-                acc = fmaf(qc[t].w, vc[t].w, acc);
-            }
-        }
-        for (int off = 32; off > 0; off >>= 1) acc = acc + __shfl_xor(acc, off, 64);
-        const float sc = acc;   // identical in every lane
-        if (lane == k) {
-            bad = !(my_lo <= sc && sc <= my_hi);
-            const bool dropped = my_hascert && (sc > my_scert || (sc == my_scert && row <= my_idcert));
-            if (!dropped && sc >= my_tau) {
-                mykey = (static_cast<uint64_t>(~mono32(sc)) << 32) | static_cast<uint32_t>(row);
-                cert = true;
-            }
-        }
-    }
+        },
+        std::make_integer_sequence<int, 16>{});
+    reads = __builtin_amdgcn_readlane(reads, 0) + __builtin_amdgcn_readlane(reads, 16) +
+            __builtin_amdgcn_readlane(reads, 32) + __builtin_amdgcn_readlane(reads, 48);
     // one of kSub counters (one address for every wavefront would serialise)
     if (lane == 0) atomicAdd(&row_reads[(blockIdx.x & (kSub - 1)) * kCntStride], reads);
     if (bad) fail[my_b] = 1;
@@ -169,13 +160,13 @@ __global__ __launch_bounds__(256) void k_rescore(
     if (pos < kSub * MQ.cand_cap) keys[MQ.cand_off + pos] = mykey;
 }
 
-template <int J>
+template <int J, bool FULL>
 static void rescore_j(const IndexView& ix, const float* qrows, const ScanQ* sq,
                       const int32_t* cbase, int64_t chunks, const int32_t* pair_cnt,
                       const uint4* pairs, int64_t pair_sub, float gamma, uint64_t* keys,
                       int32_t* cert_cnt, int32_t* fail, int32_t* row_reads, int32_t fail_qi,
                       hipStream_t stream) {
-    hipLaunchKernelGGL((k_rescore<J>), dim3(static_cast<uint32_t>(chunks)), dim3(256), 0, stream,
+    hipLaunchKernelGGL((k_rescore<J, FULL>), dim3(static_cast<uint32_t>(chunks)), dim3(256), 0, stream,
                        reinterpret_cast<const float4*>(ix.rows), ix.df / 4,
                        reinterpret_cast<const float4*>(qrows), sq, cbase, pair_cnt, pairs,
                        pair_sub, ix.scale, ix.vnorm, ix.enorm, gamma, keys, cert_cnt, fail,
@@ -198,19 +189,29 @@ void launch_rescore(const IndexView& ix, const float* qrows, const ScanQ* sq,
                     hipStream_t stream) {
     hipLaunchKernelGGL(k_chunk_base, dim3(1), dim3(64), 0, stream, pair_cnt, pair_sub, cbase);
     if (chunks <= 0) return;
-#define PVS_RS(N)                                                                              \
-    case N:                                                                                    \
-        rescore_j<N>(ix, qrows, sq, cbase, chunks, pair_cnt, pairs, pair_sub, gamma, keys,     \
-                     cert_cnt, fail, row_reads, fail_qi, stream);                              \
+    const int J = group_chunks(ix.df);
+    const bool full = J > 0 && ix.df / 4 == 16 * J;
+#define PVS_RS(N)                                                                                  \
+    case N:                                                                                        \
+        if (full)                                                                                  \
+            rescore_j<N, true>(ix, qrows, sq, cbase, chunks, pair_cnt, pairs, pair_sub, gamma, keys, \
+                               cert_cnt, fail, row_reads, fail_qi, stream);                        \
+        else                                                                                       \
+            rescore_j<N, false>(ix, qrows, sq, cbase, chunks, pair_cnt, pairs, pair_sub, gamma,     \
+                                keys, cert_cnt, fail, row_reads, fail_qi, stream);                 \
         break;
-    switch (row_chunks(ix.df)) {
+    switch (J) {
         PVS_RS(1)
         PVS_RS(2)
         PVS_RS(3)
         PVS_RS(4)
+        PVS_RS(6)
         PVS_RS(8)
+        PVS_RS(12)
         PVS_RS(16)
         default:
+            rescore_j<0, false>(ix, qrows, sq, cbase, chunks, pair_cnt, pairs, pair_sub, gamma, keys,
+                                cert_cnt, fail, row_reads, fail_qi, stream);
             break;
     }
 #undef PVS_RS

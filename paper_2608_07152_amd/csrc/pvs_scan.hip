@@ -810,14 +810,21 @@ __global__ __launch_bounds__(512, 1) void k_scan_mfma_r1(
         v16i acc[NQT];
 #pragma unroll
         for (int u = 0; u < NQT; ++u) acc[u] = v16i{};
+        // LDS tiles: the fragments of step s + 1 are read while step s
+        // multiplies (two register sets, used alternately)
+        v4i vb[2][NL > 0 ? NL : 1];
+#pragma unroll
+        for (int u = 0; u < NL; ++u) vb[0][u] = bsm[u * 64 + lane];
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
             const int p = s % P;
+            if (s + 1 < NS) {
 #pragma unroll
-            for (int u = 0; u < NL; ++u) {
-                const v4i vb = bsm[(s * NL + u) * 64 + lane];
-                acc[u] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[p], vb, acc[u], 0, 0, 0);
+                for (int u = 0; u < NL; ++u) vb[(s + 1) & 1][u] = bsm[((s + 1) * NL + u) * 64 + lane];
             }
+#pragma unroll
+            for (int u = 0; u < NL; ++u)
+                acc[u] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[p], vb[s & 1][u], acc[u], 0, 0, 0);
 #pragma unroll
             for (int j = 0; j < NG; ++j)
                 acc[NL + j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[p], g[s & 1][j], acc[NL + j], 0, 0, 0);

@@ -1,10 +1,12 @@
 """The authoritative float32 score follows one fixed order (reading R6 of the
-dense channel): lane l of a wavefront accumulates q_j * v_j with a fused
-multiply-add over j = 256 t + 4 l + i in (t, i) order, then the 64 lane sums
-are combined by an xor butterfly (offsets 32, 16, .., 1).  This test
-recomputes that order on the CPU with exactly rounded float32 operations and
-requires the GPU's scores (pvs_scores, and the ranks pvs_next emits) to
-match bit for bit."""
+dense channel): a group of 16 lanes scores a row; lane j takes the float4
+chunks c = 16 t + j of the row and the query and accumulates their products
+with a fused multiply-add in (t, x, y, z, w) order, then the 16 lane sums are
+added as a balanced pairwise tree (partners j ^ 1, j ^ 2, j ^ 4, j ^ 8).
+This test recomputes that order on the CPU with exactly rounded float32
+operations and requires the GPU's scores (pvs_scores, and the ranks pvs_next
+emits) to match bit for bit.  Rows of more than 1,024 floats are scored in
+segments on the device; the order is the same."""
 from fractions import Fraction
 
 import numpy as np
@@ -42,17 +44,16 @@ def r6_score(q: np.ndarray, v: np.ndarray) -> np.float32:
     vp[:d] = v
     df4 = df // 4
     lanes = []
-    for lane in range(64):
+    for j in range(16):
         acc = F32(0)
-        t = 0
-        while 64 * t + lane < df4:
+        c = j
+        while c < df4:
             for i in range(4):
-                j = 256 * t + 4 * lane + i
-                acc = _fma32(qp[j], vp[j], acc)
-            t += 1
+                acc = _fma32(qp[4 * c + i], vp[4 * c + i], acc)
+            c += 16
         lanes.append(acc)
-    for off in (32, 16, 8, 4, 2, 1):
-        lanes = [_add32(lanes[l], lanes[l ^ off]) for l in range(64)]
+    for off in (1, 2, 4, 8):
+        lanes = [_add32(lanes[j], lanes[j ^ off]) for j in range(16)]
     return lanes[0]
 
 
@@ -63,7 +64,7 @@ def E():
     return eahr
 
 
-@pytest.mark.parametrize("d", [100, 128, 768])
+@pytest.mark.parametrize("d", [100, 128, 768, 1100])
 def test_scores_follow_the_fixed_order_bit_for_bit(E, d):
     w = datagen.workload("tiny", n=300, d=d)
     x, _ = datagen.corpus(w)
