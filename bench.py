@@ -84,14 +84,13 @@ def parse():
 
 
 # committed PMC summaries: kernel class -> (file, sources whose hash it records)
+SCAN_SOURCES = ["paper_2608_07152_amd/csrc/pvs_scan.hip", "paper_2608_07152_amd/csrc/pvs_device.h"]
+RANK_SOURCES = ["paper_2608_07152_amd/csrc/pvs_rank.hip", "paper_2608_07152_amd/csrc/pvs_device.h"]
 TRAFFIC_FILES = {
-    "rescore": ("profiles/k_rescore_passage_b256_traffic.txt", ["paper_2608_07152_amd/csrc/pvs_rank.hip"]),
-    "k_scan_mfma<8>": ("profiles/k_scan_mfma_wide_passage_b256_traffic.txt",
-                       ["paper_2608_07152_amd/csrc/pvs_scan.hip"]),
-    "k_scan_mfma<4>": ("profiles/k_scan_mfma_wide4_passage_b256_traffic.txt",
-                       ["paper_2608_07152_amd/csrc/pvs_scan.hip"]),
-    "k_scan_gemv<1>": ("profiles/k_scan_gemv1_passage_b1_traffic.txt",
-                       ["paper_2608_07152_amd/csrc/pvs_scan.hip"]),
+    "rescore": ("profiles/k_rescore_passage_b256_traffic.txt", RANK_SOURCES),
+    "k_scan_mfma<8>": ("profiles/k_scan_mfma_r1_8tile_passage_b256_traffic.txt", SCAN_SOURCES),
+    "k_scan_mfma<4>": ("profiles/k_scan_mfma_r1_4tile_passage_b256_traffic.txt", SCAN_SOURCES),
+    "k_scan_gemv<1>": ("profiles/k_scan_gemv1_passage_b1_traffic.txt", SCAN_SOURCES),
 }
 
 
