@@ -649,9 +649,16 @@ struct QFields {          // the fields of a scanning query the epilogue reads
     int32_t has_cert;
 };
 
-__device__ __forceinline__ float wave_min(float v) {
-    for (int off = 32; off > 0; off >>= 1) v = fminf(v, __shfl_xor(v, off, 64));
-    return v;
+// Largest value of lanes 0..31 (lanes 32..63 hold copies of them), in every
+// lane: four DPP steps inside each row of 16 lanes (partners j ^ 1, j ^ 2,
+// the mirrored lane within 8 and within 16), then the two rows.
+__device__ __forceinline__ float max32(float v) {
+    v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false)));
+    v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false)));
+    v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xF, 0xF, false)));
+    v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x140, 0xF, 0xF, false)));
+    return fmaxf(__int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0)),
+                 __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16)));
 }
 
 // Smallest integer dot product with which a row can pass scaled_threshold x
@@ -724,17 +731,24 @@ __global__ __launch_bounds__(512, 1) void k_scan_mfma_r1(
     ScanOut o) {
     constexpr int W = 8;
     constexpr int NL = NQT - NG;            // tiles whose fragments stay in LDS
-    static_assert(P >= 2 && P <= NS, "ring depth");
+    // the refills of the last P steps load the next half-block's first P
+    // steps into the slots step s % P names for them, which needs NS % P == 0
+    static_assert(P >= 2 && P <= NS && NS % P == 0, "ring depth must divide the step count");
     extern __shared__ __align__(16) unsigned char lds[];
     v4i* bsm = reinterpret_cast<v4i*>(lds);                                    // [NS][NL][64]
     QFields* s_qf = reinterpret_cast<QFields*>(lds + static_cast<size_t>(NS) * NL * 1024);
     float* s_meta = reinterpret_cast<float*>(s_qf + NQT * 32);                 // [W][3][32]
     int32_t* s_evals = reinterpret_cast<int32_t*>(s_meta + W * 3 * 32);        // [NQT * 32]
-    int32_t* s_ent = s_evals + NQT * 32;                                        // [W][2][64]
+    // pass list per wavefront: room for a row of every tile when NQT <= 4
+    // (one overflow check per accumulator row), else 64 entries (a check
+    // per tile and row)
+    constexpr bool kRowCheck = NQT <= 4;
+    constexpr int CAP = kRowCheck ? 64 * (NQT + 1) : 64;
+    int32_t* s_ent = s_evals + NQT * 32;                                        // [W][2][CAP]
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: scalar block indices
-    int32_t* ent = s_ent + wave * 128;       // this wavefront's list: dot products, then packed indices
+    int32_t* ent = s_ent + wave * 2 * CAP;   // this wavefront's list: dot products, then packed indices
     for (int i = tid; i < NS * NL * 64; i += 64 * W) {
         const int s = i / (NL * 64), rest = i % (NL * 64);
         bsm[i] = qfrag[s * NQT * 64 + rest];        // tiles 0 .. NL - 1 of step s
@@ -803,10 +817,9 @@ __global__ __launch_bounds__(512, 1) void k_scan_mfma_r1(
             meta[32 + lane] = nv0;
             meta[64 + lane] = nev0;
         }
-        const float nvb = wave_max(visible ? nv0 : 0.0f);
-        const float nevb = wave_max(visible ? nev0 : 0.0f);
-        const float s_hi = wave_max(visible ? sv0 : 0.0f);
-        const float s_lo = wave_min(visible ? sv0 : INFINITY);
+        const float nvb = max32(visible ? nv0 : 0.0f);
+        const float nevb = max32(visible ? nev0 : 0.0f);
+        const float s_hi = max32(visible ? sv0 : 0.0f);
         v16i acc[NQT];
 #pragma unroll
         for (int u = 0; u < NQT; ++u) acc[u] = v16i{};
@@ -867,46 +880,49 @@ __global__ __launch_bounds__(512, 1) void k_scan_mfma_r1(
         }
         const int sub = static_cast<int>((hb >> 1) & (kSub - 1));
         const uint32_t row_base = static_cast<uint32_t>((hb >> 1) * 64 + 32 * (hb & 1));
+        // the exact test of list entries [0, n), 64 at a time
         auto flush = [&](int n) {
             __builtin_amdgcn_wave_barrier();
-            bool ok = false;
-            int32_t dot = 0;
-            int rih = 0, qb = 0, half = 0;
-            if (lane < n) {
-                dot = ent[lane];
-                const int x = ent[64 + lane];
-                const int r = x & 15, sl = (x >> 4) & 63;
-                half = sl >> 5;
-                rih = 8 * (r >> 2) + 4 * half + (r & 3);
-                qb = 32 * (x >> 10) + (sl & 31);
-                const QFields f = s_qf[qb];
-                ScanQ Q{};
-                Q.sq = f.sq;
-                Q.nq = f.nq;
-                Q.nqh = f.nqh;
-                Q.neq = f.neq;
-                float lo, hi;
-                pair_interval(Q, meta[rih], meta[32 + rih], meta[64 + rih], dot, gamma, lo, hi);
-                ok = hi >= f.tau && (!f.has_cert || lo <= f.s_cert);
-            }
-            // records of the upper rows after those of the lower ones, so
-            // that the records of one row stay adjacent
-            const uint64_t b0 = __ballot(ok && half == 0), b1 = __ballot(ok && half == 1);
-            const int n0 = __popcll(b0), tot = n0 + __popcll(b1);
-            if (tot) {
-                int base = 0;
-                if (lane == 0) base = atomicAdd(&o.pair_cnt[sub * kCntStride], tot);
-                base = __builtin_amdgcn_readfirstlane(base);
-                if (ok) {
-                    const uint64_t bm = half ? b1 : b0;
-                    const int pos = base + (half ? n0 : 0) +
-                                    static_cast<int>(__builtin_amdgcn_mbcnt_hi(
-                                        static_cast<uint32_t>(bm >> 32),
-                                        __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(bm), 0u)));
-                    if (pos < o.pair_sub)
-                        o.pairs[sub * o.pair_sub + pos] = make_uint4(row_base + rih, static_cast<uint32_t>(o.qbase + qb),
-                                                                     static_cast<uint32_t>(dot), 0u);
-                    atomicAdd(&s_evals[qb], 1);
+            for (int c0 = 0; c0 < n; c0 += 64) {
+                bool ok = false;
+                int32_t dot = 0;
+                int rih = 0, qb = 0, half = 0;
+                if (c0 + lane < n) {
+                    dot = ent[c0 + lane];
+                    const int x = ent[CAP + c0 + lane];
+                    const int r = x & 15, sl = (x >> 4) & 63;
+                    half = sl >> 5;
+                    rih = 8 * (r >> 2) + 4 * half + (r & 3);
+                    qb = 32 * (x >> 10) + (sl & 31);
+                    const QFields f = s_qf[qb];
+                    ScanQ Q{};
+                    Q.sq = f.sq;
+                    Q.nq = f.nq;
+                    Q.nqh = f.nqh;
+                    Q.neq = f.neq;
+                    float lo, hi;
+                    pair_interval(Q, meta[rih], meta[32 + rih], meta[64 + rih], dot, gamma, lo, hi);
+                    ok = hi >= f.tau && (!f.has_cert || lo <= f.s_cert);
+                }
+                // records of the upper rows after those of the lower ones,
+                // so that the records of one row stay adjacent
+                const uint64_t b0 = __ballot(ok && half == 0), b1 = __ballot(ok && half == 1);
+                const int n0 = __popcll(b0), tot = n0 + __popcll(b1);
+                if (tot) {
+                    int base = 0;
+                    if (lane == 0) base = atomicAdd(&o.pair_cnt[sub * kCntStride], tot);
+                    base = __builtin_amdgcn_readfirstlane(base);
+                    if (ok) {
+                        const uint64_t bm = half ? b1 : b0;
+                        const int pos = base + (half ? n0 : 0) +
+                                        static_cast<int>(__builtin_amdgcn_mbcnt_hi(
+                                            static_cast<uint32_t>(bm >> 32),
+                                            __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(bm), 0u)));
+                        if (pos < o.pair_sub)
+                            o.pairs[sub * o.pair_sub + pos] = make_uint4(
+                                row_base + rih, static_cast<uint32_t>(o.qbase + qb), static_cast<uint32_t>(dot), 0u);
+                        atomicAdd(&s_evals[qb], 1);
+                    }
                 }
             }
             __builtin_amdgcn_wave_barrier();
@@ -914,13 +930,19 @@ __global__ __launch_bounds__(512, 1) void k_scan_mfma_r1(
         int fill = 0;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
+            if constexpr (kRowCheck) {   // room for the passes of every tile of this row
+                if (fill > CAP - 64 * NQT) {
+                    flush(fill);
+                    fill = 0;
+                }
+            }
 #pragma unroll
             for (int uu = 0; uu < NQT; ++uu) {
                 const bool pass = svr[r] * static_cast<float>(acc[uu][r]) >= thq[uu];
                 const uint64_t bal = __ballot(pass);
                 if (!bal) continue;
                 const int n = __popcll(bal);
-                if (fill + n > 64) {
+                if (!kRowCheck && fill + n > CAP) {
                     flush(fill);
                     fill = 0;
                 }
@@ -929,7 +951,7 @@ __global__ __launch_bounds__(512, 1) void k_scan_mfma_r1(
                                                static_cast<uint32_t>(bal >> 32),
                                                __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(bal), 0u)));
                     ent[pos] = acc[uu][r];
-                    ent[64 + pos] = r | (lane << 4) | (uu << 10);
+                    ent[CAP + pos] = r | (lane << 4) | (uu << 10);
                 }
                 fill += n;
             }
@@ -963,7 +985,8 @@ static bool r1_launch(const IndexView& ix, const uint64_t* vis, int64_t nblocks,
     if (const char* e = std::getenv("EAHR_MFMA_KERNEL"))
         if (std::strcmp(e, "wide") == 0) return false;
     constexpr size_t lds = static_cast<size_t>(NS) * (NQT - NG) * 1024 + NQT * 32 * sizeof(QFields) +
-                           8 * 96 * sizeof(float) + NQT * 32 * sizeof(int32_t) + 8 * 128 * sizeof(int32_t);
+                           8 * 96 * sizeof(float) + NQT * 32 * sizeof(int32_t) +
+                           8 * 2 * (NQT <= 4 ? 64 * (NQT + 1) : 64) * sizeof(int32_t);
     static std::atomic<int> ready{0};   // 1: LDS attribute set, -1: refused
     if (ready.load() == 0) {
         const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_scan_mfma_r1<NQT, NG, NS, P>),

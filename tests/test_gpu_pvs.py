@@ -337,8 +337,10 @@ def test_index_freed_before_its_states(E, tiny):
 @pytest.fixture(scope="module", params=[384, 768], ids=["d384", "d768"])
 def wide_d(request, E):
     # dimensions with an unrolled single-pass MFMA kernel (12 and 24 K steps);
-    # 37,000 rows: several blocks per workgroup and a ragged last block
-    w = datagen.workload("tiny", n=37_000, d=request.param, centers=64)
+    # 230,000 rows: 7,188 half-blocks, so each of the 2,048 wavefronts of a
+    # full grid takes three or four (its code ring runs on into the next
+    # half-block), and a ragged last block
+    w = datagen.workload("tiny", n=230_000, d=request.param, centers=64)
     x, _ = datagen.corpus(w)
     return w, x, E.pvs_build(x)
 
@@ -367,11 +369,12 @@ def test_single_pass_mfma_scan_agrees(E, wide_d, monkeypatch, B):
 
 
 def test_single_pass_mfma_scan_with_deletes(E, monkeypatch):
-    w = datagen.workload("tiny", n=9_000, d=768, centers=16)
+    # 200,000 rows: several half-blocks per wavefront
+    w = datagen.workload("tiny", n=200_000, d=768, centers=16)
     x, _ = datagen.corpus(w)
     idx = E.pvs_build(x)
     rng = np.random.default_rng(3)
-    dels = np.sort(rng.choice(w.n, 1500, replace=False))
+    dels = np.sort(rng.choice(w.n, 33_000, replace=False))
     E.pvs_delete(idx, dels)
     e1 = E.pvs_snapshot(idx)
     visible = np.ones(w.n, bool)
