@@ -624,26 +624,25 @@ __global__ __launch_bounds__(256, 2) void k_scan_mfma_wide(
 
 // ------------------------------------------------ single-pass MFMA scan, LDS queries
 // Query batches of up to 32 NQT queries in one pass over the codes.  A
-// workgroup of 8 wavefronts (two per SIMD) holds the query fragments of the
-// first NQT - NG tiles for every K step in LDS for the whole kernel; the
-// last NG tiles are read from global memory (L2-resident, shared by every
-// workgroup) two steps ahead.  Each wavefront takes one 32-row half of a
-// 64-row code block at a time and computes all NQT tiles for it (NQT
-// accumulators of 32 x 32), its code fragments streaming into a register
-// ring P steps deep that runs on into the next half-block, so the epilogue
-// of one half-block overlaps the loads of the next and the other
-// wavefront's MFMAs.  Vector memory loads complete in issue order for the
-// wait counters, so every load is issued at least two steps before the
-// step that waits for it.
+// workgroup of W wavefronts per CU (three per SIMD with four tiles, two
+// with eight) holds the query fragments of the first NQT - NG tiles for
+// every K step in LDS for the whole kernel; the last NG tiles are read from
+// global memory (L2-resident, shared by every workgroup) two steps ahead.
+// Each wavefront takes one 32-row half of a 64-row code block at a time and
+// computes all NQT tiles for it (NQT accumulators of 32 x 32): the LDS
+// fragments of the next K step are read while the current one multiplies,
+// and its code fragments stream into a register ring P steps deep that runs
+// on into the next half-block, so the epilogue of one half-block overlaps
+// the loads of the next and the other wavefronts' MFMAs.  Vector memory
+// loads complete in issue order for the wait counters, so every load is
+// issued at least two steps before the step that waits for it.
 //
-// Epilogue: a per-half-block integer pre-test.  For query b a row can be a
-// candidate only where c = (s_q s_v) dot >= thr_b (block_threshold over the
-// half-block's largest norms); with s_v in [s_lo, s_hi] over its visible
-// rows that needs dot >= (thr_b / s_q) / s_hi (thr_b >= 0) or
-// (thr_b / s_q) / s_lo (thr_b < 0), loosened by a relative margin and one
-// unit (dot_bound).  A lane compares the largest of its 16 accumulators of
-// a tile with that bound, and only where it passes are the exact intervals
-// of its pairs computed.
+// Epilogue: one compare per accumulator pre-tests s_v * dot against the
+// half-block's threshold thq (scaled_threshold of block_threshold over the
+// half-block's largest norms); the compare's lane mask places the passing
+// pairs in a per-wavefront list in LDS, and each list is given the exact
+// interval test densely, one pair per lane, with one atomic per 64 pairs
+// for the records.
 struct QFields {          // the fields of a scanning query the epilogue reads
     float tau, s_cert, sq, nq, nqh, neq, wmax;
     int32_t has_cert;
@@ -661,75 +660,13 @@ __device__ __forceinline__ float max32(float v) {
                  __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16)));
 }
 
-// Smallest integer dot product with which a row can pass scaled_threshold x
-// (fl(s_v * dot) >= x, s_v in [s_lo, s_hi]); INT32_MIN passes every row,
-// INT32_MAX none.
-__device__ __forceinline__ int32_t dot_bound(float x, float s_lo, float s_hi) {
-    if (!(x > -INFINITY)) return INT32_MIN;
-    const float xl = x - fabsf(x) * 0x1p-22f - 0x1p-120f;   // then s_v * dot >= xl
-    const float y = (xl >= 0.0f) ? xl / s_hi : xl / s_lo;
-    if (!(y > -2.0e9f)) return INT32_MIN;
-    if (!(y < 2.0e9f)) return INT32_MAX;
-    return static_cast<int32_t>(floorf(y - fabsf(y) * 0x1p-20f)) - 1;
-}
-
-// Records of one 32-row half-block h of block blk (lane l: query q0 + 32 uu
-// + l % 32, rows 8 (r / 4) + 4 (l / 32) + r % 4 of the half), written row by
-// row as in emit_pairs.
-template <int NQT>
-__device__ __forceinline__ void emit_half(const uint32_t (&mask)[NQT], const v16i (&acc)[NQT],
-                                          int64_t blk, int h, int lane, int32_t q0, int sub,
-                                          const ScanOut& o) {
-    int mine = 0;
-#pragma unroll
-    for (int uu = 0; uu < NQT; ++uu) mine += __popc(mask[uu]);
-    for (int off = 32; off > 0; off >>= 1) mine += __shfl_xor(mine, off, 64);
-    if (mine == 0) return;
-    int base = 0;
-    if (lane == 0) base = atomicAdd(&o.pair_cnt[sub * kCntStride], mine);
-    int run = __builtin_amdgcn_readfirstlane(base);
-    const int cap = static_cast<int>(o.pair_sub);
-    uint4* dst = o.pairs + sub * o.pair_sub;
-    const uint32_t below = (1u << (lane & 31)) - 1u;
-    const bool upper = lane >= 32;
-    uint32_t row0 = static_cast<uint32_t>(blk * 64 + 32 * h) + 4 * (lane >> 5);
-    uint32_t qid = static_cast<uint32_t>(q0 + (lane & 31));
-    asm volatile("" : "+v"(row0), "+v"(qid));   // as in emit_pairs
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-        int ca = 0, cb = 0;
-#pragma unroll
-        for (int uu = 0; uu < NQT; ++uu) {
-            const uint64_t bal = __ballot((mask[uu] >> r) & 1u);
-            ca += __popc(static_cast<uint32_t>(bal));
-            cb += __popc(static_cast<uint32_t>(bal >> 32));
-        }
-        if (ca + cb == 0) continue;
-        int at = run + (upper ? ca : 0);
-#pragma unroll
-        for (int uu = 0; uu < NQT; ++uu) {
-            const uint64_t bal = __ballot((mask[uu] >> r) & 1u);
-            const uint32_t m = upper ? static_cast<uint32_t>(bal >> 32) : static_cast<uint32_t>(bal);
-            if ((mask[uu] >> r) & 1u) {
-                const int p = at + __popc(m & below);
-                if (p < cap)
-                    dst[p] = make_uint4(row0 + 8 * (r >> 2) + (r & 3), qid + 32 * uu,
-                                        static_cast<uint32_t>(acc[uu][r]), 0u);
-            }
-            at += __popc(m);
-        }
-        run += ca + cb;
-    }
-}
-
-template <int NQT, int NG, int NS, int P>
-__global__ __launch_bounds__(512, 1) void k_scan_mfma_r1(
+template <int NQT, int NG, int NS, int P, int W>
+__global__ __launch_bounds__(64 * W, 1) void k_scan_mfma_r1(
     const uint4* __restrict__ codes, const float* __restrict__ scale,
     const float* __restrict__ vnorm, const float* __restrict__ enorm,
     const uint64_t* __restrict__ vis, int64_t nblocks, int32_t nchunk,
     const v4i* __restrict__ qfrag, const ScanQ* __restrict__ sq, int32_t nq, float gamma,
     ScanOut o) {
-    constexpr int W = 8;
     constexpr int NL = NQT - NG;            // tiles whose fragments stay in LDS
     // the refills of the last P steps load the next half-block's first P
     // steps into the slots step s % P names for them, which needs NS % P == 0
@@ -978,26 +915,26 @@ static int cu_count() {
 // for them); false when the index has another step count or the kernel
 // cannot get its LDS.  EAHR_MFMA_KERNEL=wide (testing) keeps the older
 // kernel.
-template <int NQT, int NG, int NS, int P>
+template <int NQT, int NG, int NS, int P, int W>
 static bool r1_launch(const IndexView& ix, const uint64_t* vis, int64_t nblocks, const v4i* qfrag,
                       const ScanQ* sq, int32_t nq, float gamma, const ScanOut& o, hipStream_t stream) {
     if (ix.nchunk / 2 != NS) return false;
     if (const char* e = std::getenv("EAHR_MFMA_KERNEL"))
         if (std::strcmp(e, "wide") == 0) return false;
     constexpr size_t lds = static_cast<size_t>(NS) * (NQT - NG) * 1024 + NQT * 32 * sizeof(QFields) +
-                           8 * 96 * sizeof(float) + NQT * 32 * sizeof(int32_t) +
-                           8 * 2 * (NQT <= 4 ? 64 * (NQT + 1) : 64) * sizeof(int32_t);
+                           W * 96 * sizeof(float) + NQT * 32 * sizeof(int32_t) +
+                           W * 2 * (NQT <= 4 ? 64 * (NQT + 1) : 64) * sizeof(int32_t);
     static std::atomic<int> ready{0};   // 1: LDS attribute set, -1: refused
     if (ready.load() == 0) {
-        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_scan_mfma_r1<NQT, NG, NS, P>),
+        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_scan_mfma_r1<NQT, NG, NS, P, W>),
                                                  hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
         ready.store(e == hipSuccess ? 1 : -1);
         if (e != hipSuccess) (void)hipGetLastError();
     }
     if (ready.load() < 0) return false;
-    const int64_t groups = (2 * nblocks + 7) / 8;
+    const int64_t groups = (2 * nblocks + W - 1) / W;
     const uint32_t g = static_cast<uint32_t>(std::min<int64_t>(groups, cu_count()));
-    hipLaunchKernelGGL((k_scan_mfma_r1<NQT, NG, NS, P>), dim3(g), dim3(512), lds, stream, ix.codes, ix.scale,
+    hipLaunchKernelGGL((k_scan_mfma_r1<NQT, NG, NS, P, W>), dim3(g), dim3(64 * W), lds, stream, ix.codes, ix.scale,
                        ix.vnorm, ix.enorm, vis, nblocks, ix.nchunk, qfrag, sq, nq, gamma, o);
     return true;
 }
@@ -1010,13 +947,13 @@ static void mfma_pass(const IndexView& ix, const uint64_t* vis, int64_t nblocks,
     const uint32_t grid = static_cast<uint32_t>((waves + 3) / 4);
     if constexpr (NQT == 8) {
         // 256 queries, d = 768: six tiles in LDS, two from L2; d = 384: all in LDS
-        if (!sample && (r1_launch<8, 2, 24, 6>(ix, vis, nblocks, qfrag, sq, nq, gamma, o, stream) ||
-                        r1_launch<8, 0, 12, 6>(ix, vis, nblocks, qfrag, sq, nq, gamma, o, stream)))
+        if (!sample && (r1_launch<8, 2, 24, 6, 8>(ix, vis, nblocks, qfrag, sq, nq, gamma, o, stream) ||
+                        r1_launch<8, 0, 12, 6, 8>(ix, vis, nblocks, qfrag, sq, nq, gamma, o, stream)))
             return;
     }
     if constexpr (NQT == 4) {
-        if (!sample && (r1_launch<4, 0, 24, 8>(ix, vis, nblocks, qfrag, sq, nq, gamma, o, stream) ||
-                        r1_launch<4, 0, 12, 6>(ix, vis, nblocks, qfrag, sq, nq, gamma, o, stream)))
+        if (!sample && (r1_launch<4, 0, 24, 8, 12>(ix, vis, nblocks, qfrag, sq, nq, gamma, o, stream) ||
+                        r1_launch<4, 0, 12, 6, 12>(ix, vis, nblocks, qfrag, sq, nq, gamma, o, stream)))
             return;
     }
     if (sample) {
