@@ -564,7 +564,7 @@ pbm_gpu_state::~pbm_gpu_state() {
     const bool sw = hipGetDevice(&cur) == hipSuccess && cur != device;
     if (sw) (void)hipSetDevice(device);
     if (stream) (void)hipStreamSynchronize(stream);
-    for (pbm_buf* b : {&d_qptr, &d_qterm, &d_qw, &d_H, &d_post, &d_tasks, &d_keyoff, &d_cnt, &d_keys})
+    for (pbm_buf* b : {&d_qptr, &d_qterm, &d_qw, &d_H, &d_post, &d_tasks, &d_keyoff, &d_cnt, &d_keys, &d_ent})
         if (b->p) (void)hipFree(b->p);
     for (pbm_buf* b : {&h_H, &h_post, &h_tasks, &h_keyoff, &h_cnt, &h_keys})
         if (b->p) (void)hipHostFree(b->p);
@@ -604,6 +604,9 @@ T* as(const pbm_buf& b) {
 
 // Closed GPU states kept per index for reuse.
 constexpr size_t kFreeGpuStates = 4;
+// Largest table of block-max entries per (query term, range) a state keeps
+// on the device; beyond it the expansions find entries by binary search.
+constexpr size_t kEntTableMax = size_t(1) << 30;
 
 }  // namespace
 
@@ -615,6 +618,7 @@ extern "C" int pbm_gpu_open(const pbm_index* ix, const eahr_sparse_query* q, int
         EAHR_FAIL(EAHR_E_RANGE, "pbm_gpu_open: range_size %d exceeds %d", ix->range_size,
                   static_cast<int>(pbmg::kMaxRangeSize));
     for (int32_t b = 0; b < B; ++b) EAHR_TRY(pbm_check_query(ix, &q[b]));
+    const auto t_open = std::chrono::steady_clock::now();
     {
         std::lock_guard<std::mutex> lk(ix->dev_mu);
         EAHR_TRY(upload_locked(ix));
@@ -678,6 +682,9 @@ extern "C" int pbm_gpu_open(const pbm_index* ix, const eahr_sparse_query* q, int
     // H(R) and the postings count of every (query, range), a chunk of
     // queries per launch; each query's ranges with H > 0 in bound order
     const int64_t nr = ix->n_ranges;
+    const size_t ent_bytes = qterm.size() * static_cast<size_t>(std::max<int64_t>(nr, 0)) * sizeof(int64_t);
+    st->ent_ok = nr > 0 && !qterm.empty() && ent_bytes <= kEntTableMax;
+    if (st->ent_ok) EAHR_TRY(grow_dev(st->d_ent, ent_bytes));
     if (nr > 0 && B > 0) {
         const int32_t chunk = static_cast<int32_t>(std::max<int64_t>(1, std::min<int64_t>(B, kBoundPairs / nr)));
         const size_t pairs = static_cast<size_t>(chunk) * static_cast<size_t>(nr);
@@ -689,7 +696,8 @@ extern "C" int pbm_gpu_open(const pbm_index* ix, const eahr_sparse_query* q, int
         for (int32_t b0 = 0; b0 < B; b0 += chunk) {
             const int32_t nb = std::min(chunk, B - b0);
             const pbmg::QueryView qv{as<int32_t>(st->d_qptr) + b0, as<int32_t>(st->d_qterm), as<float>(st->d_qw), nb};
-            pbmg::launch_bounds(v, qv, as<float>(st->d_H), as<int32_t>(st->d_post), s);
+            pbmg::launch_bounds(v, qv, as<float>(st->d_H), as<int32_t>(st->d_post),
+                                st->ent_ok ? as<int64_t>(st->d_ent) : nullptr, s);
             HIP_TRY(hipGetLastError());
             const size_t n = static_cast<size_t>(nb) * static_cast<size_t>(nr);
             HIP_TRY(hipMemcpyAsync(st->h_H.p, st->d_H.p, n * sizeof(float), hipMemcpyDeviceToHost, s));
@@ -713,6 +721,9 @@ extern "C" int pbm_gpu_open(const pbm_index* ix, const eahr_sparse_query* q, int
         std::lock_guard<std::mutex> lk(ix->free_mu);
         ix->open_states += 1;
     }
+    if (::eahr::trace_on())
+        std::fprintf(stderr, "pbm_gpu open queries=%d ranges=%lld ms=%.2f\n", B, static_cast<long long>(nr),
+                     std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t_open).count());
     *out = st.release();
     return EAHR_OK;
 }
@@ -797,13 +808,19 @@ extern "C" int pbm_gpu_next(pbm_gpu_state* st, const int32_t* m, int64_t* const*
     const auto t0 = std::chrono::steady_clock::now();
     int64_t rounds = 0;
     size_t all_tasks = 0, all_keys = 0;
+    double t_host = 0, t_dev = 0, t_pool = 0;   // trace: host steps, device rounds, pool appends
+    auto since = [](std::chrono::steady_clock::time_point t) {
+        return std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t).count();
+    };
     std::vector<int32_t> round;
     std::vector<size_t> need(static_cast<size_t>(B), 0);
     for (;;) {
+        auto tr = std::chrono::steady_clock::now();
         ::eahr::parallel_for(B, ::eahr::host_threads(), [&](int64_t b) {
             auto& c = st->call[b];
             if (!c.done && !c.run_pending) c.run_pending = advance(static_cast<int32_t>(b));
         });
+        t_host += since(tr);
         // the runs of this round: queries in order while the keys fit (the
         // first one always runs)
         round.clear();
@@ -820,6 +837,7 @@ extern "C" int pbm_gpu_next(pbm_gpu_state* st, const int32_t* m, int64_t* const*
             tasks += c.run.size();
         }
         if (round.empty()) break;
+        tr = std::chrono::steady_clock::now();
         EAHR_TRY(grow_dev(st->d_tasks, tasks * sizeof(pbmg::Task)));
         EAHR_TRY(grow_pinned(st->h_tasks, tasks * sizeof(pbmg::Task)));
         EAHR_TRY(grow_dev(st->d_keys, std::max<size_t>(1, keys) * sizeof(uint64_t)));
@@ -837,8 +855,10 @@ extern "C" int pbm_gpu_next(pbm_gpu_state* st, const int32_t* m, int64_t* const*
         HIP_TRY(hipMemcpyAsync(st->d_keyoff.p, hoff, static_cast<size_t>(B) * sizeof(int64_t),
                                hipMemcpyHostToDevice, s));
         HIP_TRY(hipMemsetAsync(dcnt, 0, 3 * static_cast<size_t>(B) * sizeof(int32_t), s));
-        pbmg::launch_expand(v, qv, as<pbmg::Task>(st->d_tasks), static_cast<int32_t>(tasks), as<int64_t>(st->d_keyoff),
-                            dcnt, dcnt + B, dcnt + 2 * B, as<uint64_t>(st->d_keys), s);
+        if (pbmg::launch_expand(v, qv, as<pbmg::Task>(st->d_tasks), static_cast<int32_t>(tasks),
+                                st->ent_ok ? as<int64_t>(st->d_ent) : nullptr, as<int64_t>(st->d_keyoff), dcnt,
+                                dcnt + B, dcnt + 2 * B, as<uint64_t>(st->d_keys), s) != 0)
+            EAHR_FAIL(EAHR_E_HIP, "pbm_gpu_next: the expansion kernel cannot get %d ids of LDS", ix->range_size);
         HIP_TRY(hipGetLastError());
         HIP_TRY(hipMemcpyAsync(st->h_cnt.p, dcnt, 3 * static_cast<size_t>(B) * sizeof(int32_t),
                                hipMemcpyDeviceToHost, s));
@@ -848,6 +868,8 @@ extern "C" int pbm_gpu_next(pbm_gpu_state* st, const int32_t* m, int64_t* const*
         ++rounds;
         all_tasks += tasks;
         all_keys += keys;
+        t_dev += since(tr);
+        tr = std::chrono::steady_clock::now();
         const int32_t* kc = as<int32_t>(st->h_cnt);
         const int32_t* sc = kc + B;
         const int32_t* fl = kc + 2 * B;
@@ -868,6 +890,7 @@ extern "C" int pbm_gpu_next(pbm_gpu_state* st, const int32_t* m, int64_t* const*
             }
             c.run_pending = false;
         });
+        t_pool += since(tr);
     }
     for (int32_t b = 0; b < B; ++b) {
         pbm_state& S = st->q[b];
@@ -881,9 +904,10 @@ extern "C" int pbm_gpu_next(pbm_gpu_state* st, const int32_t* m, int64_t* const*
         else status[b] = EAHR_LIST_OPEN;
     }
     if (::eahr::trace_on())
-        std::fprintf(stderr, "pbm_gpu next queries=%d device_rounds=%lld tasks=%zu keys=%zu ms=%.2f\n", B,
-                     static_cast<long long>(rounds), all_tasks, all_keys,
-                     std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count());
+        std::fprintf(stderr,
+                     "pbm_gpu next queries=%d device_rounds=%lld tasks=%zu keys=%zu ms=%.2f host_ms=%.2f "
+                     "device_ms=%.2f pool_ms=%.2f\n",
+                     B, static_cast<long long>(rounds), all_tasks, all_keys, since(t0), t_host, t_dev, t_pool);
     return EAHR_OK;
 }
 

@@ -139,6 +139,9 @@ struct pbm_gpu_state {
     // tasks, key offsets, counters (key counts, scored counts, fail flags)
     // and keys
     pbm_buf d_qptr, d_qterm, d_qw, d_H, d_post, d_tasks, d_keyoff, d_cnt, d_keys;
+    // block-max entry of every (query term, range), when it fits kEntTableMax
+    pbm_buf d_ent;
+    bool ent_ok = false;
     // pinned host mirrors
     pbm_buf h_H, h_post, h_tasks, h_keyoff, h_cnt, h_keys;
     ~pbm_gpu_state();

@@ -43,15 +43,20 @@ struct Task {
 // H[b * n_ranges + r] = H(R) of query b, accumulated in float32 over the
 // query's terms in ascending order (one rounding per multiply and add), and
 // post[b * n_ranges + r] = the number of the query's postings inside R.
-void launch_bounds(const IndexView& ix, const QueryView& q, float* H, int32_t* post, hipStream_t s);
+// With ent (may be null): ent[i * n_ranges + r] = the block-max entry of term
+// slot i (index into qterm) for range r, or -1.
+void launch_bounds(const IndexView& ix, const QueryView& q, float* H, int32_t* post, int64_t* ent,
+                   hipStream_t s);
 
 // Scores every document of every task's range that carries a term of the
 // task's query (S(x) accumulated like H, in LDS), then for each such
 // document: scored[b] += 1; fail[b] = 1 when S(x) > H(R); and when S(x) > 0
 // its key (~ord(S) << 32 | id) at keys[key_off[b] + atomicAdd(key_cnt[b])].
-// key_off regions must hold the postings of the query's tasks.
-void launch_expand(const IndexView& ix, const QueryView& q, const Task* tasks, int32_t ntasks,
-                   const int64_t* key_off, int32_t* key_cnt, int32_t* scored, int32_t* fail,
-                   uint64_t* keys, hipStream_t s);
+// key_off regions must hold the postings of the query's tasks.  ent: the
+// table of launch_bounds for these queries, or null (entries found by
+// binary search).  Returns 0, or -1 when the kernel cannot get its LDS.
+int launch_expand(const IndexView& ix, const QueryView& q, const Task* tasks, int32_t ntasks,
+                  const int64_t* ent, const int64_t* key_off, int32_t* key_cnt, int32_t* scored,
+                  int32_t* fail, uint64_t* keys, hipStream_t s);
 
 }  // namespace pbmg
