@@ -16,6 +16,13 @@
 // (L(x_dag), x_dag) must precede (U(y), y) for every other remaining y, and
 // L(x_dag) > B strictly.
 //
+// A fixing takes the best of the items it compares, so with |A| positions
+// fixed only the best K - |A| + 1 both-seen items can still be fixed or be
+// the strongest rival of a fixed one (an item behind them stays third or
+// later until the K-th position is fixed).  The heap keeps those; the rest
+// are dropped when found, against a cutoff item with at least that many kept
+// items at or before it.
+//
 // Bookkeeping without per-item hashing: each list keeps its prefix sorted by
 // id, so the ranks of a round are radix-sorted and merge-joined against the
 // other list to find items seen by both; a bitmap of live positions per list
@@ -41,6 +48,7 @@
 // order because (F, id) is a total order.
 #pragma once
 #include <algorithm>
+#include <cstddef>
 #include <cstdint>
 #include <vector>
 
@@ -219,7 +227,8 @@ struct Fusion {
     const Params* P = nullptr;
     int threads = 1;
     List L[2];
-    std::vector<Scored> both;   // binary heap of unfixed both-seen items
+    std::vector<Scored> both;   // binary heap of the best unfixed both-seen items
+    std::vector<Scored> fresh;  // both-seen items of a one-part append
     std::vector<int64_t> A;     // fixed prefix
     bool resolved = false;
     bool dup = false;           // an id repeated inside one list
@@ -262,6 +271,43 @@ struct Fusion {
 
     bool fixed(int64_t x) const { return std::find(A.begin(), A.end(), x) != A.end(); }
 
+    // (F, id) order: a before b
+    bool better(const Scored& a, const Scored& b) const { return HeapLess{P}(b, a); }
+    // how many of the best both-seen items can still matter (at least 1)
+    size_t keep() const {
+        const int64_t m = P->K - static_cast<int64_t>(A.size()) + 1;
+        return static_cast<size_t>(m < 1 ? 1 : m);
+    }
+    // An item that every kept item precedes or equals, with at least keep()
+    // items at or before it; items behind it are never kept.
+    struct Cut {
+        Scored s{};
+        bool on = false;
+    };
+    Cut cut;
+    // Collector of the both-seen items of one part of an append: drops items
+    // behind its cutoff and, once it holds many, keeps only its best m (its
+    // m-th best becoming its cutoff), so a part stores O(m) items.
+    struct Sink {
+        std::vector<Scored>* out;
+        Cut cut;
+        size_t m;
+    };
+    Sink sink(std::vector<Scored>& out) const { return Sink{&out, cut, keep()}; }
+    void prune(std::vector<Scored>& v, size_t m, Cut& c) const {
+        std::nth_element(v.begin(), v.begin() + static_cast<std::ptrdiff_t>(m - 1), v.end(),
+                         [this](const Scored& a, const Scored& b) { return better(a, b); });
+        v.resize(m);
+        c.s = v[m - 1];
+        c.on = true;
+    }
+    static size_t prune_at(size_t m) { return m > (SIZE_MAX - 64) / 2 ? SIZE_MAX : 2 * m + 64; }
+    void offer(Sink& k, const Scored& x) const {
+        if (k.cut.on && !better(x, k.cut.s)) return;
+        k.out->push_back(x);
+        if (k.out->size() >= prune_at(k.m)) prune(*k.out, k.m, k.cut);
+    }
+
     // Back to an empty fusion with both lists open, keeping the memory.
     void reset() {
         for (auto& l : L) {
@@ -272,6 +318,7 @@ struct Fusion {
             l.cursor = 0;
         }
         both.clear();
+        cut = Cut{};
         A.clear();
         resolved = false;
         dup = false;
@@ -301,7 +348,7 @@ struct Fusion {
     // append run concurrently (the other list is not written meanwhile).
     template <bool Atomic>
     void direct_part(int i, const int64_t* ids, int64_t p0, int64_t j0, int64_t j1,
-                     std::vector<Scored>& out, bool& rep) {
+                     Sink& out, bool& rep) {
         List& me = L[i];
         List& other = L[1 - i];
         auto clear_bit = [](std::vector<uint64_t>& b, int64_t p) {
@@ -332,8 +379,8 @@ struct Fusion {
             clear_bit(other.alive, ro - 1);
             if (!fixed(x)) {
                 const int64_t r0 = (i == 0) ? rank : ro, r1 = (i == 0) ? ro : rank;
-                out.push_back(Scored{g_double(*P, 0, r0) + g_double(*P, 1, r1),
-                                     static_cast<int32_t>(r0), static_cast<int32_t>(r1), x});
+                offer(out, Scored{g_double(*P, 0, r0) + g_double(*P, 1, r1),
+                                 static_cast<int32_t>(r0), static_cast<int32_t>(r1), x});
             }
         }
     }
@@ -355,14 +402,18 @@ struct Fusion {
                         : 1;
         if (parts <= 1) {
             bool rep = false;
-            direct_part<false>(i, ids, p0, 0, n, both, rep);
+            fresh.clear();
+            Sink k = sink(fresh);
+            direct_part<false>(i, ids, p0, 0, n, k, rep);
             dup |= rep;
+            both.insert(both.end(), fresh.begin(), fresh.end());
         } else {
             std::vector<std::vector<Scored>> found(static_cast<size_t>(parts));
             std::vector<uint8_t> rep(static_cast<size_t>(parts), 0);
             parallel_for(parts, parts, [&](int64_t t) {
                 bool r = false;
-                direct_part<true>(i, ids, p0, n * t / parts, n * (t + 1) / parts, found[t], r);
+                Sink k = sink(found[t]);
+                direct_part<true>(i, ids, p0, n * t / parts, n * (t + 1) / parts, k, r);
                 rep[t] = r;
             });
             for (int t = 0; t < parts; ++t) {
@@ -376,6 +427,12 @@ struct Fusion {
     // Heap order after items were pushed behind position heap0: one push per
     // new item, or a linear rebuild when many were added.
     void restore_heap(size_t heap0) {
+        const size_t m = keep();
+        if (both.size() >= prune_at(m)) {
+            prune(both, m, cut);
+            std::make_heap(both.begin(), both.end(), HeapLess{P});
+            return;
+        }
         const size_t added = both.size() - heap0;
         if (added > heap0 / 8) {
             std::make_heap(both.begin(), both.end(), HeapLess{P});
@@ -430,7 +487,8 @@ struct Fusion {
         // merge-join with the other list: items now seen by both
         const size_t heap0 = both.size();
         std::vector<std::vector<Scored>> found(parts > 1 ? parts : 0);
-        auto join = [&](size_t a, size_t ae, size_t b, size_t be, std::vector<Scored>& out, bool atomic) {
+        auto join = [&](size_t a, size_t ae, size_t b, size_t be, std::vector<Scored>& items, bool atomic) {
+            Sink out = sink(items);
             // ids interleave at random: the advance is branch-free, only a
             // match (rarer) branches
             while (a < ae && b < be) {
@@ -451,8 +509,8 @@ struct Fusion {
                     const int64_t x = static_cast<int64_t>(xa);
                     if (!fixed(x)) {
                         const int64_t r0 = (i == 0) ? ri : rj, r1 = (i == 0) ? rj : ri;
-                        out.push_back(Scored{g_double(*P, 0, r0) + g_double(*P, 1, r1),
-                                             static_cast<int32_t>(r0), static_cast<int32_t>(r1), x});
+                        offer(out, Scored{g_double(*P, 0, r0) + g_double(*P, 1, r1),
+                                         static_cast<int32_t>(r0), static_cast<int32_t>(r1), x});
                     }
                     ++a;
                     ++b;
@@ -483,7 +541,9 @@ struct Fusion {
             return eq;
         };
         if (parts == 1) {
-            join(0, batch.size(), 0, ob.size(), both, false);
+            fresh.clear();
+            join(0, batch.size(), 0, ob.size(), fresh, false);
+            both.insert(both.end(), fresh.begin(), fresh.end());
             dup |= merge(0, me.by_id.size(), 0, batch.size());
         } else {
             std::vector<uint8_t> eq(parts, 0);
@@ -505,7 +565,7 @@ struct Fusion {
     // updates when parts of one append run concurrently.
     template <bool Atomic>
     void closed_part(int i, const int64_t* ids, int64_t p0, int64_t j0, int64_t j1,
-                     std::vector<Scored>& out, bool& rep) {
+                     Sink& out, bool& rep) {
         List& me = L[i];
         List& other = L[1 - i];
         auto clear_bit = [](std::vector<uint64_t>& b, int64_t p) {
@@ -532,8 +592,8 @@ struct Fusion {
             clear_bit(other.alive, ro - 1);
             if (!fixed(x)) {
                 const int64_t r0 = (i == 0) ? rank : ro, r1 = (i == 0) ? ro : rank;
-                out.push_back(Scored{g_double(*P, 0, r0) + g_double(*P, 1, r1),
-                                     static_cast<int32_t>(r0), static_cast<int32_t>(r1), x});
+                offer(out, Scored{g_double(*P, 0, r0) + g_double(*P, 1, r1),
+                                 static_cast<int32_t>(r0), static_cast<int32_t>(r1), x});
             }
         }
     }
@@ -555,14 +615,18 @@ struct Fusion {
                         : 1;
         if (parts <= 1) {
             bool rep = false;
-            closed_part<false>(i, ids, p0, 0, n, both, rep);
+            fresh.clear();
+            Sink k = sink(fresh);
+            closed_part<false>(i, ids, p0, 0, n, k, rep);
             dup |= rep;
+            both.insert(both.end(), fresh.begin(), fresh.end());
         } else {
             std::vector<std::vector<Scored>> found(static_cast<size_t>(parts));
             std::vector<uint8_t> rep(static_cast<size_t>(parts), 0);
             parallel_for(parts, parts, [&](int64_t t) {
                 bool r = false;
-                closed_part<true>(i, ids, p0, n * t / parts, n * (t + 1) / parts, found[t], r);
+                Sink k = sink(found[t]);
+                closed_part<true>(i, ids, p0, n * t / parts, n * (t + 1) / parts, k, r);
                 rep[t] = r;
             });
             for (int t = 0; t < parts; ++t) {

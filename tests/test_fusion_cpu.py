@@ -343,3 +343,24 @@ def test_frozen_schedule_hand_worked_case():
     top, st = eahr.eahr_fuse_lists(a, a, K=2, schedule="frozen")
     assert list(top) == [0, 1]
     assert (st["dense_depth"], st["sparse_depth"], st["rounds"]) == (48, 32, 2)
+
+
+@pytest.mark.parametrize("K", [1, 3, 20])
+def test_fuse_lists_exhausted_with_few_kept_both_seen_items(K):
+    """Nearly reversed lists of 300,000 ids are both read to the end, and
+    almost every id becomes seen by both lists in the last rounds (appends
+    split over host threads).  Only the best K - |A| + 1 of them can still be
+    fixed, so the fusion keeps those and drops the rest as they are found
+    (Sec. 2.2).  At equal weights mirrored ranks give equal F, decided by id,
+    and the heads tie until both lists end."""
+    rng = np.random.default_rng(21 + K)
+    n = 300_000
+    a = rng.permutation(n)
+    b = a[::-1].copy()
+    swap = np.flatnonzero(rng.random(n // 2) < 0.5) * 2
+    b[swap], b[swap + 1] = b[swap + 1].copy(), b[swap].copy()
+    for wts in ((1, 1), (2, 1)):
+        got, st = eahr.eahr_fuse_lists(a, b, K=K, w_dense=wts[0], w_sparse=wts[1])
+        assert list(got) == rrf.rrf_topk([a, b], list(wts), 60, K)
+        if wts == (1, 1):   # the mirrored heads tie until both lists end
+            assert st["dense_status"] == eahr.LIST_EXHAUSTED and st["sparse_status"] == eahr.LIST_EXHAUSTED
