@@ -358,7 +358,14 @@ struct Fusion {
         };
         int32_t* mine = pos[i].data();
         const int32_t* theirs = pos[1 - i].data();
+        // the rank arrays are read at random ids: fetch a few ids ahead
+        constexpr int64_t kAhead = 16;
         for (int64_t j = j0; j < j1; ++j) {
+            if (j + kAhead < j1) {
+                const int64_t y = ids[j + kAhead];
+                __builtin_prefetch(mine + y, 1, 0);
+                __builtin_prefetch(theirs + y, 0, 0);
+            }
             const int64_t x = ids[j];
             const int64_t rank = p0 + j + 1;
             int32_t prev;
