@@ -35,11 +35,13 @@
 // order only for the items it holds), and repeats with a second bitmap.
 //
 // Once the lists together hold at least 1/16 of the id range [0, universe)
-// (when the caller knows it), both lists switch to direct rank arrays
-// indexed by id: an append then costs O(ranks appended) whatever the depth,
-// where a merge into the id order costs O(depth).  This keeps schedules that
-// append few ranks at a time to deep lists (checks every 16 ranks, the
-// frozen scheduler) linear in the depth reached.
+// (when the caller knows it) while both are open, both lists switch to direct
+// rank arrays indexed by id: an append then costs O(ranks appended) whatever
+// the depth, where a merge into the id order costs O(depth).  This keeps
+// schedules that append few ranks at a time to deep lists (checks every 16
+// ranks, the frozen scheduler) linear in the depth reached.  A list appended
+// after the other closed stays with the bitmaps, which are also linear and
+// touch a bit per id instead of two rank arrays of 4 bytes per id.
 //
 // A long append (either kind) is split over `threads` host threads: the sort
 // by id digit by digit, the joins and merges over ranges of ids (equal ids
@@ -50,6 +52,8 @@
 #include <algorithm>
 #include <cstddef>
 #include <cstdint>
+#include <memory>
+#include <utility>
 #include <vector>
 
 #include "host_parallel.h"
@@ -187,9 +191,30 @@ inline double g_double(const Params& P, int i, int64_t r) {
     return static_cast<double>(P.w[i]) / static_cast<double>(r + P.w[i] * (P.k - 1));
 }
 
+// Leaves new elements of a vector uninitialised on resize (they are written
+// right after, in parallel for long appends).
+template <typename T>
+struct NoInit : std::allocator<T> {
+    template <typename U>
+    struct rebind {
+        using other = NoInit<U>;
+    };
+    NoInit() = default;
+    template <typename U>
+    NoInit(const NoInit<U>&) noexcept {}
+    template <typename U>
+    void construct(U* p) noexcept {
+        ::new (static_cast<void*>(p)) U;
+    }
+    template <typename U, typename... A>
+    void construct(U* p, A&&... a) {
+        ::new (static_cast<void*>(p)) U(std::forward<A>(a)...);
+    }
+};
+
 struct Fusion {
     struct List {
-        std::vector<int64_t> ids;      // exact prefix read so far
+        std::vector<int64_t, NoInit<int64_t>> ids;   // exact prefix read so far
         std::vector<uint64_t> by_id;   // (id << 32 | rank), ascending id
         std::vector<uint64_t> alive;   // bit p: position p is an unfixed single-list item
         bool open = true;
@@ -453,7 +478,9 @@ struct Fusion {
     // and the bookkeeping is no longer meaningful).
     void append(int i, const int64_t* ids, int64_t n) {
         if (n <= 0) return;
-        if (!direct && universe > 0 && (L[0].size() + L[1].size() + n) * kDirectShare >= universe)
+        // (with the other list closed the bitmaps already cost O(n) per append)
+        if (!direct && L[1 - i].open && universe > 0 &&
+            (L[0].size() + L[1].size() + n) * kDirectShare >= universe)
             enter_direct_mode();
         if (direct) {
             append_direct(i, ids, n);
@@ -611,15 +638,25 @@ struct Fusion {
         List& me = L[i];
         const int64_t p0 = me.size();
         me.grow(n);
-        me.ids.insert(me.ids.end(), ids, ids + n);
         const size_t heap0 = both.size();
-        int64_t xmax = 0;
-        for (int64_t j = 0; j < n; ++j) xmax = std::max(xmax, ids[j]);
-        const size_t words = static_cast<size_t>(xmax >> 6) + 1;
-        if (seen[i].size() < words) seen[i].resize(std::max(words, seen[i].size() * 2), 0);
         const int parts = (threads > 1 && n >= kParallelAppend)
                         ? static_cast<int>(std::min<int64_t>(threads, n / (kParallelAppend / 4)))
                         : 1;
+        // the ids join the list and give the largest id (in parts when long)
+        me.ids.resize(static_cast<size_t>(p0 + n));
+        std::vector<int64_t> part_max(static_cast<size_t>(parts), 0);
+        parallel_for(parts, parts, [&](int64_t t) {
+            int64_t m = 0;
+            int64_t* dst = me.ids.data() + p0;
+            for (int64_t j = n * t / parts, e = n * (t + 1) / parts; j < e; ++j) {
+                dst[j] = ids[j];
+                m = std::max(m, ids[j]);
+            }
+            part_max[t] = m;
+        });
+        const int64_t xmax = *std::max_element(part_max.begin(), part_max.end());
+        const size_t words = static_cast<size_t>(xmax >> 6) + 1;
+        if (seen[i].size() < words) seen[i].resize(std::max(words, seen[i].size() * 2), 0);
         if (parts <= 1) {
             bool rep = false;
             fresh.clear();

@@ -364,3 +364,74 @@ def test_fuse_lists_exhausted_with_few_kept_both_seen_items(K):
         assert list(got) == rrf.rrf_topk([a, b], list(wts), 60, K)
         if wts == (1, 1):   # the mirrored heads tie until both lists end
             assert st["dense_status"] == eahr.LIST_EXHAUSTED and st["sparse_status"] == eahr.LIST_EXHAUSTED
+
+
+def _fusion_modes_exe(tmp_path_factory):
+    import shutil
+    import subprocess
+    if shutil.which("g++") is None:
+        pytest.skip("needs g++")
+    here = os.path.dirname(os.path.abspath(__file__))
+    exe = tmp_path_factory.mktemp("fusion_modes") / "fusion_modes"
+    subprocess.run(["g++", "-O2", "-std=c++17", "-pthread", "-I",
+                    os.path.join(here, "..", "paper_2608_07152_amd", "csrc"),
+                    os.path.join(here, "native", "fusion_modes.cpp"), "-o", str(exe)], check=True)
+    return exe
+
+
+@pytest.fixture(scope="module")
+def fusion_modes(tmp_path_factory):
+    return _fusion_modes_exe(tmp_path_factory)
+
+
+def _run_modes(exe, tmp_path, a, b, K, wts, threads):
+    import subprocess
+    pa, pb = tmp_path / "a.bin", tmp_path / "b.bin"
+    np.asarray(a, dtype=np.int64).tofile(pa)
+    np.asarray(b, dtype=np.int64).tofile(pb)
+    r = subprocess.run([str(exe), str(pa), str(pb), str(K), "60", str(wts[0]), str(wts[1]), str(threads)],
+                       capture_output=True, text=True, timeout=600)
+    assert r.returncode == 0, r.stderr
+    out = r.stdout.split()
+    if out == ["dup"]:
+        return out, None
+    return [int(x) for x in out], [int(x) for x in r.stderr.split()[1:3]]
+
+
+@pytest.mark.parametrize("threads", [1, 8])
+@pytest.mark.parametrize("closed", ["sparse", "dense"])
+def test_fusion_reads_deep_after_one_list_closed(fusion_modes, tmp_path, threads, closed):
+    """Depth doubling with the id range unknown (as eahr_topk runs it): one
+    short list closes early and the other is read to depth 524,288 with the
+    bitmaps, in parts by position over host threads when long; the fixed
+    Top-K equals complete-list RRF (Sec. 2.1, 2.2), and a repeat deep in the
+    open list is reported."""
+    rng = np.random.default_rng(31)
+    n = 600_000
+    a = rng.permutation(n)
+    short = rng.permutation(np.concatenate([a[n - 250_000:n - 247_000], rng.choice(a[:1000], 40, replace=False)]))
+    for K, wts in ((20, (1, 1)), (5, (2, 1))):
+        lists = (a, short) if closed == "sparse" else (short, a)
+        got, depth = _run_modes(fusion_modes, tmp_path, *lists, K, wts, threads)
+        assert got == rrf.rrf_topk(list(lists), list(wts), 60, K), (K, wts)
+        long_side = 0 if closed == "sparse" else 1
+        assert depth[1 - long_side] == len(short) and depth[long_side] > 300_000, depth
+    bad = np.concatenate([a[:400_000], a[300_000:300_001], a[400_000:]])
+    lists = (bad, short) if closed == "sparse" else (short, bad)
+    assert _run_modes(fusion_modes, tmp_path, *lists, 20, (1, 1), threads)[0] == ["dup"]
+
+
+@pytest.mark.parametrize("threads", [1, 8])
+def test_fusion_reads_deep_with_both_lists_open(fusion_modes, tmp_path, threads):
+    """Both lists stay open while read deep: the id-order merges, split over
+    host threads when long; the Top-K equals complete-list RRF."""
+    rng = np.random.default_rng(32)
+    n = 400_000
+    a = rng.permutation(n)
+    b = a.copy()
+    for s0 in range(0, n, 40_000):
+        b[s0:s0 + 40_000] = rng.permutation(b[s0:s0 + 40_000])
+    b = np.concatenate([b[150_000:], b[:150_000]])
+    got, depth = _run_modes(fusion_modes, tmp_path, a, b, 20, (1, 1), threads)
+    assert got == rrf.rrf_topk([a, b], [1, 1], 60, 20)
+    assert min(depth) > 100_000, depth
