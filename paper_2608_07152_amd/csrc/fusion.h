@@ -191,27 +191,6 @@ inline double g_double(const Params& P, int i, int64_t r) {
     return static_cast<double>(P.w[i]) / static_cast<double>(r + P.w[i] * (P.k - 1));
 }
 
-// Leaves new elements of a vector uninitialised on resize (they are written
-// right after, in parallel for long appends).
-template <typename T>
-struct NoInit : std::allocator<T> {
-    template <typename U>
-    struct rebind {
-        using other = NoInit<U>;
-    };
-    NoInit() = default;
-    template <typename U>
-    NoInit(const NoInit<U>&) noexcept {}
-    template <typename U>
-    void construct(U* p) noexcept {
-        ::new (static_cast<void*>(p)) U;
-    }
-    template <typename U, typename... A>
-    void construct(U* p, A&&... a) {
-        ::new (static_cast<void*>(p)) U(std::forward<A>(a)...);
-    }
-};
-
 struct Fusion {
     struct List {
         std::vector<int64_t, NoInit<int64_t>> ids;   // exact prefix read so far

@@ -5,8 +5,10 @@
 #include <condition_variable>
 #include <cstdint>
 #include <functional>
+#include <memory>
 #include <mutex>
 #include <thread>
+#include <utility>
 #include <vector>
 
 namespace eahr {
@@ -124,6 +126,41 @@ void parallel_for(int64_t n, int threads, F&& f) {
     const std::function<void(int64_t)> work = [&](int64_t i) { f(i); };
     const int extra = static_cast<int>(std::min<int64_t>(threads, n)) - 1;
     WorkerPool::get().run(n, extra, work);
+}
+
+// Allocator that leaves new elements of a vector uninitialised on resize
+// (for buffers written right after, in parallel when long).
+template <typename T>
+struct NoInit : std::allocator<T> {
+    template <typename U>
+    struct rebind {
+        using other = NoInit<U>;
+    };
+    NoInit() = default;
+    template <typename U>
+    NoInit(const NoInit<U>&) noexcept {}
+    template <typename U>
+    void construct(U* p) noexcept {
+        ::new (static_cast<void*>(p)) U;
+    }
+    template <typename U, typename... A>
+    void construct(U* p, A&&... a) {
+        ::new (static_cast<void*>(p)) U(std::forward<A>(a)...);
+    }
+};
+
+// f(i, lo, hi) over [0, n[i]) of every item i, cut into pieces of at most
+// `piece` elements that run on up to `threads` threads: a few long items
+// use every thread, many short ones one each.
+template <typename F>
+void parallel_pieces(const std::vector<int64_t>& n, int64_t piece, int threads, F&& f) {
+    struct Piece {
+        int64_t i, lo, hi;
+    };
+    std::vector<Piece> ps;
+    for (int64_t i = 0; i < static_cast<int64_t>(n.size()); ++i)
+        for (int64_t lo = 0; lo < n[i]; lo += piece) ps.push_back(Piece{i, lo, std::min(n[i], lo + piece)});
+    parallel_for(static_cast<int64_t>(ps.size()), threads, [&](int64_t k) { f(ps[k].i, ps[k].lo, ps[k].hi); });
 }
 
 }  // namespace eahr

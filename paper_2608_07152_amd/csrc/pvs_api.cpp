@@ -1128,15 +1128,21 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
         g_prof.scan_rounds += 1;
     }
 
-    // append the certified keys of every query to its cache (in parallel)
+    // append the certified keys of every query to its cache, in pieces over
+    // the host threads (a few deep queries use them all)
     std::vector<uint8_t> usable(nq, 0);
-    for (int32_t i = 0; i < nq; ++i)
+    std::vector<int64_t> grow(nq, 0), at(nq, 0);
+    for (int32_t i = 0; i < nq; ++i) {
         usable[i] = !h_fail[i] && cert_all[i] == h_cert[i];
-    eahr::parallel_for(nq, eahr::host_threads(), [&](int64_t i) {
-        if (!usable[i] || h_cert[i] == 0) return;
-        const uint64_t* kp = st->h_packed + h_offs[i];
+        if (!usable[i] || h_cert[i] == 0) continue;
         auto& c = st->q[todo[i]].cache;
-        c.insert(c.end(), kp, kp + h_cert[i]);
+        at[i] = static_cast<int64_t>(c.size());
+        grow[i] = h_cert[i];
+        c.resize(c.size() + static_cast<size_t>(h_cert[i]));
+    }
+    eahr::parallel_pieces(grow, int64_t(1) << 18, eahr::host_threads(), [&](int64_t i, int64_t lo, int64_t hi) {
+        std::memcpy(st->q[todo[i]].cache.data() + at[i] + lo, st->h_packed + h_offs[i] + lo,
+                    static_cast<size_t>(hi - lo) * sizeof(uint64_t));
     });
     if (trace) {
         tp[5] = clk::now();
@@ -1208,31 +1214,35 @@ extern "C" int pvs_next(pvs_state* st, int32_t m, const uint8_t* active, int64_t
         if (guard > 200) EAHR_FAIL(EAHR_E_HIP, "pvs_next: scan loop did not converge");
         EAHR_TRY(scan_round(st, todo, m));
     }
-    // decode the emitted ranks of every query (in parallel)
+    // decode the emitted ranks of every query, in pieces over the host threads
     std::vector<int64_t> took(B, 0);
-    eahr::parallel_for(B, eahr::host_threads(), [&](int64_t b) {
-        if (active && !active[b]) return;
-        auto& Q = st->q[b];
+    for (int32_t b = 0; b < B; ++b) {
+        if (active && !active[b]) continue;
+        const auto& Q = st->q[b];
         if (Q.failed) {
             count[b] = 0;
             status[b] = EAHR_LIST_FAILED;
-            return;
+            continue;
         }
-        const int64_t avail = static_cast<int64_t>(Q.cache.size()) - Q.emitted;
-        const int64_t take = std::min<int64_t>(m, avail);
-        const uint64_t* kp = Q.cache.data() + Q.emitted;
+        took[b] = std::min<int64_t>(m, static_cast<int64_t>(Q.cache.size()) - Q.emitted);
+    }
+    eahr::parallel_pieces(took, int64_t(1) << 17, eahr::host_threads(), [&](int64_t b, int64_t lo, int64_t hi) {
+        const uint64_t* kp = st->q[b].cache.data() + st->q[b].emitted;
         int64_t* oi = ids + b * static_cast<int64_t>(m);
         float* os = scores + b * static_cast<int64_t>(m);
-        for (int64_t j = 0; j < take; ++j) {
+        for (int64_t j = lo; j < hi; ++j) {
             oi[j] = key_id(kp[j]);
             os[j] = key_score(kp[j]);
         }
-        Q.emitted += take;
-        took[b] = take;
-        count[b] = static_cast<int32_t>(take);
-        status[b] = (Q.emitted >= st->n_vis) ? EAHR_LIST_EXHAUSTED : EAHR_LIST_OPEN;
     });
-    for (int32_t b = 0; b < B; ++b) st->stats.emitted += took[b];
+    for (int32_t b = 0; b < B; ++b) {
+        if ((active && !active[b]) || st->q[b].failed) continue;
+        auto& Q = st->q[b];
+        Q.emitted += took[b];
+        count[b] = static_cast<int32_t>(took[b]);
+        status[b] = (Q.emitted >= st->n_vis) ? EAHR_LIST_EXHAUSTED : EAHR_LIST_OPEN;
+        st->stats.emitted += took[b];
+    }
     return EAHR_OK;
 }
 

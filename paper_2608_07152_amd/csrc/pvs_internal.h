@@ -7,7 +7,12 @@
 #include <vector>
 
 #include "eahr.h"
+#include "host_parallel.h"
 #include "pvs_kernels.h"
+
+// A query's certified ranks as sort keys; grown without zero-filling (the
+// keys are copied in right after).
+using KeyCache = std::vector<uint64_t, ::eahr::NoInit<uint64_t>>;
 
 namespace pvs {
 // Threshold estimation samples every stride-th code block, with the stride
@@ -95,7 +100,7 @@ struct ScanBuffers {
     uint64_t* h_packed = nullptr;
     int64_t h_packed_cap = 0;
     // certified-rank caches of the closed state (emptied, capacity kept)
-    std::vector<std::vector<uint64_t>> caches;
+    std::vector<KeyCache> caches;
 };
 
 struct pvs_index {
@@ -139,7 +144,7 @@ struct pvs_state {
         int32_t id_cert = -1;
         // certified ranks in order, as their sort keys (~mono(s32) << 32 | id);
         // ids and scores are decoded only when emitted
-        std::vector<uint64_t> cache;
+        KeyCache cache;
         int64_t emitted = 0;            // ranks returned by pvs_next
         bool failed = false;
         bool cert_exhausted = false;    // every visible row certified
@@ -158,7 +163,7 @@ struct pvs_state {
     float *qscale = nullptr, *qnorm = nullptr, *qenorm = nullptr, *qhnorm = nullptr;
     uint32_t* qflags = nullptr;
     std::vector<Query> q;
-    std::vector<std::vector<uint64_t>> recycled;   // caches adopted from the index
+    std::vector<KeyCache> recycled;   // caches adopted from the index
     pvs_counters stats{};
     // per-query scan buffers, sized for buf_nq queries and buf_sample rows
     int32_t buf_nq = 0;
