@@ -1053,7 +1053,7 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
 
     // 3. rescore, order and pack the certified ranks
     const int64_t chunks = pvs::rescore_chunks(h_pcnt, pair_sub);
-    pvs::launch_rescore(v, st->qrows, st->scanq, d_pcnt, st->pairs, pair_sub, d_cbase, chunks,
+    pvs::launch_rescore(v, st->qrows, st->scanq, nq, d_pcnt, st->pairs, pair_sub, d_cbase, chunks,
                         ix->gamma, st->keys, d_cert, d_fail, d_reads, st->test_fail_qi, s);
     EAHR_TRY(mark(4));
     // only the certified keys are ordered; a query whose key region overflowed

@@ -117,10 +117,12 @@ void launch_select(const float* sample_lo, const float* sample_hi, int64_t n, in
 // row_reads[s * kCntStride] (zeroed by the caller) sum to the number of row
 // loads, one per run of records of one row inside a wavefront's share.
 // fail_qi (tests only, -1 otherwise): the state query whose rescored scores
-// are judged against a zero-width interval, so that its list fails.
+// are judged against a zero-width interval, so that its list fails.  nq: the
+// scan's queries (records refer to sq[0, nq)); when their float32 query rows
+// fit in LDS, workgroups copy them there once instead of reloading them.
 constexpr int kRescoreChunk = 256;
 int64_t rescore_chunks(const int32_t* pair_cnt, int64_t pair_sub);
-void launch_rescore(const IndexView& ix, const float* qrows, const ScanQ* sq,
+void launch_rescore(const IndexView& ix, const float* qrows, const ScanQ* sq, int32_t nq,
                     const int32_t* pair_cnt, const uint4* pairs, int64_t pair_sub,
                     int32_t* cbase, int64_t chunks, float gamma, uint64_t* keys,
                     int32_t* cert_cnt, int32_t* fail, int32_t* row_reads, int32_t fail_qi,

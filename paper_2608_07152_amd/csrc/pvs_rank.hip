@@ -10,6 +10,7 @@
 // descending, id ascending).  Keys are unique inside a query; the segmented
 // sort orders each query's certified keys.
 #include <algorithm>
+#include <atomic>
 
 #include "pvs_device.h"
 
@@ -30,20 +31,20 @@ __global__ __launch_bounds__(64) void k_chunk_base(const int32_t* __restrict__ p
     }
 }
 
-// One workgroup per chunk, one wavefront per quarter of it.  Lane j holds the
-// wavefront's record j and everything about it that does not need the score:
-// its interval (the scan's arithmetic on the same inputs, so identical to the
-// scan's), its query's threshold and last certified key.  Each 16-lane group
-// g then scores records 16 g .. 16 g + 15 one after another (the group's
-// lanes hold the record's row and query row in the fixed order of the
-// authoritative score, so four records are scored at once), and the record's
-// own lane judges its score.  Records of one row are adjacent, so a group
-// loads the row once for them; likewise the query row.  At the end the keys
-// of each query are appended to its region with one atomic.
+// The records of quarter `wave` of chunk x (one wavefront, 64 records).
+// Lane j first prepares record j (its interval from the recorded dot with
+// the scan's arithmetic, its query's tau and last certified key); each
+// 16-lane group g then scores records 16 g .. 16 g + 15 one after another
+// (the group's lanes hold the record's row and query row in the fixed order
+// of the authoritative score, so four records are scored at once), and the
+// record's own lane judges its score.  Records of one row are adjacent, so a
+// group loads the row once for them; likewise the query row, which comes
+// from LDS (slot = the record's query in the scan) when LDSQ.  At the end
+// the keys of each query are appended to its region with one atomic.
 // J: chunks per lane (0: rows scored in segments); FULL: df / 4 == 16 J.
-template <int J, bool FULL>
-__global__ __launch_bounds__(256) void k_rescore(
-    const float4* __restrict__ rows, int32_t df4, const float4* __restrict__ qrows,
+template <int J, bool FULL, bool LDSQ>
+__device__ __forceinline__ void rescore_quarter(
+    int x, int wave, const float4* __restrict__ rows, int32_t df4, const float4* __restrict__ qsrc,
     const ScanQ* __restrict__ sq, const int32_t* __restrict__ cbase,
     const int32_t* __restrict__ pair_cnt, const uint4* __restrict__ pairs, int64_t pair_sub,
     const float* __restrict__ scale, const float* __restrict__ vnorm,
@@ -53,9 +54,7 @@ __global__ __launch_bounds__(256) void k_rescore(
     constexpr int PER_WAVE = kRescoreChunk / 4;
     static_assert(PER_WAVE == 64, "one record per lane");
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
     // the sub-region of this chunk: the last s with cbase[s] <= chunk
-    const int x = blockIdx.x;
     int slo = 0, shi = kSub;
     while (shi - slo > 1) {
         const int mid = (slo + shi) >> 1;
@@ -99,7 +98,7 @@ __global__ __launch_bounds__(256) void k_rescore(
             constexpr int i = decltype(I_)::value;
             // the group's record i, held by lane 16 g + i
             const int32_t row = bcast16<i>(my_row);
-            const int32_t qi = bcast16<i>(my_qi);
+            const int32_t qi = bcast16<i>(LDSQ ? my_b : my_qi);   // LDSQ: the LDS slot
             if (16 * g + i < n) {   // the same in every lane of the group
                 float sc;
                 if constexpr (J > 0) {
@@ -108,14 +107,14 @@ __global__ __launch_bounds__(256) void k_rescore(
                         prow = row;
                         ++reads;
                     }
-                    if (qi != pqi) {
-                        load_chunks<J, FULL>(qrows + static_cast<int64_t>(qi) * df4, j, df4, q);
+                    if (qi != pqi) {   // from LDS when LDSQ
+                        load_chunks<J, FULL>(qsrc + static_cast<int64_t>(qi) * df4, j, df4, q);
                         pqi = qi;
                     }
                     sc = group_dot<J, FULL>(v, q, j, df4);
                 } else {
                     sc = group_score_seg(rows + static_cast<int64_t>(row) * df4,
-                                         qrows + static_cast<int64_t>(qi) * df4, j, df4);
+                                         qsrc + static_cast<int64_t>(qi) * df4, j, df4);
                     ++reads;
                 }
                 if (j == i) {
@@ -160,17 +159,75 @@ __global__ __launch_bounds__(256) void k_rescore(
     if (pos < kSub * MQ.cand_cap) keys[MQ.cand_off + pos] = mykey;
 }
 
+// One wavefront per quarter of a chunk of kRescoreChunk records.  LDSQ: a
+// workgroup of sixteen wavefronts takes four chunks and first copies the
+// scan's nq float32 query rows to LDS, and the groups read their query rows
+// from there instead of reloading them from L2 per record (the loads that
+// bound the kernel when records of one row belong to different queries).
+// Workgroups that each loop over many chunks after one copy measured slower
+// (on a three-query scan, 9.3 against 3.8 ms).
+template <int J, bool FULL, bool LDSQ>
+__global__ __launch_bounds__(LDSQ ? 1024 : 256) void k_rescore(
+    const float4* __restrict__ rows, int32_t df4, const float4* __restrict__ qrows,
+    const ScanQ* __restrict__ sq, int32_t nq, const int32_t* __restrict__ cbase,
+    const int32_t* __restrict__ pair_cnt, const uint4* __restrict__ pairs, int64_t pair_sub,
+    const float* __restrict__ scale, const float* __restrict__ vnorm,
+    const float* __restrict__ enorm, float gamma, uint64_t* __restrict__ keys,
+    int32_t* __restrict__ cert_cnt, int32_t* __restrict__ fail, int32_t* __restrict__ row_reads,
+    int32_t fail_qi) {
+    if constexpr (LDSQ) {
+        extern __shared__ float4 s_q[];   // query row b at s_q[b * df4]
+        for (int k = threadIdx.x; k < nq * df4; k += blockDim.x) {
+            const int b = k / df4;
+            s_q[k] = qrows[static_cast<int64_t>(sq[b].qi) * df4 + (k - b * df4)];
+        }
+        __syncthreads();
+        const int x = static_cast<int>(blockIdx.x) * 4 + static_cast<int>(threadIdx.x >> 8);
+        if (x < cbase[kSub])
+            rescore_quarter<J, FULL, true>(x, (threadIdx.x >> 6) & 3, rows, df4, s_q, sq, cbase, pair_cnt, pairs,
+                                           pair_sub, scale, vnorm, enorm, gamma, keys, cert_cnt, fail, row_reads,
+                                           fail_qi);
+    } else {
+        rescore_quarter<J, FULL, false>(blockIdx.x, threadIdx.x >> 6, rows, df4, qrows, sq, cbase, pair_cnt, pairs,
+                                        pair_sub, scale, vnorm, enorm, gamma, keys, cert_cnt, fail, row_reads,
+                                        fail_qi);
+    }
+}
+
+// LDS of the query-row variant: at most a gfx950 CU's 160 KiB.
+constexpr size_t kRescoreLdsMax = 160 * 1024;
+
 template <int J, bool FULL>
-static void rescore_j(const IndexView& ix, const float* qrows, const ScanQ* sq,
+static void rescore_j(const IndexView& ix, const float* qrows, const ScanQ* sq, int32_t nq,
                       const int32_t* cbase, int64_t chunks, const int32_t* pair_cnt,
                       const uint4* pairs, int64_t pair_sub, float gamma, uint64_t* keys,
                       int32_t* cert_cnt, int32_t* fail, int32_t* row_reads, int32_t fail_qi,
                       hipStream_t stream) {
-    hipLaunchKernelGGL((k_rescore<J, FULL>), dim3(static_cast<uint32_t>(chunks)), dim3(256), 0, stream,
-                       reinterpret_cast<const float4*>(ix.rows), ix.df / 4,
-                       reinterpret_cast<const float4*>(qrows), sq, cbase, pair_cnt, pairs,
-                       pair_sub, ix.scale, ix.vnorm, ix.enorm, gamma, keys, cert_cnt, fail,
-                       row_reads, fail_qi);
+    const int32_t df4 = ix.df / 4;
+    const size_t lds = static_cast<size_t>(nq) * df4 * sizeof(float4);
+    // one query: its row stays in the groups' registers anyway
+    if constexpr (J > 0) {
+        static std::atomic<int> ready{0};   // 1: LDS attribute set, -1: refused
+        if (nq > 1 && lds <= kRescoreLdsMax && ready.load() == 0) {
+            const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_rescore<J, FULL, true>),
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                     static_cast<int>(kRescoreLdsMax));
+            ready.store(e == hipSuccess ? 1 : -1);
+            if (e != hipSuccess) (void)hipGetLastError();
+        }
+        if (nq > 1 && lds <= kRescoreLdsMax && ready.load() > 0) {
+            const uint32_t groups = static_cast<uint32_t>((chunks + 3) / 4);
+            hipLaunchKernelGGL((k_rescore<J, FULL, true>), dim3(groups), dim3(1024), lds, stream,
+                               reinterpret_cast<const float4*>(ix.rows), df4,
+                               reinterpret_cast<const float4*>(qrows), sq, nq, cbase, pair_cnt, pairs, pair_sub,
+                               ix.scale, ix.vnorm, ix.enorm, gamma, keys, cert_cnt, fail, row_reads, fail_qi);
+            return;
+        }
+    }
+    hipLaunchKernelGGL((k_rescore<J, FULL, false>), dim3(static_cast<uint32_t>(chunks)), dim3(256), 0, stream,
+                       reinterpret_cast<const float4*>(ix.rows), df4, reinterpret_cast<const float4*>(qrows), sq,
+                       nq, cbase, pair_cnt, pairs, pair_sub, ix.scale, ix.vnorm, ix.enorm, gamma, keys, cert_cnt,
+                       fail, row_reads, fail_qi);
 }
 
 int64_t rescore_chunks(const int32_t* pair_cnt, int64_t pair_sub) {
@@ -182,7 +239,7 @@ int64_t rescore_chunks(const int32_t* pair_cnt, int64_t pair_sub) {
     return c;
 }
 
-void launch_rescore(const IndexView& ix, const float* qrows, const ScanQ* sq,
+void launch_rescore(const IndexView& ix, const float* qrows, const ScanQ* sq, int32_t nq,
                     const int32_t* pair_cnt, const uint4* pairs, int64_t pair_sub,
                     int32_t* cbase, int64_t chunks, float gamma, uint64_t* keys,
                     int32_t* cert_cnt, int32_t* fail, int32_t* row_reads, int32_t fail_qi,
@@ -191,14 +248,14 @@ void launch_rescore(const IndexView& ix, const float* qrows, const ScanQ* sq,
     if (chunks <= 0) return;
     const int J = group_chunks(ix.df);
     const bool full = J > 0 && ix.df / 4 == 16 * J;
-#define PVS_RS(N)                                                                                  \
-    case N:                                                                                        \
-        if (full)                                                                                  \
-            rescore_j<N, true>(ix, qrows, sq, cbase, chunks, pair_cnt, pairs, pair_sub, gamma, keys, \
-                               cert_cnt, fail, row_reads, fail_qi, stream);                        \
-        else                                                                                       \
-            rescore_j<N, false>(ix, qrows, sq, cbase, chunks, pair_cnt, pairs, pair_sub, gamma,     \
-                                keys, cert_cnt, fail, row_reads, fail_qi, stream);                 \
+#define PVS_RS(N)                                                                                      \
+    case N:                                                                                            \
+        if (full)                                                                                      \
+            rescore_j<N, true>(ix, qrows, sq, nq, cbase, chunks, pair_cnt, pairs, pair_sub, gamma, keys, \
+                               cert_cnt, fail, row_reads, fail_qi, stream);                            \
+        else                                                                                           \
+            rescore_j<N, false>(ix, qrows, sq, nq, cbase, chunks, pair_cnt, pairs, pair_sub, gamma,     \
+                                keys, cert_cnt, fail, row_reads, fail_qi, stream);                     \
         break;
     switch (J) {
         PVS_RS(1)
@@ -210,7 +267,7 @@ void launch_rescore(const IndexView& ix, const float* qrows, const ScanQ* sq,
         PVS_RS(12)
         PVS_RS(16)
         default:
-            rescore_j<0, false>(ix, qrows, sq, cbase, chunks, pair_cnt, pairs, pair_sub, gamma, keys,
+            rescore_j<0, false>(ix, qrows, sq, nq, cbase, chunks, pair_cnt, pairs, pair_sub, gamma, keys,
                                 cert_cnt, fail, row_reads, fail_qi, stream);
             break;
     }
