@@ -907,7 +907,8 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
         const int64_t have = static_cast<int64_t>(Q.cache.size());
         const int64_t avail = have - Q.emitted;
         const int64_t need = std::max<int64_t>(1, m - avail);
-        const int64_t spec = std::min(std::max(pvs::kSpecFactor * (Q.emitted + m), pvs::kSpecFloor) - have,
+        const int64_t spec_floor = std::max(pvs::kSpecFloor, pvs::kSpecFloorBudget / nq);
+        const int64_t spec = std::min(std::max(pvs::kSpecFactor * (Q.emitted + m), spec_floor) - have,
                                       pvs::kSpecBudget / nq);
         const int64_t target = std::max({need, mmin, spec}) + lower_overlap(st, b);
         double k = (stride == 1) ? static_cast<double>(target)

@@ -46,12 +46,17 @@ constexpr int64_t kTargetBudget = 8192;
 // to an extra scan.  Measured on 8.8M x 768 (queries/s at batch 256 / 1 / 64):
 // factor 8 and 2^20 ranks 1,860 / 90 / 1,085; 8 and 2^22 2,355 / 106 / 1,128;
 // 16 and 2^22 2,338 / 117 / 1,241; 2^23 and 2^24 are slower again.
-// A scan certifies at least kSpecFloor ranks per query (within the same
-// budget): a round of a batch scan costs about as much as rescoring a few
-// thousand ranks per query, so shallow requests are served ahead.
+// A scan certifies at least max(kSpecFloor, kSpecFloorBudget / queries)
+// ranks per query (within the same budget): a round of a batch scan costs
+// about as much as rescoring a few thousand ranks per query, and a round of
+// a single-query scan (the whole code array streamed once) as much as
+// rescoring about 10^5, so shallow requests are served ahead.  Measured on
+// 8.8M x 768, single requests: floor budget 2^16 179 queries/s, 2^17 252,
+// 2^18 247 (4096 alone: 182; batches of 64 and 256 unchanged).
 constexpr int64_t kSpecFactor = 16;
 constexpr int64_t kSpecBudget = int64_t(1) << 22;
 constexpr int64_t kSpecFloor = 4096;
+constexpr int64_t kSpecFloorBudget = int64_t(1) << 17;
 // Scans of at least this many queries use the Int8 MFMA kernel; smaller ones
 // the dot4 GEMV kernel, which streams the codes at the HBM rate for up to 8
 // queries in one pass.  EAHR_SCAN_PATH=gemv|mfma forces one path (testing).
