@@ -84,3 +84,23 @@ def test_scores_follow_the_fixed_order_bit_for_bit(E, d):
         for k in range(cnt[b]):
             want = r6_score(q[b], x[ids[b, k]])
             assert np.array(sc[b, k], F32).view(np.int32) == np.array(want, F32).view(np.int32)
+
+
+@pytest.mark.parametrize("d", [128, 768])
+@pytest.mark.parametrize("B", [1, 2, 60])
+def test_rescored_scores_follow_the_fixed_order_bit_for_bit(E, d, B):
+    """The emitted scores come from rescoring, which holds a one-query scan's
+    query row in registers, reads the query rows of a scan from LDS when they
+    fit (two queries at d = 128 and 768, sixty at d = 128) and from memory
+    otherwise (sixty at d = 768): every path follows the fixed order."""
+    w = datagen.workload("tiny", n=400, d=d)
+    x, _ = datagen.corpus(w)
+    q, _ = datagen.queries(w, count=B)
+    idx = E.pvs_build(x)
+    st = E.pvs_open(idx, q)
+    ids, sc, cnt, _ = E.pvs_next(st, 4)
+    for b in sorted({0, B // 2, B - 1}):
+        assert cnt[b] == 4
+        for k in range(cnt[b]):
+            want = r6_score(q[b], x[ids[b, k]])
+            assert np.array(sc[b, k], F32).view(np.int32) == np.array(want, F32).view(np.int32), (b, k)
