@@ -52,7 +52,9 @@ constexpr int64_t kTargetBudget = 8192;
 // a single-query scan (the whole code array streamed once) as much as
 // rescoring about 10^5, so shallow requests are served ahead.  Measured on
 // 8.8M x 768, single requests: floor budget 2^16 179 queries/s, 2^17 252,
-// 2^18 247 (4096 alone: 182; batches of 64 and 256 unchanged).
+// 2^18 247 (4096 alone: 182; batches of 64 and 256 unchanged).  Re-measured
+// after the other changes (ms per batch-256 / batch-64 step): floor 4096 and
+// 2^22 ranks 94.8 / 43.3; 8192 99.9 / 49.0; 2048 100.5 / 46.1; 2^23 94.4 / 44.0.
 constexpr int64_t kSpecFactor = 16;
 constexpr int64_t kSpecBudget = int64_t(1) << 22;
 constexpr int64_t kSpecFloor = 4096;
