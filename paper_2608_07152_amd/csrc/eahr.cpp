@@ -73,6 +73,7 @@ struct RawBuf {   // uninitialised growable host buffer
 // ranks), kept between calls so that their memory is reused rather than
 // faulted in again; concurrent calls each take their own.
 struct TopkWork {
+    ::eahr::Helper sparse;   // runs each round's sparse channel beside the dense one
     std::vector<Fusion> F;
     RawBuf<int64_t> dids;
     RawBuf<float> dscores;
@@ -413,7 +414,14 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
         const auto t_round = std::chrono::steady_clock::now();
         double r_dense = 0, r_sparse = 0;
         // sparse channel on worker threads while the dense channel runs on the GPU
-        std::thread sparse_thread;
+        bool sparse_running = false;
+        struct WaitSparse {   // the job refers to this round's locals
+            ::eahr::Helper& h;
+            bool& running;
+            ~WaitSparse() {
+                if (running) h.wait();
+            }
+        } wait_sparse{W.sparse, sparse_running};
         std::atomic<bool> sparse_done{false};
         std::atomic<int64_t> sparse_cost_done{0};   // postings of the queries finished
         int64_t sparse_cost = 0;
@@ -463,7 +471,10 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
         };
         bool any_sparse = false;
         for (int32_t b = 0; b < B; ++b) any_sparse |= sact[b] != 0;
-        if (any_sparse) sparse_thread = std::thread(sparse_work);
+        if (any_sparse) {
+            W.sparse.post(sparse_work);
+            sparse_running = true;
+        }
         int dense_rc = EAHR_OK;
         if (m > 0) {
             const auto t0 = std::chrono::steady_clock::now();
@@ -480,7 +491,7 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
             for (int32_t b = 0; b < B; ++b) nd += dact[b];
             const int64_t cap = std::min<int64_t>(kFillMaxDepth, kFillBudget / std::max<int64_t>(nd, 1));
             int64_t ahead = depth;
-            while (dense_rc == EAHR_OK && !merged && sparse_thread.joinable() && ahead <= cap / ep.growth &&
+            while (dense_rc == EAHR_OK && !merged && sparse_running && ahead <= cap / ep.growth &&
                    !sparse_done.load(std::memory_order_acquire)) {
                 // remaining sparse time: from the share of postings of the
                 // finished queries (a first call scores about its postings),
@@ -510,7 +521,10 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
             r_dense = ms_since(t0);
             t_dense += r_dense;
         }
-        if (sparse_thread.joinable()) sparse_thread.join();
+        if (sparse_running) {
+            W.sparse.wait();
+            sparse_running = false;
+        }
         EAHR_TRY(dense_rc);
         for (int32_t b = 0; b < B; ++b)
             if (sparse_rc[b] != EAHR_OK) {

@@ -128,6 +128,62 @@ void parallel_for(int64_t n, int threads, F&& f) {
     WorkerPool::get().run(n, extra, work);
 }
 
+// One long-lived thread that runs one job at a time for its owner, started
+// on first use: the owner posts a job, goes on with its own work and waits
+// for the job later (cheaper than a thread per job when jobs are short).
+class Helper {
+public:
+    Helper() = default;
+    Helper(const Helper&) = delete;
+    Helper& operator=(const Helper&) = delete;
+    ~Helper() {
+        {
+            std::lock_guard<std::mutex> lk(mu_);
+            stop_ = true;
+        }
+        cv_.notify_all();
+        if (t_.joinable()) t_.join();
+    }
+    // Starts f; the previous job must have been waited for.
+    void post(std::function<void()> f) {
+        {
+            std::lock_guard<std::mutex> lk(mu_);
+            if (!t_.joinable()) t_ = std::thread([this] { loop(); });
+            job_ = std::move(f);
+            state_ = 1;
+        }
+        cv_.notify_all();
+    }
+    // Waits for the posted job to finish (returns at once if none is).
+    void wait() {
+        std::unique_lock<std::mutex> lk(mu_);
+        cv_.wait(lk, [&] { return state_ != 1 && state_ != 2; });
+        state_ = 0;
+    }
+
+private:
+    void loop() {
+        std::unique_lock<std::mutex> lk(mu_);
+        for (;;) {
+            cv_.wait(lk, [&] { return state_ == 1 || stop_; });
+            if (stop_) return;
+            state_ = 2;
+            std::function<void()> f = std::move(job_);
+            lk.unlock();
+            f();
+            lk.lock();
+            state_ = 3;
+            cv_.notify_all();
+        }
+    }
+    std::mutex mu_;
+    std::condition_variable cv_;
+    std::thread t_;
+    std::function<void()> job_;
+    int state_ = 0;   // 0 idle, 1 posted, 2 running, 3 done
+    bool stop_ = false;
+};
+
 // Allocator that leaves new elements of a vector uninitialised on resize
 // (for buffers written right after, in parallel when long).
 template <typename T>

@@ -1,6 +1,8 @@
 // Stress test of the host worker pool: several threads post jobs of random
 // sizes and thread counts at once, and items post nested jobs.  Every item
-// must run exactly once and every call must return.
+// must run exactly once and every call must return.  The same work also runs
+// as jobs of long-lived helper threads (posted, overlapped with the poster's
+// own work, waited for), as the fusion runs its sparse channel.
 #include <atomic>
 #include <cstdio>
 #include <random>
@@ -39,6 +41,25 @@ int main(int argc, char** argv) {
         std::vector<std::thread> ts;
         std::vector<long> got(4);
         for (int t = 0; t < 4; ++t) ts.emplace_back([rep, t, &got] { got[t] = work(0, rep * 10u + t); });
+        for (auto& t : ts) t.join();
+        for (long g : got) want += g;
+    }
+    // helpers: each of 4 threads owns one and posts a job per round
+    {
+        std::vector<std::thread> ts;
+        std::vector<long> got(4, 0);
+        for (int t = 0; t < 4; ++t)
+            ts.emplace_back([reps, t, &got] {
+                eahr::Helper h;
+                for (int rep = 0; rep < reps; ++rep) {
+                    long side = 0;
+                    h.post([&] { side = work(0, 7000u + rep * 10u + t); });
+                    const long mine = work(0, 9000u + rep * 10u + t);
+                    h.wait();
+                    got[t] += side + mine;
+                }
+                h.wait();   // nothing posted: returns at once
+            });
         for (auto& t : ts) t.join();
         for (long g : got) want += g;
     }
