@@ -1029,21 +1029,60 @@ void launch_scan_mfma(const IndexView& ix, const uint64_t* vis, int64_t nblocks,
 // One workgroup per query: tau = the k-th largest finite value among the
 // sampled lower bounds (midpoint == 0) or the sampled interval midpoints
 // (lo + hi) / 2 (midpoint == 1), by radix select over order-preserving keys,
-// 8 bits per pass; -inf when fewer than k are finite.  Then sample_hits =
-// sampled pairs with hi >= tau.
+// 8 bits per pass below the leading bits that every key shares; -inf when
+// fewer than k are finite.  Then sample_hits = sampled pairs with hi >= tau.
 __device__ __forceinline__ float select_value(const float* x, const float* y, int64_t i, int midpoint) {
     const float lo = x[i];
     return (midpoint && lo != -INFINITY) ? 0.5f * lo + 0.5f * y[i] : lo;
 }
 
+// Calls f(value) for every value of a query's sample (-inf: not finite),
+// reading 16 bytes per lane and four of them at a time: one workgroup per
+// query cannot hide the latency of 4-byte loads (a single request's select
+// ran at about 30 GB/s).  Rows of the sample start 16-byte aligned (they hold
+// whole 64-row blocks); a tail of n % 4 values, or a sample that is not
+// aligned, is read one value at a time.
+template <typename F>
+__device__ __forceinline__ void for_values(const float* x, const float* y, int64_t n, int midpoint, F&& f) {
+    constexpr int U = 4;
+    const float4* x4 = reinterpret_cast<const float4*>(x);
+    const float4* y4 = reinterpret_cast<const float4*>(y);
+    const bool aligned = ((reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(y)) & 15u) == 0;
+    const int64_t n4 = aligned ? n >> 2 : 0;
+    for (int64_t i0 = threadIdx.x; i0 < n4; i0 += static_cast<int64_t>(blockDim.x) * U) {
+        float4 a[U], c[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t i = i0 + static_cast<int64_t>(u) * blockDim.x;
+            a[u] = i < n4 ? x4[i] : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+            c[u] = (midpoint && i < n4) ? y4[i] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const float lo[4] = {a[u].x, a[u].y, a[u].z, a[u].w};
+            const float hi[4] = {c[u].x, c[u].y, c[u].z, c[u].w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) f((midpoint && lo[e] != -INFINITY) ? 0.5f * lo[e] + 0.5f * hi[e] : lo[e]);
+        }
+    }
+    for (int64_t i = 4 * n4 + threadIdx.x; i < n; i += blockDim.x) f(select_value(x, y, i, midpoint));
+}
+
 __global__ __launch_bounds__(1024) void k_select(const float* __restrict__ sample_lo,
                                                  const float* __restrict__ sample_hi, int64_t n,
                                                  int64_t ld, int midpoint, ScanQ* __restrict__ sq) {
-    __shared__ uint32_t hist[256];
+    // 32 copies of the digit histogram, lane l counting into copy l % 32: the
+    // keys of one query cluster in a few digits, and updates of one address
+    // from many lanes would be applied one at a time (stride 257 puts a
+    // digit's copies in different banks)
+    constexpr int kCopies = 32, kStride = 257;
+    __shared__ uint32_t hist[kCopies * kStride];
     __shared__ uint32_t s_digit;
     __shared__ uint32_t s_rest;
     __shared__ uint32_t s_total;
     __shared__ uint32_t s_hits;
+    __shared__ uint32_t s_kmin;
+    __shared__ uint32_t s_kmax;
     __shared__ float s_tau;
     const int b = blockIdx.x;
     const float* x = sample_lo + b * ld;
@@ -1052,31 +1091,63 @@ __global__ __launch_bounds__(1024) void k_select(const float* __restrict__ sampl
     if (threadIdx.x == 0) {
         s_total = 0;
         s_hits = 0;
+        s_kmin = 0xffffffffu;
+        s_kmax = 0u;
     }
     __syncthreads();
-    uint32_t local = 0;
-    for (int64_t i = threadIdx.x; i < n; i += blockDim.x) local += (x[i] != -INFINITY);
-    atomicAdd(&s_total, local);
+    // count, and the smallest and largest key: the bits they share are
+    // shared by every key, so the digit passes start below them
+    uint32_t local = 0, kmin = 0xffffffffu, kmax = 0u;
+    for_values(x, y, n, midpoint, [&](float v) {
+        if (v == -INFINITY) return;
+        const uint32_t key = mono32(v);
+        ++local;
+        kmin = key < kmin ? key : kmin;
+        kmax = key > kmax ? key : kmax;
+    });
+    for (int off = 32; off > 0; off >>= 1) {
+        local += __shfl_xor(local, off, 64);
+        const uint32_t a = __shfl_xor(kmin, off, 64), c = __shfl_xor(kmax, off, 64);
+        kmin = a < kmin ? a : kmin;
+        kmax = c > kmax ? c : kmax;
+    }
+    if ((threadIdx.x & 63) == 0) {
+        atomicAdd(&s_total, local);
+        atomicMin(&s_kmin, kmin);
+        atomicMax(&s_kmax, kmax);
+    }
     __syncthreads();
     const uint32_t total = s_total;
     if (k == 0 || k > total) {
         if (threadIdx.x == 0) s_tau = -INFINITY;
     } else {
-        uint32_t prefix = 0, pmask = 0;
-        for (int pass = 0; pass < 4; ++pass) {
-            const int shift = 24 - 8 * pass;
-            for (int i = threadIdx.x; i < 256; i += blockDim.x) hist[i] = 0;
+        const uint32_t lo = s_kmin, hi = s_kmax;
+        const int common = (lo == hi) ? 32 : __clz(lo ^ hi);
+        uint32_t pmask = (common == 32) ? 0xffffffffu : ~(0xffffffffu >> common);
+        uint32_t prefix = lo & pmask;
+        // the k-th largest key, digit by digit (8 bits, the last one fewer)
+        for (int bits = 32 - common; bits > 0;) {
+            const int w = bits < 8 ? bits : 8;
+            const int shift = bits - w;
+            const uint32_t dmask = (1u << w) - 1u;
+            for (int i = threadIdx.x; i < kCopies * kStride; i += blockDim.x) hist[i] = 0;
             __syncthreads();
-            for (int64_t i = threadIdx.x; i < n; i += blockDim.x) {
-                const float v = select_value(x, y, i, midpoint);
-                if (v == -INFINITY) continue;
+            uint32_t* mine = hist + (threadIdx.x & (kCopies - 1)) * kStride;
+            for_values(x, y, n, midpoint, [&](float v) {
+                if (v == -INFINITY) return;
                 const uint32_t key = mono32(v);
-                if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+                if ((key & pmask) == prefix) atomicAdd(&mine[(key >> shift) & dmask], 1u);
+            });
+            __syncthreads();
+            for (int d = threadIdx.x; d <= static_cast<int>(dmask); d += blockDim.x) {
+                uint32_t c = 0;
+                for (int r = 0; r < kCopies; ++r) c += hist[r * kStride + d];
+                hist[d] = c;   // copy 0 holds the sums (each d read and written by one thread)
             }
             __syncthreads();
             if (threadIdx.x == 0) {
                 uint32_t cum = 0;
-                int dgt = 255;
+                int dgt = static_cast<int>(dmask);
                 for (; dgt > 0; --dgt) {
                     if (cum + hist[dgt] >= k) break;
                     cum += hist[dgt];
@@ -1086,8 +1157,9 @@ __global__ __launch_bounds__(1024) void k_select(const float* __restrict__ sampl
             }
             __syncthreads();
             prefix |= s_digit << shift;
-            pmask |= 255u << shift;
+            pmask |= dmask << shift;
             k = s_rest;
+            bits -= w;
             __syncthreads();
         }
         if (threadIdx.x == 0) s_tau = unmono32(prefix);
@@ -1095,7 +1167,7 @@ __global__ __launch_bounds__(1024) void k_select(const float* __restrict__ sampl
     __syncthreads();
     const float tau = s_tau;
     uint32_t hits = 0;
-    for (int64_t i = threadIdx.x; i < n; i += blockDim.x) hits += (y[i] != -INFINITY && y[i] >= tau);
+    for_values(y, y, n, 0, [&](float v) { hits += (v != -INFINITY && v >= tau); });
     atomicAdd(&s_hits, hits);
     __syncthreads();
     if (threadIdx.x == 0) {
