@@ -309,42 +309,82 @@ __global__ __launch_bounds__(256) void k_sort_tiles(uint64_t* __restrict__ keys,
     for (int i = threadIdx.x; i < m; i += 256) k[i] = s[i];
 }
 
-// One merge level: runs of length `run` are merged pairwise.  An element's
-// output slot is its offset in its own run plus the number of keys of the
-// partner run that precede it (binary search; smaller keys, and for the right
-// run also equal ones, so the merge is stable).
+// One merge level: runs of length `run` (a multiple of kSortTile) are merged
+// pairwise, by merge path.  Workgroup (x, b) writes outputs
+// [x kSortTile, (x + 1) kSortTile) of query b, which lie in one pair of runs:
+// searches on the pair's cross diagonals give the parts of the left and
+// right runs that fill them (the left run first among equal keys; keys are
+// unique inside a query), those are staged in LDS, and each thread merges
+// eight consecutive outputs after a search of its own diagonal there.
 __global__ __launch_bounds__(256) void k_merge(const uint64_t* __restrict__ src,
                                                uint64_t* __restrict__ dst,
                                                const int32_t* __restrict__ cnt,
                                                const ScanQ* __restrict__ sq, int64_t run) {
+    constexpr int T = kSortTile;
+    constexpr int PER = T / 256;
+    static_assert(T % 256 == 0, "eight outputs per thread");
+    __shared__ uint64_t seg[T];   // the left part, then the right part
+    __shared__ uint64_t out[T];
+    __shared__ int64_t s_split[2];
     const int b = blockIdx.y;
     const int64_t n = cnt[b];
-    const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-    if (i >= n) return;
+    const int64_t o0 = static_cast<int64_t>(blockIdx.x) * T;
+    if (o0 >= n) return;
+    const int64_t o1 = min(o0 + T, n);
     const uint64_t* s = src + sq[b].cand_off;
     uint64_t* d = dst + sq[b].cand_off;
-    const uint64_t key = s[i];
-    const int64_t start = (i / (2 * run)) * (2 * run);
+    const int64_t start = (o0 / (2 * run)) * (2 * run);
     const int64_t mid = min(start + run, n);
     const int64_t end = min(start + 2 * run, n);
-    int64_t lo, hi, own;
-    if (i < mid) {
-        lo = mid;
-        hi = end;
-        own = i - start;
-    } else {
-        lo = start;
-        hi = mid;
-        own = i - mid;
+    const int64_t la = mid - start, lb = end - mid;
+    const uint64_t* A = s + start;
+    const uint64_t* B = s + mid;
+    // Left-run elements among the first `diag` outputs of the pair: the
+    // first m with A[m] > B[diag - 1 - m], searched by a wavefront 64 ways at
+    // a time (four dependent loads for runs of millions, not twenty).
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    if (wave < 2) {
+        const int64_t diag = (wave == 0 ? o0 : o1) - start;
+        int64_t lo = diag > lb ? diag - lb : 0, hi = diag < la ? diag : la;
+        while (lo < hi) {   // the same in every lane
+            const int64_t m = lo + ((hi - lo) * lane) / 64;   // in [lo, hi), ascending with the lane
+            const bool p = A[m] <= B[diag - 1 - m];           // true exactly below the answer
+            const int c = __popcll(__ballot(p));              // lanes below the answer
+            const int64_t m_below = __shfl(m, c > 0 ? c - 1 : 0, 64);
+            const int64_t m_at = __shfl(m, c < 64 ? c : 63, 64);
+            const int64_t nlo = c > 0 ? m_below + 1 : lo;
+            hi = c < 64 ? m_at : hi;
+            lo = nlo;
+        }
+        if (lane == 0) s_split[wave] = lo;
     }
-    const int64_t first = lo;
-    const bool left = i < mid;   // ties (none expected) go to the left run first
-    while (lo < hi) {
-        const int64_t m = (lo + hi) >> 1;
-        if (s[m] < key || (!left && s[m] == key)) lo = m + 1;
-        else hi = m;
+    __syncthreads();
+    const int64_t a0 = s_split[0], a1 = s_split[1];
+    const int64_t b0 = (o0 - start) - a0, b1 = (o1 - start) - a1;
+    const int na = static_cast<int>(a1 - a0), nb = static_cast<int>(b1 - b0);
+    for (int i = threadIdx.x; i < na + nb; i += 256) seg[i] = i < na ? A[a0 + i] : B[b0 + i - na];
+    __syncthreads();
+    // this thread's outputs [t0, t0 + PER) of the tile
+    const int t0 = threadIdx.x * PER;
+    if (t0 < na + nb) {
+        const uint64_t* sa = seg;
+        const uint64_t* sb = seg + na;
+        int lo = t0 > nb ? t0 - nb : 0, hi = t0 < na ? t0 : na;
+        while (lo < hi) {
+            const int m = (lo + hi) >> 1;
+            if (sa[m] <= sb[t0 - 1 - m]) lo = m + 1;
+            else hi = m;
+        }
+        int ia = lo, ib = t0 - lo;
+        const int t1 = min(t0 + PER, na + nb);
+        for (int t = t0; t < t1; ++t) {
+            const bool takea = ib >= nb || (ia < na && sa[ia] <= sb[ib]);
+            out[t] = takea ? sa[ia++] : sb[ib++];
+        }
     }
-    d[start + own + (lo - first)] = key;
+    __syncthreads();
+    for (int i = threadIdx.x; i < na + nb; i += 256) d[o0 + i] = out[i];
 }
 
 uint64_t* launch_segmented_sort(uint64_t* keys, uint64_t* tmp, const int32_t* cnt,
@@ -356,7 +396,7 @@ uint64_t* launch_segmented_sort(uint64_t* keys, uint64_t* tmp, const int32_t* cn
     uint64_t* a = keys;
     uint64_t* b = tmp;
     for (int64_t run = kSortTile; run < max_cnt; run *= 2) {
-        const int64_t g = (max_cnt + 255) / 256;
+        const int64_t g = (max_cnt + kSortTile - 1) / kSortTile;
         hipLaunchKernelGGL(k_merge, dim3(static_cast<uint32_t>(g), nq), dim3(256), 0, stream, a, b,
                            cnt, sq, run);
         uint64_t* t = a;
