@@ -373,6 +373,8 @@ pvs_state::~pvs_state() {
     release_scan_buffers();
     for (auto& e : ev)
         if (e) (void)hipEventDestroy(e);
+    for (auto& e : copy_ev)
+        if (e) (void)hipEventDestroy(e);
 }
 
 void pvs_state::release_scan_buffers() {
@@ -874,6 +876,11 @@ static int full_scan_round(pvs_state* st, std::vector<int32_t>& todo) {
     return EAHR_OK;
 }
 
+// Certified keys of a scan travel to the host in kCopyPieces copies once
+// there are at least kCopyPieceMin keys per piece.
+constexpr int kCopyPieces = 4;
+constexpr int64_t kCopyPieceMin = int64_t(1) << 18;
+
 // One scan round over the queries in `todo`; removes the queries it finished.
 //  1. sample pass + select: tau and the sampled hit count of every query;
 //  2. candidate regions sized from the hits (host), main scan;
@@ -1059,7 +1066,8 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     EAHR_TRY(mark(4));
     // only the certified keys are ordered; a query whose key region overflowed
     // (it is scanned again) keeps the region's worth
-    HIP_TRY(hipMemcpyAsync(st->h_counts, d_cert, nq * sizeof(int32_t), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipMemcpyAsync(st->h_counts, d_cert, 2 * static_cast<size_t>(nq) * sizeof(int32_t),
+                           hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
     const std::vector<int32_t> cert_all(st->h_counts, st->h_counts + nq);
     int64_t max_cert = 0;
@@ -1074,30 +1082,71 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     }
     if (clamped)
         HIP_TRY(hipMemcpyAsync(d_cert, st->h_counts, nq * sizeof(int32_t), hipMemcpyHostToDevice, s));
+    // the packed layout: query i's keys at h_offs[i] (the pack kernel's
+    // exclusive prefix of the same counts)
+    const int32_t* h_cert = st->h_counts;
+    const int32_t* h_fail = st->h_counts + nq;
+    std::vector<int64_t> h_offs(static_cast<size_t>(nq) + 1, 0);
+    for (int32_t i = 0; i < nq; ++i) h_offs[i + 1] = h_offs[i] + h_cert[i];
+    const int64_t n_packed = h_offs[nq];
+    EAHR_TRY(ensure_host_packed(st, n_packed));
     EAHR_TRY(mark(6));
     uint64_t* sorted = pvs::launch_segmented_sort(st->keys, st->keys_tmp, d_cert, st->scanq, nq, max_cert, s);
     pvs::launch_pack(sorted, d_cert, st->scanq, nq, max_cert, d_offs, st->packed, s);
     EAHR_TRY(mark(5));
     HIP_TRY(hipGetLastError());
-    EAHR_TRY(ensure_host_packed(st, kept));
-    HIP_TRY(hipMemcpyAsync(st->h_counts, st->counts, (3 * static_cast<size_t>(nq) + 2) * sizeof(int32_t),
-                           hipMemcpyDeviceToHost, s));
     if (prof)
         HIP_TRY(hipMemcpyAsync(st->h_counts + reads_counts_at(nq), d_reads,
                                static_cast<size_t>(pvs::kSub) * pvs::kCntStride * sizeof(int32_t),
                                hipMemcpyDeviceToHost, s));
-    HIP_TRY(hipStreamSynchronize(s));
-    tp[3] = clk::now();
-    const int32_t* h_cert = st->h_counts;
-    const int32_t* h_fail = st->h_counts + nq;
-    const int32_t* h_offs = st->h_counts + 2 * nq;
+    // The keys come back in pieces, each followed by an event: the host
+    // appends a piece to the caches while the next one is still in flight.
+    const int pieces = n_packed >= kCopyPieceMin * kCopyPieces ? kCopyPieces : 1;
+    if (!st->copy_ev[0])
+        for (auto& e : st->copy_ev) HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+    std::vector<int64_t> cut(static_cast<size_t>(pieces) + 1, 0);
+    for (int p = 0; p < pieces; ++p) {
+        cut[p + 1] = n_packed * (p + 1) / pieces;
+        if (cut[p + 1] > cut[p])
+            HIP_TRY(hipMemcpyAsync(st->h_packed + cut[p], st->packed + cut[p],
+                                   static_cast<size_t>(cut[p + 1] - cut[p]) * sizeof(uint64_t),
+                                   hipMemcpyDeviceToHost, s));
+        HIP_TRY(hipEventRecord(st->copy_ev[p], s));
+    }
+    // caches grow by the certified keys of every usable query
+    std::vector<uint8_t> usable(nq, 0);
+    std::vector<int64_t> at(nq, 0);
+    for (int32_t i = 0; i < nq; ++i) {
+        usable[i] = !h_fail[i] && cert_all[i] == h_cert[i];
+        if (!usable[i] || h_cert[i] == 0) continue;
+        auto& c = st->q[todo[i]].cache;
+        at[i] = static_cast<int64_t>(c.size());
+        c.resize(c.size() + static_cast<size_t>(h_cert[i]));
+    }
     int64_t row_reads = 0;
-    if (prof)
-        for (int i = 0; i < pvs::kSub; ++i) row_reads += st->h_counts[reads_counts_at(nq) + i * pvs::kCntStride];
-    if (h_offs[nq] > 0)
-        HIP_TRY(hipMemcpy(st->h_packed, st->packed, static_cast<size_t>(h_offs[nq]) * sizeof(uint64_t),
-                          hipMemcpyDeviceToHost));
-    tp[4] = clk::now();
+    std::vector<int64_t> part(nq), first(nq);
+    for (int p = 0; p < pieces; ++p) {
+        HIP_TRY(hipEventSynchronize(st->copy_ev[p]));
+        if (p == 0) {
+            tp[3] = clk::now();
+            if (prof)
+                for (int i = 0; i < pvs::kSub; ++i)
+                    row_reads += st->h_counts[reads_counts_at(nq) + i * pvs::kCntStride];
+        }
+        if (p == pieces - 1) tp[4] = clk::now();
+        // the part of each query's keys inside [cut[p], cut[p + 1]), in
+        // pieces over the host threads (a few deep queries use them all)
+        for (int32_t i = 0; i < nq; ++i) {
+            const int64_t lo = std::max(h_offs[i], cut[p]), hi = std::min(h_offs[i + 1], cut[p + 1]);
+            part[i] = (usable[i] && hi > lo) ? hi - lo : 0;
+            first[i] = lo - h_offs[i];
+        }
+        eahr::parallel_pieces(part, int64_t(1) << 18, eahr::host_threads(), [&](int64_t i, int64_t lo, int64_t hi) {
+            const int64_t o = first[i] + lo;
+            std::memcpy(st->q[todo[i]].cache.data() + at[i] + o, st->h_packed + h_offs[i] + o,
+                        static_cast<size_t>(hi - lo) * sizeof(uint64_t));
+        });
+    }
     if (prof) {
         float t[4];
         HIP_TRY(hipEventElapsedTime(&t[0], st->ev[0], st->ev[1]));
@@ -1114,10 +1163,10 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
         const int64_t pass_bytes = st->n_rows * (static_cast<int64_t>(ix->d) + 12) + nblocks * 8;
         g_prof.scan_bytes += launches * pass_bytes;
         // kernel variant of the first launch (the only one when nq fits one pass)
-        const int first = static_cast<int>(std::min<int64_t>(nq, per));
-        int v = mfma ? 8 + (pvs::mfma_tiles_for(first) == 1 ? 0 : pvs::mfma_tiles_for(first) == 2 ? 1
-                            : pvs::mfma_tiles_for(first) == 4 ? 2 : 3)
-                     : first - 1;
+        const int first_q = static_cast<int>(std::min<int64_t>(nq, per));
+        int v = mfma ? 8 + (pvs::mfma_tiles_for(first_q) == 1 ? 0 : pvs::mfma_tiles_for(first_q) == 2 ? 1
+                            : pvs::mfma_tiles_for(first_q) == 4 ? 2 : 3)
+                     : first_q - 1;
         g_prof.variant_ms[v] += t[1];
         g_prof.variant_launches[v] += launches;
         g_prof.variant_bytes[v] += launches * pass_bytes;
@@ -1128,23 +1177,6 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
         g_prof.sort_ms += t[3];
         g_prof.scan_rounds += 1;
     }
-
-    // append the certified keys of every query to its cache, in pieces over
-    // the host threads (a few deep queries use them all)
-    std::vector<uint8_t> usable(nq, 0);
-    std::vector<int64_t> grow(nq, 0), at(nq, 0);
-    for (int32_t i = 0; i < nq; ++i) {
-        usable[i] = !h_fail[i] && cert_all[i] == h_cert[i];
-        if (!usable[i] || h_cert[i] == 0) continue;
-        auto& c = st->q[todo[i]].cache;
-        at[i] = static_cast<int64_t>(c.size());
-        grow[i] = h_cert[i];
-        c.resize(c.size() + static_cast<size_t>(h_cert[i]));
-    }
-    eahr::parallel_pieces(grow, int64_t(1) << 18, eahr::host_threads(), [&](int64_t i, int64_t lo, int64_t hi) {
-        std::memcpy(st->q[todo[i]].cache.data() + at[i] + lo, st->h_packed + h_offs[i] + lo,
-                    static_cast<size_t>(hi - lo) * sizeof(uint64_t));
-    });
     if (trace) {
         tp[5] = clk::now();
         auto ms = [&](int a, int b) { return std::chrono::duration<double, std::milli>(tp[b] - tp[a]).count(); };

@@ -195,6 +195,7 @@ struct pvs_state {
     // normal containment check (App. A.1); -1: off
     int32_t test_fail_qi = -1;
     hipEvent_t ev[7] = {};             // profiling events (created on first use)
+    hipEvent_t copy_ev[4] = {};        // ends of the pieces of a key copy
     pvs::ScanQ* h_scanq = nullptr;     // pinned host mirrors
     int32_t* h_counts = nullptr;
     uint64_t* h_packed = nullptr;
