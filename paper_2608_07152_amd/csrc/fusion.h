@@ -240,12 +240,13 @@ struct Fusion {
     // closed-list mode: seen[i] has bit x set when list i holds id x
     bool bitmaps = false;
     std::vector<uint64_t> seen[2];
-    // direct mode: pos[i][x] is the 1-based rank of id x in list i (0: not
-    // in it); entered once the lists hold universe / kDirectShare ranks
+    // direct mode: pos[2 x + i] is the 1-based rank of id x in list i (0:
+    // not in it; both ranks of an id share a cache line); entered once the
+    // lists hold universe / kDirectShare ranks
     static constexpr int64_t kDirectShare = 16;
     int64_t universe = 0;       // ids lie in [0, universe); 0: not known
     bool direct = false;
-    std::vector<int32_t> pos[2];
+    std::vector<int32_t> pos;
 
     static bool test_bit(const std::vector<uint64_t>& b, int64_t x) {
         const size_t w = static_cast<size_t>(x >> 6);
@@ -330,16 +331,16 @@ struct Fusion {
         for (auto& b : seen) std::fill(b.begin(), b.end(), 0ull);
         direct = false;
         universe = 0;
-        for (auto& p : pos) std::vector<int32_t>().swap(p);   // only deep queries need them
+        std::vector<int32_t>().swap(pos);   // only deep queries need it
     }
 
     void enter_direct_mode() {
         for (int i = 0; i < 2; ++i)
             for (int64_t x : L[i].ids) universe = std::max(universe, x + 1);
+        pos.assign(2 * static_cast<size_t>(universe), 0);
         for (int i = 0; i < 2; ++i) {
-            pos[i].assign(static_cast<size_t>(universe), 0);
             for (int64_t p = 0; p < L[i].size(); ++p) {
-                int32_t& r = pos[i][static_cast<size_t>(L[i].ids[p])];
+                int32_t& r = pos[2 * static_cast<size_t>(L[i].ids[p]) + i];
                 if (r) dup = true;
                 else r = static_cast<int32_t>(p + 1);
             }
@@ -360,31 +361,27 @@ struct Fusion {
             if (Atomic) __atomic_fetch_and(&b[static_cast<size_t>(p >> 6)], m, __ATOMIC_RELAXED);
             else b[static_cast<size_t>(p >> 6)] &= m;
         };
-        int32_t* mine = pos[i].data();
-        const int32_t* theirs = pos[1 - i].data();
-        // the rank arrays are read at random ids: fetch a few ids ahead
+        int32_t* const ranks = pos.data();
+        // the rank pairs are read at random ids: fetch a few ids ahead
         constexpr int64_t kAhead = 16;
         for (int64_t j = j0; j < j1; ++j) {
-            if (j + kAhead < j1) {
-                const int64_t y = ids[j + kAhead];
-                __builtin_prefetch(mine + y, 1, 0);
-                __builtin_prefetch(theirs + y, 0, 0);
-            }
+            if (j + kAhead < j1) __builtin_prefetch(ranks + 2 * ids[j + kAhead], 1, 0);
             const int64_t x = ids[j];
             const int64_t rank = p0 + j + 1;
+            int32_t* const mine = ranks + 2 * x + i;
             int32_t prev;
             if (Atomic) {
-                prev = __atomic_exchange_n(&mine[x], static_cast<int32_t>(rank), __ATOMIC_RELAXED);
+                prev = __atomic_exchange_n(mine, static_cast<int32_t>(rank), __ATOMIC_RELAXED);
             } else {
-                prev = mine[x];
-                if (!prev) mine[x] = static_cast<int32_t>(rank);
+                prev = *mine;
+                if (!prev) *mine = static_cast<int32_t>(rank);
             }
             if (prev) {
                 rep = true;
                 clear_bit(me.alive, rank - 1);
                 continue;
             }
-            const int64_t ro = theirs[x];
+            const int64_t ro = ranks[2 * x + 1 - i];
             if (!ro) continue;
             clear_bit(me.alive, rank - 1);
             clear_bit(other.alive, ro - 1);
@@ -405,7 +402,7 @@ struct Fusion {
         for (int64_t j = 0; j < n; ++j) xmax = std::max(xmax, ids[j]);
         if (xmax >= universe) {   // an id beyond the announced range
             universe = xmax + 1;
-            for (auto& p : pos) p.resize(static_cast<size_t>(universe), 0);
+            pos.resize(2 * static_cast<size_t>(universe), 0);
         }
         const size_t heap0 = both.size();
         const int parts = (threads > 1 && n >= kParallelAppend)
