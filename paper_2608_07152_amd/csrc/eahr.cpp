@@ -9,11 +9,13 @@
 #include <cstdint>
 #include <cstdio>
 #include <cstring>
+#include <map>
 #include <memory>
 #include <mutex>
 #include <new>
 #include <string>
 #include <thread>
+#include <tuple>
 #include <vector>
 
 #include "common.h"
@@ -51,6 +53,21 @@ using ::eahr::parallel_for;
 // share of its queries still to finish).
 constexpr int64_t kFillMaxDepth = int64_t(1) << 17;
 constexpr int64_t kFillBudget = int64_t(1) << 25;
+
+// Rates measured by earlier calls on the same pair of indexes and sparse
+// generator: time per posting of a first sparse round (which scores about
+// all of its queries' postings) and dense time per rank certified ahead.
+// With both known, the first round certifies ahead in one scan, to the
+// deepest depth level whose estimated time fits in kAheadSlack times the
+// sparse channel's expected time, instead of in steps of one level (a scan
+// each) while it runs.
+struct Rates {
+    double sparse_ms_per_posting = 0.0;
+    double dense_ms_per_rank = 0.0;
+};
+constexpr double kAheadSlack = 1.25;
+std::mutex g_rates_mu;
+std::map<std::tuple<const void*, const void*, int32_t>, Rates> g_rates;
 
 double ms_since(std::chrono::steady_clock::time_point t0) {
     return std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
@@ -394,6 +411,17 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
     int64_t depth = ep.depth0;
     double fill_ms = 0.0;            // measured cost of dense work-ahead
     int64_t fill_ranks = 0;
+    const std::tuple<const void*, const void*, int32_t> rates_key{dense, sparse, ep.sparse_generator};
+    Rates rates;
+    {
+        std::lock_guard<std::mutex> lk(g_rates_mu);
+        const auto it = g_rates.find(rates_key);
+        if (it != g_rates.end()) rates = it->second;
+    }
+    double first_sparse_ms = -1.0;   // the first round's sparse time and postings
+    int64_t first_sparse_cost = 0;
+    bool first_round = true;
+    std::vector<uint8_t> retired(B, 0);
     for (bool doubling = ep.schedule == EAHR_SCHED_DOUBLING; doubling;) {
         bool any = false;
         for (int32_t b = 0; b < B; ++b) any |= !F[b].resolved && !failed[b];
@@ -478,18 +506,44 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
         int dense_rc = EAHR_OK;
         if (m > 0) {
             const auto t0 = std::chrono::steady_clock::now();
-            int64_t* ids = dids.get(static_cast<size_t>(B) * m);
-            float* sc = dscores.get(static_cast<size_t>(B) * m);
-            dense_rc = merged ? pvs_merge_next(merged, static_cast<int32_t>(m), dact.data(), ids, sc,
-                                               dcnt.data(), dsts.data())
-                              : pvs_next(cl.st, static_cast<int32_t>(m), dact.data(), ids, sc,
-                                         dcnt.data(), dsts.data());
-            // While the sparse channel is still busy, certify the dense ranks
-            // of the next depths ahead (they are served from the cache later;
-            // the output does not depend on it).
             int64_t nd = 0;
             for (int32_t b = 0; b < B; ++b) nd += dact[b];
             const int64_t cap = std::min<int64_t>(kFillMaxDepth, kFillBudget / std::max<int64_t>(nd, 1));
+            if (first_round && !merged && sparse_running && rates.sparse_ms_per_posting > 0.0 &&
+                rates.dense_ms_per_rank > 0.0) {
+                // certify ahead, in one scan, to the deepest level the sparse
+                // channel's expected time pays for; worth a scan of its own
+                // only beyond what a first scan certifies anyway
+                const double expect = rates.sparse_ms_per_posting * static_cast<double>(sparse_cost);
+                const double per_level = rates.dense_ms_per_rank * static_cast<double>(nd);
+                const int64_t floor = std::max(pvs::kSpecFloor, pvs::kSpecFloorBudget / std::max<int64_t>(nd, 1));
+                int64_t ahead = 0;
+                for (int64_t l = depth; l <= cap && per_level * static_cast<double>(l) <= kAheadSlack * expect;
+                     l *= ep.growth)
+                    ahead = l;
+                if (ahead > std::max(depth * ep.growth, floor)) {
+                    int64_t added = 0;
+                    dense_rc = pvs_fill_exact(cl.st, ahead, dact.data(), &added);
+                    if (added > 0) {
+                        fill_ms += ms_since(t0);
+                        fill_ranks += added;
+                    }
+                    if (::eahr::trace_on())
+                        std::fprintf(stderr, "eahr ahead depth=%lld expected_sparse_ms=%.2f added=%lld fill_ms=%.2f\n",
+                                     static_cast<long long>(ahead), expect, static_cast<long long>(added),
+                                     ms_since(t0));
+                }
+            }
+            int64_t* ids = dids.get(static_cast<size_t>(B) * m);
+            float* sc = dscores.get(static_cast<size_t>(B) * m);
+            if (dense_rc == EAHR_OK)
+                dense_rc = merged ? pvs_merge_next(merged, static_cast<int32_t>(m), dact.data(), ids, sc,
+                                                   dcnt.data(), dsts.data())
+                                  : pvs_next(cl.st, static_cast<int32_t>(m), dact.data(), ids, sc,
+                                             dcnt.data(), dsts.data());
+            // While the sparse channel is still busy, certify the dense ranks
+            // of the next depths ahead (they are served from the cache later;
+            // the output does not depend on it).
             int64_t ahead = depth;
             while (dense_rc == EAHR_OK && !merged && sparse_running && ahead <= cap / ep.growth &&
                    !sparse_done.load(std::memory_order_acquire)) {
@@ -524,7 +578,12 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
         if (sparse_running) {
             W.sparse.wait();
             sparse_running = false;
+            if (first_round) {
+                first_sparse_ms = r_sparse;
+                first_sparse_cost = sparse_cost;
+            }
         }
+        first_round = false;
         EAHR_TRY(dense_rc);
         for (int32_t b = 0; b < B; ++b)
             if (sparse_rc[b] != EAHR_OK) {
@@ -581,6 +640,13 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
             F[b].certify();
         };
         parallel_for(B, threads, certify_one);
+        // settled queries read no further dense ranks
+        if (cl.st)
+            for (int32_t b = 0; b < B; ++b)
+                if ((F[b].resolved || failed[b]) && !retired[b]) {
+                    pvs_retire(cl.st, b);
+                    retired[b] = 1;
+                }
         const double r_fuse = ms_since(t0);
         t_fuse += r_fuse;
         if (::eahr::trace_on()) {
@@ -598,6 +664,13 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
                          static_cast<long long>(open_q));
         }
         depth = (depth > (INT64_MAX / ep.growth)) ? INT64_MAX : depth * ep.growth;
+    }
+    if (!merged && (fill_ranks > 0 || (first_sparse_ms > 0.0 && first_sparse_cost > 0))) {
+        std::lock_guard<std::mutex> lk(g_rates_mu);
+        Rates& r = g_rates[rates_key];
+        if (fill_ranks > 0) r.dense_ms_per_rank = fill_ms / static_cast<double>(fill_ranks);
+        if (first_sparse_ms > 0.0 && first_sparse_cost > 0)
+            r.sparse_ms_per_posting = first_sparse_ms / static_cast<double>(first_sparse_cost);
     }
     // a rescored score outside its interval fails its query even when the
     // failure came from work-ahead that no pvs_next has reported yet

@@ -373,8 +373,6 @@ pvs_state::~pvs_state() {
     release_scan_buffers();
     for (auto& e : ev)
         if (e) (void)hipEventDestroy(e);
-    for (auto& e : copy_ev)
-        if (e) (void)hipEventDestroy(e);
 }
 
 void pvs_state::release_scan_buffers() {
@@ -428,6 +426,7 @@ static void donate_buffers(pvs_state* st, ScanBuffers& b) {
         if (kept + bytes > kRecycleBytes) break;
         kept += bytes;
         Q.cache.clear();
+        Q.pend_n = 0;
         b.caches.push_back(std::move(Q.cache));
     }
     st->buf_nq = 0;
@@ -771,6 +770,38 @@ static inline float key_score(uint64_t key) {
     return f;
 }
 
+// Certified ranks of a query: its cache, then the keys of its last scan
+// still in the pinned copy.
+static int64_t certified_count(const pvs_state::Query& Q) {
+    return static_cast<int64_t>(Q.cache.size()) + Q.pend_n;
+}
+
+// Appends every query's keys still in the pinned copy to its cache (before
+// a scan overwrites the copy), in pieces over the host threads.
+static void flush_pending(pvs_state* st) {
+    const int32_t B = st->B;
+    std::vector<int64_t> n(B, 0), at(B, 0);
+    bool any = false;
+    for (int32_t b = 0; b < B; ++b) {
+        auto& Q = st->q[b];
+        if (Q.pend_n <= 0) continue;
+        at[b] = static_cast<int64_t>(Q.cache.size());
+        n[b] = Q.pend_n;
+        Q.cache.resize(Q.cache.size() + static_cast<size_t>(Q.pend_n));
+        any = true;
+    }
+    if (!any) return;
+    eahr::parallel_pieces(n, int64_t(1) << 18, eahr::host_threads(), [&](int64_t b, int64_t lo, int64_t hi) {
+        const auto& Q = st->q[b];
+        std::memcpy(st->q[b].cache.data() + at[b] + lo, st->h_packed + Q.pend_off + lo,
+                    static_cast<size_t>(hi - lo) * sizeof(uint64_t));
+    });
+    for (int32_t b = 0; b < B; ++b) {
+        st->q[b].pend_off = 0;
+        st->q[b].pend_n = 0;
+    }
+}
+
 // Certified ranks of query b that may still have lo <= s_cert: they score at
 // most s_cert + 2 * wmax, because lo >= s32 - 2 * wmax.
 static int64_t lower_overlap(const pvs_state* st, int32_t b) {
@@ -876,11 +907,6 @@ static int full_scan_round(pvs_state* st, std::vector<int32_t>& todo) {
     return EAHR_OK;
 }
 
-// Certified keys of a scan travel to the host in kCopyPieces copies once
-// there are at least kCopyPieceMin keys per piece.
-constexpr int kCopyPieces = 4;
-constexpr int64_t kCopyPieceMin = int64_t(1) << 18;
-
 // One scan round over the queries in `todo`; removes the queries it finished.
 //  1. sample pass + select: tau and the sampled hit count of every query;
 //  2. candidate regions sized from the hits (host), main scan;
@@ -889,6 +915,9 @@ constexpr int64_t kCopyPieceMin = int64_t(1) << 18;
 // their candidates; queries that certified too few ranks again with a lower
 // threshold.
 static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
+    // the pinned copy is about to be reused, and the targets below read
+    // complete caches
+    flush_pending(st);
     if (st->generator == EAHR_GEN_FULL_SCAN) return full_scan_round(st, todo);
     const pvs_index* ix = st->ix;
     hipStream_t s = ix->stream;
@@ -915,7 +944,8 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
         const int64_t avail = have - Q.emitted;
         const int64_t need = std::max<int64_t>(1, m - avail);
         const int64_t spec_floor = std::max(pvs::kSpecFloor, pvs::kSpecFloorBudget / nq);
-        const int64_t spec = std::min(std::max(pvs::kSpecFactor * (Q.emitted + m), spec_floor) - have,
+        const int64_t spec = st->spec_off ? 0
+                           : std::min(std::max(pvs::kSpecFactor * (Q.emitted + m), spec_floor) - have,
                                       pvs::kSpecBudget / nq);
         const int64_t target = std::max({need, mmin, spec}) + lower_overlap(st, b);
         double k = (stride == 1) ? static_cast<double>(target)
@@ -941,7 +971,7 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
 
     const bool trace = ::eahr::trace_on();
     using clk = std::chrono::steady_clock;
-    clk::time_point tp[6];
+    clk::time_point tp[5];
     tp[0] = clk::now();
     // 1. threshold and candidate estimate from the sampled blocks
     HIP_TRY(hipMemcpyAsync(st->scanq, st->h_scanq, nq * sizeof(ScanQ), hipMemcpyHostToDevice, s));
@@ -1069,6 +1099,7 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     HIP_TRY(hipMemcpyAsync(st->h_counts, d_cert, 2 * static_cast<size_t>(nq) * sizeof(int32_t),
                            hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
+    tp[3] = clk::now();
     const std::vector<int32_t> cert_all(st->h_counts, st->h_counts + nq);
     int64_t max_cert = 0;
     bool clamped = false;
@@ -1099,53 +1130,24 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
         HIP_TRY(hipMemcpyAsync(st->h_counts + reads_counts_at(nq), d_reads,
                                static_cast<size_t>(pvs::kSub) * pvs::kCntStride * sizeof(int32_t),
                                hipMemcpyDeviceToHost, s));
-    // The keys come back in pieces, each followed by an event: the host
-    // appends a piece to the caches while the next one is still in flight.
-    const int pieces = n_packed >= kCopyPieceMin * kCopyPieces ? kCopyPieces : 1;
-    if (!st->copy_ev[0])
-        for (auto& e : st->copy_ev) HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
-    std::vector<int64_t> cut(static_cast<size_t>(pieces) + 1, 0);
-    for (int p = 0; p < pieces; ++p) {
-        cut[p + 1] = n_packed * (p + 1) / pieces;
-        if (cut[p + 1] > cut[p])
-            HIP_TRY(hipMemcpyAsync(st->h_packed + cut[p], st->packed + cut[p],
-                                   static_cast<size_t>(cut[p + 1] - cut[p]) * sizeof(uint64_t),
-                                   hipMemcpyDeviceToHost, s));
-        HIP_TRY(hipEventRecord(st->copy_ev[p], s));
-    }
-    // caches grow by the certified keys of every usable query
+    // The keys come back into the pinned copy; they stay there (pending)
+    // until the next scan round, which appends them to the caches, while the
+    // ranks they hold are emitted straight from the copy.
+    if (n_packed > 0)
+        HIP_TRY(hipMemcpyAsync(st->h_packed, st->packed, static_cast<size_t>(n_packed) * sizeof(uint64_t),
+                               hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    tp[4] = clk::now();
+    int64_t row_reads = 0;
+    if (prof)
+        for (int i = 0; i < pvs::kSub; ++i) row_reads += st->h_counts[reads_counts_at(nq) + i * pvs::kCntStride];
     std::vector<uint8_t> usable(nq, 0);
-    std::vector<int64_t> at(nq, 0);
     for (int32_t i = 0; i < nq; ++i) {
         usable[i] = !h_fail[i] && cert_all[i] == h_cert[i];
         if (!usable[i] || h_cert[i] == 0) continue;
-        auto& c = st->q[todo[i]].cache;
-        at[i] = static_cast<int64_t>(c.size());
-        c.resize(c.size() + static_cast<size_t>(h_cert[i]));
-    }
-    int64_t row_reads = 0;
-    std::vector<int64_t> part(nq), first(nq);
-    for (int p = 0; p < pieces; ++p) {
-        HIP_TRY(hipEventSynchronize(st->copy_ev[p]));
-        if (p == 0) {
-            tp[3] = clk::now();
-            if (prof)
-                for (int i = 0; i < pvs::kSub; ++i)
-                    row_reads += st->h_counts[reads_counts_at(nq) + i * pvs::kCntStride];
-        }
-        if (p == pieces - 1) tp[4] = clk::now();
-        // the part of each query's keys inside [cut[p], cut[p + 1]), in
-        // pieces over the host threads (a few deep queries use them all)
-        for (int32_t i = 0; i < nq; ++i) {
-            const int64_t lo = std::max(h_offs[i], cut[p]), hi = std::min(h_offs[i + 1], cut[p + 1]);
-            part[i] = (usable[i] && hi > lo) ? hi - lo : 0;
-            first[i] = lo - h_offs[i];
-        }
-        eahr::parallel_pieces(part, int64_t(1) << 18, eahr::host_threads(), [&](int64_t i, int64_t lo, int64_t hi) {
-            const int64_t o = first[i] + lo;
-            std::memcpy(st->q[todo[i]].cache.data() + at[i] + o, st->h_packed + h_offs[i] + o,
-                        static_cast<size_t>(hi - lo) * sizeof(uint64_t));
-        });
+        auto& Q = st->q[todo[i]];
+        Q.pend_off = h_offs[i];
+        Q.pend_n = h_cert[i];
     }
     if (prof) {
         float t[4];
@@ -1178,16 +1180,15 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
         g_prof.scan_rounds += 1;
     }
     if (trace) {
-        tp[5] = clk::now();
         auto ms = [&](int a, int b) { return std::chrono::duration<double, std::milli>(tp[b] - tp[a]).count(); };
         int64_t certified = 0;
         for (int32_t i = 0; i < nq; ++i) certified += h_cert[i];
         std::fprintf(stderr,
                      "pvs scan_round queries=%d path=%s stride=%lld pool=%lld kept=%lld certified=%lld "
-                     "sample_ms=%.2f scan_ms=%.2f rank_ms=%.2f copy_ms=%.2f decode_ms=%.2f\n",
+                     "sample_ms=%.2f scan_ms=%.2f rescore_ms=%.2f order_copy_ms=%.2f\n",
                      nq, mfma ? "mfma" : "gemv", static_cast<long long>(stride),
                      static_cast<long long>(total), static_cast<long long>(kept),
-                     static_cast<long long>(certified), ms(0, 1), ms(1, 2), ms(2, 3), ms(3, 4), ms(4, 5));
+                     static_cast<long long>(certified), ms(0, 1), ms(1, 2), ms(2, 3), ms(3, 4));
     }
     st->stats.candidates += kept;
     std::vector<int32_t> keep;
@@ -1209,12 +1210,13 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
         const int64_t c = h_cert[i];
         st->stats.certified += c;
         if (c > 0) {
+            const uint64_t last = st->h_packed[h_offs[i] + c - 1];
             Q.has_cert = true;
-            Q.s_cert = key_score(Q.cache.back());
-            Q.id_cert = key_id(Q.cache.back());
+            Q.s_cert = key_score(last);
+            Q.id_cert = key_id(last);
         }
-        const int64_t avail = static_cast<int64_t>(Q.cache.size()) - Q.emitted;
-        if (static_cast<int64_t>(Q.cache.size()) >= st->n_vis) {
+        const int64_t avail = certified_count(Q) - Q.emitted;
+        if (certified_count(Q) >= st->n_vis) {
             Q.cert_exhausted = true;
             Q.retries = 0;
         } else if (avail >= m) {
@@ -1239,8 +1241,9 @@ extern "C" int pvs_next(pvs_state* st, int32_t m, const uint8_t* active, int64_t
     for (int32_t b = 0; b < B; ++b) {
         if (active && !active[b]) continue;
         auto& Q = st->q[b];
+        if (Q.retired) EAHR_FAIL(EAHR_E_INVALID, "pvs_next: query %d was retired", b);
         if (Q.failed || Q.cert_exhausted) continue;
-        const int64_t avail = static_cast<int64_t>(Q.cache.size()) - Q.emitted;
+        const int64_t avail = certified_count(Q) - Q.emitted;
         if (avail < m) todo.push_back(b);
     }
     for (int guard = 0; !todo.empty(); ++guard) {
@@ -1257,15 +1260,19 @@ extern "C" int pvs_next(pvs_state* st, int32_t m, const uint8_t* active, int64_t
             status[b] = EAHR_LIST_FAILED;
             continue;
         }
-        took[b] = std::min<int64_t>(m, static_cast<int64_t>(Q.cache.size()) - Q.emitted);
+        took[b] = std::min<int64_t>(m, certified_count(Q) - Q.emitted);
     }
     eahr::parallel_pieces(took, int64_t(1) << 17, eahr::host_threads(), [&](int64_t b, int64_t lo, int64_t hi) {
-        const uint64_t* kp = st->q[b].cache.data() + st->q[b].emitted;
+        // ranks emitted + j: from the cache, then from the pinned copy
+        const auto& Q = st->q[b];
+        const int64_t in_cache = static_cast<int64_t>(Q.cache.size()) - Q.emitted;
         int64_t* oi = ids + b * static_cast<int64_t>(m);
         float* os = scores + b * static_cast<int64_t>(m);
         for (int64_t j = lo; j < hi; ++j) {
-            oi[j] = key_id(kp[j]);
-            os[j] = key_score(kp[j]);
+            const uint64_t k = j < in_cache ? Q.cache[static_cast<size_t>(Q.emitted + j)]
+                                            : st->h_packed[Q.pend_off + (j - in_cache)];
+            oi[j] = key_id(k);
+            os[j] = key_score(k);
         }
     });
     for (int32_t b = 0; b < B; ++b) {
@@ -1286,9 +1293,9 @@ int pvs_fill(pvs_state* st, int64_t depth, const uint8_t* active, int64_t* added
     for (int32_t b = 0; b < st->B; ++b) {
         if (active && !active[b]) continue;
         const auto& Q = st->q[b];
-        before += static_cast<int64_t>(Q.cache.size());
-        if (Q.failed || Q.cert_exhausted) continue;
-        if (static_cast<int64_t>(Q.cache.size()) >= depth) continue;
+        before += certified_count(Q);
+        if (Q.failed || Q.cert_exhausted || Q.retired) continue;
+        if (certified_count(Q) >= depth) continue;
         todo.push_back(b);
         m = std::max<int64_t>(m, depth - Q.emitted);
     }
@@ -1300,10 +1307,25 @@ int pvs_fill(pvs_state* st, int64_t depth, const uint8_t* active, int64_t* added
     if (added) {
         int64_t after = 0;
         for (int32_t b = 0; b < st->B; ++b)
-            if (!active || active[b]) after += static_cast<int64_t>(st->q[b].cache.size());
+            if (!active || active[b]) after += certified_count(st->q[b]);
         *added = after - before;
     }
     return EAHR_OK;
+}
+
+int pvs_fill_exact(pvs_state* st, int64_t depth, const uint8_t* active, int64_t* added) {
+    if (!st) EAHR_FAIL(EAHR_E_INVALID, "pvs_fill: bad arguments");
+    st->spec_off = true;
+    const int rc = pvs_fill(st, depth, active, added);
+    st->spec_off = false;
+    return rc;
+}
+
+void pvs_retire(pvs_state* st, int32_t b) {
+    if (!st || b < 0 || b >= st->B) return;
+    auto& Q = st->q[b];
+    Q.retired = true;
+    Q.pend_n = 0;
 }
 
 bool pvs_query_failed(const pvs_state* st, int32_t b) {

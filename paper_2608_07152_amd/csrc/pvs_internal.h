@@ -72,6 +72,13 @@ enum class ScanPath { Auto, Gemv, Mfma };
 // sparse channel of a round is still running, so the GPU works ahead.
 // `added` (optional) receives the number of ranks certified by the call.
 int pvs_fill(pvs_state* st, int64_t depth, const uint8_t* active, int64_t* added);
+// pvs_fill whose scans certify about `depth` ranks per query and nothing
+// further ahead (the caller sized the depth itself).
+int pvs_fill_exact(pvs_state* st, int64_t depth, const uint8_t* active, int64_t* added);
+// The caller reads no further ranks of query b (its request is settled): the
+// query's certified keys that are still in a scan's pinned copy are not
+// moved to its cache any more, and pvs_next / pvs_fill skip the query.
+void pvs_retire(pvs_state* st, int32_t b);
 // Whether query b of a state has failed (a rescored score outside its
 // interval), also in work-ahead that pvs_next has not reported yet.
 bool pvs_query_failed(const pvs_state* st, int32_t b);
@@ -152,6 +159,10 @@ struct pvs_state {
         // certified ranks in order, as their sort keys (~mono(s32) << 32 | id);
         // ids and scores are decoded only when emitted
         KeyCache cache;
+        // the keys of its last scan that follow the cache, still in that
+        // scan's pinned copy (h_packed[pend_off .. pend_off + pend_n))
+        int64_t pend_off = 0, pend_n = 0;
+        bool retired = false;           // no further ranks will be read (pvs_retire)
         int64_t emitted = 0;            // ranks returned by pvs_next
         bool failed = false;
         bool cert_exhausted = false;    // every visible row certified
@@ -187,6 +198,7 @@ struct pvs_state {
     uint64_t* keys_tmp = nullptr;
     uint64_t* packed = nullptr;
     pvs::ScanPath path = pvs::ScanPath::Auto;
+    bool spec_off = false;             // scans certify no further ahead than asked
     // test knob: first-attempt key regions and pool divided by this, so that
     // the overflow and rescan paths run (results do not change)
     int64_t cap_shrink = 1;
@@ -195,7 +207,6 @@ struct pvs_state {
     // normal containment check (App. A.1); -1: off
     int32_t test_fail_qi = -1;
     hipEvent_t ev[7] = {};             // profiling events (created on first use)
-    hipEvent_t copy_ev[4] = {};        // ends of the pieces of a key copy
     pvs::ScanQ* h_scanq = nullptr;     // pinned host mirrors
     int32_t* h_counts = nullptr;
     uint64_t* h_packed = nullptr;
