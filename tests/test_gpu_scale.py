@@ -54,3 +54,28 @@ def test_mid_eahr_topk_matches_complete_rrf(mid):
     for_each_parallel(lambda b: check_fusion_run(q[b], x, vn, post, qs[b], ids[b], cnt[b], stats[b],
                                                  rec.ranks(b, 0), rec.ranks(b, 1), (1, 1), S[b]),
                       range(len(q)))
+
+
+def test_mid_eahr_topk_repeated_calls_agree(mid):
+    """Later calls size their first round's work-ahead from the rates the
+    earlier ones measured (one deep scan instead of one per depth level) and
+    emit certified ranks straight from the scans' pinned copies; the result
+    does not depend on either (Sec. 2.4: scheduling changes the work, not the
+    result)."""
+    E, w, x, lab, q, qlab, idx = mid
+    post = datagen.bm25_impacts(w, datagen.sparse_docs(w, lab))
+    qs = datagen.sparse_queries(w, qlab)
+    pbm = E.pbm_build(post.term_ptr, post.doc, post.impact, w.n, 4096)
+    runs = []
+    for _ in range(3):
+        with E.RankRecorder() as rec:
+            ids, cnt, stt, _ = E.eahr_topk(idx, pbm, q, qs, K=20)
+        runs.append((ids, cnt, stt, [(rec.ranks(b, 0), rec.ranks(b, 1)) for b in range(len(q))]))
+    ids0, cnt0, stt0, read0 = runs[0]
+    assert np.all(stt0 == 0) and np.all(cnt0 == 20)
+    for ids, cnt, stt, read in runs[1:]:
+        assert np.array_equal(ids, ids0) and np.array_equal(cnt, cnt0) and np.array_equal(stt, stt0)
+        for b in range(len(q)):
+            for lst in range(2):   # the same ranks read, bit for bit, in both lists
+                assert np.array_equal(read[b][lst][0], read0[b][lst][0]), (b, lst)
+                assert np.array_equal(read[b][lst][1].view(np.uint32), read0[b][lst][1].view(np.uint32)), (b, lst)
