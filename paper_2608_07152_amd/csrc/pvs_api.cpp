@@ -1268,12 +1268,15 @@ extern "C" int pvs_next(pvs_state* st, int32_t m, const uint8_t* active, int64_t
         const int64_t in_cache = static_cast<int64_t>(Q.cache.size()) - Q.emitted;
         int64_t* oi = ids + b * static_cast<int64_t>(m);
         float* os = scores + b * static_cast<int64_t>(m);
-        for (int64_t j = lo; j < hi; ++j) {
-            const uint64_t k = j < in_cache ? Q.cache[static_cast<size_t>(Q.emitted + j)]
-                                            : st->h_packed[Q.pend_off + (j - in_cache)];
-            oi[j] = key_id(k);
-            os[j] = key_score(k);
-        }
+        auto decode = [&](const uint64_t* kp, int64_t j0, int64_t j1) {   // kp[0] is rank emitted + j0
+            for (int64_t j = j0; j < j1; ++j) {
+                oi[j] = key_id(kp[j - j0]);
+                os[j] = key_score(kp[j - j0]);
+            }
+        };
+        const int64_t mid = std::min(std::max(in_cache, lo), hi);
+        if (mid > lo) decode(Q.cache.data() + Q.emitted + lo, lo, mid);
+        if (hi > mid) decode(st->h_packed + Q.pend_off + (mid - in_cache), mid, hi);
     });
     for (int32_t b = 0; b < B; ++b) {
         if ((active && !active[b]) || st->q[b].failed) continue;
