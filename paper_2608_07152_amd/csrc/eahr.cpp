@@ -56,13 +56,15 @@ constexpr int64_t kFillBudget = int64_t(1) << 25;
 
 // Rates measured by earlier calls on the same pair of indexes and sparse
 // generator: time per posting of a first sparse round (which scores about
-// all of its queries' postings) and dense time per rank certified ahead.
+// all of its queries' postings), per host thread it could use (one per
+// query, up to the pool's size; the GPU generator counts as one), and dense
+// time per rank certified ahead.
 // With both known, the first round certifies ahead in one scan, to the
 // deepest depth level whose estimated time fits in kAheadSlack times the
 // sparse channel's expected time, instead of in steps of one level (a scan
 // each) while it runs.
 struct Rates {
-    double sparse_ms_per_posting = 0.0;
+    double sparse_ms_per_posting = 0.0;   // times the threads the round could use
     double dense_ms_per_rank = 0.0;
 };
 constexpr double kAheadSlack = 1.25;
@@ -418,8 +420,9 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
         const auto it = g_rates.find(rates_key);
         if (it != g_rates.end()) rates = it->second;
     }
-    double first_sparse_ms = -1.0;   // the first round's sparse time and postings
+    double first_sparse_ms = -1.0;   // the first round's sparse time, postings and threads
     int64_t first_sparse_cost = 0;
+    int64_t first_sparse_par = 1;
     bool first_round = true;
     std::vector<uint8_t> retired(B, 0);
     for (bool doubling = ep.schedule == EAHR_SCHED_DOUBLING; doubling;) {
@@ -452,9 +455,15 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
         } wait_sparse{W.sparse, sparse_running};
         std::atomic<bool> sparse_done{false};
         std::atomic<int64_t> sparse_cost_done{0};   // postings of the queries finished
-        int64_t sparse_cost = 0;
+        int64_t sparse_cost = 0, sparse_queries = 0;
         for (int32_t b = 0; b < B; ++b)
-            if (sact[b]) sparse_cost += cost[b];
+            if (sact[b]) {
+                sparse_cost += cost[b];
+                sparse_queries += 1;
+            }
+        // threads the round's sparse work can use (one per query)
+        const int64_t sparse_par =
+            gpu_sparse ? 1 : std::max<int64_t>(1, std::min<int64_t>(std::max(1, threads - 1), sparse_queries));
         const auto t_sparse0 = std::chrono::steady_clock::now();
         auto sparse_work = [&]() {
             const auto t0 = std::chrono::steady_clock::now();
@@ -514,7 +523,8 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
                 // certify ahead, in one scan, to the deepest level the sparse
                 // channel's expected time pays for; worth a scan of its own
                 // only beyond what a first scan certifies anyway
-                const double expect = rates.sparse_ms_per_posting * static_cast<double>(sparse_cost);
+                const double expect = rates.sparse_ms_per_posting * static_cast<double>(sparse_cost) /
+                                      static_cast<double>(sparse_par);
                 const double per_level = rates.dense_ms_per_rank * static_cast<double>(nd);
                 const int64_t floor = std::max(pvs::kSpecFloor, pvs::kSpecFloorBudget / std::max<int64_t>(nd, 1));
                 int64_t ahead = 0;
@@ -581,6 +591,7 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
             if (first_round) {
                 first_sparse_ms = r_sparse;
                 first_sparse_cost = sparse_cost;
+                first_sparse_par = sparse_par;
             }
         }
         first_round = false;
@@ -670,7 +681,8 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
         Rates& r = g_rates[rates_key];
         if (fill_ranks > 0) r.dense_ms_per_rank = fill_ms / static_cast<double>(fill_ranks);
         if (first_sparse_ms > 0.0 && first_sparse_cost > 0)
-            r.sparse_ms_per_posting = first_sparse_ms / static_cast<double>(first_sparse_cost);
+            r.sparse_ms_per_posting =
+                first_sparse_ms * static_cast<double>(first_sparse_par) / static_cast<double>(first_sparse_cost);
     }
     // a rescored score outside its interval fails its query even when the
     // failure came from work-ahead that no pvs_next has reported yet
