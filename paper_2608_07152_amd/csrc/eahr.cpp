@@ -526,12 +526,12 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
                 const double expect = rates.sparse_ms_per_posting * static_cast<double>(sparse_cost) /
                                       static_cast<double>(sparse_par);
                 const double per_level = rates.dense_ms_per_rank * static_cast<double>(nd);
-                const int64_t floor = std::max(pvs::kSpecFloor, pvs::kSpecFloorBudget / std::max<int64_t>(nd, 1));
+                const int64_t first_scan = std::max(pvs::kSpecFloor, pvs::kSpecFloorBudget / std::max<int64_t>(nd, 1));
                 int64_t ahead = 0;
                 for (int64_t l = depth; l <= cap && per_level * static_cast<double>(l) <= kAheadSlack * expect;
                      l *= ep.growth)
                     ahead = l;
-                if (ahead > std::max(depth * ep.growth, floor)) {
+                if (ahead > std::max(depth * ep.growth, first_scan)) {
                     int64_t added = 0;
                     dense_rc = pvs_fill_exact(cl.st, ahead, dact.data(), &added);
                     if (added > 0) {
