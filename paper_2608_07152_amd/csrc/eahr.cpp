@@ -549,8 +549,11 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
             if (dense_rc == EAHR_OK)
                 dense_rc = merged ? pvs_merge_next(merged, static_cast<int32_t>(m), dact.data(), ids, sc,
                                                    dcnt.data(), dsts.data())
-                                  : pvs_next(cl.st, static_cast<int32_t>(m), dact.data(), ids, sc,
-                                             dcnt.data(), dsts.data());
+                                  : obs ? pvs_next(cl.st, static_cast<int32_t>(m), dact.data(), ids, sc,
+                                                   dcnt.data(), dsts.data())
+                                        // the fusion needs the ids only
+                                        : pvs_next_ids(cl.st, static_cast<int32_t>(m), dact.data(), ids,
+                                                       dcnt.data(), dsts.data());
             // While the sparse channel is still busy, certify the dense ranks
             // of the next depths ahead (they are served from the cache later;
             // the output does not depend on it).

@@ -1232,10 +1232,9 @@ static int scan_round(pvs_state* st, std::vector<int32_t>& todo, int32_t m) {
     return EAHR_OK;
 }
 
-extern "C" int pvs_next(pvs_state* st, int32_t m, const uint8_t* active, int64_t* ids,
-                        float* scores, int32_t* count, int32_t* status) {
-    if (!st || m < 0 || (m > 0 && (!ids || !scores)) || !count || !status)
-        EAHR_FAIL(EAHR_E_INVALID, "pvs_next: bad arguments");
+// pvs_next; scores may be null (then only ids are written).
+static int next_ranks(pvs_state* st, int32_t m, const uint8_t* active, int64_t* ids, float* scores,
+                      int32_t* count, int32_t* status) {
     const int32_t B = st->B;
     std::vector<int32_t> todo;
     for (int32_t b = 0; b < B; ++b) {
@@ -1267,12 +1266,15 @@ extern "C" int pvs_next(pvs_state* st, int32_t m, const uint8_t* active, int64_t
         const auto& Q = st->q[b];
         const int64_t in_cache = static_cast<int64_t>(Q.cache.size()) - Q.emitted;
         int64_t* oi = ids + b * static_cast<int64_t>(m);
-        float* os = scores + b * static_cast<int64_t>(m);
+        float* os = scores ? scores + b * static_cast<int64_t>(m) : nullptr;
         auto decode = [&](const uint64_t* kp, int64_t j0, int64_t j1) {   // kp[0] is rank emitted + j0
-            for (int64_t j = j0; j < j1; ++j) {
-                oi[j] = key_id(kp[j - j0]);
-                os[j] = key_score(kp[j - j0]);
-            }
+            if (scores)
+                for (int64_t j = j0; j < j1; ++j) {
+                    oi[j] = key_id(kp[j - j0]);
+                    os[j] = key_score(kp[j - j0]);
+                }
+            else
+                for (int64_t j = j0; j < j1; ++j) oi[j] = key_id(kp[j - j0]);
         };
         const int64_t mid = std::min(std::max(in_cache, lo), hi);
         if (mid > lo) decode(Q.cache.data() + Q.emitted + lo, lo, mid);
@@ -1289,6 +1291,20 @@ extern "C" int pvs_next(pvs_state* st, int32_t m, const uint8_t* active, int64_t
     return EAHR_OK;
 }
 
+
+extern "C" int pvs_next(pvs_state* st, int32_t m, const uint8_t* active, int64_t* ids,
+                        float* scores, int32_t* count, int32_t* status) {
+    if (!st || m < 0 || (m > 0 && (!ids || !scores)) || !count || !status)
+        EAHR_FAIL(EAHR_E_INVALID, "pvs_next: bad arguments");
+    return next_ranks(st, m, active, ids, scores, count, status);
+}
+
+int pvs_next_ids(pvs_state* st, int32_t m, const uint8_t* active, int64_t* ids, int32_t* count,
+                 int32_t* status) {
+    if (!st || m < 0 || (m > 0 && !ids) || !count || !status)
+        EAHR_FAIL(EAHR_E_INVALID, "pvs_next: bad arguments");
+    return next_ranks(st, m, active, ids, nullptr, count, status);
+}
 int pvs_fill(pvs_state* st, int64_t depth, const uint8_t* active, int64_t* added) {
     if (!st || depth < 0) EAHR_FAIL(EAHR_E_INVALID, "pvs_fill: bad arguments");
     std::vector<int32_t> todo;

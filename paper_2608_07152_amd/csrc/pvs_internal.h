@@ -66,6 +66,9 @@ constexpr int32_t kMfmaMinQueries = 9;
 enum class ScanPath { Auto, Gemv, Mfma };
 }  // namespace pvs
 
+// pvs_next without scores: only the ids of the emitted ranks are written.
+int pvs_next_ids(pvs_state* st, int32_t m, const uint8_t* active, int64_t* ids, int32_t* count,
+                 int32_t* status);
 // Deepen the certified caches of the active queries of a state to `depth`
 // ranks each (or to exhaustion) without emitting anything; a later pvs_next
 // is then served from the caches.  The host fusion calls it while the CPU
