@@ -68,6 +68,8 @@ struct Rates {
     double dense_ms_per_rank = 0.0;
 };
 constexpr double kAheadSlack = 1.25;
+// Sparse rounds shorter than this (as the previous one was) run inline.
+constexpr double kInlineSparseMs = 0.1;
 std::mutex g_rates_mu;
 std::map<std::tuple<const void*, const void*, int32_t>, Rates> g_rates;
 
@@ -425,6 +427,7 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
     int64_t first_sparse_par = 1;
     bool first_round = true;
     std::vector<uint8_t> retired(B, 0);
+    double last_sparse_ms = -1.0;    // the previous round's sparse time
     for (bool doubling = ep.schedule == EAHR_SCHED_DOUBLING; doubling;) {
         bool any = false;
         for (int32_t b = 0; b < B; ++b) any |= !F[b].resolved && !failed[b];
@@ -508,7 +511,13 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
         };
         bool any_sparse = false;
         for (int32_t b = 0; b < B; ++b) any_sparse |= sact[b] != 0;
-        if (any_sparse) {
+        // A short sparse round beside dense ranks that are already certified
+        // runs on this thread after them: handing it to the helper thread and
+        // back costs more than the overlap saves.
+        const bool sparse_inline = any_sparse && !gpu_sparse && !merged && last_sparse_ms >= 0.0 &&
+                                   last_sparse_ms < kInlineSparseMs &&
+                                   (m == 0 || pvs_covered(cl.st, m, dact.data()));
+        if (any_sparse && !sparse_inline) {
             W.sparse.post(sparse_work);
             sparse_running = true;
         }
@@ -588,6 +597,7 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
             r_dense = ms_since(t0);
             t_dense += r_dense;
         }
+        if (sparse_inline) sparse_work();
         if (sparse_running) {
             W.sparse.wait();
             sparse_running = false;
@@ -597,6 +607,7 @@ static int topk_impl(const pvs_index* dense, int64_t epoch, pvs_merge* merged,
                 first_sparse_par = sparse_par;
             }
         }
+        if (any_sparse) last_sparse_ms = r_sparse;
         first_round = false;
         EAHR_TRY(dense_rc);
         for (int32_t b = 0; b < B; ++b)

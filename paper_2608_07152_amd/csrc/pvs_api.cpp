@@ -1340,6 +1340,17 @@ int pvs_fill_exact(pvs_state* st, int64_t depth, const uint8_t* active, int64_t*
     return rc;
 }
 
+bool pvs_covered(const pvs_state* st, int32_t m, const uint8_t* active) {
+    if (!st) return false;
+    for (int32_t b = 0; b < st->B; ++b) {
+        if (active && !active[b]) continue;
+        const auto& Q = st->q[b];
+        if (Q.failed || Q.cert_exhausted || Q.retired) continue;
+        if (certified_count(Q) - Q.emitted < m) return false;
+    }
+    return true;
+}
+
 void pvs_retire(pvs_state* st, int32_t b) {
     if (!st || b < 0 || b >= st->B) return;
     auto& Q = st->q[b];

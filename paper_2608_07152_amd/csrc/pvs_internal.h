@@ -66,6 +66,9 @@ constexpr int32_t kMfmaMinQueries = 9;
 enum class ScanPath { Auto, Gemv, Mfma };
 }  // namespace pvs
 
+// Whether pvs_next(m) on the active queries would be served from certified
+// ranks alone (no scan).
+bool pvs_covered(const pvs_state* st, int32_t m, const uint8_t* active);
 // pvs_next without scores: only the ids of the emitted ranks are written.
 int pvs_next_ids(pvs_state* st, int32_t m, const uint8_t* active, int64_t* ids, int32_t* count,
                  int32_t* status);
