@@ -62,7 +62,9 @@ constexpr int64_t kFillBudget = int64_t(1) << 25;
 // With both known, the first round certifies ahead in one scan, to the
 // deepest depth level whose estimated time fits in kAheadSlack times the
 // sparse channel's expected time, instead of in steps of one level (a scan
-// each) while it runs.
+// each) while it runs.  Entries are a few bytes and live as long as the
+// process; an index allocated where a freed one was starts from that one's
+// rates, which only sizes work.
 struct Rates {
     double sparse_ms_per_posting = 0.0;   // times the threads the round could use
     double dense_ms_per_rank = 0.0;
