@@ -237,9 +237,14 @@ struct Fusion {
     bool resolved = false;
     bool dup = false;           // an id repeated inside one list
     std::vector<uint64_t> batch, tmp, merged;
-    // closed-list mode: seen[i] has bit x set when list i holds id x
+    // closed-list mode: seen[i] has bit x set when list i holds id x; for
+    // the closed list c = cum_list, cum[w] counts its ids below word w, so an
+    // id's position in c's id order is cum[w] plus the set bits below it in
+    // word w (a rank costs two reads instead of a binary search)
     bool bitmaps = false;
     std::vector<uint64_t> seen[2];
+    std::vector<uint32_t> cum;
+    int cum_list = -1;
     // direct mode: pos[2 x + i] is the 1-based rank of id x in list i (0:
     // not in it; both ranks of an id share a cache line); entered once the
     // lists hold universe / kDirectShare ranks
@@ -269,9 +274,23 @@ struct Fusion {
     // rank (1-based) of id x in list i, from its id order; x must be in it
     int64_t rank_of(int i, int64_t x) const {
         const auto& v = L[i].by_id;
+        if (cum_list == i) {
+            const size_t w = static_cast<size_t>(x >> 6);
+            const uint64_t below = seen[i][w] & ((1ull << (x & 63)) - 1);
+            return static_cast<int64_t>(v[cum[w] + static_cast<uint32_t>(__builtin_popcountll(below))] & 0xffffffffu);
+        }
         const uint64_t key = static_cast<uint64_t>(x) << 32;
         const auto it = std::lower_bound(v.begin(), v.end(), key);
         return static_cast<int64_t>(*it & 0xffffffffu);
+    }
+    // prefix counts of closed list c's id bitmap (its id order is complete:
+    // every rank it holds was merged in while the other list was open)
+    void count_closed(int c) {
+        const auto& b = seen[c];
+        cum.resize(b.size() + 1);
+        cum[0] = 0;
+        for (size_t w = 0; w < b.size(); ++w) cum[w + 1] = cum[w] + static_cast<uint32_t>(__builtin_popcountll(b[w]));
+        cum_list = c;
     }
 
     bool fixed(int64_t x) const { return std::find(A.begin(), A.end(), x) != A.end(); }
@@ -329,6 +348,7 @@ struct Fusion {
         dup = false;
         bitmaps = false;
         for (auto& b : seen) std::fill(b.begin(), b.end(), 0ull);
+        cum_list = -1;
         direct = false;
         universe = 0;
         std::vector<int32_t>().swap(pos);   // only deep queries need it
@@ -611,6 +631,7 @@ struct Fusion {
     // Append to list i while the other list is closed (see the file header).
     void append_closed_other(int i, const int64_t* ids, int64_t n) {
         if (!bitmaps) enter_bitmap_mode();
+        if (cum_list != 1 - i) count_closed(1 - i);
         List& me = L[i];
         const int64_t p0 = me.size();
         me.grow(n);

@@ -422,6 +422,22 @@ def test_fusion_reads_deep_after_one_list_closed(fusion_modes, tmp_path, threads
 
 
 @pytest.mark.parametrize("threads", [1, 8])
+def test_fusion_closed_list_shares_most_ids(fusion_modes, tmp_path, threads):
+    """A short list made of the long list's last ids, reversed: it closes
+    first, and nearly every later rank of the long list is found in it, so
+    each one's rank in the closed list is looked up (from the closed list's
+    id bitmap and id order); the Top-K equals complete-list RRF."""
+    rng = np.random.default_rng(33)
+    n = 300_000
+    a = rng.permutation(n)
+    short = a[::-1][:120_000].copy()
+    for K, wts in ((20, (1, 1)), (10, (1, 2))):
+        got, depth = _run_modes(fusion_modes, tmp_path, a, short, K, wts, threads)
+        assert got == rrf.rrf_topk([a, short], list(wts), 60, K), (K, wts)
+        assert depth[1] == len(short) and depth[0] > n - len(short), depth
+
+
+@pytest.mark.parametrize("threads", [1, 8])
 def test_fusion_reads_deep_with_both_lists_open(fusion_modes, tmp_path, threads):
     """Both lists stay open while read deep: the id-order merges, split over
     host threads when long; the Top-K equals complete-list RRF."""
